@@ -1,0 +1,140 @@
+"""Workload descriptions.
+
+Each workload names the client population (K clients, C clusters, batch B per
+cluster, L classes), the synthetic data set (N_ex images of H x W x Cin, a
+Dirichlet(alpha) label split), the split CNN (a list of layers and the cut
+index), the compute precision and the optimiser / fusion schedule.
+
+Layer tuples:
+    ("conv", cin, cout, residual)   3x3 conv, stride 1, zero pad 1, bias, ReLU;
+                                    residual=True adds the layer input before
+                                    the ReLU (requires cin == cout)
+    ("maxpool",)                    2x2 / stride 2 max pool
+    ("avgpool",)                    global average pool over H x W
+    ("linear", cin, cout)           fully connected layer producing the logits
+
+The client segment is layers[:cut]; the server segment is layers[cut:].
+
+Parameter layout (one flat fp32 vector of P entries per replica): for every
+conv / linear layer in order, its weight followed by its bias.  Conv weights
+are stored [cout][3][3][cin] (output channel, kernel row, kernel column,
+input channel); linear weights [cout][cin].
+"""
+from __future__ import annotations
+
+import copy
+
+_CIFAR_CLIENT = [("conv", 3, 32, False), ("conv", 32, 64, False), ("maxpool",)]
+_SERVER_NARROW = [("conv", 64, 128, False), ("conv", 128, 128, False), ("maxpool",),
+                  ("avgpool",), ("linear", 128, 10)]
+# Wide residual server: 64->256, then three 256->256 convs whose output is
+# ReLU(conv(x) + b + x).
+_SERVER_WIDE = [("conv", 64, 256, False), ("conv", 256, 256, True), ("conv", 256, 256, True),
+                ("conv", 256, 256, True), ("maxpool",), ("avgpool",), ("linear", 256, 10)]
+
+_CIFAR_DATA = dict(N_ex=50000, H=32, W=32, Cin=3, L=10, noise_std=0.5)
+
+CONFIGS = {
+    # Tiny reference workload: 16 clients in 2 random clusters of 8.
+    "tiny": dict(
+        K=16, C=2, B=8, L=4, N_ex=512, H=8, W=8, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="random",
+        layers=[("conv", 3, 8, False), ("maxpool",),
+                ("conv", 8, 16, False), ("avgpool",), ("linear", 16, 4)],
+        cut=2, dtype="f32", lr=0.05, momentum=0.0, F=5, T=10, seed=0),
+    # Single-workload GPSL baseline (C = 1).
+    "gpsl": dict(
+        K=256, C=1, B=64, alpha=0.3, rule="random", **_CIFAR_DATA,
+        layers=_CIFAR_CLIENT + _SERVER_NARROW, cut=3,
+        dtype="f32", lr=0.05, momentum=0.9, F=0, T=500, seed=0),
+    # Four random clusters of 64 clients.
+    "gcpsl4": dict(
+        K=256, C=4, B=64, alpha=0.3, rule="random", **_CIFAR_DATA,
+        layers=_CIFAR_CLIENT + _SERVER_NARROW, cut=3,
+        dtype="f32", lr=0.05, momentum=0.9, F=50, T=500, seed=0),
+    # Eight size-balanced clusters, bf16 activations/weights, fp32 masters.
+    "gcpsl8": dict(
+        K=256, C=8, B=64, alpha=0.3, rule="size", **_CIFAR_DATA,
+        layers=_CIFAR_CLIENT + _SERVER_NARROW, cut=3,
+        dtype="bf16", lr=0.05, momentum=0.9, F=25, T=1000, seed=0),
+    # Sixteen label-aware clusters, B=128, wide residual server, bf16.
+    "gcpsl16": dict(
+        K=256, C=16, B=128, alpha=0.1, rule="label_l1", **_CIFAR_DATA,
+        layers=_CIFAR_CLIENT + _SERVER_WIDE, cut=3,
+        dtype="bf16", lr=0.05, momentum=0.9, F=50, T=1000, seed=0),
+    # Small parity workloads whose GEMM sizes are ragged against every tile
+    # size (M, N and K tails; more than one N tile; a residual layer).
+    "ragged": dict(
+        K=24, C=3, B=20, L=7, N_ex=1400, H=12, W=12, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="size",
+        layers=[("conv", 3, 8, False), ("conv", 8, 24, False), ("maxpool",),
+                ("conv", 24, 136, False), ("conv", 136, 136, True), ("maxpool",),
+                ("avgpool",), ("linear", 136, 7)],
+        cut=3, dtype="f32", lr=0.05, momentum=0.9, F=3, T=7, seed=0),
+    "ragged_bf16": dict(
+        K=24, C=3, B=20, L=7, N_ex=1400, H=12, W=12, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="label_l1",
+        layers=[("conv", 3, 8, False), ("conv", 8, 24, False), ("maxpool",),
+                ("conv", 24, 136, False), ("conv", 136, 136, True), ("maxpool",),
+                ("avgpool",), ("linear", 136, 7)],
+        cut=3, dtype="bf16", lr=0.05, momentum=0.9, F=3, T=7, seed=0),
+}
+
+
+def get_config(name: str, **overrides) -> dict:
+    """Return a deep copy of a named workload with optional field overrides."""
+    cfg = copy.deepcopy(CONFIGS[name])
+    cfg.update(overrides)
+    cfg["name"] = name
+    return cfg
+
+
+def model_layers(cfg: dict) -> list:
+    """Layer list with the spatial size each layer sees: (spec, H_in, W_in, C_in)."""
+    h, w, c = cfg["H"], cfg["W"], cfg["Cin"]
+    out = []
+    for spec in cfg["layers"]:
+        out.append((spec, h, w, c))
+        kind = spec[0]
+        if kind == "conv":
+            c = spec[2]
+        elif kind == "maxpool":
+            h, w = h // 2, w // 2
+        elif kind == "avgpool":
+            h, w = 1, 1
+        elif kind == "linear":
+            c = spec[2]
+    return out
+
+
+def param_layout(cfg: dict) -> list:
+    """[(layer_index, 'w'|'b', shape, offset)] in the flat parameter order."""
+    out, off = [], 0
+    for i, spec in enumerate(cfg["layers"]):
+        if spec[0] == "conv":
+            shapes = [("w", (spec[2], 3, 3, spec[1])), ("b", (spec[2],))]
+        elif spec[0] == "linear":
+            shapes = [("w", (spec[2], spec[1])), ("b", (spec[2],))]
+        else:
+            continue
+        for tag, shp in shapes:
+            n = 1
+            for d in shp:
+                n *= d
+            out.append((i, tag, shp, off))
+            off += n
+    return out
+
+
+def param_counts(cfg: dict) -> tuple:
+    """(P_client, P_server): parameter counts of the two segments."""
+    pc = ps = 0
+    for i, tag, shp, off in param_layout(cfg):
+        n = 1
+        for d in shp:
+            n *= d
+        if i < cfg["cut"]:
+            pc += n
+        else:
+            ps += n
+    return pc, ps

@@ -1,0 +1,207 @@
+"""Split CNN forward and backward pass in fp64 (Sec. III-A, Alg. 2).
+
+A participating client evaluates the client segment up to the cut, the
+server finishes the forward pass and the loss, and returns the cut gradient,
+from which the client segment's gradient follows (Sec. III-A; Alg. 2, the
+cluster-local round).  On one device the cut gradient is simply the
+gradient with respect to the cut activation.  The client-gradient average of
+Sec. III-B is the gradient of the batch-mean loss: a b_k/B weighted mean of
+the active clients' mean gradients, i.e. centralised mini-batch SGD on the
+cluster's batch.
+
+Layer definitions (readings; the paper's ResNet-18 is replaced by the
+workloads' plain CNNs):
+  conv       3x3 cross-correlation, stride 1, zero padding 1, bias, then ReLU;
+             with residual, ReLU(conv(x) + b + x).  ReLU'(0) = 0.
+  maxpool    2x2, stride 2; the gradient goes to the first maximum of the
+             window in row-major order (strict >).
+  avgpool    mean over the spatial positions.
+  linear     logits = h W^T + b.
+  loss       softmax cross-entropy, mean over the batch.
+
+bf16 workloads round to bf16 (round-to-nearest-even) at these points and keep
+everything else in fp64: the gathered images; the conv and linear weight
+matrices (biases stay at the master's precision); every conv output after
+its ReLU; the average-pool output; the gradient with respect to each conv's
+pre-activation; and each input gradient a conv returns (including the cut
+gradient).  Logits, loss, logit gradients, parameter gradients stay unrounded.
+
+Conv uses im2col with a library matmul for the forward pass and the weight
+gradient, and the textbook col2im scatter for the input gradient.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from gcpsl_inputs import param_layout
+
+
+def round_bf16(x):
+    """Round fp64 values to the nearest bf16 value, ties to even.
+
+    bf16 keeps 8 significant bits and the fp32 exponent range; below 2^-126
+    its values are multiples of 2^-133."""
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)
+    r = np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)
+    tiny = np.abs(x) < 2.0 ** -126
+    if np.any(tiny):
+        r = np.where(tiny, np.ldexp(np.rint(np.ldexp(x, 133)), -133), r)
+    return r
+
+
+def _identity(x):
+    return np.asarray(x, dtype=np.float64)
+
+
+def rounder(dtype: str):
+    return round_bf16 if dtype == "bf16" else _identity
+
+
+# ----------------------------------------------------------------- layers
+
+def im2col3x3(x):
+    """[Bt,H,W,Ci] -> [Bt*H*W, 9*Ci], column order (kernel row, kernel col, ci)."""
+    Bt, H, W, Ci = x.shape
+    xp = np.zeros((Bt, H + 2, W + 2, Ci))
+    xp[:, 1:-1, 1:-1, :] = x
+    cols = np.empty((Bt, H, W, 3, 3, Ci))
+    for r in range(3):
+        for s in range(3):
+            cols[:, :, :, r, s, :] = xp[:, r:r + H, s:s + W, :]
+    return cols.reshape(Bt * H * W, 9 * Ci)
+
+
+def conv3x3_forward(x, w, b):
+    """Pre-activation y[b,h,w,o] = b[o] + sum_{r,s,i} x[b,h+r-1,w+s-1,i] w[o,r,s,i]."""
+    Bt, H, W, _ = x.shape
+    Co = w.shape[0]
+    return (im2col3x3(x) @ w.reshape(Co, -1).T + b).reshape(Bt, H, W, Co)
+
+
+def conv3x3_backward(x, w, gp):
+    """Given dL/dpre gp [Bt,H,W,Co]: (dL/dx, dL/dw, dL/db)."""
+    Bt, H, W, Ci = x.shape
+    Co = w.shape[0]
+    gf = gp.reshape(-1, Co)
+    dw = (gf.T @ im2col3x3(x)).reshape(w.shape)
+    db = gf.sum(axis=0)
+    dcols = (gf @ w.reshape(Co, -1)).reshape(Bt, H, W, 3, 3, Ci)
+    dxp = np.zeros((Bt, H + 2, W + 2, Ci))
+    for r in range(3):
+        for s in range(3):
+            dxp[:, r:r + H, s:s + W, :] += dcols[:, :, :, r, s, :]
+    return dxp[:, 1:-1, 1:-1, :], dw, db
+
+
+def _windows(x):
+    Bt, H, W, C = x.shape
+    return (x.reshape(Bt, H // 2, 2, W // 2, 2, C).transpose(0, 1, 3, 2, 4, 5)
+            .reshape(Bt, H // 2, W // 2, 4, C))
+
+
+def maxpool2_forward(x):
+    """(pooled, arg) with arg the first row-major maximum of each 2x2 window."""
+    win = _windows(x)
+    arg = np.argmax(win, axis=3)
+    return np.take_along_axis(win, arg[:, :, :, None, :], axis=3)[:, :, :, 0, :], arg
+
+
+def maxpool2_backward(gz, arg):
+    Bt, Hh, Wh, C = gz.shape
+    win = np.zeros((Bt, Hh, Wh, 4, C))
+    np.put_along_axis(win, arg[:, :, :, None, :], gz[:, :, :, None, :], axis=3)
+    return (win.reshape(Bt, Hh, Wh, 2, 2, C).transpose(0, 1, 3, 2, 4, 5)
+            .reshape(Bt, 2 * Hh, 2 * Wh, C))
+
+
+def softmax_xent(logits, y):
+    """Mean softmax cross-entropy and its gradient with respect to the logits."""
+    Bt = logits.shape[0]
+    z = logits - logits.max(axis=1, keepdims=True)
+    lse = np.log(np.exp(z).sum(axis=1))
+    rows = np.arange(Bt)
+    loss = float(np.mean(lse - z[rows, y]))
+    d = np.exp(z - lse[:, None])
+    d[rows, y] -= 1.0
+    return loss, d / Bt
+
+
+# --------------------------------------------------------- parameter views
+
+def unflatten(cfg, theta):
+    """{layer index: {'w': array, 'b': array}} views into a flat vector."""
+    out = {}
+    for i, tag, shp, off in param_layout(cfg):
+        n = int(np.prod(shp))
+        out.setdefault(i, {})[tag] = theta[off:off + n].reshape(shp)
+    return out
+
+
+# ------------------------------------------------------------- split step
+
+def split_forward_backward(cfg, theta, x, y, keep=False):
+    """One cluster-local round's loss and flat gradient for one replica.
+
+    theta: flat parameters (fp64 view of the fp32 master); x: [B,H,W,Cin]
+    gathered images; y: [B] labels.  Returns (loss, grad[P], record) where
+    record (if keep) holds every intermediate tensor, keyed by name."""
+    rnd = rounder(cfg["dtype"])
+    layers = cfg["layers"]
+    p = unflatten(cfg, np.asarray(theta, dtype=np.float64))
+    rec = {}
+    acts = [rnd(x)]
+    args = {}
+    for i, spec in enumerate(layers):
+        a = acts[-1]
+        kind = spec[0]
+        if kind == "conv":
+            pre = conv3x3_forward(a, rnd(p[i]["w"]), p[i]["b"])
+            if spec[3]:
+                pre = pre + a
+            if keep:
+                rec[f"pre{i}"] = pre
+            out = rnd(np.maximum(pre, 0.0))
+        elif kind == "maxpool":
+            out, args[i] = maxpool2_forward(a)
+        elif kind == "avgpool":
+            out = rnd(a.mean(axis=(1, 2)))
+        elif kind == "linear":
+            out = a @ rnd(p[i]["w"]).T + p[i]["b"]
+        else:
+            raise ValueError(kind)
+        acts.append(out)
+    loss, g = softmax_xent(acts[-1], y)
+    if keep:
+        rec["acts"] = acts
+        rec["dlogits"] = g
+    grad = np.zeros(len(theta))
+    gview = unflatten(cfg, grad)
+    for i in range(len(layers) - 1, -1, -1):
+        spec = layers[i]
+        a_in, a_out = acts[i], acts[i + 1]
+        kind = spec[0]
+        if kind == "linear":
+            gview[i]["w"][...] = g.T @ a_in
+            gview[i]["b"][...] = g.sum(axis=0)
+            g = g @ rnd(p[i]["w"])
+        elif kind == "avgpool":
+            Bt, H, W, C = a_in.shape
+            g = np.broadcast_to((g / (H * W))[:, None, None, :], a_in.shape).copy()
+        elif kind == "maxpool":
+            g = maxpool2_backward(g, args[i])
+        elif kind == "conv":
+            gp = rnd(g * (a_out > 0))
+            if keep:
+                rec[f"gpre{i}"] = gp
+            dx, dw, db = conv3x3_backward(a_in, rnd(p[i]["w"]), gp)
+            gview[i]["w"][...] = dw
+            gview[i]["b"][...] = db
+            if i == 0:
+                g = None
+                break
+            g = dx + gp if spec[3] else dx
+            g = rnd(g)
+        if keep:
+            rec[f"gin{i}"] = g
+    return loss, grad, rec

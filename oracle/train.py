@@ -1,0 +1,104 @@
+"""GCPSL training loop (Alg. 2), SGD update and sample-weighted fusion (Eq. 5).
+
+Alg. 2: build the fixed clusters (Alg. 1), start every split-model replica
+from the same parameters, run the clusters' GPSL rounds side by side, and at
+the synchronisation points fuse client and server parameters with the weights
+q_n = |D_{C_n}| / |D| and give the fused model to every replica (Sec. IV-D).
+Optimiser state stays local to each cluster and is never fused (Sec. IV-D).
+
+Readings:
+  * Parameters and momentum are held as fp32 values (the workloads keep fp32
+    master weights); each update is computed in fp64 and rounded once to
+    fp32 when stored.
+  * SGD with momentum, PyTorch convention: v <- mu v + g, theta <- theta -
+    lr v, v starts at 0; no Nesterov term, no weight decay.
+  * Fusion happens after every F-th round (1-based: after rounds F, 2F, ...);
+    all clusters advance in lockstep.  F = 0 disables fusion.
+  * Fused value: (sum_n n_n theta_n) / W accumulated in fp64 in cluster
+    order and rounded once to fp32, n_n = |D_{C_n}|, W = sum_n n_n (the
+    dropped epoch remainder still counts in n_n).  For fp32 replicas every
+    product n_n theta_n and every partial sum is exact in fp64, so fusing
+    identical replicas returns them unchanged, bit for bit.
+  * The reported loss of a round is the forward loss before that round's
+    update.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from gcpsl_inputs import client_stats, init_params, make_dataset
+
+from .assign import assign
+from .model import split_forward_backward
+from .sampler import active_clients, batch_indices, cluster_examples
+
+
+def sgd_update(theta, mom, grad, lr, mu):
+    """In place on fp32 state: v <- mu v + g; theta <- theta - lr v."""
+    v = mu * mom.astype(np.float64) + grad
+    mom[...] = v.astype(np.float32)
+    theta[...] = (theta.astype(np.float64) - lr * mom.astype(np.float64)).astype(np.float32)
+
+
+def fuse(thetas, weights):
+    """Eq. 5: sum_n (n_n / W) theta_n, accumulated in fp64 in cluster order."""
+    W = int(sum(int(w) for w in weights))
+    acc = np.zeros(np.shape(thetas[0]), dtype=np.float64)
+    for th, w in zip(thetas, weights):
+        acc += float(int(w)) * np.asarray(th, dtype=np.float64)
+    return (acc / W).astype(np.float32)
+
+
+class GCPSLOracle:
+    """State of one GCPSL run: C replicas, their momenta, the participation log."""
+
+    def __init__(self, cfg, data=None, theta0=None, cluster_of_client=None):
+        self.cfg = cfg
+        self.images, self.labels, self.coe = data if data is not None else make_dataset(cfg)
+        counts, hist = client_stats(cfg, self.labels, self.coe)
+        if cluster_of_client is None:
+            cluster_of_client = assign(cfg["rule"], cfg["K"], cfg["C"], cfg["seed"], counts, hist)
+        self.assignment = np.asarray(cluster_of_client, dtype=np.int32)
+        self.ids = cluster_examples(self.coe, self.assignment, cfg["C"])
+        self.weights = [len(x) for x in self.ids]
+        t0 = init_params(cfg) if theta0 is None else theta0
+        self.theta = [np.asarray(t0, dtype=np.float32).copy() for _ in range(cfg["C"])]
+        self.mom = [np.zeros_like(self.theta[0]) for _ in range(cfg["C"])]
+        self.active = []
+        self.losses = []
+
+    def batch(self, step, n):
+        idx = batch_indices(self.ids[n], self.cfg["B"], self.cfg["seed"], n, step)
+        return idx, self.images[idx].astype(np.float64), self.labels[idx].astype(np.int64)
+
+    def round(self, step, replicas=None):
+        """One local round for the given replicas (default: all).
+
+        Returns (losses, grads) per replica; updates theta / momentum and
+        records |A_{n,t}| for every cluster when all replicas ran."""
+        cfg = self.cfg
+        reps = range(cfg["C"]) if replicas is None else replicas
+        losses, grads, active = {}, {}, {}
+        for n in reps:
+            idx, x, y = self.batch(step, n)
+            active[n] = active_clients(idx, self.coe)
+            loss, g, _ = split_forward_backward(cfg, self.theta[n], x, y)
+            sgd_update(self.theta[n], self.mom[n], g, cfg["lr"], cfg["momentum"])
+            losses[n], grads[n] = loss, g
+        if replicas is None:
+            self.active.append([active[n] for n in range(cfg["C"])])
+            self.losses.append([losses[n] for n in range(cfg["C"])])
+        return losses, grads
+
+    def fuse(self):
+        fused = fuse(self.theta, self.weights)
+        for n in range(self.cfg["C"]):
+            self.theta[n] = fused.copy()
+
+    def run(self, steps, F=None):
+        F = self.cfg["F"] if F is None else F
+        for s in range(steps):
+            self.round(s)
+            if F and (s + 1) % F == 0:
+                self.fuse()
+        return self

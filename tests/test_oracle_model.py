@@ -1,0 +1,248 @@
+"""Pins for the oracle's split forward/backward pass.
+
+Each layer is checked against its textbook loop definition, the whole split
+step against central finite differences and against torch.autograd on the
+unsplit model (a library implementation; C = 1 makes the split model the
+plain CNN, Sec. III-A), and the bf16 rounding primitive against torch's
+float32 -> bfloat16 conversion.
+"""
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as tF
+
+from gcpsl_inputs import get_config, init_params, make_dataset, param_layout
+from oracle.model import (conv3x3_backward, conv3x3_forward, maxpool2_backward,
+                          maxpool2_forward, round_bf16, softmax_xent, split_forward_backward)
+
+torch.set_num_threads(4)
+
+
+# ------------------------------------------------------------ bf16 rounding
+
+def test_round_bf16_matches_torch_on_fp32_values():
+    rng = np.random.default_rng(0)
+    x = np.concatenate([
+        rng.standard_normal(20000).astype(np.float32) * np.float32(3.0),
+        (rng.standard_normal(2000) * 1e-30).astype(np.float32),
+        (rng.standard_normal(2000) * 1e-39).astype(np.float32),   # fp32 subnormals
+        np.array([0.0, -0.0, 1.0, 65504.0, 3e38, -3e38], dtype=np.float32),
+    ])
+    # exact ties: low 16 bits = 0x8000, both even and odd kept parts
+    bits = rng.integers(0, 2**31, size=4000, dtype=np.uint32) & np.uint32(0xFFFF0000)
+    bits = bits | np.uint32(0x8000)
+    ties = bits.view(np.float32)
+    ties = ties[np.isfinite(ties)]
+    x = np.concatenate([x, ties])
+    want = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    got = round_bf16(x.astype(np.float64))
+    assert np.array_equal(got, want)
+
+
+def test_round_bf16_on_fp64_values_is_single_rounding():
+    # 1 + 2^-8 + 2^-40 lies just above the tie between 1 and 1 + 2^-7:
+    # correct rounding goes up; rounding via fp32 first would hit the tie and
+    # go to even (1).
+    v = 1.0 + 2.0 ** -8 + 2.0 ** -40
+    assert round_bf16(np.array([v]))[0] == 1.0 + 2.0 ** -7
+    assert round_bf16(np.array([1.0 + 2.0 ** -8]))[0] == 1.0          # tie -> even
+    assert round_bf16(np.array([1.0 + 3 * 2.0 ** -8]))[0] == 1.0 + 2.0 ** -6  # tie -> even
+
+
+# ------------------------------------------------------ textbook definitions
+
+def _conv_loops(x, w, b):
+    Bt, H, W, Ci = x.shape
+    Co = w.shape[0]
+    y = np.zeros((Bt, H, W, Co))
+    for n in range(Bt):
+        for h in range(H):
+            for ww in range(W):
+                for o in range(Co):
+                    acc = b[o]
+                    for r in range(3):
+                        for s in range(3):
+                            hh, wc = h + r - 1, ww + s - 1
+                            if 0 <= hh < H and 0 <= wc < W:
+                                acc += np.dot(x[n, hh, wc, :], w[o, r, s, :])
+                    y[n, h, ww, o] = acc
+    return y
+
+
+def test_conv_forward_matches_loops():
+    rng = np.random.default_rng(1)
+    x = rng.standard_normal((2, 5, 4, 3))
+    w = rng.standard_normal((4, 3, 3, 3))
+    b = rng.standard_normal(4)
+    assert np.allclose(conv3x3_forward(x, w, b), _conv_loops(x, w, b), rtol=1e-13, atol=1e-13)
+
+
+def test_conv_backward_matches_loops():
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((2, 4, 3, 2))
+    w = rng.standard_normal((3, 3, 3, 2))
+    gp = rng.standard_normal((2, 4, 3, 3))
+    dx, dw, db = conv3x3_backward(x, w, gp)
+    Bt, H, W, Ci = x.shape
+    edx = np.zeros_like(x)
+    edw = np.zeros_like(w)
+    for n in range(Bt):
+        for h in range(H):
+            for ww in range(W):
+                for o in range(3):
+                    for r in range(3):
+                        for s in range(3):
+                            hh, wc = h + r - 1, ww + s - 1
+                            if 0 <= hh < H and 0 <= wc < W:
+                                edw[o, r, s, :] += gp[n, h, ww, o] * x[n, hh, wc, :]
+                                edx[n, hh, wc, :] += gp[n, h, ww, o] * w[o, r, s, :]
+    assert np.allclose(dx, edx, atol=1e-13)
+    assert np.allclose(dw, edw, atol=1e-13)
+    assert np.allclose(db, gp.sum(axis=(0, 1, 2)), atol=1e-13)
+
+
+def test_maxpool_first_max_tie_rule():
+    x = np.zeros((1, 2, 4, 1))
+    # window 0: (0,0)=1, (0,1)=3, (1,0)=3, (1,1)=2 -> first max is (0,1)
+    x[0, 0, 0, 0], x[0, 0, 1, 0], x[0, 1, 0, 0], x[0, 1, 1, 0] = 1, 3, 3, 2
+    # window 1: all equal -> (0,0)
+    x[0, :, 2:, 0] = 5
+    z, arg = maxpool2_forward(x)
+    assert z[0, 0, :, 0].tolist() == [3, 5]
+    assert arg[0, 0, :, 0].tolist() == [1, 0]
+    g = maxpool2_backward(np.array([[[[7.0], [9.0]]]]), arg)
+    want = np.zeros((1, 2, 4, 1))
+    want[0, 0, 1, 0] = 7
+    want[0, 0, 2, 0] = 9
+    assert np.array_equal(g, want)
+
+
+def test_softmax_xent_matches_torch():
+    rng = np.random.default_rng(3)
+    logits = rng.standard_normal((9, 5)) * 4
+    y = rng.integers(0, 5, size=9)
+    loss, d = softmax_xent(logits, y)
+    t = torch.tensor(logits, requires_grad=True)
+    tl = tF.cross_entropy(t, torch.tensor(y))
+    tl.backward()
+    assert loss == pytest.approx(tl.item(), rel=1e-14)
+    assert np.allclose(d, t.grad.numpy(), atol=1e-15)
+
+
+# ------------------------------------------------- whole-step pins (fp64)
+
+def _batch(cfg, B=None, seed=0):
+    images, labels, _ = make_dataset(cfg)
+    rng = np.random.default_rng(seed)
+    idx = rng.choice(len(labels), size=B or cfg["B"], replace=False)
+    return images[idx].astype(np.float64), labels[idx].astype(np.int64)
+
+
+class _RoundFwd(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, x):
+        return torch.from_numpy(round_bf16(x.detach().numpy()))
+
+    @staticmethod
+    def backward(ctx, g):
+        return g
+
+
+class _RoundBwd(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, x):
+        return x.clone()
+
+    @staticmethod
+    def backward(ctx, g):
+        return torch.from_numpy(round_bf16(g.detach().numpy()))
+
+
+def torch_split_model_loss(cfg, theta, x, y):
+    """Loss and gradient of the unsplit CNN via torch.autograd in fp64.
+
+    bf16 workloads insert rounding nodes at the documented points: forward
+    rounding of inputs, weights, conv outputs and the pooled feature;
+    backward rounding of each conv's pre-activation gradient and of the
+    gradient a conv returns for its input."""
+    bf16 = cfg["dtype"] == "bf16"
+    rf = _RoundFwd.apply if bf16 else (lambda t: t)
+    rb = _RoundBwd.apply if bf16 else (lambda t: t)
+    th = torch.tensor(np.asarray(theta, dtype=np.float64), requires_grad=True)
+    views = {}
+    for i, tag, shp, off in param_layout(cfg):
+        n = int(np.prod(shp))
+        views.setdefault(i, {})[tag] = th[off:off + n].reshape(shp)
+    a = rf(torch.tensor(x).permute(0, 3, 1, 2))
+    for i, spec in enumerate(cfg["layers"]):
+        if spec[0] == "conv":
+            a_in = rb(a) if i > 0 else a
+            w = rf(views[i]["w"]).permute(0, 3, 1, 2)
+            pre = tF.conv2d(a_in, w, views[i]["b"], padding=1)
+            if spec[3]:
+                pre = pre + a_in
+            a = rf(torch.relu(rb(pre)))
+        elif spec[0] == "maxpool":
+            a = tF.max_pool2d(a, 2)
+        elif spec[0] == "avgpool":
+            a = rf(a.mean(dim=(2, 3)))
+        elif spec[0] == "linear":
+            a = a @ rf(views[i]["w"]).T + views[i]["b"]
+    loss = tF.cross_entropy(a, torch.tensor(y))
+    loss.backward()
+    return loss.item(), th.grad.numpy()
+
+
+@pytest.mark.parametrize("name", ["tiny", "ragged", "ragged_bf16"])
+def test_split_step_matches_torch_autograd(name):
+    cfg = get_config(name)
+    theta = init_params(cfg)
+    x, y = _batch(cfg)
+    loss, grad, _ = split_forward_backward(cfg, theta, x, y)
+    tloss, tgrad = torch_split_model_loss(cfg, theta, x, y)
+    assert loss == pytest.approx(tloss, rel=1e-12)
+    for i, tag, shp, off in param_layout(cfg):
+        n = int(np.prod(shp))
+        a, b = grad[off:off + n], tgrad[off:off + n]
+        assert np.allclose(a, b, rtol=1e-9, atol=1e-12 * np.abs(b).max()), (i, tag)
+
+
+def test_split_step_matches_torch_autograd_wide_residual_server():
+    # the 16-cluster server stack (64->256, three residual 256->256) on a
+    # reduced batch and image size
+    cfg = get_config("gcpsl16", dtype="f32", H=8, W=8, N_ex=200, B=4)
+    theta = init_params(cfg)
+    x, y = _batch(cfg)
+    loss, grad, _ = split_forward_backward(cfg, theta, x, y)
+    tloss, tgrad = torch_split_model_loss(cfg, theta, x, y)
+    assert loss == pytest.approx(tloss, rel=1e-12)
+    assert np.allclose(grad, tgrad, rtol=1e-9, atol=1e-12 * np.abs(tgrad).max())
+
+
+def test_split_step_finite_differences():
+    cfg = get_config("tiny")
+    theta = init_params(cfg).astype(np.float64)
+    x, y = _batch(cfg, seed=5)
+    loss, grad, rec = split_forward_backward(cfg, theta, x, y, keep=True)
+    # guard: no ReLU pre-activation and no max-pool runner-up within reach of
+    # the perturbation, so the loss is smooth around theta
+    for key, v in rec.items():
+        if key.startswith("pre"):
+            assert np.abs(v).min() > 1e-6, key
+    for i, spec in enumerate(cfg["layers"]):
+        if spec[0] == "maxpool":
+            a = rec["acts"][i]
+            Bt, H, W, C = a.shape
+            win = np.sort(a.reshape(Bt, H // 2, 2, W // 2, 2, C).transpose(0, 1, 3, 5, 2, 4)
+                          .reshape(-1, 4), axis=1)
+            live = win[:, 3] > 0
+            assert (win[live, 3] - win[live, 2]).min() > 1e-6
+    rng = np.random.default_rng(0)
+    coords = rng.choice(len(theta), size=60, replace=False)
+    h = 1e-6
+    for j in coords:
+        tp, tm = theta.copy(), theta.copy()
+        tp[j] += h
+        tm[j] -= h
+        fd = (split_forward_backward(cfg, tp, x, y)[0] - split_forward_backward(cfg, tm, x, y)[0]) / (2 * h)
+        assert abs(fd - grad[j]) <= 1e-8 + 1e-6 * abs(grad[j]), (j, fd, grad[j])

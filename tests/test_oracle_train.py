@@ -1,0 +1,95 @@
+"""Pins for the oracle's SGD update, fusion (Eq. 5) and the training loop (Alg. 2)."""
+import numpy as np
+import pytest
+import torch
+
+from gcpsl_inputs import get_config, init_params
+from oracle.train import GCPSLOracle, fuse, sgd_update
+
+
+def test_sgd_two_steps_closed_form():
+    # v1 = g0, theta1 = theta0 - lr g0; v2 = mu g0 + g1, theta2 = theta1 - lr v2
+    theta = np.array([1.0, -2.0], dtype=np.float32)
+    mom = np.zeros(2, dtype=np.float32)
+    sgd_update(theta, mom, np.array([0.5, 0.25]), 0.1, 0.9)
+    assert np.allclose(theta, [0.95, -2.025], rtol=1e-7)
+    sgd_update(theta, mom, np.array([-1.0, 2.0]), 0.1, 0.9)
+    assert np.allclose(mom, [-0.55, 2.225], rtol=1e-7)
+    assert np.allclose(theta, [1.005, -2.2475], rtol=1e-7)
+
+
+def test_sgd_matches_torch_optimizer():
+    rng = np.random.default_rng(0)
+    t0 = rng.standard_normal(50).astype(np.float32)
+    grads = [rng.standard_normal(50) for _ in range(4)]
+    theta, mom = t0.copy(), np.zeros(50, dtype=np.float32)
+    p = torch.nn.Parameter(torch.tensor(t0, dtype=torch.float64))
+    opt = torch.optim.SGD([p], lr=0.05, momentum=0.9)
+    for g in grads:
+        sgd_update(theta, mom, g, 0.05, 0.9)
+        p.grad = torch.tensor(g)
+        opt.step()
+    assert np.allclose(theta, p.detach().numpy(), rtol=1e-6, atol=1e-7)
+
+
+def test_fusion_worked_example():
+    # weights 1, 2, 5 (W = 8): (1*[8,0] + 2*[0,4] + 5*[0.8,-1.6]) / 8 = [1.5, 0]
+    th = [np.array([8.0, 0.0], np.float32), np.array([0.0, 4.0], np.float32),
+          np.array([0.8, -1.6], np.float32)]
+    assert np.allclose(fuse(th, [1, 2, 5]), [1.5, 0.0], atol=1e-7)
+
+
+def test_fusion_of_identical_replicas_is_bit_exact_identity():
+    rng = np.random.default_rng(1)
+    t = (rng.standard_normal(100000) * np.exp(rng.uniform(-20, 20, 100000))).astype(np.float32)
+    for weights in ([12544, 13151, 13337, 10968], [1, 1], [155, 11279, 7, 3, 99991]):
+        out = fuse([t.copy() for _ in weights], weights)
+        assert out.dtype == np.float32 and np.array_equal(out, t)
+
+
+def test_fusion_weights_sum_to_one_exactly():
+    # constant replicas c_n: the result is the exact weighted mean
+    w = [3, 5, 8]
+    th = [np.full(4, c, np.float32) for c in (1.0, 2.0, 4.0)]
+    assert np.all(fuse(th, w) == np.float32((3 * 1 + 5 * 2 + 8 * 4) / 16))
+
+
+def test_single_cluster_gcpsl_equals_gpsl():
+    # C = 1: fusion over one replica is the identity, so any fusion interval
+    # gives the GPSL run bit for bit
+    cfg = get_config("tiny", C=1)
+    a = GCPSLOracle(cfg).run(6, F=2)
+    b = GCPSLOracle(cfg).run(6, F=0)
+    assert np.array_equal(a.theta[0], b.theta[0])
+    assert a.losses == b.losses
+
+
+def test_fusion_leaves_momentum_local_and_replicas_equal():
+    cfg = get_config("tiny")
+    o = GCPSLOracle(cfg).run(5, F=5)
+    assert np.array_equal(o.theta[0], o.theta[1])
+    assert not np.array_equal(o.mom[0], o.mom[1]) or cfg["momentum"] == 0.0
+    cfg = get_config("ragged")
+    o = GCPSLOracle(cfg).run(3, F=3)
+    assert all(np.array_equal(o.theta[0], t) for t in o.theta)
+    assert not np.array_equal(o.mom[0], o.mom[1])
+
+
+def test_replicas_start_equal_and_train_apart():
+    cfg = get_config("ragged")
+    o = GCPSLOracle(cfg)
+    t0 = init_params(cfg)
+    assert all(np.array_equal(t, t0) for t in o.theta)
+    o.run(2, F=0)
+    assert not np.array_equal(o.theta[0], o.theta[1])
+    assert len(o.active) == 2 and all(1 <= a <= cfg["B"] for row in o.active for a in row)
+
+
+def test_tiny_workload_learns():
+    # The class-mean images are separable: 200 rounds must take the mean
+    # loss well below the chance level log(4).
+    cfg = get_config("tiny")
+    o = GCPSLOracle(cfg).run(200)
+    L = np.array(o.losses).mean(axis=1)
+    assert abs(L[:5].mean() - np.log(4)) < 0.1
+    assert L[-20:].mean() < 0.5
