@@ -1,0 +1,225 @@
+/*
+ * gcpsl.h -- C ABI of the GCPSL hot path on one MI355X (gfx950).
+ *
+ * GCPSL (Kohankhaki, Rentschler, Schmeink, "Concurrent Split Learning Through
+ * Stable Client Clustering") assigns K stable clients to C fixed clusters
+ * (Alg. 1), runs one GPSL workload with batch B per cluster (Sec. IV-B,
+ * Alg. 2) and periodically fuses the client and server segments of the
+ * cluster replicas with sample-count weights (Eq. 5).  This library runs all
+ * C cluster workloads side by side on one GPU: every kernel is batched over
+ * the replica index.
+ *
+ * Conventions shared by every call:
+ *   - Return value: GCPSL_OK (0) or a negative GCPSL_E* code.  On error,
+ *     gcpsl_last_error() returns a thread-local message describing it.  No
+ *     call aborts, throws or prints.
+ *   - Device memory is owned by the caller.  The library never allocates
+ *     device memory: it works in the caller's buffers and in one caller-owned
+ *     workspace of gcpsl_workspace_bytes() bytes.  Device pointers passed to
+ *     gcpsl_create must stay valid until gcpsl_destroy.
+ *   - Device work is enqueued on the caller's HIP stream (hipStream_t passed
+ *     as void*; NULL is the default stream) and returns without waiting.
+ *     Argument and state errors are reported synchronously, before any work
+ *     is enqueued.  A failed kernel launch returns GCPSL_EHIP.
+ *   - A context is not thread-safe: calls on one context must not overlap.
+ *
+ * Layouts: activations are NHWC.  Parameters of one replica form one flat
+ * fp32 vector of P entries: for every conv / linear layer in order, its weight
+ * then its bias; conv weights are [cout][3][3][cin], linear weights
+ * [cout][cin].  The client segment's parameters come first (P_client entries).
+ */
+#ifndef GCPSL_H
+#define GCPSL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GCPSL_OK 0
+#define GCPSL_EINVAL (-1)       /* bad argument: sizes, null pointers, rule   */
+#define GCPSL_ESTATE (-2)       /* call out of order (e.g. step not sampled) */
+#define GCPSL_EHIP (-3)         /* HIP runtime or launch error               */
+#define GCPSL_EUNSUPPORTED (-4) /* valid request outside what is implemented */
+
+/* Assignment rules of Alg. 1 (Sec. IV-A). */
+#define GCPSL_RULE_RANDOM 0   /* permute, then round-robin                   */
+#define GCPSL_RULE_SIZE 1     /* size-balanced: lightest allowed cluster     */
+#define GCPSL_RULE_LABEL_L1 2 /* greedy label-histogram L1 placement         */
+
+/* Compute precisions. */
+#define GCPSL_F32 0  /* fp32 activations and weights                        */
+#define GCPSL_BF16 1 /* bf16 activations and weights, fp32 master weights   */
+
+/* Layer kinds of the split CNN. */
+#define GCPSL_CONV3X3 1 /* 3x3, stride 1, zero pad 1, bias, ReLU            */
+#define GCPSL_MAXPOOL2 2 /* 2x2 max pool, stride 2                           */
+#define GCPSL_AVGPOOL 3  /* global average pool                              */
+#define GCPSL_LINEAR 4   /* fully connected layer producing the logits       */
+
+/* Layer flags. */
+#define GCPSL_RESIDUAL 1 /* conv output is ReLU(conv(x) + b + x); cin == cout */
+
+typedef struct gcpsl_layer {
+  int32_t kind;  /* GCPSL_CONV3X3 ... GCPSL_LINEAR                         */
+  int32_t cin;   /* input channels (conv, linear); ignored for pools       */
+  int32_t cout;  /* output channels (conv, linear); ignored for pools      */
+  int32_t flags; /* GCPSL_RESIDUAL or 0                                    */
+} gcpsl_layer;
+
+/*
+ * Supported model shapes: layer 0 is a conv; every max pool follows a conv and
+ * sees an even H and W; the last two layers are GCPSL_AVGPOOL then
+ * GCPSL_LINEAR (cout = L), optionally preceded by one max pool; conv channel
+ * counts are either 3 (the image layer) or multiples of 8.  Other shapes
+ * return GCPSL_EUNSUPPORTED.
+ */
+typedef struct gcpsl_desc {
+  int32_t K;          /* clients (Sec. III-A), 1..65536                     */
+  int32_t C;          /* clusters = concurrent replicas, 1..1024            */
+  int32_t B;          /* examples per cluster batch (Eq. 3), >= 1           */
+  int32_t L;          /* classes                                            */
+  int32_t H, W, Cin;  /* image shape (NHWC)                                 */
+  int32_t dtype;      /* GCPSL_F32 or GCPSL_BF16                            */
+  int64_t n_examples; /* |D|                                                */
+  int32_t n_layers;   /* entries of `layers`                                */
+  int32_t cut;        /* client segment = layers[0, cut)                    */
+  const gcpsl_layer *layers; /* host, copied at create                      */
+  float lr;           /* SGD learning rate                                  */
+  float momentum;     /* SGD momentum mu: v <- mu v + g, theta -= lr v      */
+  uint64_t seed;      /* sampler seed                                       */
+  int64_t max_steps;  /* rows of the participation table (steps recorded)   */
+  int32_t max_window; /* largest nsteps accepted by gcpsl_sample, >= 1      */
+  int32_t reserved;   /* must be 0                                          */
+  const int32_t *client_of_example; /* host [n_examples], in [0, K)         */
+  const int32_t *cluster_of_client; /* host [K], in [0, C) (Alg. 1 output)  */
+  const float *images;   /* device [n_examples][H][W][Cin] fp32             */
+  const int32_t *labels; /* device [n_examples], in [0, L)                  */
+  float *theta;          /* device [C][P] fp32 masters, in/out              */
+  float *momentum_buf;   /* device [C][P] fp32 momentum, in/out             */
+  void *workspace;       /* device, >= gcpsl_workspace_bytes(), 256-aligned */
+  size_t workspace_bytes;
+} gcpsl_desc;
+
+typedef struct gcpsl_ctx gcpsl_ctx;
+
+/* Parameter counts of one replica: P (total) and P_client (entries of the
+ * client segment, which come first).  Host only.  EINVAL / EUNSUPPORTED on a
+ * bad model description. */
+int gcpsl_param_count(const gcpsl_desc *d, int64_t *P, int64_t *P_client);
+
+/* Workspace size in bytes for this description.  Host only. */
+int gcpsl_workspace_bytes(const gcpsl_desc *d, size_t *bytes);
+
+/*
+ * Static client clustering, Alg. 1 (Sec. IV-A).  Host only, no device work.
+ *   rule RANDOM:   Fisher-Yates permutation of the clients (SplitMix64 stream
+ *                  seeded with seed + 0x41535349474E, bounded draws by
+ *                  Lemire's multiply-shift with rejection), then client
+ *                  perm[i] -> cluster i mod C.  counts/hist may be NULL.
+ *   rule SIZE:     clients in (count desc, id asc) order, each to the allowed
+ *                  cluster (fewer than ceil(K/C) clients) with the smallest
+ *                  summed count, ties to the lower index.  Needs counts.
+ *   rule LABEL_L1: same order; each client with samples goes to the allowed
+ *                  cluster whose label histogram after placement has the
+ *                  smallest L1 distance between normalised histograms and
+ *                  the global one (exact integer comparison), ties to the
+ *                  smaller summed count, then the lower index; a client with
+ *                  no samples goes to the allowed cluster with the fewest
+ *                  clients.  Needs counts and hist.
+ * counts: host [K] int64 sample counts; hist: host [K][L] int64 class
+ * histograms (row k sums to counts[k]); cluster_of_client: host [K] output,
+ * caller-owned.  EINVAL on K < 1, C < 1, C > K, unknown rule, missing
+ * metadata or negative counts.
+ */
+int gcpsl_assign(int32_t K, int32_t C, int32_t rule, uint64_t seed, const int64_t *counts,
+                 const int64_t *hist, int32_t L, int32_t *cluster_of_client);
+
+/*
+ * Create a context: validates the description, builds each cluster's example
+ * list (ascending global id) and its fusion weight n_n = |D_{C_n}| (Eq. 5),
+ * and uploads them into the workspace (synchronous copies).  Replicas are not
+ * initialised here: the caller fills theta with C equal copies (Alg. 2,
+ * "initialize all split-model replicas equally") and zeroes momentum_buf.
+ * EINVAL if any cluster holds fewer than B examples, on null pointers,
+ * out-of-range ids or a too-small workspace; EUNSUPPORTED on an unsupported
+ * model shape; EHIP on a failed copy.
+ */
+int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out);
+
+/*
+ * Cluster-local global sampling (Eq. 1, Eq. 3) for local rounds
+ * [step, step + nsteps), with the gather of the sampled images and labels.
+ * Cluster n draws its batch from its own pooled examples: epoch
+ * e = step / S_n, S_n = floor(n_n / B), takes positions [tB, (t+1)B),
+ * t = step mod S_n, of a keyed Feistel permutation of [0, n_n) (key from
+ * seed, n, e); so every batch has exactly B distinct examples of the cluster.
+ * Also records |A_{n,t}| (clients supplying >= 1 example, Sec. III-A) for
+ * each sampled step below max_steps.
+ * idx_out: device [nsteps][C][B] int32 global example ids, or NULL.
+ * The gathered inputs stay staged until the next gcpsl_sample call; each
+ * staged step can then be run once or more by gcpsl_step.
+ * EINVAL: step < 0, nsteps < 1 or > max_window.
+ */
+int gcpsl_sample(gcpsl_ctx *ctx, int64_t step, int32_t nsteps, int32_t *idx_out, void *stream);
+
+/*
+ * One local round of every cluster (Alg. 2 inner loop): client-segment
+ * forward to the cut, server-segment forward, softmax cross-entropy (mean
+ * over B), server backward, cut-gradient hand-off (same buffer on one GPU),
+ * client backward, and the SGD update of both segments of every replica
+ * (v <- mu v + g; theta <- theta - lr v).  The client gradient is that of
+ * the batch-mean loss, which is the b_k/B-weighted average of the active
+ * clients' gradients (Sec. III-B).
+ * loss_out: device [C] fp32, the forward loss of each cluster before the
+ * update, or NULL.  ESTATE if `step` is not among the staged steps.
+ */
+int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *stream);
+
+/*
+ * Fusion and broadcast, Eq. 5 (Sec. IV-D): theta_bar = sum_n (n_n / W)
+ * theta_n over both segments, accumulated in fp64 in cluster order, divided
+ * once by W = sum_n n_n and rounded once to fp32, then written to every
+ * replica.  Momentum is not touched (optimizer state stays local).
+ */
+int gcpsl_fuse(gcpsl_ctx *ctx, void *stream);
+
+/*
+ * Direct data participation (Sec. V-E): over the recorded horizon
+ * [0, T_h), T_h = 1 + the largest step run by gcpsl_step (capped at
+ * max_steps), active_slots = sum_t sum_n |A_{n,t}| and total_slots = K T_h;
+ * participation = active / total.  per_step: host [T_h][C] int32 or NULL
+ * (caller-owned, at least max_steps * C entries).  Synchronises the device.
+ */
+int gcpsl_participation(gcpsl_ctx *ctx, int64_t *active_slots, int64_t *total_slots,
+                        int32_t *per_step);
+
+/* Host copy of the per-cluster example counts n_n: sizes host [C] int64. */
+int gcpsl_cluster_sizes(gcpsl_ctx *ctx, int64_t *sizes);
+
+/*
+ * Device view of a named workspace tensor, for inspection by tests.  Names:
+ * "x" (staged inputs [max_window][C][B][H][W][Cin]), "idx", "y"
+ * ([max_window][C][B] int32), "hits" ([max_steps][C] int32, |A_{n,t}| of
+ * every sampled step), "act<i>" (output of layer i, [C][B][...]),
+ * "gpre<i>" (gradient w.r.t. conv layer i's pre-activation), "gin<i>"
+ * (gradient w.r.t. the input of conv layer i when layer i-1 is a max pool),
+ * "dh" ([C][B][channels] fp32 gradient of the pooled feature), "grad"
+ * ([C][P] fp32 last gradient).  dtype receives GCPSL_F32, GCPSL_BF16 or -1
+ * for int32.  EINVAL on an unknown name.
+ */
+int gcpsl_tensor(gcpsl_ctx *ctx, const char *name, void **ptr, int64_t *numel, int32_t *dtype);
+
+/* Release the context (host metadata only; device memory is the caller's). */
+void gcpsl_destroy(gcpsl_ctx *ctx);
+
+/* Thread-local description of the last error, "" if none. */
+const char *gcpsl_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GCPSL_H */

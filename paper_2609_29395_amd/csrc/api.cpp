@@ -1,0 +1,524 @@
+// Host runtime of the C ABI: model plan, workspace layout and the order of
+// kernel launches for sampling, one local round, fusion and participation.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "runtime.h"
+
+// ------------------------------------------------------------------ errors
+namespace {
+thread_local std::string g_err;
+}
+void gcpsl_clear_error() { g_err.clear(); }
+int gcpsl_fail(int code, const std::string &msg) {
+  g_err = msg;
+  return code;
+}
+extern "C" const char *gcpsl_last_error(void) { return g_err.c_str(); }
+
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+struct LayerInfo {
+  gcpsl_layer spec{};
+  int H = 0, W = 0, Ci = 0;   // input geometry (per example)
+  int Ho = 0, Wo = 0, Co = 0; // output geometry
+  int64_t w_off = -1, b_off = -1, nw = 0;
+  bool stored = false;        // output activation kept in the workspace
+  size_t act_off = 0;
+  int64_t act_rs = 0;         // elements per replica of the output
+  size_t gpre_off = 0, gin_off = 0, wf_off = 0, wd_off = 0;
+  bool has_gin = false;
+  int Kp = 0, Kdp = 0;
+  int splits = 1, chunk = 0;
+};
+
+struct Plan {
+  int dtype = 0, esz = 4;
+  int K = 0, C = 0, B = 0, L = 0, H = 0, W = 0, Cin = 0;
+  int64_t n_examples = 0, max_steps = 0;
+  int max_window = 1;
+  std::vector<LayerInfo> ly;
+  int64_t P = 0, Pc = 0;
+  int head_conv = -1, avg_idx = -1, lin_idx = -1;
+  bool head_maxpool = false;
+  int Ch_head = 0;
+  int64_t x_rs = 0;  // elements of one staged step: C * B * H * W * Cin
+  size_t off_ids = 0, off_off = 0, off_coe = 0, off_fw = 0, off_hits = 0, off_idx = 0, off_y = 0,
+         off_x = 0, off_dh = 0, off_grad = 0, off_part = 0, off_dbpart = 0, off_loss = 0;
+  size_t total = 0;
+};
+
+int build_plan(const gcpsl_desc *d, Plan &p) {
+  if (!d) return gcpsl_fail(GCPSL_EINVAL, "null description");
+  if (d->dtype != GCPSL_F32 && d->dtype != GCPSL_BF16) return gcpsl_fail(GCPSL_EINVAL, "unknown dtype");
+  if (d->K < 1 || d->K > 65536) return gcpsl_fail(GCPSL_EINVAL, "K must be in [1, 65536]");
+  if (d->C < 1 || d->C > 1024) return gcpsl_fail(GCPSL_EINVAL, "C must be in [1, 1024]");
+  if (d->C > d->K) return gcpsl_fail(GCPSL_EINVAL, "C must not exceed K");
+  if (d->B < 1 || d->L < 2 || d->H < 1 || d->W < 1 || d->Cin < 1)
+    return gcpsl_fail(GCPSL_EINVAL, "B, L, H, W, Cin out of range");
+  if (d->n_examples < 1 || d->n_examples > INT32_MAX)
+    return gcpsl_fail(GCPSL_EINVAL, "n_examples must be in [1, 2^31)");
+  if (d->max_steps < 1 || d->max_window < 1) return gcpsl_fail(GCPSL_EINVAL, "max_steps and max_window must be >= 1");
+  if (d->reserved != 0) return gcpsl_fail(GCPSL_EINVAL, "reserved must be 0");
+  if (!d->layers || d->n_layers < 3) return gcpsl_fail(GCPSL_EINVAL, "need at least conv, avgpool, linear");
+  if (d->cut < 1 || d->cut > d->n_layers - 2) return gcpsl_fail(GCPSL_EINVAL, "cut outside the model");
+  if ((int64_t)d->B * d->H * d->W > INT32_MAX / 4) return gcpsl_fail(GCPSL_EUNSUPPORTED, "batch too large");
+
+  p.dtype = d->dtype;
+  p.esz = d->dtype == GCPSL_BF16 ? 2 : 4;
+  p.K = d->K; p.C = d->C; p.B = d->B; p.L = d->L; p.H = d->H; p.W = d->W; p.Cin = d->Cin;
+  p.n_examples = d->n_examples;
+  p.max_steps = d->max_steps;
+  p.max_window = d->max_window;
+  const int n = d->n_layers;
+  p.ly.assign(n, LayerInfo());
+  int H = d->H, W = d->W, c = d->Cin;
+  int64_t P = 0;
+  for (int i = 0; i < n; ++i) {
+    LayerInfo &l = p.ly[i];
+    l.spec = d->layers[i];
+    l.H = H; l.W = W; l.Ci = c;
+    const int kind = l.spec.kind;
+    if (kind == GCPSL_CONV3X3) {
+      if (l.spec.cin != c) return gcpsl_fail(GCPSL_EINVAL, "conv cin does not match its input");
+      if (!(c == 3 && i == 0) && c % 8 != 0)
+        return gcpsl_fail(GCPSL_EUNSUPPORTED, "conv cin must be a multiple of 8 (or 3 for layer 0)");
+      if (l.spec.cout < 8 || l.spec.cout % 8 != 0)
+        return gcpsl_fail(GCPSL_EUNSUPPORTED, "conv cout must be a positive multiple of 8");
+      if ((l.spec.flags & GCPSL_RESIDUAL) && l.spec.cin != l.spec.cout)
+        return gcpsl_fail(GCPSL_EINVAL, "residual conv needs cin == cout");
+      if (l.spec.flags & ~GCPSL_RESIDUAL) return gcpsl_fail(GCPSL_EINVAL, "unknown layer flag");
+      if (i > 0 && p.ly[i - 1].spec.kind != GCPSL_CONV3X3 && p.ly[i - 1].spec.kind != GCPSL_MAXPOOL2)
+        return gcpsl_fail(GCPSL_EUNSUPPORTED, "conv must follow a conv or a max pool");
+      l.Co = l.spec.cout; l.Ho = H; l.Wo = W;
+      l.nw = (int64_t)l.Co * 9 * l.Ci;
+      l.w_off = P; P += l.nw;
+      l.b_off = P; P += l.Co;
+      c = l.Co;
+    } else if (kind == GCPSL_MAXPOOL2) {
+      if (i == 0 || p.ly[i - 1].spec.kind != GCPSL_CONV3X3)
+        return gcpsl_fail(GCPSL_EUNSUPPORTED, "max pool must follow a conv");
+      if (H % 2 || W % 2) return gcpsl_fail(GCPSL_EINVAL, "max pool needs even H and W");
+      H /= 2; W /= 2;
+      l.Co = c; l.Ho = H; l.Wo = W;
+    } else if (kind == GCPSL_AVGPOOL) {
+      if (i != n - 2) return gcpsl_fail(GCPSL_EUNSUPPORTED, "avgpool must be the second-to-last layer");
+      l.Co = c; l.Ho = 1; l.Wo = 1;
+    } else if (kind == GCPSL_LINEAR) {
+      if (i != n - 1) return gcpsl_fail(GCPSL_EUNSUPPORTED, "linear must be the last layer");
+      if (l.spec.cin != c || l.spec.cout != d->L)
+        return gcpsl_fail(GCPSL_EINVAL, "linear must map the pooled channels to L classes");
+      l.Co = l.spec.cout; l.Ho = 1; l.Wo = 1;
+      l.nw = (int64_t)l.Co * l.Ci;
+      l.w_off = P; P += l.nw;
+      l.b_off = P; P += l.Co;
+    } else {
+      return gcpsl_fail(GCPSL_EINVAL, "unknown layer kind");
+    }
+    if (i == d->cut - 1) p.Pc = P;
+  }
+  if (d->layers[0].kind != GCPSL_CONV3X3) return gcpsl_fail(GCPSL_EUNSUPPORTED, "layer 0 must be a conv");
+  p.P = P;
+  p.avg_idx = n - 2;
+  p.lin_idx = n - 1;
+  if (p.ly[n - 3].spec.kind == GCPSL_MAXPOOL2) {
+    p.head_maxpool = true;
+    p.head_conv = n - 4;
+  } else {
+    p.head_conv = n - 3;
+  }
+  if (p.head_conv < 0 || p.ly[p.head_conv].spec.kind != GCPSL_CONV3X3)
+    return gcpsl_fail(GCPSL_EUNSUPPORTED, "avgpool must follow a conv or a conv + max pool");
+  p.Ch_head = p.ly[p.head_conv].Co;
+
+  // workspace layout
+  const int C = p.C, B = p.B;
+  const int bk = p.dtype == GCPSL_BF16 ? 64 : 32;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  p.off_ids = take(sizeof(int32_t) * p.n_examples);
+  p.off_off = take(sizeof(int64_t) * (C + 1));
+  p.off_coe = take(sizeof(int32_t) * p.n_examples);
+  p.off_fw = take(sizeof(double) * C);
+  p.off_hits = take(sizeof(int32_t) * p.max_steps * C);
+  p.off_idx = take(sizeof(int32_t) * (size_t)p.max_window * C * B);
+  p.off_y = take(sizeof(int32_t) * (size_t)p.max_window * C * B);
+  p.x_rs = (int64_t)C * B * p.H * p.W * p.Cin;
+  p.off_x = take((size_t)p.esz * p.max_window * p.x_rs);
+  size_t part = 0, dbpart = 0;
+  for (int i = 0; i < n; ++i) {
+    LayerInfo &l = p.ly[i];
+    const int kind = l.spec.kind;
+    if (kind == GCPSL_CONV3X3 || (kind == GCPSL_MAXPOOL2 && !(p.head_maxpool && i == n - 3))) {
+      l.stored = true;
+      l.act_rs = (int64_t)B * l.Ho * l.Wo * l.Co;
+      l.act_off = take((size_t)p.esz * C * l.act_rs);
+    } else if (kind == GCPSL_AVGPOOL) {
+      l.stored = true;
+      l.act_rs = (int64_t)B * l.Co;
+      l.act_off = take((size_t)p.esz * C * l.act_rs);
+    }
+    if (kind == GCPSL_CONV3X3) {
+      const int64_t rs = (int64_t)B * l.H * l.W;
+      l.gpre_off = take((size_t)p.esz * C * rs * l.Co);
+      if (i > 0 && p.ly[i - 1].spec.kind == GCPSL_MAXPOOL2) {
+        l.has_gin = true;
+        l.gin_off = take((size_t)p.esz * C * rs * l.Ci);
+      }
+      l.Kp = round_up(9 * l.Ci, bk);
+      l.wf_off = take((size_t)p.esz * C * l.Co * l.Kp);
+      if (i > 0) {
+        l.Kdp = round_up(9 * l.Co, bk);
+        l.wd_off = take((size_t)p.esz * C * l.Ci * l.Kdp);
+      }
+      // split-K over pixels for the weight gradient
+      const int M = B * l.H * l.W;
+      const int kt = wgrad_k_tile(p.dtype);
+      const int nkt = (M + kt - 1) / kt;
+      const int bm = l.Co > 64 ? 128 : (l.Co > 32 ? 64 : 32);
+      const int nwc = 9 * l.Ci;
+      const int bn = nwc > 64 ? 128 : (nwc > 32 ? 64 : 32);
+      const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
+      int splits = (int)std::min<int64_t>(std::max(1, nkt / 4), (1024 + tiles - 1) / tiles);
+      splits = std::max(1, splits);
+      const int per = (nkt + splits - 1) / splits;
+      l.chunk = per * kt;
+      l.splits = (M + l.chunk - 1) / l.chunk;
+      if (l.splits > 1) {
+        part = std::max(part, (size_t)l.splits * C * l.nw);
+        dbpart = std::max(dbpart, (size_t)l.splits * C * l.Co);
+      }
+    }
+  }
+  p.off_dh = take(sizeof(float) * (size_t)C * B * p.Ch_head);
+  p.off_grad = take(sizeof(float) * (size_t)C * p.P);
+  p.off_part = take(sizeof(float) * std::max<size_t>(part, 1));
+  p.off_dbpart = take(sizeof(float) * std::max<size_t>(dbpart, 1));
+  p.off_loss = take(sizeof(float) * C);
+  p.total = o;
+  return GCPSL_OK;
+}
+
+}  // namespace
+
+struct gcpsl_ctx {
+  Plan plan;
+  gcpsl_desc desc;
+  std::vector<int64_t> sizes;
+  char *ws = nullptr;
+  int64_t staged_lo = -1;
+  int staged_n = 0;
+  int64_t horizon = 0;
+  template <typename T> T *at(size_t off) const { return reinterpret_cast<T *>(ws + off); }
+};
+
+extern "C" int gcpsl_param_count(const gcpsl_desc *d, int64_t *P, int64_t *P_client) {
+  gcpsl_clear_error();
+  Plan p;
+  const int rc = build_plan(d, p);
+  if (rc) return rc;
+  if (P) *P = p.P;
+  if (P_client) *P_client = p.Pc;
+  return GCPSL_OK;
+}
+
+extern "C" int gcpsl_workspace_bytes(const gcpsl_desc *d, size_t *bytes) {
+  gcpsl_clear_error();
+  if (!bytes) return gcpsl_fail(GCPSL_EINVAL, "null output");
+  Plan p;
+  const int rc = build_plan(d, p);
+  if (rc) return rc;
+  *bytes = p.total;
+  return GCPSL_OK;
+}
+
+#define HIP_TRY(expr)                                                                       \
+  do {                                                                                      \
+    const hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess) return gcpsl_fail(GCPSL_EHIP, std::string(#expr ": ") + hipGetErrorString(e_)); \
+  } while (0)
+
+extern "C" int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out) {
+  gcpsl_clear_error();
+  if (!out) return gcpsl_fail(GCPSL_EINVAL, "null output");
+  *out = nullptr;
+  Plan p;
+  int rc = build_plan(d, p);
+  if (rc) return rc;
+  if (!d->client_of_example || !d->cluster_of_client || !d->images || !d->labels || !d->theta ||
+      !d->momentum_buf || !d->workspace)
+    return gcpsl_fail(GCPSL_EINVAL, "null pointer in description");
+  if (reinterpret_cast<uintptr_t>(d->workspace) % kAlign)
+    return gcpsl_fail(GCPSL_EINVAL, "workspace must be 256-byte aligned");
+  if (reinterpret_cast<uintptr_t>(d->theta) % 16 || reinterpret_cast<uintptr_t>(d->momentum_buf) % 16)
+    return gcpsl_fail(GCPSL_EINVAL, "theta and momentum must be 16-byte aligned");
+  if (d->workspace_bytes < p.total)
+    return gcpsl_fail(GCPSL_EINVAL, "workspace too small: need " + std::to_string(p.total) + " bytes");
+  if (!std::isfinite(d->lr) || !std::isfinite(d->momentum)) return gcpsl_fail(GCPSL_EINVAL, "lr and momentum must be finite");
+  for (int32_t k = 0; k < d->K; ++k)
+    if (d->cluster_of_client[k] < 0 || d->cluster_of_client[k] >= d->C)
+      return gcpsl_fail(GCPSL_EINVAL, "cluster_of_client out of range");
+  // per-cluster example lists in ascending global id (CSR)
+  std::vector<int64_t> off(p.C + 1, 0);
+  for (int64_t e = 0; e < d->n_examples; ++e) {
+    const int32_t k = d->client_of_example[e];
+    if (k < 0 || k >= d->K) return gcpsl_fail(GCPSL_EINVAL, "client_of_example out of range");
+    off[d->cluster_of_client[k] + 1] += 1;
+  }
+  for (int n = 0; n < p.C; ++n) {
+    if (off[n + 1] < p.B)
+      return gcpsl_fail(GCPSL_EINVAL, "cluster " + std::to_string(n) + " holds " +
+                                          std::to_string(off[n + 1]) + " < B examples");
+    off[n + 1] += off[n];
+  }
+  std::vector<int32_t> ids(d->n_examples);
+  std::vector<int64_t> fill(off.begin(), off.end() - 1);
+  for (int64_t e = 0; e < d->n_examples; ++e) ids[fill[d->cluster_of_client[d->client_of_example[e]]]++] = (int32_t)e;
+  std::vector<double> fw(p.C);
+  std::vector<int64_t> sizes(p.C);
+  for (int n = 0; n < p.C; ++n) {
+    sizes[n] = off[n + 1] - off[n];
+    fw[n] = (double)sizes[n];
+  }
+  char *ws = reinterpret_cast<char *>(d->workspace);
+  HIP_TRY(hipMemcpy(ws + p.off_ids, ids.data(), sizeof(int32_t) * ids.size(), hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(ws + p.off_off, off.data(), sizeof(int64_t) * off.size(), hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(ws + p.off_coe, d->client_of_example, sizeof(int32_t) * d->n_examples, hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(ws + p.off_fw, fw.data(), sizeof(double) * fw.size(), hipMemcpyHostToDevice));
+  HIP_TRY(hipMemset(ws + p.off_hits, 0, sizeof(int32_t) * p.max_steps * p.C));
+  gcpsl_ctx *ctx = new gcpsl_ctx();
+  ctx->plan = std::move(p);
+  ctx->desc = *d;
+  ctx->desc.layers = nullptr;
+  ctx->desc.client_of_example = nullptr;
+  ctx->desc.cluster_of_client = nullptr;
+  ctx->sizes = std::move(sizes);
+  ctx->ws = ws;
+  *out = ctx;
+  return GCPSL_OK;
+}
+
+extern "C" void gcpsl_destroy(gcpsl_ctx *ctx) { delete ctx; }
+
+extern "C" int gcpsl_cluster_sizes(gcpsl_ctx *ctx, int64_t *sizes) {
+  gcpsl_clear_error();
+  if (!ctx || !sizes) return gcpsl_fail(GCPSL_EINVAL, "null argument");
+  std::copy(ctx->sizes.begin(), ctx->sizes.end(), sizes);
+  return GCPSL_OK;
+}
+
+#define LAUNCH(expr)                                                                      \
+  do {                                                                                    \
+    const hipError_t e_ = (expr);                                                         \
+    if (e_ != hipSuccess) return gcpsl_fail(GCPSL_EHIP, std::string("launch failed: ") + hipGetErrorString(e_)); \
+  } while (0)
+
+extern "C" int gcpsl_sample(gcpsl_ctx *ctx, int64_t step, int32_t nsteps, int32_t *idx_out, void *stream) {
+  gcpsl_clear_error();
+  if (!ctx) return gcpsl_fail(GCPSL_EINVAL, "null context");
+  const Plan &p = ctx->plan;
+  if (step < 0) return gcpsl_fail(GCPSL_EINVAL, "step must be >= 0");
+  if (nsteps < 1 || nsteps > p.max_window) return gcpsl_fail(GCPSL_EINVAL, "nsteps outside [1, max_window]");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  int32_t *idx = ctx->at<int32_t>(p.off_idx);
+  LAUNCH(launch_sample(ctx->at<int32_t>(p.off_ids), ctx->at<int64_t>(p.off_off), ctx->at<int32_t>(p.off_coe),
+                       ctx->desc.labels, idx, ctx->at<int32_t>(p.off_y), ctx->at<int32_t>(p.off_hits), p.C, p.B,
+                       p.K, ctx->desc.seed, step, nsteps, p.max_steps, s));
+  LAUNCH(launch_gather(ctx->desc.images, idx, ctx->ws + p.off_x, p.dtype, (int64_t)nsteps * p.C * p.B,
+                       (int64_t)p.H * p.W * p.Cin, s));
+  if (idx_out)
+    HIP_TRY(hipMemcpyAsync(idx_out, idx, sizeof(int32_t) * (size_t)nsteps * p.C * p.B, hipMemcpyDeviceToDevice, s));
+  ctx->staged_lo = step;
+  ctx->staged_n = nsteps;
+  return GCPSL_OK;
+}
+
+extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *stream) {
+  gcpsl_clear_error();
+  if (!ctx) return gcpsl_fail(GCPSL_EINVAL, "null context");
+  if (ctx->staged_lo < 0 || step < ctx->staged_lo || step >= ctx->staged_lo + ctx->staged_n)
+    return gcpsl_fail(GCPSL_ESTATE, "step " + std::to_string(step) + " has not been sampled");
+  const Plan &p = ctx->plan;
+  const gcpsl_desc &d = ctx->desc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int C = p.C, B = p.B, n = (int)p.ly.size();
+  const int64_t slot = step - ctx->staged_lo;
+  char *ws = ctx->ws;
+  const void *x_in = ws + p.off_x + (size_t)p.esz * slot * p.x_rs;
+  const int32_t *y = ctx->at<int32_t>(p.off_y) + slot * C * B;
+  float *grad = ctx->at<float>(p.off_grad);
+  float *loss = loss_out ? loss_out : ctx->at<float>(p.off_loss);
+
+  // compute copies of the conv weights
+  for (int i = 0; i < n; ++i) {
+    const LayerInfo &l = p.ly[i];
+    if (l.spec.kind != GCPSL_CONV3X3) continue;
+    LAUNCH(launch_prep_weights(p.dtype, d.theta, p.P, C, l.w_off, l.Co, l.Ci, ws + l.wf_off, l.Kp,
+                               i > 0 ? ws + l.wd_off : nullptr, l.Kdp, s));
+  }
+
+  // forward: client segment to the cut, server segment to the loss
+  auto input_of = [&](int i) -> const void * { return i == 0 ? x_in : (const void *)(ws + p.ly[i - 1].act_off); };
+  for (int i = 0; i < n; ++i) {
+    const LayerInfo &l = p.ly[i];
+    const int kind = l.spec.kind;
+    if (kind == GCPSL_CONV3X3) {
+      ConvArgs a{};
+      a.src = input_of(i);
+      a.wt = ws + l.wf_off;
+      a.out = ws + l.act_off;
+      a.bias = d.theta + l.b_off;
+      a.res = (l.spec.flags & GCPSL_RESIDUAL) ? a.src : nullptr;
+      a.mask = nullptr;
+      a.Bt = B; a.H = l.H; a.W = l.W; a.Csrc = l.Ci; a.N = l.Co; a.K = 9 * l.Ci; a.Kp = l.Kp;
+      a.src_rs = (int64_t)B * l.H * l.W * l.Ci;
+      a.wt_rs = (int64_t)l.Co * l.Kp;
+      a.out_rs = l.act_rs;
+      a.bias_rs = p.P;
+      a.C = C;
+      a.epi = EPI_FWD;
+      LAUNCH(launch_conv(p.dtype, a, s));
+    } else if (kind == GCPSL_MAXPOOL2) {
+      if (!l.stored) continue;  // fused into the head
+      LAUNCH(launch_maxpool_fwd(p.dtype, input_of(i), ws + l.act_off, C, B, l.H, l.W, l.Ci, s));
+    } else if (kind == GCPSL_AVGPOOL) {
+      const LayerInfo &hc = p.ly[p.head_conv];
+      LAUNCH(launch_head_pool(p.dtype, ws + hc.act_off, ws + l.act_off, C, B, hc.Ho, hc.Wo, hc.Co,
+                              p.head_maxpool ? 1 : 0, s));
+    } else if (kind == GCPSL_LINEAR) {
+      LAUNCH(launch_linear_ce(p.dtype, ws + p.ly[p.avg_idx].act_off, y, d.theta, p.P, l.w_off, l.b_off, grad,
+                              ctx->at<float>(p.off_dh), loss, C, B, l.Ci, l.Co, s));
+    }
+  }
+
+  // backward: head pooling, then every conv from the top down
+  {
+    const LayerInfo &hc = p.ly[p.head_conv];
+    LAUNCH(launch_head_pool_bwd(p.dtype, ws + hc.act_off, ctx->at<float>(p.off_dh), ws + hc.gpre_off, C, B,
+                                hc.Ho, hc.Wo, hc.Co, p.head_maxpool ? 1 : 0, s));
+  }
+  int i = p.head_conv;
+  while (i >= 0) {
+    const LayerInfo &l = p.ly[i];
+    // weight and bias gradient
+    WgradArgs w{};
+    w.g = ws + l.gpre_off;
+    w.x = input_of(i);
+    w.Bt = B; w.H = l.H; w.W = l.W; w.Ci = l.Ci; w.Co = l.Co;
+    w.g_rs = (int64_t)B * l.H * l.W * l.Co;
+    w.x_rs = (int64_t)B * l.H * l.W * l.Ci;
+    w.C = C;
+    w.splits = l.splits;
+    w.chunk = l.chunk;
+    if (l.splits == 1) {
+      w.dw = grad + l.w_off; w.dw_rs = p.P; w.dw_ss = 0;
+      w.db = grad + l.b_off; w.db_rs = p.P; w.db_ss = 0;
+    } else {
+      w.dw = ctx->at<float>(p.off_part); w.dw_rs = l.nw; w.dw_ss = (int64_t)C * l.nw;
+      w.db = ctx->at<float>(p.off_dbpart); w.db_rs = l.Co; w.db_ss = (int64_t)C * l.Co;
+    }
+    LAUNCH(launch_wgrad(p.dtype, w, s));
+    if (l.splits > 1)
+      LAUNCH(launch_wgrad_reduce(w.dw, w.db, l.splits, w.dw_ss, w.dw_rs, w.db_ss, w.db_rs, grad, p.P, l.w_off,
+                                 l.b_off, l.nw, l.Co, C, s));
+    if (i == 0) break;
+    // input gradient (the cut gradient when layer i-1 is the client's last pool)
+    const LayerInfo &prev = p.ly[i - 1];
+    const bool through_pool = prev.spec.kind == GCPSL_MAXPOOL2;
+    ConvArgs a{};
+    a.src = ws + l.gpre_off;
+    a.wt = ws + l.wd_off;
+    a.out = through_pool ? ws + l.gin_off : ws + prev.gpre_off;
+    a.bias = nullptr;
+    a.res = (l.spec.flags & GCPSL_RESIDUAL) ? a.src : nullptr;
+    a.mask = through_pool ? nullptr : (const void *)(ws + prev.act_off);
+    a.Bt = B; a.H = l.H; a.W = l.W; a.Csrc = l.Co; a.N = l.Ci; a.K = 9 * l.Co; a.Kp = l.Kdp;
+    a.src_rs = (int64_t)B * l.H * l.W * l.Co;
+    a.wt_rs = (int64_t)l.Ci * l.Kdp;
+    a.out_rs = (int64_t)B * l.H * l.W * l.Ci;
+    a.bias_rs = 0;
+    a.C = C;
+    a.epi = EPI_DGRAD;
+    LAUNCH(launch_conv(p.dtype, a, s));
+    if (through_pool) {
+      const LayerInfo &pc = p.ly[i - 2];
+      LAUNCH(launch_maxpool_bwd(p.dtype, ws + pc.act_off, ws + l.gin_off, ws + pc.gpre_off, C, B, pc.Ho, pc.Wo,
+                                pc.Co, s));
+      i -= 2;
+    } else {
+      i -= 1;
+    }
+  }
+
+  LAUNCH(launch_sgd(d.theta, d.momentum_buf, grad, (int64_t)C * p.P, d.lr, d.momentum, s));
+  ctx->horizon = std::max<int64_t>(ctx->horizon, std::min<int64_t>(step + 1, p.max_steps));
+  return GCPSL_OK;
+}
+
+extern "C" int gcpsl_fuse(gcpsl_ctx *ctx, void *stream) {
+  gcpsl_clear_error();
+  if (!ctx) return gcpsl_fail(GCPSL_EINVAL, "null context");
+  const Plan &p = ctx->plan;
+  double W = 0.0;
+  for (int64_t v : ctx->sizes) W += (double)v;
+  LAUNCH(launch_fuse(ctx->desc.theta, ctx->at<double>(p.off_fw), W, p.C, p.P, reinterpret_cast<hipStream_t>(stream)));
+  return GCPSL_OK;
+}
+
+extern "C" int gcpsl_participation(gcpsl_ctx *ctx, int64_t *active_slots, int64_t *total_slots, int32_t *per_step) {
+  gcpsl_clear_error();
+  if (!ctx || !active_slots || !total_slots) return gcpsl_fail(GCPSL_EINVAL, "null argument");
+  const Plan &p = ctx->plan;
+  HIP_TRY(hipDeviceSynchronize());
+  const int64_t T = ctx->horizon;
+  std::vector<int32_t> hits((size_t)std::max<int64_t>(T, 1) * p.C, 0);
+  if (T > 0) HIP_TRY(hipMemcpy(hits.data(), ctx->ws + p.off_hits, sizeof(int32_t) * T * p.C, hipMemcpyDeviceToHost));
+  int64_t act = 0;
+  for (int64_t i = 0; i < T * p.C; ++i) act += hits[i];
+  *active_slots = act;
+  *total_slots = (int64_t)p.K * T;
+  if (per_step && T > 0) std::copy(hits.begin(), hits.begin() + T * p.C, per_step);
+  return GCPSL_OK;
+}
+
+extern "C" int gcpsl_tensor(gcpsl_ctx *ctx, const char *name, void **ptr, int64_t *numel, int32_t *dtype) {
+  gcpsl_clear_error();
+  if (!ctx || !name || !ptr || !numel || !dtype) return gcpsl_fail(GCPSL_EINVAL, "null argument");
+  const Plan &p = ctx->plan;
+  const std::string nm(name);
+  const int64_t CB = (int64_t)p.C * p.B;
+  auto put = [&](size_t off, int64_t ne, int32_t dt) {
+    *ptr = ctx->ws + off;
+    *numel = ne;
+    *dtype = dt;
+    return GCPSL_OK;
+  };
+  if (nm == "x") return put(p.off_x, (int64_t)p.max_window * p.x_rs, p.dtype);
+  if (nm == "idx") return put(p.off_idx, (int64_t)p.max_window * CB, -1);
+  if (nm == "y") return put(p.off_y, (int64_t)p.max_window * CB, -1);
+  if (nm == "hits") return put(p.off_hits, p.max_steps * p.C, -1);
+  if (nm == "dh") return put(p.off_dh, CB * p.Ch_head, GCPSL_F32);
+  if (nm == "grad") return put(p.off_grad, (int64_t)p.C * p.P, GCPSL_F32);
+  for (size_t i = 0; i < p.ly.size(); ++i) {
+    const LayerInfo &l = p.ly[i];
+    const std::string k = std::to_string(i);
+    if (nm == "act" + k && l.stored) return put(l.act_off, (int64_t)p.C * l.act_rs, p.dtype);
+    if (l.spec.kind == GCPSL_CONV3X3) {
+      const int64_t rs = (int64_t)p.B * l.H * l.W;
+      if (nm == "gpre" + k) return put(l.gpre_off, p.C * rs * l.Co, p.dtype);
+      if (nm == "gin" + k && l.has_gin) return put(l.gin_off, p.C * rs * l.Ci, p.dtype);
+    }
+  }
+  return gcpsl_fail(GCPSL_EINVAL, "unknown tensor " + nm);
+}

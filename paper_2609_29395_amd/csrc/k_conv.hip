@@ -1,0 +1,505 @@
+// Replica-batched implicit-GEMM 3x3 convolutions on MFMA (gfx950).
+//
+// Every pass of a conv layer is a dense contraction:
+//   forward  out[m][co] = sum_{(r,s,ci)} x[m + (r-1, s-1)][ci] W[co][r][s][ci]
+//   dgrad    dx[m][ci]  = sum_{(r,s,co)} g[m + (r-1, s-1)][co] W[co][2-r][2-s][ci]
+//            (a forward conv of g with the flipped, transposed weights)
+//   wgrad    dW[co][(r,s,ci)] = sum_m g[m][co] x[m + (r-1, s-1)][ci]
+// with m = (b, h, w) over the batch and the image.  One workgroup computes a
+// BM x BN output tile of one replica; replicas are folded into the linear
+// workgroup index, so one launch covers all C clusters.
+//
+// Tiles are staged through LDS in "k-contiguous" rows of 128 bytes (64 bf16
+// or 32 fp32 k values) plus 16 bytes of padding, double buffered with one
+// barrier per k tile.  4 waves in a 2x2 layout each own a (BM/2) x (BN/2)
+// sub-tile of 16x16 MFMA blocks.  A lane's operand fragment is 8 consecutive
+// k values of one row: one v_mfma_f32_16x16x32_bf16, or eight
+// v_mfma_f32_16x16x4_f32 (lane group g feeds k = 8g + j to the j-th), so the
+// fp32 and bf16 paths share the LDS layout and the tile loop.
+#include "runtime.h"
+
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+template <typename T> struct Frag;
+template <> struct Frag<bf16_t> { uint4 q; };
+template <> struct Frag<float> { float v[8]; };
+
+__device__ __forceinline__ void load_frag(Frag<bf16_t> &f, const bf16_t *p) {
+  f.q = *reinterpret_cast<const uint4 *>(p);
+}
+__device__ __forceinline__ void load_frag(Frag<float> &f, const float *p) {
+  const uint4 x = *reinterpret_cast<const uint4 *>(p);
+  const uint4 y = *reinterpret_cast<const uint4 *>(p + 4);
+  f.v[0] = __uint_as_float(x.x); f.v[1] = __uint_as_float(x.y);
+  f.v[2] = __uint_as_float(x.z); f.v[3] = __uint_as_float(x.w);
+  f.v[4] = __uint_as_float(y.x); f.v[5] = __uint_as_float(y.y);
+  f.v[6] = __uint_as_float(y.z); f.v[7] = __uint_as_float(y.w);
+}
+
+__device__ __forceinline__ void mma(f32x4_t &acc, const Frag<bf16_t> &a, const Frag<bf16_t> &b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a.q),
+                                                __builtin_bit_cast(bf16x8_t, b.q), acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mma(f32x4_t &acc, const Frag<float> &a, const Frag<float> &b) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[j], b.v[j], acc, 0, 0, 0);
+}
+
+template <typename T> struct Pack {
+  T v[16 / sizeof(T)];
+};
+
+// Shared tile geometry and the MFMA loop over one staged k tile.
+template <typename T, int BM, int BN> struct Tile {
+  static constexpr int VEC = ElemT<T>::VEC;
+  static constexpr int BK = 128 / (int)sizeof(T);
+  static constexpr int LDR = BK + 16 / (int)sizeof(T);
+  static constexpr int TM = BM / 32, TN = BN / 32;
+
+  __device__ static __forceinline__ void compute(f32x4_t (&acc)[TM][TN], const T *As, const T *Bs,
+                                                 int wm0, int wn0, int lane) {
+    const int li = lane & 15, lg = lane >> 4;
+#pragma unroll
+    for (int kg = 0; kg < BK / 32; ++kg) {
+      Frag<T> a[TM], b[TN];
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) load_frag(a[tm], As + (wm0 + tm * 16 + li) * LDR + kg * 32 + lg * 8);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) load_frag(b[tn], Bs + (wn0 + tn * 16 + li) * LDR + kg * 32 + lg * 8);
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) mma(acc[tm][tn], a[tm], b[tn]);
+    }
+  }
+};
+
+// ------------------------------------------------------ forward / dgrad
+template <typename T, int BM, int BN, bool VA>
+__global__ void __launch_bounds__(256)
+conv_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
+  using E = ElemT<T>;
+  using TL = Tile<T, BM, BN>;
+  constexpr int VEC = TL::VEC, BK = TL::BK, LDR = TL::LDR;
+  constexpr int AV = BM / 32, BV = BN / 32;
+  __shared__ __attribute__((aligned(16))) T As[2][BM * LDR];
+  __shared__ __attribute__((aligned(16))) T Bs[2][BN * LDR];
+
+  const int tid = threadIdx.x;
+  const uint32_t t = xcd_swizzle(blockIdx.x, (uint32_t)(MT * NT * a.C));
+  const int nt = (int)(t % (uint32_t)NT);
+  const uint32_t rest = t / (uint32_t)NT;
+  const int mt = (int)(rest % (uint32_t)MT);
+  const int rep = (int)(rest / (uint32_t)MT);
+  const int M = a.Bt * a.H * a.W;
+  const int m0 = mt * BM, n0 = nt * BN;
+  const T *src = reinterpret_cast<const T *>(a.src) + rep * a.src_rs;
+  const T *wt = reinterpret_cast<const T *>(a.wt) + rep * a.wt_rs;
+
+  const int kv = tid & 7, rrow = tid >> 3;
+  int ab[AV], ah[AV], aw[AV];
+  bool aok[AV];
+#pragma unroll
+  for (int j = 0; j < AV; ++j) {
+    const int m = m0 + rrow + 32 * j;
+    aok[j] = m < M;
+    const uint32_t mm = aok[j] ? (uint32_t)m : 0u;
+    const uint32_t q = fdiv(mm, fd_w);
+    aw[j] = (int)(mm - q * (uint32_t)a.W);
+    ab[j] = (int)fdiv(q, fd_h);
+    ah[j] = (int)(q - (uint32_t)ab[j] * (uint32_t)a.H);
+  }
+
+  uint4 ra[AV], rb[BV];
+  auto load_tiles = [&](int kt) {
+    const int k0 = kt * BK + kv * VEC;
+    if constexpr (VA) {
+      int r = 0, s = 0, c = 0;
+      const bool kok = k0 < a.K;
+      if (kok) {
+        const int rs = (int)fdiv((uint32_t)k0, fd_c);
+        c = k0 - rs * a.Csrc;
+        r = (rs * 11) >> 5;  // rs / 3 for rs < 9
+        s = rs - 3 * r;
+      }
+#pragma unroll
+      for (int j = 0; j < AV; ++j) {
+        const int hh = ah[j] + r - 1, ww = aw[j] + s - 1;
+        if (kok && aok[j] && (unsigned)hh < (unsigned)a.H && (unsigned)ww < (unsigned)a.W)
+          ra[j] = *reinterpret_cast<const uint4 *>(
+              src + ((int64_t)(ab[j] * a.H + hh) * a.W + ww) * a.Csrc + c);
+        else
+          ra[j] = make_uint4(0, 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < AV; ++j) {
+        Pack<T> pk;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const int k = k0 + e;
+          T v = T(0);
+          if (k < a.K && aok[j]) {
+            const int rs = (int)fdiv((uint32_t)k, fd_c);
+            const int c = k - rs * a.Csrc;
+            const int r = (rs * 11) >> 5, s = rs - 3 * r;
+            const int hh = ah[j] + r - 1, ww = aw[j] + s - 1;
+            if ((unsigned)hh < (unsigned)a.H && (unsigned)ww < (unsigned)a.W)
+              v = src[((int64_t)(ab[j] * a.H + hh) * a.W + ww) * a.Csrc + c];
+          }
+          pk.v[e] = v;
+        }
+        ra[j] = __builtin_bit_cast(uint4, pk);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < BV; ++j) {
+      const int n = n0 + rrow + 32 * j;
+      rb[j] = n < a.N ? *reinterpret_cast<const uint4 *>(wt + (int64_t)n * a.Kp + k0)
+                      : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store_tiles = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < AV; ++j)
+      *reinterpret_cast<uint4 *>(&As[buf][(rrow + 32 * j) * LDR + kv * VEC]) = ra[j];
+#pragma unroll
+    for (int j = 0; j < BV; ++j)
+      *reinterpret_cast<uint4 *>(&Bs[buf][(rrow + 32 * j) * LDR + kv * VEC]) = rb[j];
+  };
+
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave >> 1) * (BM / 2), wn0 = (wave & 1) * (BN / 2);
+  f32x4_t acc[TL::TM][TL::TN];
+#pragma unroll
+  for (int i = 0; i < TL::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TL::TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = a.Kp / BK;
+  load_tiles(0);
+  store_tiles(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) load_tiles(kt + 1);
+    TL::compute(acc, As[buf], Bs[buf], wm0, wn0, lane);
+    if (kt + 1 < nk) store_tiles(buf ^ 1);
+    __syncthreads();
+  }
+
+  // epilogue
+  const int li = lane & 15, lg = lane >> 4;
+  T *out = reinterpret_cast<T *>(a.out) + rep * a.out_rs;
+  const T *res = a.res ? reinterpret_cast<const T *>(a.res) + rep * a.out_rs : nullptr;
+  const T *msk = a.mask ? reinterpret_cast<const T *>(a.mask) + rep * a.out_rs : nullptr;
+#pragma unroll
+  for (int tn = 0; tn < TL::TN; ++tn) {
+    const int n = n0 + wn0 + tn * 16 + li;
+    const bool nok = n < a.N;
+    const float bias = (a.epi == EPI_FWD && nok) ? a.bias[rep * a.bias_rs + n] : 0.f;
+#pragma unroll
+    for (int tm = 0; tm < TL::TM; ++tm) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + wm0 + tm * 16 + lg * 4 + r;
+        if (m < M && nok) {
+          const int64_t o = (int64_t)m * a.N + n;
+          float v = acc[tm][tn][r];
+          if (a.epi == EPI_FWD) {
+            v += bias;
+            if (res) v += E::to_f(res[o]);
+            v = fmaxf(v, 0.f);
+          } else {
+            if (res) v += E::to_f(res[o]);
+            if (msk && !(E::to_f(msk[o]) > 0.f)) v = 0.f;
+          }
+          out[o] = E::from_f(v);
+        }
+      }
+    }
+  }
+}
+
+// --------------------------------------------------------------- wgrad
+template <typename T>
+__device__ __forceinline__ void transpose_block(const uint4 (&in)[ElemT<T>::VEC],
+                                                uint4 (&out)[ElemT<T>::VEC]);
+
+// 8 pixels x 8 bf16 channels -> 8 channels x 8 pixels.
+template <>
+__device__ __forceinline__ void transpose_block<bf16_t>(const uint4 (&in)[8], uint4 (&out)[8]) {
+  uint32_t w[8][4];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    w[e][0] = in[e].x; w[e][1] = in[e].y; w[e][2] = in[e].z; w[e][3] = in[e].w;
+  }
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    uint32_t o[4];
+    const int wi = q >> 1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t lo = w[2 * j][wi], hi = w[2 * j + 1][wi];
+      o[j] = (q & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+    }
+    out[q] = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+// 4 pixels x 4 fp32 channels -> 4 channels x 4 pixels.
+template <>
+__device__ __forceinline__ void transpose_block<float>(const uint4 (&in)[4], uint4 (&out)[4]) {
+  out[0] = make_uint4(in[0].x, in[1].x, in[2].x, in[3].x);
+  out[1] = make_uint4(in[0].y, in[1].y, in[2].y, in[3].y);
+  out[2] = make_uint4(in[0].z, in[1].z, in[2].z, in[3].z);
+  out[3] = make_uint4(in[0].w, in[1].w, in[2].w, in[3].w);
+}
+
+template <typename T, int BM, int BN, bool VB>
+__global__ void __launch_bounds__(256)
+wgrad_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
+  using TL = Tile<T, BM, BN>;
+  constexpr int VEC = TL::VEC, BK = TL::BK, LDR = TL::LDR;
+  constexpr int PB = BK / VEC;  // pixel blocks per k tile
+  constexpr int NA = (BM / VEC) * PB, NB = (BN / VEC) * PB;
+  constexpr int ITER = (NA + NB + 255) / 256;
+  static_assert(NA <= 256, "A blocks must fit one pass");
+  __shared__ __attribute__((aligned(16))) T As[2][BM * LDR];
+  __shared__ __attribute__((aligned(16))) T Bs[2][BN * LDR];
+  __shared__ float red[PB][BM];
+
+  const int tid = threadIdx.x;
+  const uint32_t total = (uint32_t)(MT * NT * a.splits * a.C);
+  const uint32_t t = xcd_swizzle(blockIdx.x, total);
+  const int nt = (int)(t % (uint32_t)NT);
+  uint32_t rest = t / (uint32_t)NT;
+  const int mt = (int)(rest % (uint32_t)MT);
+  rest /= (uint32_t)MT;
+  const int split = (int)(rest % (uint32_t)a.splits);
+  const int rep = (int)(rest / (uint32_t)a.splits);
+  const int M = a.Bt * a.H * a.W;
+  const int NW = 9 * a.Ci;
+  const int p_begin = split * a.chunk;
+  const int p_end = min(M, p_begin + a.chunk);
+  const int nk = (p_end - p_begin + BK - 1) / BK;
+  const int m0 = mt * BM, n0 = nt * BN;
+  const T *G = reinterpret_cast<const T *>(a.g) + rep * a.g_rs;
+  const T *X = reinterpret_cast<const T *>(a.x) + rep * a.x_rs;
+  const bool do_bias = (nt == 0) && a.db != nullptr;
+
+  // blocks owned by this thread
+  int kind[ITER], rowb[ITER], pb[ITER], br[ITER], bs[ITER], bc[ITER];
+  bool bvalid[ITER];
+#pragma unroll
+  for (int it = 0; it < ITER; ++it) {
+    const int i = tid + 256 * it;
+    if (i < NA) {
+      kind[it] = 0;
+      rowb[it] = i / PB;
+      pb[it] = i % PB;
+    } else if (i < NA + NB) {
+      kind[it] = 1;
+      rowb[it] = (i - NA) / PB;
+      pb[it] = (i - NA) % PB;
+    } else {
+      kind[it] = 2;
+      rowb[it] = 0;
+      pb[it] = 0;
+    }
+    br[it] = bs[it] = bc[it] = 0;
+    bvalid[it] = false;
+    if (kind[it] == 1) {
+      const int kk0 = n0 + rowb[it] * VEC;
+      bvalid[it] = kk0 < NW;
+      if (VB && bvalid[it]) {
+        const int rs = (int)fdiv((uint32_t)kk0, fd_c);
+        bc[it] = kk0 - rs * a.Ci;
+        br[it] = (rs * 11) >> 5;
+        bs[it] = rs - 3 * br[it];
+      }
+    }
+  }
+
+  uint4 reg[ITER][VEC];
+  float bsum[VEC];
+#pragma unroll
+  for (int q = 0; q < VEC; ++q) bsum[q] = 0.f;
+
+  auto load_tiles = [&](int kt) {
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+      const int pbase = p_begin + kt * BK + pb[it] * VEC;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const int p = pbase + e;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (kind[it] == 0) {
+          const int c0 = m0 + rowb[it] * VEC;
+          if (p < p_end && c0 < a.Co) v = *reinterpret_cast<const uint4 *>(G + (int64_t)p * a.Co + c0);
+        } else if (kind[it] == 1 && p < p_end && bvalid[it]) {
+          const uint32_t q1 = fdiv((uint32_t)p, fd_w);
+          const int w = (int)((uint32_t)p - q1 * (uint32_t)a.W);
+          const int b = (int)fdiv(q1, fd_h);
+          const int h = (int)(q1 - (uint32_t)b * (uint32_t)a.H);
+          if constexpr (VB) {
+            const int hh = h + br[it] - 1, ww = w + bs[it] - 1;
+            if ((unsigned)hh < (unsigned)a.H && (unsigned)ww < (unsigned)a.W)
+              v = *reinterpret_cast<const uint4 *>(X + ((int64_t)(b * a.H + hh) * a.W + ww) * a.Ci + bc[it]);
+          } else {
+            Pack<T> pk;
+            const int kk0 = n0 + rowb[it] * VEC;
+#pragma unroll
+            for (int q = 0; q < VEC; ++q) {
+              const int kk = kk0 + q;
+              T val = T(0);
+              if (kk < NW) {
+                const int rs = (int)fdiv((uint32_t)kk, fd_c);
+                const int c = kk - rs * a.Ci;
+                const int r = (rs * 11) >> 5, s = rs - 3 * r;
+                const int hh = h + r - 1, ww = w + s - 1;
+                if ((unsigned)hh < (unsigned)a.H && (unsigned)ww < (unsigned)a.W)
+                  val = X[((int64_t)(b * a.H + hh) * a.W + ww) * a.Ci + c];
+              }
+              pk.v[q] = val;
+            }
+            v = __builtin_bit_cast(uint4, pk);
+          }
+        }
+        reg[it][e] = v;
+      }
+    }
+  };
+  auto store_tiles = [&](int buf) {
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+      if (kind[it] == 2) continue;
+      if (kind[it] == 0 && do_bias) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          Pack<T> p = __builtin_bit_cast(Pack<T>, reg[it][e]);
+#pragma unroll
+          for (int q = 0; q < VEC; ++q) bsum[q] += ElemT<T>::to_f(p.v[q]);
+        }
+      }
+      uint4 o[VEC];
+      transpose_block<T>(reg[it], o);
+      T *dst = kind[it] == 0 ? As[buf] : Bs[buf];
+#pragma unroll
+      for (int q = 0; q < VEC; ++q)
+        *reinterpret_cast<uint4 *>(&dst[(rowb[it] * VEC + q) * LDR + pb[it] * VEC]) = o[q];
+    }
+  };
+
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave >> 1) * (BM / 2), wn0 = (wave & 1) * (BN / 2);
+  f32x4_t acc[TL::TM][TL::TN];
+#pragma unroll
+  for (int i = 0; i < TL::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TL::TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  if (nk > 0) {
+    load_tiles(0);
+    store_tiles(0);
+  }
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) load_tiles(kt + 1);
+    TL::compute(acc, As[buf], Bs[buf], wm0, wn0, lane);
+    if (kt + 1 < nk) store_tiles(buf ^ 1);
+    __syncthreads();
+  }
+
+  const int li = lane & 15, lg = lane >> 4;
+  float *dw = a.dw + split * a.dw_ss + rep * a.dw_rs;
+#pragma unroll
+  for (int tn = 0; tn < TL::TN; ++tn) {
+    const int n = n0 + wn0 + tn * 16 + li;
+#pragma unroll
+    for (int tm = 0; tm < TL::TM; ++tm)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + wm0 + tm * 16 + lg * 4 + r;
+        if (m < a.Co && n < NW) dw[(int64_t)m * NW + n] = acc[tm][tn][r];
+      }
+  }
+
+  if (do_bias) {
+    if (kind[0] == 0) {
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) red[pb[0]][rowb[0] * VEC + q] = bsum[q];
+    }
+    __syncthreads();
+    if (tid < BM) {
+      const int co = m0 + tid;
+      if (co < a.Co) {
+        float s = 0.f;
+#pragma unroll
+        for (int i = 0; i < PB; ++i) s += red[i][tid];
+        a.db[split * a.db_ss + rep * a.db_rs + co] = s;
+      }
+    }
+  }
+}
+
+template <typename T, int BM, int BN, bool VA>
+hipError_t run_conv(const ConvArgs &a, hipStream_t s) {
+  const int M = a.Bt * a.H * a.W;
+  const int MT = (M + BM - 1) / BM, NT = (a.N + BN - 1) / BN;
+  const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Csrc);
+  const uint32_t blocks = (uint32_t)MT * NT * a.C;
+  hipLaunchKernelGGL((conv_kernel<T, BM, BN, VA>), dim3(blocks), dim3(256), 0, s, a, fw, fh, fc, MT, NT);
+  return hipGetLastError();
+}
+
+template <typename T, bool VA>
+hipError_t pick_conv(const ConvArgs &a, hipStream_t s) {
+  if (a.N > 64) return run_conv<T, 128, 128, VA>(a, s);
+  if (a.N > 32) return run_conv<T, 128, 64, VA>(a, s);
+  return run_conv<T, 128, 32, VA>(a, s);
+}
+
+template <typename T, int BM, int BN, bool VB>
+hipError_t run_wgrad(const WgradArgs &a, hipStream_t s) {
+  const int MT = (a.Co + BM - 1) / BM, NT = (9 * a.Ci + BN - 1) / BN;
+  const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Ci);
+  const uint32_t blocks = (uint32_t)MT * NT * a.splits * a.C;
+  hipLaunchKernelGGL((wgrad_kernel<T, BM, BN, VB>), dim3(blocks), dim3(256), 0, s, a, fw, fh, fc, MT, NT);
+  return hipGetLastError();
+}
+
+template <typename T, int BM, bool VB>
+hipError_t pick_wgrad_n(const WgradArgs &a, hipStream_t s) {
+  const int NW = 9 * a.Ci;
+  if (NW > 64) return run_wgrad<T, BM, 128, VB>(a, s);
+  if (NW > 32) return run_wgrad<T, BM, 64, VB>(a, s);
+  return run_wgrad<T, BM, 32, VB>(a, s);
+}
+
+template <typename T, bool VB>
+hipError_t pick_wgrad(const WgradArgs &a, hipStream_t s) {
+  if (a.Co > 64) return pick_wgrad_n<T, 128, VB>(a, s);
+  if (a.Co > 32) return pick_wgrad_n<T, 64, VB>(a, s);
+  return pick_wgrad_n<T, 32, VB>(a, s);
+}
+
+}  // namespace
+
+int wgrad_k_tile(int dtype) { return dtype == GCPSL_BF16 ? 64 : 32; }
+
+hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s) {
+  if (dtype == GCPSL_BF16)
+    return (a.Csrc % 8 == 0) ? pick_conv<bf16_t, true>(a, s) : pick_conv<bf16_t, false>(a, s);
+  return (a.Csrc % 4 == 0) ? pick_conv<float, true>(a, s) : pick_conv<float, false>(a, s);
+}
+
+hipError_t launch_wgrad(int dtype, const WgradArgs &a, hipStream_t s) {
+  if (dtype == GCPSL_BF16)
+    return (a.Ci % 8 == 0) ? pick_wgrad<bf16_t, true>(a, s) : pick_wgrad<bf16_t, false>(a, s);
+  return (a.Ci % 4 == 0) ? pick_wgrad<float, true>(a, s) : pick_wgrad<float, false>(a, s);
+}

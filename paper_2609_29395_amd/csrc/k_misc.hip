@@ -1,0 +1,485 @@
+// Sampling, gather, pools, the classifier head, SGD and fusion kernels.
+#include "rng.h"
+#include "runtime.h"
+
+namespace {
+
+constexpr int kMaxBitmapWords = 2048;  // clients tracked per cluster: K <= 65536
+
+// ---------------------------------------------------------------- sampling
+// Eq. 1 / Eq. 3: cluster n's batch at local round `step` is B distinct
+// examples of its own pool: positions [tB, (t+1)B) of the keyed permutation
+// of epoch e = step / S_n, S_n = floor(n_n / B).  Also counts the distinct
+// clients of the batch, |A_{n,t}| (Sec. III-A).
+__global__ void __launch_bounds__(256)
+sample_kernel(const int32_t *__restrict__ ids, const int64_t *__restrict__ off,
+              const int32_t *__restrict__ coe, const int32_t *__restrict__ labels,
+              int32_t *__restrict__ idx, int32_t *__restrict__ y, int32_t *__restrict__ hits,
+              int C, int B, int K, uint64_t seed, int64_t step0, int64_t max_steps) {
+  __shared__ uint32_t bitmap[kMaxBitmapWords];
+  __shared__ int count;
+  const int n = blockIdx.x, j = blockIdx.y, tid = threadIdx.x;
+  const int64_t step = step0 + j;
+  const int64_t lo = off[n];
+  const uint32_t nn = (uint32_t)(off[n + 1] - lo);
+  const int64_t S = nn / (uint32_t)B;
+  const int64_t e = step / S, t = step % S;
+  const uint64_t key = gc_sample_key(seed, (uint64_t)n, (uint64_t)e);
+  const int words = (K + 31) >> 5;
+  for (int w = tid; w < words; w += blockDim.x) bitmap[w] = 0u;
+  if (tid == 0) count = 0;
+  __syncthreads();
+  for (int i = tid; i < B; i += blockDim.x) {
+    const uint32_t p = (uint32_t)(t * B + i);
+    const int32_t ex = ids[lo + gc_permute(p, nn, key)];
+    const int64_t o = ((int64_t)j * C + n) * B + i;
+    idx[o] = ex;
+    y[o] = labels[ex];
+    const int32_t c = coe[ex];
+    atomicOr(&bitmap[c >> 5], 1u << (c & 31));
+  }
+  __syncthreads();
+  int local = 0;
+  for (int w = tid; w < words; w += blockDim.x) local += __popc(bitmap[w]);
+  atomicAdd(&count, local);
+  __syncthreads();
+  if (tid == 0 && step < max_steps) hits[step * C + n] = count;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+gather_kernel(const float *__restrict__ images, const int32_t *__restrict__ idx, T *__restrict__ x,
+              int64_t row_elems) {
+  const int64_t row = blockIdx.x;
+  const float *src = images + (int64_t)idx[row] * row_elems;
+  T *dst = x + row * row_elems;
+  if ((row_elems & 3) == 0) {
+    const int64_t nv = row_elems >> 2;
+    for (int64_t v = threadIdx.x; v < nv; v += blockDim.x) {
+      const float4 f = reinterpret_cast<const float4 *>(src)[v];
+      if constexpr (sizeof(T) == 4) {
+        reinterpret_cast<float4 *>(dst)[v] = f;
+      } else {
+        const uint32_t lo = (uint32_t)f32_to_bf16(f.x) | ((uint32_t)f32_to_bf16(f.y) << 16);
+        const uint32_t hi = (uint32_t)f32_to_bf16(f.z) | ((uint32_t)f32_to_bf16(f.w) << 16);
+        reinterpret_cast<uint2 *>(dst)[v] = make_uint2(lo, hi);
+      }
+    }
+  } else {
+    for (int64_t v = threadIdx.x; v < row_elems; v += blockDim.x) dst[v] = ElemT<T>::from_f(src[v]);
+  }
+}
+
+// ------------------------------------------------------ weight preparation
+// Compute copies of one conv layer's weights from the fp32 masters:
+//   wf[co][k], k = (r, s, ci) < 9 ci, rows zero-padded to Kp (forward);
+//   wd[ci][kk], kk = (r', s', co), wd[ci][(r', s', co)] = W[co][2-r'][2-s'][ci]
+//   rows zero-padded to Kdp (input gradient as a forward conv).
+template <typename T>
+__global__ void __launch_bounds__(256)
+prep_kernel(const float *__restrict__ theta, int64_t P, int64_t w_off, int co, int ci,
+            T *__restrict__ wf, int Kp, T *__restrict__ wd, int Kdp) {
+  const int rep = blockIdx.y;
+  const float *w = theta + rep * P + w_off;
+  const int K = 9 * ci, Kd = 9 * co;
+  const int64_t nf = (int64_t)co * Kp, nd = wd ? (int64_t)ci * Kdp : 0;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nf + nd;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    if (i < nf) {
+      const int n = (int)(i / Kp), k = (int)(i % Kp);
+      wf[rep * nf + i] = ElemT<T>::from_f(k < K ? w[(int64_t)n * K + k] : 0.f);
+    } else {
+      const int64_t i2 = i - nf;
+      const int c = (int)(i2 / Kdp), kk = (int)(i2 % Kdp);
+      float v = 0.f;
+      if (kk < Kd) {
+        const int rs = kk / co, o = kk % co;
+        const int r = rs / 3, s = rs % 3;
+        v = w[(int64_t)o * K + ((2 - r) * 3 + (2 - s)) * ci + c];
+      }
+      wd[rep * nd + i2] = ElemT<T>::from_f(v);
+    }
+  }
+}
+
+// -------------------------------------------------------------- max pool
+// 2x2 / stride 2 over a [N][H][W][Ch] batch (N = C * B).  The backward pass
+// routes each pooled gradient to the first maximum of its window in
+// row-major order (strict >) and applies the producing conv's ReLU mask
+// (output > 0).
+template <typename T>
+__global__ void __launch_bounds__(256)
+maxpool_fwd_kernel(const T *__restrict__ x, T *__restrict__ z, int64_t total, int H, int W, int Ch) {
+  const int Ho = H >> 1, Wo = W >> 1;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int c = (int)(i % Ch);
+    int64_t r = i / Ch;
+    const int wo = (int)(r % Wo);
+    r /= Wo;
+    const int ho = (int)(r % Ho);
+    const int64_t bi = r / Ho;
+    const int64_t base = ((bi * H + 2 * ho) * W + 2 * wo) * Ch + c;
+    float m = ElemT<T>::to_f(x[base]);
+    T best = x[base];
+    const int64_t o[3] = {base + Ch, base + (int64_t)W * Ch, base + (int64_t)W * Ch + Ch};
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      const float v = ElemT<T>::to_f(x[o[q]]);
+      if (v > m) {
+        m = v;
+        best = x[o[q]];
+      }
+    }
+    z[i] = best;
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+maxpool_bwd_kernel(const T *__restrict__ a, const T *__restrict__ gz, T *__restrict__ gpre,
+                   int64_t total, int H, int W, int Ch) {
+  const int Ho = H >> 1, Wo = W >> 1;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int c = (int)(i % Ch);
+    int64_t r = i / Ch;
+    const int wo = (int)(r % Wo);
+    r /= Wo;
+    const int ho = (int)(r % Ho);
+    const int64_t bi = r / Ho;
+    const int64_t base = ((bi * H + 2 * ho) * W + 2 * wo) * Ch + c;
+    const int64_t o[4] = {base, base + Ch, base + (int64_t)W * Ch, base + (int64_t)W * Ch + Ch};
+    float v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = ElemT<T>::to_f(a[o[q]]);
+    int arg = 0;
+#pragma unroll
+    for (int q = 1; q < 4; ++q)
+      if (v[q] > v[arg]) arg = q;
+    const T g = gz[i];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) gpre[o[q]] = (q == arg && v[q] > 0.f) ? g : T(0);
+  }
+}
+
+// ------------------------------------------------------------------ head
+// Pooled feature h[n][c] = mean over positions of (optionally 2x2-max-pooled)
+// last conv output.
+template <typename T>
+__global__ void __launch_bounds__(256)
+head_pool_kernel(const T *__restrict__ a, T *__restrict__ h, int64_t total, int H, int W, int Ch,
+                 int maxpool) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int c = (int)(i % Ch);
+    const int64_t bi = i / Ch;
+    const T *src = a + bi * H * W * Ch + c;
+    float s = 0.f;
+    int npos;
+    if (maxpool) {
+      const int Ho = H >> 1, Wo = W >> 1;
+      npos = Ho * Wo;
+      for (int ho = 0; ho < Ho; ++ho)
+        for (int wo = 0; wo < Wo; ++wo) {
+          const int64_t b0 = ((int64_t)(2 * ho) * W + 2 * wo) * Ch;
+          float m = ElemT<T>::to_f(src[b0]);
+          m = fmaxf(m, ElemT<T>::to_f(src[b0 + Ch]));
+          m = fmaxf(m, ElemT<T>::to_f(src[b0 + (int64_t)W * Ch]));
+          m = fmaxf(m, ElemT<T>::to_f(src[b0 + (int64_t)W * Ch + Ch]));
+          s += m;
+        }
+    } else {
+      npos = H * W;
+      for (int p = 0; p < npos; ++p) s += ElemT<T>::to_f(src[(int64_t)p * Ch]);
+    }
+    h[i] = ElemT<T>::from_f(s / (float)npos);
+  }
+}
+
+// Linear layer and mean softmax cross-entropy for one replica per workgroup:
+// logits = h W^T + b, loss = mean_b (logsumexp - logit_y),
+// dlogits = (softmax - onehot) / B, dW = dlogits^T h, db = sum_b dlogits,
+// dh = dlogits W.  bf16 workloads use the bf16-rounded weight matrix.
+template <typename T>
+__global__ void __launch_bounds__(256)
+linear_ce_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
+                 const float *__restrict__ theta, int64_t P, int64_t w_off, int64_t b_off,
+                 float *__restrict__ grad, float *__restrict__ dh, float *__restrict__ loss, int Bt,
+                 int Ch, int L) {
+  extern __shared__ float sh[];
+  float *lg = sh;              // [Bt][L] logits, then dlogits
+  float *lossb = sh + Bt * L;  // [Bt]
+  const int rep = blockIdx.x, tid = threadIdx.x;
+  const T *hr = h + (int64_t)rep * Bt * Ch;
+  const float *Wl = theta + rep * P + w_off;
+  const float *bl = theta + rep * P + b_off;
+  auto wv = [&](int j, int c) { return ElemT<T>::to_f(ElemT<T>::from_f(Wl[(int64_t)j * Ch + c])); };
+  for (int i = tid; i < Bt * L; i += blockDim.x) {
+    const int b = i / L, j = i % L;
+    float s = bl[j];
+    for (int c = 0; c < Ch; ++c) s += ElemT<T>::to_f(hr[(int64_t)b * Ch + c]) * wv(j, c);
+    lg[i] = s;
+  }
+  __syncthreads();
+  for (int b = tid; b < Bt; b += blockDim.x) {
+    float m = lg[b * L];
+    for (int j = 1; j < L; ++j) m = fmaxf(m, lg[b * L + j]);
+    float s = 0.f;
+    for (int j = 0; j < L; ++j) s += expf(lg[b * L + j] - m);
+    const float lse = logf(s);
+    const int yb = y[(int64_t)rep * Bt + b];
+    lossb[b] = lse - (lg[b * L + yb] - m);
+    for (int j = 0; j < L; ++j) {
+      const float p = expf(lg[b * L + j] - m - lse);
+      lg[b * L + j] = (p - (j == yb ? 1.f : 0.f)) / (float)Bt;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float s = 0.f;
+    for (int b = 0; b < Bt; ++b) s += lossb[b];
+    loss[rep] = s / (float)Bt;
+  }
+  float *g = grad + rep * P;
+  for (int i = tid; i < L * Ch; i += blockDim.x) {
+    const int j = i / Ch, c = i % Ch;
+    float s = 0.f;
+    for (int b = 0; b < Bt; ++b) s += lg[b * L + j] * ElemT<T>::to_f(hr[(int64_t)b * Ch + c]);
+    g[w_off + i] = s;
+  }
+  for (int j = tid; j < L; j += blockDim.x) {
+    float s = 0.f;
+    for (int b = 0; b < Bt; ++b) s += lg[b * L + j];
+    g[b_off + j] = s;
+  }
+  float *dhr = dh + (int64_t)rep * Bt * Ch;
+  for (int i = tid; i < Bt * Ch; i += blockDim.x) {
+    const int b = i / Ch, c = i % Ch;
+    float s = 0.f;
+    for (int j = 0; j < L; ++j) s += lg[b * L + j] * wv(j, c);
+    dhr[i] = s;
+  }
+}
+
+// Gradient of the head pooling, with the last conv's ReLU mask:
+// gpre = mask * route(dh / npos) (route = first maximum if max pooled).
+template <typename T>
+__global__ void __launch_bounds__(256)
+head_pool_bwd_kernel(const T *__restrict__ a, const float *__restrict__ dh, T *__restrict__ gpre,
+                     int64_t total, int H, int W, int Ch, int maxpool) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int c = (int)(i % Ch);
+    int64_t r = i / Ch;
+    if (maxpool) {
+      const int Ho = H >> 1, Wo = W >> 1;
+      const int wo = (int)(r % Wo);
+      r /= Wo;
+      const int ho = (int)(r % Ho);
+      const int64_t bi = r / Ho;
+      const T g = ElemT<T>::from_f(dh[bi * Ch + c] / (float)(Ho * Wo));
+      const int64_t base = ((bi * H + 2 * ho) * W + 2 * wo) * Ch + c;
+      const int64_t o[4] = {base, base + Ch, base + (int64_t)W * Ch, base + (int64_t)W * Ch + Ch};
+      float v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = ElemT<T>::to_f(a[o[q]]);
+      int arg = 0;
+#pragma unroll
+      for (int q = 1; q < 4; ++q)
+        if (v[q] > v[arg]) arg = q;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) gpre[o[q]] = (q == arg && v[q] > 0.f) ? g : T(0);
+    } else {
+      const int64_t bi = r / ((int64_t)H * W);
+      const T g = ElemT<T>::from_f(dh[bi * Ch + c] / (float)(H * W));
+      gpre[i] = ElemT<T>::to_f(a[i]) > 0.f ? g : T(0);
+    }
+  }
+}
+
+// ----------------------------------------------------- split-K reduction
+// grad[w_off + j] = sum over splits (in order) of the partial weight
+// gradients; grad[b_off + c] likewise for the bias.
+__global__ void __launch_bounds__(256)
+wgrad_reduce_kernel(const float *__restrict__ dw, const float *__restrict__ db, int splits,
+                    int64_t dw_ss, int64_t dw_rs, int64_t db_ss, int64_t db_rs,
+                    float *__restrict__ grad, int64_t P, int64_t w_off, int64_t b_off, int64_t nw,
+                    int co) {
+  const int rep = blockIdx.y;
+  for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < nw + co;
+       j += (int64_t)gridDim.x * blockDim.x) {
+    float s = 0.f;
+    if (j < nw) {
+      for (int k = 0; k < splits; ++k) s += dw[k * dw_ss + rep * dw_rs + j];
+      grad[rep * P + w_off + j] = s;
+    } else {
+      const int64_t c = j - nw;
+      for (int k = 0; k < splits; ++k) s += db[k * db_ss + rep * db_rs + c];
+      grad[rep * P + b_off + c] = s;
+    }
+  }
+}
+
+// ------------------------------------------------------------------- SGD
+__global__ void __launch_bounds__(256)
+sgd_kernel(float *__restrict__ theta, float *__restrict__ mom, const float *__restrict__ grad,
+           int64_t n, float lr, float mu) {
+  const int64_t nv = n >> 2;
+  float4 *t4 = reinterpret_cast<float4 *>(theta);
+  float4 *m4 = reinterpret_cast<float4 *>(mom);
+  const float4 *g4 = reinterpret_cast<const float4 *>(grad);
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nv;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    float4 v = m4[i], t = t4[i];
+    const float4 g = g4[i];
+    v.x = mu * v.x + g.x; v.y = mu * v.y + g.y; v.z = mu * v.z + g.z; v.w = mu * v.w + g.w;
+    t.x -= lr * v.x; t.y -= lr * v.y; t.z -= lr * v.z; t.w -= lr * v.w;
+    m4[i] = v;
+    t4[i] = t;
+  }
+  for (int64_t i = 4 * nv + blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const float v = mu * mom[i] + grad[i];
+    mom[i] = v;
+    theta[i] -= lr * v;
+  }
+}
+
+// ---------------------------------------------------------------- fusion
+// Eq. 5: theta_bar[p] = (sum_n w_n theta_n[p]) / W in fp64, in cluster order,
+// rounded once to fp32 and written back to every replica.
+__global__ void __launch_bounds__(256)
+fuse_kernel(float *__restrict__ theta, const double *__restrict__ w, double W, int C, int64_t P) {
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < P;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    double acc = 0.0;
+    for (int n = 0; n < C; ++n) acc += w[n] * (double)theta[n * P + p];
+    const float v = (float)(acc / W);
+    for (int n = 0; n < C; ++n) theta[n * P + p] = v;
+  }
+}
+
+inline unsigned grid_for(int64_t n, int per = 256, unsigned cap = 65535u * 8u) {
+  const int64_t g = (n + per - 1) / per;
+  return (unsigned)(g < 1 ? 1 : (g > cap ? cap : g));
+}
+
+}  // namespace
+
+hipError_t launch_sample(const int32_t *ids, const int64_t *off, const int32_t *coe,
+                         const int32_t *labels, int32_t *idx, int32_t *y, int32_t *hits, int C,
+                         int B, int K, uint64_t seed, int64_t step0, int nsteps, int64_t max_steps,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(sample_kernel, dim3(C, nsteps), dim3(256), 0, s, ids, off, coe, labels, idx, y,
+                     hits, C, B, K, seed, step0, max_steps);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const float *images, const int32_t *idx, void *x, int dtype, int64_t rows,
+                         int64_t row_elems, hipStream_t s) {
+  if (dtype == GCPSL_BF16)
+    hipLaunchKernelGGL(gather_kernel<bf16_t>, dim3((unsigned)rows), dim3(256), 0, s, images, idx,
+                       (bf16_t *)x, row_elems);
+  else
+    hipLaunchKernelGGL(gather_kernel<float>, dim3((unsigned)rows), dim3(256), 0, s, images, idx,
+                       (float *)x, row_elems);
+  return hipGetLastError();
+}
+
+hipError_t launch_prep_weights(int dtype, const float *theta, int64_t P, int C, int64_t w_off,
+                               int co, int ci, void *wf, int Kp, void *wd, int Kdp, hipStream_t s) {
+  const int64_t n = (int64_t)co * Kp + (wd ? (int64_t)ci * Kdp : 0);
+  const dim3 grid(grid_for(n, 256, 4096), C);
+  if (dtype == GCPSL_BF16)
+    hipLaunchKernelGGL(prep_kernel<bf16_t>, grid, dim3(256), 0, s, theta, P, w_off, co, ci,
+                       (bf16_t *)wf, Kp, (bf16_t *)wd, Kdp);
+  else
+    hipLaunchKernelGGL(prep_kernel<float>, grid, dim3(256), 0, s, theta, P, w_off, co, ci,
+                       (float *)wf, Kp, (float *)wd, Kdp);
+  return hipGetLastError();
+}
+
+hipError_t launch_maxpool_fwd(int dtype, const void *x, void *z, int C, int Bt, int H, int W, int Ch,
+                              hipStream_t s) {
+  const int64_t total = (int64_t)C * Bt * (H / 2) * (W / 2) * Ch;
+  if (dtype == GCPSL_BF16)
+    hipLaunchKernelGGL(maxpool_fwd_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s,
+                       (const bf16_t *)x, (bf16_t *)z, total, H, W, Ch);
+  else
+    hipLaunchKernelGGL(maxpool_fwd_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s,
+                       (const float *)x, (float *)z, total, H, W, Ch);
+  return hipGetLastError();
+}
+
+hipError_t launch_maxpool_bwd(int dtype, const void *a, const void *gz, void *gpre, int C, int Bt,
+                              int H, int W, int Ch, hipStream_t s) {
+  const int64_t total = (int64_t)C * Bt * (H / 2) * (W / 2) * Ch;
+  if (dtype == GCPSL_BF16)
+    hipLaunchKernelGGL(maxpool_bwd_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s,
+                       (const bf16_t *)a, (const bf16_t *)gz, (bf16_t *)gpre, total, H, W, Ch);
+  else
+    hipLaunchKernelGGL(maxpool_bwd_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s,
+                       (const float *)a, (const float *)gz, (float *)gpre, total, H, W, Ch);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_pool(int dtype, const void *a, void *h, int C, int Bt, int H, int W, int Ch,
+                            int maxpool, hipStream_t s) {
+  const int64_t total = (int64_t)C * Bt * Ch;
+  if (dtype == GCPSL_BF16)
+    hipLaunchKernelGGL(head_pool_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s,
+                       (const bf16_t *)a, (bf16_t *)h, total, H, W, Ch, maxpool);
+  else
+    hipLaunchKernelGGL(head_pool_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s,
+                       (const float *)a, (float *)h, total, H, W, Ch, maxpool);
+  return hipGetLastError();
+}
+
+hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const float *theta, int64_t P,
+                            int64_t w_off, int64_t b_off, float *grad, float *dh, float *loss, int C,
+                            int Bt, int Ch, int L, hipStream_t s) {
+  const size_t shm = sizeof(float) * ((size_t)Bt * L + Bt);
+  if (dtype == GCPSL_BF16)
+    hipLaunchKernelGGL(linear_ce_kernel<bf16_t>, dim3(C), dim3(256), shm, s, (const bf16_t *)h, y,
+                       theta, P, w_off, b_off, grad, dh, loss, Bt, Ch, L);
+  else
+    hipLaunchKernelGGL(linear_ce_kernel<float>, dim3(C), dim3(256), shm, s, (const float *)h, y,
+                       theta, P, w_off, b_off, grad, dh, loss, Bt, Ch, L);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_pool_bwd(int dtype, const void *a, const float *dh, void *gpre, int C, int Bt,
+                                int H, int W, int Ch, int maxpool, hipStream_t s) {
+  const int64_t total = maxpool ? (int64_t)C * Bt * (H / 2) * (W / 2) * Ch : (int64_t)C * Bt * H * W * Ch;
+  if (dtype == GCPSL_BF16)
+    hipLaunchKernelGGL(head_pool_bwd_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s,
+                       (const bf16_t *)a, dh, (bf16_t *)gpre, total, H, W, Ch, maxpool);
+  else
+    hipLaunchKernelGGL(head_pool_bwd_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s,
+                       (const float *)a, dh, (float *)gpre, total, H, W, Ch, maxpool);
+  return hipGetLastError();
+}
+
+hipError_t launch_wgrad_reduce(const float *dw, const float *db, int splits, int64_t dw_ss,
+                               int64_t dw_rs, int64_t db_ss, int64_t db_rs, float *grad, int64_t P,
+                               int64_t w_off, int64_t b_off, int64_t nw, int co, int C,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(grid_for(nw + co, 256, 4096), C), dim3(256), 0, s, dw,
+                     db, splits, dw_ss, dw_rs, db_ss, db_rs, grad, P, w_off, b_off, nw, co);
+  return hipGetLastError();
+}
+
+hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t n, float lr, float mu,
+                      hipStream_t s) {
+  hipLaunchKernelGGL(sgd_kernel, dim3(grid_for(n / 4 + 1, 256, 8192)), dim3(256), 0, s, theta, mom,
+                     grad, n, lr, mu);
+  return hipGetLastError();
+}
+
+hipError_t launch_fuse(float *theta, const double *weights, double W, int C, int64_t P,
+                       hipStream_t s) {
+  hipLaunchKernelGGL(fuse_kernel, dim3(grid_for(P, 256, 8192)), dim3(256), 0, s, theta, weights, W, C,
+                     P);
+  return hipGetLastError();
+}

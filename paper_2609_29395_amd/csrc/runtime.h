@@ -1,0 +1,80 @@
+// Host runtime internals: error state, the layer plan and kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/gcpsl.h"
+#include "common.h"
+
+// ----------------------------------------------------------------- errors
+void gcpsl_clear_error();
+int gcpsl_fail(int code, const std::string &msg);
+
+// ------------------------------------------------------------ kernel args
+
+// Implicit-GEMM 3x3 conv, forward or input-gradient form:
+//   out[m][n] = epi( sum_k A[m][k] * Wt[n][k] ),  m = (b, h, w), k = (r, s, c)
+//   A[m][k] = src[b][h + r - 1][w + s - 1][c] (zero outside the image).
+enum ConvEpi { EPI_FWD = 0, EPI_DGRAD = 1 };
+struct ConvArgs {
+  const void *src;   // [C][Bt][H][W][Csrc]
+  const void *wt;    // [C][N][Kp]  (k = (r, s, c), rows zero-padded to Kp)
+  void *out;         // [C][Bt][H][W][N]
+  const float *bias; // fwd: [C][...] bias of this layer (stride bias_rs)
+  const void *res;   // residual input [C][Bt][H][W][N] or null
+  const void *mask;  // dgrad: mask source [C][Bt][H][W][N] (value > 0) or null
+  int Bt, H, W, Csrc, N, K, Kp;
+  int64_t src_rs, wt_rs, out_rs, bias_rs;  // per-replica strides (elements)
+  int C;
+  int epi;
+};
+
+// Weight gradient: dW[co][kk] = sum_p G[p][co] X(p, kk), kk = (r, s, ci),
+// and (optionally) db[co] = sum_p G[p][co].  Split over pixel ranges.
+struct WgradArgs {
+  const void *g;  // [C][Bt][H][W][Co] pre-activation gradient
+  const void *x;  // [C][Bt][H][W][Ci] layer input
+  float *dw;      // split s, replica r: dw + s*dw_ss + r*dw_rs, [Co][9Ci]
+  float *db;      // db + s*db_ss + r*db_rs, [Co]
+  int Bt, H, W, Ci, Co;
+  int64_t g_rs, x_rs, dw_rs, dw_ss, db_rs, db_ss;
+  int C, splits, chunk;  // pixel chunk per split (multiple of the k tile)
+};
+
+// ---------------------------------------------------------------- launchers
+hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s);
+hipError_t launch_wgrad(int dtype, const WgradArgs &a, hipStream_t s);
+int wgrad_k_tile(int dtype);
+
+hipError_t launch_sample(const int32_t *ids, const int64_t *off, const int32_t *coe,
+                         const int32_t *labels, int32_t *idx, int32_t *y, int32_t *hits,
+                         int C, int B, int K, uint64_t seed, int64_t step0, int nsteps,
+                         int64_t max_steps, hipStream_t s);
+hipError_t launch_gather(const float *images, const int32_t *idx, void *x, int dtype,
+                         int64_t rows, int64_t row_elems, hipStream_t s);
+hipError_t launch_prep_weights(int dtype, const float *theta, int64_t P, int C, int64_t w_off,
+                               int co, int ci, void *wf, int Kp, void *wd, int Kdp,
+                               hipStream_t s);
+hipError_t launch_maxpool_fwd(int dtype, const void *x, void *z, int C, int Bt, int H, int W,
+                              int Ch, hipStream_t s);
+hipError_t launch_maxpool_bwd(int dtype, const void *a, const void *gz, void *gpre, int C,
+                              int Bt, int H, int W, int Ch, hipStream_t s);
+hipError_t launch_head_pool(int dtype, const void *a, void *h, int C, int Bt, int H, int W,
+                            int Ch, int maxpool, hipStream_t s);
+hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const float *theta,
+                            int64_t P, int64_t w_off, int64_t b_off, float *grad, float *dh,
+                            float *loss, int C, int Bt, int Ch, int L, hipStream_t s);
+hipError_t launch_head_pool_bwd(int dtype, const void *a, const float *dh, void *gpre, int C,
+                                int Bt, int H, int W, int Ch, int maxpool, hipStream_t s);
+hipError_t launch_wgrad_reduce(const float *dw, const float *db, int splits, int64_t dw_ss,
+                               int64_t dw_rs, int64_t db_ss, int64_t db_rs, float *grad,
+                               int64_t P, int64_t w_off, int64_t b_off, int64_t nw, int co,
+                               int C, hipStream_t s);
+hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t n, float lr,
+                      float mu, hipStream_t s);
+hipError_t launch_fuse(float *theta, const double *weights, double W, int C, int64_t P,
+                       hipStream_t s);

@@ -1,0 +1,243 @@
+"""ctypes binding of libgcpsl.so (include/gcpsl.h): argument marshalling only.
+
+Every computation of the hot path runs in the library's HIP kernels.  PyTorch
+is used for device memory (the caller-owned buffers the C ABI works in) and
+for the stream handle.  If the library has not been built, every entry point
+raises; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgcpsl.so")
+
+OK, EINVAL, ESTATE, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4
+RULES = {"random": 0, "size": 1, "label_l1": 2}
+DTYPES = {"f32": 0, "bf16": 1}
+CONV3X3, MAXPOOL2, AVGPOOL, LINEAR = 1, 2, 3, 4
+RESIDUAL = 1
+
+EXPORTS = ["gcpsl_param_count", "gcpsl_workspace_bytes", "gcpsl_assign", "gcpsl_create",
+           "gcpsl_sample", "gcpsl_step", "gcpsl_fuse", "gcpsl_participation",
+           "gcpsl_cluster_sizes", "gcpsl_tensor", "gcpsl_destroy", "gcpsl_last_error"]
+
+
+class GCPSLError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"gcpsl error {code}: {msg}")
+        self.code = code
+
+
+class Layer(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("cin", C.c_int32), ("cout", C.c_int32), ("flags", C.c_int32)]
+
+
+class Desc(C.Structure):
+    _fields_ = [
+        ("K", C.c_int32), ("C", C.c_int32), ("B", C.c_int32), ("L", C.c_int32),
+        ("H", C.c_int32), ("W", C.c_int32), ("Cin", C.c_int32), ("dtype", C.c_int32),
+        ("n_examples", C.c_int64), ("n_layers", C.c_int32), ("cut", C.c_int32),
+        ("layers", C.POINTER(Layer)), ("lr", C.c_float), ("momentum", C.c_float),
+        ("seed", C.c_uint64), ("max_steps", C.c_int64), ("max_window", C.c_int32),
+        ("reserved", C.c_int32), ("client_of_example", C.POINTER(C.c_int32)),
+        ("cluster_of_client", C.POINTER(C.c_int32)), ("images", C.c_void_p),
+        ("labels", C.c_void_p), ("theta", C.c_void_p), ("momentum_buf", C.c_void_p),
+        ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    """Load libgcpsl.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2609_29395_amd.build`")
+    L = C.CDLL(LIB_PATH)
+    vp, i32, i64, u64 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64
+    P = C.POINTER
+    L.gcpsl_param_count.argtypes = [P(Desc), P(i64), P(i64)]
+    L.gcpsl_workspace_bytes.argtypes = [P(Desc), P(C.c_size_t)]
+    L.gcpsl_assign.argtypes = [i32, i32, i32, u64, P(i64), P(i64), i32, P(i32)]
+    L.gcpsl_create.argtypes = [P(Desc), P(vp)]
+    L.gcpsl_sample.argtypes = [vp, i64, i32, vp, vp]
+    L.gcpsl_step.argtypes = [vp, i64, vp, vp]
+    L.gcpsl_fuse.argtypes = [vp, vp]
+    L.gcpsl_participation.argtypes = [vp, P(i64), P(i64), P(i32)]
+    L.gcpsl_cluster_sizes.argtypes = [vp, P(i64)]
+    L.gcpsl_tensor.argtypes = [vp, C.c_char_p, P(vp), P(i64), P(i32)]
+    L.gcpsl_destroy.argtypes = [vp]
+    L.gcpsl_destroy.restype = None
+    L.gcpsl_last_error.restype = C.c_char_p
+    for name in EXPORTS:
+        if name not in ("gcpsl_destroy", "gcpsl_last_error"):
+            getattr(L, name).restype = C.c_int
+    _lib = L
+    return L
+
+
+def _check(rc):
+    if rc != OK:
+        raise GCPSLError(rc, lib().gcpsl_last_error().decode())
+
+
+def _i32p(a):
+    return a.ctypes.data_as(C.POINTER(C.c_int32))
+
+
+def _i64p(a):
+    return a.ctypes.data_as(C.POINTER(C.c_int64))
+
+
+def layers_struct(layers):
+    arr = (Layer * len(layers))()
+    for i, spec in enumerate(layers):
+        kind = spec[0]
+        if kind == "conv":
+            arr[i] = Layer(CONV3X3, spec[1], spec[2], RESIDUAL if spec[3] else 0)
+        elif kind == "maxpool":
+            arr[i] = Layer(MAXPOOL2, 0, 0, 0)
+        elif kind == "avgpool":
+            arr[i] = Layer(AVGPOOL, 0, 0, 0)
+        elif kind == "linear":
+            arr[i] = Layer(LINEAR, spec[1], spec[2], 0)
+        else:
+            raise ValueError(kind)
+    return arr
+
+
+def assign(rule, K, C_, seed, counts=None, hist=None):
+    """gcpsl_assign: Alg. 1 cluster_of_client (host)."""
+    out = np.zeros(K, dtype=np.int32)
+    cnt = None if counts is None else np.ascontiguousarray(counts, dtype=np.int64)
+    h = None if hist is None else np.ascontiguousarray(hist, dtype=np.int64)
+    L = 0 if h is None else h.shape[1]
+    _check(lib().gcpsl_assign(K, C_, RULES[rule] if isinstance(rule, str) else rule, seed,
+                              None if cnt is None else _i64p(cnt), None if h is None else _i64p(h),
+                              L, _i32p(out)))
+    return out
+
+
+def make_desc(cfg, client_of_example, cluster_of_client, max_steps=None, max_window=1):
+    """Host part of gcpsl_desc for a workload (device pointers filled by Context)."""
+    d = Desc()
+    d.K, d.C, d.B, d.L = cfg["K"], cfg["C"], cfg["B"], cfg["L"]
+    d.H, d.W, d.Cin = cfg["H"], cfg["W"], cfg["Cin"]
+    d.dtype = DTYPES[cfg["dtype"]]
+    d.n_examples = cfg["N_ex"]
+    keep = {"layers": layers_struct(cfg["layers"]),
+            "coe": np.ascontiguousarray(client_of_example, dtype=np.int32),
+            "coc": np.ascontiguousarray(cluster_of_client, dtype=np.int32)}
+    d.n_layers = len(cfg["layers"])
+    d.cut = cfg["cut"]
+    d.layers = C.cast(keep["layers"], C.POINTER(Layer))
+    d.lr, d.momentum = cfg["lr"], cfg["momentum"]
+    d.seed = cfg["seed"]
+    d.max_steps = max_steps if max_steps is not None else cfg["T"]
+    d.max_window = max_window
+    d.reserved = 0
+    d.client_of_example = _i32p(keep["coe"])
+    d.cluster_of_client = _i32p(keep["coc"])
+    return d, keep
+
+
+def param_count(desc):
+    P, Pc = C.c_int64(), C.c_int64()
+    _check(lib().gcpsl_param_count(C.byref(desc), C.byref(P), C.byref(Pc)))
+    return P.value, Pc.value
+
+
+def workspace_bytes(desc):
+    n = C.c_size_t()
+    _check(lib().gcpsl_workspace_bytes(C.byref(desc), C.byref(n)))
+    return n.value
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return C.c_void_p(s.cuda_stream)
+
+
+class Context:
+    """One gcpsl_ctx with the caller-owned device buffers it works in."""
+
+    def __init__(self, cfg, images, labels, client_of_example, cluster_of_client, theta0,
+                 max_steps=None, max_window=1, device="cuda"):
+        import torch
+        self.cfg = cfg
+        desc, self._keep = make_desc(cfg, client_of_example, cluster_of_client, max_steps, max_window)
+        self.P, self.P_client = param_count(desc)
+        t0 = torch.as_tensor(np.asarray(theta0, dtype=np.float32))
+        if t0.numel() != self.P:
+            raise ValueError(f"theta0 has {t0.numel()} entries, the model has {self.P}")
+        self.images = torch.as_tensor(np.asarray(images, dtype=np.float32)).to(device).contiguous()
+        self.labels = torch.as_tensor(np.asarray(labels, dtype=np.int32)).to(device).contiguous()
+        self.theta = t0.to(device).reshape(1, -1).repeat(cfg["C"], 1).contiguous()
+        self.mom = torch.zeros_like(self.theta)
+        nbytes = workspace_bytes(desc)
+        self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+        base = self.workspace.data_ptr()
+        self._ws_off = (-base) % 256
+        desc.images = self.images.data_ptr()
+        desc.labels = self.labels.data_ptr()
+        desc.theta = self.theta.data_ptr()
+        desc.momentum_buf = self.mom.data_ptr()
+        desc.workspace = base + self._ws_off
+        desc.workspace_bytes = nbytes
+        self.desc = desc
+        h = C.c_void_p()
+        _check(lib().gcpsl_create(C.byref(desc), C.byref(h)))
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            lib().gcpsl_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def sample(self, step, nsteps=1, idx_out=None, stream=None):
+        ptr = None if idx_out is None else C.c_void_p(idx_out.data_ptr())
+        _check(lib().gcpsl_sample(self._h, step, nsteps, ptr, _stream(stream)))
+
+    def step(self, step, loss_out=None, stream=None):
+        ptr = None if loss_out is None else C.c_void_p(loss_out.data_ptr())
+        _check(lib().gcpsl_step(self._h, step, ptr, _stream(stream)))
+
+    def fuse(self, stream=None):
+        _check(lib().gcpsl_fuse(self._h, _stream(stream)))
+
+    def participation(self):
+        a, t = C.c_int64(), C.c_int64()
+        T = self.desc.max_steps
+        per = np.zeros((T, self.cfg["C"]), dtype=np.int32)
+        _check(lib().gcpsl_participation(self._h, C.byref(a), C.byref(t), _i32p(per)))
+        steps = t.value // self.cfg["K"] if self.cfg["K"] else 0
+        return a.value, t.value, per[:steps]
+
+    def cluster_sizes(self):
+        out = np.zeros(self.cfg["C"], dtype=np.int64)
+        _check(lib().gcpsl_cluster_sizes(self._h, _i64p(out)))
+        return out
+
+    def tensor(self, name):
+        """torch view of a named workspace tensor (gcpsl_tensor)."""
+        import torch
+        ptr, n, dt = C.c_void_p(), C.c_int64(), C.c_int32()
+        _check(lib().gcpsl_tensor(self._h, name.encode(), C.byref(ptr), C.byref(n), C.byref(dt)))
+        tdt = {0: torch.float32, 1: torch.bfloat16, -1: torch.int32}[dt.value]
+        esz = torch.tensor([], dtype=tdt).element_size()
+        off = ptr.value - self.workspace.data_ptr()
+        return self.workspace[off:off + n.value * esz].view(tdt)

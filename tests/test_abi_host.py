@@ -1,0 +1,164 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+The library must load, export every function include/gcpsl.h declares, run
+Alg. 1 on the host bit-exactly like the oracle, and reject bad arguments with
+the documented codes before touching the device.
+"""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from gcpsl_inputs import client_stats, get_config, make_dataset, param_counts
+from oracle.assign import assign as oracle_assign
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+g = pytest.importorskip("paper_2609_29395_amd.gcpsl")
+
+if not os.path.exists(g.LIB_PATH):
+    pytest.skip("libgcpsl.so not built", allow_module_level=True)
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "gcpsl.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gcpsl_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    lib = g.lib()
+    names = header_functions()
+    assert set(names) == set(g.EXPORTS), names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_library_has_no_cuda_symbols():
+    out = os.popen(f"nm -D --defined-only {g.LIB_PATH}").read()
+    assert "cuda" not in out.lower()
+
+
+@pytest.mark.parametrize("name", ["tiny", "gcpsl4", "gcpsl8", "gcpsl16", "ragged", "ragged_bf16"])
+def test_assign_matches_oracle_bit_exact(name):
+    cfg = get_config(name)
+    _, labels, coe = make_dataset(cfg)
+    counts, hist = client_stats(cfg, labels, coe)
+    for rule in ("random", "size", "label_l1"):
+        for seed in (0, 1, 12345):
+            want = oracle_assign(rule, cfg["K"], cfg["C"], seed, counts, hist)
+            got = g.assign(rule, cfg["K"], cfg["C"], seed, counts, hist)
+            assert np.array_equal(got, want), (rule, seed)
+
+
+def test_assign_random_many_shapes():
+    for K, Cc in [(1, 1), (2, 2), (3, 2), (17, 5), (1000, 7), (65536, 64)]:
+        for seed in (0, 2**63 + 5):
+            assert np.array_equal(g.assign("random", K, Cc, seed), oracle_assign("random", K, Cc, seed))
+
+
+def test_assign_label_l1_random_histograms():
+    rng = np.random.default_rng(7)
+    for trial in range(20):
+        K, Cc, L = int(rng.integers(2, 60)), int(rng.integers(1, 9)), int(rng.integers(1, 12))
+        Cc = min(Cc, K)
+        hist = rng.integers(0, 30, size=(K, L)) * (rng.random((K, L)) < 0.5)
+        counts = hist.sum(1)
+        for rule in ("size", "label_l1"):
+            assert np.array_equal(g.assign(rule, K, Cc, 0, counts, hist),
+                                  oracle_assign(rule, K, Cc, 0, counts, hist))
+
+
+def test_assign_errors():
+    counts = np.ones(4, dtype=np.int64)
+    with pytest.raises(g.GCPSLError) as e:
+        g.assign("random", 4, 5, 0)
+    assert e.value.code == g.EINVAL
+    with pytest.raises(g.GCPSLError) as e:
+        g.assign(7, 4, 2, 0, counts)
+    assert e.value.code == g.EINVAL
+    with pytest.raises(g.GCPSLError) as e:
+        g.assign("size", 4, 2, 0)
+    assert e.value.code == g.EINVAL
+    with pytest.raises(g.GCPSLError) as e:
+        g.assign("label_l1", 4, 2, 0, counts)
+    assert e.value.code == g.EINVAL
+    bad = np.array([[1, 0], [0, 1], [1, 1], [2, 0]])
+    with pytest.raises(g.GCPSLError) as e:
+        g.assign("label_l1", 4, 2, 0, np.array([1, 1, 1, 1]), bad)  # row 2 sums to 2 != 1
+    assert e.value.code == g.EINVAL
+
+
+@pytest.mark.parametrize("name", ["tiny", "gpsl", "gcpsl16", "ragged"])
+def test_param_count_matches_layout(name):
+    cfg = get_config(name)
+    _, labels, coe = make_dataset(cfg)
+    d, keep = g.make_desc(cfg, coe, np.zeros(cfg["K"], np.int32))
+    P, Pc = g.param_count(d)
+    pc, ps = param_counts(cfg)
+    assert (P, Pc) == (pc + ps, pc)
+    assert g.workspace_bytes(d) > 0
+
+
+def test_survey_parameter_counts():
+    assert param_counts(get_config("tiny")) == (224, 1236)
+    assert param_counts(get_config("gpsl")) == (19392, 222730)
+    assert param_counts(get_config("gcpsl16")) == (19392, 1920522)
+
+
+def _desc(cfg, **over):
+    _, labels, coe = make_dataset(cfg)
+    d, keep = g.make_desc(cfg, coe, np.arange(cfg["K"], dtype=np.int32) % cfg["C"])
+    for k, v in over.items():
+        setattr(d, k, v)
+    return d, keep
+
+
+def _create(d):
+    h = C.c_void_p()
+    rc = g.lib().gcpsl_create(C.byref(d), C.byref(h))
+    return rc, g.lib().gcpsl_last_error().decode()
+
+
+def test_create_rejects_bad_descriptions_before_device_work():
+    cfg = get_config("tiny")
+    fake = 1 << 20  # never dereferenced: every case fails validation first
+    base = dict(images=fake, labels=fake, theta=fake, momentum_buf=fake, workspace=fake,
+                workspace_bytes=1 << 40)
+    d, k = _desc(cfg, **base)
+    d.images = None
+    assert _create(d)[0] == g.EINVAL
+    d, k = _desc(cfg, **dict(base, workspace_bytes=16))
+    rc, msg = _create(d)
+    assert rc == g.EINVAL and "workspace" in msg
+    d, k = _desc(cfg, **dict(base, workspace=fake + 8))
+    assert _create(d)[0] == g.EINVAL
+    d, k = _desc(cfg, **dict(base, B=10**6))
+    rc, msg = _create(d)
+    assert rc == g.EINVAL and "< B" in msg
+    d, k = _desc(cfg, **dict(base, reserved=1))
+    assert _create(d)[0] == g.EINVAL
+    d, k = _desc(cfg, **dict(base, dtype=9))
+    assert _create(d)[0] == g.EINVAL
+
+
+def test_unsupported_models_are_reported():
+    cfg = get_config("tiny", layers=[("conv", 3, 12, False), ("maxpool",), ("conv", 12, 16, False),
+                                     ("avgpool",), ("linear", 16, 4)])
+    d, k = _desc(cfg)
+    with pytest.raises(g.GCPSLError) as e:
+        g.param_count(d)
+    assert e.value.code == g.EUNSUPPORTED
+    cfg = get_config("tiny", layers=[("conv", 3, 8, False), ("avgpool",), ("conv", 8, 16, False),
+                                     ("linear", 16, 4)])
+    d, k = _desc(cfg)
+    with pytest.raises(g.GCPSLError) as e:
+        g.param_count(d)
+    assert e.value.code in (g.EUNSUPPORTED, g.EINVAL)
+    cfg = get_config("tiny", layers=[("conv", 3, 8, True), ("maxpool",), ("conv", 8, 16, False),
+                                     ("avgpool",), ("linear", 16, 4)])
+    d, k = _desc(cfg)
+    with pytest.raises(g.GCPSLError) as e:
+        g.param_count(d)
+    assert e.value.code == g.EINVAL

@@ -1,0 +1,232 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Bar: bit-exact on sampled indices, labels, gathered inputs (as values),
+cluster assignments, participation counts and fusion of given replicas;
+floating point within tol = 1e-4 (fp32 workloads) or 2e-2 (bf16 workloads),
+tested per tensor as ||a - b||_2 <= tol ||b||_2 and max|a - b| <= tol max|b|,
+and elementwise relative for the per-cluster losses.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gcpsl_inputs import client_stats, get_config, init_params, make_dataset
+from oracle.model import round_bf16, split_forward_backward
+from oracle.sampler import active_clients, batch_indices, cluster_examples
+from oracle.train import GCPSLOracle, fuse as oracle_fuse
+
+pytestmark = pytest.mark.gpu
+
+from paper_2609_29395_amd import driver, gcpsl  # noqa: E402
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def close(a, b, tol):
+    a = np.asarray(a, dtype=np.float64).ravel()
+    b = np.asarray(b, dtype=np.float64).ravel()
+    assert a.shape == b.shape, (a.shape, b.shape)
+    nb = np.linalg.norm(b)
+    err = np.linalg.norm(a - b)
+    mx = np.abs(b).max() if b.size else 0.0
+    ok = err <= tol * nb + 1e-30 and np.abs(a - b).max() <= tol * mx + 1e-30
+    return ok, (err / (nb + 1e-30), np.abs(a - b).max() / (mx + 1e-30))
+
+
+def _np(t):
+    if t.dtype == torch.bfloat16:
+        t = t.float()
+    return t.cpu().numpy()
+
+
+# ---------------------------------------------------------------- sampling
+
+@pytest.mark.parametrize("name,window,starts", [
+    ("tiny", 4, [0, 20, 97]),
+    ("ragged", 3, [0, 21, 500]),
+    ("gcpsl4", 2, [0, 195, 196]),
+    ("gcpsl16", 2, [0, 1, 87, 999]),
+])
+def test_sample_and_gather_bit_exact(name, window, starts):
+    cfg = get_config(name)
+    images, labels, coe = make_dataset(cfg)
+    ctx, assignment = driver.setup(cfg, max_steps=1000, max_window=window)
+    ids = cluster_examples(coe, assignment, cfg["C"])
+    assert ctx.cluster_sizes().tolist() == [len(x) for x in ids]
+    C, B = cfg["C"], cfg["B"]
+    out = torch.zeros(window, C, B, dtype=torch.int32, device="cuda")
+    for s0 in starts:
+        ctx.sample(s0, window, out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        ys = _np(ctx.tensor("y")).reshape(-1, C, B)
+        xs = _np(ctx.tensor("x")).reshape(-1, C, B, cfg["H"], cfg["W"], cfg["Cin"])
+        for j in range(window):
+            for n in range(C):
+                want = batch_indices(ids[n], B, cfg["seed"], n, s0 + j)
+                assert np.array_equal(got[j, n], want), (s0, j, n)
+                assert np.array_equal(ys[j, n], labels[want])
+                ref = images[want].astype(np.float64)
+                if cfg["dtype"] == "bf16":
+                    ref = round_bf16(ref)
+                assert np.array_equal(xs[j, n].astype(np.float64), ref)
+    # per-step |A_{n,t}| of every sampled step
+    hits = _np(ctx.tensor("hits")).reshape(-1, C)
+    for s0 in starts:
+        for j in range(window):
+            for n in range(C):
+                want = active_clients(batch_indices(ids[n], B, cfg["seed"], n, s0 + j), coe)
+                assert hits[s0 + j, n] == want
+
+
+# ------------------------------------------------------- multi-step runs
+
+@pytest.mark.parametrize("name", ["tiny", "ragged", "ragged_bf16"])
+def test_run_parity_with_fusion(name):
+    cfg = get_config(name)
+    T = cfg["T"]
+    ctx, assignment = driver.setup(cfg)
+    losses = torch.zeros(T, cfg["C"], device="cuda")
+    driver.train(ctx, T, losses=losses)
+    torch.cuda.synchronize()
+    ref = GCPSLOracle(cfg, cluster_of_client=assignment).run(T)
+    tol = TOL[cfg["dtype"]]
+    got_l, want_l = losses.cpu().numpy(), np.array(ref.losses)
+    assert np.all(np.abs(got_l - want_l) <= tol * np.abs(want_l)), (got_l, want_l)
+    th, mo = ctx.theta.cpu().numpy(), ctx.mom.cpu().numpy()
+    for n in range(cfg["C"]):
+        ok, e = close(th[n], ref.theta[n], tol)
+        assert ok, ("theta", n, e)
+        ok, e = close(mo[n], ref.mom[n], tol)
+        assert ok, ("momentum", n, e)
+    a, t, per = ctx.participation()
+    assert t == cfg["K"] * T
+    assert np.array_equal(per, np.array(ref.active)) and a == int(np.sum(ref.active))
+
+
+@pytest.mark.parametrize("name", ["ragged", "ragged_bf16", "tiny"])
+def test_intermediates_one_round(name):
+    cfg = get_config(name)
+    ctx, assignment = driver.setup(cfg)
+    ctx.sample(0)
+    loss = torch.zeros(cfg["C"], device="cuda")
+    ctx.step(0, loss)
+    torch.cuda.synchronize()
+    o = GCPSLOracle(cfg, cluster_of_client=assignment)
+    tol = TOL[cfg["dtype"]]
+    C = cfg["C"]
+    grads = _np(ctx.tensor("grad")).reshape(C, -1)
+    for n in range(C):
+        idx, x, y = o.batch(0, n)
+        l, g, rec = split_forward_backward(cfg, o.theta[n], x, y, keep=True)
+        assert abs(loss[n].item() - l) <= tol * abs(l)
+        for i, spec in enumerate(cfg["layers"]):
+            name_i = f"act{i}"
+            try:
+                t = _np(ctx.tensor(name_i)).reshape(C, -1)[n]
+            except gcpsl.GCPSLError:
+                t = None
+            if t is not None and spec[0] != "linear":
+                ok, e = close(t, rec["acts"][i + 1], tol)
+                assert ok, (name_i, n, e)
+            if spec[0] == "conv":
+                ok, e = close(_np(ctx.tensor(f"gpre{i}")).reshape(C, -1)[n], rec[f"gpre{i}"], tol)
+                assert ok, (f"gpre{i}", n, e)
+                if i > 0 and cfg["layers"][i - 1][0] == "maxpool":
+                    ok, e = close(_np(ctx.tensor(f"gin{i}")).reshape(C, -1)[n], rec[f"gin{i}"], tol)
+                    assert ok, (f"gin{i}", n, e)
+        ok, e = close(grads[n], g, tol)
+        assert ok, ("grad", n, e)
+
+
+# ------------------------------------------------------------------ fusion
+
+def test_fusion_bit_exact_against_oracle_on_given_replicas():
+    cfg = get_config("ragged")
+    ctx, assignment = driver.setup(cfg)
+    driver.train(ctx, 3, F=0)
+    torch.cuda.synchronize()
+    before = ctx.theta.cpu().numpy()
+    assert not np.array_equal(before[0], before[1])
+    ctx.fuse()
+    torch.cuda.synchronize()
+    after = ctx.theta.cpu().numpy()
+    want = oracle_fuse(list(before), ctx.cluster_sizes().tolist())
+    for n in range(cfg["C"]):
+        assert np.array_equal(after[n], want)
+    assert not np.array_equal(ctx.mom[0].cpu().numpy(), ctx.mom[1].cpu().numpy())
+
+
+def test_fusion_of_identical_replicas_is_identity():
+    cfg = get_config("gcpsl16")
+    ctx, _ = driver.setup(cfg)
+    before = ctx.theta.clone()
+    ctx.fuse()
+    torch.cuda.synchronize()
+    assert torch.equal(ctx.theta, before)
+
+
+# ------------------------------------------------ full sizes, sampled outputs
+
+@pytest.mark.parametrize("name", ["gpsl", "gcpsl4", "gcpsl8", "gcpsl16"])
+def test_full_size_round_sampled_replicas(name):
+    cfg = get_config(name)
+    ctx, assignment = driver.setup(cfg)
+    C = cfg["C"]
+    ctx.sample(0)
+    loss = torch.zeros(C, device="cuda")
+    ctx.step(0, loss)
+    torch.cuda.synchronize()
+    tol = TOL[cfg["dtype"]]
+    o = GCPSLOracle(cfg, cluster_of_client=assignment)
+    grads = _np(ctx.tensor("grad")).reshape(C, -1)
+    th = ctx.theta.cpu().numpy()
+    for n in sorted({0, C - 1}):
+        idx, x, y = o.batch(0, n)
+        l, g, _ = split_forward_backward(cfg, o.theta[n], x, y)
+        assert abs(loss[n].item() - l) <= tol * abs(l), (n, loss[n].item(), l)
+        ok, e = close(grads[n], g, tol)
+        assert ok, ("grad", n, e)
+        want = o.theta[n].astype(np.float64) - cfg["lr"] * g
+        ok, e = close(th[n], want, tol)
+        assert ok, ("theta", n, e)
+    # participation of the round, every cluster
+    a, t, per = ctx.participation()
+    ids = cluster_examples(make_dataset(cfg)[2], assignment, C)
+    coe = make_dataset(cfg)[2]
+    assert per.shape == (1, C)
+    for n in range(C):
+        assert per[0, n] == active_clients(batch_indices(ids[n], cfg["B"], cfg["seed"], n, 0), coe)
+
+
+# ------------------------------------------------------ invariants, errors
+
+def test_two_runs_are_bit_identical():
+    cfg = get_config("ragged_bf16")
+    outs = []
+    for _ in range(2):
+        ctx, _ = driver.setup(cfg)
+        driver.train(ctx, 4)
+        torch.cuda.synchronize()
+        outs.append(ctx.theta.cpu().numpy())
+    assert np.array_equal(outs[0], outs[1])
+
+
+def test_state_errors():
+    cfg = get_config("tiny")
+    ctx, _ = driver.setup(cfg, max_window=2)
+    with pytest.raises(gcpsl.GCPSLError) as e:
+        ctx.step(0)
+    assert e.value.code == gcpsl.ESTATE
+    with pytest.raises(gcpsl.GCPSLError) as e:
+        ctx.sample(0, 3)
+    assert e.value.code == gcpsl.EINVAL
+    ctx.sample(4, 2)
+    with pytest.raises(gcpsl.GCPSLError) as e:
+        ctx.step(6)
+    assert e.value.code == gcpsl.ESTATE
+    ctx.step(5)
+    ctx.step(4)
+    torch.cuda.synchronize()
+    with pytest.raises(gcpsl.GCPSLError):
+        ctx.tensor("nope")
