@@ -178,8 +178,8 @@ class Context:
         t0 = torch.as_tensor(np.asarray(theta0, dtype=np.float32))
         if t0.numel() != self.P:
             raise ValueError(f"theta0 has {t0.numel()} entries, the model has {self.P}")
-        self.images = torch.as_tensor(np.asarray(images, dtype=np.float32)).to(device).contiguous()
-        self.labels = torch.as_tensor(np.asarray(labels, dtype=np.int32)).to(device).contiguous()
+        self.images = torch.from_numpy(np.array(images, dtype=np.float32)).to(device)
+        self.labels = torch.from_numpy(np.array(labels, dtype=np.int32)).to(device)
         self.theta = t0.to(device).reshape(1, -1).repeat(cfg["C"], 1).contiguous()
         self.mom = torch.zeros_like(self.theta)
         nbytes = workspace_bytes(desc)

@@ -74,6 +74,8 @@ def test_sample_and_gather_bit_exact(name, window, starts):
     hits = _np(ctx.tensor("hits")).reshape(-1, C)
     for s0 in starts:
         for j in range(window):
+            if s0 + j >= hits.shape[0]:
+                continue  # beyond max_steps: not recorded
             for n in range(C):
                 want = active_clients(batch_indices(ids[n], B, cfg["seed"], n, s0 + j), coe)
                 assert hits[s0 + j, n] == want
@@ -168,8 +170,44 @@ def test_fusion_of_identical_replicas_is_identity():
 
 # ------------------------------------------------ full sizes, sampled outputs
 
+def _windows(a, shape):
+    Bt, H, W, Ch = shape
+    return (np.asarray(a).reshape(Bt, H // 2, 2, W // 2, 2, Ch).transpose(0, 1, 3, 5, 2, 4)
+            .reshape(-1, 4))
+
+
+def routing_flips(act_ref, gpre_gpu, gpre_ref, shape, tie):
+    """Windows where the GPU routes a max-pool gradient to another pixel than
+    the oracle.  Where rounding decides between two pixels whose values are
+    within (rel, abs) = tie of each other -- rel of the window maximum, abs of
+    the tensor's largest value, since a one-ulp difference in an upstream
+    input moves every later value by an amount set by that scale -- both
+    choices are correct; any other difference is a bug.  Returns the number
+    of (valid) flips."""
+    rel, absolute = tie
+    A = _windows(act_ref, shape)
+    G = _windows(gpre_gpu, shape) != 0
+    R = _windows(gpre_ref, shape) != 0
+    bad = np.flatnonzero((G != R).any(axis=1))
+    scale = np.abs(A).max()
+    for w in bad:
+        top = A[w].max()
+        chosen = np.flatnonzero(G[w] | R[w])
+        # every pixel either side picked is (within rounding) a maximum of its
+        # window, or a ReLU-clamped value near zero
+        assert np.all(top - A[w][chosen] <= rel * abs(top) + absolute * scale), \
+            (w, A[w], G[w], R[w])
+    return len(bad)
+
+
 @pytest.mark.parametrize("name", ["gpsl", "gcpsl4", "gcpsl8", "gcpsl16"])
 def test_full_size_round_sampled_replicas(name):
+    """One round at the workload's real size; replicas 0 and C-1 recomputed by
+    the oracle.  Forward activations, loss and the updated parameters are held
+    to the parity bar.  Gradients are held to it too unless a max-pool routing
+    decision flipped at a near-tie (checked valid above); one such flip moves
+    |dL/dz| / npos to a neighbouring pixel and was measured at 2e-4 relative on
+    the 64-example gradient, so the gradient bound then widens to 5e-3 (fp32)."""
     cfg = get_config(name)
     ctx, assignment = driver.setup(cfg)
     C = cfg["C"]
@@ -178,22 +216,38 @@ def test_full_size_round_sampled_replicas(name):
     ctx.step(0, loss)
     torch.cuda.synchronize()
     tol = TOL[cfg["dtype"]]
+    # fp32: a few ulp (2^-23) of the window max plus 1e-6 of the scale;
+    # bf16: one ulp is 2^-8 = 3.9e-3, so 2e-2 of the max and 1e-3 of the scale
+    tie = (1e-5, 1e-6) if cfg["dtype"] == "f32" else (2e-2, 1e-3)
     o = GCPSLOracle(cfg, cluster_of_client=assignment)
     grads = _np(ctx.tensor("grad")).reshape(C, -1)
     th = ctx.theta.cpu().numpy()
+    layers = cfg["layers"]
     for n in sorted({0, C - 1}):
         idx, x, y = o.batch(0, n)
-        l, g, _ = split_forward_backward(cfg, o.theta[n], x, y)
+        l, g, rec = split_forward_backward(cfg, o.theta[n], x, y, keep=True)
         assert abs(loss[n].item() - l) <= tol * abs(l), (n, loss[n].item(), l)
-        ok, e = close(grads[n], g, tol)
-        assert ok, ("grad", n, e)
+        flips = 0
+        for i, spec in enumerate(layers):
+            if spec[0] != "conv":
+                continue
+            act = _np(ctx.tensor(f"act{i}")).reshape(C, -1)[n]
+            ok, e = close(act, rec["acts"][i + 1], tol)
+            assert ok, (f"act{i}", n, e)
+            if i + 1 < len(layers) and layers[i + 1][0] == "maxpool":
+                shape = rec["acts"][i + 1].shape
+                gp = _np(ctx.tensor(f"gpre{i}")).reshape(C, -1)[n]
+                flips += routing_flips(rec["acts"][i + 1], gp, rec[f"gpre{i}"], shape, tie)
+        gtol = tol if (flips == 0 or cfg["dtype"] == "bf16") else 5e-3
+        ok, e = close(grads[n], g, gtol)
+        assert ok, ("grad", n, flips, e)
         want = o.theta[n].astype(np.float64) - cfg["lr"] * g
         ok, e = close(th[n], want, tol)
         assert ok, ("theta", n, e)
     # participation of the round, every cluster
     a, t, per = ctx.participation()
-    ids = cluster_examples(make_dataset(cfg)[2], assignment, C)
     coe = make_dataset(cfg)[2]
+    ids = cluster_examples(coe, assignment, C)
     assert per.shape == (1, C)
     for n in range(C):
         assert per[0, n] == active_clients(batch_indices(ids[n], cfg["B"], cfg["seed"], n, 0), coe)
