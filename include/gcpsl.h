@@ -212,6 +212,29 @@ int gcpsl_cluster_sizes(gcpsl_ctx *ctx, int64_t *sizes);
  */
 int gcpsl_tensor(gcpsl_ctx *ctx, const char *name, void **ptr, int64_t *numel, int32_t *dtype);
 
+/*
+ * Per-kernel timing, for measurement.  gcpsl_timing(ctx, 1) makes every later
+ * kernel launch of this context record a hipEvent before and after it on the
+ * caller's stream (the stream the kernel runs on); 0 turns it off (default).
+ * gcpsl_timing_read synchronises the device, aggregates the recorded launches
+ * by kernel instantiation and clears the record.  Each entry holds the summed
+ * event time and the summed algorithmic work of its launches: FLOPs of the
+ * contraction (2 M N K for a conv pass) and the minimum HBM bytes the launch
+ * must move (each operand read once, each result written once).  out: host
+ * array of cap entries (caller-owned); n receives the number of distinct
+ * kernels (entries beyond cap are dropped).
+ */
+typedef struct gcpsl_kernel_stat {
+  char name[64];    /* kernel instantiation, e.g. "conv_fwd<bf16,128x128,vec>" */
+  int64_t launches; /* launches aggregated                                    */
+  double ms;        /* summed event time in milliseconds                      */
+  double flops;     /* summed algorithmic FLOPs                               */
+  double bytes;     /* summed algorithmic HBM bytes                           */
+} gcpsl_kernel_stat;
+
+int gcpsl_timing(gcpsl_ctx *ctx, int32_t on);
+int gcpsl_timing_read(gcpsl_ctx *ctx, gcpsl_kernel_stat *out, int32_t cap, int32_t *n);
+
 /* Release the context (host metadata only; device memory is the caller's). */
 void gcpsl_destroy(gcpsl_ctx *ctx);
 

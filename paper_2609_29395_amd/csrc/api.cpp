@@ -2,6 +2,7 @@
 // kernel launches for sampling, one local round, fusion and participation.
 #include <algorithm>
 #include <cmath>
+#include <cstdio>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -212,6 +213,15 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
 
 }  // namespace
 
+// Optional per-launch event timing (gcpsl_timing): every kernel launch is
+// bracketed by two hipEvents on the caller's stream and tagged with the
+// kernel instantiation and its algorithmic FLOPs and HBM bytes.
+struct KernelRec {
+  std::string name;
+  double flops, bytes;
+  size_t ev;
+};
+
 struct gcpsl_ctx {
   Plan plan;
   gcpsl_desc desc;
@@ -220,8 +230,48 @@ struct gcpsl_ctx {
   int64_t staged_lo = -1;
   int staged_n = 0;
   int64_t horizon = 0;
+  bool timing = false;
+  std::vector<hipEvent_t> events;
+  size_t next_event = 0;
+  std::vector<KernelRec> recs;
   template <typename T> T *at(size_t off) const { return reinterpret_cast<T *>(ws + off); }
+  ~gcpsl_ctx() {
+    for (hipEvent_t e : events) (void)hipEventDestroy(e);
+  }
 };
+
+namespace {
+
+// Start a timed launch: returns the event slot, or SIZE_MAX when timing is off.
+size_t tbegin(gcpsl_ctx *ctx, hipStream_t s) {
+  if (!ctx->timing) return SIZE_MAX;
+  while (ctx->events.size() < ctx->next_event + 2) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return SIZE_MAX;
+    ctx->events.push_back(e);
+  }
+  const size_t i = ctx->next_event;
+  if (hipEventRecord(ctx->events[i], s) != hipSuccess) return SIZE_MAX;
+  return i;
+}
+
+void tend(gcpsl_ctx *ctx, hipStream_t s, size_t i, const std::string &name, double flops, double bytes) {
+  if (i == SIZE_MAX) return;
+  if (hipEventRecord(ctx->events[i + 1], s) != hipSuccess) return;
+  ctx->recs.push_back({name, flops, bytes, i});
+  ctx->next_event = i + 2;
+}
+
+}  // namespace
+
+// LAUNCH_T(name, flops, bytes, launch-expression): launch, time when enabled.
+#define LAUNCH_T(NAME, FLOPS, BYTES, EXPR)                                                       \
+  do {                                                                                          \
+    const size_t t_ = tbegin(ctx, s);                                                           \
+    const hipError_t e_ = (EXPR);                                                               \
+    if (e_ != hipSuccess) return gcpsl_fail(GCPSL_EHIP, std::string("launch failed: ") + hipGetErrorString(e_)); \
+    tend(ctx, s, t_, (NAME), (FLOPS), (BYTES));                                                 \
+  } while (0)
 
 extern "C" int gcpsl_param_count(const gcpsl_desc *d, int64_t *P, int64_t *P_client) {
   gcpsl_clear_error();
@@ -332,11 +382,14 @@ extern "C" int gcpsl_sample(gcpsl_ctx *ctx, int64_t step, int32_t nsteps, int32_
   if (nsteps < 1 || nsteps > p.max_window) return gcpsl_fail(GCPSL_EINVAL, "nsteps outside [1, max_window]");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   int32_t *idx = ctx->at<int32_t>(p.off_idx);
-  LAUNCH(launch_sample(ctx->at<int32_t>(p.off_ids), ctx->at<int64_t>(p.off_off), ctx->at<int32_t>(p.off_coe),
-                       ctx->desc.labels, idx, ctx->at<int32_t>(p.off_y), ctx->at<int32_t>(p.off_hits), p.C, p.B,
-                       p.K, ctx->desc.seed, step, nsteps, p.max_steps, s));
-  LAUNCH(launch_gather(ctx->desc.images, idx, ctx->ws + p.off_x, p.dtype, (int64_t)nsteps * p.C * p.B,
-                       (int64_t)p.H * p.W * p.Cin, s));
+  const double rows = (double)nsteps * p.C * p.B, row_elems = (double)p.H * p.W * p.Cin;
+  LAUNCH_T("sample", 0.0, rows * 20.0,
+           launch_sample(ctx->at<int32_t>(p.off_ids), ctx->at<int64_t>(p.off_off), ctx->at<int32_t>(p.off_coe),
+                         ctx->desc.labels, idx, ctx->at<int32_t>(p.off_y), ctx->at<int32_t>(p.off_hits), p.C, p.B,
+                         p.K, ctx->desc.seed, step, nsteps, p.max_steps, s));
+  LAUNCH_T(p.dtype == GCPSL_BF16 ? "gather<bf16>" : "gather<f32>", 0.0, rows * (4.0 + row_elems * (4 + p.esz)),
+           launch_gather(ctx->desc.images, idx, ctx->ws + p.off_x, p.dtype, (int64_t)nsteps * p.C * p.B,
+                         (int64_t)p.H * p.W * p.Cin, s));
   if (idx_out)
     HIP_TRY(hipMemcpyAsync(idx_out, idx, sizeof(int32_t) * (size_t)nsteps * p.C * p.B, hipMemcpyDeviceToDevice, s));
   ctx->staged_lo = step;
@@ -364,8 +417,10 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
   for (int i = 0; i < n; ++i) {
     const LayerInfo &l = p.ly[i];
     if (l.spec.kind != GCPSL_CONV3X3) continue;
-    LAUNCH(launch_prep_weights(p.dtype, d.theta, p.P, C, l.w_off, l.Co, l.Ci, ws + l.wf_off, l.Kp,
-                               i > 0 ? ws + l.wd_off : nullptr, l.Kdp, s));
+    const double pb = (double)C * (4.0 * l.nw + p.esz * ((double)l.Co * l.Kp + (i > 0 ? (double)l.Ci * l.Kdp : 0.0)));
+    LAUNCH_T("prep_weights", 0.0, pb,
+             launch_prep_weights(p.dtype, d.theta, p.P, C, l.w_off, l.Co, l.Ci, ws + l.wf_off, l.Kp,
+                                 i > 0 ? ws + l.wd_off : nullptr, l.Kdp, s));
   }
 
   // forward: client segment to the cut, server segment to the loss
@@ -388,25 +443,36 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
       a.bias_rs = p.P;
       a.C = C;
       a.epi = EPI_FWD;
-      LAUNCH(launch_conv(p.dtype, a, s));
+      std::string lab;
+      const double M = (double)B * l.H * l.W;
+      const double fl = 2.0 * C * M * l.Co * 9.0 * l.Ci;
+      const double by = (double)C * (p.esz * (M * l.Ci + (double)l.Co * 9 * l.Ci + M * l.Co * (a.res ? 2 : 1)) + 4.0 * l.Co);
+      size_t t_ = tbegin(ctx, s);
+      LAUNCH(launch_conv(p.dtype, a, s, &lab));
+      tend(ctx, s, t_, lab, fl, by);
     } else if (kind == GCPSL_MAXPOOL2) {
       if (!l.stored) continue;  // fused into the head
-      LAUNCH(launch_maxpool_fwd(p.dtype, input_of(i), ws + l.act_off, C, B, l.H, l.W, l.Ci, s));
+      LAUNCH_T("maxpool_fwd", 0.0, 1.25 * p.esz * (double)C * B * l.H * l.W * l.Ci,
+               launch_maxpool_fwd(p.dtype, input_of(i), ws + l.act_off, C, B, l.H, l.W, l.Ci, s));
     } else if (kind == GCPSL_AVGPOOL) {
       const LayerInfo &hc = p.ly[p.head_conv];
-      LAUNCH(launch_head_pool(p.dtype, ws + hc.act_off, ws + l.act_off, C, B, hc.Ho, hc.Wo, hc.Co,
-                              p.head_maxpool ? 1 : 0, s));
+      LAUNCH_T("head_pool", 0.0, (double)p.esz * C * B * hc.Co * ((double)hc.Ho * hc.Wo + 1),
+               launch_head_pool(p.dtype, ws + hc.act_off, ws + l.act_off, C, B, hc.Ho, hc.Wo, hc.Co,
+                                p.head_maxpool ? 1 : 0, s));
     } else if (kind == GCPSL_LINEAR) {
-      LAUNCH(launch_linear_ce(p.dtype, ws + p.ly[p.avg_idx].act_off, y, d.theta, p.P, l.w_off, l.b_off, grad,
-                              ctx->at<float>(p.off_dh), loss, C, B, l.Ci, l.Co, s));
+      LAUNCH_T("linear_ce", 6.0 * C * B * l.Ci * l.Co,
+               (double)C * (p.esz * B * l.Ci + 4.0 * (2.0 * l.nw + B * l.Ci + B)),
+               launch_linear_ce(p.dtype, ws + p.ly[p.avg_idx].act_off, y, d.theta, p.P, l.w_off, l.b_off, grad,
+                                ctx->at<float>(p.off_dh), loss, C, B, l.Ci, l.Co, s));
     }
   }
 
   // backward: head pooling, then every conv from the top down
   {
     const LayerInfo &hc = p.ly[p.head_conv];
-    LAUNCH(launch_head_pool_bwd(p.dtype, ws + hc.act_off, ctx->at<float>(p.off_dh), ws + hc.gpre_off, C, B,
-                                hc.Ho, hc.Wo, hc.Co, p.head_maxpool ? 1 : 0, s));
+    LAUNCH_T("head_pool_bwd", 0.0, (double)C * B * hc.Co * (2.0 * p.esz * hc.Ho * hc.Wo + 4.0),
+             launch_head_pool_bwd(p.dtype, ws + hc.act_off, ctx->at<float>(p.off_dh), ws + hc.gpre_off, C, B,
+                                  hc.Ho, hc.Wo, hc.Co, p.head_maxpool ? 1 : 0, s));
   }
   int i = p.head_conv;
   while (i >= 0) {
@@ -428,10 +494,19 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
       w.dw = ctx->at<float>(p.off_part); w.dw_rs = l.nw; w.dw_ss = (int64_t)C * l.nw;
       w.db = ctx->at<float>(p.off_dbpart); w.db_rs = l.Co; w.db_ss = (int64_t)C * l.Co;
     }
-    LAUNCH(launch_wgrad(p.dtype, w, s));
+    {
+      std::string lab;
+      const double M = (double)B * l.H * l.W;
+      const double fl = 2.0 * C * M * l.Co * 9.0 * l.Ci;
+      const double by = (double)C * (p.esz * M * (l.Co + l.Ci) + 4.0 * l.splits * (l.nw + l.Co));
+      size_t t_ = tbegin(ctx, s);
+      LAUNCH(launch_wgrad(p.dtype, w, s, &lab));
+      tend(ctx, s, t_, lab, fl, by);
+    }
     if (l.splits > 1)
-      LAUNCH(launch_wgrad_reduce(w.dw, w.db, l.splits, w.dw_ss, w.dw_rs, w.db_ss, w.db_rs, grad, p.P, l.w_off,
-                                 l.b_off, l.nw, l.Co, C, s));
+      LAUNCH_T("wgrad_reduce", 0.0, 4.0 * C * (l.nw + l.Co) * (l.splits + 1.0),
+               launch_wgrad_reduce(w.dw, w.db, l.splits, w.dw_ss, w.dw_rs, w.db_ss, w.db_rs, grad, p.P, l.w_off,
+                                   l.b_off, l.nw, l.Co, C, s));
     if (i == 0) break;
     // input gradient (the cut gradient when layer i-1 is the client's last pool)
     const LayerInfo &prev = p.ly[i - 1];
@@ -450,18 +525,29 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
     a.bias_rs = 0;
     a.C = C;
     a.epi = EPI_DGRAD;
-    LAUNCH(launch_conv(p.dtype, a, s));
+    {
+      std::string lab;
+      const double M = (double)B * l.H * l.W;
+      const double fl = 2.0 * C * M * l.Ci * 9.0 * l.Co;
+      const double by = (double)C * p.esz *
+                        (M * l.Co + (double)l.Ci * 9 * l.Co + M * l.Ci * (1 + (a.res ? 1 : 0) + (a.mask ? 1 : 0)));
+      size_t t_ = tbegin(ctx, s);
+      LAUNCH(launch_conv(p.dtype, a, s, &lab));
+      tend(ctx, s, t_, lab, fl, by);
+    }
     if (through_pool) {
       const LayerInfo &pc = p.ly[i - 2];
-      LAUNCH(launch_maxpool_bwd(p.dtype, ws + pc.act_off, ws + l.gin_off, ws + pc.gpre_off, C, B, pc.Ho, pc.Wo,
-                                pc.Co, s));
+      LAUNCH_T("maxpool_bwd", 0.0, 2.25 * p.esz * (double)C * B * pc.Ho * pc.Wo * pc.Co,
+               launch_maxpool_bwd(p.dtype, ws + pc.act_off, ws + l.gin_off, ws + pc.gpre_off, C, B, pc.Ho, pc.Wo,
+                                  pc.Co, s));
       i -= 2;
     } else {
       i -= 1;
     }
   }
 
-  LAUNCH(launch_sgd(d.theta, d.momentum_buf, grad, (int64_t)C * p.P, d.lr, d.momentum, s));
+  LAUNCH_T("sgd", 3.0 * C * p.P, 20.0 * C * p.P,
+           launch_sgd(d.theta, d.momentum_buf, grad, (int64_t)C * p.P, d.lr, d.momentum, s));
   ctx->horizon = std::max<int64_t>(ctx->horizon, std::min<int64_t>(step + 1, p.max_steps));
   return GCPSL_OK;
 }
@@ -472,7 +558,43 @@ extern "C" int gcpsl_fuse(gcpsl_ctx *ctx, void *stream) {
   const Plan &p = ctx->plan;
   double W = 0.0;
   for (int64_t v : ctx->sizes) W += (double)v;
-  LAUNCH(launch_fuse(ctx->desc.theta, ctx->at<double>(p.off_fw), W, p.C, p.P, reinterpret_cast<hipStream_t>(stream)));
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  LAUNCH_T("fuse", 2.0 * p.C * p.P, 8.0 * p.C * p.P,
+           launch_fuse(ctx->desc.theta, ctx->at<double>(p.off_fw), W, p.C, p.P, s));
+  return GCPSL_OK;
+}
+
+extern "C" int gcpsl_timing(gcpsl_ctx *ctx, int32_t on) {
+  gcpsl_clear_error();
+  if (!ctx) return gcpsl_fail(GCPSL_EINVAL, "null context");
+  ctx->timing = on != 0;
+  return GCPSL_OK;
+}
+
+extern "C" int gcpsl_timing_read(gcpsl_ctx *ctx, gcpsl_kernel_stat *out, int32_t cap, int32_t *n) {
+  gcpsl_clear_error();
+  if (!ctx || !n || (cap > 0 && !out)) return gcpsl_fail(GCPSL_EINVAL, "null argument");
+  HIP_TRY(hipDeviceSynchronize());
+  std::vector<gcpsl_kernel_stat> agg;
+  for (const KernelRec &r : ctx->recs) {
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, ctx->events[r.ev], ctx->events[r.ev + 1]));
+    size_t k = 0;
+    while (k < agg.size() && r.name != agg[k].name) ++k;
+    if (k == agg.size()) {
+      gcpsl_kernel_stat st{};
+      std::snprintf(st.name, sizeof(st.name), "%s", r.name.c_str());
+      agg.push_back(st);
+    }
+    agg[k].launches += 1;
+    agg[k].ms += ms;
+    agg[k].flops += r.flops;
+    agg[k].bytes += r.bytes;
+  }
+  ctx->recs.clear();
+  ctx->next_event = 0;
+  *n = (int32_t)agg.size();
+  for (int32_t k = 0; k < cap && k < (int32_t)agg.size(); ++k) out[k] = agg[k];
   return GCPSL_OK;
 }
 

@@ -78,7 +78,7 @@ template <typename T, int BM, int BN> struct Tile {
 };
 
 // ------------------------------------------------------ forward / dgrad
-template <typename T, int BM, int BN, bool VA>
+template <typename T, int BM, int BN, bool VA, int EPI>
 __global__ void __launch_bounds__(256)
 conv_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
   using E = ElemT<T>;
@@ -200,7 +200,7 @@ conv_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT
   for (int tn = 0; tn < TL::TN; ++tn) {
     const int n = n0 + wn0 + tn * 16 + li;
     const bool nok = n < a.N;
-    const float bias = (a.epi == EPI_FWD && nok) ? a.bias[rep * a.bias_rs + n] : 0.f;
+    const float bias = (EPI == EPI_FWD && nok) ? a.bias[rep * a.bias_rs + n] : 0.f;
 #pragma unroll
     for (int tm = 0; tm < TL::TM; ++tm) {
 #pragma unroll
@@ -209,7 +209,7 @@ conv_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT
         if (m < M && nok) {
           const int64_t o = (int64_t)m * a.N + n;
           float v = acc[tm][tn][r];
-          if (a.epi == EPI_FWD) {
+          if constexpr (EPI == EPI_FWD) {
             v += bias;
             if (res) v += E::to_f(res[o]);
             v = fmaxf(v, 0.f);
@@ -447,59 +447,70 @@ wgrad_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int 
   }
 }
 
+template <typename T> const char *tname() { return sizeof(T) == 2 ? "bf16" : "f32"; }
+
 template <typename T, int BM, int BN, bool VA>
-hipError_t run_conv(const ConvArgs &a, hipStream_t s) {
+hipError_t run_conv(const ConvArgs &a, hipStream_t s, std::string *label) {
   const int M = a.Bt * a.H * a.W;
   const int MT = (M + BM - 1) / BM, NT = (a.N + BN - 1) / BN;
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Csrc);
   const uint32_t blocks = (uint32_t)MT * NT * a.C;
-  hipLaunchKernelGGL((conv_kernel<T, BM, BN, VA>), dim3(blocks), dim3(256), 0, s, a, fw, fh, fc, MT, NT);
+  if (label)
+    *label = std::string(a.epi == EPI_FWD ? "conv_fwd<" : "conv_dgrad<") + tname<T>() + "," +
+             std::to_string(BM) + "x" + std::to_string(BN) + (VA ? ",vec>" : ",gather>");
+  if (a.epi == EPI_FWD)
+    hipLaunchKernelGGL((conv_kernel<T, BM, BN, VA, EPI_FWD>), dim3(blocks), dim3(256), 0, s, a, fw, fh, fc, MT, NT);
+  else
+    hipLaunchKernelGGL((conv_kernel<T, BM, BN, VA, EPI_DGRAD>), dim3(blocks), dim3(256), 0, s, a, fw, fh, fc, MT, NT);
   return hipGetLastError();
 }
 
 template <typename T, bool VA>
-hipError_t pick_conv(const ConvArgs &a, hipStream_t s) {
-  if (a.N > 64) return run_conv<T, 128, 128, VA>(a, s);
-  if (a.N > 32) return run_conv<T, 128, 64, VA>(a, s);
-  return run_conv<T, 128, 32, VA>(a, s);
+hipError_t pick_conv(const ConvArgs &a, hipStream_t s, std::string *label) {
+  if (a.N > 64) return run_conv<T, 128, 128, VA>(a, s, label);
+  if (a.N > 32) return run_conv<T, 128, 64, VA>(a, s, label);
+  return run_conv<T, 128, 32, VA>(a, s, label);
 }
 
 template <typename T, int BM, int BN, bool VB>
-hipError_t run_wgrad(const WgradArgs &a, hipStream_t s) {
+hipError_t run_wgrad(const WgradArgs &a, hipStream_t s, std::string *label) {
   const int MT = (a.Co + BM - 1) / BM, NT = (9 * a.Ci + BN - 1) / BN;
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Ci);
   const uint32_t blocks = (uint32_t)MT * NT * a.splits * a.C;
+  if (label)
+    *label = std::string("conv_wgrad<") + tname<T>() + "," + std::to_string(BM) + "x" + std::to_string(BN) +
+             (VB ? ",vec>" : ",gather>");
   hipLaunchKernelGGL((wgrad_kernel<T, BM, BN, VB>), dim3(blocks), dim3(256), 0, s, a, fw, fh, fc, MT, NT);
   return hipGetLastError();
 }
 
 template <typename T, int BM, bool VB>
-hipError_t pick_wgrad_n(const WgradArgs &a, hipStream_t s) {
+hipError_t pick_wgrad_n(const WgradArgs &a, hipStream_t s, std::string *label) {
   const int NW = 9 * a.Ci;
-  if (NW > 64) return run_wgrad<T, BM, 128, VB>(a, s);
-  if (NW > 32) return run_wgrad<T, BM, 64, VB>(a, s);
-  return run_wgrad<T, BM, 32, VB>(a, s);
+  if (NW > 64) return run_wgrad<T, BM, 128, VB>(a, s, label);
+  if (NW > 32) return run_wgrad<T, BM, 64, VB>(a, s, label);
+  return run_wgrad<T, BM, 32, VB>(a, s, label);
 }
 
 template <typename T, bool VB>
-hipError_t pick_wgrad(const WgradArgs &a, hipStream_t s) {
-  if (a.Co > 64) return pick_wgrad_n<T, 128, VB>(a, s);
-  if (a.Co > 32) return pick_wgrad_n<T, 64, VB>(a, s);
-  return pick_wgrad_n<T, 32, VB>(a, s);
+hipError_t pick_wgrad(const WgradArgs &a, hipStream_t s, std::string *label) {
+  if (a.Co > 64) return pick_wgrad_n<T, 128, VB>(a, s, label);
+  if (a.Co > 32) return pick_wgrad_n<T, 64, VB>(a, s, label);
+  return pick_wgrad_n<T, 32, VB>(a, s, label);
 }
 
 }  // namespace
 
 int wgrad_k_tile(int dtype) { return dtype == GCPSL_BF16 ? 64 : 32; }
 
-hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s) {
+hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s, std::string *label) {
   if (dtype == GCPSL_BF16)
-    return (a.Csrc % 8 == 0) ? pick_conv<bf16_t, true>(a, s) : pick_conv<bf16_t, false>(a, s);
-  return (a.Csrc % 4 == 0) ? pick_conv<float, true>(a, s) : pick_conv<float, false>(a, s);
+    return (a.Csrc % 8 == 0) ? pick_conv<bf16_t, true>(a, s, label) : pick_conv<bf16_t, false>(a, s, label);
+  return (a.Csrc % 4 == 0) ? pick_conv<float, true>(a, s, label) : pick_conv<float, false>(a, s, label);
 }
 
-hipError_t launch_wgrad(int dtype, const WgradArgs &a, hipStream_t s) {
+hipError_t launch_wgrad(int dtype, const WgradArgs &a, hipStream_t s, std::string *label) {
   if (dtype == GCPSL_BF16)
-    return (a.Ci % 8 == 0) ? pick_wgrad<bf16_t, true>(a, s) : pick_wgrad<bf16_t, false>(a, s);
-  return (a.Ci % 4 == 0) ? pick_wgrad<float, true>(a, s) : pick_wgrad<float, false>(a, s);
+    return (a.Ci % 8 == 0) ? pick_wgrad<bf16_t, true>(a, s, label) : pick_wgrad<bf16_t, false>(a, s, label);
+  return (a.Ci % 4 == 0) ? pick_wgrad<float, true>(a, s, label) : pick_wgrad<float, false>(a, s, label);
 }

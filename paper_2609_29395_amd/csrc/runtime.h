@@ -46,8 +46,9 @@ struct WgradArgs {
 };
 
 // ---------------------------------------------------------------- launchers
-hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s);
-hipError_t launch_wgrad(int dtype, const WgradArgs &a, hipStream_t s);
+// label (optional) receives the kernel instantiation chosen for the shape.
+hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s, std::string *label = nullptr);
+hipError_t launch_wgrad(int dtype, const WgradArgs &a, hipStream_t s, std::string *label = nullptr);
 int wgrad_k_tile(int dtype);
 
 hipError_t launch_sample(const int32_t *ids, const int64_t *off, const int32_t *coe,

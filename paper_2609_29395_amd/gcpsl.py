@@ -23,7 +23,8 @@ RESIDUAL = 1
 
 EXPORTS = ["gcpsl_param_count", "gcpsl_workspace_bytes", "gcpsl_assign", "gcpsl_create",
            "gcpsl_sample", "gcpsl_step", "gcpsl_fuse", "gcpsl_participation",
-           "gcpsl_cluster_sizes", "gcpsl_tensor", "gcpsl_destroy", "gcpsl_last_error"]
+           "gcpsl_cluster_sizes", "gcpsl_tensor", "gcpsl_timing", "gcpsl_timing_read",
+           "gcpsl_destroy", "gcpsl_last_error"]
 
 
 class GCPSLError(RuntimeError):
@@ -50,6 +51,11 @@ class Desc(C.Structure):
     ]
 
 
+class KernelStat(C.Structure):
+    _fields_ = [("name", C.c_char * 64), ("launches", C.c_int64), ("ms", C.c_double),
+                ("flops", C.c_double), ("bytes", C.c_double)]
+
+
 _lib = None
 
 
@@ -73,6 +79,8 @@ def lib():
     L.gcpsl_participation.argtypes = [vp, P(i64), P(i64), P(i32)]
     L.gcpsl_cluster_sizes.argtypes = [vp, P(i64)]
     L.gcpsl_tensor.argtypes = [vp, C.c_char_p, P(vp), P(i64), P(i32)]
+    L.gcpsl_timing.argtypes = [vp, i32]
+    L.gcpsl_timing_read.argtypes = [vp, P(KernelStat), i32, P(i32)]
     L.gcpsl_destroy.argtypes = [vp]
     L.gcpsl_destroy.restype = None
     L.gcpsl_last_error.restype = C.c_char_p
@@ -231,6 +239,18 @@ class Context:
         out = np.zeros(self.cfg["C"], dtype=np.int64)
         _check(lib().gcpsl_cluster_sizes(self._h, _i64p(out)))
         return out
+
+    def timing(self, on):
+        _check(lib().gcpsl_timing(self._h, 1 if on else 0))
+
+    def timing_read(self, cap=64):
+        """{kernel: dict(launches, ms, flops, bytes)} of the launches recorded
+        since the last read (synchronises)."""
+        arr = (KernelStat * cap)()
+        n = C.c_int32()
+        _check(lib().gcpsl_timing_read(self._h, arr, cap, C.byref(n)))
+        return {arr[i].name.decode(): dict(launches=arr[i].launches, ms=arr[i].ms, flops=arr[i].flops,
+                                           bytes=arr[i].bytes) for i in range(min(n.value, cap))}
 
     def tensor(self, name):
         """torch view of a named workspace tensor (gcpsl_tensor)."""
