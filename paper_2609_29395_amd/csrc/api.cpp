@@ -138,6 +138,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   if (p.head_conv < 0 || p.ly[p.head_conv].spec.kind != GCPSL_CONV3X3)
     return gcpsl_fail(GCPSL_EUNSUPPORTED, "avgpool must follow a conv or a conv + max pool");
   p.Ch_head = p.ly[p.head_conv].Co;
+  if (linear_ce_lds_bytes(d->B, p.Ch_head, d->L) > kMaxLinearLds)
+    return gcpsl_fail(GCPSL_EUNSUPPORTED, "classifier head too large for one workgroup (B * channels)");
 
   // workspace layout
   const int C = p.C, B = p.B;
@@ -187,11 +189,12 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
       const int M = B * l.H * l.W;
       const int kt = wgrad_k_tile(p.dtype);
       const int nkt = (M + kt - 1) / kt;
-      const int bm = l.Co > 64 ? 128 : (l.Co > 32 ? 64 : 32);
+      int bm, bn;
+      wgrad_tile(p.dtype, l.Co, l.Ci, &bm, &bn);
       const int nwc = 9 * l.Ci;
-      const int bn = nwc > 64 ? 128 : (nwc > 32 ? 64 : 32);
       const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
-      int splits = (int)std::min<int64_t>(std::max(1, nkt / 4), (1024 + tiles - 1) / tiles);
+      const int64_t target = bm * bn >= 256 * 128 ? 512 : 1024;  // workgroups to fill 256 CUs
+      int splits = (int)std::min<int64_t>(std::max(1, nkt / 4), (target + tiles - 1) / tiles);
       splits = std::max(1, splits);
       const int per = (nkt + splits - 1) / splits;
       l.chunk = per * kt;

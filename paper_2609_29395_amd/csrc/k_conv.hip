@@ -53,11 +53,13 @@ template <typename T> struct Pack {
 };
 
 // Shared tile geometry and the MFMA loop over one staged k tile.
-template <typename T, int BM, int BN> struct Tile {
+template <typename T, int BM, int BN, int WM = 2, int WN = 2> struct Tile {
   static constexpr int VEC = ElemT<T>::VEC;
   static constexpr int BK = 128 / (int)sizeof(T);
   static constexpr int LDR = BK + 16 / (int)sizeof(T);
-  static constexpr int TM = BM / 32, TN = BN / 32;
+  static constexpr int NT = 64 * WM * WN;  // threads per workgroup
+  static constexpr int TM = BM / WM / 16, TN = BN / WN / 16;
+  static_assert(TM >= 1 && TN >= 1, "wave tile must hold a 16x16 block");
 
   __device__ static __forceinline__ void compute(f32x4_t (&acc)[TM][TN], const T *As, const T *Bs,
                                                  int wm0, int wn0, int lane) {
@@ -78,13 +80,14 @@ template <typename T, int BM, int BN> struct Tile {
 };
 
 // ------------------------------------------------------ forward / dgrad
-template <typename T, int BM, int BN, bool VA, int EPI>
-__global__ void __launch_bounds__(256)
+template <typename T, int BM, int BN, int WM, int WN, bool VA, int EPI>
+__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(WM * WN >= 8 ? 4 : 2)))
 conv_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
   using E = ElemT<T>;
-  using TL = Tile<T, BM, BN>;
+  using TL = Tile<T, BM, BN, WM, WN>;
   constexpr int VEC = TL::VEC, BK = TL::BK, LDR = TL::LDR;
-  constexpr int AV = BM / 32, BV = BN / 32;
+  constexpr int RP = TL::NT / 8;  // tile rows loaded per pass (8 vectors per row)
+  constexpr int AV = (BM + RP - 1) / RP, BV = (BN + RP - 1) / RP;  // last pass may be partial
   __shared__ __attribute__((aligned(16))) T As[2][BM * LDR];
   __shared__ __attribute__((aligned(16))) T Bs[2][BN * LDR];
 
@@ -104,7 +107,7 @@ conv_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT
   bool aok[AV];
 #pragma unroll
   for (int j = 0; j < AV; ++j) {
-    const int m = m0 + rrow + 32 * j;
+    const int m = m0 + rrow + RP * j;
     aok[j] = m < M;
     const uint32_t mm = aok[j] ? (uint32_t)m : 0u;
     const uint32_t q = fdiv(mm, fd_w);
@@ -113,8 +116,10 @@ conv_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT
     ah[j] = (int)(q - (uint32_t)ab[j] * (uint32_t)a.H);
   }
 
-  uint4 ra[AV], rb[BV];
-  auto load_tiles = [&](int kt) {
+  // Two register sets: tile kt+2 is fetched while tile kt is multiplied, so
+  // each global load has two k tiles of MFMA work to arrive in.
+  uint4 ra0[AV], rb0[BV], ra1[AV], rb1[BV];
+  auto load_tiles = [&](int kt, uint4 (&ra)[AV], uint4 (&rb)[BV]) {
     const int k0 = kt * BK + kv * VEC;
     if constexpr (VA) {
       int r = 0, s = 0, c = 0;
@@ -157,22 +162,24 @@ conv_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT
     }
 #pragma unroll
     for (int j = 0; j < BV; ++j) {
-      const int n = n0 + rrow + 32 * j;
-      rb[j] = n < a.N ? *reinterpret_cast<const uint4 *>(wt + (int64_t)n * a.Kp + k0)
-                      : make_uint4(0, 0, 0, 0);
+      const int n = n0 + rrow + RP * j;
+      rb[j] = (n < a.N && rrow + RP * j < BN) ? *reinterpret_cast<const uint4 *>(wt + (int64_t)n * a.Kp + k0)
+                                               : make_uint4(0, 0, 0, 0);
     }
   };
-  auto store_tiles = [&](int buf) {
+  auto store_tiles = [&](int buf, const uint4 (&ra)[AV], const uint4 (&rb)[BV]) {
 #pragma unroll
     for (int j = 0; j < AV; ++j)
-      *reinterpret_cast<uint4 *>(&As[buf][(rrow + 32 * j) * LDR + kv * VEC]) = ra[j];
+      if (BM % RP == 0 || rrow + RP * j < BM)
+        *reinterpret_cast<uint4 *>(&As[buf][(rrow + RP * j) * LDR + kv * VEC]) = ra[j];
 #pragma unroll
     for (int j = 0; j < BV; ++j)
-      *reinterpret_cast<uint4 *>(&Bs[buf][(rrow + 32 * j) * LDR + kv * VEC]) = rb[j];
+      if (BN % RP == 0 || rrow + RP * j < BN)
+        *reinterpret_cast<uint4 *>(&Bs[buf][(rrow + RP * j) * LDR + kv * VEC]) = rb[j];
   };
 
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm0 = (wave >> 1) * (BM / 2), wn0 = (wave & 1) * (BN / 2);
+  const int wm0 = (wave / WN) * (BM / WM), wn0 = (wave % WN) * (BN / WN);
   f32x4_t acc[TL::TM][TL::TN];
 #pragma unroll
   for (int i = 0; i < TL::TM; ++i)
@@ -180,15 +187,21 @@ conv_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT
     for (int j = 0; j < TL::TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int nk = a.Kp / BK;
-  load_tiles(0);
-  store_tiles(0);
+  load_tiles(0, ra0, rb0);
+  if (nk > 1) load_tiles(1, ra1, rb1);
+  store_tiles(0, ra0, rb0);
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load_tiles(kt + 1);
-    TL::compute(acc, As[buf], Bs[buf], wm0, wn0, lane);
-    if (kt + 1 < nk) store_tiles(buf ^ 1);
+  for (int kt = 0; kt < nk; kt += 2) {
+    if (kt + 2 < nk) load_tiles(kt + 2, ra0, rb0);
+    TL::compute(acc, As[0], Bs[0], wm0, wn0, lane);
+    if (kt + 1 < nk) store_tiles(1, ra1, rb1);
     __syncthreads();
+    if (kt + 1 < nk) {
+      if (kt + 3 < nk) load_tiles(kt + 3, ra1, rb1);
+      TL::compute(acc, As[1], Bs[1], wm0, wn0, lane);
+      if (kt + 2 < nk) store_tiles(0, ra0, rb0);
+      __syncthreads();
+    }
   }
 
   // epilogue
@@ -259,15 +272,16 @@ __device__ __forceinline__ void transpose_block<float>(const uint4 (&in)[4], uin
   out[3] = make_uint4(in[0].w, in[1].w, in[2].w, in[3].w);
 }
 
-template <typename T, int BM, int BN, bool VB>
-__global__ void __launch_bounds__(256)
+template <typename T, int BM, int BN, int WM, int WN, bool VB>
+__global__ void __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(WM * WN >= 8 ? 4 : 2)))
 wgrad_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
-  using TL = Tile<T, BM, BN>;
+  using TL = Tile<T, BM, BN, WM, WN>;
   constexpr int VEC = TL::VEC, BK = TL::BK, LDR = TL::LDR;
+  constexpr int NTH = TL::NT;
   constexpr int PB = BK / VEC;  // pixel blocks per k tile
   constexpr int NA = (BM / VEC) * PB, NB = (BN / VEC) * PB;
-  constexpr int ITER = (NA + NB + 255) / 256;
-  static_assert(NA <= 256, "A blocks must fit one pass");
+  constexpr int ITER = (NA + NB + NTH - 1) / NTH;
+  static_assert(NA <= NTH, "A blocks must fit one pass");
   __shared__ __attribute__((aligned(16))) T As[2][BM * LDR];
   __shared__ __attribute__((aligned(16))) T Bs[2][BN * LDR];
   __shared__ float red[PB][BM];
@@ -296,7 +310,7 @@ wgrad_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int 
   bool bvalid[ITER];
 #pragma unroll
   for (int it = 0; it < ITER; ++it) {
-    const int i = tid + 256 * it;
+    const int i = tid + NTH * it;
     if (i < NA) {
       kind[it] = 0;
       rowb[it] = i / PB;
@@ -324,12 +338,15 @@ wgrad_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int 
     }
   }
 
-  uint4 reg[ITER][VEC];
+  // DEPTH register sets of prefetched blocks (tile kt + DEPTH is in flight
+  // while tile kt is multiplied).
+  constexpr int DEPTH = WM * WN >= 8 ? 1 : 2;
+  uint4 reg0[ITER][VEC], reg1[DEPTH == 2 ? ITER : 1][VEC];
   float bsum[VEC];
 #pragma unroll
   for (int q = 0; q < VEC; ++q) bsum[q] = 0.f;
 
-  auto load_tiles = [&](int kt) {
+  auto load_tiles = [&](int kt, auto &reg) {
 #pragma unroll
     for (int it = 0; it < ITER; ++it) {
       const int pbase = p_begin + kt * BK + pb[it] * VEC;
@@ -373,7 +390,7 @@ wgrad_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int 
       }
     }
   };
-  auto store_tiles = [&](int buf) {
+  auto store_tiles = [&](int buf, auto &reg) {
 #pragma unroll
     for (int it = 0; it < ITER; ++it) {
       if (kind[it] == 2) continue;
@@ -395,24 +412,45 @@ wgrad_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int 
   };
 
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm0 = (wave >> 1) * (BM / 2), wn0 = (wave & 1) * (BN / 2);
+  const int wm0 = (wave / WN) * (BM / WM), wn0 = (wave % WN) * (BN / WN);
   f32x4_t acc[TL::TM][TL::TN];
 #pragma unroll
   for (int i = 0; i < TL::TM; ++i)
 #pragma unroll
     for (int j = 0; j < TL::TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  if (nk > 0) {
-    load_tiles(0);
-    store_tiles(0);
-  }
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load_tiles(kt + 1);
-    TL::compute(acc, As[buf], Bs[buf], wm0, wn0, lane);
-    if (kt + 1 < nk) store_tiles(buf ^ 1);
+  if constexpr (DEPTH == 2) {
+    if (nk > 0) {
+      load_tiles(0, reg0);
+      if (nk > 1) load_tiles(1, reg1);
+      store_tiles(0, reg0);
+    }
     __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+      if (kt + 2 < nk) load_tiles(kt + 2, reg0);
+      TL::compute(acc, As[0], Bs[0], wm0, wn0, lane);
+      if (kt + 1 < nk) store_tiles(1, reg1);
+      __syncthreads();
+      if (kt + 1 < nk) {
+        if (kt + 3 < nk) load_tiles(kt + 3, reg1);
+        TL::compute(acc, As[1], Bs[1], wm0, wn0, lane);
+        if (kt + 2 < nk) store_tiles(0, reg0);
+        __syncthreads();
+      }
+    }
+  } else {
+    if (nk > 0) {
+      load_tiles(0, reg0);
+      store_tiles(0, reg0);
+    }
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      const int buf = kt & 1;
+      if (kt + 1 < nk) load_tiles(kt + 1, reg0);
+      TL::compute(acc, As[buf], Bs[buf], wm0, wn0, lane);
+      if (kt + 1 < nk) store_tiles(buf ^ 1, reg0);
+      __syncthreads();
+    }
   }
 
   const int li = lane & 15, lg = lane >> 4;
@@ -449,7 +487,7 @@ wgrad_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int 
 
 template <typename T> const char *tname() { return sizeof(T) == 2 ? "bf16" : "f32"; }
 
-template <typename T, int BM, int BN, bool VA>
+template <typename T, int BM, int BN, bool VA, int WM = 2, int WN = 2>
 hipError_t run_conv(const ConvArgs &a, hipStream_t s, std::string *label) {
   const int M = a.Bt * a.H * a.W;
   const int MT = (M + BM - 1) / BM, NT = (a.N + BN - 1) / BN;
@@ -457,36 +495,50 @@ hipError_t run_conv(const ConvArgs &a, hipStream_t s, std::string *label) {
   const uint32_t blocks = (uint32_t)MT * NT * a.C;
   if (label)
     *label = std::string(a.epi == EPI_FWD ? "conv_fwd<" : "conv_dgrad<") + tname<T>() + "," +
-             std::to_string(BM) + "x" + std::to_string(BN) + (VA ? ",vec>" : ",gather>");
+             std::to_string(BM) + "x" + std::to_string(BN) + ",w" + std::to_string(WM * WN) +
+             (VA ? ",vec>" : ",gather>");
+  const dim3 threads(64 * WM * WN);
   if (a.epi == EPI_FWD)
-    hipLaunchKernelGGL((conv_kernel<T, BM, BN, VA, EPI_FWD>), dim3(blocks), dim3(256), 0, s, a, fw, fh, fc, MT, NT);
+    hipLaunchKernelGGL((conv_kernel<T, BM, BN, WM, WN, VA, EPI_FWD>), dim3(blocks), threads, 0, s, a, fw, fh, fc, MT, NT);
   else
-    hipLaunchKernelGGL((conv_kernel<T, BM, BN, VA, EPI_DGRAD>), dim3(blocks), dim3(256), 0, s, a, fw, fh, fc, MT, NT);
+    hipLaunchKernelGGL((conv_kernel<T, BM, BN, WM, WN, VA, EPI_DGRAD>), dim3(blocks), threads, 0, s, a, fw, fh, fc, MT, NT);
   return hipGetLastError();
 }
 
 template <typename T, bool VA>
 hipError_t pick_conv(const ConvArgs &a, hipStream_t s, std::string *label) {
-  if (a.N > 64) return run_conv<T, 128, 128, VA>(a, s, label);
-  if (a.N > 32) return run_conv<T, 128, 64, VA>(a, s, label);
-  return run_conv<T, 128, 32, VA>(a, s, label);
+  // 16-bit tiles run 8 waves (4 per SIMD at two workgroups per CU): the extra
+  // resident waves hide LDS and global latency better than larger wave tiles.
+  if constexpr (sizeof(T) == 2) {
+    if (a.N > 64) return run_conv<T, 128, 128, VA, 4, 2>(a, s, label);
+    if (a.N > 32) return run_conv<T, 128, 64, VA, 4, 2>(a, s, label);
+    return run_conv<T, 128, 32, VA, 4, 2>(a, s, label);
+  } else {
+    if (a.N > 64) return run_conv<T, 128, 128, VA>(a, s, label);
+    if (a.N > 32) return run_conv<T, 128, 64, VA>(a, s, label);
+    return run_conv<T, 128, 32, VA>(a, s, label);
+  }
 }
 
-template <typename T, int BM, int BN, bool VB>
+template <typename T, int BM, int BN, bool VB, int WM = 2, int WN = 2>
 hipError_t run_wgrad(const WgradArgs &a, hipStream_t s, std::string *label) {
   const int MT = (a.Co + BM - 1) / BM, NT = (9 * a.Ci + BN - 1) / BN;
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Ci);
   const uint32_t blocks = (uint32_t)MT * NT * a.splits * a.C;
   if (label)
     *label = std::string("conv_wgrad<") + tname<T>() + "," + std::to_string(BM) + "x" + std::to_string(BN) +
-             (VB ? ",vec>" : ",gather>");
-  hipLaunchKernelGGL((wgrad_kernel<T, BM, BN, VB>), dim3(blocks), dim3(256), 0, s, a, fw, fh, fc, MT, NT);
+             ",w" + std::to_string(WM * WN) + (VB ? ",vec>" : ",gather>");
+  hipLaunchKernelGGL((wgrad_kernel<T, BM, BN, WM, WN, VB>), dim3(blocks), dim3(64 * WM * WN), 0, s, a, fw, fh, fc,
+                     MT, NT);
   return hipGetLastError();
 }
 
 template <typename T, int BM, bool VB>
 hipError_t pick_wgrad_n(const WgradArgs &a, hipStream_t s, std::string *label) {
   const int NW = 9 * a.Ci;
+  if constexpr (sizeof(T) == 2 && BM == 128) {
+    if (NW > 64) return run_wgrad<T, BM, 128, VB, 2, 4>(a, s, label);
+  }
   if (NW > 64) return run_wgrad<T, BM, 128, VB>(a, s, label);
   if (NW > 32) return run_wgrad<T, BM, 64, VB>(a, s, label);
   return run_wgrad<T, BM, 32, VB>(a, s, label);
@@ -494,14 +546,22 @@ hipError_t pick_wgrad_n(const WgradArgs &a, hipStream_t s, std::string *label) {
 
 template <typename T, bool VB>
 hipError_t pick_wgrad(const WgradArgs &a, hipStream_t s, std::string *label) {
-  if (a.Co > 64) return pick_wgrad_n<T, 128, VB>(a, s, label);
-  if (a.Co > 32) return pick_wgrad_n<T, 64, VB>(a, s, label);
+  int bm, bn;
+  wgrad_tile(sizeof(T) == 2 ? GCPSL_BF16 : GCPSL_F32, a.Co, a.Ci, &bm, &bn);
+  if (bm == 128) return pick_wgrad_n<T, 128, VB>(a, s, label);
+  if (bm == 64) return pick_wgrad_n<T, 64, VB>(a, s, label);
   return pick_wgrad_n<T, 32, VB>(a, s, label);
 }
 
 }  // namespace
 
 int wgrad_k_tile(int dtype) { return dtype == GCPSL_BF16 ? 64 : 32; }
+
+void wgrad_tile(int dtype, int Co, int Ci, int *bm, int *bn) {
+  const int nw = 9 * Ci;
+  *bm = Co > 64 ? 128 : (Co > 32 ? 64 : 32);
+  *bn = nw > 64 ? 128 : (nw > 32 ? 64 : 32);
+}
 
 hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s, std::string *label) {
   if (dtype == GCPSL_BF16)

@@ -75,29 +75,52 @@ gather_kernel(const float *__restrict__ images, const int32_t *__restrict__ idx,
 //   wf[co][k], k = (r, s, ci) < 9 ci, rows zero-padded to Kp (forward);
 //   wd[ci][kk], kk = (r', s', co), wd[ci][(r', s', co)] = W[co][2-r'][2-s'][ci]
 //   rows zero-padded to Kdp (input gradient as a forward conv).
+// wf is a row copy; wd is a transpose of 64 x 64 (co, ci) blocks per kernel
+// tap, staged through LDS so both the reads and the writes are coalesced.
 template <typename T>
 __global__ void __launch_bounds__(256)
-prep_kernel(const float *__restrict__ theta, int64_t P, int64_t w_off, int co, int ci,
-            T *__restrict__ wf, int Kp, T *__restrict__ wd, int Kdp) {
+prep_wf_kernel(const float *__restrict__ theta, int64_t P, int64_t w_off, int co, int ci,
+               T *__restrict__ wf, int Kp) {
   const int rep = blockIdx.y;
   const float *w = theta + rep * P + w_off;
-  const int K = 9 * ci, Kd = 9 * co;
-  const int64_t nf = (int64_t)co * Kp, nd = wd ? (int64_t)ci * Kdp : 0;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nf + nd;
+  const int K = 9 * ci;
+  const int64_t nf = (int64_t)co * Kp;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nf;
        i += (int64_t)gridDim.x * blockDim.x) {
-    if (i < nf) {
-      const int n = (int)(i / Kp), k = (int)(i % Kp);
-      wf[rep * nf + i] = ElemT<T>::from_f(k < K ? w[(int64_t)n * K + k] : 0.f);
-    } else {
-      const int64_t i2 = i - nf;
-      const int c = (int)(i2 / Kdp), kk = (int)(i2 % Kdp);
-      float v = 0.f;
-      if (kk < Kd) {
-        const int rs = kk / co, o = kk % co;
-        const int r = rs / 3, s = rs % 3;
-        v = w[(int64_t)o * K + ((2 - r) * 3 + (2 - s)) * ci + c];
-      }
-      wd[rep * nd + i2] = ElemT<T>::from_f(v);
+    const int n = (int)(i / Kp), k = (int)(i % Kp);
+    wf[rep * nf + i] = ElemT<T>::from_f(k < K ? w[(int64_t)n * K + k] : 0.f);
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+prep_wd_kernel(const float *__restrict__ theta, int64_t P, int64_t w_off, int co, int ci,
+               T *__restrict__ wd, int Kdp) {
+  __shared__ float tile[64][65];
+  const int rep = blockIdx.z;
+  const int tap = blockIdx.y;  // (r', s') of the flipped kernel
+  const int nco = (co + 63) / 64;
+  const int cb = blockIdx.x % nco, ib = blockIdx.x / nco;
+  const int rs_src = 8 - tap;  // (2 - r') * 3 + (2 - s')
+  const float *w = theta + rep * P + w_off;
+  const int K = 9 * ci;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int r = ty; r < 64; r += 4) {
+    const int o = cb * 64 + r, c = ib * 64 + tx;
+    tile[r][tx] = (o < co && c < ci) ? w[(int64_t)o * K + rs_src * ci + c] : 0.f;
+  }
+  __syncthreads();
+  T *dst = wd + (int64_t)rep * ci * Kdp;
+  for (int r = ty; r < 64; r += 4) {
+    const int c = ib * 64 + r, o = cb * 64 + tx;
+    if (c < ci && o < co) dst[(int64_t)c * Kdp + tap * co + o] = ElemT<T>::from_f(tile[tx][r]);
+  }
+  // zero the row padding once per row (by the first tap/co block)
+  if (tap == 0 && cb == 0) {
+    for (int r = ty; r < 64; r += 4) {
+      const int c = ib * 64 + r;
+      if (c >= ci) continue;
+      for (int k = 9 * co + tx; k < Kdp; k += 64) dst[(int64_t)c * Kdp + k] = T(0);
     }
   }
 }
@@ -200,29 +223,36 @@ head_pool_kernel(const T *__restrict__ a, T *__restrict__ h, int64_t total, int 
 // Linear layer and mean softmax cross-entropy for one replica per workgroup:
 // logits = h W^T + b, loss = mean_b (logsumexp - logit_y),
 // dlogits = (softmax - onehot) / B, dW = dlogits^T h, db = sum_b dlogits,
-// dh = dlogits W.  bf16 workloads use the bf16-rounded weight matrix.
+// dh = dlogits W.  bf16 workloads use the bf16-rounded weight matrix.  The
+// pooled features, the weights and the logits are staged in LDS so every
+// global access is coalesced; each sum runs in a fixed order.
 template <typename T>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(1024)
 linear_ce_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
                  const float *__restrict__ theta, int64_t P, int64_t w_off, int64_t b_off,
                  float *__restrict__ grad, float *__restrict__ dh, float *__restrict__ loss, int Bt,
                  int Ch, int L) {
   extern __shared__ float sh[];
-  float *lg = sh;              // [Bt][L] logits, then dlogits
-  float *lossb = sh + Bt * L;  // [Bt]
-  const int rep = blockIdx.x, tid = threadIdx.x;
+  float *hs = sh;                      // [Bt][Ch]
+  float *ws = hs + (int64_t)Bt * Ch;   // [L][Ch]
+  float *lg = ws + (int64_t)L * Ch;    // [Bt][L] logits, then dlogits
+  float *lossb = lg + Bt * L;          // [Bt]
+  const int rep = blockIdx.x, tid = threadIdx.x, nt = blockDim.x;
   const T *hr = h + (int64_t)rep * Bt * Ch;
   const float *Wl = theta + rep * P + w_off;
   const float *bl = theta + rep * P + b_off;
-  auto wv = [&](int j, int c) { return ElemT<T>::to_f(ElemT<T>::from_f(Wl[(int64_t)j * Ch + c])); };
-  for (int i = tid; i < Bt * L; i += blockDim.x) {
+  for (int i = tid; i < Bt * Ch; i += nt) hs[i] = ElemT<T>::to_f(hr[i]);
+  for (int i = tid; i < L * Ch; i += nt) ws[i] = ElemT<T>::to_f(ElemT<T>::from_f(Wl[i]));
+  __syncthreads();
+  for (int i = tid; i < Bt * L; i += nt) {
     const int b = i / L, j = i % L;
+    const float *hb = hs + (int64_t)b * Ch, *wj = ws + (int64_t)j * Ch;
     float s = bl[j];
-    for (int c = 0; c < Ch; ++c) s += ElemT<T>::to_f(hr[(int64_t)b * Ch + c]) * wv(j, c);
+    for (int c = 0; c < Ch; ++c) s += hb[c] * wj[c];
     lg[i] = s;
   }
   __syncthreads();
-  for (int b = tid; b < Bt; b += blockDim.x) {
+  for (int b = tid; b < Bt; b += nt) {
     float m = lg[b * L];
     for (int j = 1; j < L; ++j) m = fmaxf(m, lg[b * L + j]);
     float s = 0.f;
@@ -242,22 +272,22 @@ linear_ce_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
     loss[rep] = s / (float)Bt;
   }
   float *g = grad + rep * P;
-  for (int i = tid; i < L * Ch; i += blockDim.x) {
+  for (int i = tid; i < L * Ch; i += nt) {
     const int j = i / Ch, c = i % Ch;
     float s = 0.f;
-    for (int b = 0; b < Bt; ++b) s += lg[b * L + j] * ElemT<T>::to_f(hr[(int64_t)b * Ch + c]);
+    for (int b = 0; b < Bt; ++b) s += lg[b * L + j] * hs[(int64_t)b * Ch + c];
     g[w_off + i] = s;
   }
-  for (int j = tid; j < L; j += blockDim.x) {
+  for (int j = tid; j < L; j += nt) {
     float s = 0.f;
     for (int b = 0; b < Bt; ++b) s += lg[b * L + j];
     g[b_off + j] = s;
   }
   float *dhr = dh + (int64_t)rep * Bt * Ch;
-  for (int i = tid; i < Bt * Ch; i += blockDim.x) {
+  for (int i = tid; i < Bt * Ch; i += nt) {
     const int b = i / Ch, c = i % Ch;
     float s = 0.f;
-    for (int j = 0; j < L; ++j) s += lg[b * L + j] * wv(j, c);
+    for (int j = 0; j < L; ++j) s += lg[b * L + j] * ws[(int64_t)j * Ch + c];
     dhr[i] = s;
   }
 }
@@ -389,14 +419,21 @@ hipError_t launch_gather(const float *images, const int32_t *idx, void *x, int d
 
 hipError_t launch_prep_weights(int dtype, const float *theta, int64_t P, int C, int64_t w_off,
                                int co, int ci, void *wf, int Kp, void *wd, int Kdp, hipStream_t s) {
-  const int64_t n = (int64_t)co * Kp + (wd ? (int64_t)ci * Kdp : 0);
-  const dim3 grid(grid_for(n, 256, 4096), C);
-  if (dtype == GCPSL_BF16)
-    hipLaunchKernelGGL(prep_kernel<bf16_t>, grid, dim3(256), 0, s, theta, P, w_off, co, ci,
-                       (bf16_t *)wf, Kp, (bf16_t *)wd, Kdp);
-  else
-    hipLaunchKernelGGL(prep_kernel<float>, grid, dim3(256), 0, s, theta, P, w_off, co, ci,
-                       (float *)wf, Kp, (float *)wd, Kdp);
+  const dim3 grid(grid_for((int64_t)co * Kp, 256, 4096), C);
+  const dim3 gridd(((co + 63) / 64) * ((ci + 63) / 64), 9, C);
+  if (dtype == GCPSL_BF16) {
+    hipLaunchKernelGGL(prep_wf_kernel<bf16_t>, grid, dim3(256), 0, s, theta, P, w_off, co, ci,
+                       (bf16_t *)wf, Kp);
+    if (wd)
+      hipLaunchKernelGGL(prep_wd_kernel<bf16_t>, gridd, dim3(256), 0, s, theta, P, w_off, co, ci,
+                         (bf16_t *)wd, Kdp);
+  } else {
+    hipLaunchKernelGGL(prep_wf_kernel<float>, grid, dim3(256), 0, s, theta, P, w_off, co, ci,
+                       (float *)wf, Kp);
+    if (wd)
+      hipLaunchKernelGGL(prep_wd_kernel<float>, gridd, dim3(256), 0, s, theta, P, w_off, co, ci,
+                         (float *)wd, Kdp);
+  }
   return hipGetLastError();
 }
 
@@ -439,12 +476,21 @@ hipError_t launch_head_pool(int dtype, const void *a, void *h, int C, int Bt, in
 hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const float *theta, int64_t P,
                             int64_t w_off, int64_t b_off, float *grad, float *dh, float *loss, int C,
                             int Bt, int Ch, int L, hipStream_t s) {
-  const size_t shm = sizeof(float) * ((size_t)Bt * L + Bt);
+  const size_t shm = linear_ce_lds_bytes(Bt, Ch, L);
+  if (shm > kMaxLinearLds) return hipErrorInvalidValue;
+  if (shm > 64 * 1024) {
+    const hipError_t e = dtype == GCPSL_BF16
+        ? hipFuncSetAttribute(reinterpret_cast<const void *>(linear_ce_kernel<bf16_t>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm)
+        : hipFuncSetAttribute(reinterpret_cast<const void *>(linear_ce_kernel<float>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    if (e != hipSuccess) return e;
+  }
   if (dtype == GCPSL_BF16)
-    hipLaunchKernelGGL(linear_ce_kernel<bf16_t>, dim3(C), dim3(256), shm, s, (const bf16_t *)h, y,
+    hipLaunchKernelGGL(linear_ce_kernel<bf16_t>, dim3(C), dim3(1024), shm, s, (const bf16_t *)h, y,
                        theta, P, w_off, b_off, grad, dh, loss, Bt, Ch, L);
   else
-    hipLaunchKernelGGL(linear_ce_kernel<float>, dim3(C), dim3(256), shm, s, (const float *)h, y,
+    hipLaunchKernelGGL(linear_ce_kernel<float>, dim3(C), dim3(1024), shm, s, (const float *)h, y,
                        theta, P, w_off, b_off, grad, dh, loss, Bt, Ch, L);
   return hipGetLastError();
 }

@@ -50,6 +50,9 @@ struct WgradArgs {
 hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s, std::string *label = nullptr);
 hipError_t launch_wgrad(int dtype, const WgradArgs &a, hipStream_t s, std::string *label = nullptr);
 int wgrad_k_tile(int dtype);
+// Workgroup tile (rows = output channels, cols = 9 * input channels) the
+// weight-gradient launcher uses for a layer; the split-K plan depends on it.
+void wgrad_tile(int dtype, int Co, int Ci, int *bm, int *bn);
 
 hipError_t launch_sample(const int32_t *ids, const int64_t *off, const int32_t *coe,
                          const int32_t *labels, int32_t *idx, int32_t *y, int32_t *hits,
@@ -66,6 +69,11 @@ hipError_t launch_maxpool_bwd(int dtype, const void *a, const void *gz, void *gp
                               int Bt, int H, int W, int Ch, hipStream_t s);
 hipError_t launch_head_pool(int dtype, const void *a, void *h, int C, int Bt, int H, int W,
                             int Ch, int maxpool, hipStream_t s);
+// LDS the classifier-head kernel stages (pooled features, weights, logits).
+constexpr size_t kMaxLinearLds = 160 * 1024;
+inline size_t linear_ce_lds_bytes(int Bt, int Ch, int L) {
+  return sizeof(float) * ((size_t)Bt * Ch + (size_t)L * Ch + (size_t)Bt * L + Bt);
+}
 hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const float *theta,
                             int64_t P, int64_t w_off, int64_t b_off, float *grad, float *dh,
                             float *loss, int C, int Bt, int Ch, int L, hipStream_t s);
