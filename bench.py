@@ -18,7 +18,6 @@ fraction.  The CPU oracle is timed on a bounded sample on the host cores.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -42,23 +41,16 @@ DESCRIPTIONS = {
 }
 
 
-def kernel_source_hash():
-    h = hashlib.sha256()
-    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2609_29395_amd", "csrc"))):
-        with open(os.path.join(ROOT, "paper_2609_29395_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
-
-
 def load_traffic(workload, kernel):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
     None when it is absent or the kernels changed since it was taken."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
+    from paper_2609_29395_amd.profile_summary import source_hash
     with open(path) as fh:
         rec = json.load(fh)
-    if rec.get("source_hash") != kernel_source_hash():
+    if rec.get("source_hash") != source_hash():
         return None
     entry = rec.get("kernels", {}).get(f"{workload}:{kernel}")
     return None if entry is None else entry.get("bytes_per_launch")

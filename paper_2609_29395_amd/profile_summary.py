@@ -1,0 +1,127 @@
+"""Summaries of rocprofv3 output for the kernels of this library.
+
+  python -m paper_2609_29395_amd.profile_summary copy [--mib N] [--reps R]
+      Run a plain device copy of a known size (the calibration kernel for the
+      FETCH_SIZE / WRITE_SIZE counters).
+  python -m paper_2609_29395_amd.profile_summary stats TRACE_DIR OUT.md CMD...
+      Write a Markdown summary of `rocprofv3 --kernel-trace --stats` CSV output.
+  python -m paper_2609_29395_amd.profile_summary traffic FETCH_DIR WRITE_DIR COPY_FETCH_DIR COPY_WRITE_DIR WORKLOAD OUT.json
+      Combine two counter runs of the workload (FETCH_SIZE, then WRITE_SIZE)
+      into HBM bytes per launch for every kernel, each counter scaled by what
+      it reads for the copy of known size (runs COPY_FETCH_DIR, COPY_WRITE_DIR).
+"""
+from __future__ import annotations
+
+import collections
+import csv
+import glob
+import hashlib
+import json
+import os
+import re
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+COPY_MIB = 256
+
+
+def kernel_label(name: str) -> str:
+    """rocprof's demangled name -> the label gcpsl_timing reports."""
+    m = re.search(r"conv_kernel<(unsigned short|float), (\d+), (\d+), (\d+), (\d+), (true|false), (\d)>", name)
+    if m:
+        t = "bf16" if m.group(1) == "unsigned short" else "f32"
+        kind = "conv_fwd" if m.group(7) == "0" else "conv_dgrad"
+        w = int(m.group(4)) * int(m.group(5))
+        return f"{kind}<{t},{m.group(2)}x{m.group(3)},w{w},{'vec' if m.group(6) == 'true' else 'gather'}>"
+    m = re.search(r"wgrad_kernel<(unsigned short|float), (\d+), (\d+), (\d+), (\d+), (true|false)>", name)
+    if m:
+        t = "bf16" if m.group(1) == "unsigned short" else "f32"
+        w = int(m.group(4)) * int(m.group(5))
+        return f"conv_wgrad<{t},{m.group(2)}x{m.group(3)},w{w},{'vec' if m.group(6) == 'true' else 'gather'}>"
+    m = re.search(r"::(\w+?)(_kernel)?[<(]", name)
+    return m.group(1) if m else name
+
+
+def source_hash():
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2609_29395_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        with open(os.path.join(d, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def copy(mib=COPY_MIB, reps=5):
+    import torch
+    n = mib * 1024 * 1024 // 4
+    a = torch.ones(n, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(f"copied {mib} MiB x {reps}")
+
+
+def _one(pattern):
+    files = glob.glob(pattern, recursive=True)
+    if not files:
+        raise FileNotFoundError(pattern)
+    return files[0]
+
+
+def stats(trace_dir, out_md, cmd):
+    rows = list(csv.DictReader(open(_one(os.path.join(trace_dir, "**", "*kernel_stats.csv")))))
+    total = sum(float(r["TotalDurationNs"]) for r in rows)
+    lines = [f"# Kernel time summary", "", f"Command: `{' '.join(cmd)}`", "",
+             "| kernel (label) | calls | total ms | avg us | % |", "|---|---|---|---|---|"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        lines.append(f"| {kernel_label(r['Name'])} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.3f} | "
+                     f"{float(r['AverageNs']) / 1e3:.2f} | {100 * float(r['TotalDurationNs']) / total:.2f} |")
+    lines += ["", f"Sum of kernel time: {total / 1e6:.3f} ms", ""]
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
+
+
+def _counter_per_dispatch(d, counter):
+    rows = list(csv.DictReader(open(_one(os.path.join(d, "**", "*counter_collection.csv")))))
+    per = collections.defaultdict(list)
+    for r in rows:
+        if r["Counter_Name"] == counter:
+            per[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+    return per
+
+
+def traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload, out_json):
+    fetch = _counter_per_dispatch(fetch_dir, "FETCH_SIZE")
+    write = _counter_per_dispatch(write_dir, "WRITE_SIZE")
+    expect_kib = COPY_MIB * 1024.0
+    samples = lambda per: [v for vs in per.values() for v in vs if v > 0.25 * expect_kib]
+    cf = samples(_counter_per_dispatch(copy_fetch_dir, "FETCH_SIZE"))
+    cw = samples(_counter_per_dispatch(copy_write_dir, "WRITE_SIZE"))
+    f_fac = (sum(cf) / len(cf)) / expect_kib if cf else 1.0
+    w_fac = (sum(cw) / len(cw)) / expect_kib if cw else 1.0
+    out = {"source_hash": source_hash(), "copy_mib": COPY_MIB, "fetch_factor": f_fac,
+           "write_factor": w_fac, "kernels": {}}
+    for k in set(fetch) | set(write):
+        fv, wv = fetch.get(k, []), write.get(k, [])
+        fk = sum(fv) / len(fv) if fv else 0.0
+        wk = sum(wv) / len(wv) if wv else 0.0
+        out["kernels"][f"{workload}:{kernel_label(k)}"] = {
+            "launches": max(len(fv), len(wv)), "fetch_kib": fk, "write_kib": wk,
+            "bytes_per_launch": 1024.0 * (fk / f_fac + wk / w_fac)}
+    with open(out_json, "w") as fh:
+        json.dump(out, fh, indent=1, sort_keys=True)
+    print(json.dumps(out, indent=1, sort_keys=True))
+
+
+if __name__ == "__main__":
+    what = sys.argv[1]
+    if what == "copy":
+        copy()
+    elif what == "stats":
+        stats(sys.argv[2], sys.argv[3], sys.argv[4:])
+    elif what == "traffic":
+        traffic(*sys.argv[2:8])
+    else:
+        raise SystemExit(__doc__)
