@@ -174,6 +174,11 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
     }
     if (kind == GCPSL_CONV3X3) {
       const int64_t rs = (int64_t)B * l.H * l.W;
+      // kernels address one replica's tensors with 32-bit byte offsets and
+      // mark invalid lanes with offset 2^31
+      if ((int64_t)p.esz * rs * std::max(l.Ci, l.Co) >= (1ll << 31) ||
+          (int64_t)p.esz * std::max(l.Co, l.Ci) * (9 * (int64_t)std::max(l.Ci, l.Co) + 64) >= (1ll << 31))
+        return gcpsl_fail(GCPSL_EUNSUPPORTED, "per-replica layer tensors must stay below 2 GiB");
       l.gpre_off = take((size_t)p.esz * C * rs * l.Co);
       if (i > 0 && p.ly[i - 1].spec.kind == GCPSL_MAXPOOL2) {
         l.has_gin = true;
