@@ -201,7 +201,11 @@ int gcpsl_cluster_sizes(gcpsl_ctx *ctx, int64_t *sizes);
 
 /*
  * Device view of a named workspace tensor, for inspection by tests.  Names:
- * "x" (staged inputs [max_window][C][B][H][W][Cin]), "idx", "y"
+ * "x" (staged inputs [max_window][C][B][H][W][Cx]; Cx = Cin when Cin is a
+ * multiple of 8 (bf16) / 4 (fp32), otherwise the image layer's im2col rows:
+ * Cx = 9 Cin rounded up to that multiple, column (r, s, c) = pixel
+ * (h + r - 1, w + s - 1) channel c, zero outside the image and in the padding),
+ * "idx", "y"
  * ([max_window][C][B] int32), "hits" ([max_steps][C] int32, |A_{n,t}| of
  * every sampled step), "act<i>" (output of layer i, [C][B][...]),
  * "gpre<i>" (gradient w.r.t. conv layer i's pre-activation), "gin<i>"

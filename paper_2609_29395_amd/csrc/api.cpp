@@ -50,7 +50,11 @@ struct Plan {
   int head_conv = -1, avg_idx = -1, lin_idx = -1;
   bool head_maxpool = false;
   int Ch_head = 0;
-  int64_t x_rs = 0;  // elements of one staged step: C * B * H * W * Cin
+  // The image layer's input is staged as im2col rows when its channel count
+  // is not a whole number of 16-byte vectors: Kc columns per pixel.
+  bool col0 = false;
+  int Kc = 0;
+  int64_t x_rs = 0;  // elements of one staged step: C * B * H * W * (Kc or Cin)
   size_t off_ids = 0, off_off = 0, off_coe = 0, off_fw = 0, off_hits = 0, off_idx = 0, off_y = 0,
          off_x = 0, off_dh = 0, off_grad = 0, off_part = 0, off_dbpart = 0, off_loss = 0;
   size_t total = 0;
@@ -157,7 +161,12 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   p.off_hits = take(sizeof(int32_t) * p.max_steps * C);
   p.off_idx = take(sizeof(int32_t) * (size_t)p.max_window * C * B);
   p.off_y = take(sizeof(int32_t) * (size_t)p.max_window * C * B);
-  p.x_rs = (int64_t)C * B * p.H * p.W * p.Cin;
+  {
+    const int vec = 16 / p.esz;
+    p.col0 = p.Cin % vec != 0;
+    p.Kc = p.col0 ? round_up(9 * p.Cin, vec) : p.Cin;
+  }
+  p.x_rs = (int64_t)C * B * p.H * p.W * p.Kc;
   p.off_x = take((size_t)p.esz * p.max_window * p.x_rs);
   size_t part = 0, dbpart = 0;
   for (int i = 0; i < n; ++i) {
@@ -195,8 +204,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
       const int kt = wgrad_k_tile(p.dtype);
       const int nkt = (M + kt - 1) / kt;
       int bm, bn;
-      wgrad_tile(p.dtype, l.Co, l.Ci, &bm, &bn);
-      const int nwc = 9 * l.Ci;
+      const int nwc = (i == 0 && p.col0) ? p.Kc : 9 * l.Ci;
+      wgrad_tile(p.dtype, l.Co, nwc, &bm, &bn);
       const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
       const int64_t target = bm * bn >= 256 * 128 ? 512 : 1024;  // workgroups to fill 256 CUs
       int splits = (int)std::min<int64_t>(std::max(1, nkt / 4), (target + tiles - 1) / tiles);
@@ -395,9 +404,15 @@ extern "C" int gcpsl_sample(gcpsl_ctx *ctx, int64_t step, int32_t nsteps, int32_
            launch_sample(ctx->at<int32_t>(p.off_ids), ctx->at<int64_t>(p.off_off), ctx->at<int32_t>(p.off_coe),
                          ctx->desc.labels, idx, ctx->at<int32_t>(p.off_y), ctx->at<int32_t>(p.off_hits), p.C, p.B,
                          p.K, ctx->desc.seed, step, nsteps, p.max_steps, s));
-  LAUNCH_T(p.dtype == GCPSL_BF16 ? "gather<bf16>" : "gather<f32>", 0.0, rows * (4.0 + row_elems * (4 + p.esz)),
-           launch_gather(ctx->desc.images, idx, ctx->ws + p.off_x, p.dtype, (int64_t)nsteps * p.C * p.B,
-                         (int64_t)p.H * p.W * p.Cin, s));
+  if (p.col0)
+    LAUNCH_T(p.dtype == GCPSL_BF16 ? "gather_im2col<bf16>" : "gather_im2col<f32>", 0.0,
+             rows * (4.0 + row_elems * 4 + (double)p.H * p.W * p.Kc * p.esz),
+             launch_gather_im2col(ctx->desc.images, idx, ctx->ws + p.off_x, p.dtype, (int64_t)nsteps * p.C * p.B,
+                                  p.H, p.W, p.Cin, p.Kc, s));
+  else
+    LAUNCH_T(p.dtype == GCPSL_BF16 ? "gather<bf16>" : "gather<f32>", 0.0, rows * (4.0 + row_elems * (4 + p.esz)),
+             launch_gather(ctx->desc.images, idx, ctx->ws + p.off_x, p.dtype, (int64_t)nsteps * p.C * p.B,
+                           (int64_t)p.H * p.W * p.Cin, s));
   if (idx_out)
     HIP_TRY(hipMemcpyAsync(idx_out, idx, sizeof(int32_t) * (size_t)nsteps * p.C * p.B, hipMemcpyDeviceToDevice, s));
   ctx->staged_lo = step;
@@ -444,8 +459,12 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
       a.bias = d.theta + l.b_off;
       a.res = (l.spec.flags & GCPSL_RESIDUAL) ? a.src : nullptr;
       a.mask = nullptr;
-      a.Bt = B; a.H = l.H; a.W = l.W; a.Csrc = l.Ci; a.N = l.Co; a.K = 9 * l.Ci; a.Kp = l.Kp;
-      a.src_rs = (int64_t)B * l.H * l.W * l.Ci;
+      const bool col = i == 0 && p.col0;
+      a.Bt = B; a.H = l.H; a.W = l.W; a.N = l.Co; a.Kp = l.Kp;
+      a.Csrc = col ? p.Kc : l.Ci;
+      a.K = col ? p.Kc : 9 * l.Ci;
+      a.taps = col ? 1 : 9;
+      a.src_rs = (int64_t)B * l.H * l.W * a.Csrc;
       a.wt_rs = (int64_t)l.Co * l.Kp;
       a.out_rs = l.act_rs;
       a.bias_rs = p.P;
@@ -489,9 +508,13 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
     WgradArgs w{};
     w.g = ws + l.gpre_off;
     w.x = input_of(i);
-    w.Bt = B; w.H = l.H; w.W = l.W; w.Ci = l.Ci; w.Co = l.Co;
+    const bool col = i == 0 && p.col0;
+    w.Bt = B; w.H = l.H; w.W = l.W; w.Co = l.Co;
+    w.Ci = col ? p.Kc : l.Ci;
+    w.taps = col ? 1 : 9;
+    w.nw = 9 * l.Ci;
     w.g_rs = (int64_t)B * l.H * l.W * l.Co;
-    w.x_rs = (int64_t)B * l.H * l.W * l.Ci;
+    w.x_rs = (int64_t)B * l.H * l.W * w.Ci;
     w.C = C;
     w.splits = l.splits;
     w.chunk = l.chunk;
@@ -533,6 +556,7 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
     a.bias_rs = 0;
     a.C = C;
     a.epi = EPI_DGRAD;
+    a.taps = 9;
     {
       std::string lab;
       const double M = (double)B * l.H * l.W;

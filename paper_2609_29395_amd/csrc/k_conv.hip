@@ -189,9 +189,10 @@ conv_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT
   auto load_tiles = [&](int kt, uint4 (&ra)[AV], uint4 (&rb)[BV]) {
     const int k0 = kt * BK + kv * VEC;
     if constexpr (VA) {
-      // tap (r, s) and channel of this thread's 16-byte vector
-      const int rs = (int)fdiv((uint32_t)k0, fd_c);
-      const int c = k0 - rs * a.Csrc;
+      // tap (r, s) and channel of this thread's 16-byte vector (im2col rows:
+      // the centre tap, channel k0)
+      const int rs = a.taps == 1 ? 4 : (int)fdiv((uint32_t)k0, fd_c);
+      const int c = k0 - (a.taps == 1 ? 0 : rs * a.Csrc);
       const int r = (rs * 11) >> 5;  // rs / 3 for rs < 9
       const int tap = ((r - 1) * a.W + (rs - 3 * r - 1)) * a.Csrc + c;
       const uint32_t live = k0 < a.K ? 1u : 0u;
@@ -396,7 +397,7 @@ wgrad_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int 
   const int split = __builtin_amdgcn_readfirstlane((int)(rest % (uint32_t)a.splits));
   const int rep = __builtin_amdgcn_readfirstlane((int)(rest / (uint32_t)a.splits));
   const int M = a.Bt * a.H * a.W;
-  const int NW = 9 * a.Ci;
+  const int NW = a.taps == 1 ? a.Ci : 9 * a.Ci;  // columns of the (padded) im2col operand
   const int p_begin = split * a.chunk;
   const int p_end = min(M, p_begin + a.chunk);
   const int nk = (p_end - p_begin + BK - 1) / BK;
@@ -430,8 +431,8 @@ wgrad_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int 
       const int kk0 = n0 + rowb[it] * VEC;
       bvalid[it] = kk0 < NW;
       if (VB && bvalid[it]) {
-        const int rs = (int)fdiv((uint32_t)kk0, fd_c);
-        bc[it] = kk0 - rs * a.Ci;
+        const int rs = a.taps == 1 ? 4 : (int)fdiv((uint32_t)kk0, fd_c);
+        bc[it] = kk0 - (a.taps == 1 ? 0 : rs * a.Ci);
         br[it] = (rs * 11) >> 5;
         bs[it] = rs - 3 * br[it];
       }
@@ -465,7 +466,12 @@ wgrad_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int 
         continue;
       }
       if constexpr (VB) {
-        if (kind[it] == 1) {
+        if (kind[it] == 1 && a.taps == 1) {
+          // im2col rows: contiguous pixels, like the gradient operand
+          const uint32_t o0 = bvalid[it] ? ((uint32_t)pbase * (uint32_t)a.Ci + (uint32_t)bc[it]) * ESZ : kOob;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) reg[it][e] = buffer_load16(rsx, o0 + (uint32_t)(e * a.Ci) * ESZ, 0);
+        } else if (kind[it] == 1) {
           const uint32_t q1 = fdiv((uint32_t)pbase, fd_w);
           const int w0 = (int)((uint32_t)pbase - q1 * (uint32_t)a.W);
           const int b = (int)fdiv(q1, fd_h);
@@ -586,7 +592,7 @@ wgrad_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int 
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = m0 + wm0 + tm * 16 + lg * 4 + r;
-        if (m < a.Co && n < NW) dw[(int64_t)m * NW + n] = acc[tm][tn][r];
+        if (m < a.Co && n < a.nw) dw[(int64_t)m * a.nw + n] = acc[tm][tn][r];
       }
   }
 
@@ -647,7 +653,7 @@ hipError_t pick_conv(const ConvArgs &a, hipStream_t s, std::string *label) {
 
 template <typename T, int BM, int BN, bool VB, int WM = 2, int WN = 2>
 hipError_t run_wgrad(const WgradArgs &a, hipStream_t s, std::string *label) {
-  const int MT = (a.Co + BM - 1) / BM, NT = (9 * a.Ci + BN - 1) / BN;
+  const int MT = (a.Co + BM - 1) / BM, NT = ((a.taps == 1 ? a.Ci : 9 * a.Ci) + BN - 1) / BN;
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Ci);
   const uint32_t blocks = (uint32_t)MT * NT * a.splits * a.C;
   if (label)
@@ -660,7 +666,7 @@ hipError_t run_wgrad(const WgradArgs &a, hipStream_t s, std::string *label) {
 
 template <typename T, int BM, bool VB>
 hipError_t pick_wgrad_n(const WgradArgs &a, hipStream_t s, std::string *label) {
-  const int NW = 9 * a.Ci;
+  const int NW = a.taps == 1 ? a.Ci : 9 * a.Ci;
   if constexpr (sizeof(T) == 2 && BM == 128) {
     if (NW > 64) return run_wgrad<T, BM, 128, VB, 2, 4>(a, s, label);
   }
@@ -672,7 +678,7 @@ hipError_t pick_wgrad_n(const WgradArgs &a, hipStream_t s, std::string *label) {
 template <typename T, bool VB>
 hipError_t pick_wgrad(const WgradArgs &a, hipStream_t s, std::string *label) {
   int bm, bn;
-  wgrad_tile(sizeof(T) == 2 ? GCPSL_BF16 : GCPSL_F32, a.Co, a.Ci, &bm, &bn);
+  wgrad_tile(sizeof(T) == 2 ? GCPSL_BF16 : GCPSL_F32, a.Co, a.taps == 1 ? a.Ci : 9 * a.Ci, &bm, &bn);
   if (bm == 128) return pick_wgrad_n<T, 128, VB>(a, s, label);
   if (bm == 64) return pick_wgrad_n<T, 64, VB>(a, s, label);
   return pick_wgrad_n<T, 32, VB>(a, s, label);
@@ -682,8 +688,8 @@ hipError_t pick_wgrad(const WgradArgs &a, hipStream_t s, std::string *label) {
 
 int wgrad_k_tile(int dtype) { return dtype == GCPSL_BF16 ? 64 : 32; }
 
-void wgrad_tile(int dtype, int Co, int Ci, int *bm, int *bn) {
-  const int nw = 9 * Ci;
+void wgrad_tile(int dtype, int Co, int ncols, int *bm, int *bn) {
+  const int nw = ncols;
   *bm = Co > 64 ? 128 : (Co > 32 ? 64 : 32);
   *bn = nw > 64 ? 128 : (nw > 32 ? 64 : 32);
 }
@@ -695,10 +701,11 @@ hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s, std::string 
 }
 
 hipError_t launch_wgrad(int dtype, const WgradArgs &a, hipStream_t s, std::string *label) {
-  // vector path: whole 16-byte channel vectors and pixel blocks within one image row
+  // vector path: whole 16-byte channel vectors and pixel blocks within one
+  // image row (im2col rows need no image-row structure)
   if (dtype == GCPSL_BF16)
-    return (a.Ci % 8 == 0 && a.W % 8 == 0) ? pick_wgrad<bf16_t, true>(a, s, label)
-                                           : pick_wgrad<bf16_t, false>(a, s, label);
-  return (a.Ci % 4 == 0 && a.W % 4 == 0) ? pick_wgrad<float, true>(a, s, label)
-                                         : pick_wgrad<float, false>(a, s, label);
+    return (a.Ci % 8 == 0 && (a.taps == 1 || a.W % 8 == 0)) ? pick_wgrad<bf16_t, true>(a, s, label)
+                                                            : pick_wgrad<bf16_t, false>(a, s, label);
+  return (a.Ci % 4 == 0 && (a.taps == 1 || a.W % 4 == 0)) ? pick_wgrad<float, true>(a, s, label)
+                                                          : pick_wgrad<float, false>(a, s, label);
 }

@@ -70,6 +70,46 @@ gather_kernel(const float *__restrict__ images, const int32_t *__restrict__ idx,
   }
 }
 
+// Gather for a first layer with few channels: each staged pixel holds its
+// 3x3 neighbourhood (k = (r, s, c), zero outside the image and beyond 9 Cin
+// up to Kc), so that layer runs as a plain GEMM with K = Kc.  The image is
+// staged in LDS when it fits.
+template <typename T>
+__global__ void __launch_bounds__(256)
+gather_im2col_kernel(const float *__restrict__ images, const int32_t *__restrict__ idx,
+                     T *__restrict__ x, int H, int W, int Cin, int Kc, int use_lds) {
+  extern __shared__ float img[];
+  constexpr int VEC = ElemT<T>::VEC;
+  const int64_t row = blockIdx.x;
+  const int64_t n = (int64_t)H * W * Cin;
+  const float *src = images + (int64_t)idx[row] * n;
+  if (use_lds) {
+    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) img[i] = src[i];
+    __syncthreads();
+  }
+  const float *from = use_lds ? img : src;
+  T *dst = x + row * (int64_t)H * W * Kc;
+  const int K9 = 9 * Cin;
+  for (int p = threadIdx.x; p < H * W; p += blockDim.x) {
+    const int h = p / W, w = p % W;
+    for (int k0 = 0; k0 < Kc; k0 += VEC) {
+      struct { T v[VEC]; } pk;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const int k = k0 + e;
+        float v = 0.f;
+        if (k < K9) {
+          const int rs = k / Cin, c = k - rs * Cin;
+          const int hh = h + rs / 3 - 1, ww = w + rs % 3 - 1;
+          if ((unsigned)hh < (unsigned)H && (unsigned)ww < (unsigned)W) v = from[(hh * W + ww) * Cin + c];
+        }
+        pk.v[e] = ElemT<T>::from_f(v);
+      }
+      *reinterpret_cast<uint4 *>(dst + (int64_t)p * Kc + k0) = __builtin_bit_cast(uint4, pk);
+    }
+  }
+}
+
 // ------------------------------------------------------ weight preparation
 // Compute copies of one conv layer's weights from the fp32 masters:
 //   wf[co][k], k = (r, s, ci) < 9 ci, rows zero-padded to Kp (forward);
@@ -414,6 +454,20 @@ hipError_t launch_gather(const float *images, const int32_t *idx, void *x, int d
   else
     hipLaunchKernelGGL(gather_kernel<float>, dim3((unsigned)rows), dim3(256), 0, s, images, idx,
                        (float *)x, row_elems);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_im2col(const float *images, const int32_t *idx, void *x, int dtype, int64_t rows,
+                                int H, int W, int Cin, int Kc, hipStream_t s) {
+  const size_t img = sizeof(float) * (size_t)H * W * Cin;
+  const int use_lds = img <= 64 * 1024 ? 1 : 0;
+  const size_t shm = use_lds ? img : 0;
+  if (dtype == GCPSL_BF16)
+    hipLaunchKernelGGL(gather_im2col_kernel<bf16_t>, dim3((unsigned)rows), dim3(256), shm, s, images, idx,
+                       (bf16_t *)x, H, W, Cin, Kc, use_lds);
+  else
+    hipLaunchKernelGGL(gather_im2col_kernel<float>, dim3((unsigned)rows), dim3(256), shm, s, images, idx,
+                       (float *)x, H, W, Cin, Kc, use_lds);
   return hipGetLastError();
 }
 

@@ -31,6 +31,7 @@ struct ConvArgs {
   int64_t src_rs, wt_rs, out_rs, bias_rs;  // per-replica strides (elements)
   int C;
   int epi;
+  int taps;  // 9: 3x3 implicit GEMM; 1: src already holds im2col rows, A[m][k] = src[m][k]
 };
 
 // Weight gradient: dW[co][kk] = sum_p G[p][co] X(p, kk), kk = (r, s, ci),
@@ -43,6 +44,8 @@ struct WgradArgs {
   int Bt, H, W, Ci, Co;
   int64_t g_rs, x_rs, dw_rs, dw_ss, db_rs, db_ss;
   int C, splits, chunk;  // pixel chunk per split (multiple of the k tile)
+  int taps;  // 9: x is the layer input; 1: x holds im2col rows of Ci columns
+  int nw;    // weight-gradient row length written (9 * input channels)
 };
 
 // ---------------------------------------------------------------- launchers
@@ -52,7 +55,7 @@ hipError_t launch_wgrad(int dtype, const WgradArgs &a, hipStream_t s, std::strin
 int wgrad_k_tile(int dtype);
 // Workgroup tile (rows = output channels, cols = 9 * input channels) the
 // weight-gradient launcher uses for a layer; the split-K plan depends on it.
-void wgrad_tile(int dtype, int Co, int Ci, int *bm, int *bn);
+void wgrad_tile(int dtype, int Co, int ncols, int *bm, int *bn);
 
 hipError_t launch_sample(const int32_t *ids, const int64_t *off, const int32_t *coe,
                          const int32_t *labels, int32_t *idx, int32_t *y, int32_t *hits,
@@ -60,6 +63,9 @@ hipError_t launch_sample(const int32_t *ids, const int64_t *off, const int32_t *
                          int64_t max_steps, hipStream_t s);
 hipError_t launch_gather(const float *images, const int32_t *idx, void *x, int dtype,
                          int64_t rows, int64_t row_elems, hipStream_t s);
+// Gather with im2col: x[row][pixel][k], k = (r, s, c) < 9 Cin, zero to Kc.
+hipError_t launch_gather_im2col(const float *images, const int32_t *idx, void *x, int dtype,
+                                int64_t rows, int H, int W, int Cin, int Kc, hipStream_t s);
 hipError_t launch_prep_weights(int dtype, const float *theta, int64_t P, int C, int64_t w_off,
                                int co, int ci, void *wf, int Kp, void *wd, int Kdp,
                                hipStream_t s);

@@ -11,7 +11,7 @@ import pytest
 import torch
 
 from gcpsl_inputs import client_stats, get_config, init_params, make_dataset
-from oracle.model import round_bf16, split_forward_backward
+from oracle.model import im2col3x3, round_bf16, split_forward_backward
 from oracle.sampler import active_clients, batch_indices, cluster_examples
 from oracle.train import GCPSLOracle, fuse as oracle_fuse
 
@@ -60,7 +60,10 @@ def test_sample_and_gather_bit_exact(name, window, starts):
         torch.cuda.synchronize()
         got = out.cpu().numpy()
         ys = _np(ctx.tensor("y")).reshape(-1, C, B)
-        xs = _np(ctx.tensor("x")).reshape(-1, C, B, cfg["H"], cfg["W"], cfg["Cin"])
+        H, W, Cin = cfg["H"], cfg["W"], cfg["Cin"]
+        vec = 8 if cfg["dtype"] == "bf16" else 4
+        kc = Cin if Cin % vec == 0 else -(-9 * Cin // vec) * vec
+        xs = _np(ctx.tensor("x")).reshape(-1, C, B, H, W, kc)
         for j in range(window):
             for n in range(C):
                 want = batch_indices(ids[n], B, cfg["seed"], n, s0 + j)
@@ -69,6 +72,9 @@ def test_sample_and_gather_bit_exact(name, window, starts):
                 ref = images[want].astype(np.float64)
                 if cfg["dtype"] == "bf16":
                     ref = round_bf16(ref)
+                if kc != Cin:  # staged as im2col rows of the image layer
+                    ref = np.concatenate([im2col3x3(ref).reshape(B, H, W, 9 * Cin),
+                                          np.zeros((B, H, W, kc - 9 * Cin))], axis=3)
                 assert np.array_equal(xs[j, n].astype(np.float64), ref)
     # per-step |A_{n,t}| of every sampled step
     hits = _np(ctx.tensor("hits")).reshape(-1, C)
