@@ -27,12 +27,15 @@ COPY_MIB = 256
 
 def kernel_label(name: str) -> str:
     """rocprof's demangled name -> the label gcpsl_timing reports."""
-    m = re.search(r"conv_kernel<(unsigned short|float), (\d+), (\d+), (\d+), (\d+), (true|false), (\d)>", name)
+    m = re.search(r"conv_kernel<(unsigned short|float), (\d+), (\d+), (\d+), (\d+), (true|false), (\d), "
+                  r"(\d+), (\d+), (\d+)>", name)
     if m:
         t = "bf16" if m.group(1) == "unsigned short" else "f32"
         kind = "conv_fwd" if m.group(7) == "0" else "conv_dgrad"
         w = int(m.group(4)) * int(m.group(5))
-        return f"{kind}<{t},{m.group(2)}x{m.group(3)},w{w},{'vec' if m.group(6) == 'true' else 'gather'}>"
+        k = int(m.group(9)) // (2 if t == "bf16" else 4)
+        return (f"{kind}<{t},{m.group(2)}x{m.group(3)}x{k},w{w},"
+                f"{'vec' if m.group(6) == 'true' else 'gather'}>")
     m = re.search(r"wgrad_kernel<(unsigned short|float), (\d+), (\d+), (\d+), (\d+), (true|false)>", name)
     if m:
         t = "bf16" if m.group(1) == "unsigned short" else "f32"
