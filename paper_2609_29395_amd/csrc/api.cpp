@@ -205,11 +205,28 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
       const int nkt = (M + kt - 1) / kt;
       int bm, bn;
       const int nwc = (i == 0 && p.col0) ? p.Kc : 9 * l.Ci;
-      wgrad_tile(p.dtype, l.Co, nwc, &bm, &bn);
-      const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
-      const int64_t target = bm * bn >= 256 * 128 ? 512 : 1024;  // workgroups to fill 256 CUs
-      int splits = (int)std::min<int64_t>(std::max(1, nkt / 4), (target + tiles - 1) / tiles);
-      splits = std::max(1, splits);
+      int splits;
+      if (wgrad_lds_ok(p.dtype, l.Co, (i == 0 && p.col0) ? p.Kc : l.Ci)) {
+        // one 8-wave workgroup per CU: pick the split count that minimises
+        // (rounds of 256 workgroups) x (k tiles per workgroup + the cost of
+        // writing and re-reading a partial tile, about 16 k tiles)
+        int bk;
+        wgrad_lds_tile(&bm, &bn, &bk);
+        const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
+        int64_t best = -1;
+        splits = 1;
+        for (int sp = 1; sp <= std::min(16, nkt); ++sp) {
+          const int64_t rounds = (tiles * sp + 255) / 256;
+          const int64_t cost = rounds * ((nkt + sp - 1) / sp + (sp > 1 ? 16 : 0));
+          if (best < 0 || cost < best) best = cost, splits = sp;
+        }
+      } else {
+        wgrad_tile(p.dtype, l.Co, nwc, &bm, &bn);
+        const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
+        const int64_t target = bm * bn >= 256 * 128 ? 512 : 1024;  // workgroups to fill 256 CUs
+        splits = (int)std::min<int64_t>(std::max(1, nkt / 4), (target + tiles - 1) / tiles);
+        splits = std::max(1, splits);
+      }
       const int per = (nkt + splits - 1) / splits;
       l.chunk = per * kt;
       l.splits = (M + l.chunk - 1) / l.chunk;

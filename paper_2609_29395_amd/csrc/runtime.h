@@ -53,6 +53,11 @@ struct WgradArgs {
 hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s, std::string *label = nullptr);
 hipError_t launch_wgrad(int dtype, const WgradArgs &a, hipStream_t s, std::string *label = nullptr);
 int wgrad_k_tile(int dtype);
+// bf16 weight gradient with LDS-direct tile copies and transposing LDS reads
+// (k_wgrad_lds.hip): usable when wgrad_lds_ok; needs chunk % 64 == 0.
+bool wgrad_lds_ok(int dtype, int Co, int Ci);
+void wgrad_lds_tile(int *bm, int *bn, int *bk);
+hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *label);
 // Workgroup tile (rows = output channels, cols = 9 * input channels) the
 // weight-gradient launcher uses for a layer; the split-K plan depends on it.
 void wgrad_tile(int dtype, int Co, int ncols, int *bm, int *bn);
