@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OBJDIR = os.path.join(os.path.dirname(HERE), "_build", "gcpsl")
 LIB = os.path.join(HERE, "libgcpsl.so")
-SOURCES = ["api.cpp", "assign.cpp", "k_conv.hip", "k_misc.hip", "k_wgrad_lds.hip"]
+SOURCES = ["api.cpp", "assign.cpp", "k_conv.hip", "k_misc.hip", "k_wgrad_lds.hip", "k_conv_lds.hip"]
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
@@ -42,7 +42,7 @@ def _compile(src: str) -> str:
 def build(verbose: bool = False) -> str:
     """Compile every HIP/C++ source for gfx950 and link libgcpsl.so."""
     os.makedirs(OBJDIR, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(5, len(SOURCES))) as ex:
+    with cf.ThreadPoolExecutor(max_workers=min(6, len(SOURCES))) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
     cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]

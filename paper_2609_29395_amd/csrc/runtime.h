@@ -58,6 +58,9 @@ int wgrad_k_tile(int dtype);
 bool wgrad_lds_ok(int dtype, int Co, int Ci);
 void wgrad_lds_tile(int *bm, int *bn, int *bk);
 hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *label);
+// bf16 forward / dgrad with LDS-direct tile copies (k_conv_lds.hip).
+bool conv_lds_ok(int dtype, const ConvArgs &a);
+hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label);
 // Workgroup tile (rows = output channels, cols = 9 * input channels) the
 // weight-gradient launcher uses for a layer; the split-K plan depends on it.
 void wgrad_tile(int dtype, int Co, int ncols, int *bm, int *bn);
