@@ -12,8 +12,9 @@
 // zero through the buffer range check.  Rows are XOR-swizzled in 16-byte
 // chunks (chunk ^ ((row >> 1) & 7)) so that the 16 rows of one fragment read
 // hit all banks.  Three LDS stages rotate; the fragment reads are inline asm
-// with their own lgkmcnt wait so the compiler does not wait for every
-// outstanding copy.
+// with explicit lgkmcnt waits so the compiler does not wait for every
+// outstanding copy, and the k loop is software-pipelined so that MFMAs
+// cover the LDS latency across the per-tile barrier.
 //
 // The MFMA takes weight fragments as its A operand and pixel fragments as B,
 // so each lane accumulates 4 consecutive output channels of one pixel.  The
@@ -69,13 +70,13 @@ __device__ __forceinline__ void read4(u32x4 (&f)[4], uint32_t addr) {
       : "v"(addr));
 }
 
-// One k group (32 values): weight fragments at wa, pixel fragments at xa.
-__device__ __forceinline__ void kgroup(f32x4_t (&acc)[4][4], uint32_t xa, uint32_t wa) {
-  u32x4 x[4], w[4];
-  read4(x, xa);
-  read4(w, wa);
+__device__ __forceinline__ void wait_lds(u32x4 (&x)[4], u32x4 (&w)[4]) {
   asm volatile("s_waitcnt lgkmcnt(0)"
                : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3]));
+}
+
+// The 16 MFMAs of one k group (32 values): weight fragments w, pixel fragments x.
+__device__ __forceinline__ void mfma_group(f32x4_t (&acc)[4][4], const u32x4 (&x)[4], const u32x4 (&w)[4]) {
 #pragma unroll
   for (int tm = 0; tm < 4; ++tm)
 #pragma unroll
@@ -142,7 +143,7 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   }
 
   // Tile kt >= nk is never multiplied; its copies only keep the count of
-  // copies in flight uniform (their stage is free by then).
+  // copies in flight uniform (their stage is free by then: no reads follow).
   const int nk = a.Kp / BK;
   char *stage0 = smem + wave * 1024;
   auto issue = [&](int kt) {
@@ -189,15 +190,37 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
 #pragma unroll
     for (int k = 0; k < 4; ++k) acc[i][k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // Software pipeline over k tiles (R0/R1: fragments of k groups 0/1):
+  //   wait R0; read R1; MFMA R0; wait R1       -- this tile's reads are done
+  //   wait own copies of tile kt+1; barrier    -- kt+1 visible, stage kt free
+  //   copy tile kt+3 into stage kt; read R0 of tile kt+1; MFMA R1
+  // so the last 16 MFMAs of a tile cover the next tile's first LDS reads.
   issue(0);
   issue(1);
+  issue(2);
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * (SA + SB)) : "memory");
+  asm volatile("s_barrier" ::: "memory");
+  u32x4 x0[4], w0[4], x1[4], w1[4];
+  read4(x0, lds0 + xa[0]);
+  read4(w0, lds0 + wa[0]);
   for (int kt = 0; kt < nk; ++kt) {
+    const uint32_t st = lds0 + (uint32_t)((kt % NS) * STAGE);
+    wait_lds(x0, w0);
+    read4(x1, st + xa[1]);
+    read4(w1, st + wa[1]);
+    mfma_group(acc, x0, w0);
+    wait_lds(x1, w1);
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(SA + SB) : "memory");
     asm volatile("s_barrier" ::: "memory");
-    issue(kt + 2);
-    const uint32_t st = lds0 + (uint32_t)((kt % NS) * STAGE);
-    kgroup(acc, st + xa[0], st + wa[0]);
-    kgroup(acc, st + xa[1], st + wa[1]);
+    __builtin_amdgcn_sched_barrier(0);
+    issue(kt + 3);
+    if (kt + 1 < nk) {
+      const uint32_t sn = lds0 + (uint32_t)(((kt + 1) % NS) * STAGE);
+      read4(x0, sn + xa[0]);
+      read4(w0, sn + wa[0]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_group(acc, x1, w1);
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();

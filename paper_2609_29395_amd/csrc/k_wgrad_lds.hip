@@ -16,10 +16,13 @@
 //
 // LDS rows are XOR-swizzled in 16-byte chunks (chunk ^ swz(row)) so that the
 // 16 pixels of one transposing read fall on all banks.  Three LDS stages
-// rotate: tile kt+2 is in flight while tile kt is multiplied; each wave waits
-// for its own copies (vmcnt), a barrier publishes them.  The LDS reads are
-// inline asm so that the compiler does not add a wait for every outstanding
-// copy before them; each read group ends with its own lgkmcnt wait.
+// rotate: while tile kt is multiplied the copies of the next two tiles are in
+// flight, and tile kt's stage is refilled once every wave has read it.  Each
+// wave waits for its own copies (vmcnt), a barrier publishes them.  The LDS
+// reads are
+// inline asm with explicit lgkmcnt waits so that the compiler does not add a
+// wait for every outstanding copy before them, and the k loop is
+// software-pipelined so that MFMAs cover the LDS latency across the barrier.
 //
 // Workgroup: 8 waves, 128 (co) x 256 (columns) outputs, 64 x 64 per wave.
 // The bias gradient rides along in the column-tile-0 workgroups: every wave
@@ -72,21 +75,26 @@ __device__ __forceinline__ void mma(f32x4_t &acc, const u32x4 &a, const u32x4 &b
                                                 acc, 0, 0, 0);
 }
 
-// k group G (32 pixels) of the stage at byte address sa (A) / sa + A_BYTES (B).
+// Fragments of k group G (32 pixels) of the stage at byte address sa: g (A
+// operand) and x (B operand); the reads stay in flight until wait_lds.
 template <int G>
-__device__ __forceinline__ void kgroup(f32x4_t (&acc)[4][4], f32x4_t &bacc, const uint32_t (&ra)[4],
-                                       const uint32_t (&rb)[4], uint32_t sa, bool bias, int wn) {
-  u32x4 a[4], b[4];
-  read_frag<G * 32 * ROWA, ROWA>(a[0], sa + ra[0]);
-  read_frag<G * 32 * ROWA, ROWA>(a[1], sa + ra[1]);
-  read_frag<G * 32 * ROWA, ROWA>(a[2], sa + ra[2]);
-  read_frag<G * 32 * ROWA, ROWA>(a[3], sa + ra[3]);
-  read_frag<G * 32 * ROWB, ROWB>(b[0], sa + rb[0]);
-  read_frag<G * 32 * ROWB, ROWB>(b[1], sa + rb[1]);
-  read_frag<G * 32 * ROWB, ROWB>(b[2], sa + rb[2]);
-  read_frag<G * 32 * ROWB, ROWB>(b[3], sa + rb[3]);
+__device__ __forceinline__ void read_group(u32x4 (&a)[4], u32x4 (&b)[4], const uint32_t (&ra)[4],
+                                           const uint32_t (&rb)[4], uint32_t sa) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) read_frag<G * 32 * ROWA, ROWA>(a[i], sa + ra[i]);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) read_frag<G * 32 * ROWB, ROWB>(b[i], sa + rb[i]);
+}
+
+__device__ __forceinline__ void wait_lds(u32x4 (&a)[4], u32x4 (&b)[4]) {
   asm volatile("s_waitcnt lgkmcnt(0)"
                : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
+}
+
+// The MFMAs of one k group; with bias, the wave's g fragment wn also meets a
+// ones fragment (column sums of g).
+__device__ __forceinline__ void mfma_group(f32x4_t (&acc)[4][4], f32x4_t &bacc, const u32x4 (&a)[4],
+                                           const u32x4 (&b)[4], bool bias, int wn) {
 #pragma unroll
   for (int tm = 0; tm < 4; ++tm) {
 #pragma unroll
@@ -205,17 +213,31 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
     for (int k = 0; k < 4; ++k) acc[i][k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   f32x4_t bacc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // Software pipeline over k tiles (R0/R1: fragments of k groups 0/1):
+  //   wait R0; read R1; MFMA R0; wait R1       -- this tile's reads are done
+  //   wait own copies of tile kt+1; barrier    -- kt+1 visible, stage kt free
+  //   copy tile kt+3 into stage kt; read R0 of tile kt+1; MFMA R1
+  // so the last MFMAs of a tile cover the next tile's first LDS reads.
   issue(0);
   issue(1);
+  issue(2);
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * (SA + SB)) : "memory");
+  asm volatile("s_barrier" ::: "memory");
+  u32x4 a0[4], b0[4], a1[4], b1[4];
+  if (nk > 0) read_group<0>(a0, b0, ra, rb, lds0);
   for (int kt = 0; kt < nk; ++kt) {
-    // tile kt is the older of the two in flight; then every wave's copies
-    // of it have landed and every wave is done with the stage refilled next
+    const uint32_t st = lds0 + (uint32_t)((kt % NS) * STAGE);
+    wait_lds(a0, b0);
+    read_group<1>(a1, b1, ra, rb, st);
+    mfma_group(acc, bacc, a0, b0, do_bias, wn);
+    wait_lds(a1, b1);
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(SA + SB) : "memory");
     asm volatile("s_barrier" ::: "memory");
-    issue(kt + 2);
-    const uint32_t sa = lds0 + (uint32_t)((kt % NS) * STAGE);
-    kgroup<0>(acc, bacc, ra, rb, sa, do_bias, wn);
-    kgroup<1>(acc, bacc, ra, rb, sa, do_bias, wn);
+    __builtin_amdgcn_sched_barrier(0);
+    issue(kt + 3);
+    if (kt + 1 < nk) read_group<0>(a0, b0, ra, rb, lds0 + (uint32_t)(((kt + 1) % NS) * STAGE));
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_group(acc, bacc, a1, b1, do_bias, wn);
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
