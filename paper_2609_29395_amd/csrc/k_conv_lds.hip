@@ -6,22 +6,27 @@
 //
 // (dgrad is a forward conv of g with the flipped, transposed weights Wd).
 // Both operands are k-contiguous: a k tile (64 values, 128 bytes per row) of
-// 128 pixel rows (gathered per kernel tap from the NHWC activation) and of
-// 256 weight rows is copied into LDS by buffer loads that write LDS directly;
+// 256 pixel rows (gathered per kernel tap from the NHWC activation) and of BN
+// weight rows is copied into LDS by buffer loads that write LDS directly;
 // taps outside the image, pixels past the batch and weight rows past N read
 // zero through the buffer range check.  Rows are XOR-swizzled in 16-byte
 // chunks (chunk ^ ((row >> 1) & 7)) so that the 16 rows of one fragment read
-// hit all banks.  Three LDS stages rotate; the fragment reads are inline asm
-// with explicit lgkmcnt waits so the compiler does not wait for every
-// outstanding copy, and the k loop is software-pipelined so that MFMAs
-// cover the LDS latency across the per-tile barrier.
+// hit all banks.  The fragment reads are inline asm with explicit lgkmcnt
+// waits so the compiler does not wait for every outstanding copy.
+//
+// The workgroup tile is large (256 pixels x up to 256 channels) because the
+// per-CU vector-memory path, not LDS or the MFMA pipe, bounds a k tile: the
+// bytes copied per MFMA fall as the tile grows.  Two LDS stages: the copy of
+// tile kt+1 is issued right after the barrier that starts tile kt and has
+// all of tile kt's MFMAs to land.
 //
 // The MFMA takes weight fragments as its A operand and pixel fragments as B,
 // so each lane accumulates 4 consecutive output channels of one pixel.  The
-// epilogue stages the fp32 tile through LDS and then works on 8 consecutive
-// channels per lane: 16-byte loads of the residual and mask, 16-byte stores.
-//
-// Workgroup: 8 waves, 128 pixels x 256 output channels, 64 x 64 per wave.
+// epilogue stages the fp32 tile through LDS, 64 pixel rows per pass, then
+// works on 8 consecutive channels per lane: 16-byte loads of the residual and
+// mask, 16-byte stores.
+#include <utility>
+
 #include "runtime.h"
 
 namespace {
@@ -32,17 +37,25 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
 
-constexpr int BM = 128, BN = 256, BK = 64, NS = 3, NTHR = 512;
+constexpr int BM = 256, BK = 64, NTHR = 512;
 constexpr int ROW = BK * 2;  // bytes per LDS row
-constexpr int A_BYTES = BM * ROW, B_BYTES = BN * ROW;
-constexpr int STAGE = A_BYTES + B_BYTES;
-constexpr int SA = A_BYTES / (NTHR * 16), SB = B_BYTES / (NTHR * 16);
-constexpr int LDS_BYTES = NS * STAGE;
-constexpr int EP_LD = 68;  // floats per staged epilogue row (64 + 4 padding)
 constexpr uint32_t kOob = 0x80000000u;
 constexpr int kBufferFlags = 0x00020000;
-static_assert(SA * NTHR * 16 == A_BYTES && SB * NTHR * 16 == B_BYTES, "copies must tile the stage");
-static_assert(8 * 64 * EP_LD * 4 <= LDS_BYTES, "epilogue staging must fit the stages");
+
+template <int BN, int WM, int WN> struct Cfg {
+  static constexpr int A_BYTES = BM * ROW, B_BYTES = BN * ROW;
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int SA = A_BYTES / (NTHR * 16), SB = B_BYTES / (NTHR * 16);  // copies per thread
+  static constexpr int TM = BM / WM / 16, TN = BN / WN / 16;                    // fragments per wave
+  static constexpr int WNW = BN / WN;                                            // wave tile width
+  static constexpr int EP_LD = WNW + 4;  // floats per staged epilogue row
+  static constexpr int EP_BYTES = 8 * 64 * EP_LD * 4;
+  static constexpr int LDS_BYTES = 2 * STAGE > EP_BYTES ? 2 * STAGE : EP_BYTES;
+  static_assert(WM * WN * 64 == NTHR, "8 waves");
+  static_assert(SA * NTHR * 16 == A_BYTES && SB * NTHR * 16 == B_BYTES, "copies must tile the stage");
+  static_assert(TM % 4 == 0 && TN >= 1, "wave tile: multiples of 64 pixels");
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+};
 
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
@@ -59,36 +72,75 @@ __device__ __forceinline__ void mma(f32x4_t &acc, const u32x4 &a, const u32x4 &b
                                                 acc, 0, 0, 0);
 }
 
-// Four fragments 16 rows (2048 bytes) apart.
-__device__ __forceinline__ void read4(u32x4 (&f)[4], uint32_t addr) {
-  asm volatile(
-      "ds_read_b128 %0, %4\n\t"
-      "ds_read_b128 %1, %4 offset:2048\n\t"
-      "ds_read_b128 %2, %4 offset:4096\n\t"
-      "ds_read_b128 %3, %4 offset:6144"
-      : "=&v"(f[0]), "=&v"(f[1]), "=&v"(f[2]), "=&v"(f[3])
-      : "v"(addr));
+// T fragments 16 rows (2048 bytes) apart; the reads stay in flight.  The
+// offsets are template constants (an asm immediate must be one).
+template <int OFF>
+__device__ __forceinline__ void read_frag(u32x4 &f, uint32_t addr) {
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(f) : "v"(addr), "n"(OFF));
+}
+template <int T, int... I>
+__device__ __forceinline__ void read_frags_seq(u32x4 (&f)[T], uint32_t addr, std::integer_sequence<int, I...>) {
+  (read_frag<I * 2048>(f[I], addr), ...);
+}
+template <int T>
+__device__ __forceinline__ void read_frags(u32x4 (&f)[T], uint32_t addr) {
+  read_frags_seq<T>(f, addr, std::make_integer_sequence<int, T>{});
 }
 
-__device__ __forceinline__ void wait_lds(u32x4 (&x)[4], u32x4 (&w)[4]) {
-  asm volatile("s_waitcnt lgkmcnt(0)"
-               : "+v"(x[0]), "+v"(x[1]), "+v"(x[2]), "+v"(x[3]), "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3]));
-}
-
-// The 16 MFMAs of one k group (32 values): weight fragments w, pixel fragments x.
-__device__ __forceinline__ void mfma_group(f32x4_t (&acc)[4][4], const u32x4 (&x)[4], const u32x4 (&w)[4]) {
+// Wait for every outstanding LDS read, then mark the fragments as produced
+// here so that no use of them is scheduled before the wait.
+template <int TA, int TB>
+__device__ __forceinline__ void wait_frags(u32x4 (&x)[TA], u32x4 (&w)[TB]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
-  for (int tm = 0; tm < 4; ++tm)
+  for (int t = 0; t < TA; ++t) asm volatile("" : "+v"(x[t]));
 #pragma unroll
-    for (int tn = 0; tn < 4; ++tn) mma(acc[tm][tn], w[tn], x[tm]);
+  for (int t = 0; t < TB; ++t) asm volatile("" : "+v"(w[t]));
 }
 
 __device__ __forceinline__ float bf2f(uint32_t bits16) { return bf16_to_f32((bf16_t)bits16); }
 __device__ __forceinline__ uint32_t f2bf(float f) { return (uint32_t)f32_to_bf16(f); }
 
-template <int EPI, bool TAPS1>
+// Copies of k tile kt into its stage: this thread's SA pixel-row and SB
+// weight-row 16-byte pieces.  The buffer resources are built here from plain
+// pointers: a buffer-resource value passed into a function or lambda of a
+// kernel template makes the host compilation pass drop the kernel's launch
+// stub without a diagnostic.
+template <typename CF, bool TAPS1>
+__device__ __forceinline__ void issue_tile(int kt, char *stage0, const ConvArgs &a, FastDiv fd_c, const void *src,
+                                           const void *wt, const int *achunk, const int *arowoff,
+                                           const uint32_t *amask, const uint32_t *boff) {
+  const __amdgpu_buffer_rsrc_t rsa = rsrc(src, (uint32_t)(a.src_rs * 2));
+  const __amdgpu_buffer_rsrc_t rsb = rsrc(wt, (uint32_t)((int64_t)a.N * a.Kp * 2));
+  char *sa = stage0 + (kt & 1) * CF::STAGE;
+#pragma unroll
+  for (int q = 0; q < CF::SA; ++q) {
+    const int k = kt * BK + 8 * achunk[q];
+    uint32_t off;
+    if constexpr (TAPS1) {
+      off = ((amask[q] != 0u) & (k < a.K)) ? (uint32_t)(arowoff[q] + k) * 2u : kOob;
+    } else {
+      // k past K has rs >= 9, outside the mask
+      const int rs = (int)fdiv((uint32_t)k, fd_c);
+      const int c = k - rs * a.Csrc;
+      const int r = (rs * 11) >> 5;  // rs / 3 for rs < 9
+      const int tap = ((r - 1) * a.W + (rs - 3 * r - 1)) * a.Csrc + c;
+      off = ((amask[q] >> min(rs, 31)) & 1u) ? (uint32_t)(arowoff[q] + tap) * 2u : kOob;
+    }
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(sa + q * NTHR * 16), 16, off, 0, 0, 0);
+  }
+  const uint32_t kb = (uint32_t)(kt * BK * 2);
+#pragma unroll
+  for (int q = 0; q < CF::SB; ++q)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, LDS_PTR(sa + CF::A_BYTES + q * NTHR * 16), 16,
+                                             boff[q] == kOob ? kOob : boff[q] + kb, 0, 0, 0);
+}
+
+template <int BN, int WM, int WN, int EPI, bool TAPS1>
 __global__ void __launch_bounds__(NTHR)
 conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
+  using CF = Cfg<BN, WM, WN>;
+  constexpr int SA = CF::SA, SB = CF::SB, TM = CF::TM, TN = CF::TN;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -101,8 +153,6 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   const int m0 = mt * BM, n0 = nt * BN;
   const bf16_t *src = reinterpret_cast<const bf16_t *>(a.src) + rep * a.src_rs;
   const bf16_t *wt = reinterpret_cast<const bf16_t *>(a.wt) + rep * a.wt_rs;
-  const __amdgpu_buffer_rsrc_t rsa = rsrc(src, (uint32_t)(a.src_rs * 2));
-  const __amdgpu_buffer_rsrc_t rsb = rsrc(wt, (uint32_t)((int64_t)a.N * a.Kp * 2));
 
   // This thread's copies: byte q*8192 + wave*1024 + lane*16 of the A (pixel)
   // and B (weight) regions of a stage.  Row and swizzled chunk are fixed;
@@ -142,180 +192,177 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
                       : kOob;
   }
 
-  // Tile kt >= nk is never multiplied; its copies only keep the count of
-  // copies in flight uniform (their stage is free by then: no reads follow).
   const int nk = a.Kp / BK;
   char *stage0 = smem + wave * 1024;
   auto issue = [&](int kt) {
-    char *sa = stage0 + (kt % NS) * STAGE;
-#pragma unroll
-    for (int q = 0; q < SA; ++q) {
-      const int k = kt * BK + 8 * achunk[q];
-      uint32_t off;
-      if constexpr (TAPS1) {
-        off = ((amask[q] != 0u) & (k < a.K)) ? (uint32_t)(arowoff[q] + k) * 2u : kOob;
-      } else {
-        // k past K has rs >= 9, outside the mask
-        const int rs = (int)fdiv((uint32_t)k, fd_c);
-        const int c = k - rs * a.Csrc;
-        const int r = (rs * 11) >> 5;  // rs / 3 for rs < 9
-        const int tap = ((r - 1) * a.W + (rs - 3 * r - 1)) * a.Csrc + c;
-        off = ((amask[q] >> min(rs, 31)) & 1u) ? (uint32_t)(arowoff[q] + tap) * 2u : kOob;
-      }
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(sa + q * NTHR * 16), 16, off, 0, 0, 0);
-    }
-    const uint32_t kb = kt < nk ? (uint32_t)(kt * BK * 2) : kOob;
-#pragma unroll
-    for (int q = 0; q < SB; ++q)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, LDS_PTR(sa + A_BYTES + q * NTHR * 16), 16,
-                                               boff[q] == kOob ? kOob : boff[q] + kb, 0, 0, 0);
+    issue_tile<CF, TAPS1>(kt, stage0, a, fd_c, src, wt, achunk, arowoff, amask, boff);
   };
 
   // fragment read addresses: lane (li, lg) reads row li of a 16-row block,
-  // chunk 4*kg + lg; rows of one wave's blocks are 16 apart (2048 bytes)
+  // chunk 4*kg + lg; the swizzle depends on li only
   const int li = lane & 15, lg = lane >> 4;
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave / WN, wn = wave % WN;
   const uint32_t lds0 = (uint32_t)(size_t)LDS_PTR(smem);
   uint32_t xa[2], wa[2];
 #pragma unroll
   for (int kg = 0; kg < 2; ++kg) {
     const int ph = ((4 * kg + lg) ^ swz(li)) * 16;
-    xa[kg] = (uint32_t)((wm * 64 + li) * ROW + ph);
-    wa[kg] = (uint32_t)(A_BYTES + (wn * 64 + li) * ROW + ph);
+    xa[kg] = (uint32_t)((wm * TM * 16 + li) * ROW + ph);
+    wa[kg] = (uint32_t)(CF::A_BYTES + (wn * TN * 16 + li) * ROW + ph);
   }
 
-  f32x4_t acc[4][4];
+  f32x4_t acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int k = 0; k < 4; ++k) acc[i][k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int k = 0; k < TN; ++k) acc[i][k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // Software pipeline over k tiles (R0/R1: fragments of k groups 0/1):
-  //   wait R0; read R1; MFMA R0; wait R1       -- this tile's reads are done
-  //   wait own copies of tile kt+1; barrier    -- kt+1 visible, stage kt free
-  //   copy tile kt+3 into stage kt; read R0 of tile kt+1; MFMA R1
-  // so the last 16 MFMAs of a tile cover the next tile's first LDS reads.
   issue(0);
-  issue(1);
-  issue(2);
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * (SA + SB)) : "memory");
-  asm volatile("s_barrier" ::: "memory");
-  u32x4 x0[4], w0[4], x1[4], w1[4];
-  read4(x0, lds0 + xa[0]);
-  read4(w0, lds0 + wa[0]);
   for (int kt = 0; kt < nk; ++kt) {
-    const uint32_t st = lds0 + (uint32_t)((kt % NS) * STAGE);
-    wait_lds(x0, w0);
-    read4(x1, st + xa[1]);
-    read4(w1, st + wa[1]);
-    mfma_group(acc, x0, w0);
-    wait_lds(x1, w1);
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(SA + SB) : "memory");
+    // own copies of tile kt have landed; after the barrier every wave's
+    // have, and every wave is done with tile kt-1, whose stage is refilled
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     asm volatile("s_barrier" ::: "memory");
-    __builtin_amdgcn_sched_barrier(0);
-    issue(kt + 3);
-    if (kt + 1 < nk) {
-      const uint32_t sn = lds0 + (uint32_t)(((kt + 1) % NS) * STAGE);
-      read4(x0, sn + xa[0]);
-      read4(w0, sn + wa[0]);
+    if (kt + 1 < nk) issue(kt + 1);
+    const uint32_t st = lds0 + (uint32_t)((kt & 1) * CF::STAGE);
+#pragma unroll
+    for (int kg = 0; kg < 2; ++kg) {
+      u32x4 x[TM], w[TN];
+      read_frags<TM>(x, st + xa[kg]);
+      read_frags<TN>(w, st + wa[kg]);
+      wait_frags<TM, TN>(x, w);
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) mma(acc[tm][tn], w[tn], x[tm]);
     }
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_group(acc, x1, w1);
   }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
-  // epilogue: stage the wave's 64 x 64 fp32 tile as [pixel][channel]
-  float *ep = reinterpret_cast<float *>(smem) + wave * 64 * EP_LD;
-#pragma unroll
-  for (int tm = 0; tm < 4; ++tm)
-#pragma unroll
-    for (int tn = 0; tn < 4; ++tn)
-      *reinterpret_cast<f32x4_t *>(ep + (tm * 16 + li) * EP_LD + tn * 16 + lg * 4) = acc[tm][tn];
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-  const int seg = lane & 7;                      // channels 8*seg .. 8*seg+7 of the wave tile
-  const int n = n0 + wn * 64 + 8 * seg;
-  if (n >= a.N) return;
+  // epilogue: 64 pixel rows of the wave tile per pass, staged as
+  // [pixel][channel] fp32, then 8 channels per lane
+  constexpr int SEGS = CF::WNW / 8;  // 8-channel segments per row
+  constexpr int RSTEP = 64 / SEGS;   // rows per lane step
+  float *ep = reinterpret_cast<float *>(smem) + wave * 64 * CF::EP_LD;
+  const int seg = lane % SEGS;
+  const int n = n0 + wn * CF::WNW + 8 * seg;
+  const bool nok = n < a.N;
   float bias[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) bias[e] = EPI == EPI_FWD ? a.bias[rep * a.bias_rs + n + e] : 0.f;
+  for (int e = 0; e < 8; ++e) bias[e] = (EPI == EPI_FWD && nok) ? a.bias[rep * a.bias_rs + n + e] : 0.f;
   bf16_t *out = reinterpret_cast<bf16_t *>(a.out) + rep * a.out_rs;
   const bf16_t *res = a.res ? reinterpret_cast<const bf16_t *>(a.res) + rep * a.out_rs : nullptr;
   const bf16_t *msk = a.mask ? reinterpret_cast<const bf16_t *>(a.mask) + rep * a.out_rs : nullptr;
+#pragma unroll
+  for (int pass = 0; pass < TM / 4; ++pass) {
+#pragma unroll
+    for (int tm = 0; tm < 4; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+        *reinterpret_cast<f32x4_t *>(ep + (tm * 16 + li) * CF::EP_LD + tn * 16 + lg * 4) = acc[pass * 4 + tm][tn];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (nok) {
 #pragma unroll 2
-  for (int i = 0; i < 8; ++i) {
-    const int r = (lane >> 3) + 8 * i;  // pixel row of the wave tile
-    const int m = m0 + wm * 64 + r;
-    if (m >= M) break;
-    const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(ep + r * EP_LD + 8 * seg);
-    const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(ep + r * EP_LD + 8 * seg + 4);
-    float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    const int64_t o = (int64_t)m * a.N + n;
-    if (res) {
-      const uint4 rv = *reinterpret_cast<const uint4 *>(res + o);
-      const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
+      for (int i = 0; i < SEGS; ++i) {
+        const int r = lane / SEGS + RSTEP * i;  // pixel row of this pass
+        const int m = m0 + wm * TM * 16 + pass * 64 + r;
+        if (m >= M) break;
+        const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(ep + r * CF::EP_LD + 8 * seg);
+        const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(ep + r * CF::EP_LD + 8 * seg + 4);
+        float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        const int64_t o = (int64_t)m * a.N + n;
+        if (res) {
+          const uint4 rv = *reinterpret_cast<const uint4 *>(res + o);
+          const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        v[2 * e] += bf2f(rw[e] & 0xffffu);
-        v[2 * e + 1] += bf2f(rw[e] >> 16);
-      }
-    }
-    if constexpr (EPI == EPI_FWD) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e] + bias[e], 0.f);
-    } else {
-      if (msk) {
-        const uint4 mv = *reinterpret_cast<const uint4 *>(msk + o);
-        const uint32_t mw[4] = {mv.x, mv.y, mv.z, mv.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          if (!(bf2f(mw[e] & 0xffffu) > 0.f)) v[2 * e] = 0.f;
-          if (!(bf2f(mw[e] >> 16) > 0.f)) v[2 * e + 1] = 0.f;
+          for (int e = 0; e < 4; ++e) {
+            v[2 * e] += bf2f(rw[e] & 0xffffu);
+            v[2 * e + 1] += bf2f(rw[e] >> 16);
+          }
         }
+        if constexpr (EPI == EPI_FWD) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e] + bias[e], 0.f);
+        } else {
+          if (msk) {
+            const uint4 mv = *reinterpret_cast<const uint4 *>(msk + o);
+            const uint32_t mw[4] = {mv.x, mv.y, mv.z, mv.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              if (!(bf2f(mw[e] & 0xffffu) > 0.f)) v[2 * e] = 0.f;
+              if (!(bf2f(mw[e] >> 16) > 0.f)) v[2 * e + 1] = 0.f;
+            }
+          }
+        }
+        uint4 ov;
+        ov.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
+        ov.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
+        ov.z = f2bf(v[4]) | (f2bf(v[5]) << 16);
+        ov.w = f2bf(v[6]) | (f2bf(v[7]) << 16);
+        *reinterpret_cast<uint4 *>(out + o) = ov;
       }
     }
-    uint4 ov;
-    ov.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
-    ov.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
-    ov.z = f2bf(v[4]) | (f2bf(v[5]) << 16);
-    ov.w = f2bf(v[6]) | (f2bf(v[7]) << 16);
-    *reinterpret_cast<uint4 *>(out + o) = ov;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
+}
+
+template <int BN, int WM, int WN>
+void grid(const ConvArgs &a, int *MT, int *NT) {
+  const int M = a.Bt * a.H * a.W;
+  *MT = (M + BM - 1) / BM;
+  *NT = (a.N + BN - 1) / BN;
 }
 
 }  // namespace
 
 bool conv_lds_ok(int dtype, const ConvArgs &a) {
-  return dtype == GCPSL_BF16 && a.N >= 128 && a.N % 8 == 0 && a.Csrc % 8 == 0 && a.Kp % BK == 0;
+  return dtype == GCPSL_BF16 && a.N > 64 && a.N % 8 == 0 && a.Csrc % 8 == 0 && a.Kp % BK == 0;
 }
 
+// Every instantiation is named in this (non-template) function, which is
+// what makes the compiler emit the host-side launch stubs.
 hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label) {
+#define CONV_LDS_K(BN, WM, WN, E, T) conv_lds_kernel<BN, WM, WN, E, T>
+#define CONV_LDS_ATTR(BN, WM, WN)                                                                       \
+  for (const void *f : {reinterpret_cast<const void *>(&CONV_LDS_K(BN, WM, WN, EPI_FWD, false)),           \
+                        reinterpret_cast<const void *>(&CONV_LDS_K(BN, WM, WN, EPI_FWD, true)),            \
+                        reinterpret_cast<const void *>(&CONV_LDS_K(BN, WM, WN, EPI_DGRAD, false)),         \
+                        reinterpret_cast<const void *>(&CONV_LDS_K(BN, WM, WN, EPI_DGRAD, true))}) {       \
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,               \
+                                             Cfg<BN, WM, WN>::LDS_BYTES);                                 \
+    if (e != hipSuccess) return e;                                                                        \
+  }
   static bool attr = false;
   if (!attr) {
-    for (const void *f : {reinterpret_cast<const void *>(&conv_lds_kernel<EPI_FWD, false>),
-                          reinterpret_cast<const void *>(&conv_lds_kernel<EPI_FWD, true>),
-                          reinterpret_cast<const void *>(&conv_lds_kernel<EPI_DGRAD, false>),
-                          reinterpret_cast<const void *>(&conv_lds_kernel<EPI_DGRAD, true>)}) {
-      const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
-      if (e != hipSuccess) return e;
-    }
+    CONV_LDS_ATTR(256, 2, 4)
+    CONV_LDS_ATTR(128, 4, 2)
     attr = true;
   }
-  const int M = a.Bt * a.H * a.W;
-  const int MT = (M + BM - 1) / BM, NT = (a.N + BN - 1) / BN;
+  const bool wide = a.N > 128;
+  int MT, NT;
+  if (wide) grid<256, 2, 4>(a, &MT, &NT);
+  else grid<128, 4, 2>(a, &MT, &NT);
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Csrc);
-  const uint32_t blocks = (uint32_t)MT * NT * a.C;
-  if (label) *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16,128x256x64,w8,lds>";
-  const dim3 g(blocks), b(NTHR);
-  if (a.epi == EPI_FWD) {
-    if (a.taps == 1) hipLaunchKernelGGL((conv_lds_kernel<EPI_FWD, true>), g, b, LDS_BYTES, s, a, fw, fh, fc, MT, NT);
-    else hipLaunchKernelGGL((conv_lds_kernel<EPI_FWD, false>), g, b, LDS_BYTES, s, a, fw, fh, fc, MT, NT);
+  const dim3 g((uint32_t)MT * NT * a.C), b(NTHR);
+  if (label)
+    *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + (wide ? "<bf16,256x256x64,w8,lds>"
+                                                                              : "<bf16,256x128x64,w8,lds>");
+#define CONV_LDS_GO(BN, WM, WN, E, T) \
+  hipLaunchKernelGGL((CONV_LDS_K(BN, WM, WN, E, T)), g, b, (Cfg<BN, WM, WN>::LDS_BYTES), s, a, fw, fh, fc, MT, NT)
+  const bool fwd = a.epi == EPI_FWD, t1 = a.taps == 1;
+  if (wide) {
+    if (fwd) { if (t1) CONV_LDS_GO(256, 2, 4, EPI_FWD, true); else CONV_LDS_GO(256, 2, 4, EPI_FWD, false); }
+    else { if (t1) CONV_LDS_GO(256, 2, 4, EPI_DGRAD, true); else CONV_LDS_GO(256, 2, 4, EPI_DGRAD, false); }
   } else {
-    if (a.taps == 1) hipLaunchKernelGGL((conv_lds_kernel<EPI_DGRAD, true>), g, b, LDS_BYTES, s, a, fw, fh, fc, MT, NT);
-    else hipLaunchKernelGGL((conv_lds_kernel<EPI_DGRAD, false>), g, b, LDS_BYTES, s, a, fw, fh, fc, MT, NT);
+    if (fwd) { if (t1) CONV_LDS_GO(128, 4, 2, EPI_FWD, true); else CONV_LDS_GO(128, 4, 2, EPI_FWD, false); }
+    else { if (t1) CONV_LDS_GO(128, 4, 2, EPI_DGRAD, true); else CONV_LDS_GO(128, 4, 2, EPI_DGRAD, false); }
   }
+#undef CONV_LDS_GO
+#undef CONV_LDS_ATTR
+#undef CONV_LDS_K
   return hipGetLastError();
 }
