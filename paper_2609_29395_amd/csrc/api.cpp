@@ -211,7 +211,7 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
         // (rounds of 256 workgroups) x (k tiles per workgroup + the cost of
         // writing and re-reading a partial tile, about 16 k tiles)
         int bk;
-        wgrad_lds_tile(&bm, &bn, &bk);
+        wgrad_lds_tile(l.Co, &bm, &bn, &bk);
         const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
         int64_t best = -1;
         splits = 1;

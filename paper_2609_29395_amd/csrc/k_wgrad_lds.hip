@@ -5,7 +5,7 @@
 // with p = (b, h, w) running over a chunk of the batch's pixels (split-K).
 // Both operands are stored pixel-major (NHWC): the reduction index is the
 // outer dimension.  A k tile of 64 pixels is copied into LDS exactly as it
-// lies in memory -- 64 rows of 128 output channels (g) and 64 rows of 256
+// lies in memory -- 64 rows of BM output channels (g) and 64 rows of BN
 // im2col columns (x, shifted per kernel tap) -- by buffer loads that write LDS
 // directly, so no registers stage the tiles and out-of-image taps,
 // out-of-chunk pixels and ragged columns are zero-filled by the buffer range
@@ -15,19 +15,17 @@
 // and lane i receives channel i of the 4 pixels.
 //
 // LDS rows are XOR-swizzled in 16-byte chunks (chunk ^ swz(row)) so that the
-// 16 pixels of one transposing read fall on all banks.  Three LDS stages
-// rotate: while tile kt is multiplied the copies of the next two tiles are in
-// flight, and tile kt's stage is refilled once every wave has read it.  Each
-// wave waits for its own copies (vmcnt), a barrier publishes them.  The LDS
-// reads are
+// 16 pixels of one transposing read fall on all banks.  The LDS reads are
 // inline asm with explicit lgkmcnt waits so that the compiler does not add a
-// wait for every outstanding copy before them, and the k loop is
-// software-pipelined so that MFMAs cover the LDS latency across the barrier.
+// wait for every outstanding copy before them.
 //
-// Workgroup: 8 waves, 128 (co) x 256 (columns) outputs, 64 x 64 per wave.
-// The bias gradient rides along in the column-tile-0 workgroups: every wave
-// multiplies one of its g fragments by a ones fragment (one extra MFMA per
-// k group).
+// The workgroup tile is large (up to 256 x 256 outputs, 8 waves) because the
+// per-CU vector-memory path bounds a k tile: the bytes copied per MFMA fall
+// as the tile grows.  Two LDS stages: the copy of tile kt+1 is issued right
+// after the barrier that starts tile kt and has all of tile kt's MFMAs to
+// land.  The bias gradient rides along in the column-tile-0 workgroups: each
+// wave multiplies BPW of its g fragments by a ones fragment (one extra MFMA
+// per fragment and k group), together covering the workgroup's rows.
 #include "runtime.h"
 
 namespace {
@@ -39,16 +37,24 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
 
-constexpr int BM = 128, BN = 256, BK = 64, NS = 3, NTHR = 512;
-constexpr int ROWA = BM * 2, ROWB = BN * 2;  // bytes per LDS row
-constexpr int A_BYTES = BK * ROWA, B_BYTES = BK * ROWB;
-constexpr int STAGE = A_BYTES + B_BYTES;
-constexpr int SA = A_BYTES / (NTHR * 16), SB = B_BYTES / (NTHR * 16);  // 16-byte copies per thread
-constexpr int LDS_BYTES = NS * STAGE;
+constexpr int BK = 64, NTHR = 512;
 constexpr uint32_t kOob = 0x80000000u;
 constexpr int kBufferFlags = 0x00020000;
-static_assert(SA * NTHR * 16 == A_BYTES && SB * NTHR * 16 == B_BYTES, "copies must tile the stage");
-static_assert(SA + SB <= 63, "per-wave copies per tile must fit the vmcnt field");
+constexpr int kDead = 1 << 30;  // row index that fails every pixel test
+
+template <int BM, int BN, int WM, int WN> struct Cfg {
+  static constexpr int ROWA = BM * 2, ROWB = BN * 2;  // bytes per LDS row
+  static constexpr int A_BYTES = BK * ROWA, B_BYTES = BK * ROWB;
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int SA = A_BYTES / (NTHR * 16), SB = B_BYTES / (NTHR * 16);  // copies per thread
+  static constexpr int TM = BM / WM / 16, TN = BN / WN / 16;                    // fragments per wave
+  static constexpr int BPW = TM / WN;                                            // bias fragments per wave
+  static constexpr int LDS_BYTES = 2 * STAGE;
+  static_assert(WM * WN * 64 == NTHR, "8 waves");
+  static_assert(SA * NTHR * 16 == A_BYTES && SB * NTHR * 16 == B_BYTES, "copies must tile the stage");
+  static_assert(BPW >= 1 && BPW * WN == TM, "bias fragments split evenly over the waves of a row");
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+};
 
 __device__ __forceinline__ int swz(int row) { return ((row & 3) | ((row >> 1) & 4)) << 1; }
 
@@ -75,40 +81,80 @@ __device__ __forceinline__ void mma(f32x4_t &acc, const u32x4 &a, const u32x4 &b
                                                 acc, 0, 0, 0);
 }
 
-// Fragments of k group G (32 pixels) of the stage at byte address sa: g (A
-// operand) and x (B operand); the reads stay in flight until wait_lds.
-template <int G>
-__device__ __forceinline__ void read_group(u32x4 (&a)[4], u32x4 (&b)[4], const uint32_t (&ra)[4],
-                                           const uint32_t (&rb)[4], uint32_t sa) {
+// Copies of k tile kt into its stage.  The buffer resources are built here
+// from plain pointers: a buffer-resource value passed into a function or
+// lambda of a kernel template makes the host compilation pass drop the
+// kernel's launch stub without a diagnostic.
+template <typename CF, bool TAPS1>
+__device__ __forceinline__ void issue_tile(int kt, char *stage0, const WgradArgs &a, FastDiv fd_w, FastDiv fd_h,
+                                           const void *G, const void *X, int M, int p_begin, int p_end,
+                                           const int *arow, const int *acol, const int *brow, const int *bci,
+                                           const int *bdh, const int *bdw) {
+  const __amdgpu_buffer_rsrc_t rsg = rsrc(G, (uint32_t)((int64_t)M * a.Co * 2));
+  const __amdgpu_buffer_rsrc_t rsx = rsrc(X, (uint32_t)((int64_t)M * a.Ci * 2));
+  char *sa = stage0 + (kt & 1) * CF::STAGE;
+  const int pt = p_begin + kt * BK;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) read_frag<G * 32 * ROWA, ROWA>(a[i], sa + ra[i]);
+  for (int q = 0; q < CF::SA; ++q) {
+    const int p = pt + arow[q];
+    const uint32_t off = p < p_end ? ((uint32_t)p * (uint32_t)a.Co + (uint32_t)acol[q]) * 2u : kOob;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsg, LDS_PTR(sa + q * NTHR * 16), 16, off, 0, 0, 0);
+  }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) read_frag<G * 32 * ROWB, ROWB>(b[i], sa + rb[i]);
-}
-
-__device__ __forceinline__ void wait_lds(u32x4 (&a)[4], u32x4 (&b)[4]) {
-  asm volatile("s_waitcnt lgkmcnt(0)"
-               : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
-}
-
-// The MFMAs of one k group; with bias, the wave's g fragment wn also meets a
-// ones fragment (column sums of g).
-__device__ __forceinline__ void mfma_group(f32x4_t (&acc)[4][4], f32x4_t &bacc, const u32x4 (&a)[4],
-                                           const u32x4 (&b)[4], bool bias, int wn) {
-#pragma unroll
-  for (int tm = 0; tm < 4; ++tm) {
-#pragma unroll
-    for (int tn = 0; tn < 4; ++tn) mma(acc[tm][tn], a[tm], b[tn]);
-    if (bias && tm == wn) {
-      const uint32_t one2 = 0x3F803F80u;  // two bf16 ones
-      mma(bacc, a[tm], u32x4{one2, one2, one2, one2});
+  for (int q = 0; q < CF::SB; ++q) {
+    const int p = pt + brow[q];
+    bool ok = p < p_end;
+    int src = p;
+    if constexpr (!TAPS1) {
+      const uint32_t q1 = fdiv((uint32_t)p, fd_w);
+      const int w = p - (int)q1 * a.W;
+      const int h = (int)q1 - (int)fdiv(q1, fd_h) * a.H;
+      ok = ok & ((unsigned)(h + bdh[q]) < (unsigned)a.H) & ((unsigned)(w + bdw[q]) < (unsigned)a.W);
+      src = p + bdh[q] * a.W + bdw[q];
     }
+    const uint32_t off = ok ? ((uint32_t)src * (uint32_t)a.Ci + (uint32_t)bci[q]) * 2u : kOob;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, LDS_PTR(sa + CF::A_BYTES + q * NTHR * 16), 16, off, 0, 0, 0);
   }
 }
 
-template <bool TAPS1>
+// Fragments of k group KG (32 pixels) of the stage at byte address st, then
+// their MFMAs; with bias, g fragments b0 .. b0+BPW-1 also meet a ones
+// fragment (column sums of g).
+template <typename CF, int KG>
+__device__ __forceinline__ void kgroup(f32x4_t (&acc)[CF::TM][CF::TN], f32x4_t (&bacc)[CF::BPW],
+                                       const uint32_t (&ra)[CF::TM], const uint32_t (&rb)[CF::TN], uint32_t st,
+                                       bool bias, int b0) {
+  constexpr int TM = CF::TM, TN = CF::TN;
+  u32x4 a[TM], b[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) read_frag<KG * 32 * CF::ROWA, CF::ROWA>(a[i], st + ra[i]);
+#pragma unroll
+  for (int i = 0; i < TN; ++i) read_frag<KG * 32 * CF::ROWB, CF::ROWB>(b[i], st + rb[i]);
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < TM; ++i) asm volatile("" : "+v"(a[i]));
+#pragma unroll
+  for (int i = 0; i < TN; ++i) asm volatile("" : "+v"(b[i]));
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) mma(acc[tm][tn], a[tm], b[tn]);
+  if (bias) {
+    const uint32_t one2 = 0x3F803F80u;  // two bf16 ones
+    const u32x4 ones = u32x4{one2, one2, one2, one2};
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int i = 0; i < CF::BPW; ++i)
+        if (tm == b0 + i) mma(bacc[i], a[tm], ones);
+  }
+}
+
+template <int BM, int BN, int WM, int WN, bool TAPS1>
 __global__ void __launch_bounds__(NTHR)
 wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
+  using CF = Cfg<BM, BN, WM, WN>;
+  constexpr int SA = CF::SA, SB = CF::SB, TM = CF::TM, TN = CF::TN, BPW = CF::BPW;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -129,20 +175,17 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
   const bf16_t *G = reinterpret_cast<const bf16_t *>(a.g) + rep * a.g_rs;
   const bf16_t *X = reinterpret_cast<const bf16_t *>(a.x) + rep * a.x_rs;
   const bool do_bias = (nt == 0) && a.db != nullptr;
-  const __amdgpu_buffer_rsrc_t rsg = rsrc(G, (uint32_t)((int64_t)M * a.Co * 2));
-  const __amdgpu_buffer_rsrc_t rsx = rsrc(X, (uint32_t)((int64_t)M * a.Ci * 2));
 
   // This thread's copies: byte q*8192 + wave*1024 + lane*16 of the A and B
   // regions of a stage.  The row and the swizzled column it fills are the
   // same for every k tile; only the pixel advances.  A column outside the
   // operand gets a row index past any chunk, so its pixel test fails.
-  constexpr int kDead = 1 << 30;
   int arow[SA], acol[SA];
 #pragma unroll
   for (int q = 0; q < SA; ++q) {
     const int byte = q * NTHR * 16 + wave * 1024 + lane * 16;
-    const int row = byte / ROWA;
-    const int co = m0 + 8 * (((byte % ROWA) / 16) ^ swz(row));
+    const int row = byte / CF::ROWA;
+    const int co = m0 + 8 * (((byte % CF::ROWA) / 16) ^ swz(row));
     arow[q] = co < a.Co ? row : kDead;
     acol[q] = co;
   }
@@ -150,8 +193,8 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
 #pragma unroll
   for (int q = 0; q < SB; ++q) {
     const int byte = q * NTHR * 16 + wave * 1024 + lane * 16;
-    const int row = byte / ROWB;
-    const int kk = n0 + 8 * (((byte % ROWB) / 16) ^ swz(row));
+    const int row = byte / CF::ROWB;
+    const int kk = n0 + 8 * (((byte % CF::ROWB) / 16) ^ swz(row));
     brow[q] = kk < NW ? row : kDead;
     if constexpr (TAPS1) {
       bci[q] = kk; bdh[q] = 0; bdw[q] = 0;
@@ -163,102 +206,69 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
       bdw[q] = rs - 3 * r - 1;
     }
   }
-
-  // Tile kt >= nk starts at or past p_end: all its copies read zero.
   char *stage0 = smem + wave * 1024;
-  auto issue = [&](int kt) {
-    char *sa = stage0 + (kt % NS) * STAGE;
-    const int pt = p_begin + kt * BK;
-#pragma unroll
-    for (int q = 0; q < SA; ++q) {
-      const int p = pt + arow[q];
-      const uint32_t off = p < p_end ? ((uint32_t)p * (uint32_t)a.Co + (uint32_t)acol[q]) * 2u : kOob;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsg, LDS_PTR(sa + q * NTHR * 16), 16, off, 0, 0, 0);
-    }
-#pragma unroll
-    for (int q = 0; q < SB; ++q) {
-      const int p = pt + brow[q];
-      bool ok = p < p_end;
-      int src = p;
-      if constexpr (!TAPS1) {
-        const uint32_t q1 = fdiv((uint32_t)p, fd_w);
-        const int w = p - (int)q1 * a.W;
-        const int h = (int)q1 - (int)fdiv(q1, fd_h) * a.H;
-        ok = ok & ((unsigned)(h + bdh[q]) < (unsigned)a.H) & ((unsigned)(w + bdw[q]) < (unsigned)a.W);
-        src = p + bdh[q] * a.W + bdw[q];
-      }
-      const uint32_t off = ok ? ((uint32_t)src * (uint32_t)a.Ci + (uint32_t)bci[q]) * 2u : kOob;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, LDS_PTR(sa + A_BYTES + q * NTHR * 16), 16, off, 0, 0, 0);
-    }
-  };
 
   // fragment read addresses (relative to a stage)
   const int j = lane & 15, lg = lane >> 4;
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave / WN, wn = wave % WN;
   const int frow = 8 * lg + (j >> 2);
   const int fsw = swz(frow);
   const int half = ((j & 3) >> 1);
-  uint32_t ra[4], rb[4];
+  uint32_t ra[TM], rb[TN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    ra[i] = (uint32_t)(frow * ROWA + (((8 * wm + 2 * i + half) ^ fsw) * 16) + (j & 1) * 8);
-    rb[i] = (uint32_t)(A_BYTES + frow * ROWB + (((8 * wn + 2 * i + half) ^ fsw) * 16) + (j & 1) * 8);
-  }
+  for (int i = 0; i < TM; ++i)
+    ra[i] = (uint32_t)(frow * CF::ROWA + (((2 * (wm * TM + i) + half) ^ fsw) * 16) + (j & 1) * 8);
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+    rb[i] = (uint32_t)(CF::A_BYTES + frow * CF::ROWB + (((2 * (wn * TN + i) + half) ^ fsw) * 16) + (j & 1) * 8);
   const uint32_t lds0 = (uint32_t)(size_t)LDS_PTR(smem);
 
-  f32x4_t acc[4][4];
+  f32x4_t acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int k = 0; k < 4; ++k) acc[i][k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  f32x4_t bacc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int k = 0; k < TN; ++k) acc[i][k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  f32x4_t bacc[BPW];
+#pragma unroll
+  for (int i = 0; i < BPW; ++i) bacc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int b0 = wn * BPW;
 
-  // Software pipeline over k tiles (R0/R1: fragments of k groups 0/1):
-  //   wait R0; read R1; MFMA R0; wait R1       -- this tile's reads are done
-  //   wait own copies of tile kt+1; barrier    -- kt+1 visible, stage kt free
-  //   copy tile kt+3 into stage kt; read R0 of tile kt+1; MFMA R1
-  // so the last MFMAs of a tile cover the next tile's first LDS reads.
-  issue(0);
-  issue(1);
-  issue(2);
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * (SA + SB)) : "memory");
-  asm volatile("s_barrier" ::: "memory");
-  u32x4 a0[4], b0[4], a1[4], b1[4];
-  if (nk > 0) read_group<0>(a0, b0, ra, rb, lds0);
+  issue_tile<CF, TAPS1>(0, stage0, a, fd_w, fd_h, G, X, M, p_begin, p_end, arow, acol, brow, bci, bdh, bdw);
   for (int kt = 0; kt < nk; ++kt) {
-    const uint32_t st = lds0 + (uint32_t)((kt % NS) * STAGE);
-    wait_lds(a0, b0);
-    read_group<1>(a1, b1, ra, rb, st);
-    mfma_group(acc, bacc, a0, b0, do_bias, wn);
-    wait_lds(a1, b1);
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(SA + SB) : "memory");
+    // own copies of tile kt have landed; after the barrier every wave's
+    // have, and every wave is done with tile kt-1, whose stage is refilled
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     asm volatile("s_barrier" ::: "memory");
-    __builtin_amdgcn_sched_barrier(0);
-    issue(kt + 3);
-    if (kt + 1 < nk) read_group<0>(a0, b0, ra, rb, lds0 + (uint32_t)(((kt + 1) % NS) * STAGE));
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_group(acc, bacc, a1, b1, do_bias, wn);
+    if (kt + 1 < nk)
+      issue_tile<CF, TAPS1>(kt + 1, stage0, a, fd_w, fd_h, G, X, M, p_begin, p_end, arow, acol, brow, bci, bdh,
+                            bdw);
+    const uint32_t st = lds0 + (uint32_t)((kt & 1) * CF::STAGE);
+    kgroup<CF, 0>(acc, bacc, ra, rb, st, do_bias, b0);
+    kgroup<CF, 1>(acc, bacc, ra, rb, st, do_bias, b0);
   }
+  // nk == 0 leaves the first copy in flight
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
   float *dw = a.dw + split * a.dw_ss + rep * a.dw_rs;
 #pragma unroll
-  for (int tn = 0; tn < 4; ++tn) {
-    const int n = n0 + wn * 64 + tn * 16 + j;
+  for (int tn = 0; tn < TN; ++tn) {
+    const int n = n0 + (wn * TN + tn) * 16 + j;
 #pragma unroll
-    for (int tm = 0; tm < 4; ++tm)
+    for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int m = m0 + wm * 64 + tm * 16 + lg * 4 + r;
+        const int m = m0 + (wm * TM + tm) * 16 + lg * 4 + r;
         if (m < a.Co && n < a.nw) dw[(int64_t)m * a.nw + n] = acc[tm][tn][r];
       }
   }
   if (do_bias && j == 0) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int co = m0 + wm * 64 + wn * 16 + lg * 4 + r;
-      if (co < a.Co) a.db[split * a.db_ss + rep * a.db_rs + co] = bacc[r];
-    }
+    for (int i = 0; i < BPW; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int co = m0 + (wm * TM + b0 + i) * 16 + lg * 4 + r;
+        if (co < a.Co) a.db[split * a.db_ss + rep * a.db_rs + co] = bacc[i][r];
+      }
   }
 }
 
@@ -268,30 +278,45 @@ bool wgrad_lds_ok(int dtype, int Co, int Ci) {
   return dtype == GCPSL_BF16 && Co >= 128 && Co % 8 == 0 && Ci % 8 == 0;
 }
 
-void wgrad_lds_tile(int *bm, int *bn, int *bk) {
-  *bm = BM;
-  *bn = BN;
+void wgrad_lds_tile(int Co, int *bm, int *bn, int *bk) {
+  *bm = Co > 128 ? 256 : 128;
+  *bn = 256;
   *bk = BK;
 }
 
+// Every instantiation is named in this (non-template) function.
 hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *label) {
+#define WG_K(BM, BN, WM, WN, T) wgrad_lds_kernel<BM, BN, WM, WN, T>
+#define WG_ATTR(BM, BN, WM, WN)                                                                               \
+  for (const void *f : {reinterpret_cast<const void *>(&WG_K(BM, BN, WM, WN, true)),                        \
+                        reinterpret_cast<const void *>(&WG_K(BM, BN, WM, WN, false))}) {                    \
+    const hipError_t e =                                                                                     \
+        hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, Cfg<BM, BN, WM, WN>::LDS_BYTES); \
+    if (e != hipSuccess) return e;                                                                           \
+  }
   static bool attr = false;
   if (!attr) {
-    for (const void *f : {reinterpret_cast<const void *>(&wgrad_lds_kernel<true>),
-                          reinterpret_cast<const void *>(&wgrad_lds_kernel<false>)}) {
-      const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
-      if (e != hipSuccess) return e;
-    }
+    WG_ATTR(256, 256, 2, 4)
+    WG_ATTR(128, 256, 2, 4)
     attr = true;
   }
+  const bool wide = a.Co > 128;
+  const int BM = wide ? 256 : 128, BN = 256;
   const int NW = a.taps == 1 ? a.Ci : 9 * a.Ci;
   const int MT = (a.Co + BM - 1) / BM, NT = (NW + BN - 1) / BN;
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Ci);
-  const uint32_t blocks = (uint32_t)MT * NT * a.splits * a.C;
-  if (label) *label = "conv_wgrad<bf16,128x256,w8,lds>";
-  if (a.taps == 1)
-    hipLaunchKernelGGL(wgrad_lds_kernel<true>, dim3(blocks), dim3(NTHR), LDS_BYTES, s, a, fw, fh, fc, MT, NT);
-  else
-    hipLaunchKernelGGL(wgrad_lds_kernel<false>, dim3(blocks), dim3(NTHR), LDS_BYTES, s, a, fw, fh, fc, MT, NT);
+  const dim3 g((uint32_t)MT * NT * a.splits * a.C), b(NTHR);
+  if (label) *label = wide ? "conv_wgrad<bf16,256x256,w8,lds>" : "conv_wgrad<bf16,128x256,w8,lds>";
+#define WG_GO(BM, BN, WM, WN, T) \
+  hipLaunchKernelGGL((WG_K(BM, BN, WM, WN, T)), g, b, (Cfg<BM, BN, WM, WN>::LDS_BYTES), s, a, fw, fh, fc, MT, NT)
+  const bool t1 = a.taps == 1;
+  if (wide) {
+    if (t1) WG_GO(256, 256, 2, 4, true); else WG_GO(256, 256, 2, 4, false);
+  } else {
+    if (t1) WG_GO(128, 256, 2, 4, true); else WG_GO(128, 256, 2, 4, false);
+  }
+#undef WG_GO
+#undef WG_ATTR
+#undef WG_K
   return hipGetLastError();
 }
