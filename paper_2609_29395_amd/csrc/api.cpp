@@ -207,16 +207,17 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
       const int nwc = (i == 0 && p.col0) ? p.Kc : 9 * l.Ci;
       int splits;
       if (wgrad_lds_ok(p.dtype, l.Co, (i == 0 && p.col0) ? p.Kc : l.Ci)) {
-        // one 8-wave workgroup per CU: pick the split count that minimises
-        // (rounds of 256 workgroups) x (k tiles per workgroup + the cost of
-        // writing and re-reading a partial tile, about 16 k tiles)
-        int bk;
-        wgrad_lds_tile(l.Co, &bm, &bn, &bk);
+        // pick the split count that minimises (rounds of 256 x per_cu
+        // workgroups) x (k tiles per workgroup + the cost of writing and
+        // re-reading a partial tile, about 16 k tiles)
+        int bk, per_cu;
+        wgrad_lds_tile(l.Co, &bm, &bn, &bk, &per_cu);
         const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
+        const int64_t slots = 256 * (int64_t)per_cu;
         int64_t best = -1;
         splits = 1;
         for (int sp = 1; sp <= std::min(16, nkt); ++sp) {
-          const int64_t rounds = (tiles * sp + 255) / 256;
+          const int64_t rounds = (tiles * sp + slots - 1) / slots;
           const int64_t cost = rounds * ((nkt + sp - 1) / sp + (sp > 1 ? 16 : 0));
           if (best < 0 || cost < best) best = cost, splits = sp;
         }

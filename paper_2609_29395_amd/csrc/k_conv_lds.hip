@@ -14,7 +14,7 @@
 // hit all banks.  The fragment reads are inline asm with explicit lgkmcnt
 // waits so the compiler does not wait for every outstanding copy.
 //
-// The workgroup tile is large (256 pixels x up to 256 channels) because the
+// The workgroup tile is large (256 pixels x 32 .. 256 channels) because the
 // per-CU vector-memory path, not LDS or the MFMA pipe, bounds a k tile: the
 // bytes copied per MFMA fall as the tile grows.  Two LDS stages: the copy of
 // tile kt+1 is issued right after the barrier that starts tile kt and has
@@ -45,14 +45,16 @@ constexpr int kBufferFlags = 0x00020000;
 template <int BN, int WM, int WN> struct Cfg {
   static constexpr int A_BYTES = BM * ROW, B_BYTES = BN * ROW;
   static constexpr int STAGE = A_BYTES + B_BYTES;
-  static constexpr int SA = A_BYTES / (NTHR * 16), SB = B_BYTES / (NTHR * 16);  // copies per thread
+  // copies per thread; a narrow weight tile leaves the last B copy to the
+  // first waves only
+  static constexpr int SA = A_BYTES / (NTHR * 16), SB = (B_BYTES + NTHR * 16 - 1) / (NTHR * 16);
   static constexpr int TM = BM / WM / 16, TN = BN / WN / 16;                    // fragments per wave
   static constexpr int WNW = BN / WN;                                            // wave tile width
   static constexpr int EP_LD = WNW + 4;  // floats per staged epilogue row
   static constexpr int EP_BYTES = 8 * 64 * EP_LD * 4;
   static constexpr int LDS_BYTES = 2 * STAGE > EP_BYTES ? 2 * STAGE : EP_BYTES;
   static_assert(WM * WN * 64 == NTHR, "8 waves");
-  static_assert(SA * NTHR * 16 == A_BYTES && SB * NTHR * 16 == B_BYTES, "copies must tile the stage");
+  static_assert(SA * NTHR * 16 == A_BYTES && B_BYTES % 1024 == 0, "copies must tile the stage");
   static_assert(TM % 4 == 0 && TN >= 1, "wave tile: multiples of 64 pixels");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 };
@@ -107,8 +109,8 @@ __device__ __forceinline__ uint32_t f2bf(float f) { return (uint32_t)f32_to_bf16
 // kernel template makes the host compilation pass drop the kernel's launch
 // stub without a diagnostic.
 template <typename CF, bool TAPS1>
-__device__ __forceinline__ void issue_tile(int kt, char *stage0, const ConvArgs &a, FastDiv fd_c, const void *src,
-                                           const void *wt, const int *achunk, const int *arowoff,
+__device__ __forceinline__ void issue_tile(int kt, char *stage0, int wave, const ConvArgs &a, FastDiv fd_c,
+                                           const void *src, const void *wt, const int *achunk, const int *arowoff,
                                            const uint32_t *amask, const uint32_t *boff) {
   const __amdgpu_buffer_rsrc_t rsa = rsrc(src, (uint32_t)(a.src_rs * 2));
   const __amdgpu_buffer_rsrc_t rsb = rsrc(wt, (uint32_t)((int64_t)a.N * a.Kp * 2));
@@ -132,8 +134,9 @@ __device__ __forceinline__ void issue_tile(int kt, char *stage0, const ConvArgs 
   const uint32_t kb = (uint32_t)(kt * BK * 2);
 #pragma unroll
   for (int q = 0; q < CF::SB; ++q)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, LDS_PTR(sa + CF::A_BYTES + q * NTHR * 16), 16,
-                                             boff[q] == kOob ? kOob : boff[q] + kb, 0, 0, 0);
+    if (q * NTHR * 16 + wave * 1024 < CF::B_BYTES)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, LDS_PTR(sa + CF::A_BYTES + q * NTHR * 16), 16,
+                                               boff[q] == kOob ? kOob : boff[q] + kb, 0, 0, 0);
 }
 
 template <int BN, int WM, int WN, int EPI, bool TAPS1>
@@ -188,14 +191,14 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
     const int byte = q * NTHR * 16 + wave * 1024 + lane * 16;
     const int row = byte / ROW;
     const int n = n0 + row;
-    boff[q] = n < a.N ? ((uint32_t)n * (uint32_t)a.Kp + (uint32_t)(8 * (((byte % ROW) / 16) ^ swz(row)))) * 2u
+    boff[q] = (n < a.N && byte < CF::B_BYTES) ? ((uint32_t)n * (uint32_t)a.Kp + (uint32_t)(8 * (((byte % ROW) / 16) ^ swz(row)))) * 2u
                       : kOob;
   }
 
   const int nk = a.Kp / BK;
   char *stage0 = smem + wave * 1024;
   auto issue = [&](int kt) {
-    issue_tile<CF, TAPS1>(kt, stage0, a, fd_c, src, wt, achunk, arowoff, amask, boff);
+    issue_tile<CF, TAPS1>(kt, stage0, wave, a, fd_c, src, wt, achunk, arowoff, amask, boff);
   };
 
   // fragment read addresses: lane (li, lg) reads row li of a 16-row block,
@@ -320,7 +323,7 @@ void grid(const ConvArgs &a, int *MT, int *NT) {
 }  // namespace
 
 bool conv_lds_ok(int dtype, const ConvArgs &a) {
-  return dtype == GCPSL_BF16 && a.N > 64 && a.N % 8 == 0 && a.Csrc % 8 == 0 && a.Kp % BK == 0;
+  return dtype == GCPSL_BF16 && a.N % 8 == 0 && a.Csrc % 8 == 0 && a.Kp % BK == 0;
 }
 
 // Every instantiation is named in this (non-template) function, which is
@@ -340,27 +343,33 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   if (!attr) {
     CONV_LDS_ATTR(256, 2, 4)
     CONV_LDS_ATTR(128, 4, 2)
+    CONV_LDS_ATTR(64, 4, 2)
+    CONV_LDS_ATTR(32, 4, 2)
     attr = true;
   }
-  const bool wide = a.N > 128;
+  // the narrowest weight tile that covers N (256 beyond 128)
+  const int bn = a.N > 128 ? 256 : a.N > 64 ? 128 : a.N > 32 ? 64 : 32;
   int MT, NT;
-  if (wide) grid<256, 2, 4>(a, &MT, &NT);
-  else grid<128, 4, 2>(a, &MT, &NT);
+  if (bn == 256) grid<256, 2, 4>(a, &MT, &NT);
+  else if (bn == 128) grid<128, 4, 2>(a, &MT, &NT);
+  else if (bn == 64) grid<64, 4, 2>(a, &MT, &NT);
+  else grid<32, 4, 2>(a, &MT, &NT);
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Csrc);
   const dim3 g((uint32_t)MT * NT * a.C), b(NTHR);
   if (label)
-    *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + (wide ? "<bf16,256x256x64,w8,lds>"
-                                                                              : "<bf16,256x128x64,w8,lds>");
+    *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16,256x" + std::to_string(bn) +
+             "x64,w8,lds>";
 #define CONV_LDS_GO(BN, WM, WN, E, T) \
   hipLaunchKernelGGL((CONV_LDS_K(BN, WM, WN, E, T)), g, b, (Cfg<BN, WM, WN>::LDS_BYTES), s, a, fw, fh, fc, MT, NT)
+#define CONV_LDS_SEL(BN, WM, WN)                                                                          \
+  if (fwd) { if (t1) CONV_LDS_GO(BN, WM, WN, EPI_FWD, true); else CONV_LDS_GO(BN, WM, WN, EPI_FWD, false); }   \
+  else { if (t1) CONV_LDS_GO(BN, WM, WN, EPI_DGRAD, true); else CONV_LDS_GO(BN, WM, WN, EPI_DGRAD, false); }
   const bool fwd = a.epi == EPI_FWD, t1 = a.taps == 1;
-  if (wide) {
-    if (fwd) { if (t1) CONV_LDS_GO(256, 2, 4, EPI_FWD, true); else CONV_LDS_GO(256, 2, 4, EPI_FWD, false); }
-    else { if (t1) CONV_LDS_GO(256, 2, 4, EPI_DGRAD, true); else CONV_LDS_GO(256, 2, 4, EPI_DGRAD, false); }
-  } else {
-    if (fwd) { if (t1) CONV_LDS_GO(128, 4, 2, EPI_FWD, true); else CONV_LDS_GO(128, 4, 2, EPI_FWD, false); }
-    else { if (t1) CONV_LDS_GO(128, 4, 2, EPI_DGRAD, true); else CONV_LDS_GO(128, 4, 2, EPI_DGRAD, false); }
-  }
+  if (bn == 256) { CONV_LDS_SEL(256, 2, 4) }
+  else if (bn == 128) { CONV_LDS_SEL(128, 4, 2) }
+  else if (bn == 64) { CONV_LDS_SEL(64, 4, 2) }
+  else { CONV_LDS_SEL(32, 4, 2) }
+#undef CONV_LDS_SEL
 #undef CONV_LDS_GO
 #undef CONV_LDS_ATTR
 #undef CONV_LDS_K

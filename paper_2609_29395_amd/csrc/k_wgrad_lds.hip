@@ -44,19 +44,33 @@ constexpr int kDead = 1 << 30;  // row index that fails every pixel test
 
 template <int BM, int BN, int WM, int WN> struct Cfg {
   static constexpr int ROWA = BM * 2, ROWB = BN * 2;  // bytes per LDS row
+  static constexpr int CHA = ROWA / 16, CHB = ROWB / 16;  // 16-byte chunks per row
   static constexpr int A_BYTES = BK * ROWA, B_BYTES = BK * ROWB;
   static constexpr int STAGE = A_BYTES + B_BYTES;
   static constexpr int SA = A_BYTES / (NTHR * 16), SB = B_BYTES / (NTHR * 16);  // copies per thread
   static constexpr int TM = BM / WM / 16, TN = BN / WN / 16;                    // fragments per wave
-  static constexpr int BPW = TM / WN;                                            // bias fragments per wave
+  static constexpr int BPW = (TM + WN - 1) / WN;  // bias fragments per wave: those with tm % WN == wn
   static constexpr int LDS_BYTES = 2 * STAGE;
+  static constexpr int WNS = WN;
   static_assert(WM * WN * 64 == NTHR, "8 waves");
   static_assert(SA * NTHR * 16 == A_BYTES && SB * NTHR * 16 == B_BYTES, "copies must tile the stage");
-  static_assert(BPW >= 1 && BPW * WN == TM, "bias fragments split evenly over the waves of a row");
+  static_assert(TM % WN == 0 || WN % TM == 0, "bias fragments split evenly over the waves of a row");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 };
 
-__device__ __forceinline__ int swz(int row) { return ((row & 3) | ((row >> 1) & 4)) << 1; }
+// XOR applied to the 16-byte chunk index of LDS row `row` (CH chunks per
+// row).  A transposing read touches 16 rows (4 per lane group, lane groups 8
+// rows apart) at the same two chunks; the XOR spreads them so that each bank
+// holds exactly two of the 16 pieces, and it depends only on row bits 0, 1
+// and 3, which are the same for both halves of a fragment and for every k
+// group.  Rows of 256 bytes or more start on bank 0; 128-byte rows alternate
+// halves of the banks, so there the row's low bit already separates pairs.
+template <int CH>
+__device__ __forceinline__ int swz(int row) {
+  static_assert(CH == 8 || CH >= 16, "row width");
+  if constexpr (CH >= 16) return ((row & 3) | ((row >> 1) & 4)) << 1;
+  else return (((row >> 1) & 1) | ((row >> 2) & 2)) << 1;
+}
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) {
   const uint64_t p = reinterpret_cast<uint64_t>(base);
@@ -118,12 +132,12 @@ __device__ __forceinline__ void issue_tile(int kt, char *stage0, const WgradArgs
 }
 
 // Fragments of k group KG (32 pixels) of the stage at byte address st, then
-// their MFMAs; with bias, g fragments b0 .. b0+BPW-1 also meet a ones
-// fragment (column sums of g).
+// their MFMAs; with bias, the g fragments tm with tm % WN == wn also meet a
+// ones fragment (column sums of g).
 template <typename CF, int KG>
 __device__ __forceinline__ void kgroup(f32x4_t (&acc)[CF::TM][CF::TN], f32x4_t (&bacc)[CF::BPW],
                                        const uint32_t (&ra)[CF::TM], const uint32_t (&rb)[CF::TN], uint32_t st,
-                                       bool bias, int b0) {
+                                       bool bias, int wn) {
   constexpr int TM = CF::TM, TN = CF::TN;
   u32x4 a[TM], b[TN];
 #pragma unroll
@@ -144,9 +158,7 @@ __device__ __forceinline__ void kgroup(f32x4_t (&acc)[CF::TM][CF::TN], f32x4_t (
     const u32x4 ones = u32x4{one2, one2, one2, one2};
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int i = 0; i < CF::BPW; ++i)
-        if (tm == b0 + i) mma(bacc[i], a[tm], ones);
+      if (tm % CF::WNS == wn) mma(bacc[tm / CF::WNS], a[tm], ones);
   }
 }
 
@@ -185,7 +197,7 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
   for (int q = 0; q < SA; ++q) {
     const int byte = q * NTHR * 16 + wave * 1024 + lane * 16;
     const int row = byte / CF::ROWA;
-    const int co = m0 + 8 * (((byte % CF::ROWA) / 16) ^ swz(row));
+    const int co = m0 + 8 * (((byte % CF::ROWA) / 16) ^ swz<CF::CHA>(row));
     arow[q] = co < a.Co ? row : kDead;
     acol[q] = co;
   }
@@ -194,7 +206,7 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
   for (int q = 0; q < SB; ++q) {
     const int byte = q * NTHR * 16 + wave * 1024 + lane * 16;
     const int row = byte / CF::ROWB;
-    const int kk = n0 + 8 * (((byte % CF::ROWB) / 16) ^ swz(row));
+    const int kk = n0 + 8 * (((byte % CF::ROWB) / 16) ^ swz<CF::CHB>(row));
     brow[q] = kk < NW ? row : kDead;
     if constexpr (TAPS1) {
       bci[q] = kk; bdh[q] = 0; bdw[q] = 0;
@@ -212,15 +224,15 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
   const int j = lane & 15, lg = lane >> 4;
   const int wm = wave / WN, wn = wave % WN;
   const int frow = 8 * lg + (j >> 2);
-  const int fsw = swz(frow);
+  const int fsa = swz<CF::CHA>(frow), fsb = swz<CF::CHB>(frow);
   const int half = ((j & 3) >> 1);
   uint32_t ra[TM], rb[TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
-    ra[i] = (uint32_t)(frow * CF::ROWA + (((2 * (wm * TM + i) + half) ^ fsw) * 16) + (j & 1) * 8);
+    ra[i] = (uint32_t)(frow * CF::ROWA + (((2 * (wm * TM + i) + half) ^ fsa) * 16) + (j & 1) * 8);
 #pragma unroll
   for (int i = 0; i < TN; ++i)
-    rb[i] = (uint32_t)(CF::A_BYTES + frow * CF::ROWB + (((2 * (wn * TN + i) + half) ^ fsw) * 16) + (j & 1) * 8);
+    rb[i] = (uint32_t)(CF::A_BYTES + frow * CF::ROWB + (((2 * (wn * TN + i) + half) ^ fsb) * 16) + (j & 1) * 8);
   const uint32_t lds0 = (uint32_t)(size_t)LDS_PTR(smem);
 
   f32x4_t acc[TM][TN];
@@ -231,7 +243,6 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
   f32x4_t bacc[BPW];
 #pragma unroll
   for (int i = 0; i < BPW; ++i) bacc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  const int b0 = wn * BPW;
 
   issue_tile<CF, TAPS1>(0, stage0, a, fd_w, fd_h, G, X, M, p_begin, p_end, arow, acol, brow, bci, bdh, bdw);
   for (int kt = 0; kt < nk; ++kt) {
@@ -243,8 +254,8 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
       issue_tile<CF, TAPS1>(kt + 1, stage0, a, fd_w, fd_h, G, X, M, p_begin, p_end, arow, acol, brow, bci, bdh,
                             bdw);
     const uint32_t st = lds0 + (uint32_t)((kt & 1) * CF::STAGE);
-    kgroup<CF, 0>(acc, bacc, ra, rb, st, do_bias, b0);
-    kgroup<CF, 1>(acc, bacc, ra, rb, st, do_bias, b0);
+    kgroup<CF, 0>(acc, bacc, ra, rb, st, do_bias, wn);
+    kgroup<CF, 1>(acc, bacc, ra, rb, st, do_bias, wn);
   }
   // nk == 0 leaves the first copy in flight
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -263,25 +274,35 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
   }
   if (do_bias && j == 0) {
 #pragma unroll
-    for (int i = 0; i < BPW; ++i)
+    for (int i = 0; i < BPW; ++i) {
+      const int tm = wn + WN * i;
+      if (tm >= TM) break;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int co = m0 + (wm * TM + b0 + i) * 16 + lg * 4 + r;
+        const int co = m0 + (wm * TM + tm) * 16 + lg * 4 + r;
         if (co < a.Co) a.db[split * a.db_ss + rep * a.db_rs + co] = bacc[i][r];
       }
+    }
   }
 }
 
 }  // namespace
 
 bool wgrad_lds_ok(int dtype, int Co, int Ci) {
-  return dtype == GCPSL_BF16 && Co >= 128 && Co % 8 == 0 && Ci % 8 == 0;
+  return dtype == GCPSL_BF16 && Co >= 64 && Co % 8 == 0 && Ci % 8 == 0;
 }
 
-void wgrad_lds_tile(int Co, int *bm, int *bn, int *bk) {
-  *bm = Co > 128 ? 256 : 128;
-  *bn = 256;
+// Tile of a layer (rows = output channels, columns of the im2col operand)
+// and how many such workgroups one CU holds (LDS-limited).
+void wgrad_lds_tile(int Co, int *bm, int *bn, int *bk, int *per_cu) {
   *bk = BK;
+  if (Co > 128) {
+    *bm = 256; *bn = 256; *per_cu = 160 * 1024 / Cfg<256, 256, 2, 4>::LDS_BYTES;
+  } else if (Co > 64) {
+    *bm = 128; *bn = 256; *per_cu = 160 * 1024 / Cfg<128, 256, 2, 4>::LDS_BYTES;
+  } else {
+    *bm = 64; *bn = 128; *per_cu = 160 * 1024 / Cfg<64, 128, 1, 8>::LDS_BYTES;
+  }
 }
 
 // Every instantiation is named in this (non-template) function.
@@ -298,22 +319,25 @@ hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *labe
   if (!attr) {
     WG_ATTR(256, 256, 2, 4)
     WG_ATTR(128, 256, 2, 4)
+    WG_ATTR(64, 128, 1, 8)
     attr = true;
   }
-  const bool wide = a.Co > 128;
-  const int BM = wide ? 256 : 128, BN = 256;
+  int BM, BN, bk, per_cu;
+  wgrad_lds_tile(a.Co, &BM, &BN, &bk, &per_cu);
   const int NW = a.taps == 1 ? a.Ci : 9 * a.Ci;
   const int MT = (a.Co + BM - 1) / BM, NT = (NW + BN - 1) / BN;
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Ci);
   const dim3 g((uint32_t)MT * NT * a.splits * a.C), b(NTHR);
-  if (label) *label = wide ? "conv_wgrad<bf16,256x256,w8,lds>" : "conv_wgrad<bf16,128x256,w8,lds>";
+  if (label) *label = "conv_wgrad<bf16," + std::to_string(BM) + "x" + std::to_string(BN) + ",w8,lds>";
 #define WG_GO(BM, BN, WM, WN, T) \
   hipLaunchKernelGGL((WG_K(BM, BN, WM, WN, T)), g, b, (Cfg<BM, BN, WM, WN>::LDS_BYTES), s, a, fw, fh, fc, MT, NT)
   const bool t1 = a.taps == 1;
-  if (wide) {
+  if (BM == 256) {
     if (t1) WG_GO(256, 256, 2, 4, true); else WG_GO(256, 256, 2, 4, false);
-  } else {
+  } else if (BM == 128) {
     if (t1) WG_GO(128, 256, 2, 4, true); else WG_GO(128, 256, 2, 4, false);
+  } else {
+    if (t1) WG_GO(64, 128, 1, 8, true); else WG_GO(64, 128, 1, 8, false);
   }
 #undef WG_GO
 #undef WG_ATTR
