@@ -6,7 +6,7 @@
 //
 // (dgrad is a forward conv of g with the flipped, transposed weights Wd).
 // Both operands are k-contiguous: a k tile (64 values, 128 bytes per row) of
-// 256 pixel rows (gathered per kernel tap from the NHWC activation) and of BN
+// BM pixel rows (gathered per kernel tap from the NHWC activation) and of BN
 // weight rows is copied into LDS by buffer loads that write LDS directly;
 // taps outside the image, pixels past the batch and weight rows past N read
 // zero through the buffer range check.  Rows are XOR-swizzled in 16-byte
@@ -24,7 +24,7 @@
 // so each lane accumulates 4 consecutive output channels of one pixel.  The
 // epilogue stages the fp32 tile through LDS, 64 pixel rows per pass, then
 // works on 8 consecutive channels per lane: 16-byte loads of the residual and
-// mask, 16-byte stores.
+// mask (all of a pass issued together), 16-byte stores.
 #include <utility>
 
 #include "runtime.h"
@@ -37,12 +37,13 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
 
-constexpr int BM = 256, BK = 64, NTHR = 512;
+constexpr int BK = 64, NTHR = 512;
 constexpr int ROW = BK * 2;  // bytes per LDS row
 constexpr uint32_t kOob = 0x80000000u;
 constexpr int kBufferFlags = 0x00020000;
 
-template <int BN, int WM, int WN> struct Cfg {
+template <int BM_, int BN, int WM, int WN> struct Cfg {
+  static constexpr int BM = BM_;
   static constexpr int A_BYTES = BM * ROW, B_BYTES = BN * ROW;
   static constexpr int STAGE = A_BYTES + B_BYTES;
   // copies per thread; a narrow weight tile leaves the last B copy to the
@@ -139,10 +140,10 @@ __device__ __forceinline__ void issue_tile(int kt, char *stage0, int wave, const
                                                boff[q] == kOob ? kOob : boff[q] + kb, 0, 0, 0);
 }
 
-template <int BN, int WM, int WN, int EPI, bool TAPS1>
+template <int BM, int BN, int WM, int WN, int EPI, bool TAPS1>
 __global__ void __launch_bounds__(NTHR)
 conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
-  using CF = Cfg<BN, WM, WN>;
+  using CF = Cfg<BM, BN, WM, WN>;
   constexpr int SA = CF::SA, SB = CF::SB, TM = CF::TM, TN = CF::TN;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -256,6 +257,8 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   bf16_t *out = reinterpret_cast<bf16_t *>(a.out) + rep * a.out_rs;
   const bf16_t *res = a.res ? reinterpret_cast<const bf16_t *>(a.res) + rep * a.out_rs : nullptr;
   const bf16_t *msk = a.mask ? reinterpret_cast<const bf16_t *>(a.mask) + rep * a.out_rs : nullptr;
+  const __amdgpu_buffer_rsrc_t rsr = rsrc(res ? res : out, (uint32_t)(a.out_rs * 2));
+  const __amdgpu_buffer_rsrc_t rsm = rsrc(msk ? msk : out, (uint32_t)(a.out_rs * 2));
 #pragma unroll
   for (int pass = 0; pass < TM / 4; ++pass) {
 #pragma unroll
@@ -266,46 +269,52 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    if (nok) {
-#pragma unroll 2
-      for (int i = 0; i < SEGS; ++i) {
-        const int r = lane / SEGS + RSTEP * i;  // pixel row of this pass
-        const int m = m0 + wm * TM * 16 + pass * 64 + r;
-        if (m >= M) break;
-        const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(ep + r * CF::EP_LD + 8 * seg);
-        const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(ep + r * CF::EP_LD + 8 * seg + 4);
-        float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        const int64_t o = (int64_t)m * a.N + n;
-        if (res) {
-          const uint4 rv = *reinterpret_cast<const uint4 *>(res + o);
-          const uint32_t rw[4] = {rv.x, rv.y, rv.z, rv.w};
+    // every residual and mask load of the pass is issued before any is
+    // used; rows past M (and channels past N) read zero and store nothing
+    uint4 rv[SEGS], mv[SEGS];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            v[2 * e] += bf2f(rw[e] & 0xffffu);
-            v[2 * e + 1] += bf2f(rw[e] >> 16);
-          }
+    for (int i = 0; i < SEGS; ++i) {
+      const int m = m0 + wm * TM * 16 + pass * 64 + lane / SEGS + RSTEP * i;
+      const uint32_t off = (nok && m < M) ? (uint32_t)((int64_t)m * a.N + n) * 2u : kOob;
+      rv[i] = res ? __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsr, off, 0, 0))
+                  : make_uint4(0, 0, 0, 0);
+      if constexpr (EPI == EPI_DGRAD)
+        mv[i] = msk ? __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsm, off, 0, 0))
+                    : make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
+    }
+#pragma unroll
+    for (int i = 0; i < SEGS; ++i) {
+      const int r = lane / SEGS + RSTEP * i;  // pixel row of this pass
+      const int m = m0 + wm * TM * 16 + pass * 64 + r;
+      const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(ep + r * CF::EP_LD + 8 * seg);
+      const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(ep + r * CF::EP_LD + 8 * seg + 4);
+      float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      if (res) {
+        const uint32_t rw[4] = {rv[i].x, rv[i].y, rv[i].z, rv[i].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[2 * e] += bf2f(rw[e] & 0xffffu);
+          v[2 * e + 1] += bf2f(rw[e] >> 16);
         }
-        if constexpr (EPI == EPI_FWD) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e] + bias[e], 0.f);
-        } else {
-          if (msk) {
-            const uint4 mv = *reinterpret_cast<const uint4 *>(msk + o);
-            const uint32_t mw[4] = {mv.x, mv.y, mv.z, mv.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              if (!(bf2f(mw[e] & 0xffffu) > 0.f)) v[2 * e] = 0.f;
-              if (!(bf2f(mw[e] >> 16) > 0.f)) v[2 * e + 1] = 0.f;
-            }
-          }
-        }
-        uint4 ov;
-        ov.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
-        ov.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
-        ov.z = f2bf(v[4]) | (f2bf(v[5]) << 16);
-        ov.w = f2bf(v[6]) | (f2bf(v[7]) << 16);
-        *reinterpret_cast<uint4 *>(out + o) = ov;
       }
+      if constexpr (EPI == EPI_FWD) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e] + bias[e], 0.f);
+      } else {
+        // without a mask source every value passes (ones)
+        const uint32_t mw[4] = {mv[i].x, mv[i].y, mv[i].z, mv[i].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (!(bf2f(mw[e] & 0xffffu) > 0.f)) v[2 * e] = 0.f;
+          if (!(bf2f(mw[e] >> 16) > 0.f)) v[2 * e + 1] = 0.f;
+        }
+      }
+      uint4 ov;
+      ov.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
+      ov.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
+      ov.z = f2bf(v[4]) | (f2bf(v[5]) << 16);
+      ov.w = f2bf(v[6]) | (f2bf(v[7]) << 16);
+      if (nok && m < M) *reinterpret_cast<uint4 *>(out + (int64_t)m * a.N + n) = ov;
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -313,7 +322,7 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   }
 }
 
-template <int BN, int WM, int WN>
+template <int BM, int BN>
 void grid(const ConvArgs &a, int *MT, int *NT) {
   const int M = a.Bt * a.H * a.W;
   *MT = (M + BM - 1) / BM;
@@ -329,46 +338,48 @@ bool conv_lds_ok(int dtype, const ConvArgs &a) {
 // Every instantiation is named in this (non-template) function, which is
 // what makes the compiler emit the host-side launch stubs.
 hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label) {
-#define CONV_LDS_K(BN, WM, WN, E, T) conv_lds_kernel<BN, WM, WN, E, T>
-#define CONV_LDS_ATTR(BN, WM, WN)                                                                       \
-  for (const void *f : {reinterpret_cast<const void *>(&CONV_LDS_K(BN, WM, WN, EPI_FWD, false)),           \
-                        reinterpret_cast<const void *>(&CONV_LDS_K(BN, WM, WN, EPI_FWD, true)),            \
-                        reinterpret_cast<const void *>(&CONV_LDS_K(BN, WM, WN, EPI_DGRAD, false)),         \
-                        reinterpret_cast<const void *>(&CONV_LDS_K(BN, WM, WN, EPI_DGRAD, true))}) {       \
+#define CONV_LDS_K(BM, BN, WM, WN, E, T) conv_lds_kernel<BM, BN, WM, WN, E, T>
+#define CONV_LDS_ATTR(BM, BN, WM, WN)                                                                   \
+  for (const void *f : {reinterpret_cast<const void *>(&CONV_LDS_K(BM, BN, WM, WN, EPI_FWD, false)),       \
+                        reinterpret_cast<const void *>(&CONV_LDS_K(BM, BN, WM, WN, EPI_FWD, true)),        \
+                        reinterpret_cast<const void *>(&CONV_LDS_K(BM, BN, WM, WN, EPI_DGRAD, false)),     \
+                        reinterpret_cast<const void *>(&CONV_LDS_K(BM, BN, WM, WN, EPI_DGRAD, true))}) {   \
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,               \
-                                             Cfg<BN, WM, WN>::LDS_BYTES);                                 \
+                                             Cfg<BM, BN, WM, WN>::LDS_BYTES);                             \
     if (e != hipSuccess) return e;                                                                        \
   }
   static bool attr = false;
   if (!attr) {
-    CONV_LDS_ATTR(256, 2, 4)
-    CONV_LDS_ATTR(128, 4, 2)
-    CONV_LDS_ATTR(64, 4, 2)
-    CONV_LDS_ATTR(32, 4, 2)
+    CONV_LDS_ATTR(256, 256, 2, 4)
+    CONV_LDS_ATTR(256, 128, 4, 2)
+    CONV_LDS_ATTR(256, 64, 4, 2)
+    CONV_LDS_ATTR(256, 32, 4, 2)
     attr = true;
   }
   // the narrowest weight tile that covers N (256 beyond 128)
   const int bn = a.N > 128 ? 256 : a.N > 64 ? 128 : a.N > 32 ? 64 : 32;
+  const int bm = 256;
   int MT, NT;
-  if (bn == 256) grid<256, 2, 4>(a, &MT, &NT);
-  else if (bn == 128) grid<128, 4, 2>(a, &MT, &NT);
-  else if (bn == 64) grid<64, 4, 2>(a, &MT, &NT);
-  else grid<32, 4, 2>(a, &MT, &NT);
+  if (bn == 256) grid<256, 256>(a, &MT, &NT);
+  else if (bn == 128) grid<256, 128>(a, &MT, &NT);
+  else if (bn == 64) grid<256, 64>(a, &MT, &NT);
+  else grid<256, 32>(a, &MT, &NT);
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Csrc);
   const dim3 g((uint32_t)MT * NT * a.C), b(NTHR);
   if (label)
-    *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16,256x" + std::to_string(bn) +
-             "x64,w8,lds>";
-#define CONV_LDS_GO(BN, WM, WN, E, T) \
-  hipLaunchKernelGGL((CONV_LDS_K(BN, WM, WN, E, T)), g, b, (Cfg<BN, WM, WN>::LDS_BYTES), s, a, fw, fh, fc, MT, NT)
-#define CONV_LDS_SEL(BN, WM, WN)                                                                          \
-  if (fwd) { if (t1) CONV_LDS_GO(BN, WM, WN, EPI_FWD, true); else CONV_LDS_GO(BN, WM, WN, EPI_FWD, false); }   \
-  else { if (t1) CONV_LDS_GO(BN, WM, WN, EPI_DGRAD, true); else CONV_LDS_GO(BN, WM, WN, EPI_DGRAD, false); }
+    *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16," + std::to_string(bm) + "x" +
+             std::to_string(bn) + "x64,w8,lds>";
+#define CONV_LDS_GO(BM, BN, WM, WN, E, T)                                                                  \
+  hipLaunchKernelGGL((CONV_LDS_K(BM, BN, WM, WN, E, T)), g, b, (Cfg<BM, BN, WM, WN>::LDS_BYTES), s, a, fw, fh, \
+                     fc, MT, NT)
+#define CONV_LDS_SEL(BM, BN, WM, WN)                                                                        \
+  if (fwd) { if (t1) CONV_LDS_GO(BM, BN, WM, WN, EPI_FWD, true); else CONV_LDS_GO(BM, BN, WM, WN, EPI_FWD, false); } \
+  else { if (t1) CONV_LDS_GO(BM, BN, WM, WN, EPI_DGRAD, true); else CONV_LDS_GO(BM, BN, WM, WN, EPI_DGRAD, false); }
   const bool fwd = a.epi == EPI_FWD, t1 = a.taps == 1;
-  if (bn == 256) { CONV_LDS_SEL(256, 2, 4) }
-  else if (bn == 128) { CONV_LDS_SEL(128, 4, 2) }
-  else if (bn == 64) { CONV_LDS_SEL(64, 4, 2) }
-  else { CONV_LDS_SEL(32, 4, 2) }
+  if (bn == 256) { CONV_LDS_SEL(256, 256, 2, 4) }
+  else if (bn == 128) { CONV_LDS_SEL(256, 128, 4, 2) }
+  else if (bn == 64) { CONV_LDS_SEL(256, 64, 4, 2) }
+  else { CONV_LDS_SEL(256, 32, 4, 2) }
 #undef CONV_LDS_SEL
 #undef CONV_LDS_GO
 #undef CONV_LDS_ATTR
