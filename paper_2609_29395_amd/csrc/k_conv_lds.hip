@@ -14,7 +14,7 @@
 // hit all banks.  The fragment reads are inline asm with explicit lgkmcnt
 // waits so the compiler does not wait for every outstanding copy.
 //
-// The workgroup tile is large (256 pixels x 32 .. 256 channels) because the
+// The workgroup tile is large (up to 256 pixels x 256 channels) because the
 // per-CU vector-memory path, not LDS or the MFMA pipe, bounds a k tile: the
 // bytes copied per MFMA fall as the tile grows.  Two LDS stages: the copy of
 // tile kt+1 is issued right after the barrier that starts tile kt and has
@@ -116,21 +116,36 @@ __device__ __forceinline__ void issue_tile(int kt, char *stage0, int wave, const
   const __amdgpu_buffer_rsrc_t rsa = rsrc(src, (uint32_t)(a.src_rs * 2));
   const __amdgpu_buffer_rsrc_t rsb = rsrc(wt, (uint32_t)((int64_t)a.N * a.Kp * 2));
   char *sa = stage0 + (kt & 1) * CF::STAGE;
+  if (!TAPS1 && a.Csrc % BK == 0) {
+    // the whole k tile lies in one kernel tap: tap and its offset are
+    // workgroup-uniform
+    const int cpt = a.Csrc / BK;  // k tiles per tap
+    const int rs = __builtin_amdgcn_readfirstlane(kt / cpt);
+    const int r = (rs * 11) >> 5;  // rs / 3 for rs < 9
+    const int tap = __builtin_amdgcn_readfirstlane(((r - 1) * a.W + (rs - 3 * r - 1)) * a.Csrc +
+                                                   (kt - rs * cpt) * BK);
 #pragma unroll
-  for (int q = 0; q < CF::SA; ++q) {
-    const int k = kt * BK + 8 * achunk[q];
-    uint32_t off;
-    if constexpr (TAPS1) {
-      off = ((amask[q] != 0u) & (k < a.K)) ? (uint32_t)(arowoff[q] + k) * 2u : kOob;
-    } else {
-      // k past K has rs >= 9, outside the mask
-      const int rs = (int)fdiv((uint32_t)k, fd_c);
-      const int c = k - rs * a.Csrc;
-      const int r = (rs * 11) >> 5;  // rs / 3 for rs < 9
-      const int tap = ((r - 1) * a.W + (rs - 3 * r - 1)) * a.Csrc + c;
-      off = ((amask[q] >> min(rs, 31)) & 1u) ? (uint32_t)(arowoff[q] + tap) * 2u : kOob;
+    for (int q = 0; q < CF::SA; ++q) {
+      const uint32_t off = ((amask[q] >> rs) & 1u) ? (uint32_t)(arowoff[q] + tap + 8 * achunk[q]) * 2u : kOob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(sa + q * NTHR * 16), 16, off, 0, 0, 0);
     }
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(sa + q * NTHR * 16), 16, off, 0, 0, 0);
+  } else {
+#pragma unroll
+    for (int q = 0; q < CF::SA; ++q) {
+      const int k = kt * BK + 8 * achunk[q];
+      uint32_t off;
+      if constexpr (TAPS1) {
+        off = ((amask[q] != 0u) & (k < a.K)) ? (uint32_t)(arowoff[q] + k) * 2u : kOob;
+      } else {
+        // k past K has rs >= 9, outside the mask
+        const int rs = (int)fdiv((uint32_t)k, fd_c);
+        const int c = k - rs * a.Csrc;
+        const int r = (rs * 11) >> 5;  // rs / 3 for rs < 9
+        const int tap = ((r - 1) * a.W + (rs - 3 * r - 1)) * a.Csrc + c;
+        off = ((amask[q] >> min(rs, 31)) & 1u) ? (uint32_t)(arowoff[q] + tap) * 2u : kOob;
+      }
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(sa + q * NTHR * 16), 16, off, 0, 0, 0);
+    }
   }
   const uint32_t kb = (uint32_t)(kt * BK * 2);
 #pragma unroll
@@ -352,16 +367,21 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   if (!attr) {
     CONV_LDS_ATTR(256, 256, 2, 4)
     CONV_LDS_ATTR(256, 128, 4, 2)
+    CONV_LDS_ATTR(128, 64, 2, 4)
     CONV_LDS_ATTR(256, 64, 4, 2)
     CONV_LDS_ATTR(256, 32, 4, 2)
     attr = true;
   }
-  // the narrowest weight tile that covers N (256 beyond 128)
+  // the narrowest weight tile that covers N (256 beyond 128); a 64-wide
+  // tile over a long k loop takes 128 pixels (48 KB of LDS: three
+  // workgroups per CU hide more latency), over a short one 256 (less fixed
+  // cost per output)
   const int bn = a.N > 128 ? 256 : a.N > 64 ? 128 : a.N > 32 ? 64 : 32;
-  const int bm = 256;
+  const int bm = (bn == 64 && a.Kp >= 16 * BK) ? 128 : 256;
   int MT, NT;
   if (bn == 256) grid<256, 256>(a, &MT, &NT);
   else if (bn == 128) grid<256, 128>(a, &MT, &NT);
+  else if (bn == 64 && bm == 128) grid<128, 64>(a, &MT, &NT);
   else if (bn == 64) grid<256, 64>(a, &MT, &NT);
   else grid<256, 32>(a, &MT, &NT);
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Csrc);
@@ -378,6 +398,7 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   const bool fwd = a.epi == EPI_FWD, t1 = a.taps == 1;
   if (bn == 256) { CONV_LDS_SEL(256, 256, 2, 4) }
   else if (bn == 128) { CONV_LDS_SEL(256, 128, 4, 2) }
+  else if (bn == 64 && bm == 128) { CONV_LDS_SEL(128, 64, 2, 4) }
   else if (bn == 64) { CONV_LDS_SEL(256, 64, 4, 2) }
   else { CONV_LDS_SEL(256, 32, 4, 2) }
 #undef CONV_LDS_SEL
