@@ -116,14 +116,17 @@ __device__ __forceinline__ void issue_tile(int kt, char *stage0, int wave, const
   const __amdgpu_buffer_rsrc_t rsa = rsrc(src, (uint32_t)(a.src_rs * 2));
   const __amdgpu_buffer_rsrc_t rsb = rsrc(wt, (uint32_t)((int64_t)a.N * a.Kp * 2));
   char *sa = stage0 + (kt & 1) * CF::STAGE;
+  int kcol = kt * BK;  // first weight column of the tile
   if (!TAPS1 && a.Csrc % BK == 0) {
-    // the whole k tile lies in one kernel tap: tap and its offset are
-    // workgroup-uniform
-    const int cpt = a.Csrc / BK;  // k tiles per tap
-    const int rs = __builtin_amdgcn_readfirstlane(kt / cpt);
+    // The whole k tile lies in one kernel tap (tap and offset are
+    // workgroup-uniform), and tiles run tap-fastest: k tile kt is channel
+    // block kt / 9 of tap kt % 9, so the 9 taps reuse one 64-channel window
+    // of pixel rows while it is in L2.
+    const int cb = __builtin_amdgcn_readfirstlane(kt / 9);
+    const int rs = kt - 9 * cb;
     const int r = (rs * 11) >> 5;  // rs / 3 for rs < 9
-    const int tap = __builtin_amdgcn_readfirstlane(((r - 1) * a.W + (rs - 3 * r - 1)) * a.Csrc +
-                                                   (kt - rs * cpt) * BK);
+    const int tap = __builtin_amdgcn_readfirstlane(((r - 1) * a.W + (rs - 3 * r - 1)) * a.Csrc + cb * BK);
+    kcol = rs * a.Csrc + cb * BK;
 #pragma unroll
     for (int q = 0; q < CF::SA; ++q) {
       const uint32_t off = ((amask[q] >> rs) & 1u) ? (uint32_t)(arowoff[q] + tap + 8 * achunk[q]) * 2u : kOob;
@@ -147,7 +150,7 @@ __device__ __forceinline__ void issue_tile(int kt, char *stage0, int wave, const
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(sa + q * NTHR * 16), 16, off, 0, 0, 0);
     }
   }
-  const uint32_t kb = (uint32_t)(kt * BK * 2);
+  const uint32_t kb = (uint32_t)(kcol * 2);
 #pragma unroll
   for (int q = 0; q < CF::SB; ++q)
     if (q * NTHR * 16 + wave * 1024 < CF::B_BYTES)
