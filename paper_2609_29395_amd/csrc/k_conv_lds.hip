@@ -56,7 +56,7 @@ template <int BM_, int BN, int WM, int WN> struct Cfg {
   static constexpr int LDS_BYTES = 2 * STAGE > EP_BYTES ? 2 * STAGE : EP_BYTES;
   static_assert(WM * WN * 64 == NTHR, "8 waves");
   static_assert(SA * NTHR * 16 == A_BYTES && B_BYTES % 1024 == 0, "copies must tile the stage");
-  static_assert(TM % 4 == 0 && TN >= 1, "wave tile: multiples of 64 pixels");
+  static_assert(TM % 4 == 0 && TN >= 1, "wave tile: multiples of 64 pixels (two halves per k group)");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 };
 
@@ -81,13 +81,14 @@ template <int OFF>
 __device__ __forceinline__ void read_frag(u32x4 &f, uint32_t addr) {
   asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(f) : "v"(addr), "n"(OFF));
 }
-template <int T, int... I>
+template <int T, int START, int... I>
 __device__ __forceinline__ void read_frags_seq(u32x4 (&f)[T], uint32_t addr, std::integer_sequence<int, I...>) {
-  (read_frag<I * 2048>(f[I], addr), ...);
+  (read_frag<(START + I) * 2048>(f[I], addr), ...);
 }
-template <int T>
+// fragments START .. START+T-1 of a 16-row-block column
+template <int T, int START = 0>
 __device__ __forceinline__ void read_frags(u32x4 (&f)[T], uint32_t addr) {
-  read_frags_seq<T>(f, addr, std::make_integer_sequence<int, T>{});
+  read_frags_seq<T, START>(f, addr, std::make_integer_sequence<int, T>{});
 }
 
 // Wait for every outstanding LDS read, then mark the fragments as produced
@@ -99,6 +100,12 @@ __device__ __forceinline__ void wait_frags(u32x4 (&x)[TA], u32x4 (&w)[TB]) {
   for (int t = 0; t < TA; ++t) asm volatile("" : "+v"(x[t]));
 #pragma unroll
   for (int t = 0; t < TB; ++t) asm volatile("" : "+v"(w[t]));
+}
+template <int TA>
+__device__ __forceinline__ void wait_frags(u32x4 (&x)[TA]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int t = 0; t < TA; ++t) asm volatile("" : "+v"(x[t]));
 }
 
 __device__ __forceinline__ float bf2f(uint32_t bits16) { return bf16_to_f32((bf16_t)bits16); }
@@ -247,16 +254,27 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
     asm volatile("s_barrier" ::: "memory");
     if (kt + 1 < nk) issue(kt + 1);
     const uint32_t st = lds0 + (uint32_t)((kt & 1) * CF::STAGE);
+    // per k group: the second half of the pixel fragments is read while the
+    // first half is multiplied
 #pragma unroll
     for (int kg = 0; kg < 2; ++kg) {
-      u32x4 x[TM], w[TN];
-      read_frags<TM>(x, st + xa[kg]);
+      constexpr int H = TM / 2;
+      u32x4 w[TN], x0[H], x1[H];
       read_frags<TN>(w, st + wa[kg]);
-      wait_frags<TM, TN>(x, w);
+      read_frags<H>(x0, st + xa[kg]);
+      wait_frags<H, TN>(x0, w);
+      read_frags<H, H>(x1, st + xa[kg]);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm)
+      for (int tm = 0; tm < H; ++tm)
 #pragma unroll
-        for (int tn = 0; tn < TN; ++tn) mma(acc[tm][tn], w[tn], x[tm]);
+        for (int tn = 0; tn < TN; ++tn) mma(acc[tm][tn], w[tn], x0[tm]);
+      __builtin_amdgcn_sched_barrier(0);
+      wait_frags<H>(x1);
+#pragma unroll
+      for (int tm = 0; tm < H; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) mma(acc[H + tm][tn], w[tn], x1[tm]);
     }
   }
   __syncthreads();
