@@ -37,26 +37,29 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
 
-constexpr int BK = 64, NTHR = 512;
+constexpr int BK = 64;
 constexpr int ROW = BK * 2;  // bytes per LDS row
 constexpr uint32_t kOob = 0x80000000u;
 constexpr int kBufferFlags = 0x00020000;
 
 template <int BM_, int BN, int WM, int WN> struct Cfg {
   static constexpr int BM = BM_;
+  static constexpr int NW = WM * WN, NTHR = 64 * NW;  // waves, threads
   static constexpr int A_BYTES = BM * ROW, B_BYTES = BN * ROW;
   static constexpr int STAGE = A_BYTES + B_BYTES;
   // copies per thread; a narrow weight tile leaves the last B copy to the
   // first waves only
   static constexpr int SA = A_BYTES / (NTHR * 16), SB = (B_BYTES + NTHR * 16 - 1) / (NTHR * 16);
-  static constexpr int TM = BM / WM / 16, TN = BN / WN / 16;                    // fragments per wave
-  static constexpr int WNW = BN / WN;                                            // wave tile width
+  static constexpr int TM = BM / WM / 16, TN = BN / WN / 16;  // fragments per wave
+  static constexpr int WNW = BN / WN;                          // wave tile width
+  // epilogue: PF pixel fragments (16 * PF rows) per pass through LDS
+  static constexpr int PF = NW > 8 ? 2 : 4;
   static constexpr int EP_LD = WNW + 4;  // floats per staged epilogue row
-  static constexpr int EP_BYTES = 8 * 64 * EP_LD * 4;
+  static constexpr int EP_BYTES = NW * 16 * PF * EP_LD * 4;
   static constexpr int LDS_BYTES = 2 * STAGE > EP_BYTES ? 2 * STAGE : EP_BYTES;
-  static_assert(WM * WN * 64 == NTHR, "8 waves");
+  static_assert(NW == 8 || NW == 16, "8 or 16 waves");
   static_assert(SA * NTHR * 16 == A_BYTES && B_BYTES % 1024 == 0, "copies must tile the stage");
-  static_assert(TM % 4 == 0 && TN >= 1, "wave tile: multiples of 64 pixels (two halves per k group)");
+  static_assert(TM % PF == 0 && TM % 2 == 0 && TN >= 1, "wave tile: whole epilogue passes, two halves per k group");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 };
 
@@ -137,7 +140,7 @@ __device__ __forceinline__ void issue_tile(int kt, char *stage0, int wave, const
 #pragma unroll
     for (int q = 0; q < CF::SA; ++q) {
       const uint32_t off = ((amask[q] >> rs) & 1u) ? (uint32_t)(arowoff[q] + tap + 8 * achunk[q]) * 2u : kOob;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(sa + q * NTHR * 16), 16, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(sa + q * CF::NTHR * 16), 16, off, 0, 0, 0);
     }
   } else {
 #pragma unroll
@@ -154,22 +157,22 @@ __device__ __forceinline__ void issue_tile(int kt, char *stage0, int wave, const
         const int tap = ((r - 1) * a.W + (rs - 3 * r - 1)) * a.Csrc + c;
         off = ((amask[q] >> min(rs, 31)) & 1u) ? (uint32_t)(arowoff[q] + tap) * 2u : kOob;
       }
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(sa + q * NTHR * 16), 16, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(sa + q * CF::NTHR * 16), 16, off, 0, 0, 0);
     }
   }
   const uint32_t kb = (uint32_t)(kcol * 2);
 #pragma unroll
   for (int q = 0; q < CF::SB; ++q)
-    if (q * NTHR * 16 + wave * 1024 < CF::B_BYTES)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, LDS_PTR(sa + CF::A_BYTES + q * NTHR * 16), 16,
+    if (q * CF::NTHR * 16 + wave * 1024 < CF::B_BYTES)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, LDS_PTR(sa + CF::A_BYTES + q * CF::NTHR * 16), 16,
                                                boff[q] == kOob ? kOob : boff[q] + kb, 0, 0, 0);
 }
 
 template <int BM, int BN, int WM, int WN, int EPI, bool TAPS1>
-__global__ void __launch_bounds__(NTHR)
+__global__ void __launch_bounds__(64 * WM * WN)
 conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
   using CF = Cfg<BM, BN, WM, WN>;
-  constexpr int SA = CF::SA, SB = CF::SB, TM = CF::TM, TN = CF::TN;
+  constexpr int SA = CF::SA, SB = CF::SB, TM = CF::TM, TN = CF::TN, NTHR = CF::NTHR, PF = CF::PF;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -279,11 +282,13 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   }
   __syncthreads();
 
-  // epilogue: 64 pixel rows of the wave tile per pass, staged as
+  // epilogue: 16 * PF pixel rows of the wave tile per pass, staged as
   // [pixel][channel] fp32, then 8 channels per lane
+  constexpr int PR = 16 * PF;        // rows per pass
   constexpr int SEGS = CF::WNW / 8;  // 8-channel segments per row
   constexpr int RSTEP = 64 / SEGS;   // rows per lane step
-  float *ep = reinterpret_cast<float *>(smem) + wave * 64 * CF::EP_LD;
+  constexpr int ITS = PR / RSTEP;    // lane steps per pass
+  float *ep = reinterpret_cast<float *>(smem) + wave * PR * CF::EP_LD;
   const int seg = lane % SEGS;
   const int n = n0 + wn * CF::WNW + 8 * seg;
   const bool nok = n < a.N;
@@ -296,21 +301,21 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   const __amdgpu_buffer_rsrc_t rsr = rsrc(res ? res : out, (uint32_t)(a.out_rs * 2));
   const __amdgpu_buffer_rsrc_t rsm = rsrc(msk ? msk : out, (uint32_t)(a.out_rs * 2));
 #pragma unroll
-  for (int pass = 0; pass < TM / 4; ++pass) {
+  for (int pass = 0; pass < TM / PF; ++pass) {
 #pragma unroll
-    for (int tm = 0; tm < 4; ++tm)
+    for (int tm = 0; tm < PF; ++tm)
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn)
-        *reinterpret_cast<f32x4_t *>(ep + (tm * 16 + li) * CF::EP_LD + tn * 16 + lg * 4) = acc[pass * 4 + tm][tn];
+        *reinterpret_cast<f32x4_t *>(ep + (tm * 16 + li) * CF::EP_LD + tn * 16 + lg * 4) = acc[pass * PF + tm][tn];
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     // every residual and mask load of the pass is issued before any is
     // used; rows past M (and channels past N) read zero and store nothing
-    uint4 rv[SEGS], mv[SEGS];
+    uint4 rv[ITS], mv[ITS];
 #pragma unroll
-    for (int i = 0; i < SEGS; ++i) {
-      const int m = m0 + wm * TM * 16 + pass * 64 + lane / SEGS + RSTEP * i;
+    for (int i = 0; i < ITS; ++i) {
+      const int m = m0 + wm * TM * 16 + pass * PR + lane / SEGS + RSTEP * i;
       const uint32_t off = (nok && m < M) ? (uint32_t)((int64_t)m * a.N + n) * 2u : kOob;
       rv[i] = res ? __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsr, off, 0, 0))
                   : make_uint4(0, 0, 0, 0);
@@ -319,9 +324,9 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
                     : make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
     }
 #pragma unroll
-    for (int i = 0; i < SEGS; ++i) {
+    for (int i = 0; i < ITS; ++i) {
       const int r = lane / SEGS + RSTEP * i;  // pixel row of this pass
-      const int m = m0 + wm * TM * 16 + pass * 64 + r;
+      const int m = m0 + wm * TM * 16 + pass * PR + r;
       const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(ep + r * CF::EP_LD + 8 * seg);
       const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(ep + r * CF::EP_LD + 8 * seg + 4);
       float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
@@ -386,7 +391,7 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   }
   static bool attr = false;
   if (!attr) {
-    CONV_LDS_ATTR(256, 256, 2, 4)
+    CONV_LDS_ATTR(256, 256, 4, 4)
     CONV_LDS_ATTR(256, 128, 4, 2)
     CONV_LDS_ATTR(128, 64, 2, 4)
     CONV_LDS_ATTR(256, 64, 4, 2)
@@ -406,18 +411,18 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   else if (bn == 64) grid<256, 64>(a, &MT, &NT);
   else grid<256, 32>(a, &MT, &NT);
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Csrc);
-  const dim3 g((uint32_t)MT * NT * a.C), b(NTHR);
+  const dim3 g((uint32_t)MT * NT * a.C);
   if (label)
     *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16," + std::to_string(bm) + "x" +
-             std::to_string(bn) + "x64,w8,lds>";
+             std::to_string(bn) + "x64,w" + (bn == 256 ? "16" : "8") + ",lds>";
 #define CONV_LDS_GO(BM, BN, WM, WN, E, T)                                                                  \
-  hipLaunchKernelGGL((CONV_LDS_K(BM, BN, WM, WN, E, T)), g, b, (Cfg<BM, BN, WM, WN>::LDS_BYTES), s, a, fw, fh, \
-                     fc, MT, NT)
+  hipLaunchKernelGGL((CONV_LDS_K(BM, BN, WM, WN, E, T)), g, dim3(Cfg<BM, BN, WM, WN>::NTHR),                 \
+                     (Cfg<BM, BN, WM, WN>::LDS_BYTES), s, a, fw, fh, fc, MT, NT)
 #define CONV_LDS_SEL(BM, BN, WM, WN)                                                                        \
   if (fwd) { if (t1) CONV_LDS_GO(BM, BN, WM, WN, EPI_FWD, true); else CONV_LDS_GO(BM, BN, WM, WN, EPI_FWD, false); } \
   else { if (t1) CONV_LDS_GO(BM, BN, WM, WN, EPI_DGRAD, true); else CONV_LDS_GO(BM, BN, WM, WN, EPI_DGRAD, false); }
   const bool fwd = a.epi == EPI_FWD, t1 = a.taps == 1;
-  if (bn == 256) { CONV_LDS_SEL(256, 256, 2, 4) }
+  if (bn == 256) { CONV_LDS_SEL(256, 256, 4, 4) }
   else if (bn == 128) { CONV_LDS_SEL(256, 128, 4, 2) }
   else if (bn == 64 && bm == 128) { CONV_LDS_SEL(128, 64, 2, 4) }
   else if (bn == 64) { CONV_LDS_SEL(256, 64, 4, 2) }

@@ -41,10 +41,11 @@ def kernel_label(name: str) -> str:
         t = "bf16" if m.group(1) == "unsigned short" else "f32"
         w = int(m.group(4)) * int(m.group(5))
         return f"conv_wgrad<{t},{m.group(2)}x{m.group(3)},w{w},{'vec' if m.group(6) == 'true' else 'gather'}>"
-    m = re.search(r"conv_lds_kernel<(\d+), (\d+), \d+, \d+, (\d), (true|false)>", name)
+    m = re.search(r"conv_lds_kernel<(\d+), (\d+), (\d+), (\d+), (\d), (true|false)>", name)
     if m:
-        kind = "conv_fwd" if m.group(3) == "0" else "conv_dgrad"
-        return f"{kind}<bf16,{m.group(1)}x{m.group(2)}x64,w8,lds>"
+        kind = "conv_fwd" if m.group(5) == "0" else "conv_dgrad"
+        w = int(m.group(3)) * int(m.group(4))
+        return f"{kind}<bf16,{m.group(1)}x{m.group(2)}x64,w{w},lds>"
     m = re.search(r"wgrad_lds_kernel<(\d+), (\d+), \d+, \d+, (true|false)>", name)
     if m:
         return f"conv_wgrad<bf16,{m.group(1)}x{m.group(2)},w8,lds>"
