@@ -37,23 +37,28 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
 
-constexpr int BK = 64, NTHR = 512;
+constexpr int BK = 64;
 constexpr uint32_t kOob = 0x80000000u;
 constexpr int kBufferFlags = 0x00020000;
 constexpr int kDead = 1 << 30;  // row index that fails every pixel test
 
 template <int BM, int BN, int WM, int WN> struct Cfg {
+  static constexpr int NW = WM * WN, NTHR = 64 * NW;  // waves, threads
   static constexpr int ROWA = BM * 2, ROWB = BN * 2;  // bytes per LDS row
   static constexpr int CHA = ROWA / 16, CHB = ROWB / 16;  // 16-byte chunks per row
   static constexpr int A_BYTES = BK * ROWA, B_BYTES = BK * ROWB;
   static constexpr int STAGE = A_BYTES + B_BYTES;
   static constexpr int SA = A_BYTES / (NTHR * 16), SB = B_BYTES / (NTHR * 16);  // copies per thread
+  // rows between a thread's successive copies: a multiple of 16, so the
+  // swizzled column (row bits 0, 1, 3) is the same for all of them
+  static constexpr int QROWA = NTHR * 16 / ROWA, QROWB = NTHR * 16 / ROWB;
   static constexpr int TM = BM / WM / 16, TN = BN / WN / 16;                    // fragments per wave
   static constexpr int BPW = (TM + WN - 1) / WN;  // bias fragments per wave: those with tm % WN == wn
   static constexpr int LDS_BYTES = 2 * STAGE;
   static constexpr int WNS = WN;
-  static_assert(WM * WN * 64 == NTHR, "8 waves");
+  static_assert(NW == 8 || NW == 16, "8 or 16 waves");
   static_assert(SA * NTHR * 16 == A_BYTES && SB * NTHR * 16 == B_BYTES, "copies must tile the stage");
+  static_assert(QROWA % 16 == 0 && QROWB % 16 == 0, "copy rows keep the swizzle");
   static_assert(TM % WN == 0 || WN % TM == 0, "bias fragments split evenly over the waves of a row");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 };
@@ -102,32 +107,32 @@ __device__ __forceinline__ void mma(f32x4_t &acc, const u32x4 &a, const u32x4 &b
 template <typename CF, bool TAPS1>
 __device__ __forceinline__ void issue_tile(int kt, char *stage0, const WgradArgs &a, FastDiv fd_w, FastDiv fd_h,
                                            const void *G, const void *X, int M, int p_begin, int p_end,
-                                           const int *arow, const int *acol, const int *brow, const int *bci,
-                                           const int *bdh, const int *bdw) {
+                                           int arow, int acol, int brow, int bci, int btap) {
   const __amdgpu_buffer_rsrc_t rsg = rsrc(G, (uint32_t)((int64_t)M * a.Co * 2));
   const __amdgpu_buffer_rsrc_t rsx = rsrc(X, (uint32_t)((int64_t)M * a.Ci * 2));
   char *sa = stage0 + (kt & 1) * CF::STAGE;
   const int pt = p_begin + kt * BK;
 #pragma unroll
   for (int q = 0; q < CF::SA; ++q) {
-    const int p = pt + arow[q];
-    const uint32_t off = p < p_end ? ((uint32_t)p * (uint32_t)a.Co + (uint32_t)acol[q]) * 2u : kOob;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsg, LDS_PTR(sa + q * NTHR * 16), 16, off, 0, 0, 0);
+    const int p = pt + arow + q * CF::QROWA;
+    const uint32_t off = p < p_end ? ((uint32_t)p * (uint32_t)a.Co + (uint32_t)acol) * 2u : kOob;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsg, LDS_PTR(sa + q * CF::NTHR * 16), 16, off, 0, 0, 0);
   }
 #pragma unroll
   for (int q = 0; q < CF::SB; ++q) {
-    const int p = pt + brow[q];
+    const int p = pt + brow + q * CF::QROWB;
     bool ok = p < p_end;
     int src = p;
     if constexpr (!TAPS1) {
+      const int dh = (btap & 3) - 1, dw = (btap >> 2) - 1;
       const uint32_t q1 = fdiv((uint32_t)p, fd_w);
       const int w = p - (int)q1 * a.W;
       const int h = (int)q1 - (int)fdiv(q1, fd_h) * a.H;
-      ok = ok & ((unsigned)(h + bdh[q]) < (unsigned)a.H) & ((unsigned)(w + bdw[q]) < (unsigned)a.W);
-      src = p + bdh[q] * a.W + bdw[q];
+      ok = ok & ((unsigned)(h + dh) < (unsigned)a.H) & ((unsigned)(w + dw) < (unsigned)a.W);
+      src = p + dh * a.W + dw;
     }
-    const uint32_t off = ok ? ((uint32_t)src * (uint32_t)a.Ci + (uint32_t)bci[q]) * 2u : kOob;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, LDS_PTR(sa + CF::A_BYTES + q * NTHR * 16), 16, off, 0, 0, 0);
+    const uint32_t off = ok ? ((uint32_t)src * (uint32_t)a.Ci + (uint32_t)bci) * 2u : kOob;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, LDS_PTR(sa + CF::A_BYTES + q * CF::NTHR * 16), 16, off, 0, 0, 0);
   }
 }
 
@@ -163,10 +168,10 @@ __device__ __forceinline__ void kgroup(f32x4_t (&acc)[CF::TM][CF::TN], f32x4_t (
 }
 
 template <int BM, int BN, int WM, int WN, bool TAPS1>
-__global__ void __launch_bounds__(NTHR)
+__global__ void __launch_bounds__(64 * WM * WN)
 wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
   using CF = Cfg<BM, BN, WM, WN>;
-  constexpr int SA = CF::SA, SB = CF::SB, TM = CF::TM, TN = CF::TN, BPW = CF::BPW;
+  constexpr int TM = CF::TM, TN = CF::TN, BPW = CF::BPW;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -188,34 +193,29 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
   const bf16_t *X = reinterpret_cast<const bf16_t *>(a.x) + rep * a.x_rs;
   const bool do_bias = (nt == 0) && a.db != nullptr;
 
-  // This thread's copies: byte q*8192 + wave*1024 + lane*16 of the A and B
-  // regions of a stage.  The row and the swizzled column it fills are the
-  // same for every k tile; only the pixel advances.  A column outside the
-  // operand gets a row index past any chunk, so its pixel test fails.
-  int arow[SA], acol[SA];
-#pragma unroll
-  for (int q = 0; q < SA; ++q) {
-    const int byte = q * NTHR * 16 + wave * 1024 + lane * 16;
-    const int row = byte / CF::ROWA;
-    const int co = m0 + 8 * (((byte % CF::ROWA) / 16) ^ swz<CF::CHA>(row));
-    arow[q] = co < a.Co ? row : kDead;
-    acol[q] = co;
+  // This thread's copies: bytes q*NTHR*16 + wave*1024 + lane*16 of the A and
+  // B regions of a stage, i.e. rows row0 + q*QROW at one swizzled column.
+  // Only the pixel advances from tile to tile.  A column outside the operand
+  // gets a row index past any chunk, so its pixel test fails.
+  const int byte0 = wave * 1024 + lane * 16;
+  int arow, acol;
+  {
+    const int row = byte0 / CF::ROWA;
+    acol = m0 + 8 * (((byte0 % CF::ROWA) / 16) ^ swz<CF::CHA>(row));
+    arow = acol < a.Co ? row : kDead;
   }
-  int brow[SB], bci[SB], bdh[SB], bdw[SB];
-#pragma unroll
-  for (int q = 0; q < SB; ++q) {
-    const int byte = q * NTHR * 16 + wave * 1024 + lane * 16;
-    const int row = byte / CF::ROWB;
-    const int kk = n0 + 8 * (((byte % CF::ROWB) / 16) ^ swz<CF::CHB>(row));
-    brow[q] = kk < NW ? row : kDead;
+  int brow, bci, btap;  // btap: (row offset + 1) | (column offset + 1) << 2
+  {
+    const int row = byte0 / CF::ROWB;
+    const int kk = n0 + 8 * (((byte0 % CF::ROWB) / 16) ^ swz<CF::CHB>(row));
+    brow = kk < NW ? row : kDead;
     if constexpr (TAPS1) {
-      bci[q] = kk; bdh[q] = 0; bdw[q] = 0;
+      bci = kk; btap = 1 | (1 << 2);
     } else {
       const int rs = (int)fdiv((uint32_t)kk, fd_c);
-      bci[q] = kk - rs * a.Ci;
+      bci = kk - rs * a.Ci;
       const int r = (rs * 11) >> 5;  // rs / 3 for rs < 9
-      bdh[q] = r - 1;
-      bdw[q] = rs - 3 * r - 1;
+      btap = (r & 3) | (((rs - 3 * r) & 3) << 2);
     }
   }
   char *stage0 = smem + wave * 1024;
@@ -244,15 +244,15 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
 #pragma unroll
   for (int i = 0; i < BPW; ++i) bacc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  issue_tile<CF, TAPS1>(0, stage0, a, fd_w, fd_h, G, X, M, p_begin, p_end, arow, acol, brow, bci, bdh, bdw);
+  issue_tile<CF, TAPS1>(0, stage0, a, fd_w, fd_h, G, X, M, p_begin, p_end, arow, acol, brow, bci, btap);
   for (int kt = 0; kt < nk; ++kt) {
     // own copies of tile kt have landed; after the barrier every wave's
     // have, and every wave is done with tile kt-1, whose stage is refilled
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     asm volatile("s_barrier" ::: "memory");
     if (kt + 1 < nk)
-      issue_tile<CF, TAPS1>(kt + 1, stage0, a, fd_w, fd_h, G, X, M, p_begin, p_end, arow, acol, brow, bci, bdh,
-                            bdw);
+      issue_tile<CF, TAPS1>(kt + 1, stage0, a, fd_w, fd_h, G, X, M, p_begin, p_end, arow, acol, brow, bci,
+                            btap);
     const uint32_t st = lds0 + (uint32_t)((kt & 1) * CF::STAGE);
     kgroup<CF, 0>(acc, bacc, ra, rb, st, do_bias, wn);
     kgroup<CF, 1>(acc, bacc, ra, rb, st, do_bias, wn);
@@ -327,10 +327,12 @@ hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *labe
   const int NW = a.taps == 1 ? a.Ci : 9 * a.Ci;
   const int MT = (a.Co + BM - 1) / BM, NT = (NW + BN - 1) / BN;
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Ci);
-  const dim3 g((uint32_t)MT * NT * a.splits * a.C), b(NTHR);
-  if (label) *label = "conv_wgrad<bf16," + std::to_string(BM) + "x" + std::to_string(BN) + ",w8,lds>";
-#define WG_GO(BM, BN, WM, WN, T) \
-  hipLaunchKernelGGL((WG_K(BM, BN, WM, WN, T)), g, b, (Cfg<BM, BN, WM, WN>::LDS_BYTES), s, a, fw, fh, fc, MT, NT)
+  const dim3 g((uint32_t)MT * NT * a.splits * a.C);
+  if (label)
+    *label = "conv_wgrad<bf16," + std::to_string(BM) + "x" + std::to_string(BN) + ",w8,lds>";
+#define WG_GO(BM, BN, WM, WN, T)                                                                             \
+  hipLaunchKernelGGL((WG_K(BM, BN, WM, WN, T)), g, dim3(Cfg<BM, BN, WM, WN>::NTHR), (Cfg<BM, BN, WM, WN>::LDS_BYTES), \
+                     s, a, fw, fh, fc, MT, NT)
   const bool t1 = a.taps == 1;
   if (BM == 256) {
     if (t1) WG_GO(256, 256, 2, 4, true); else WG_GO(256, 256, 2, 4, false);
