@@ -42,6 +42,14 @@ CONFIGS = {
         layers=[("conv", 3, 8, False), ("maxpool",),
                 ("conv", 8, 16, False), ("avgpool",), ("linear", 16, 4)],
         cut=2, dtype="f32", lr=0.05, momentum=0.0, F=5, T=10, seed=0),
+    # The tiny workload clustered by the paper's label-aware move search
+    # (Eq. 4) instead of at random.
+    "tiny_jsd": dict(
+        K=16, C=2, B=8, L=4, N_ex=512, H=8, W=8, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="label_jsd",
+        layers=[("conv", 3, 8, False), ("maxpool",),
+                ("conv", 8, 16, False), ("avgpool",), ("linear", 16, 4)],
+        cut=2, dtype="f32", lr=0.05, momentum=0.0, F=5, T=10, seed=0),
     # Single-workload GPSL baseline (C = 1).
     "gpsl": dict(
         K=256, C=1, B=64, alpha=0.3, rule="random", **_CIFAR_DATA,

@@ -48,6 +48,7 @@ extern "C" {
 #define GCPSL_RULE_RANDOM 0   /* permute, then round-robin                   */
 #define GCPSL_RULE_SIZE 1     /* size-balanced: lightest allowed cluster     */
 #define GCPSL_RULE_LABEL_L1 2 /* greedy label-histogram L1 placement         */
+#define GCPSL_RULE_LABEL_JSD 3 /* Eq. 4 move search: size + JSD objective     */
 
 /* Compute precisions. */
 #define GCPSL_F32 0  /* fp32 activations and weights                        */
@@ -129,6 +130,15 @@ int gcpsl_workspace_bytes(const gcpsl_desc *d, size_t *bytes);
  *                  smaller summed count, then the lower index; a client with
  *                  no samples goes to the allowed cluster with the fewest
  *                  clients.  Needs counts and hist.
+ *   rule LABEL_JSD: the paper's label-aware rule (Eq. 4, Alg. 1): start from
+ *                  the SIZE assignment, then repeatedly apply the single-client
+ *                  move with the lowest J = sum_n |w_n - |D|/C| / |D| +
+ *                  sum_n (w_n/|D|) JSD(p_n, p) (nats) while it lowers J, at
+ *                  most 4K moves; a move keeps the source at >= floor(K/C) - s
+ *                  and the destination at <= ceil(K/C) + s clients,
+ *                  s = max(1, K/(4C)); first strict minimum in (client,
+ *                  destination) order.  Needs counts and hist with at least
+ *                  one sample.
  * counts: host [K] int64 sample counts; hist: host [K][L] int64 class
  * histograms (row k sums to counts[k]); cluster_of_client: host [K] output,
  * caller-owned.  EINVAL on K < 1, C < 1, C > K, unknown rule, missing

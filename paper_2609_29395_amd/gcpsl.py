@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgcpsl.so")
 
 OK, EINVAL, ESTATE, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4
-RULES = {"random": 0, "size": 1, "label_l1": 2}
+RULES = {"random": 0, "size": 1, "label_l1": 2, "label_jsd": 3}
 DTYPES = {"f32": 0, "bf16": 1}
 CONV3X3, MAXPOOL2, AVGPOOL, LINEAR = 1, 2, 3, 4
 RESIDUAL = 1

@@ -162,3 +162,34 @@ def test_unsupported_models_are_reported():
     with pytest.raises(g.GCPSLError) as e:
         g.param_count(d)
     assert e.value.code == g.EINVAL
+
+
+@pytest.mark.parametrize("name", ["tiny", "gcpsl4", "gcpsl8", "gcpsl16", "ragged"])
+def test_assign_label_jsd_matches_oracle_bit_exact(name):
+    """The paper's label-aware move search (Eq. 4) on each workload's client
+    histograms: same clusters as the oracle, bit for bit."""
+    from oracle.assign import assign_label_jsd
+    cfg = get_config(name)
+    _, labels, coe = make_dataset(cfg)
+    counts, hist = client_stats(cfg, labels, coe)
+    want = assign_label_jsd(cfg["K"], cfg["C"], counts, hist)[0]
+    got = g.assign("label_jsd", cfg["K"], cfg["C"], 0, counts, hist)
+    assert np.array_equal(got, want)
+
+
+def test_assign_label_jsd_random_instances():
+    from oracle.assign import assign_label_jsd
+    rng = np.random.default_rng(21)
+    for trial in range(25):
+        K = int(rng.integers(2, 48))
+        Cc = int(rng.integers(1, min(K, 7) + 1))
+        L = int(rng.integers(1, 9))
+        hist = rng.integers(0, 25, size=(K, L)) * (rng.random((K, L)) < 0.4)
+        if hist.sum() == 0:
+            hist[0, 0] = 1
+        counts = hist.sum(1)
+        assert np.array_equal(g.assign("label_jsd", K, Cc, 0, counts, hist),
+                              assign_label_jsd(K, Cc, counts, hist)[0]), trial
+    with pytest.raises(g.GCPSLError) as e:
+        g.assign("label_jsd", 4, 2, 0, np.zeros(4, np.int64), np.zeros((4, 3), np.int64))
+    assert e.value.code == g.EINVAL

@@ -89,7 +89,7 @@ def test_sample_and_gather_bit_exact(name, window, starts):
 
 # ------------------------------------------------------- multi-step runs
 
-@pytest.mark.parametrize("name", ["tiny", "ragged", "ragged_bf16"])
+@pytest.mark.parametrize("name", ["tiny", "tiny_jsd", "ragged", "ragged_bf16"])
 def test_run_parity_with_fusion(name):
     cfg = get_config(name)
     T = cfg["T"]
