@@ -43,14 +43,15 @@ DESCRIPTIONS = {
 
 def load_traffic(workload, kernel):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when it is absent or the kernels changed since it was taken."""
+    None when it is absent or the kernel's source changed since it was taken."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
-    from paper_2609_29395_amd.profile_summary import source_hash
+    from paper_2609_29395_amd.profile_summary import file_hash, kernel_source
     with open(path) as fh:
         rec = json.load(fh)
-    if rec.get("source_hash") != source_hash():
+    src = kernel_source(kernel)
+    if rec.get("source_hashes", {}).get(src) != file_hash(src):
         return None
     entry = rec.get("kernels", {}).get(f"{workload}:{kernel}")
     return None if entry is None else entry.get("bytes_per_launch")
@@ -78,6 +79,42 @@ def cpu_baseline(cfg, assignment, budget_s):
                       f"{dt:.1f} s; the rate per example equals the C-cluster rate"}
 
 
+def _timed(fn):
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    fn()
+    torch.cuda.synchronize()
+    return time.perf_counter() - t0
+
+
+def schedule_control(cfg, ctx, start, steps):
+    """Concurrent against sequential execution of the cluster workloads on
+    this GPU (the one-GPU analogue of Eq. 6's comparison): the same rounds,
+    once with all clusters of a step in one launch per kernel, once with the
+    clusters run one after another through gcpsl_step_replica.  Lockstep:
+    `steps` rounds of the workload's own schedule.  Epoch barrier: one system
+    epoch of R slots in which cluster n takes r_n = floor(n_n / B) rounds."""
+    from paper_2609_29395_amd import driver
+    out = {}
+    conc = _timed(lambda: driver.train(ctx, steps, start=start))
+    seq = _timed(lambda: driver.train(ctx, steps, start=start + steps, serial=True))
+    out["lockstep"] = {"rounds_per_cluster": steps, "concurrent_ms_per_step": round(conc * 1e3 / steps, 3),
+                       "sequential_ms_per_step": round(seq * 1e3 / steps, 3), "speedup": round(seq / conc, 3)}
+    ectx, _ = driver.setup(cfg, max_steps=1, schedule="epoch")
+    rounds, R = ectx.epoch_rounds()
+    driver.train(ectx, min(R, 4), start=0)  # warm-up slots
+    conc = _timed(lambda: driver.train(ectx, R, start=R))
+    seq = _timed(lambda: driver.train(ectx, R, start=2 * R, serial=True))
+    work = int(rounds.sum())
+    out["epoch"] = {"slots_per_epoch": int(R), "cluster_rounds_per_epoch": work,
+                    "eq6_ideal_speedup": round(work / R, 3),
+                    "concurrent_s": round(conc, 4), "sequential_s": round(seq, 4), "speedup": round(seq / conc, 3),
+                    "concurrent_examples_per_s": round(work * cfg["B"] / conc, 1)}
+    ectx.close()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -87,6 +124,9 @@ def main():
     ap.add_argument("--timing-steps", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-schedule-control", action="store_true",
+                    help="skip the concurrent-vs-sequential cluster execution control")
+    ap.add_argument("--control-steps", type=int, default=10)
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -100,7 +140,7 @@ def main():
 
     cfg = get_config(args.workload)
     C, B, F = cfg["C"], cfg["B"], cfg["F"]
-    total = args.warmup + args.steps + args.timing_steps
+    total = args.warmup + args.steps + args.timing_steps + 2 * args.control_steps
     print(f"bench: workload {args.workload} C={C} B={B} F={F} warmup={args.warmup} steps={args.steps}",
           file=sys.stderr, flush=True)
     torch.cuda.set_device(0)
@@ -174,6 +214,10 @@ def main():
         "kernel_ms_per_step": round(kernel_ms / nsteps, 4),
         "roofline": roof,
     }
+    if not args.no_schedule_control:
+        out["schedule_control"] = schedule_control(cfg, ctx, args.warmup + args.steps + args.timing_steps,
+                                                   args.control_steps)
+        print(f"bench: schedule control {out['schedule_control']}", file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, assignment, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -15,6 +15,10 @@ Layer tuples:
 
 The client segment is layers[:cut]; the server segment is layers[cut:].
 
+schedule (default "lockstep"): "lockstep" runs every cluster's round at every
+step and fuses every F steps; "epoch" runs the epoch-barrier schedule (each
+cluster floor(n_n / B) rounds per system epoch, fusion after the epoch).
+
 Parameter layout (one flat fp32 vector of P entries per replica): for every
 conv / linear layer in order, its weight followed by its bias.  Conv weights
 are stored [cout][3][3][cin] (output channel, kernel row, kernel column,
@@ -86,6 +90,29 @@ CONFIGS = {
                 ("conv", 24, 136, False), ("conv", 136, 136, True), ("maxpool",),
                 ("avgpool",), ("linear", 136, 7)],
         cut=3, dtype="bf16", lr=0.05, momentum=0.9, F=3, T=7, seed=0),
+    # Epoch-barrier schedule (fusion after every system epoch) on unequal
+    # clusters: tiny with B=32 (6 and 9 rounds per epoch), and the ragged
+    # shapes under label-L1 clustering with B=100 (7, 4 and 2 rounds).
+    "tiny_epoch": dict(
+        K=16, C=2, B=32, L=4, N_ex=512, H=8, W=8, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="random",
+        layers=[("conv", 3, 8, False), ("maxpool",),
+                ("conv", 8, 16, False), ("avgpool",), ("linear", 16, 4)],
+        cut=2, dtype="f32", lr=0.05, momentum=0.9, F=0, T=18, seed=0, schedule="epoch"),
+    "ragged_epoch": dict(
+        K=24, C=3, B=100, L=7, N_ex=1400, H=12, W=12, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="label_l1",
+        layers=[("conv", 3, 8, False), ("conv", 8, 24, False), ("maxpool",),
+                ("conv", 24, 136, False), ("conv", 136, 136, True), ("maxpool",),
+                ("avgpool",), ("linear", 136, 7)],
+        cut=3, dtype="f32", lr=0.05, momentum=0.9, F=0, T=10, seed=0, schedule="epoch"),
+    "ragged_bf16_epoch": dict(
+        K=24, C=3, B=100, L=7, N_ex=1400, H=12, W=12, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="label_l1",
+        layers=[("conv", 3, 8, False), ("conv", 8, 24, False), ("maxpool",),
+                ("conv", 24, 136, False), ("conv", 136, 136, True), ("maxpool",),
+                ("avgpool",), ("linear", 136, 7)],
+        cut=3, dtype="bf16", lr=0.05, momentum=0.9, F=0, T=10, seed=0, schedule="epoch"),
 }
 
 
@@ -93,6 +120,7 @@ def get_config(name: str, **overrides) -> dict:
     """Return a deep copy of a named workload with optional field overrides."""
     cfg = copy.deepcopy(CONFIGS[name])
     cfg.update(overrides)
+    cfg.setdefault("schedule", "lockstep")
     cfg["name"] = name
     return cfg
 

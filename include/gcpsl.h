@@ -54,6 +54,11 @@ extern "C" {
 #define GCPSL_F32 0  /* fp32 activations and weights                        */
 #define GCPSL_BF16 1 /* bf16 activations and weights, fp32 master weights   */
 
+/* Round schedules (Sec. III-A, Sec. IV-D). */
+#define GCPSL_SCHED_LOCKSTEP 0 /* every cluster takes one local round per step  */
+#define GCPSL_SCHED_EPOCH 1    /* epoch barrier: a cluster takes floor(n_n/B)
+                                  rounds per system epoch, then waits          */
+
 /* Layer kinds of the split CNN. */
 #define GCPSL_CONV3X3 1 /* 3x3, stride 1, zero pad 1, bias, ReLU            */
 #define GCPSL_MAXPOOL2 2 /* 2x2 max pool, stride 2                           */
@@ -93,7 +98,7 @@ typedef struct gcpsl_desc {
   uint64_t seed;      /* sampler seed                                       */
   int64_t max_steps;  /* rows of the participation table (steps recorded)   */
   int32_t max_window; /* largest nsteps accepted by gcpsl_sample, >= 1      */
-  int32_t reserved;   /* must be 0                                          */
+  int32_t schedule;   /* GCPSL_SCHED_LOCKSTEP or GCPSL_SCHED_EPOCH          */
   const int32_t *client_of_example; /* host [n_examples], in [0, K)         */
   const int32_t *cluster_of_client; /* host [K], in [0, C) (Alg. 1 output)  */
   const float *images;   /* device [n_examples][H][W][Cin] fp32             */
@@ -160,15 +165,25 @@ int gcpsl_assign(int32_t K, int32_t C, int32_t rule, uint64_t seed, const int64_
 int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out);
 
 /*
- * Cluster-local global sampling (Eq. 1, Eq. 3) for local rounds
+ * Steps.  A step is one slot of the round schedule.
+ *   LOCKSTEP: at step s every cluster takes its local round s.
+ *   EPOCH (the system epoch of Sec. III-A and Eq. 6 of Sec. IV-D): with
+ *     r_n = floor(n_n / B) rounds of cluster n per epoch and R = max_n r_n
+ *     slots per system epoch, step s = m R + t is slot t of system epoch m;
+ *     cluster n takes its local round m r_n + t when t < r_n and otherwise
+ *     waits at the fusion barrier: no batch, no update, no participating
+ *     client.  The caller fuses (gcpsl_fuse) after slot R - 1 of each epoch.
+ *
+ * Cluster-local global sampling (Eq. 1, Eq. 3) for steps
  * [step, step + nsteps), with the gather of the sampled images and labels.
- * Cluster n draws its batch from its own pooled examples: epoch
- * e = step / S_n, S_n = floor(n_n / B), takes positions [tB, (t+1)B),
- * t = step mod S_n, of a keyed Feistel permutation of [0, n_n) (key from
+ * Cluster n draws its batch at local round s from its own pooled examples:
+ * epoch e = s / S_n, S_n = floor(n_n / B), takes positions [tB, (t+1)B),
+ * t = s mod S_n, of a keyed Feistel permutation of [0, n_n) (key from
  * seed, n, e); so every batch has exactly B distinct examples of the cluster.
- * Also records |A_{n,t}| (clients supplying >= 1 example, Sec. III-A) for
- * each sampled step below max_steps.
- * idx_out: device [nsteps][C][B] int32 global example ids, or NULL.
+ * Also records |A_{n,t}| (clients supplying >= 1 example, Sec. III-A; 0 for
+ * a waiting cluster) for each sampled step below max_steps.
+ * idx_out: device [nsteps][C][B] int32 global example ids (-1 for a waiting
+ * cluster), or NULL.
  * The gathered inputs stay staged until the next gcpsl_sample call; each
  * staged step can then be run once or more by gcpsl_step.
  * EINVAL: step < 0, nsteps < 1 or > max_window.
@@ -176,7 +191,8 @@ int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out);
 int gcpsl_sample(gcpsl_ctx *ctx, int64_t step, int32_t nsteps, int32_t *idx_out, void *stream);
 
 /*
- * One local round of every cluster (Alg. 2 inner loop): client-segment
+ * One local round of every cluster that takes one at this step (all clusters
+ * under LOCKSTEP; Alg. 2 inner loop): client-segment
  * forward to the cut, server-segment forward, softmax cross-entropy (mean
  * over B), server backward, cut-gradient hand-off (same buffer on one GPU),
  * client backward, and the SGD update of both segments of every replica
@@ -187,6 +203,24 @@ int gcpsl_sample(gcpsl_ctx *ctx, int64_t step, int32_t nsteps, int32_t *idx_out,
  * update, or NULL.  ESTATE if `step` is not among the staged steps.
  */
 int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *stream);
+
+/*
+ * The local round of one cluster only, exactly as gcpsl_step computes it for
+ * that cluster (same kernels, same arithmetic, bit-identical results): the
+ * clusters of a step may run one after another instead of side by side,
+ * which is the sequential execution that Eq. 6 compares with the concurrent
+ * one.  loss_out: device [C] (only entry `replica` is written) or NULL.
+ * EINVAL if replica is outside [0, C) or the cluster waits at this step;
+ * ESTATE if `step` is not staged.
+ */
+int gcpsl_step_replica(gcpsl_ctx *ctx, int64_t step, int32_t replica, float *loss_out, void *stream);
+
+/*
+ * Rounds of the epoch schedule: rounds host [C] receives r_n = floor(n_n / B)
+ * and slots the system-epoch length R = max_n r_n (Eq. 6).  Host only; valid
+ * under either schedule.
+ */
+int gcpsl_epoch_rounds(gcpsl_ctx *ctx, int64_t *rounds, int64_t *slots);
 
 /*
  * Fusion and broadcast, Eq. 5 (Sec. IV-D): theta_bar = sum_n (n_n / W)

@@ -5,7 +5,8 @@ paper ("Concurrent Split Learning Through Stable Client Clustering") and the
 readings of it listed in the design notes: static client clustering
 (Alg. 1), cluster-local GPSL sampling (Eq. 1, Eq. 3), the split forward and
 backward pass, the SGD update, sample-weighted fusion (Eq. 5) and direct data
-participation (Sec. V-E, Eq. 7).  Floating point is fp64 throughout; for the
+participation (Sec. V-E, Eq. 7), and the epoch-barrier round schedule
+(Sec. III-A, Eq. 6).  Floating point is fp64 throughout; for the
 bf16 workloads the oracle rounds to bf16 (round-to-nearest-even) at the same
 points the GPU path does.
 
@@ -19,6 +20,9 @@ Parity status of each part (pins live in tests/test_oracle_*.py):
   model layers, split step, SGD        pinned (textbook loops, finite
                                         differences, torch.autograd)
   fusion                               pinned (identity, worked example)
+  epoch-barrier schedule (Eq. 6)       pinned (worked example, waiting
+                                        clusters untouched, equal lengths
+                                        reduce to the lockstep schedule)
   multi-step end-to-end values         parity unpinned: the paper prints no
                                         worked example of a training run
 """

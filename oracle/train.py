@@ -21,6 +21,15 @@ Readings:
     identical replicas returns them unchanged, bit for bit.
   * The reported loss of a round is the forward loss before that round's
     update.
+
+Epoch-barrier schedule (Sec. III-A, Sec. IV-D "Schedule and Cost", Eq. 6):
+cluster n takes r_n = floor(n_n / B) local rounds per epoch (the sampler's
+epoch length); the system epoch has R = max_n r_n slots.  At slot t of
+system epoch m every cluster with t < r_n takes its local round m r_n + t
+(epoch m, batch position t); the others wait at the fusion barrier without
+updates and without participating clients.  After the last slot the
+replicas are fused.  Sequential execution of the same work needs sum_n r_n
+round slots, concurrent execution R: S = sum_n r_n / R <= N, E = S / N.
 """
 from __future__ import annotations
 
@@ -31,6 +40,19 @@ from gcpsl_inputs import client_stats, init_params, make_dataset
 from .assign import assign
 from .model import split_forward_backward
 from .sampler import active_clients, batch_indices, cluster_examples
+
+
+def epoch_rounds(weights, B):
+    """r_n = floor(n_n / B) local rounds of each cluster per epoch, and the
+    system-epoch length R = max_n r_n."""
+    r = [int(w) // B for w in weights]
+    return r, max(r)
+
+
+def ideal_schedule_speedup(rounds):
+    """Eq. 6: S = sum_n r_n / max_n r_n and E = S / N."""
+    S = sum(rounds) / max(rounds)
+    return S, S / len(rounds)
 
 
 def sgd_update(theta, mom, grad, lr, mu):
@@ -94,6 +116,33 @@ class GCPSLOracle:
         fused = fuse(self.theta, self.weights)
         for n in range(self.cfg["C"]):
             self.theta[n] = fused.copy()
+
+    def slot(self, s):
+        """Slot s of the epoch-barrier schedule; fuses after the epoch's last
+        slot.  Returns {cluster: loss} of the clusters that took a round."""
+        cfg = self.cfg
+        rounds, R = epoch_rounds(self.weights, cfg["B"])
+        m, t = divmod(s, R)
+        losses, active = {}, []
+        for n in range(cfg["C"]):
+            if t < rounds[n]:
+                idx, x, y = self.batch(m * rounds[n] + t, n)
+                active.append(active_clients(idx, self.coe))
+                loss, g, _ = split_forward_backward(cfg, self.theta[n], x, y)
+                sgd_update(self.theta[n], self.mom[n], g, cfg["lr"], cfg["momentum"])
+                losses[n] = loss
+            else:
+                active.append(0)  # waits at the barrier: no batch, no update
+        self.active.append(active)
+        self.losses.append([losses.get(n, float("nan")) for n in range(cfg["C"])])
+        if t == R - 1:
+            self.fuse()
+        return losses
+
+    def run_epoch_schedule(self, slots):
+        for s in range(slots):
+            self.slot(s)
+        return self
 
     def run(self, steps, F=None):
         F = self.cfg["F"] if F is None else F

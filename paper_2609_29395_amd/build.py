@@ -17,7 +17,7 @@ LIB = os.path.join(HERE, "libgcpsl.so")
 SOURCES = ["api.cpp", "assign.cpp", "k_conv.hip", "k_misc.hip", "k_wgrad_lds.hip", "k_conv_lds.hip"]
 ARCH = "gfx950"
 FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
+    f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wshadow", "-Wno-unused-function",
     # keep the compiler from emitting packed fp32 arithmetic
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
@@ -36,6 +36,12 @@ def _compile(src: str) -> str:
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
+    # report compiler warnings (the host pass's note about the gfx-only
+    # packed-fp32 feature flag is expected)
+    warn = [ln for ln in r.stderr.splitlines() if "warning:" in ln and "packed-fp32-ops" not in ln
+            and "unused during compilation" not in ln]
+    if warn:
+        print(f"{src}:\n" + "\n".join(warn), file=sys.stderr)
     return obj
 
 

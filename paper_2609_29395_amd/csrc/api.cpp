@@ -55,8 +55,10 @@ struct Plan {
   bool col0 = false;
   int Kc = 0;
   int64_t x_rs = 0;  // elements of one staged step: C * B * H * W * (Kc or Cin)
+  int schedule = GCPSL_SCHED_LOCKSTEP;
   size_t off_ids = 0, off_off = 0, off_coe = 0, off_fw = 0, off_hits = 0, off_idx = 0, off_y = 0,
-         off_x = 0, off_dh = 0, off_grad = 0, off_part = 0, off_dbpart = 0, off_loss = 0;
+         off_x = 0, off_dh = 0, off_grad = 0, off_part = 0, off_dbpart = 0, off_loss = 0, off_order = 0,
+         off_ident = 0;
   size_t total = 0;
 };
 
@@ -71,7 +73,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   if (d->n_examples < 1 || d->n_examples > INT32_MAX)
     return gcpsl_fail(GCPSL_EINVAL, "n_examples must be in [1, 2^31)");
   if (d->max_steps < 1 || d->max_window < 1) return gcpsl_fail(GCPSL_EINVAL, "max_steps and max_window must be >= 1");
-  if (d->reserved != 0) return gcpsl_fail(GCPSL_EINVAL, "reserved must be 0");
+  if (d->schedule != GCPSL_SCHED_LOCKSTEP && d->schedule != GCPSL_SCHED_EPOCH)
+    return gcpsl_fail(GCPSL_EINVAL, "unknown schedule");
   if (!d->layers || d->n_layers < 3) return gcpsl_fail(GCPSL_EINVAL, "need at least conv, avgpool, linear");
   if (d->cut < 1 || d->cut > d->n_layers - 2) return gcpsl_fail(GCPSL_EINVAL, "cut outside the model");
   if ((int64_t)d->B * d->H * d->W > INT32_MAX / 4) return gcpsl_fail(GCPSL_EUNSUPPORTED, "batch too large");
@@ -80,6 +83,7 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   p.esz = d->dtype == GCPSL_BF16 ? 2 : 4;
   p.K = d->K; p.C = d->C; p.B = d->B; p.L = d->L; p.H = d->H; p.W = d->W; p.Cin = d->Cin;
   p.n_examples = d->n_examples;
+  p.schedule = d->schedule;
   p.max_steps = d->max_steps;
   p.max_window = d->max_window;
   const int n = d->n_layers;
@@ -158,6 +162,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   p.off_off = take(sizeof(int64_t) * (C + 1));
   p.off_coe = take(sizeof(int32_t) * p.n_examples);
   p.off_fw = take(sizeof(double) * C);
+  p.off_order = take(sizeof(int32_t) * C);  // clusters by epoch rounds, descending
+  p.off_ident = take(sizeof(int32_t) * C);  // 0, 1, ..., C-1
   p.off_hits = take(sizeof(int32_t) * p.max_steps * C);
   p.off_idx = take(sizeof(int32_t) * (size_t)p.max_window * C * B);
   p.off_y = take(sizeof(int32_t) * (size_t)p.max_window * C * B);
@@ -210,8 +216,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
         // pick the split count that minimises (rounds of 256 x per_cu
         // workgroups) x (k tiles per workgroup + the cost of writing and
         // re-reading a partial tile, about 16 k tiles)
-        int bk, per_cu;
-        wgrad_lds_tile(l.Co, &bm, &bn, &bk, &per_cu);
+        int tile_bk, per_cu;
+        wgrad_lds_tile(l.Co, &bm, &bn, &tile_bk, &per_cu);
         const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
         const int64_t slots = 256 * (int64_t)per_cu;
         int64_t best = -1;
@@ -261,6 +267,9 @@ struct gcpsl_ctx {
   Plan plan;
   gcpsl_desc desc;
   std::vector<int64_t> sizes;
+  std::vector<int64_t> rounds;  // r_n = floor(n_n / B)
+  std::vector<int32_t> order;   // clusters by r_n descending, then index
+  int64_t R = 0;                // max_n r_n: slots of a system epoch
   char *ws = nullptr;
   int64_t staged_lo = -1;
   int staged_n = 0;
@@ -382,6 +391,17 @@ extern "C" int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out) {
   HIP_TRY(hipMemcpy(ws + p.off_coe, d->client_of_example, sizeof(int32_t) * d->n_examples, hipMemcpyHostToDevice));
   HIP_TRY(hipMemcpy(ws + p.off_fw, fw.data(), sizeof(double) * fw.size(), hipMemcpyHostToDevice));
   HIP_TRY(hipMemset(ws + p.off_hits, 0, sizeof(int32_t) * p.max_steps * p.C));
+  // epoch schedule: the clusters taking a round at slot t are those with
+  // r_n > t, a prefix of `order`
+  std::vector<int64_t> rounds(p.C);
+  std::vector<int32_t> order(p.C), ident(p.C);
+  for (int n = 0; n < p.C; ++n) {
+    rounds[n] = sizes[n] / p.B;
+    order[n] = ident[n] = n;
+  }
+  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return rounds[a] > rounds[b]; });
+  HIP_TRY(hipMemcpy(ws + p.off_order, order.data(), sizeof(int32_t) * p.C, hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(ws + p.off_ident, ident.data(), sizeof(int32_t) * p.C, hipMemcpyHostToDevice));
   gcpsl_ctx *ctx = new gcpsl_ctx();
   ctx->plan = std::move(p);
   ctx->desc = *d;
@@ -389,6 +409,9 @@ extern "C" int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out) {
   ctx->desc.client_of_example = nullptr;
   ctx->desc.cluster_of_client = nullptr;
   ctx->sizes = std::move(sizes);
+  ctx->R = rounds[order[0]];
+  ctx->rounds = std::move(rounds);
+  ctx->order = std::move(order);
   ctx->ws = ws;
   *out = ctx;
   return GCPSL_OK;
@@ -421,7 +444,8 @@ extern "C" int gcpsl_sample(gcpsl_ctx *ctx, int64_t step, int32_t nsteps, int32_
   LAUNCH_T("sample", 0.0, rows * 20.0,
            launch_sample(ctx->at<int32_t>(p.off_ids), ctx->at<int64_t>(p.off_off), ctx->at<int32_t>(p.off_coe),
                          ctx->desc.labels, idx, ctx->at<int32_t>(p.off_y), ctx->at<int32_t>(p.off_hits), p.C, p.B,
-                         p.K, ctx->desc.seed, step, nsteps, p.max_steps, s));
+                         p.K, ctx->desc.seed, step, nsteps, p.max_steps,
+                         p.schedule == GCPSL_SCHED_EPOCH ? ctx->R : 0, s));
   if (p.col0)
     LAUNCH_T(p.dtype == GCPSL_BF16 ? "gather_im2col<bf16>" : "gather_im2col<f32>", 0.0,
              rows * (4.0 + row_elems * 4 + (double)p.H * p.W * p.Kc * p.esz),
@@ -438,19 +462,20 @@ extern "C" int gcpsl_sample(gcpsl_ctx *ctx, int64_t step, int32_t nsteps, int32_
   return GCPSL_OK;
 }
 
-extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *stream) {
-  gcpsl_clear_error();
-  if (!ctx) return gcpsl_fail(GCPSL_EINVAL, "null context");
-  if (ctx->staged_lo < 0 || step < ctx->staged_lo || step >= ctx->staged_lo + ctx->staged_n)
-    return gcpsl_fail(GCPSL_ESTATE, "step " + std::to_string(step) + " has not been sampled");
+namespace {
+
+// One local round of the replicas listed in rmap (device, nrep entries; null
+// = replicas 0..nrep-1): every launch runs nrep replica slots.  The split-K
+// plan of each layer is fixed at create, so a replica's arithmetic does not
+// depend on which other replicas share the launches.
+int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float *loss_out, hipStream_t s) {
   const Plan &p = ctx->plan;
   const gcpsl_desc &d = ctx->desc;
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const int C = p.C, B = p.B, n = (int)p.ly.size();
+  const int C = nrep, B = p.B, n = (int)p.ly.size();
   const int64_t slot = step - ctx->staged_lo;
   char *ws = ctx->ws;
   const void *x_in = ws + p.off_x + (size_t)p.esz * slot * p.x_rs;
-  const int32_t *y = ctx->at<int32_t>(p.off_y) + slot * C * B;
+  const int32_t *y = ctx->at<int32_t>(p.off_y) + slot * p.C * B;
   float *grad = ctx->at<float>(p.off_grad);
   float *loss = loss_out ? loss_out : ctx->at<float>(p.off_loss);
 
@@ -460,7 +485,7 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
     if (l.spec.kind != GCPSL_CONV3X3) continue;
     const double pb = (double)C * (4.0 * l.nw + p.esz * ((double)l.Co * l.Kp + (i > 0 ? (double)l.Ci * l.Kdp : 0.0)));
     LAUNCH_T("prep_weights", 0.0, pb,
-             launch_prep_weights(p.dtype, d.theta, p.P, C, l.w_off, l.Co, l.Ci, ws + l.wf_off, l.Kp,
+             launch_prep_weights(p.dtype, d.theta, p.P, C, rmap, l.w_off, l.Co, l.Ci, ws + l.wf_off, l.Kp,
                                  i > 0 ? ws + l.wd_off : nullptr, l.Kdp, s));
   }
 
@@ -487,6 +512,7 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
       a.out_rs = l.act_rs;
       a.bias_rs = p.P;
       a.C = C;
+      a.rmap = rmap;
       a.epi = EPI_FWD;
       std::string lab;
       const double M = (double)B * l.H * l.W;
@@ -498,17 +524,17 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
     } else if (kind == GCPSL_MAXPOOL2) {
       if (!l.stored) continue;  // fused into the head
       LAUNCH_T("maxpool_fwd", 0.0, 1.25 * p.esz * (double)C * B * l.H * l.W * l.Ci,
-               launch_maxpool_fwd(p.dtype, input_of(i), ws + l.act_off, C, B, l.H, l.W, l.Ci, s));
+               launch_maxpool_fwd(p.dtype, input_of(i), ws + l.act_off, C, rmap, B, l.H, l.W, l.Ci, s));
     } else if (kind == GCPSL_AVGPOOL) {
       const LayerInfo &hc = p.ly[p.head_conv];
       LAUNCH_T("head_pool", 0.0, (double)p.esz * C * B * hc.Co * ((double)hc.Ho * hc.Wo + 1),
-               launch_head_pool(p.dtype, ws + hc.act_off, ws + l.act_off, C, B, hc.Ho, hc.Wo, hc.Co,
+               launch_head_pool(p.dtype, ws + hc.act_off, ws + l.act_off, C, rmap, B, hc.Ho, hc.Wo, hc.Co,
                                 p.head_maxpool ? 1 : 0, s));
     } else if (kind == GCPSL_LINEAR) {
       LAUNCH_T("linear_ce", 6.0 * C * B * l.Ci * l.Co,
                (double)C * (p.esz * B * l.Ci + 4.0 * (2.0 * l.nw + B * l.Ci + B)),
                launch_linear_ce(p.dtype, ws + p.ly[p.avg_idx].act_off, y, d.theta, p.P, l.w_off, l.b_off, grad,
-                                ctx->at<float>(p.off_dh), loss, C, B, l.Ci, l.Co, s));
+                                ctx->at<float>(p.off_dh), loss, C, rmap, B, l.Ci, l.Co, s));
     }
   }
 
@@ -516,7 +542,7 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
   {
     const LayerInfo &hc = p.ly[p.head_conv];
     LAUNCH_T("head_pool_bwd", 0.0, (double)C * B * hc.Co * (2.0 * p.esz * hc.Ho * hc.Wo + 4.0),
-             launch_head_pool_bwd(p.dtype, ws + hc.act_off, ctx->at<float>(p.off_dh), ws + hc.gpre_off, C, B,
+             launch_head_pool_bwd(p.dtype, ws + hc.act_off, ctx->at<float>(p.off_dh), ws + hc.gpre_off, C, rmap, B,
                                   hc.Ho, hc.Wo, hc.Co, p.head_maxpool ? 1 : 0, s));
   }
   int i = p.head_conv;
@@ -534,14 +560,15 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
     w.g_rs = (int64_t)B * l.H * l.W * l.Co;
     w.x_rs = (int64_t)B * l.H * l.W * w.Ci;
     w.C = C;
+    w.rmap = rmap;
     w.splits = l.splits;
     w.chunk = l.chunk;
     if (l.splits == 1) {
       w.dw = grad + l.w_off; w.dw_rs = p.P; w.dw_ss = 0;
       w.db = grad + l.b_off; w.db_rs = p.P; w.db_ss = 0;
     } else {
-      w.dw = ctx->at<float>(p.off_part); w.dw_rs = l.nw; w.dw_ss = (int64_t)C * l.nw;
-      w.db = ctx->at<float>(p.off_dbpart); w.db_rs = l.Co; w.db_ss = (int64_t)C * l.Co;
+      w.dw = ctx->at<float>(p.off_part); w.dw_rs = l.nw; w.dw_ss = (int64_t)p.C * l.nw;
+      w.db = ctx->at<float>(p.off_dbpart); w.db_rs = l.Co; w.db_ss = (int64_t)p.C * l.Co;
     }
     {
       std::string lab;
@@ -555,7 +582,7 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
     if (l.splits > 1)
       LAUNCH_T("wgrad_reduce", 0.0, 4.0 * C * (l.nw + l.Co) * (l.splits + 1.0),
                launch_wgrad_reduce(w.dw, w.db, l.splits, w.dw_ss, w.dw_rs, w.db_ss, w.db_rs, grad, p.P, l.w_off,
-                                   l.b_off, l.nw, l.Co, C, s));
+                                   l.b_off, l.nw, l.Co, C, rmap, s));
     if (i == 0) break;
     // input gradient (the cut gradient when layer i-1 is the client's last pool)
     const LayerInfo &prev = p.ly[i - 1];
@@ -573,6 +600,7 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
     a.out_rs = (int64_t)B * l.H * l.W * l.Ci;
     a.bias_rs = 0;
     a.C = C;
+    a.rmap = rmap;
     a.epi = EPI_DGRAD;
     a.taps = 9;
     {
@@ -588,7 +616,7 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
     if (through_pool) {
       const LayerInfo &pc = p.ly[i - 2];
       LAUNCH_T("maxpool_bwd", 0.0, 2.25 * p.esz * (double)C * B * pc.Ho * pc.Wo * pc.Co,
-               launch_maxpool_bwd(p.dtype, ws + pc.act_off, ws + l.gin_off, ws + pc.gpre_off, C, B, pc.Ho, pc.Wo,
+               launch_maxpool_bwd(p.dtype, ws + pc.act_off, ws + l.gin_off, ws + pc.gpre_off, C, rmap, B, pc.Ho, pc.Wo,
                                   pc.Co, s));
       i -= 2;
     } else {
@@ -597,8 +625,52 @@ extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *s
   }
 
   LAUNCH_T("sgd", 3.0 * C * p.P, 20.0 * C * p.P,
-           launch_sgd(d.theta, d.momentum_buf, grad, (int64_t)C * p.P, d.lr, d.momentum, s));
+           launch_sgd(d.theta, d.momentum_buf, grad, p.P, C, rmap, d.lr, d.momentum, s));
   ctx->horizon = std::max<int64_t>(ctx->horizon, std::min<int64_t>(step + 1, p.max_steps));
+  return GCPSL_OK;
+}
+
+int check_staged(gcpsl_ctx *ctx, int64_t step) {
+  if (ctx->staged_lo < 0 || step < ctx->staged_lo || step >= ctx->staged_lo + ctx->staged_n)
+    return gcpsl_fail(GCPSL_ESTATE, "step " + std::to_string(step) + " has not been sampled");
+  return GCPSL_OK;
+}
+
+// Whether cluster n takes a local round at this step.
+bool takes_round(const gcpsl_ctx *ctx, int64_t step, int n) {
+  return ctx->plan.schedule != GCPSL_SCHED_EPOCH || step % ctx->R < ctx->rounds[n];
+}
+
+}  // namespace
+
+extern "C" int gcpsl_step(gcpsl_ctx *ctx, int64_t step, float *loss_out, void *stream) {
+  gcpsl_clear_error();
+  if (!ctx) return gcpsl_fail(GCPSL_EINVAL, "null context");
+  if (int rc = check_staged(ctx, step)) return rc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const Plan &p = ctx->plan;
+  if (p.schedule != GCPSL_SCHED_EPOCH) return run_round(ctx, step, nullptr, p.C, loss_out, s);
+  int nrep = 0;
+  while (nrep < p.C && takes_round(ctx, step, ctx->order[nrep])) ++nrep;
+  return run_round(ctx, step, ctx->at<int32_t>(p.off_order), nrep, loss_out, s);
+}
+
+extern "C" int gcpsl_step_replica(gcpsl_ctx *ctx, int64_t step, int32_t replica, float *loss_out, void *stream) {
+  gcpsl_clear_error();
+  if (!ctx) return gcpsl_fail(GCPSL_EINVAL, "null context");
+  if (replica < 0 || replica >= ctx->plan.C) return gcpsl_fail(GCPSL_EINVAL, "replica outside [0, C)");
+  if (int rc = check_staged(ctx, step)) return rc;
+  if (!takes_round(ctx, step, replica))
+    return gcpsl_fail(GCPSL_EINVAL, "cluster " + std::to_string(replica) + " waits at step " + std::to_string(step));
+  return run_round(ctx, step, ctx->at<int32_t>(ctx->plan.off_ident) + replica, 1, loss_out,
+                   reinterpret_cast<hipStream_t>(stream));
+}
+
+extern "C" int gcpsl_epoch_rounds(gcpsl_ctx *ctx, int64_t *rounds, int64_t *slots) {
+  gcpsl_clear_error();
+  if (!ctx || !rounds || !slots) return gcpsl_fail(GCPSL_EINVAL, "null argument");
+  std::copy(ctx->rounds.begin(), ctx->rounds.end(), rounds);
+  *slots = ctx->R;
   return GCPSL_OK;
 }
 

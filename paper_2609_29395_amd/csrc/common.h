@@ -65,3 +65,11 @@ __device__ __forceinline__ uint32_t xcd_swizzle(uint32_t L, uint32_t total) {
   if (L >= t8) return L;
   return (L & 7u) * (t8 >> 3) + (L >> 3);
 }
+
+// ------------------------------------------------------- replica selection
+// A launch runs the replicas listed in rmap (device, one entry per replica
+// slot of its grid); a null rmap runs replica z in slot z.  The result is
+// workgroup-uniform.
+__device__ __forceinline__ int replica_of(const int32_t *rmap, int z) {
+  return rmap ? __builtin_amdgcn_readfirstlane(rmap[z]) : z;
+}

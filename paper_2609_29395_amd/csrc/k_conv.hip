@@ -140,7 +140,7 @@ conv_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT
   const int nt = __builtin_amdgcn_readfirstlane((int)(t % (uint32_t)NT));
   const uint32_t rest = t / (uint32_t)NT;
   const int mt = __builtin_amdgcn_readfirstlane((int)(rest % (uint32_t)MT));
-  const int rep = __builtin_amdgcn_readfirstlane((int)(rest / (uint32_t)MT));
+  const int rep = replica_of(a.rmap, __builtin_amdgcn_readfirstlane((int)(rest / (uint32_t)MT)));
   const int M = a.Bt * a.H * a.W;
   const int m0 = mt * BM, n0 = nt * BN;
   const T *src = reinterpret_cast<const T *>(a.src) + rep * a.src_rs;
@@ -395,7 +395,7 @@ wgrad_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int 
   const int mt = __builtin_amdgcn_readfirstlane((int)(rest % (uint32_t)MT));
   rest /= (uint32_t)MT;
   const int split = __builtin_amdgcn_readfirstlane((int)(rest % (uint32_t)a.splits));
-  const int rep = __builtin_amdgcn_readfirstlane((int)(rest / (uint32_t)a.splits));
+  const int rep = replica_of(a.rmap, __builtin_amdgcn_readfirstlane((int)(rest / (uint32_t)a.splits)));
   const int M = a.Bt * a.H * a.W;
   const int NW = a.taps == 1 ? a.Ci : 9 * a.Ci;  // columns of the (padded) im2col operand
   const int p_begin = split * a.chunk;

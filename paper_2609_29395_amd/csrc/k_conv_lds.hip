@@ -180,7 +180,7 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   const int nt = __builtin_amdgcn_readfirstlane((int)(t % (uint32_t)NT));
   const uint32_t rest = t / (uint32_t)NT;
   const int mt = __builtin_amdgcn_readfirstlane((int)(rest % (uint32_t)MT));
-  const int rep = __builtin_amdgcn_readfirstlane((int)(rest / (uint32_t)MT));
+  const int rep = replica_of(a.rmap, __builtin_amdgcn_readfirstlane((int)(rest / (uint32_t)MT)));
   const int M = a.Bt * a.H * a.W;
   const int m0 = mt * BM, n0 = nt * BN;
   const bf16_t *src = reinterpret_cast<const bf16_t *>(a.src) + rep * a.src_rs;

@@ -1,4 +1,6 @@
 // Sampling, gather, pools, the classifier head, SGD and fusion kernels.
+#include <algorithm>
+
 #include "rng.h"
 #include "runtime.h"
 
@@ -7,15 +9,20 @@ namespace {
 constexpr int kMaxBitmapWords = 2048;  // clients tracked per cluster: K <= 65536
 
 // ---------------------------------------------------------------- sampling
-// Eq. 1 / Eq. 3: cluster n's batch at local round `step` is B distinct
+// Eq. 1 / Eq. 3: cluster n's batch at its local round s is B distinct
 // examples of its own pool: positions [tB, (t+1)B) of the keyed permutation
-// of epoch e = step / S_n, S_n = floor(n_n / B).  Also counts the distinct
-// clients of the batch, |A_{n,t}| (Sec. III-A).
+// of epoch e = s / S_n, t = s mod S_n, S_n = floor(n_n / B).  Also counts the
+// distinct clients of the batch, |A_{n,t}| (Sec. III-A).
+// Lockstep schedule (R = 0): every cluster takes its round s = step at every
+// step.  Epoch-barrier schedule (R = max_n S_n slots per system epoch,
+// Sec. III-A, Sec. IV-D): step = m R + t is slot t of system epoch m; cluster
+// n takes its round m S_n + t (epoch m, position t) when t < S_n and waits
+// otherwise -- no batch (ids and labels -1) and no participating client.
 __global__ void __launch_bounds__(256)
 sample_kernel(const int32_t *__restrict__ ids, const int64_t *__restrict__ off,
               const int32_t *__restrict__ coe, const int32_t *__restrict__ labels,
               int32_t *__restrict__ idx, int32_t *__restrict__ y, int32_t *__restrict__ hits,
-              int C, int B, int K, uint64_t seed, int64_t step0, int64_t max_steps) {
+              int C, int B, int K, uint64_t seed, int64_t step0, int64_t max_steps, int64_t R) {
   __shared__ uint32_t bitmap[kMaxBitmapWords];
   __shared__ int count;
   const int n = blockIdx.x, j = blockIdx.y, tid = threadIdx.x;
@@ -23,7 +30,16 @@ sample_kernel(const int32_t *__restrict__ ids, const int64_t *__restrict__ off,
   const int64_t lo = off[n];
   const uint32_t nn = (uint32_t)(off[n + 1] - lo);
   const int64_t S = nn / (uint32_t)B;
-  const int64_t e = step / S, t = step % S;
+  const int64_t e = R > 0 ? step / R : step / S, t = R > 0 ? step % R : step % S;
+  if (t >= S) {  // waits at the epoch barrier
+    for (int i = tid; i < B; i += blockDim.x) {
+      const int64_t o = ((int64_t)j * C + n) * B + i;
+      idx[o] = -1;
+      y[o] = -1;
+    }
+    if (tid == 0 && step < max_steps) hits[step * C + n] = 0;
+    return;
+  }
   const uint64_t key = gc_sample_key(seed, (uint64_t)n, (uint64_t)e);
   const int words = (K + 31) >> 5;
   for (int w = tid; w < words; w += blockDim.x) bitmap[w] = 0u;
@@ -51,6 +67,7 @@ __global__ void __launch_bounds__(256)
 gather_kernel(const float *__restrict__ images, const int32_t *__restrict__ idx, T *__restrict__ x,
               int64_t row_elems) {
   const int64_t row = blockIdx.x;
+  if (idx[row] < 0) return;  // cluster waits at the epoch barrier
   const float *src = images + (int64_t)idx[row] * row_elems;
   T *dst = x + row * row_elems;
   if ((row_elems & 3) == 0) {
@@ -81,6 +98,7 @@ gather_im2col_kernel(const float *__restrict__ images, const int32_t *__restrict
   extern __shared__ float img[];
   constexpr int VEC = ElemT<T>::VEC;
   const int64_t row = blockIdx.x;
+  if (idx[row] < 0) return;  // cluster waits at the epoch barrier
   const int64_t n = (int64_t)H * W * Cin;
   const float *src = images + (int64_t)idx[row] * n;
   if (use_lds) {
@@ -110,6 +128,85 @@ gather_im2col_kernel(const float *__restrict__ images, const int32_t *__restrict
   }
 }
 
+// The same staging for a compile-time channel count CIN and row width KC
+// (the 3-channel image layer).  The image sits in LDS with a one-pixel zero
+// border, so no tap needs a bounds test.  A workgroup stages several
+// examples in turn: while it writes the rows of one example from LDS, the
+// 16-byte loads of the next example's image (NV4 per thread) are already in
+// flight.  A thread always fills the same VEC-column chunk of a row (the
+// thread count is a multiple of the chunks per row), so its VEC source
+// offsets are computed once; lanes of a wave write consecutive 16-byte chunks
+// of consecutive pixels.
+template <typename T, int CIN, int KC, int NV4>
+__global__ void __launch_bounds__(256)
+gather_im2col_fixed_kernel(const float *__restrict__ images, const int32_t *__restrict__ idx,
+                           T *__restrict__ x, int H, int W, FastDiv fd_w, int64_t rows, int per_wg) {
+  extern __shared__ float img[];  // [(H + 2) * (W + 2) * CIN]
+  constexpr int VEC = ElemT<T>::VEC, NCH = KC / VEC;
+  static_assert(KC % VEC == 0 && KC >= 9 * CIN, "row width");
+  const int nthr = (blockDim.x / NCH) * NCH;
+  const int tid = threadIdx.x;
+  const int Wp = W + 2, npad = (H + 2) * Wp * CIN, n4 = H * W * CIN / 4;
+  const int64_t r0 = (int64_t)blockIdx.x * per_wg;
+  const int64_t r1 = min(rows, r0 + per_wg);
+  for (int i = tid; i < npad; i += blockDim.x) img[i] = 0.f;  // the border stays zero
+  const int j = tid % NCH;
+  int off[VEC];  // source offsets; columns past 9 CIN read offset 0 and are zeroed
+  uint32_t live = 0;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    const int k = j * VEC + e;
+    const int rs = k / CIN, c = k - rs * CIN;
+    off[e] = k < 9 * CIN ? ((rs / 3) * Wp + rs % 3) * CIN + c : 0;
+    live |= (k < 9 * CIN ? 1u : 0u) << e;
+  }
+  float4 pre[NV4];
+  auto fetch = [&](int64_t row) {
+    const float4 *src = reinterpret_cast<const float4 *>(images + (int64_t)idx[row] * (4 * n4));
+#pragma unroll
+    for (int u = 0; u < NV4; ++u) {
+      const int v = tid + u * 256;
+      if (v < n4) pre[u] = src[v];
+    }
+  };
+  // rows without a batch (a cluster waiting at the epoch barrier) are skipped
+  if (r0 < r1 && idx[r0] >= 0) fetch(r0);
+  for (int64_t row = r0; row < r1; ++row) {
+    const bool has_batch = idx[row] >= 0;
+    __syncthreads();  // the previous example's reads of LDS are done
+#pragma unroll
+    for (int u = 0; u < NV4; ++u) {
+      const int v = tid + u * 256;
+      if (has_batch && v < n4) {
+        const float f[4] = {pre[u].x, pre[u].y, pre[u].z, pre[u].w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int i = 4 * v + t;
+          const int q = i / CIN, c = i - q * CIN;
+          const int h = (int)fdiv((uint32_t)q, fd_w), w = q - h * W;
+          img[((h + 1) * Wp + w + 1) * CIN + c] = f[t];
+        }
+      }
+    }
+    __syncthreads();
+    if (row + 1 < r1 && idx[row + 1] >= 0) fetch(row + 1);
+    if (has_batch && tid < nthr) {
+      T *dst = x + row * (int64_t)H * W * KC + j * VEC;
+      for (int p = tid / NCH; p < H * W; p += nthr / NCH) {
+        const int h = (int)fdiv((uint32_t)p, fd_w), w = p - h * W;
+        const float *base = img + (h * Wp + w) * CIN;
+        struct { T v[VEC]; } pk;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const float v = base[off[e]];
+          pk.v[e] = ElemT<T>::from_f(((live >> e) & 1u) ? v : 0.f);
+        }
+        *reinterpret_cast<uint4 *>(dst + (int64_t)p * KC) = __builtin_bit_cast(uint4, pk);
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------ weight preparation
 // Compute copies of one conv layer's weights from the fp32 masters:
 //   wf[co][k], k = (r, s, ci) < 9 ci, rows zero-padded to Kp (forward);
@@ -119,25 +216,22 @@ gather_im2col_kernel(const float *__restrict__ images, const int32_t *__restrict
 // tap, staged through LDS so both the reads and the writes are coalesced.
 template <typename T>
 __global__ void __launch_bounds__(256)
-prep_wf_kernel(const float *__restrict__ theta, int64_t P, int64_t w_off, int co, int ci,
-               T *__restrict__ wf, int Kp) {
-  const int rep = blockIdx.y;
-  const float *w = theta + rep * P + w_off;
+prep_wf_kernel(const float *__restrict__ theta, const int32_t *__restrict__ rmap, int64_t P, int64_t w_off, int co,
+               int ci, T *__restrict__ wf, int Kp) {
+  // one output row (blockIdx.x) of one replica (slot blockIdx.y) per workgroup
+  const int rep = replica_of(rmap, blockIdx.y), n = blockIdx.x;
   const int K = 9 * ci;
-  const int64_t nf = (int64_t)co * Kp;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nf;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int n = (int)(i / Kp), k = (int)(i % Kp);
-    wf[rep * nf + i] = ElemT<T>::from_f(k < K ? w[(int64_t)n * K + k] : 0.f);
-  }
+  const float *w = theta + rep * P + w_off + (int64_t)n * K;
+  T *dst = wf + ((int64_t)rep * co + n) * Kp;
+  for (int k = threadIdx.x; k < Kp; k += blockDim.x) dst[k] = ElemT<T>::from_f(k < K ? w[k] : 0.f);
 }
 
 template <typename T>
 __global__ void __launch_bounds__(256)
-prep_wd_kernel(const float *__restrict__ theta, int64_t P, int64_t w_off, int co, int ci,
-               T *__restrict__ wd, int Kdp) {
+prep_wd_kernel(const float *__restrict__ theta, const int32_t *__restrict__ rmap, int64_t P, int64_t w_off, int co,
+               int ci, T *__restrict__ wd, int Kdp) {
   __shared__ float tile[64][65];
-  const int rep = blockIdx.z;
+  const int rep = replica_of(rmap, blockIdx.z);
   const int tap = blockIdx.y;  // (r', s') of the flipped kernel
   const int nco = (co + 63) / 64;
   const int cb = blockIdx.x % nco, ib = blockIdx.x / nco;
@@ -166,97 +260,176 @@ prep_wd_kernel(const float *__restrict__ theta, int64_t P, int64_t w_off, int co
 }
 
 // -------------------------------------------------------------- max pool
-// 2x2 / stride 2 over a [N][H][W][Ch] batch (N = C * B).  The backward pass
+// 2x2 / stride 2 over a [N][H][W][Ch] batch (N examples).  The backward pass
 // routes each pooled gradient to the first maximum of its window in
 // row-major order (strict >) and applies the producing conv's ReLU mask
-// (output > 0).
+// (output > 0).  A thread handles one 16-byte vector of VEC channels of one
+// output position; index arithmetic is 32-bit (the launcher splits the batch
+// so a launch stays below 2^31 vectors).
+
+// One 16-byte vector of activations.
+template <typename T> struct Vec16 {
+  T v[ElemT<T>::VEC];
+};
+template <typename T>
+__device__ __forceinline__ Vec16<T> ld16(const T *p) {
+  return __builtin_bit_cast(Vec16<T>, *reinterpret_cast<const uint4 *>(p));
+}
+template <typename T>
+__device__ __forceinline__ void st16(T *p, const Vec16<T> &v) {
+  *reinterpret_cast<uint4 *>(p) = __builtin_bit_cast(uint4, v);
+}
+
+// Output vector i of a pooled [N][Ho][Wo][CV] grid -> offset of the top-left
+// input element of its window, the example and the channel vector.
+struct PoolIdx {
+  FastDiv cv, wo, ho;
+};
+__device__ __forceinline__ int64_t pool_base(uint32_t i, const PoolIdx &d, int W, int Ch, int VEC, uint32_t *bi,
+                                             int *cv) {
+  const uint32_t r = fdiv(i, d.cv);
+  *cv = (int)(i - r * d.cv.d);
+  const uint32_t r2 = fdiv(r, d.wo);
+  const int wo = (int)(r - r2 * d.wo.d);
+  *bi = fdiv(r2, d.ho);
+  const int ho = (int)(r2 - *bi * d.ho.d);
+  return (((int64_t)*bi * (2 * d.ho.d) + 2 * ho) * W + 2 * wo) * Ch + *cv * VEC;
+}
+
 template <typename T>
 __global__ void __launch_bounds__(256)
-maxpool_fwd_kernel(const T *__restrict__ x, T *__restrict__ z, int64_t total, int H, int W, int Ch) {
-  const int Ho = H >> 1, Wo = W >> 1;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int c = (int)(i % Ch);
-    int64_t r = i / Ch;
-    const int wo = (int)(r % Wo);
-    r /= Wo;
-    const int ho = (int)(r % Ho);
-    const int64_t bi = r / Ho;
-    const int64_t base = ((bi * H + 2 * ho) * W + 2 * wo) * Ch + c;
-    float m = ElemT<T>::to_f(x[base]);
-    T best = x[base];
-    const int64_t o[3] = {base + Ch, base + (int64_t)W * Ch, base + (int64_t)W * Ch + Ch};
+maxpool_fwd_kernel(const T *__restrict__ x, T *__restrict__ z, const int32_t *__restrict__ rmap, int64_t x_rs,
+                   int64_t z_rs, uint32_t total, PoolIdx d, int W, int Ch) {
+  constexpr int VEC = ElemT<T>::VEC;
+  const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+  if (i >= total) return;
+  const int rep = replica_of(rmap, blockIdx.y);
+  x += rep * x_rs;
+  z += rep * z_rs;
+  uint32_t bi;
+  int cv;
+  const int64_t base = pool_base(i, d, W, Ch, VEC, &bi, &cv);
+  const Vec16<T> q[4] = {ld16(x + base), ld16(x + base + Ch), ld16(x + base + (int64_t)W * Ch),
+                         ld16(x + base + (int64_t)W * Ch + Ch)};
+  Vec16<T> out;
 #pragma unroll
-    for (int q = 0; q < 3; ++q) {
-      const float v = ElemT<T>::to_f(x[o[q]]);
+  for (int e = 0; e < VEC; ++e) {
+    float m = ElemT<T>::to_f(q[0].v[e]);
+    T best = q[0].v[e];
+#pragma unroll
+    for (int k = 1; k < 4; ++k) {
+      const float v = ElemT<T>::to_f(q[k].v[e]);
       if (v > m) {
         m = v;
-        best = x[o[q]];
+        best = q[k].v[e];
       }
     }
-    z[i] = best;
+    out.v[e] = best;
   }
+  st16(z + (int64_t)i * VEC, out);
+}
+
+// gpre over the window of output vector i: the gradient g[e] goes to the
+// first maximum of a (if it is > 0), zero elsewhere.
+template <typename T>
+__device__ __forceinline__ void route_window(const T *__restrict__ a, T *__restrict__ gpre, int64_t base, int W,
+                                             int Ch, const Vec16<T> &g) {
+  constexpr int VEC = ElemT<T>::VEC;
+  const int64_t o[4] = {base, base + Ch, base + (int64_t)W * Ch, base + (int64_t)W * Ch + Ch};
+  Vec16<T> q[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) q[k] = ld16(a + o[k]);
+  Vec16<T> out[4];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    float v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = ElemT<T>::to_f(q[k].v[e]);
+    int arg = 0;
+#pragma unroll
+    for (int k = 1; k < 4; ++k)
+      if (v[k] > v[arg]) arg = k;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) out[k].v[e] = (k == arg && v[k] > 0.f) ? g.v[e] : T(0);
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) st16(gpre + o[k], out[k]);
 }
 
 template <typename T>
 __global__ void __launch_bounds__(256)
 maxpool_bwd_kernel(const T *__restrict__ a, const T *__restrict__ gz, T *__restrict__ gpre,
-                   int64_t total, int H, int W, int Ch) {
-  const int Ho = H >> 1, Wo = W >> 1;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int c = (int)(i % Ch);
-    int64_t r = i / Ch;
-    const int wo = (int)(r % Wo);
-    r /= Wo;
-    const int ho = (int)(r % Ho);
-    const int64_t bi = r / Ho;
-    const int64_t base = ((bi * H + 2 * ho) * W + 2 * wo) * Ch + c;
-    const int64_t o[4] = {base, base + Ch, base + (int64_t)W * Ch, base + (int64_t)W * Ch + Ch};
-    float v[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = ElemT<T>::to_f(a[o[q]]);
-    int arg = 0;
-#pragma unroll
-    for (int q = 1; q < 4; ++q)
-      if (v[q] > v[arg]) arg = q;
-    const T g = gz[i];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) gpre[o[q]] = (q == arg && v[q] > 0.f) ? g : T(0);
-  }
+                   const int32_t *__restrict__ rmap, int64_t a_rs, int64_t z_rs, uint32_t total, PoolIdx d, int W,
+                   int Ch) {
+  constexpr int VEC = ElemT<T>::VEC;
+  const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+  if (i >= total) return;
+  const int rep = replica_of(rmap, blockIdx.y);
+  a += rep * a_rs;
+  gpre += rep * a_rs;
+  gz += rep * z_rs;
+  uint32_t bi;
+  int cv;
+  const int64_t base = pool_base(i, d, W, Ch, VEC, &bi, &cv);
+  route_window(a, gpre, base, W, Ch, ld16(gz + (int64_t)i * VEC));
 }
 
 // ------------------------------------------------------------------ head
-// Pooled feature h[n][c] = mean over positions of (optionally 2x2-max-pooled)
-// last conv output.
+// Pooled feature h[n][c] = mean over positions of the (optionally 2x2 max
+// pooled) last conv output.  One workgroup per (example, block of CVB
+// channel vectors); the positions are split over G = 256 / CVB thread groups
+// whose fp32 partial sums are added in group order.
 template <typename T>
 __global__ void __launch_bounds__(256)
-head_pool_kernel(const T *__restrict__ a, T *__restrict__ h, int64_t total, int H, int W, int Ch,
-                 int maxpool) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int c = (int)(i % Ch);
-    const int64_t bi = i / Ch;
-    const T *src = a + bi * H * W * Ch + c;
-    float s = 0.f;
-    int npos;
-    if (maxpool) {
-      const int Ho = H >> 1, Wo = W >> 1;
-      npos = Ho * Wo;
-      for (int ho = 0; ho < Ho; ++ho)
-        for (int wo = 0; wo < Wo; ++wo) {
-          const int64_t b0 = ((int64_t)(2 * ho) * W + 2 * wo) * Ch;
-          float m = ElemT<T>::to_f(src[b0]);
-          m = fmaxf(m, ElemT<T>::to_f(src[b0 + Ch]));
-          m = fmaxf(m, ElemT<T>::to_f(src[b0 + (int64_t)W * Ch]));
-          m = fmaxf(m, ElemT<T>::to_f(src[b0 + (int64_t)W * Ch + Ch]));
-          s += m;
+head_pool_kernel(const T *__restrict__ a, T *__restrict__ h, const int32_t *__restrict__ rmap, int Bt, int H, int W,
+                 int Ch, int CVB, int maxpool) {
+  constexpr int VEC = ElemT<T>::VEC;
+  __shared__ float part[256 * VEC];
+  const int64_t bi = (int64_t)replica_of(rmap, blockIdx.z) * Bt + blockIdx.x;
+  const int tid = threadIdx.x;
+  const int G = 256 / CVB;
+  const int cvl = tid % CVB, g = tid / CVB;
+  const int cv = blockIdx.y * CVB + cvl;
+  const int CV = Ch / VEC;
+  const T *src = a + (int64_t)bi * H * W * Ch + cv * VEC;
+  const int Wo = maxpool ? W / 2 : W, npos = maxpool ? (H / 2) * (W / 2) : H * W;
+  float sum[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) sum[e] = 0.f;
+  if (g < G && cv < CV) {
+    for (int q = g; q < npos; q += G) {
+      const int ho = q / Wo, wo = q - ho * Wo;
+      if (maxpool) {
+        const int64_t b0 = ((int64_t)(2 * ho) * W + 2 * wo) * Ch;
+        const Vec16<T> v0 = ld16(src + b0), v1 = ld16(src + b0 + Ch), v2 = ld16(src + b0 + (int64_t)W * Ch),
+                       v3 = ld16(src + b0 + (int64_t)W * Ch + Ch);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          float m = ElemT<T>::to_f(v0.v[e]);
+          m = fmaxf(m, ElemT<T>::to_f(v1.v[e]));
+          m = fmaxf(m, ElemT<T>::to_f(v2.v[e]));
+          m = fmaxf(m, ElemT<T>::to_f(v3.v[e]));
+          sum[e] += m;
         }
-    } else {
-      npos = H * W;
-      for (int p = 0; p < npos; ++p) s += ElemT<T>::to_f(src[(int64_t)p * Ch]);
+      } else {
+        const Vec16<T> v = ld16(src + ((int64_t)ho * W + wo) * Ch);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) sum[e] += ElemT<T>::to_f(v.v[e]);
+      }
     }
-    h[i] = ElemT<T>::from_f(s / (float)npos);
+  }
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) part[tid * VEC + e] = sum[e];
+  __syncthreads();
+  if (tid < CVB && cv < CV) {
+    Vec16<T> out;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      float s = 0.f;
+      for (int k = 0; k < G; ++k) s += part[(k * CVB + tid) * VEC + e];
+      out.v[e] = ElemT<T>::from_f(s / (float)npos);
+    }
+    st16(h + (int64_t)bi * Ch + cv * VEC, out);
   }
 }
 
@@ -270,23 +443,26 @@ template <typename T>
 __global__ void __launch_bounds__(1024)
 linear_ce_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
                  const float *__restrict__ theta, int64_t P, int64_t w_off, int64_t b_off,
-                 float *__restrict__ grad, float *__restrict__ dh, float *__restrict__ loss, int Bt,
-                 int Ch, int L) {
+                 float *__restrict__ grad, float *__restrict__ dh, float *__restrict__ loss,
+                 const int32_t *__restrict__ rmap, int Bt, int Ch, int L) {
   extern __shared__ float sh[];
-  float *hs = sh;                      // [Bt][Ch]
-  float *ws = hs + (int64_t)Bt * Ch;   // [L][Ch]
-  float *lg = ws + (int64_t)L * Ch;    // [Bt][L] logits, then dlogits
+  // rows padded to Ch + 1 floats: threads of a wave that read the same
+  // column of different rows hit different banks
+  const int CP = Ch + 1;
+  float *hs = sh;                      // [Bt][CP]
+  float *ws = hs + (int64_t)Bt * CP;   // [L][CP]
+  float *lg = ws + (int64_t)L * CP;    // [Bt][L] logits, then dlogits
   float *lossb = lg + Bt * L;          // [Bt]
-  const int rep = blockIdx.x, tid = threadIdx.x, nt = blockDim.x;
+  const int rep = replica_of(rmap, blockIdx.x), tid = threadIdx.x, nt = blockDim.x;
   const T *hr = h + (int64_t)rep * Bt * Ch;
   const float *Wl = theta + rep * P + w_off;
   const float *bl = theta + rep * P + b_off;
-  for (int i = tid; i < Bt * Ch; i += nt) hs[i] = ElemT<T>::to_f(hr[i]);
-  for (int i = tid; i < L * Ch; i += nt) ws[i] = ElemT<T>::to_f(ElemT<T>::from_f(Wl[i]));
+  for (int i = tid; i < Bt * Ch; i += nt) hs[(i / Ch) * CP + i % Ch] = ElemT<T>::to_f(hr[i]);
+  for (int i = tid; i < L * Ch; i += nt) ws[(i / Ch) * CP + i % Ch] = ElemT<T>::to_f(ElemT<T>::from_f(Wl[i]));
   __syncthreads();
   for (int i = tid; i < Bt * L; i += nt) {
     const int b = i / L, j = i % L;
-    const float *hb = hs + (int64_t)b * Ch, *wj = ws + (int64_t)j * Ch;
+    const float *hb = hs + (int64_t)b * CP, *wj = ws + (int64_t)j * CP;
     float s = bl[j];
     for (int c = 0; c < Ch; ++c) s += hb[c] * wj[c];
     lg[i] = s;
@@ -315,7 +491,7 @@ linear_ce_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
   for (int i = tid; i < L * Ch; i += nt) {
     const int j = i / Ch, c = i % Ch;
     float s = 0.f;
-    for (int b = 0; b < Bt; ++b) s += lg[b * L + j] * hs[(int64_t)b * Ch + c];
+    for (int b = 0; b < Bt; ++b) s += lg[b * L + j] * hs[(int64_t)b * CP + c];
     g[w_off + i] = s;
   }
   for (int j = tid; j < L; j += nt) {
@@ -327,44 +503,52 @@ linear_ce_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
   for (int i = tid; i < Bt * Ch; i += nt) {
     const int b = i / Ch, c = i % Ch;
     float s = 0.f;
-    for (int j = 0; j < L; ++j) s += lg[b * L + j] * ws[(int64_t)j * Ch + c];
+    for (int j = 0; j < L; ++j) s += lg[b * L + j] * ws[(int64_t)j * CP + c];
     dhr[i] = s;
   }
 }
 
 // Gradient of the head pooling, with the last conv's ReLU mask:
-// gpre = mask * route(dh / npos) (route = first maximum if max pooled).
+// gpre = mask * route(dh / npos) (route = first maximum if max pooled).  A
+// thread handles one 16-byte vector of channels of one window (max pooled)
+// or one position.
 template <typename T>
 __global__ void __launch_bounds__(256)
 head_pool_bwd_kernel(const T *__restrict__ a, const float *__restrict__ dh, T *__restrict__ gpre,
-                     int64_t total, int H, int W, int Ch, int maxpool) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int c = (int)(i % Ch);
-    int64_t r = i / Ch;
-    if (maxpool) {
-      const int Ho = H >> 1, Wo = W >> 1;
-      const int wo = (int)(r % Wo);
-      r /= Wo;
-      const int ho = (int)(r % Ho);
-      const int64_t bi = r / Ho;
-      const T g = ElemT<T>::from_f(dh[bi * Ch + c] / (float)(Ho * Wo));
-      const int64_t base = ((bi * H + 2 * ho) * W + 2 * wo) * Ch + c;
-      const int64_t o[4] = {base, base + Ch, base + (int64_t)W * Ch, base + (int64_t)W * Ch + Ch};
-      float v[4];
+                     const int32_t *__restrict__ rmap, int64_t a_rs, int64_t dh_rs, uint32_t total, PoolIdx d, int W,
+                     int Ch, int maxpool) {
+  constexpr int VEC = ElemT<T>::VEC;
+  const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+  if (i >= total) return;
+  const int rep = replica_of(rmap, blockIdx.y);
+  a += rep * a_rs;
+  gpre += rep * a_rs;
+  dh += rep * dh_rs;
+  if (maxpool) {
+    uint32_t bi;
+    int cv;
+    const int64_t base = pool_base(i, d, W, Ch, VEC, &bi, &cv);
+    const float npos = (float)(d.ho.d * d.wo.d);
+    const float *dr = dh + (int64_t)bi * Ch + cv * VEC;
+    Vec16<T> g;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = ElemT<T>::to_f(a[o[q]]);
-      int arg = 0;
+    for (int e = 0; e < VEC; ++e) g.v[e] = ElemT<T>::from_f(dr[e] / npos);
+    route_window(a, gpre, base, W, Ch, g);
+  } else {
+    // d.wo = W, d.ho = H: i = ((bi * H + h) * W + w) * CV + cv
+    const uint32_t r = fdiv(i, d.cv);
+    const int cv = (int)(i - r * d.cv.d);
+    const uint32_t bi = fdiv(fdiv(r, d.wo), d.ho);
+    const float npos = (float)(d.ho.d * d.wo.d);
+    const float *dr = dh + (int64_t)bi * Ch + cv * VEC;
+    const Vec16<T> v = ld16(a + (int64_t)i * VEC);
+    Vec16<T> out;
 #pragma unroll
-      for (int q = 1; q < 4; ++q)
-        if (v[q] > v[arg]) arg = q;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) gpre[o[q]] = (q == arg && v[q] > 0.f) ? g : T(0);
-    } else {
-      const int64_t bi = r / ((int64_t)H * W);
-      const T g = ElemT<T>::from_f(dh[bi * Ch + c] / (float)(H * W));
-      gpre[i] = ElemT<T>::to_f(a[i]) > 0.f ? g : T(0);
+    for (int e = 0; e < VEC; ++e) {
+      const T g = ElemT<T>::from_f(dr[e] / npos);
+      out.v[e] = ElemT<T>::to_f(v.v[e]) > 0.f ? g : T(0);
     }
+    st16(gpre + (int64_t)i * VEC, out);
   }
 }
 
@@ -375,8 +559,8 @@ __global__ void __launch_bounds__(256)
 wgrad_reduce_kernel(const float *__restrict__ dw, const float *__restrict__ db, int splits,
                     int64_t dw_ss, int64_t dw_rs, int64_t db_ss, int64_t db_rs,
                     float *__restrict__ grad, int64_t P, int64_t w_off, int64_t b_off, int64_t nw,
-                    int co) {
-  const int rep = blockIdx.y;
+                    int co, const int32_t *__restrict__ rmap) {
+  const int rep = replica_of(rmap, blockIdx.y);
   for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < nw + co;
        j += (int64_t)gridDim.x * blockDim.x) {
     float s = 0.f;
@@ -392,41 +576,74 @@ wgrad_reduce_kernel(const float *__restrict__ dw, const float *__restrict__ db, 
 }
 
 // ------------------------------------------------------------------- SGD
+// v <- mu v + g; theta <- theta - lr v on the P parameters of the replica of
+// slot blockIdx.y.  VEC divides P, so every replica row stays aligned.
+template <int VEC> struct FVec;
+template <> struct FVec<1> { typedef float T; };
+template <> struct FVec<2> { typedef float2 T; };
+template <> struct FVec<4> { typedef float4 T; };
+
+template <int VEC>
 __global__ void __launch_bounds__(256)
-sgd_kernel(float *__restrict__ theta, float *__restrict__ mom, const float *__restrict__ grad,
-           int64_t n, float lr, float mu) {
-  const int64_t nv = n >> 2;
-  float4 *t4 = reinterpret_cast<float4 *>(theta);
-  float4 *m4 = reinterpret_cast<float4 *>(mom);
-  const float4 *g4 = reinterpret_cast<const float4 *>(grad);
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nv;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    float4 v = m4[i], t = t4[i];
-    const float4 g = g4[i];
-    v.x = mu * v.x + g.x; v.y = mu * v.y + g.y; v.z = mu * v.z + g.z; v.w = mu * v.w + g.w;
-    t.x -= lr * v.x; t.y -= lr * v.y; t.z -= lr * v.z; t.w -= lr * v.w;
+sgd_kernel(float *__restrict__ theta, float *__restrict__ mom, const float *__restrict__ grad, int64_t P,
+           const int32_t *__restrict__ rmap, float lr, float mu) {
+  typedef typename FVec<VEC>::T V;
+  const int64_t base = (int64_t)replica_of(rmap, blockIdx.y) * P;
+  V *t4 = reinterpret_cast<V *>(theta + base);
+  V *m4 = reinterpret_cast<V *>(mom + base);
+  const V *g4 = reinterpret_cast<const V *>(grad + base);
+  const int64_t nv = P / VEC;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nv; i += (int64_t)gridDim.x * blockDim.x) {
+    V v = m4[i], t = t4[i];
+    const V g = g4[i];
+    float *vf = reinterpret_cast<float *>(&v), *tf = reinterpret_cast<float *>(&t);
+    const float *gf = reinterpret_cast<const float *>(&g);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      vf[e] = mu * vf[e] + gf[e];
+      tf[e] -= lr * vf[e];
+    }
     m4[i] = v;
     t4[i] = t;
-  }
-  for (int64_t i = 4 * nv + blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const float v = mu * mom[i] + grad[i];
-    mom[i] = v;
-    theta[i] -= lr * v;
   }
 }
 
 // ---------------------------------------------------------------- fusion
 // Eq. 5: theta_bar[p] = (sum_n w_n theta_n[p]) / W in fp64, in cluster order,
-// rounded once to fp32 and written back to every replica.
+// rounded once to fp32 and written back to every replica.  A thread handles
+// VEC consecutive parameters (VEC divides P, so every replica row stays
+// aligned) and issues the loads of 16 replicas before it accumulates them.
+template <int VEC>
 __global__ void __launch_bounds__(256)
 fuse_kernel(float *__restrict__ theta, const double *__restrict__ w, double W, int C, int64_t P) {
-  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < P;
-       p += (int64_t)gridDim.x * blockDim.x) {
-    double acc = 0.0;
-    for (int n = 0; n < C; ++n) acc += w[n] * (double)theta[n * P + p];
-    const float v = (float)(acc / W);
-    for (int n = 0; n < C; ++n) theta[n * P + p] = v;
+  typedef typename FVec<VEC>::T V;
+  constexpr int U = 16;
+  const int64_t nv = P / VEC;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nv;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    double acc[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] = 0.0;
+    for (int n0 = 0; n0 < C; n0 += U) {
+      V v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (n0 + u < C) v[u] = reinterpret_cast<const V *>(theta + (int64_t)(n0 + u) * P)[i];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (n0 + u < C) {
+          const double wn = w[n0 + u];
+          const float *f = reinterpret_cast<const float *>(&v[u]);
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) acc[e] += wn * (double)f[e];
+        }
+      }
+    }
+    V out;
+    float *o = reinterpret_cast<float *>(&out);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) o[e] = (float)(acc[e] / W);
+    for (int n = 0; n < C; ++n) reinterpret_cast<V *>(theta + (int64_t)n * P)[i] = out;
   }
 }
 
@@ -440,9 +657,9 @@ inline unsigned grid_for(int64_t n, int per = 256, unsigned cap = 65535u * 8u) {
 hipError_t launch_sample(const int32_t *ids, const int64_t *off, const int32_t *coe,
                          const int32_t *labels, int32_t *idx, int32_t *y, int32_t *hits, int C,
                          int B, int K, uint64_t seed, int64_t step0, int nsteps, int64_t max_steps,
-                         hipStream_t s) {
+                         int64_t R, hipStream_t s) {
   hipLaunchKernelGGL(sample_kernel, dim3(C, nsteps), dim3(256), 0, s, ids, off, coe, labels, idx, y,
-                     hits, C, B, K, seed, step0, max_steps);
+                     hits, C, B, K, seed, step0, max_steps, R);
   return hipGetLastError();
 }
 
@@ -459,6 +676,33 @@ hipError_t launch_gather(const float *images, const int32_t *idx, void *x, int d
 
 hipError_t launch_gather_im2col(const float *images, const int32_t *idx, void *x, int dtype, int64_t rows,
                                 int H, int W, int Cin, int Kc, hipStream_t s) {
+  const size_t padded = sizeof(float) * (size_t)(H + 2) * (W + 2) * Cin;
+  const int n4 = (H * W * Cin) / 4, nv4 = (n4 + 255) / 256;
+  if (Cin == 3 && padded <= 64 * 1024 && (H * W * Cin) % 4 == 0 && nv4 <= 4 && rows > 0) {
+    // two examples per workgroup once that still leaves >= 4 workgroups per CU
+    // (measured: 1 per workgroup 4.0 TB/s, 2: 4.5 TB/s, 4: 4.2 TB/s)
+    const int per = rows >= 2048 ? 2 : 1;
+    const dim3 grid((unsigned)((rows + per - 1) / per));
+    const FastDiv fw = make_fastdiv((uint32_t)W);
+#define GIM_GO(TT, KCC, NV)                                                                                    \
+  hipLaunchKernelGGL((gather_im2col_fixed_kernel<TT, 3, KCC, NV>), grid, dim3(256), padded, s, images, idx,   \
+                     (TT *)x, H, W, fw, rows, per)
+#define GIM_NV(TT, KCC)                                                                                        \
+  do {                                                                                                         \
+    if (nv4 == 1) GIM_GO(TT, KCC, 1); else if (nv4 == 2) GIM_GO(TT, KCC, 2);                                   \
+    else if (nv4 == 3) GIM_GO(TT, KCC, 3); else GIM_GO(TT, KCC, 4);                                            \
+  } while (0)
+    if (dtype == GCPSL_BF16 && Kc == 32) {
+      GIM_NV(bf16_t, 32);
+      return hipGetLastError();
+    }
+    if (dtype == GCPSL_F32 && Kc == 28) {
+      GIM_NV(float, 28);
+      return hipGetLastError();
+    }
+#undef GIM_NV
+#undef GIM_GO
+  }
   const size_t img = sizeof(float) * (size_t)H * W * Cin;
   const int use_lds = img <= 64 * 1024 ? 1 : 0;
   const size_t shm = use_lds ? img : 0;
@@ -471,65 +715,95 @@ hipError_t launch_gather_im2col(const float *images, const int32_t *idx, void *x
   return hipGetLastError();
 }
 
-hipError_t launch_prep_weights(int dtype, const float *theta, int64_t P, int C, int64_t w_off,
+hipError_t launch_prep_weights(int dtype, const float *theta, int64_t P, int C, const int32_t *rmap, int64_t w_off,
                                int co, int ci, void *wf, int Kp, void *wd, int Kdp, hipStream_t s) {
-  const dim3 grid(grid_for((int64_t)co * Kp, 256, 4096), C);
+  const dim3 grid((unsigned)co, C);
   const dim3 gridd(((co + 63) / 64) * ((ci + 63) / 64), 9, C);
   if (dtype == GCPSL_BF16) {
-    hipLaunchKernelGGL(prep_wf_kernel<bf16_t>, grid, dim3(256), 0, s, theta, P, w_off, co, ci,
-                       (bf16_t *)wf, Kp);
+    hipLaunchKernelGGL(prep_wf_kernel<bf16_t>, grid, dim3(256), 0, s, theta, rmap, P, w_off, co, ci, (bf16_t *)wf, Kp);
     if (wd)
-      hipLaunchKernelGGL(prep_wd_kernel<bf16_t>, gridd, dim3(256), 0, s, theta, P, w_off, co, ci,
+      hipLaunchKernelGGL(prep_wd_kernel<bf16_t>, gridd, dim3(256), 0, s, theta, rmap, P, w_off, co, ci,
                          (bf16_t *)wd, Kdp);
   } else {
-    hipLaunchKernelGGL(prep_wf_kernel<float>, grid, dim3(256), 0, s, theta, P, w_off, co, ci,
-                       (float *)wf, Kp);
+    hipLaunchKernelGGL(prep_wf_kernel<float>, grid, dim3(256), 0, s, theta, rmap, P, w_off, co, ci, (float *)wf, Kp);
     if (wd)
-      hipLaunchKernelGGL(prep_wd_kernel<float>, gridd, dim3(256), 0, s, theta, P, w_off, co, ci,
-                         (float *)wd, Kdp);
+      hipLaunchKernelGGL(prep_wd_kernel<float>, gridd, dim3(256), 0, s, theta, rmap, P, w_off, co, ci, (float *)wd,
+                         Kdp);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_maxpool_fwd(int dtype, const void *x, void *z, int C, int Bt, int H, int W, int Ch,
-                              hipStream_t s) {
-  const int64_t total = (int64_t)C * Bt * (H / 2) * (W / 2) * Ch;
-  if (dtype == GCPSL_BF16)
-    hipLaunchKernelGGL(maxpool_fwd_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s,
-                       (const bf16_t *)x, (bf16_t *)z, total, H, W, Ch);
-  else
-    hipLaunchKernelGGL(maxpool_fwd_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s,
-                       (const float *)x, (float *)z, total, H, W, Ch);
+static PoolIdx pool_idx(int cv, int wo, int ho) { return PoolIdx{make_fastdiv(cv), make_fastdiv(wo), make_fastdiv(ho)}; }
+
+// Elementwise pool kernels: grid (vectors of one replica / 256, replica
+// slots).  A replica's tensors stay below 2 GiB, so its vector count fits
+// 32 bits.
+template <typename T>
+static hipError_t maxpool_fwd_t(const T *x, T *z, int C, const int32_t *rmap, int Bt, int H, int W, int Ch,
+                                hipStream_t s) {
+  constexpr int VEC = ElemT<T>::VEC;
+  const int Ho = H / 2, Wo = W / 2, CV = Ch / VEC;
+  const uint32_t tot = (uint32_t)((int64_t)Bt * Ho * Wo * CV);
+  hipLaunchKernelGGL(maxpool_fwd_kernel<T>, dim3((tot + 255) / 256, C), dim3(256), 0, s, x, z, rmap,
+                     (int64_t)Bt * H * W * Ch, (int64_t)Bt * Ho * Wo * Ch, tot, pool_idx(CV, Wo, Ho), W, Ch);
   return hipGetLastError();
 }
 
-hipError_t launch_maxpool_bwd(int dtype, const void *a, const void *gz, void *gpre, int C, int Bt,
-                              int H, int W, int Ch, hipStream_t s) {
-  const int64_t total = (int64_t)C * Bt * (H / 2) * (W / 2) * Ch;
-  if (dtype == GCPSL_BF16)
-    hipLaunchKernelGGL(maxpool_bwd_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s,
-                       (const bf16_t *)a, (const bf16_t *)gz, (bf16_t *)gpre, total, H, W, Ch);
-  else
-    hipLaunchKernelGGL(maxpool_bwd_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s,
-                       (const float *)a, (const float *)gz, (float *)gpre, total, H, W, Ch);
+template <typename T>
+static hipError_t maxpool_bwd_t(const T *a, const T *gz, T *gpre, int C, const int32_t *rmap, int Bt, int H, int W,
+                                int Ch, hipStream_t s) {
+  constexpr int VEC = ElemT<T>::VEC;
+  const int Ho = H / 2, Wo = W / 2, CV = Ch / VEC;
+  const uint32_t tot = (uint32_t)((int64_t)Bt * Ho * Wo * CV);
+  hipLaunchKernelGGL(maxpool_bwd_kernel<T>, dim3((tot + 255) / 256, C), dim3(256), 0, s, a, gz, gpre, rmap,
+                     (int64_t)Bt * H * W * Ch, (int64_t)Bt * Ho * Wo * Ch, tot, pool_idx(CV, Wo, Ho), W, Ch);
   return hipGetLastError();
 }
 
-hipError_t launch_head_pool(int dtype, const void *a, void *h, int C, int Bt, int H, int W, int Ch,
-                            int maxpool, hipStream_t s) {
-  const int64_t total = (int64_t)C * Bt * Ch;
-  if (dtype == GCPSL_BF16)
-    hipLaunchKernelGGL(head_pool_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s,
-                       (const bf16_t *)a, (bf16_t *)h, total, H, W, Ch, maxpool);
-  else
-    hipLaunchKernelGGL(head_pool_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s,
-                       (const float *)a, (float *)h, total, H, W, Ch, maxpool);
+template <typename T>
+static hipError_t head_pool_t(const T *a, T *h, int C, const int32_t *rmap, int Bt, int H, int W, int Ch,
+                              int maxpool, hipStream_t s) {
+  constexpr int VEC = ElemT<T>::VEC;
+  const int CV = Ch / VEC, CVB = std::min(CV, 256);
+  hipLaunchKernelGGL(head_pool_kernel<T>, dim3((unsigned)Bt, (unsigned)((CV + CVB - 1) / CVB), (unsigned)C), dim3(256),
+                     0, s, a, h, rmap, Bt, H, W, Ch, CVB, maxpool);
   return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t head_pool_bwd_t(const T *a, const float *dh, T *gpre, int C, const int32_t *rmap, int Bt, int H,
+                                  int W, int Ch, int maxpool, hipStream_t s) {
+  constexpr int VEC = ElemT<T>::VEC;
+  const int CV = Ch / VEC;
+  const int Ho = maxpool ? H / 2 : H, Wo = maxpool ? W / 2 : W;
+  const uint32_t tot = (uint32_t)((int64_t)Bt * Ho * Wo * CV);
+  hipLaunchKernelGGL(head_pool_bwd_kernel<T>, dim3((tot + 255) / 256, C), dim3(256), 0, s, a, dh, gpre, rmap,
+                     (int64_t)Bt * H * W * Ch, (int64_t)Bt * Ch, tot, pool_idx(CV, Wo, Ho), W, Ch, maxpool);
+  return hipGetLastError();
+}
+
+hipError_t launch_maxpool_fwd(int dtype, const void *x, void *z, int C, const int32_t *rmap, int Bt, int H, int W,
+                              int Ch, hipStream_t s) {
+  if (dtype == GCPSL_BF16) return maxpool_fwd_t((const bf16_t *)x, (bf16_t *)z, C, rmap, Bt, H, W, Ch, s);
+  return maxpool_fwd_t((const float *)x, (float *)z, C, rmap, Bt, H, W, Ch, s);
+}
+
+hipError_t launch_maxpool_bwd(int dtype, const void *a, const void *gz, void *gpre, int C, const int32_t *rmap,
+                              int Bt, int H, int W, int Ch, hipStream_t s) {
+  if (dtype == GCPSL_BF16)
+    return maxpool_bwd_t((const bf16_t *)a, (const bf16_t *)gz, (bf16_t *)gpre, C, rmap, Bt, H, W, Ch, s);
+  return maxpool_bwd_t((const float *)a, (const float *)gz, (float *)gpre, C, rmap, Bt, H, W, Ch, s);
+}
+
+hipError_t launch_head_pool(int dtype, const void *a, void *h, int C, const int32_t *rmap, int Bt, int H, int W,
+                            int Ch, int maxpool, hipStream_t s) {
+  if (dtype == GCPSL_BF16) return head_pool_t((const bf16_t *)a, (bf16_t *)h, C, rmap, Bt, H, W, Ch, maxpool, s);
+  return head_pool_t((const float *)a, (float *)h, C, rmap, Bt, H, W, Ch, maxpool, s);
 }
 
 hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const float *theta, int64_t P,
                             int64_t w_off, int64_t b_off, float *grad, float *dh, float *loss, int C,
-                            int Bt, int Ch, int L, hipStream_t s) {
+                            const int32_t *rmap, int Bt, int Ch, int L, hipStream_t s) {
   const size_t shm = linear_ce_lds_bytes(Bt, Ch, L);
   if (shm > kMaxLinearLds) return hipErrorInvalidValue;
   if (shm > 64 * 1024) {
@@ -542,44 +816,53 @@ hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const fl
   }
   if (dtype == GCPSL_BF16)
     hipLaunchKernelGGL(linear_ce_kernel<bf16_t>, dim3(C), dim3(1024), shm, s, (const bf16_t *)h, y,
-                       theta, P, w_off, b_off, grad, dh, loss, Bt, Ch, L);
+                       theta, P, w_off, b_off, grad, dh, loss, rmap, Bt, Ch, L);
   else
     hipLaunchKernelGGL(linear_ce_kernel<float>, dim3(C), dim3(1024), shm, s, (const float *)h, y,
-                       theta, P, w_off, b_off, grad, dh, loss, Bt, Ch, L);
+                       theta, P, w_off, b_off, grad, dh, loss, rmap, Bt, Ch, L);
   return hipGetLastError();
 }
 
-hipError_t launch_head_pool_bwd(int dtype, const void *a, const float *dh, void *gpre, int C, int Bt,
-                                int H, int W, int Ch, int maxpool, hipStream_t s) {
-  const int64_t total = maxpool ? (int64_t)C * Bt * (H / 2) * (W / 2) * Ch : (int64_t)C * Bt * H * W * Ch;
+hipError_t launch_head_pool_bwd(int dtype, const void *a, const float *dh, void *gpre, int C, const int32_t *rmap,
+                                int Bt, int H, int W, int Ch, int maxpool, hipStream_t s) {
   if (dtype == GCPSL_BF16)
-    hipLaunchKernelGGL(head_pool_bwd_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s,
-                       (const bf16_t *)a, dh, (bf16_t *)gpre, total, H, W, Ch, maxpool);
-  else
-    hipLaunchKernelGGL(head_pool_bwd_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s,
-                       (const float *)a, dh, (float *)gpre, total, H, W, Ch, maxpool);
-  return hipGetLastError();
+    return head_pool_bwd_t((const bf16_t *)a, dh, (bf16_t *)gpre, C, rmap, Bt, H, W, Ch, maxpool, s);
+  return head_pool_bwd_t((const float *)a, dh, (float *)gpre, C, rmap, Bt, H, W, Ch, maxpool, s);
 }
 
 hipError_t launch_wgrad_reduce(const float *dw, const float *db, int splits, int64_t dw_ss,
                                int64_t dw_rs, int64_t db_ss, int64_t db_rs, float *grad, int64_t P,
-                               int64_t w_off, int64_t b_off, int64_t nw, int co, int C,
+                               int64_t w_off, int64_t b_off, int64_t nw, int co, int C, const int32_t *rmap,
                                hipStream_t s) {
   hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(grid_for(nw + co, 256, 4096), C), dim3(256), 0, s, dw,
-                     db, splits, dw_ss, dw_rs, db_ss, db_rs, grad, P, w_off, b_off, nw, co);
+                     db, splits, dw_ss, dw_rs, db_ss, db_rs, grad, P, w_off, b_off, nw, co, rmap);
   return hipGetLastError();
 }
 
-hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t n, float lr, float mu,
-                      hipStream_t s) {
-  hipLaunchKernelGGL(sgd_kernel, dim3(grid_for(n / 4 + 1, 256, 8192)), dim3(256), 0, s, theta, mom,
-                     grad, n, lr, mu);
+hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t P, int C, const int32_t *rmap, float lr,
+                      float mu, hipStream_t s) {
+  const uintptr_t al = reinterpret_cast<uintptr_t>(theta) | reinterpret_cast<uintptr_t>(mom) |
+                       reinterpret_cast<uintptr_t>(grad);
+  if (P % 4 == 0 && al % 16 == 0)
+    hipLaunchKernelGGL(sgd_kernel<4>, dim3(grid_for(P / 4, 256, 1024), C), dim3(256), 0, s, theta, mom, grad, P, rmap,
+                       lr, mu);
+  else if (P % 2 == 0 && al % 8 == 0)
+    hipLaunchKernelGGL(sgd_kernel<2>, dim3(grid_for(P / 2, 256, 1024), C), dim3(256), 0, s, theta, mom, grad, P, rmap,
+                       lr, mu);
+  else
+    hipLaunchKernelGGL(sgd_kernel<1>, dim3(grid_for(P, 256, 1024), C), dim3(256), 0, s, theta, mom, grad, P, rmap,
+                       lr, mu);
   return hipGetLastError();
 }
 
 hipError_t launch_fuse(float *theta, const double *weights, double W, int C, int64_t P,
                        hipStream_t s) {
-  hipLaunchKernelGGL(fuse_kernel, dim3(grid_for(P, 256, 8192)), dim3(256), 0, s, theta, weights, W, C,
-                     P);
+  const uintptr_t a = reinterpret_cast<uintptr_t>(theta);
+  if (P % 4 == 0 && a % 16 == 0)
+    hipLaunchKernelGGL(fuse_kernel<4>, dim3(grid_for(P / 4, 256, 16384)), dim3(256), 0, s, theta, weights, W, C, P);
+  else if (P % 2 == 0 && a % 8 == 0)
+    hipLaunchKernelGGL(fuse_kernel<2>, dim3(grid_for(P / 2, 256, 16384)), dim3(256), 0, s, theta, weights, W, C, P);
+  else
+    hipLaunchKernelGGL(fuse_kernel<1>, dim3(grid_for(P, 256, 16384)), dim3(256), 0, s, theta, weights, W, C, P);
   return hipGetLastError();
 }

@@ -182,7 +182,7 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
   const int mt = __builtin_amdgcn_readfirstlane((int)(rest % (uint32_t)MT));
   rest /= (uint32_t)MT;
   const int split = __builtin_amdgcn_readfirstlane((int)(rest % (uint32_t)a.splits));
-  const int rep = __builtin_amdgcn_readfirstlane((int)(rest / (uint32_t)a.splits));
+  const int rep = replica_of(a.rmap, __builtin_amdgcn_readfirstlane((int)(rest / (uint32_t)a.splits)));
   const int M = a.Bt * a.H * a.W;
   const int NW = a.taps == 1 ? a.Ci : 9 * a.Ci;
   const int p_begin = split * a.chunk;

@@ -29,7 +29,8 @@ struct ConvArgs {
   const void *mask;  // dgrad: mask source [C][Bt][H][W][N] (value > 0) or null
   int Bt, H, W, Csrc, N, K, Kp;
   int64_t src_rs, wt_rs, out_rs, bias_rs;  // per-replica strides (elements)
-  int C;
+  int C;     // replica slots of the launch
+  const int32_t *rmap;  // device [C]: replica of each slot, or null (slot z = replica z)
   int epi;
   int taps;  // 9: 3x3 implicit GEMM; 1: src already holds im2col rows, A[m][k] = src[m][k]
 };
@@ -43,7 +44,8 @@ struct WgradArgs {
   float *db;      // db + s*db_ss + r*db_rs, [Co]
   int Bt, H, W, Ci, Co;
   int64_t g_rs, x_rs, dw_rs, dw_ss, db_rs, db_ss;
-  int C, splits, chunk;  // pixel chunk per split (multiple of the k tile)
+  int C, splits, chunk;  // replica slots; pixel chunk per split (multiple of the k tile)
+  const int32_t *rmap;   // device [C]: replica of each slot, or null (slot z = replica z)
   int taps;  // 9: x is the layer input; 1: x holds im2col rows of Ci columns
   int nw;    // weight-gradient row length written (9 * input channels)
 };
@@ -68,36 +70,37 @@ void wgrad_tile(int dtype, int Co, int ncols, int *bm, int *bn);
 hipError_t launch_sample(const int32_t *ids, const int64_t *off, const int32_t *coe,
                          const int32_t *labels, int32_t *idx, int32_t *y, int32_t *hits,
                          int C, int B, int K, uint64_t seed, int64_t step0, int nsteps,
-                         int64_t max_steps, hipStream_t s);
+                         int64_t max_steps, int64_t R, hipStream_t s);
 hipError_t launch_gather(const float *images, const int32_t *idx, void *x, int dtype,
                          int64_t rows, int64_t row_elems, hipStream_t s);
 // Gather with im2col: x[row][pixel][k], k = (r, s, c) < 9 Cin, zero to Kc.
 hipError_t launch_gather_im2col(const float *images, const int32_t *idx, void *x, int dtype,
                                 int64_t rows, int H, int W, int Cin, int Kc, hipStream_t s);
-hipError_t launch_prep_weights(int dtype, const float *theta, int64_t P, int C, int64_t w_off,
+hipError_t launch_prep_weights(int dtype, const float *theta, int64_t P, int C, const int32_t *rmap, int64_t w_off,
                                int co, int ci, void *wf, int Kp, void *wd, int Kdp,
                                hipStream_t s);
-hipError_t launch_maxpool_fwd(int dtype, const void *x, void *z, int C, int Bt, int H, int W,
+hipError_t launch_maxpool_fwd(int dtype, const void *x, void *z, int C, const int32_t *rmap, int Bt, int H, int W,
                               int Ch, hipStream_t s);
-hipError_t launch_maxpool_bwd(int dtype, const void *a, const void *gz, void *gpre, int C,
+hipError_t launch_maxpool_bwd(int dtype, const void *a, const void *gz, void *gpre, int C, const int32_t *rmap,
                               int Bt, int H, int W, int Ch, hipStream_t s);
-hipError_t launch_head_pool(int dtype, const void *a, void *h, int C, int Bt, int H, int W,
+hipError_t launch_head_pool(int dtype, const void *a, void *h, int C, const int32_t *rmap, int Bt, int H, int W,
                             int Ch, int maxpool, hipStream_t s);
 // LDS the classifier-head kernel stages (pooled features, weights, logits).
 constexpr size_t kMaxLinearLds = 160 * 1024;
 inline size_t linear_ce_lds_bytes(int Bt, int Ch, int L) {
-  return sizeof(float) * ((size_t)Bt * Ch + (size_t)L * Ch + (size_t)Bt * L + Bt);
+  return sizeof(float) * ((size_t)Bt * (Ch + 1) + (size_t)L * (Ch + 1) + (size_t)Bt * L + Bt);
 }
 hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const float *theta,
                             int64_t P, int64_t w_off, int64_t b_off, float *grad, float *dh,
-                            float *loss, int C, int Bt, int Ch, int L, hipStream_t s);
-hipError_t launch_head_pool_bwd(int dtype, const void *a, const float *dh, void *gpre, int C,
+                            float *loss, int C, const int32_t *rmap, int Bt, int Ch, int L, hipStream_t s);
+hipError_t launch_head_pool_bwd(int dtype, const void *a, const float *dh, void *gpre, int C, const int32_t *rmap,
                                 int Bt, int H, int W, int Ch, int maxpool, hipStream_t s);
 hipError_t launch_wgrad_reduce(const float *dw, const float *db, int splits, int64_t dw_ss,
                                int64_t dw_rs, int64_t db_ss, int64_t db_rs, float *grad,
                                int64_t P, int64_t w_off, int64_t b_off, int64_t nw, int co,
-                               int C, hipStream_t s);
-hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t n, float lr,
-                      float mu, hipStream_t s);
+                               int C, const int32_t *rmap, hipStream_t s);
+// SGD on the replicas of the launch's slots: P parameters each, row stride P.
+hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t P, int C, const int32_t *rmap,
+                      float lr, float mu, hipStream_t s);
 hipError_t launch_fuse(float *theta, const double *weights, double W, int C, int64_t P,
                        hipStream_t s);

@@ -20,9 +20,11 @@ RULES = {"random": 0, "size": 1, "label_l1": 2, "label_jsd": 3}
 DTYPES = {"f32": 0, "bf16": 1}
 CONV3X3, MAXPOOL2, AVGPOOL, LINEAR = 1, 2, 3, 4
 RESIDUAL = 1
+SCHEDULES = {"lockstep": 0, "epoch": 1}
 
 EXPORTS = ["gcpsl_param_count", "gcpsl_workspace_bytes", "gcpsl_assign", "gcpsl_create",
-           "gcpsl_sample", "gcpsl_step", "gcpsl_fuse", "gcpsl_participation",
+           "gcpsl_sample", "gcpsl_step", "gcpsl_step_replica", "gcpsl_epoch_rounds", "gcpsl_fuse",
+           "gcpsl_participation",
            "gcpsl_cluster_sizes", "gcpsl_tensor", "gcpsl_timing", "gcpsl_timing_read",
            "gcpsl_destroy", "gcpsl_last_error"]
 
@@ -44,7 +46,7 @@ class Desc(C.Structure):
         ("n_examples", C.c_int64), ("n_layers", C.c_int32), ("cut", C.c_int32),
         ("layers", C.POINTER(Layer)), ("lr", C.c_float), ("momentum", C.c_float),
         ("seed", C.c_uint64), ("max_steps", C.c_int64), ("max_window", C.c_int32),
-        ("reserved", C.c_int32), ("client_of_example", C.POINTER(C.c_int32)),
+        ("schedule", C.c_int32), ("client_of_example", C.POINTER(C.c_int32)),
         ("cluster_of_client", C.POINTER(C.c_int32)), ("images", C.c_void_p),
         ("labels", C.c_void_p), ("theta", C.c_void_p), ("momentum_buf", C.c_void_p),
         ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t),
@@ -75,6 +77,8 @@ def lib():
     L.gcpsl_create.argtypes = [P(Desc), P(vp)]
     L.gcpsl_sample.argtypes = [vp, i64, i32, vp, vp]
     L.gcpsl_step.argtypes = [vp, i64, vp, vp]
+    L.gcpsl_step_replica.argtypes = [vp, i64, i32, vp, vp]
+    L.gcpsl_epoch_rounds.argtypes = [vp, P(i64), P(i64)]
     L.gcpsl_fuse.argtypes = [vp, vp]
     L.gcpsl_participation.argtypes = [vp, P(i64), P(i64), P(i32)]
     L.gcpsl_cluster_sizes.argtypes = [vp, P(i64)]
@@ -133,7 +137,7 @@ def assign(rule, K, C_, seed, counts=None, hist=None):
     return out
 
 
-def make_desc(cfg, client_of_example, cluster_of_client, max_steps=None, max_window=1):
+def make_desc(cfg, client_of_example, cluster_of_client, max_steps=None, max_window=1, schedule="lockstep"):
     """Host part of gcpsl_desc for a workload (device pointers filled by Context)."""
     d = Desc()
     d.K, d.C, d.B, d.L = cfg["K"], cfg["C"], cfg["B"], cfg["L"]
@@ -150,7 +154,7 @@ def make_desc(cfg, client_of_example, cluster_of_client, max_steps=None, max_win
     d.seed = cfg["seed"]
     d.max_steps = max_steps if max_steps is not None else cfg["T"]
     d.max_window = max_window
-    d.reserved = 0
+    d.schedule = SCHEDULES[schedule]
     d.client_of_example = _i32p(keep["coe"])
     d.cluster_of_client = _i32p(keep["coc"])
     return d, keep
@@ -178,10 +182,11 @@ class Context:
     """One gcpsl_ctx with the caller-owned device buffers it works in."""
 
     def __init__(self, cfg, images, labels, client_of_example, cluster_of_client, theta0,
-                 max_steps=None, max_window=1, device="cuda"):
+                 max_steps=None, max_window=1, device="cuda", schedule="lockstep"):
         import torch
         self.cfg = cfg
-        desc, self._keep = make_desc(cfg, client_of_example, cluster_of_client, max_steps, max_window)
+        self.schedule = schedule
+        desc, self._keep = make_desc(cfg, client_of_example, cluster_of_client, max_steps, max_window, schedule)
         self.P, self.P_client = param_count(desc)
         t0 = torch.as_tensor(np.asarray(theta0, dtype=np.float32))
         if t0.numel() != self.P:
@@ -223,6 +228,17 @@ class Context:
     def step(self, step, loss_out=None, stream=None):
         ptr = None if loss_out is None else C.c_void_p(loss_out.data_ptr())
         _check(lib().gcpsl_step(self._h, step, ptr, _stream(stream)))
+
+    def step_replica(self, step, replica, loss_out=None, stream=None):
+        ptr = None if loss_out is None else C.c_void_p(loss_out.data_ptr())
+        _check(lib().gcpsl_step_replica(self._h, step, replica, ptr, _stream(stream)))
+
+    def epoch_rounds(self):
+        """(r_n per cluster, R = slots of a system epoch) of the epoch schedule."""
+        out = np.zeros(self.cfg["C"], dtype=np.int64)
+        R = C.c_int64()
+        _check(lib().gcpsl_epoch_rounds(self._h, _i64p(out), C.byref(R)))
+        return out, R.value
 
     def fuse(self, stream=None):
         _check(lib().gcpsl_fuse(self._h, _stream(stream)))

@@ -54,13 +54,32 @@ def kernel_label(name: str) -> str:
     return m.group(1) if m else name
 
 
-def source_hash():
+CSRC = os.path.join(ROOT, "paper_2609_29395_amd", "csrc")
+SHARED_HEADERS = ("common.h",)  # device helpers every kernel source includes
+
+
+def kernel_source(label: str) -> str:
+    """The source file that holds the kernel a timing label names."""
+    if label.startswith("conv_wgrad<") and label.endswith(",lds>"):
+        return "k_wgrad_lds.hip"
+    if label.startswith("conv_") and label.endswith(",lds>"):
+        return "k_conv_lds.hip"
+    if label.startswith("conv_"):
+        return "k_conv.hip"
+    return "k_misc.hip"
+
+
+def file_hash(name: str) -> str:
+    """Hash of one kernel source together with the shared device headers."""
     h = hashlib.sha256()
-    d = os.path.join(ROOT, "paper_2609_29395_amd", "csrc")
-    for f in sorted(os.listdir(d)):
-        with open(os.path.join(d, f), "rb") as fh:
+    for f in (name, *SHARED_HEADERS):
+        with open(os.path.join(CSRC, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
+
+
+def source_hashes() -> dict:
+    return {f: file_hash(f) for f in sorted(os.listdir(CSRC)) if f.endswith(".hip")}
 
 
 def copy(mib=COPY_MIB, reps=5):
@@ -113,7 +132,7 @@ def traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload, out_
     cw = samples(_counter_per_dispatch(copy_write_dir, "WRITE_SIZE"))
     f_fac = (sum(cf) / len(cf)) / expect_kib if cf else 1.0
     w_fac = (sum(cw) / len(cw)) / expect_kib if cw else 1.0
-    out = {"source_hash": source_hash(), "copy_mib": COPY_MIB, "fetch_factor": f_fac,
+    out = {"source_hashes": source_hashes(), "copy_mib": COPY_MIB, "fetch_factor": f_fac,
            "write_factor": w_fac, "kernels": {}}
     for k in set(fetch) | set(write):
         fv, wv = fetch.get(k, []), write.get(k, [])

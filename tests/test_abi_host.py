@@ -137,7 +137,7 @@ def test_create_rejects_bad_descriptions_before_device_work():
     d, k = _desc(cfg, **dict(base, B=400))  # clusters hold 197 and 315 examples
     rc, msg = _create(d)
     assert rc == g.EINVAL and "< B" in msg
-    d, k = _desc(cfg, **dict(base, reserved=1))
+    d, k = _desc(cfg, **dict(base, schedule=2))  # unknown schedule
     assert _create(d)[0] == g.EINVAL
     d, k = _desc(cfg, **dict(base, dtype=9))
     assert _create(d)[0] == g.EINVAL

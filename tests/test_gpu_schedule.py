@@ -1,0 +1,105 @@
+"""GPU parity of the epoch-barrier schedule (Sec. III-A; Sec. IV-D, Eq. 6)
+and of sequential against concurrent execution of the clusters, through the
+C ABI.  Floating point within the workload tolerance of the oracle (1e-4
+fp32, 2e-2 bf16, per tensor as in test_gpu_parity); participation counts
+bit-exact; sequential and concurrent GPU runs bit-identical to each other."""
+import numpy as np
+import pytest
+import torch
+
+from gcpsl_inputs import get_config
+from oracle.train import GCPSLOracle, epoch_rounds
+
+pytestmark = pytest.mark.gpu
+
+from paper_2609_29395_amd import driver, gcpsl  # noqa: E402
+from test_gpu_parity import TOL, close  # noqa: E402
+
+
+@pytest.mark.parametrize("name", ["tiny_epoch", "ragged_epoch", "ragged_bf16_epoch"])
+def test_epoch_schedule_parity(name):
+    cfg = get_config(name)
+    T = cfg["T"]
+    print(f"epoch schedule parity: {name} T={T}", flush=True)
+    ctx, assignment = driver.setup(cfg)
+    ref = GCPSLOracle(cfg, cluster_of_client=assignment)
+    rounds, R = ctx.epoch_rounds()
+    assert (rounds.tolist(), R) == epoch_rounds(ref.weights, cfg["B"])
+    assert T > R  # spans a fusion barrier
+    losses = torch.full((T, cfg["C"]), float("nan"), device="cuda")
+    driver.train(ctx, T, losses=losses)
+    torch.cuda.synchronize()
+    ref.run_epoch_schedule(T)
+    tol = TOL[cfg["dtype"]]
+    got_l, want_l = losses.cpu().numpy(), np.array(ref.losses)
+    ran = ~np.isnan(want_l)
+    assert np.array_equal(~np.isnan(got_l), ran)  # waiting clusters write no loss
+    assert np.all(np.abs(got_l[ran] - want_l[ran]) <= tol * np.abs(want_l[ran])), (got_l, want_l)
+    th, mo = ctx.theta.cpu().numpy(), ctx.mom.cpu().numpy()
+    for n in range(cfg["C"]):
+        ok, e = close(th[n], ref.theta[n], tol)
+        assert ok, ("theta", n, e)
+        ok, e = close(mo[n], ref.mom[n], tol)
+        assert ok, ("momentum", n, e)
+    a, t, per = ctx.participation()
+    assert t == cfg["K"] * T
+    assert np.array_equal(per, np.array(ref.active)) and a == int(np.sum(ref.active))
+
+
+def test_epoch_sample_marks_waiting_clusters():
+    cfg = get_config("ragged_epoch")
+    ctx, _ = driver.setup(cfg, max_window=8)
+    rounds, R = ctx.epoch_rounds()
+    out = torch.zeros(8, cfg["C"], cfg["B"], dtype=torch.int32, device="cuda")
+    ctx.sample(R - 4, 8, out)  # slots across the epoch boundary
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    for j in range(8):
+        t = (R - 4 + j) % R
+        for n in range(cfg["C"]):
+            if t < rounds[n]:
+                assert (got[j, n] >= 0).all() and len(np.unique(got[j, n])) == cfg["B"]
+            else:
+                assert (got[j, n] == -1).all()
+
+
+def _run(cfg, T, serial):
+    ctx, _ = driver.setup(cfg)
+    losses = torch.full((T, cfg["C"]), float("nan"), device="cuda")
+    driver.train(ctx, T, losses=losses, serial=serial)
+    torch.cuda.synchronize()
+    return ctx, losses.cpu().numpy()
+
+
+@pytest.mark.parametrize("name", ["tiny_epoch", "ragged_bf16_epoch", "ragged", "ragged_bf16"])
+def test_sequential_equals_concurrent_bit_for_bit(name):
+    # Eq. 6 compares running the cluster workloads one after another with
+    # running them side by side: the same rounds, so the same results
+    cfg = get_config(name)
+    T = cfg["T"]
+    print(f"sequential vs concurrent: {name} T={T}", flush=True)
+    a, la = _run(cfg, T, serial=False)
+    b, lb = _run(cfg, T, serial=True)
+    assert np.array_equal(la, lb, equal_nan=True)
+    assert torch.equal(a.theta, b.theta) and torch.equal(a.mom, b.mom)
+    assert np.array_equal(a.participation()[2], b.participation()[2])
+
+
+def test_step_replica_errors():
+    cfg = get_config("ragged_epoch")
+    ctx, _ = driver.setup(cfg)
+    rounds, R = ctx.epoch_rounds()
+    with pytest.raises(gcpsl.GCPSLError) as e:
+        ctx.step_replica(0, 0)
+    assert e.value.code == gcpsl.ESTATE  # nothing sampled yet
+    ctx.sample(R - 1)
+    waiting = [n for n in range(cfg["C"]) if rounds[n] <= R - 1]
+    assert waiting
+    with pytest.raises(gcpsl.GCPSLError) as e:
+        ctx.step_replica(R - 1, waiting[0])
+    assert e.value.code == gcpsl.EINVAL
+    with pytest.raises(gcpsl.GCPSLError) as e:
+        ctx.step_replica(R - 1, cfg["C"])
+    assert e.value.code == gcpsl.EINVAL
+    ctx.step_replica(R - 1, int(np.argmax(rounds)))
+    torch.cuda.synchronize()

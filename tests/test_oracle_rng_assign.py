@@ -7,10 +7,13 @@ import pytest
 from oracle.assign import assign, assign_label_l1, assign_random, assign_size
 from oracle.rng import MASK64, TAG_ASSIGN, SplitMix64, bounded, mix64
 
+from conftest import load_golden
+
 # SplitMix64 known-answer vector from the generator's published reference
-# implementation (state seeded with 1234567).
-SPLITMIX_1234567 = [6457827717110365317, 3203168211198807973, 9817491932198370423,
-                    4593380528125082431, 16408922859458223821]
+# implementation (state seeded with 1234567), stored in tests/golden.
+_G = load_golden("splitmix64_seed1234567.txt")
+assert _G["seed"] == [1234567]
+SPLITMIX_1234567 = _G["outputs"]
 
 
 def test_splitmix64_published_vector():

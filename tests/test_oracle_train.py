@@ -6,6 +6,8 @@ import torch
 from gcpsl_inputs import get_config, init_params
 from oracle.train import GCPSLOracle, fuse, sgd_update
 
+from conftest import load_golden
+
 
 def test_sgd_two_steps_closed_form():
     # v1 = g0, theta1 = theta0 - lr g0; v2 = mu g0 + g1, theta2 = theta1 - lr v2
@@ -33,10 +35,10 @@ def test_sgd_matches_torch_optimizer():
 
 
 def test_fusion_worked_example():
-    # weights 1, 2, 5 (W = 8): (1*[8,0] + 2*[0,4] + 5*[0.8,-1.6]) / 8 = [1.5, 0]
-    th = [np.array([8.0, 0.0], np.float32), np.array([0.0, 4.0], np.float32),
-          np.array([0.8, -1.6], np.float32)]
-    assert np.allclose(fuse(th, [1, 2, 5]), [1.5, 0.0], atol=1e-7)
+    # tests/golden: weights 1, 2, 5 (W = 8): (1*[8,0] + 2*[0,4] + 5*[0.8,-1.6]) / 8 = [1.5, 0]
+    g = load_golden("fusion_eq5_worked.txt")
+    th = [np.array(g[f"theta{n}"], np.float32) for n in range(len(g["weights"]))]
+    assert np.allclose(fuse(th, g["weights"]), g["fused"], atol=1e-7)
 
 
 def test_fusion_of_identical_replicas_is_bit_exact_identity():
