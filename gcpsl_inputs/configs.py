@@ -90,6 +90,16 @@ CONFIGS = {
                 ("conv", 24, 136, False), ("conv", 136, 136, True), ("maxpool",),
                 ("avgpool",), ("linear", 136, 7)],
         cut=3, dtype="bf16", lr=0.05, momentum=0.9, F=3, T=7, seed=0),
+    # Residual server layers whose channel counts are multiples of 64 (the
+    # residual is taken from the staged centre tap), with ragged M and no max
+    # pool (so no bf16 near-tie routing decision can move a gradient).
+    "ragged_res_bf16": dict(
+        K=24, C=3, B=19, L=7, N_ex=1400, H=8, W=8, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="label_l1",
+        layers=[("conv", 3, 16, False), ("conv", 16, 64, False),
+                ("conv", 64, 128, False), ("conv", 128, 128, True), ("conv", 128, 128, True),
+                ("avgpool",), ("linear", 128, 7)],
+        cut=2, dtype="bf16", lr=0.05, momentum=0.9, F=3, T=7, seed=0),
     # Epoch-barrier schedule (fusion after every system epoch) on unequal
     # clusters: tiny with B=32 (6 and 9 rounds per epoch), and the ragged
     # shapes under label-L1 clustering with B=100 (7, 4 and 2 rounds).

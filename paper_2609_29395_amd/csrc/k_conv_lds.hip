@@ -25,6 +25,13 @@
 // epilogue stages the fp32 tile through LDS, 64 pixel rows per pass, then
 // works on 8 consecutive channels per lane: 16-byte loads of the residual and
 // mask (all of a pass issued together), 16-byte stores.
+//
+// Residual layers add the layer input itself (cin == cout).  With 64-channel
+// wave tiles and the tap-fastest k order, the centre-tap k tile of channel
+// block cb holds exactly input[m][cb*64 .. cb*64+63] for the tile's pixels,
+// i.e. the residual of the waves whose channels are block cb: those waves add
+// it to their accumulators from LDS, and the epilogue reads no residual from
+// HBM (the epilogues of all workgroups run at once and are bandwidth-bound).
 #include <utility>
 
 #include "runtime.h"
@@ -34,6 +41,7 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
 
@@ -64,6 +72,7 @@ template <int BM_, int BN, int WM, int WN> struct Cfg {
 };
 
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+__device__ __forceinline__ int wn_of(int wave, int WN) { return wave % WN; }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) {
   const uint64_t p = reinterpret_cast<uint64_t>(base);
@@ -225,6 +234,9 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   }
 
   const int nk = a.Kp / BK;
+  // k tile of the centre tap of this wave's 64-channel block (tap-fastest
+  // order: k tile kt is channel block kt / 9, tap kt % 9)
+  const int res_kt = ((n0 + wn_of(wave, WN) * CF::WNW) / BK) * 9 + 4;
   char *stage0 = smem + wave * 1024;
   auto issue = [&](int kt) {
     issue_tile<CF, TAPS1>(kt, stage0, wave, a, fd_c, src, wt, achunk, arowoff, amask, boff);
@@ -257,6 +269,7 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
     asm volatile("s_barrier" ::: "memory");
     if (kt + 1 < nk) issue(kt + 1);
     const uint32_t st = lds0 + (uint32_t)((kt & 1) * CF::STAGE);
+    const bool add_res = a.res_lds && kt == res_kt;
     // per k group: the second half of the pixel fragments is read while the
     // first half is multiplied
 #pragma unroll
@@ -279,6 +292,32 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) mma(acc[H + tm][tn], w[tn], x1[tm]);
     }
+    if (add_res) {
+      // residual of fragment (tm, tn): 4 channels tn*16 + lg*4 .. +3 of the
+      // block at pixel row wm*TM*16 + tm*16 + li of the centre-tap A tile
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) {
+        u32x2 rv[TN];
+        const int row = wm * TM * 16 + tm * 16 + li;
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) {
+          const int ch = tn * 2 + (lg >> 1);  // 16-byte chunk of the row
+          const uint32_t ad = st + (uint32_t)(row * ROW + ((ch ^ swz(row)) * 16) + (lg & 1) * 8);
+          asm volatile("ds_read_b64 %0, %1" : "=v"(rv[tn]) : "v"(ad));
+        }
+        // the values are produced at the wait: keep every use after it
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) asm volatile("" : "+v"(rv[tn]));
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) {
+          acc[tm][tn][0] += bf2f(rv[tn][0] & 0xffffu);
+          acc[tm][tn][1] += bf2f(rv[tn][0] >> 16);
+          acc[tm][tn][2] += bf2f(rv[tn][1] & 0xffffu);
+          acc[tm][tn][3] += bf2f(rv[tn][1] >> 16);
+        }
+      }
+    }
   }
   __syncthreads();
 
@@ -296,7 +335,7 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
 #pragma unroll
   for (int e = 0; e < 8; ++e) bias[e] = (EPI == EPI_FWD && nok) ? a.bias[rep * a.bias_rs + n + e] : 0.f;
   bf16_t *out = reinterpret_cast<bf16_t *>(a.out) + rep * a.out_rs;
-  const bf16_t *res = a.res ? reinterpret_cast<const bf16_t *>(a.res) + rep * a.out_rs : nullptr;
+  const bf16_t *res = (a.res && !a.res_lds) ? reinterpret_cast<const bf16_t *>(a.res) + rep * a.out_rs : nullptr;
   const bf16_t *msk = a.mask ? reinterpret_cast<const bf16_t *>(a.mask) + rep * a.out_rs : nullptr;
   const __amdgpu_buffer_rsrc_t rsr = rsrc(res ? res : out, (uint32_t)(a.out_rs * 2));
   const __amdgpu_buffer_rsrc_t rsm = rsrc(msk ? msk : out, (uint32_t)(a.out_rs * 2));
@@ -412,12 +451,17 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   else grid<256, 32>(a, &MT, &NT);
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Csrc);
   const dim3 g((uint32_t)MT * NT * a.C);
+  // residual from the staged centre tap: residual == input, tap-fastest k
+  // order (input channels a multiple of the k tile), 64-channel wave tiles
+  ConvArgs b = a;
+  b.res_lds = (a.res != nullptr && a.res == a.src && a.taps == 9 && a.Csrc % BK == 0 && a.Csrc == a.N &&
+               (bn == 256 || bn == 128)) ? 1 : 0;
   if (label)
     *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16," + std::to_string(bm) + "x" +
              std::to_string(bn) + "x64,w" + (bn == 256 ? "16" : "8") + ",lds>";
 #define CONV_LDS_GO(BM, BN, WM, WN, E, T)                                                                  \
   hipLaunchKernelGGL((CONV_LDS_K(BM, BN, WM, WN, E, T)), g, dim3(Cfg<BM, BN, WM, WN>::NTHR),                 \
-                     (Cfg<BM, BN, WM, WN>::LDS_BYTES), s, a, fw, fh, fc, MT, NT)
+                     (Cfg<BM, BN, WM, WN>::LDS_BYTES), s, b, fw, fh, fc, MT, NT)
 #define CONV_LDS_SEL(BM, BN, WM, WN)                                                                        \
   if (fwd) { if (t1) CONV_LDS_GO(BM, BN, WM, WN, EPI_FWD, true); else CONV_LDS_GO(BM, BN, WM, WN, EPI_FWD, false); } \
   else { if (t1) CONV_LDS_GO(BM, BN, WM, WN, EPI_DGRAD, true); else CONV_LDS_GO(BM, BN, WM, WN, EPI_DGRAD, false); }

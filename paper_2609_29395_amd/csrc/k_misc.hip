@@ -554,7 +554,22 @@ head_pool_bwd_kernel(const T *__restrict__ a, const float *__restrict__ dh, T *_
 
 // ----------------------------------------------------- split-K reduction
 // grad[w_off + j] = sum over splits (in order) of the partial weight
-// gradients; grad[b_off + c] likewise for the bias.
+// gradients; grad[b_off + c] likewise for the bias.  The partials of 8
+// splits are loaded before they are added (in split order).
+__device__ __forceinline__ float ordered_sum(const float *__restrict__ p, int64_t stride, int splits) {
+  float s = 0.f;
+  int k = 0;
+  for (; k + 8 <= splits; k += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = p[(k + u) * stride];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += v[u];
+  }
+  for (; k < splits; ++k) s += p[k * stride];
+  return s;
+}
+
 __global__ void __launch_bounds__(256)
 wgrad_reduce_kernel(const float *__restrict__ dw, const float *__restrict__ db, int splits,
                     int64_t dw_ss, int64_t dw_rs, int64_t db_ss, int64_t db_rs,
@@ -563,14 +578,11 @@ wgrad_reduce_kernel(const float *__restrict__ dw, const float *__restrict__ db, 
   const int rep = replica_of(rmap, blockIdx.y);
   for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < nw + co;
        j += (int64_t)gridDim.x * blockDim.x) {
-    float s = 0.f;
     if (j < nw) {
-      for (int k = 0; k < splits; ++k) s += dw[k * dw_ss + rep * dw_rs + j];
-      grad[rep * P + w_off + j] = s;
+      grad[rep * P + w_off + j] = ordered_sum(dw + rep * dw_rs + j, dw_ss, splits);
     } else {
       const int64_t c = j - nw;
-      for (int k = 0; k < splits; ++k) s += db[k * db_ss + rep * db_rs + c];
-      grad[rep * P + b_off + c] = s;
+      grad[rep * P + b_off + c] = ordered_sum(db + rep * db_rs + c, db_ss, splits);
     }
   }
 }

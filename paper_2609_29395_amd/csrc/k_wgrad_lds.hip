@@ -37,12 +37,15 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
 
-constexpr int BK = 64;
 constexpr uint32_t kOob = 0x80000000u;
 constexpr int kBufferFlags = 0x00020000;
 constexpr int kDead = 1 << 30;  // row index that fails every pixel test
 
-template <int BM, int BN, int WM, int WN> struct Cfg {
+// BK pixels per k tile (a multiple of the 32 of one MFMA k group), NST LDS
+// stages: the copies of a tile are issued NST - 1 tiles before it is used.
+template <int BM, int BN, int WM, int WN, int BK_ = 64, int NST_ = 2> struct Cfg {
+  static constexpr int BM_ = BM, BN_ = BN, WM_ = WM, WN_ = WN;
+  static constexpr int BK = BK_, NST = NST_, KG = BK / 32;
   static constexpr int NW = WM * WN, NTHR = 64 * NW;  // waves, threads
   static constexpr int ROWA = BM * 2, ROWB = BN * 2;  // bytes per LDS row
   static constexpr int CHA = ROWA / 16, CHB = ROWB / 16;  // 16-byte chunks per row
@@ -54,13 +57,15 @@ template <int BM, int BN, int WM, int WN> struct Cfg {
   static constexpr int QROWA = NTHR * 16 / ROWA, QROWB = NTHR * 16 / ROWB;
   static constexpr int TM = BM / WM / 16, TN = BN / WN / 16;                    // fragments per wave
   static constexpr int BPW = (TM + WN - 1) / WN;  // bias fragments per wave: those with tm % WN == wn
-  static constexpr int LDS_BYTES = 2 * STAGE;
+  static constexpr int LDS_BYTES = NST * STAGE;
+  static constexpr int CPT = SA + SB;  // copies per thread per tile
   static constexpr int WNS = WN;
   static_assert(NW == 8 || NW == 16, "8 or 16 waves");
   static_assert(SA * NTHR * 16 == A_BYTES && SB * NTHR * 16 == B_BYTES, "copies must tile the stage");
   static_assert(QROWA % 16 == 0 && QROWB % 16 == 0, "copy rows keep the swizzle");
   static_assert(TM % WN == 0 || WN % TM == 0, "bias fragments split evenly over the waves of a row");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+  static_assert(BK % 32 == 0 && NST >= 2, "k tile, stages");
 };
 
 // XOR applied to the 16-byte chunk index of LDS row `row` (CH chunks per
@@ -110,8 +115,8 @@ __device__ __forceinline__ void issue_tile(int kt, char *stage0, const WgradArgs
                                            int arow, int acol, int brow, int bci, int btap) {
   const __amdgpu_buffer_rsrc_t rsg = rsrc(G, (uint32_t)((int64_t)M * a.Co * 2));
   const __amdgpu_buffer_rsrc_t rsx = rsrc(X, (uint32_t)((int64_t)M * a.Ci * 2));
-  char *sa = stage0 + (kt & 1) * CF::STAGE;
-  const int pt = p_begin + kt * BK;
+  char *sa = stage0 + (kt % CF::NST) * CF::STAGE;
+  const int pt = p_begin + kt * CF::BK;
 #pragma unroll
   for (int q = 0; q < CF::SA; ++q) {
     const int p = pt + arow + q * CF::QROWA;
@@ -167,10 +172,16 @@ __device__ __forceinline__ void kgroup(f32x4_t (&acc)[CF::TM][CF::TN], f32x4_t (
   }
 }
 
-template <int BM, int BN, int WM, int WN, bool TAPS1>
+// s_waitcnt vmcnt(N) for a compile-time N
+template <int N> __device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <int BM, int BN, int WM, int WN, int BK, int NST, bool TAPS1>
 __global__ void __launch_bounds__(64 * WM * WN)
 wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
-  using CF = Cfg<BM, BN, WM, WN>;
+  using CF = Cfg<BM, BN, WM, WN, BK, NST>;
   constexpr int TM = CF::TM, TN = CF::TN, BPW = CF::BPW;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -188,6 +199,7 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
   const int p_begin = split * a.chunk;
   const int p_end = min(M, p_begin + a.chunk);
   const int nk = (p_end - p_begin + BK - 1) / BK;
+  static_assert(CF::KG <= 2, "at most two k groups per tile");
   const int m0 = mt * BM, n0 = nt * BN;
   const bf16_t *G = reinterpret_cast<const bf16_t *>(a.g) + rep * a.g_rs;
   const bf16_t *X = reinterpret_cast<const bf16_t *>(a.x) + rep * a.x_rs;
@@ -244,18 +256,24 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
 #pragma unroll
   for (int i = 0; i < BPW; ++i) bacc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  issue_tile<CF, TAPS1>(0, stage0, a, fd_w, fd_h, G, X, M, p_begin, p_end, arow, acol, brow, bci, btap);
+#pragma unroll
+  for (int q = 0; q < NST - 1; ++q)
+    if (q < nk) issue_tile<CF, TAPS1>(q, stage0, a, fd_w, fd_h, G, X, M, p_begin, p_end, arow, acol, brow, bci, btap);
   for (int kt = 0; kt < nk; ++kt) {
-    // own copies of tile kt have landed; after the barrier every wave's
-    // have, and every wave is done with tile kt-1, whose stage is refilled
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // own copies of tile kt have landed once only the copies of the tiles
+    // issued after it (kt+1 .. kt+NST-2) are outstanding (vector memory
+    // loads complete in order); near the end every copy is waited for.
+    // After the barrier every wave's copies have landed and every wave is
+    // done with tile kt-1, whose stage receives tile kt+NST-1.
+    if (kt + NST - 2 < nk) wait_vm<(NST - 2) * CF::CPT>();
+    else wait_vm<0>();
     asm volatile("s_barrier" ::: "memory");
-    if (kt + 1 < nk)
-      issue_tile<CF, TAPS1>(kt + 1, stage0, a, fd_w, fd_h, G, X, M, p_begin, p_end, arow, acol, brow, bci,
+    if (kt + NST - 1 < nk)
+      issue_tile<CF, TAPS1>(kt + NST - 1, stage0, a, fd_w, fd_h, G, X, M, p_begin, p_end, arow, acol, brow, bci,
                             btap);
-    const uint32_t st = lds0 + (uint32_t)((kt & 1) * CF::STAGE);
+    const uint32_t st = lds0 + (uint32_t)((kt % NST) * CF::STAGE);
     kgroup<CF, 0>(acc, bacc, ra, rb, st, do_bias, wn);
-    kgroup<CF, 1>(acc, bacc, ra, rb, st, do_bias, wn);
+    if constexpr (CF::KG > 1) kgroup<CF, 1>(acc, bacc, ra, rb, st, do_bias, wn);
   }
   // nk == 0 leaves the first copy in flight
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -292,54 +310,59 @@ bool wgrad_lds_ok(int dtype, int Co, int Ci) {
   return dtype == GCPSL_BF16 && Co >= 64 && Co % 8 == 0 && Ci % 8 == 0;
 }
 
+// Tile configurations: rows (output channels) x columns (im2col columns),
+// waves, k tile, stages.  Measured on the 256-channel layers: 32-pixel tiles
+// in 4 stages and, separately, reads of the next k group pipelined against
+// the MFMAs within a wave were no faster than 64-pixel tiles in 2 stages.
+using WgBig = Cfg<256, 256, 2, 4, 64, 2>;
+using WgMid = Cfg<128, 256, 2, 4, 64, 2>;
+using WgSmall = Cfg<64, 128, 1, 8, 64, 2>;
+
 // Tile of a layer (rows = output channels, columns of the im2col operand)
 // and how many such workgroups one CU holds (LDS-limited).
 void wgrad_lds_tile(int Co, int *bm, int *bn, int *bk, int *per_cu) {
-  *bk = BK;
   if (Co > 128) {
-    *bm = 256; *bn = 256; *per_cu = 160 * 1024 / Cfg<256, 256, 2, 4>::LDS_BYTES;
+    *bm = 256; *bn = 256; *bk = WgBig::BK; *per_cu = 160 * 1024 / WgBig::LDS_BYTES;
   } else if (Co > 64) {
-    *bm = 128; *bn = 256; *per_cu = 160 * 1024 / Cfg<128, 256, 2, 4>::LDS_BYTES;
+    *bm = 128; *bn = 256; *bk = WgMid::BK; *per_cu = 160 * 1024 / WgMid::LDS_BYTES;
   } else {
-    *bm = 64; *bn = 128; *per_cu = 160 * 1024 / Cfg<64, 128, 1, 8>::LDS_BYTES;
+    *bm = 64; *bn = 128; *bk = WgSmall::BK; *per_cu = 160 * 1024 / WgSmall::LDS_BYTES;
   }
 }
 
 // Every instantiation is named in this (non-template) function.
 hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *label) {
-#define WG_K(BM, BN, WM, WN, T) wgrad_lds_kernel<BM, BN, WM, WN, T>
-#define WG_ATTR(BM, BN, WM, WN)                                                                               \
-  for (const void *f : {reinterpret_cast<const void *>(&WG_K(BM, BN, WM, WN, true)),                        \
-                        reinterpret_cast<const void *>(&WG_K(BM, BN, WM, WN, false))}) {                    \
-    const hipError_t e =                                                                                     \
-        hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, Cfg<BM, BN, WM, WN>::LDS_BYTES); \
+#define WG_K(CF, T) wgrad_lds_kernel<CF::BM_, CF::BN_, CF::WM_, CF::WN_, CF::BK, CF::NST, T>
+#define WG_ATTR(CF)                                                                                          \
+  for (const void *f : {reinterpret_cast<const void *>(&WG_K(CF, true)),                                    \
+                        reinterpret_cast<const void *>(&WG_K(CF, false))}) {                                \
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, CF::LDS_BYTES);  \
     if (e != hipSuccess) return e;                                                                           \
   }
   static bool attr = false;
   if (!attr) {
-    WG_ATTR(256, 256, 2, 4)
-    WG_ATTR(128, 256, 2, 4)
-    WG_ATTR(64, 128, 1, 8)
+    WG_ATTR(WgBig)
+    WG_ATTR(WgMid)
+    WG_ATTR(WgSmall)
     attr = true;
   }
   int BM, BN, bk, per_cu;
   wgrad_lds_tile(a.Co, &BM, &BN, &bk, &per_cu);
+  if (a.chunk % bk) return hipErrorInvalidValue;
   const int NW = a.taps == 1 ? a.Ci : 9 * a.Ci;
   const int MT = (a.Co + BM - 1) / BM, NT = (NW + BN - 1) / BN;
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Ci);
   const dim3 g((uint32_t)MT * NT * a.splits * a.C);
   if (label)
     *label = "conv_wgrad<bf16," + std::to_string(BM) + "x" + std::to_string(BN) + ",w8,lds>";
-#define WG_GO(BM, BN, WM, WN, T)                                                                             \
-  hipLaunchKernelGGL((WG_K(BM, BN, WM, WN, T)), g, dim3(Cfg<BM, BN, WM, WN>::NTHR), (Cfg<BM, BN, WM, WN>::LDS_BYTES), \
-                     s, a, fw, fh, fc, MT, NT)
+#define WG_GO(CF, T) hipLaunchKernelGGL((WG_K(CF, T)), g, dim3(CF::NTHR), (CF::LDS_BYTES), s, a, fw, fh, fc, MT, NT)
   const bool t1 = a.taps == 1;
   if (BM == 256) {
-    if (t1) WG_GO(256, 256, 2, 4, true); else WG_GO(256, 256, 2, 4, false);
+    if (t1) WG_GO(WgBig, true); else WG_GO(WgBig, false);
   } else if (BM == 128) {
-    if (t1) WG_GO(128, 256, 2, 4, true); else WG_GO(128, 256, 2, 4, false);
+    if (t1) WG_GO(WgMid, true); else WG_GO(WgMid, false);
   } else {
-    if (t1) WG_GO(64, 128, 1, 8, true); else WG_GO(64, 128, 1, 8, false);
+    if (t1) WG_GO(WgSmall, true); else WG_GO(WgSmall, false);
   }
 #undef WG_GO
 #undef WG_ATTR

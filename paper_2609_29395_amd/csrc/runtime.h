@@ -33,6 +33,7 @@ struct ConvArgs {
   const int32_t *rmap;  // device [C]: replica of each slot, or null (slot z = replica z)
   int epi;
   int taps;  // 9: 3x3 implicit GEMM; 1: src already holds im2col rows, A[m][k] = src[m][k]
+  int res_lds;  // set by the launcher: the residual (== src) is taken from the staged centre tap
 };
 
 // Weight gradient: dW[co][kk] = sum_p G[p][co] X(p, kk), kk = (r, s, ci),

@@ -46,7 +46,7 @@ def kernel_label(name: str) -> str:
         kind = "conv_fwd" if m.group(5) == "0" else "conv_dgrad"
         w = int(m.group(3)) * int(m.group(4))
         return f"{kind}<bf16,{m.group(1)}x{m.group(2)}x64,w{w},lds>"
-    m = re.search(r"wgrad_lds_kernel<(\d+), (\d+), (\d+), (\d+), (true|false)>", name)
+    m = re.search(r"wgrad_lds_kernel<(\d+), (\d+), (\d+), (\d+), (?:\d+, \d+, )?(true|false)>", name)
     if m:
         w = int(m.group(3)) * int(m.group(4))
         return f"conv_wgrad<bf16,{m.group(1)}x{m.group(2)},w{w},lds>"

@@ -89,7 +89,7 @@ def test_sample_and_gather_bit_exact(name, window, starts):
 
 # ------------------------------------------------------- multi-step runs
 
-@pytest.mark.parametrize("name", ["tiny", "tiny_jsd", "ragged", "ragged_bf16"])
+@pytest.mark.parametrize("name", ["tiny", "tiny_jsd", "ragged", "ragged_bf16", "ragged_res_bf16"])
 def test_run_parity_with_fusion(name):
     cfg = get_config(name)
     T = cfg["T"]
@@ -112,7 +112,7 @@ def test_run_parity_with_fusion(name):
     assert np.array_equal(per, np.array(ref.active)) and a == int(np.sum(ref.active))
 
 
-@pytest.mark.parametrize("name", ["ragged", "ragged_bf16", "tiny"])
+@pytest.mark.parametrize("name", ["ragged", "ragged_bf16", "ragged_res_bf16", "tiny"])
 def test_intermediates_one_round(name):
     cfg = get_config(name)
     ctx, assignment = driver.setup(cfg)
