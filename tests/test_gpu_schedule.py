@@ -103,3 +103,46 @@ def test_step_replica_errors():
     assert e.value.code == gcpsl.EINVAL
     ctx.step_replica(R - 1, int(np.argmax(rounds)))
     torch.cuda.synchronize()
+
+
+def test_cluster_of_exactly_b_examples():
+    # B = the smaller cluster's size: that cluster's epoch is one round whose
+    # batch is all of its examples (in permuted order), every round a new epoch
+    cfg = get_config("tiny", B=197, T=3, F=0)
+    ctx, assignment = driver.setup(cfg, max_window=3)
+    sizes = ctx.cluster_sizes()
+    small = int(np.argmin(sizes))
+    assert sizes[small] == cfg["B"]
+    out = torch.zeros(3, cfg["C"], cfg["B"], dtype=torch.int32, device="cuda")
+    ctx.sample(0, 3, out)
+    torch.cuda.synchronize()
+    ref = GCPSLOracle(cfg, cluster_of_client=assignment)
+    got = out.cpu().numpy()
+    for j in range(3):
+        assert np.array_equal(np.sort(got[j, small]), ref.ids[small])
+        assert not np.array_equal(got[0, small], got[1, small])  # a fresh permutation per epoch
+    losses = torch.zeros(3, cfg["C"], device="cuda")
+    for s in range(3):
+        ctx.step(s, losses[s])
+    torch.cuda.synchronize()
+    ref.run(3, F=0)
+    assert np.allclose(losses.cpu().numpy(), np.array(ref.losses), rtol=TOL["f32"])
+    for n in range(cfg["C"]):
+        ok, e = close(ctx.theta[n].cpu().numpy(), ref.theta[n], TOL["f32"])
+        assert ok, (n, e)
+
+
+def test_single_cluster_epoch_schedule_is_gpsl():
+    # C = 1: the system epoch is the cluster's epoch and fusing one replica is
+    # the identity, so the epoch schedule equals lockstep GPSL bit for bit
+    cfg = get_config("tiny_epoch", C=1, B=32)
+    ctx_e, _ = driver.setup(cfg, max_steps=20)
+    rounds, R = ctx_e.epoch_rounds()
+    assert R == rounds[0] == 512 // 32
+    T = R + 2
+    driver.train(ctx_e, T)
+    ctx_l, _ = driver.setup(cfg, max_steps=20, schedule="lockstep")
+    driver.train(ctx_l, T, F=0)
+    torch.cuda.synchronize()
+    assert torch.equal(ctx_e.theta, ctx_l.theta) and torch.equal(ctx_e.mom, ctx_l.mom)
+    assert np.array_equal(ctx_e.participation()[2], ctx_l.participation()[2])
