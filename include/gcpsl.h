@@ -79,8 +79,8 @@ typedef struct gcpsl_layer {
  * Supported model shapes: layer 0 is a conv; every max pool follows a conv and
  * sees an even H and W; the last two layers are GCPSL_AVGPOOL then
  * GCPSL_LINEAR (cout = L), optionally preceded by one max pool; conv channel
- * counts are either 3 (the image layer) or multiples of 8.  Other shapes
- * return GCPSL_EUNSUPPORTED.
+ * counts are either 3 (the image layer) or multiples of 8; at most 16 conv
+ * layers.  Other shapes return GCPSL_EUNSUPPORTED.
  */
 typedef struct gcpsl_desc {
   int32_t K;          /* clients (Sec. III-A), 1..65536                     */

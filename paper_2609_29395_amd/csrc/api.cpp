@@ -76,6 +76,11 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   if (d->schedule != GCPSL_SCHED_LOCKSTEP && d->schedule != GCPSL_SCHED_EPOCH)
     return gcpsl_fail(GCPSL_EINVAL, "unknown schedule");
   if (!d->layers || d->n_layers < 3) return gcpsl_fail(GCPSL_EINVAL, "need at least conv, avgpool, linear");
+  {
+    int convs = 0;
+    for (int i = 0; i < d->n_layers; ++i) convs += d->layers[i].kind == GCPSL_CONV3X3;
+    if (2 * convs > kMaxPrepJobs) return gcpsl_fail(GCPSL_EUNSUPPORTED, "more than 16 conv layers");
+  }
   if (d->cut < 1 || d->cut > d->n_layers - 2) return gcpsl_fail(GCPSL_EINVAL, "cut outside the model");
   if ((int64_t)d->B * d->H * d->W > INT32_MAX / 4) return gcpsl_fail(GCPSL_EUNSUPPORTED, "batch too large");
 
@@ -270,6 +275,7 @@ struct gcpsl_ctx {
   std::vector<int64_t> rounds;  // r_n = floor(n_n / B)
   std::vector<int32_t> order;   // clusters by r_n descending, then index
   int64_t R = 0;                // max_n r_n: slots of a system epoch
+  PrepJobs prep;                // weight-copy jobs of every conv layer
   char *ws = nullptr;
   int64_t staged_lo = -1;
   int staged_n = 0;
@@ -413,6 +419,11 @@ extern "C" int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out) {
   ctx->rounds = std::move(rounds);
   ctx->order = std::move(order);
   ctx->ws = ws;
+  for (size_t i = 0; i < ctx->plan.ly.size(); ++i) {
+    const LayerInfo &l = ctx->plan.ly[i];
+    if (l.spec.kind == GCPSL_CONV3X3)
+      prep_add_layer(ctx->prep, l.w_off, l.Co, l.Ci, ws + l.wf_off, l.Kp, i > 0 ? ws + l.wd_off : nullptr, l.Kdp);
+  }
   *out = ctx;
   return GCPSL_OK;
 }
@@ -479,14 +490,15 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
   float *grad = ctx->at<float>(p.off_grad);
   float *loss = loss_out ? loss_out : ctx->at<float>(p.off_loss);
 
-  // compute copies of the conv weights
-  for (int i = 0; i < n; ++i) {
-    const LayerInfo &l = p.ly[i];
-    if (l.spec.kind != GCPSL_CONV3X3) continue;
-    const double pb = (double)C * (4.0 * l.nw + p.esz * ((double)l.Co * l.Kp + (i > 0 ? (double)l.Ci * l.Kdp : 0.0)));
-    LAUNCH_T("prep_weights", 0.0, pb,
-             launch_prep_weights(p.dtype, d.theta, p.P, C, rmap, l.w_off, l.Co, l.Ci, ws + l.wf_off, l.Kp,
-                                 i > 0 ? ws + l.wd_off : nullptr, l.Kdp, s));
+  // compute copies of the conv weights (one launch for every layer)
+  {
+    double pb = 0.0;
+    for (int i = 0; i < n; ++i) {
+      const LayerInfo &l = p.ly[i];
+      if (l.spec.kind != GCPSL_CONV3X3) continue;
+      pb += (double)C * ((i > 0 ? 8.0 : 4.0) * l.nw + p.esz * ((double)l.Co * l.Kp + (i > 0 ? (double)l.Ci * l.Kdp : 0.0)));
+    }
+    LAUNCH_T("prep_weights", 0.0, pb, launch_prep_weights(p.dtype, d.theta, p.P, C, rmap, ctx->prep, s));
   }
 
   // forward: client segment to the cut, server segment to the loss

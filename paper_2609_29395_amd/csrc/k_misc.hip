@@ -208,43 +208,46 @@ gather_im2col_fixed_kernel(const float *__restrict__ images, const int32_t *__re
 }
 
 // ------------------------------------------------------ weight preparation
-// Compute copies of one conv layer's weights from the fp32 masters:
+// Compute copies of the conv layers' weights from the fp32 masters:
 //   wf[co][k], k = (r, s, ci) < 9 ci, rows zero-padded to Kp (forward);
 //   wd[ci][kk], kk = (r', s', co), wd[ci][(r', s', co)] = W[co][2-r'][2-s'][ci]
 //   rows zero-padded to Kdp (input gradient as a forward conv).
 // wf is a row copy; wd is a transpose of 64 x 64 (co, ci) blocks per kernel
 // tap, staged through LDS so both the reads and the writes are coalesced.
+// One launch covers every layer: workgroup b belongs to the job whose first
+// workgroup is the largest not above b.
 template <typename T>
 __global__ void __launch_bounds__(256)
-prep_wf_kernel(const float *__restrict__ theta, const int32_t *__restrict__ rmap, int64_t P, int64_t w_off, int co,
-               int ci, T *__restrict__ wf, int Kp) {
-  // one output row (blockIdx.x) of one replica (slot blockIdx.y) per workgroup
-  const int rep = replica_of(rmap, blockIdx.y), n = blockIdx.x;
-  const int K = 9 * ci;
-  const float *w = theta + rep * P + w_off + (int64_t)n * K;
-  T *dst = wf + ((int64_t)rep * co + n) * Kp;
-  for (int k = threadIdx.x; k < Kp; k += blockDim.x) dst[k] = ElemT<T>::from_f(k < K ? w[k] : 0.f);
-}
-
-template <typename T>
-__global__ void __launch_bounds__(256)
-prep_wd_kernel(const float *__restrict__ theta, const int32_t *__restrict__ rmap, int64_t P, int64_t w_off, int co,
-               int ci, T *__restrict__ wd, int Kdp) {
+prep_weights_kernel(const float *__restrict__ theta, const int32_t *__restrict__ rmap, int64_t P, PrepJobs jobs) {
   __shared__ float tile[64][65];
-  const int rep = replica_of(rmap, blockIdx.z);
-  const int tap = blockIdx.y;  // (r', s') of the flipped kernel
+  const int b = blockIdx.x;
+  int jn = 0;
+  while (jn + 1 < jobs.n && jobs.j[jn + 1].first <= b) ++jn;
+  const PrepJob &J = jobs.j[jn];
+  const int rep = replica_of(rmap, blockIdx.y);
+  const float *w = theta + rep * P + J.w_off;
+  const int co = J.co, ci = J.ci, K = 9 * ci;
+  const int lb = b - J.first;
+  if (J.kind == 0) {
+    // forward copy: output row lb
+    T *dst = reinterpret_cast<T *>(J.dst) + ((int64_t)rep * co + lb) * J.kpad;
+    const float *src = w + (int64_t)lb * K;
+    for (int k = threadIdx.x; k < J.kpad; k += blockDim.x) dst[k] = ElemT<T>::from_f(k < K ? src[k] : 0.f);
+    return;
+  }
+  // input-gradient copy: block (cb, ib) of tap `tap` of the flipped kernel
+  const int Kdp = J.kpad;
   const int nco = (co + 63) / 64;
-  const int cb = blockIdx.x % nco, ib = blockIdx.x / nco;
+  const int tap = lb % 9, blk = lb / 9;
+  const int cb = blk % nco, ib = blk / nco;
   const int rs_src = 8 - tap;  // (2 - r') * 3 + (2 - s')
-  const float *w = theta + rep * P + w_off;
-  const int K = 9 * ci;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   for (int r = ty; r < 64; r += 4) {
     const int o = cb * 64 + r, c = ib * 64 + tx;
     tile[r][tx] = (o < co && c < ci) ? w[(int64_t)o * K + rs_src * ci + c] : 0.f;
   }
   __syncthreads();
-  T *dst = wd + (int64_t)rep * ci * Kdp;
+  T *dst = reinterpret_cast<T *>(J.dst) + (int64_t)rep * ci * Kdp;
   for (int r = ty; r < 64; r += 4) {
     const int c = ib * 64 + r, o = cb * 64 + tx;
     if (c < ci && o < co) dst[(int64_t)c * Kdp + tap * co + o] = ElemT<T>::from_f(tile[tx][r]);
@@ -264,8 +267,7 @@ prep_wd_kernel(const float *__restrict__ theta, const int32_t *__restrict__ rmap
 // routes each pooled gradient to the first maximum of its window in
 // row-major order (strict >) and applies the producing conv's ReLU mask
 // (output > 0).  A thread handles one 16-byte vector of VEC channels of one
-// output position; index arithmetic is 32-bit (the launcher splits the batch
-// so a launch stays below 2^31 vectors).
+// output position; index arithmetic within a replica is 32-bit.
 
 // One 16-byte vector of activations.
 template <typename T> struct Vec16 {
@@ -727,21 +729,24 @@ hipError_t launch_gather_im2col(const float *images, const int32_t *idx, void *x
   return hipGetLastError();
 }
 
-hipError_t launch_prep_weights(int dtype, const float *theta, int64_t P, int C, const int32_t *rmap, int64_t w_off,
-                               int co, int ci, void *wf, int Kp, void *wd, int Kdp, hipStream_t s) {
-  const dim3 grid((unsigned)co, C);
-  const dim3 gridd(((co + 63) / 64) * ((ci + 63) / 64), 9, C);
-  if (dtype == GCPSL_BF16) {
-    hipLaunchKernelGGL(prep_wf_kernel<bf16_t>, grid, dim3(256), 0, s, theta, rmap, P, w_off, co, ci, (bf16_t *)wf, Kp);
-    if (wd)
-      hipLaunchKernelGGL(prep_wd_kernel<bf16_t>, gridd, dim3(256), 0, s, theta, rmap, P, w_off, co, ci,
-                         (bf16_t *)wd, Kdp);
-  } else {
-    hipLaunchKernelGGL(prep_wf_kernel<float>, grid, dim3(256), 0, s, theta, rmap, P, w_off, co, ci, (float *)wf, Kp);
-    if (wd)
-      hipLaunchKernelGGL(prep_wd_kernel<float>, gridd, dim3(256), 0, s, theta, rmap, P, w_off, co, ci, (float *)wd,
-                         Kdp);
+void prep_add_layer(PrepJobs &jobs, int64_t w_off, int co, int ci, void *wf, int Kp, void *wd, int Kdp) {
+  if (jobs.n + 2 > kMaxPrepJobs) return;  // the plan checks the layer count
+  jobs.j[jobs.n++] = PrepJob{w_off, wf, co, ci, Kp, 0, jobs.total};
+  jobs.total += co;
+  if (wd) {
+    jobs.j[jobs.n++] = PrepJob{w_off, wd, co, ci, Kdp, 1, jobs.total};
+    jobs.total += ((co + 63) / 64) * ((ci + 63) / 64) * 9;
   }
+}
+
+hipError_t launch_prep_weights(int dtype, const float *theta, int64_t P, int C, const int32_t *rmap,
+                               const PrepJobs &jobs, hipStream_t s) {
+  if (jobs.n == 0) return hipSuccess;
+  const dim3 grid((unsigned)jobs.total, C);
+  if (dtype == GCPSL_BF16)
+    hipLaunchKernelGGL(prep_weights_kernel<bf16_t>, grid, dim3(256), 0, s, theta, rmap, P, jobs);
+  else
+    hipLaunchKernelGGL(prep_weights_kernel<float>, grid, dim3(256), 0, s, theta, rmap, P, jobs);
   return hipGetLastError();
 }
 

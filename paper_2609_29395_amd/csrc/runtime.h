@@ -77,9 +77,26 @@ hipError_t launch_gather(const float *images, const int32_t *idx, void *x, int d
 // Gather with im2col: x[row][pixel][k], k = (r, s, c) < 9 Cin, zero to Kc.
 hipError_t launch_gather_im2col(const float *images, const int32_t *idx, void *x, int dtype,
                                 int64_t rows, int H, int W, int Cin, int Kc, hipStream_t s);
-hipError_t launch_prep_weights(int dtype, const float *theta, int64_t P, int C, const int32_t *rmap, int64_t w_off,
-                               int co, int ci, void *wf, int Kp, void *wd, int Kdp,
-                               hipStream_t s);
+// Compute copies of every conv layer's weights in one launch: per layer a
+// forward copy wf [C][co][Kp] (one workgroup per output row) and, except for
+// the image layer, an input-gradient copy wd [C][ci][Kdp] (one workgroup per
+// 64 x 64 block and kernel tap).
+struct PrepJob {
+  int64_t w_off;  // the layer's weights in a replica's parameter vector
+  void *dst;      // wf or wd of replica 0 (replica r at r * co * kpad / r * ci * kpad)
+  int co, ci, kpad;
+  int kind;   // 0 forward copy, 1 input-gradient copy
+  int first;  // first workgroup of the job
+};
+constexpr int kMaxPrepJobs = 32;
+struct PrepJobs {
+  PrepJob j[kMaxPrepJobs];
+  int n = 0, total = 0;  // jobs, workgroups per replica
+};
+// Appends the jobs of one layer (wd may be null).
+void prep_add_layer(PrepJobs &jobs, int64_t w_off, int co, int ci, void *wf, int Kp, void *wd, int Kdp);
+hipError_t launch_prep_weights(int dtype, const float *theta, int64_t P, int C, const int32_t *rmap,
+                               const PrepJobs &jobs, hipStream_t s);
 hipError_t launch_maxpool_fwd(int dtype, const void *x, void *z, int C, const int32_t *rmap, int Bt, int H, int W,
                               int Ch, hipStream_t s);
 hipError_t launch_maxpool_bwd(int dtype, const void *a, const void *gz, void *gpre, int C, const int32_t *rmap,
