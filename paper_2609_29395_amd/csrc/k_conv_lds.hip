@@ -121,7 +121,6 @@ __device__ __forceinline__ void wait_frags(u32x4 (&x)[TA]) {
 }
 
 __device__ __forceinline__ float bf2f(uint32_t bits16) { return bf16_to_f32((bf16_t)bits16); }
-__device__ __forceinline__ uint32_t f2bf(float f) { return (uint32_t)f32_to_bf16(f); }
 
 // Copies of k tile kt into its stage: this thread's SA pixel-row and SB
 // weight-row 16-byte pieces.  The buffer resources are built here from plain
@@ -390,10 +389,10 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
         }
       }
       uint4 ov;
-      ov.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
-      ov.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
-      ov.z = f2bf(v[4]) | (f2bf(v[5]) << 16);
-      ov.w = f2bf(v[6]) | (f2bf(v[7]) << 16);
+      ov.x = pack2_bf16(v[0], v[1]);
+      ov.y = pack2_bf16(v[2], v[3]);
+      ov.z = pack2_bf16(v[4], v[5]);
+      ov.w = pack2_bf16(v[6], v[7]);
       if (nok && m < M) *reinterpret_cast<uint4 *>(out + (int64_t)m * a.N + n) = ov;
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

@@ -77,8 +77,8 @@ gather_kernel(const float *__restrict__ images, const int32_t *__restrict__ idx,
       if constexpr (sizeof(T) == 4) {
         reinterpret_cast<float4 *>(dst)[v] = f;
       } else {
-        const uint32_t lo = (uint32_t)f32_to_bf16(f.x) | ((uint32_t)f32_to_bf16(f.y) << 16);
-        const uint32_t hi = (uint32_t)f32_to_bf16(f.z) | ((uint32_t)f32_to_bf16(f.w) << 16);
+        const uint32_t lo = pack2_bf16(f.x, f.y);
+        const uint32_t hi = pack2_bf16(f.z, f.w);
         reinterpret_cast<uint2 *>(dst)[v] = make_uint2(lo, hi);
       }
     }
