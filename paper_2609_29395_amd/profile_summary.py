@@ -6,6 +6,10 @@
   python -m paper_2609_29395_amd.profile_summary stats TRACE_DIR OUT.md CMD...
       Write a Markdown summary of `rocprofv3 --kernel-trace --stats` CSV output.
   python -m paper_2609_29395_amd.profile_summary traffic FETCH_DIR WRITE_DIR COPY_FETCH_DIR COPY_WRITE_DIR WORKLOAD OUT.json
+  python -m paper_2609_29395_amd.profile_summary layers TRACE_DIR OUT.md CMD...
+      Per-dispatch table of one step from `rocprofv3 --kernel-trace` CSV output.
+  python -m paper_2609_29395_amd.profile_summary gemm-ref OUT.md
+      hipBLASLt bf16 GEMMs of the convolution shapes, for comparison.
       Combine two counter runs of the workload (FETCH_SIZE, then WRITE_SIZE)
       into HBM bytes per launch for every kernel, each counter scaled by what
       it reads for the copy of known size (runs COPY_FETCH_DIR, COPY_WRITE_DIR).
@@ -143,13 +147,94 @@ def traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload, out_
             "bytes_per_launch": 1024.0 * (fk / f_fac + wk / w_fac)}
     with open(out_json, "w") as fh:
         json.dump(out, fh, indent=1, sort_keys=True)
-    print(json.dumps(out, indent=1, sort_keys=True))
+    md = os.path.join(os.path.dirname(out_json), f"{workload}_traffic.md")
+    lines = [f"# HBM traffic per launch, {workload}", "",
+             "Commands (R = repository root; B = `python $R/bench.py --steps 5 --warmup 2 --timing-steps 2 "
+             "--no-cpu-baseline --no-schedule-control`):", "",
+             "* `rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/pfetch -o run -- $B`",
+             "* `rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/pwrite -o run -- $B`",
+             "* `rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/cfetch -o run -- python "
+             "$R/paper_2609_29395_amd/profile_summary.py copy`",
+             "* `rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/cwrite -o run -- python "
+             "$R/paper_2609_29395_amd/profile_summary.py copy`",
+             f"* `python -m paper_2609_29395_amd.profile_summary traffic gpurun_out/pfetch gpurun_out/pwrite "
+             f"gpurun_out/cfetch gpurun_out/cwrite {workload} {out_json}`", "",
+             f"Calibration: a {COPY_MIB} MiB device copy reads FETCH_SIZE = {f_fac:.4f} x and WRITE_SIZE = "
+             f"{w_fac:.4f} x its size; counters are divided by these factors.",
+             "Kernel source hashes when taken: per kernel source file in `traffic.json` (`source_hashes`); "
+             "bench.py reports traffic = null for a kernel whose source file changed since.", "",
+             "| kernel | launches | FETCH KiB/launch | WRITE KiB/launch | HBM MB/launch (calibrated) |",
+             "|---|---|---|---|---|"]
+    for k, v in sorted(out["kernels"].items(), key=lambda kv: -kv[1]["bytes_per_launch"]):
+        lines.append(f"| {k.split(':', 1)[1]} | {v['launches']} | {v['fetch_kib']:.0f} | {v['write_kib']:.0f} | "
+                     f"{v['bytes_per_launch'] / 1e6:.1f} |")
+    lines.append("")
+    with open(md, "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
+
+
+def gemm_reference(out_md):
+    """hipBLASLt (torch.matmul, bf16) on the plain GEMMs with the shapes of the
+    16-cluster workload's convolutions, for comparison with the implicit-GEMM
+    kernels: M = pixels of all replicas, N = output channels, K = 9 * input
+    channels."""
+    import torch
+    shapes = [("256->256 conv as one GEMM", 524288, 256, 2304), ("64->256 conv", 524288, 256, 576),
+              ("32->64 conv (32x32 images)", 2097152, 64, 288)]
+    lines = ["# hipBLASLt reference on the convolution GEMM shapes", "",
+             f"Command: `python -m paper_2609_29395_amd.profile_summary gemm-ref {out_md}`", "",
+             "torch.matmul in bf16 (hipBLASLt), 10 timed calls after 3 warm-up calls, hipEvents.", "",
+             "| shape | M | N | K | us | TFLOP/s |", "|---|---|---|---|---|---|"]
+    for name, M, N, K in shapes:
+        a = torch.randn(M, K, device="cuda", dtype=torch.bfloat16)
+        b = torch.randn(K, N, device="cuda", dtype=torch.bfloat16)
+        for _ in range(3):
+            a @ b
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(10):
+            a @ b
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 10
+        lines.append(f"| {name} | {M} | {N} | {K} | {ms * 1e3:.1f} | {2 * M * N * K / ms / 1e9:.1f} |")
+        del a, b
+    lines.append("")
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
+
+
+def layer_table(trace_dir, out_md, cmd):
+    """Per-dispatch durations of one step (the third), in launch order."""
+    rows = list(csv.DictReader(open(_one(os.path.join(trace_dir, "**", "*kernel_trace.csv")))))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    starts = [i for i, r in enumerate(rows) if "sample_kernel" in r["Kernel_Name"]]
+    i0, i1 = starts[2], starts[3]
+    lines = ["# One step, dispatch by dispatch", "", f"Command: `{' '.join(cmd)}`", "",
+             "| # | kernel (label) | workgroups | us |", "|---|---|---|---|"]
+    tot = 0.0
+    for k, r in enumerate(rows[i0:i1]):
+        d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        tot += d
+        wg = int(r["Grid_Size_X"]) // max(1, int(r["Workgroup_Size_X"]))
+        lines.append(f"| {k} | {kernel_label(r['Kernel_Name'])} | {wg} | {d:.1f} |")
+    lines += ["", f"Sum of kernel time in the step: {tot / 1e3:.3f} ms", ""]
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
 
 
 if __name__ == "__main__":
     what = sys.argv[1]
     if what == "copy":
         copy()
+    elif what == "gemm-ref":
+        gemm_reference(sys.argv[2])
+    elif what == "layers":
+        layer_table(sys.argv[2], sys.argv[3], sys.argv[4:])
     elif what == "stats":
         stats(sys.argv[2], sys.argv[3], sys.argv[4:])
     elif what == "traffic":
