@@ -7,10 +7,10 @@ the initial parameter vector.  It contains none of the method's arithmetic
 the CPU oracle and the GPU path can take their inputs from it without
 sharing any computation.
 """
-from .configs import CONFIGS, get_config, model_layers, param_layout, param_counts
-from .synth import make_dataset, init_params, client_stats
+from .configs import CONFIGS, get_config, model_layers, norm_layout, param_layout, param_counts
+from .synth import make_dataset, init_norm_state, init_params, client_stats
 
 __all__ = [
-    "CONFIGS", "get_config", "model_layers", "param_layout", "param_counts",
-    "make_dataset", "init_params", "client_stats",
+    "CONFIGS", "get_config", "model_layers", "norm_layout", "param_layout", "param_counts",
+    "make_dataset", "init_norm_state", "init_params", "client_stats",
 ]

@@ -12,6 +12,12 @@ Layer tuples:
     ("maxpool",)                    2x2 / stride 2 max pool
     ("avgpool",)                    global average pool over H x W
     ("linear", cin, cout)           fully connected layer producing the logits
+    ("bnorm", ch)                   batch normalisation over (batch, H, W) per
+                                    channel, affine (gamma, beta), then ReLU;
+                                    follows a conv without residual, whose
+                                    output it normalises
+    ("gnorm", ch, groups)           group normalisation over (H, W, channels
+                                    of a group) per example, affine, then ReLU
 
 The client segment is layers[:cut]; the server segment is layers[cut:].
 
@@ -20,9 +26,14 @@ step and fuses every F steps; "epoch" runs the epoch-barrier schedule (each
 cluster floor(n_n / B) rounds per system epoch, fusion after the epoch).
 
 Parameter layout (one flat fp32 vector of P entries per replica): for every
-conv / linear layer in order, its weight followed by its bias.  Conv weights
-are stored [cout][3][3][cin] (output channel, kernel row, kernel column,
-input channel); linear weights [cout][cin].
+conv / linear / norm layer in order, its weight followed by its bias.  Conv
+weights are stored [cout][3][3][cin] (output channel, kernel row, kernel
+column, input channel); linear weights [cout][cin]; a norm layer's weight is
+gamma[ch], its bias beta[ch].
+
+Normalisation state (one flat fp32 vector of S entries per replica): for
+every bnorm layer in order, running mean[ch], running variance[ch] and the
+batch counter.
 """
 from __future__ import annotations
 
@@ -100,6 +111,21 @@ CONFIGS = {
                 ("conv", 64, 128, False), ("conv", 128, 128, True), ("conv", 128, 128, True),
                 ("avgpool",), ("linear", 128, 7)],
         cut=2, dtype="bf16", lr=0.05, momentum=0.9, F=3, T=7, seed=0),
+    # GroupNorm in the client segment, BatchNorm in the server segment
+    # (Sec. IV-B), whose running statistics are fused with the parameters.
+    "tiny_norm": dict(
+        K=16, C=2, B=8, L=4, N_ex=512, H=8, W=8, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="random",
+        layers=[("conv", 3, 8, False), ("gnorm", 8, 2), ("maxpool",),
+                ("conv", 8, 16, False), ("bnorm", 16), ("avgpool",), ("linear", 16, 4)],
+        cut=3, dtype="f32", lr=0.05, momentum=0.9, F=5, T=10, seed=0),
+    "ragged_norm_bf16": dict(
+        K=24, C=3, B=20, L=7, N_ex=1400, H=12, W=12, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="size",
+        layers=[("conv", 3, 8, False), ("gnorm", 8, 4), ("conv", 8, 24, False), ("gnorm", 24, 3),
+                ("maxpool",), ("conv", 24, 136, False), ("bnorm", 136),
+                ("conv", 136, 136, False), ("bnorm", 136), ("avgpool",), ("linear", 136, 7)],
+        cut=5, dtype="bf16", lr=0.05, momentum=0.9, F=3, T=7, seed=0),
     # Epoch-barrier schedule (fusion after every system epoch) on unequal
     # clusters: tiny with B=32 (6 and 9 rounds per epoch), and the ragged
     # shapes under label-L1 clustering with B=100 (7, 4 and 2 rounds).
@@ -142,6 +168,8 @@ def model_layers(cfg: dict) -> list:
     for spec in cfg["layers"]:
         out.append((spec, h, w, c))
         kind = spec[0]
+        if kind in ("bnorm", "gnorm"):
+            continue
         if kind == "conv":
             c = spec[2]
         elif kind == "maxpool":
@@ -161,6 +189,8 @@ def param_layout(cfg: dict) -> list:
             shapes = [("w", (spec[2], 3, 3, spec[1])), ("b", (spec[2],))]
         elif spec[0] == "linear":
             shapes = [("w", (spec[2], spec[1])), ("b", (spec[2],))]
+        elif spec[0] in ("bnorm", "gnorm"):
+            shapes = [("w", (spec[1],)), ("b", (spec[1],))]
         else:
             continue
         for tag, shp in shapes:
@@ -184,3 +214,16 @@ def param_counts(cfg: dict) -> tuple:
         else:
             ps += n
     return pc, ps
+
+
+def norm_layout(cfg: dict) -> list:
+    """[(layer_index, 'mean'|'var'|'count', shape, offset)] of the
+    normalisation state (bnorm layers only)."""
+    out, off = [], 0
+    for i, spec in enumerate(cfg["layers"]):
+        if spec[0] != "bnorm":
+            continue
+        for tag, shp in (("mean", (spec[1],)), ("var", (spec[1],)), ("count", (1,))):
+            out.append((i, tag, shp, off))
+            off += int(shp[0])
+    return out

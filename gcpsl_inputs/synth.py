@@ -9,8 +9,9 @@ share vector p ~ Dir(alpha * 1_K) is drawn, and the shuffled list is cut at
 floor(cumsum(p) * n_class).
 
 Initial parameters follow the PyTorch default bound: every weight and bias of
-a layer with fan-in f is drawn from U(-1/sqrt(f), 1/sqrt(f)).  All replicas
-start from this one vector.
+a layer with fan-in f is drawn from U(-1/sqrt(f), 1/sqrt(f)); normalisation
+layers start at gamma = 1, beta = 0.  All replicas start from this one
+vector.
 """
 from __future__ import annotations
 
@@ -18,7 +19,7 @@ import functools
 
 import numpy as np
 
-from .configs import param_layout
+from .configs import norm_layout, param_layout
 
 
 @functools.lru_cache(maxsize=4)
@@ -68,8 +69,23 @@ def init_params(cfg: dict) -> np.ndarray:
     theta = np.empty(total, dtype=np.float32)
     for i, tag, shp, off in layout:
         spec = cfg["layers"][i]
+        if spec[0] in ("bnorm", "gnorm"):  # gamma = 1, beta = 0 (the PyTorch default)
+            theta[off:off + int(np.prod(shp))] = 1.0 if tag == "w" else 0.0
+            continue
         fan_in = 9 * spec[1] if spec[0] == "conv" else spec[1]
         bound = 1.0 / np.sqrt(fan_in)
         n = int(np.prod(shp))
         theta[off:off + n] = rng.uniform(-bound, bound, size=n).astype(np.float32)
     return theta
+
+
+def init_norm_state(cfg: dict) -> np.ndarray:
+    """Initial normalisation state (float32[S]): running mean 0, running
+    variance 1, counter 0 for every bnorm layer (the PyTorch defaults)."""
+    layout = norm_layout(cfg)
+    total = 0 if not layout else layout[-1][3] + int(np.prod(layout[-1][2]))
+    state = np.zeros(total, dtype=np.float32)
+    for i, tag, shp, off in layout:
+        if tag == "var":
+            state[off:off + int(np.prod(shp))] = 1.0
+    return state

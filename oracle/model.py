@@ -18,13 +18,29 @@ workloads' plain CNNs):
   avgpool    mean over the spatial positions.
   linear     logits = h W^T + b.
   loss       softmax cross-entropy, mean over the batch.
+  bnorm      batch normalisation of the preceding conv's output (that conv
+             then has no ReLU of its own): per channel, mean and biased
+             variance over (batch, H, W), x_hat = (z - mean) / sqrt(var +
+             1e-5), out = ReLU(gamma x_hat + beta).  The server segment's
+             normalisation (Sec. IV-B).
+  gnorm      group normalisation (Wu and He 2018): the same with mean and
+             variance per example over (H, W, the channels of a group).  The
+             client segment's normalisation (Sec. IV-B).
+
+BatchNorm's running statistics (Sec. IV-B: running mean, running variance
+and batch counter, the server normalisation state) follow the PyTorch
+convention: with momentum 0.1, running_mean <- 0.9 running_mean + 0.1 mean,
+running_var <- 0.9 running_var + 0.1 var * n / (n - 1) (the unbiased batch
+variance over n values), counter <- counter + 1.
 
 bf16 workloads round to bf16 (round-to-nearest-even) at these points and keep
 everything else in fp64: the gathered images; the conv and linear weight
 matrices (biases stay at the master's precision); every conv output after
-its ReLU; the average-pool output; the gradient with respect to each conv's
-pre-activation; and each input gradient a conv returns (including the cut
-gradient).  Logits, loss, logit gradients, parameter gradients stay unrounded.
+its ReLU, or its raw output when a norm layer follows; every norm output
+after its ReLU; the average-pool output; the gradient with respect to each
+conv's pre-activation and each norm's pre-ReLU value; and each input
+gradient a conv returns (including the cut gradient).  Norm statistics and
+parameters stay unrounded.  Logits, loss, logit gradients, parameter gradients stay unrounded.
 
 Conv uses im2col with a library matmul for the forward pass and the weight
 gradient, and the textbook col2im scatter for the input gradient.
@@ -115,6 +131,54 @@ def maxpool2_backward(gz, arg):
             .reshape(Bt, 2 * Hh, 2 * Wh, C))
 
 
+EPS_NORM = 1e-5
+BN_MOMENTUM = 0.1
+
+
+def _group_view(z, groups):
+    """[Bt,H,W,C] -> [Bt, H*W, groups, C/groups]: per-example sets of a group."""
+    Bt, H, W, C = z.shape
+    return z.reshape(Bt, H * W, groups, C // groups)
+
+
+def norm_forward(z, gamma, beta, groups=None):
+    """Pre-ReLU output and statistics of batch (groups None) or group
+    normalisation.  Returns (u, x_hat, rstd, mean, var_biased)."""
+    if groups is None:
+        mean = z.mean(axis=(0, 1, 2))
+        var = z.var(axis=(0, 1, 2))
+        rstd = 1.0 / np.sqrt(var + EPS_NORM)
+        x_hat = (z - mean) * rstd
+    else:
+        zg = _group_view(z, groups)
+        mean = zg.mean(axis=(1, 3), keepdims=True)
+        var = zg.var(axis=(1, 3), keepdims=True)
+        rstd = 1.0 / np.sqrt(var + EPS_NORM)
+        x_hat = ((zg - mean) * rstd).reshape(z.shape)
+    return gamma * x_hat + beta, x_hat, rstd, mean, var
+
+
+def norm_backward(du, x_hat, rstd, gamma, groups=None):
+    """(dz, dgamma, dbeta) from the gradient du of the pre-ReLU output."""
+    dgamma = (du * x_hat).sum(axis=(0, 1, 2))
+    dbeta = du.sum(axis=(0, 1, 2))
+    dxh = du * gamma
+    if groups is None:
+        dz = rstd * (dxh - dxh.mean(axis=(0, 1, 2)) - x_hat * (dxh * x_hat).mean(axis=(0, 1, 2)))
+    else:
+        g = _group_view(dxh, groups)
+        xg = _group_view(x_hat, groups)
+        dz = (rstd * (g - g.mean(axis=(1, 3), keepdims=True)
+                      - xg * (g * xg).mean(axis=(1, 3), keepdims=True))).reshape(du.shape)
+    return dz, dgamma, dbeta
+
+
+def bn_running_update(mean_run, var_run, count, mean, var_biased, n):
+    """One running-statistics update (PyTorch convention, momentum 0.1)."""
+    m = BN_MOMENTUM
+    return ((1.0 - m) * mean_run + m * mean, (1.0 - m) * var_run + m * var_biased * n / (n - 1), count + 1.0)
+
+
 def softmax_xent(logits, y):
     """Mean softmax cross-entropy and its gradient with respect to the logits."""
     Bt = logits.shape[0]
@@ -145,13 +209,17 @@ def split_forward_backward(cfg, theta, x, y, keep=False):
 
     theta: flat parameters (fp64 view of the fp32 master); x: [B,H,W,Cin]
     gathered images; y: [B] labels.  Returns (loss, grad[P], record) where
-    record (if keep) holds every intermediate tensor, keyed by name."""
+    record holds each bnorm layer's batch mean, biased variance and value
+    count under "bn_batch" and (if keep) every intermediate tensor, keyed by
+    name."""
     rnd = rounder(cfg["dtype"])
     layers = cfg["layers"]
     p = unflatten(cfg, np.asarray(theta, dtype=np.float64))
     rec = {}
     acts = [rnd(x)]
     args = {}
+    norm = {}
+    rec["bn_batch"] = {}
     for i, spec in enumerate(layers):
         a = acts[-1]
         kind = spec[0]
@@ -161,7 +229,17 @@ def split_forward_backward(cfg, theta, x, y, keep=False):
                 pre = pre + a
             if keep:
                 rec[f"pre{i}"] = pre
-            out = rnd(np.maximum(pre, 0.0))
+            normed = i + 1 < len(layers) and layers[i + 1][0] in ("bnorm", "gnorm")
+            out = rnd(pre) if normed else rnd(np.maximum(pre, 0.0))
+        elif kind in ("bnorm", "gnorm"):
+            groups = spec[2] if kind == "gnorm" else None
+            u, x_hat, rstd, mean, var = norm_forward(a, p[i]["w"], p[i]["b"], groups)
+            norm[i] = (x_hat, rstd, groups)
+            if kind == "bnorm":
+                rec["bn_batch"][i] = (mean, var, a.shape[0] * a.shape[1] * a.shape[2])
+            if keep:
+                rec[f"pre{i}"] = u
+            out = rnd(np.maximum(u, 0.0))
         elif kind == "maxpool":
             out, args[i] = maxpool2_forward(a)
         elif kind == "avgpool":
@@ -190,8 +268,18 @@ def split_forward_backward(cfg, theta, x, y, keep=False):
             g = np.broadcast_to((g / (H * W))[:, None, None, :], a_in.shape).copy()
         elif kind == "maxpool":
             g = maxpool2_backward(g, args[i])
+        elif kind in ("bnorm", "gnorm"):
+            du = rnd(g * (a_out > 0))
+            if keep:
+                rec[f"gpre{i}"] = du
+            x_hat, rstd, groups = norm[i]
+            dz, dgamma, dbeta = norm_backward(du, x_hat, rstd, p[i]["w"], groups)
+            gview[i]["w"][...] = dgamma
+            gview[i]["b"][...] = dbeta
+            g = rnd(dz)
         elif kind == "conv":
-            gp = rnd(g * (a_out > 0))
+            normed = i + 1 < len(layers) and layers[i + 1][0] in ("bnorm", "gnorm")
+            gp = g if normed else rnd(g * (a_out > 0))
             if keep:
                 rec[f"gpre{i}"] = gp
             dx, dw, db = conv3x3_backward(a_in, rnd(p[i]["w"]), gp)

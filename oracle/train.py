@@ -21,6 +21,10 @@ Readings:
     identical replicas returns them unchanged, bit for bit.
   * The reported loss of a round is the forward loss before that round's
     update.
+  * The server normalisation state (each BatchNorm layer's running mean,
+    running variance and batch counter, Sec. IV-B) is updated by every round
+    of its replica and fused with the same weights as the parameters
+    (Sec. IV-D), in fp64 and rounded once to fp32 like them.
 
 Epoch-barrier schedule (Sec. III-A, Sec. IV-D "Schedule and Cost", Eq. 6):
 cluster n takes r_n = floor(n_n / B) local rounds per epoch (the sampler's
@@ -35,10 +39,10 @@ from __future__ import annotations
 
 import numpy as np
 
-from gcpsl_inputs import client_stats, init_params, make_dataset
+from gcpsl_inputs import client_stats, init_norm_state, init_params, make_dataset, norm_layout
 
 from .assign import assign
-from .model import split_forward_backward
+from .model import bn_running_update, split_forward_backward
 from .sampler import active_clients, batch_indices, cluster_examples
 
 
@@ -86,12 +90,29 @@ class GCPSLOracle:
         t0 = init_params(cfg) if theta0 is None else theta0
         self.theta = [np.asarray(t0, dtype=np.float32).copy() for _ in range(cfg["C"])]
         self.mom = [np.zeros_like(self.theta[0]) for _ in range(cfg["C"])]
+        self.norm = [init_norm_state(cfg) for _ in range(cfg["C"])]
         self.active = []
         self.losses = []
 
     def batch(self, step, n):
         idx = batch_indices(self.ids[n], self.cfg["B"], self.cfg["seed"], n, step)
         return idx, self.images[idx].astype(np.float64), self.labels[idx].astype(np.int64)
+
+    def _update_norm_state(self, n, bn_batch):
+        """Running statistics of replica n's BatchNorm layers after a round."""
+        st = self.norm[n]
+        for i, tag, shp, off in norm_layout(self.cfg):
+            if tag != "mean":
+                continue
+            ch = shp[0]
+            mean, var, count = bn_batch[i]
+            rm = st[off:off + ch].astype(np.float64)
+            rv = st[off + ch:off + 2 * ch].astype(np.float64)
+            cnt = float(st[off + 2 * ch])
+            rm, rv, cnt = bn_running_update(rm, rv, cnt, mean, var, count)
+            st[off:off + ch] = rm.astype(np.float32)
+            st[off + ch:off + 2 * ch] = rv.astype(np.float32)
+            st[off + 2 * ch] = np.float32(cnt)
 
     def round(self, step, replicas=None):
         """One local round for the given replicas (default: all).
@@ -104,8 +125,9 @@ class GCPSLOracle:
         for n in reps:
             idx, x, y = self.batch(step, n)
             active[n] = active_clients(idx, self.coe)
-            loss, g, _ = split_forward_backward(cfg, self.theta[n], x, y)
+            loss, g, rec = split_forward_backward(cfg, self.theta[n], x, y)
             sgd_update(self.theta[n], self.mom[n], g, cfg["lr"], cfg["momentum"])
+            self._update_norm_state(n, rec["bn_batch"])
             losses[n], grads[n] = loss, g
         if replicas is None:
             self.active.append([active[n] for n in range(cfg["C"])])
@@ -116,6 +138,10 @@ class GCPSLOracle:
         fused = fuse(self.theta, self.weights)
         for n in range(self.cfg["C"]):
             self.theta[n] = fused.copy()
+        if len(self.norm[0]):
+            fused_norm = fuse(self.norm, self.weights)
+            for n in range(self.cfg["C"]):
+                self.norm[n] = fused_norm.copy()
 
     def slot(self, s):
         """Slot s of the epoch-barrier schedule; fuses after the epoch's last
@@ -128,8 +154,9 @@ class GCPSLOracle:
             if t < rounds[n]:
                 idx, x, y = self.batch(m * rounds[n] + t, n)
                 active.append(active_clients(idx, self.coe))
-                loss, g, _ = split_forward_backward(cfg, self.theta[n], x, y)
+                loss, g, rec = split_forward_backward(cfg, self.theta[n], x, y)
                 sgd_update(self.theta[n], self.mom[n], g, cfg["lr"], cfg["momentum"])
+                self._update_norm_state(n, rec["bn_batch"])
                 losses[n] = loss
             else:
                 active.append(0)  # waits at the barrier: no batch, no update

@@ -158,13 +158,16 @@ class _RoundBwd(torch.autograd.Function):
         return torch.from_numpy(round_bf16(g.detach().numpy()))
 
 
-def torch_split_model_loss(cfg, theta, x, y):
+def torch_split_model_loss(cfg, theta, x, y, with_running=False):
     """Loss and gradient of the unsplit CNN via torch.autograd in fp64.
 
     bf16 workloads insert rounding nodes at the documented points: forward
     rounding of inputs, weights, conv outputs and the pooled feature;
     backward rounding of each conv's pre-activation gradient and of the
-    gradient a conv returns for its input."""
+    gradient a conv returns for its input.  Norm layers are torch's
+    batch_norm (training mode, momentum 0.1) and group_norm, eps 1e-5; a
+    conv followed by one has no ReLU and the norm's pre-ReLU gradient is
+    rounded instead."""
     bf16 = cfg["dtype"] == "bf16"
     rf = _RoundFwd.apply if bf16 else (lambda t: t)
     rb = _RoundBwd.apply if bf16 else (lambda t: t)
@@ -174,14 +177,28 @@ def torch_split_model_loss(cfg, theta, x, y):
         n = int(np.prod(shp))
         views.setdefault(i, {})[tag] = th[off:off + n].reshape(shp)
     a = rf(torch.tensor(x).permute(0, 3, 1, 2))
-    for i, spec in enumerate(cfg["layers"]):
+    layers = cfg["layers"]
+    running = {}
+    for i, spec in enumerate(layers):
         if spec[0] == "conv":
-            a_in = rb(a) if i > 0 else a
+            a_in = rb(a) if i > 0 and layers[i - 1][0] not in ("bnorm", "gnorm") else a
             w = rf(views[i]["w"]).permute(0, 3, 1, 2)
             pre = tF.conv2d(a_in, w, views[i]["b"], padding=1)
             if spec[3]:
                 pre = pre + a_in
-            a = rf(torch.relu(rb(pre)))
+            if i + 1 < len(layers) and layers[i + 1][0] in ("bnorm", "gnorm"):
+                a = rf(rb(pre))  # raw output, normalised next
+            else:
+                a = rf(torch.relu(rb(pre)))
+        elif spec[0] == "bnorm":
+            rm = torch.zeros(spec[1], dtype=torch.float64)
+            rv = torch.ones(spec[1], dtype=torch.float64)
+            u = tF.batch_norm(a, rm, rv, views[i]["w"], views[i]["b"], training=True, momentum=0.1, eps=1e-5)
+            running[i] = (rm, rv)
+            a = rf(torch.relu(rb(u)))
+        elif spec[0] == "gnorm":
+            u = tF.group_norm(a, spec[2], views[i]["w"], views[i]["b"], eps=1e-5)
+            a = rf(torch.relu(rb(u)))
         elif spec[0] == "maxpool":
             a = tF.max_pool2d(a, 2)
         elif spec[0] == "avgpool":
@@ -190,10 +207,12 @@ def torch_split_model_loss(cfg, theta, x, y):
             a = a @ rf(views[i]["w"]).T + views[i]["b"]
     loss = tF.cross_entropy(a, torch.tensor(y))
     loss.backward()
+    if with_running:
+        return loss.item(), th.grad.numpy(), {i: (m.numpy(), v.numpy()) for i, (m, v) in running.items()}
     return loss.item(), th.grad.numpy()
 
 
-@pytest.mark.parametrize("name", ["tiny", "ragged", "ragged_bf16"])
+@pytest.mark.parametrize("name", ["tiny", "ragged", "ragged_bf16", "tiny_norm", "ragged_norm_bf16"])
 def test_split_step_matches_torch_autograd(name):
     cfg = get_config(name)
     theta = init_params(cfg)
@@ -201,10 +220,14 @@ def test_split_step_matches_torch_autograd(name):
     loss, grad, _ = split_forward_backward(cfg, theta, x, y)
     tloss, tgrad = torch_split_model_loss(cfg, theta, x, y)
     assert loss == pytest.approx(tloss, rel=1e-12)
+    # absolute floor at the gradient's overall scale: the bias of a conv that
+    # feeds a BatchNorm has an exactly zero gradient (the batch mean removes
+    # it), which both sides produce as rounding noise
+    scale = np.abs(tgrad).max()
     for i, tag, shp, off in param_layout(cfg):
         n = int(np.prod(shp))
         a, b = grad[off:off + n], tgrad[off:off + n]
-        assert np.allclose(a, b, rtol=1e-9, atol=1e-12 * np.abs(b).max()), (i, tag)
+        assert np.allclose(a, b, rtol=1e-9, atol=1e-12 * max(np.abs(b).max(), 1e-3 * scale)), (i, tag)
 
 
 def test_split_step_matches_torch_autograd_wide_residual_server():
@@ -230,6 +253,70 @@ def test_split_step_finite_differences():
         if key.startswith("pre"):
             assert np.abs(v).min() > 1e-6, key
     for i, spec in enumerate(cfg["layers"]):
+        if spec[0] == "maxpool":
+            a = rec["acts"][i]
+            Bt, H, W, C = a.shape
+            win = np.sort(a.reshape(Bt, H // 2, 2, W // 2, 2, C).transpose(0, 1, 3, 5, 2, 4)
+                          .reshape(-1, 4), axis=1)
+            live = win[:, 3] > 0
+            assert (win[live, 3] - win[live, 2]).min() > 1e-6
+    rng = np.random.default_rng(0)
+    coords = rng.choice(len(theta), size=60, replace=False)
+    h = 1e-6
+    for j in coords:
+        tp, tm = theta.copy(), theta.copy()
+        tp[j] += h
+        tm[j] -= h
+        fd = (split_forward_backward(cfg, tp, x, y)[0] - split_forward_backward(cfg, tm, x, y)[0]) / (2 * h)
+        assert abs(fd - grad[j]) <= 1e-8 + 1e-6 * abs(grad[j]), (j, fd, grad[j])
+
+
+@pytest.mark.parametrize("name", ["tiny_norm", "ragged_norm_bf16"])
+def test_batchnorm_running_statistics_match_torch(name):
+    # one round's running mean / variance update (Sec. IV-B normalisation
+    # state) against torch's buffers after one training-mode batch_norm
+    from gcpsl_inputs import norm_layout
+    from oracle.model import bn_running_update
+    cfg = get_config(name)
+    theta = init_params(cfg)
+    x, y = _batch(cfg)
+    _, _, rec = split_forward_backward(cfg, theta, x, y)
+    _, _, running = torch_split_model_loss(cfg, theta, x, y, with_running=True)
+    assert sorted(rec["bn_batch"]) == sorted(running)
+    for i, (mean, var, n) in rec["bn_batch"].items():
+        ch = cfg["layers"][i][1]
+        rm, rv, cnt = bn_running_update(np.zeros(ch), np.ones(ch), 0.0, mean, var, n)
+        assert np.allclose(rm, running[i][0], rtol=1e-12, atol=1e-15)
+        assert np.allclose(rv, running[i][1], rtol=1e-12)
+        assert cnt == 1.0
+    assert [t for _, t, _, _ in norm_layout(cfg)] == ["mean", "var", "count"] * len(running)
+
+
+def test_norm_closed_forms():
+    # batch norm of a constant-shifted, scaled tensor: x_hat is the
+    # standardised tensor whatever the shift and scale; group norm with one
+    # channel per group and H = W = 1 gives zero (each set has one value)
+    from oracle.model import norm_forward
+    rng = np.random.default_rng(4)
+    z = rng.standard_normal((3, 4, 5, 6))
+    _, xh1, _, _, _ = norm_forward(z, np.ones(6), np.zeros(6))
+    _, xh2, _, _, _ = norm_forward(7.0 * z - 3.0, np.ones(6), np.zeros(6))
+    assert np.allclose(xh1, xh2, atol=1e-4)  # eps = 1e-5 sets the small difference
+    assert np.allclose(xh1.mean(axis=(0, 1, 2)), 0.0, atol=1e-12)
+    assert np.allclose((xh1 ** 2).mean(axis=(0, 1, 2)), 1.0 / (1.0 + 1e-5 / z.var(axis=(0, 1, 2))), rtol=1e-12)
+    u, _, _, _, _ = norm_forward(rng.standard_normal((2, 1, 1, 6)), np.full(6, 2.0), np.full(6, 0.5), groups=6)
+    assert np.allclose(u, 0.5)  # x_hat = 0, so u = beta
+
+
+def test_split_step_finite_differences_with_norm_layers():
+    cfg = get_config("tiny_norm")
+    theta = init_params(cfg).astype(np.float64)
+    theta += np.random.default_rng(1).uniform(-0.1, 0.1, theta.shape)  # gamma, beta off their init
+    x, y = _batch(cfg, seed=5)
+    loss, grad, rec = split_forward_backward(cfg, theta, x, y, keep=True)
+    for i, spec in enumerate(cfg["layers"]):
+        if spec[0] in ("bnorm", "gnorm"):  # no ReLU kink within reach
+            assert np.abs(rec[f"pre{i}"]).min() > 1e-6
         if spec[0] == "maxpool":
             a = rec["acts"][i]
             Bt, H, W, C = a.shape

@@ -95,3 +95,23 @@ def test_tiny_workload_learns():
     L = np.array(o.losses).mean(axis=1)
     assert abs(L[:5].mean() - np.log(4)) < 0.1
     assert L[-20:].mean() < 0.5
+
+
+def test_normalisation_state_is_fused_with_the_parameter_weights():
+    # Sec. IV-B / IV-D: each server replica's BatchNorm running mean, variance
+    # and counter evolve locally and are fused with the weights n_n / W
+    cfg = get_config("tiny_norm", F=0)
+    o = GCPSLOracle(cfg)
+    for s in range(3):
+        o.round(s)
+    assert not np.array_equal(o.norm[0], o.norm[1])
+    before = [st.astype(np.float64) for st in o.norm]
+    W = sum(o.weights)
+    want = (sum(w * st for w, st in zip(o.weights, before)) / W).astype(np.float32)
+    o.fuse()
+    for st in o.norm:
+        assert np.array_equal(st, want)
+    # the counter of every replica is 3 rounds, so the fused counter is 3
+    from gcpsl_inputs import norm_layout
+    counts = [off for _, tag, _, off in norm_layout(cfg) if tag == "count"]
+    assert all(o.norm[0][c] == 3.0 for c in counts)
