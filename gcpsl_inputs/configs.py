@@ -119,13 +119,16 @@ CONFIGS = {
         layers=[("conv", 3, 8, False), ("gnorm", 8, 2), ("maxpool",),
                 ("conv", 8, 16, False), ("bnorm", 16), ("avgpool",), ("linear", 16, 4)],
         cut=3, dtype="f32", lr=0.05, momentum=0.9, F=5, T=10, seed=0),
+    # (bf16 without a max pool: normalised bf16 values tie often, and a
+    # one-ulp difference would move a max-pool gradient; the fp32 workload
+    # above covers norm + max pool)
     "ragged_norm_bf16": dict(
         K=24, C=3, B=20, L=7, N_ex=1400, H=12, W=12, Cin=3, noise_std=0.5, alpha=0.5,
         rule="size",
         layers=[("conv", 3, 8, False), ("gnorm", 8, 4), ("conv", 8, 24, False), ("gnorm", 24, 3),
-                ("maxpool",), ("conv", 24, 136, False), ("bnorm", 136),
+                ("conv", 24, 136, False), ("bnorm", 136),
                 ("conv", 136, 136, False), ("bnorm", 136), ("avgpool",), ("linear", 136, 7)],
-        cut=5, dtype="bf16", lr=0.05, momentum=0.9, F=3, T=7, seed=0),
+        cut=4, dtype="bf16", lr=0.05, momentum=0.9, F=3, T=7, seed=0),
     # Epoch-barrier schedule (fusion after every system epoch) on unequal
     # clusters: tiny with B=32 (6 and 9 rounds per epoch), and the ragged
     # shapes under label-L1 clustering with B=100 (7, 4 and 2 rounds).

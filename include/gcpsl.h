@@ -64,23 +64,37 @@ extern "C" {
 #define GCPSL_MAXPOOL2 2 /* 2x2 max pool, stride 2                           */
 #define GCPSL_AVGPOOL 3  /* global average pool                              */
 #define GCPSL_LINEAR 4   /* fully connected layer producing the logits       */
+#define GCPSL_BATCHNORM 5 /* batch norm of the conv before it, then ReLU     */
+#define GCPSL_GROUPNORM 6 /* group norm of the conv before it, then ReLU     */
 
 /* Layer flags. */
 #define GCPSL_RESIDUAL 1 /* conv output is ReLU(conv(x) + b + x); cin == cout */
 
 typedef struct gcpsl_layer {
-  int32_t kind;  /* GCPSL_CONV3X3 ... GCPSL_LINEAR                         */
-  int32_t cin;   /* input channels (conv, linear); ignored for pools       */
-  int32_t cout;  /* output channels (conv, linear); ignored for pools      */
-  int32_t flags; /* GCPSL_RESIDUAL or 0                                    */
+  int32_t kind;   /* GCPSL_CONV3X3 ... GCPSL_GROUPNORM                     */
+  int32_t cin;    /* input channels (conv, linear, norm); ignored for pools */
+  int32_t cout;   /* output channels (conv, linear; norm: = cin)           */
+  int32_t flags;  /* GCPSL_RESIDUAL or 0                                   */
+  int32_t groups; /* GCPSL_GROUPNORM: groups (dividing the channels); else 0 */
 } gcpsl_layer;
 
 /*
- * Supported model shapes: layer 0 is a conv; every max pool follows a conv and
- * sees an even H and W; the last two layers are GCPSL_AVGPOOL then
- * GCPSL_LINEAR (cout = L), optionally preceded by one max pool; conv channel
- * counts are either 3 (the image layer) or multiples of 8; at most 16 conv
- * layers.  Other shapes return GCPSL_EUNSUPPORTED.
+ * Supported model shapes: layer 0 is a conv; every max pool follows a conv or
+ * norm layer and sees an even H and W; the last two layers are GCPSL_AVGPOOL
+ * then GCPSL_LINEAR (cout = L), optionally preceded by one max pool; conv
+ * channel counts are either 3 (the image layer) or multiples of 8; at most 16
+ * conv layers.  Other shapes return GCPSL_EUNSUPPORTED.
+ *
+ * Normalisation layers (Sec. IV-B: GroupNorm in the client segment,
+ * BatchNorm in the server segment) follow a conv without GCPSL_RESIDUAL; that
+ * conv then stores its raw output z and the norm layer applies
+ * u = gamma_c (z - mean) / sqrt(var + 1e-5) + beta_c and ReLU, with mean and
+ * biased var per channel over (batch, H, W) (batch norm) or per example over
+ * (H, W, the channels of a group) (group norm).  gamma and beta are the
+ * layer's weight and bias in the parameter vector (initial values 1 and 0).
+ * Each round also updates the replica's batch-norm running statistics
+ * (momentum 0.1: mean <- 0.9 mean + 0.1 batch mean, var <- 0.9 var + 0.1
+ * unbiased batch variance; counter + 1) in norm_state.
  */
 typedef struct gcpsl_desc {
   int32_t K;          /* clients (Sec. III-A), 1..65536                     */
@@ -105,6 +119,10 @@ typedef struct gcpsl_desc {
   const int32_t *labels; /* device [n_examples], in [0, L)                  */
   float *theta;          /* device [C][P] fp32 masters, in/out              */
   float *momentum_buf;   /* device [C][P] fp32 momentum, in/out             */
+  float *norm_state;     /* device [C][S] fp32 batch-norm running statistics
+                            (per batch-norm layer in order: running mean[ch],
+                            running variance[ch], counter), in/out; NULL if
+                            the model has no batch norm (S = 0)             */
   void *workspace;       /* device, >= gcpsl_workspace_bytes(), 256-aligned */
   size_t workspace_bytes;
 } gcpsl_desc;
@@ -115,6 +133,9 @@ typedef struct gcpsl_ctx gcpsl_ctx;
  * client segment, which come first).  Host only.  EINVAL / EUNSUPPORTED on a
  * bad model description. */
 int gcpsl_param_count(const gcpsl_desc *d, int64_t *P, int64_t *P_client);
+
+/* Entries S of one replica's normalisation state (norm_state).  Host only. */
+int gcpsl_state_count(const gcpsl_desc *d, int64_t *S);
 
 /* Workspace size in bytes for this description.  Host only. */
 int gcpsl_workspace_bytes(const gcpsl_desc *d, size_t *bytes);
@@ -226,7 +247,8 @@ int gcpsl_epoch_rounds(gcpsl_ctx *ctx, int64_t *rounds, int64_t *slots);
  * Fusion and broadcast, Eq. 5 (Sec. IV-D): theta_bar = sum_n (n_n / W)
  * theta_n over both segments, accumulated in fp64 in cluster order, divided
  * once by W = sum_n n_n and rounded once to fp32, then written to every
- * replica.  Momentum is not touched (optimizer state stays local).
+ * replica.  The server normalisation state (norm_state) is fused the same way
+ * (Sec. IV-B, IV-D).  Momentum is not touched (optimizer state stays local).
  */
 int gcpsl_fuse(gcpsl_ctx *ctx, void *stream);
 

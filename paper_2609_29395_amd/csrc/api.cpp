@@ -38,7 +38,16 @@ struct LayerInfo {
   bool has_gin = false;
   int Kp = 0, Kdp = 0;
   int splits = 1, chunk = 0;
+  bool no_relu = false;       // conv followed by a norm layer: raw output
+  int groups = 0;             // group norm: groups (0: batch norm)
+  int nstat = 0;              // norm statistics per replica
+  int64_t st_off = 0;         // batch norm: running statistics in the state vector
+  size_t mean_off = 0, rstd_off = 0, sums_off = 0;
 };
+
+bool is_norm(int kind) { return kind == GCPSL_BATCHNORM || kind == GCPSL_GROUPNORM; }
+// layers whose output is followed by ReLU and stored: conv or norm
+bool is_act(int kind) { return kind == GCPSL_CONV3X3 || is_norm(kind); }
 
 struct Plan {
   int dtype = 0, esz = 4;
@@ -46,8 +55,9 @@ struct Plan {
   int64_t n_examples = 0, max_steps = 0;
   int max_window = 1;
   std::vector<LayerInfo> ly;
-  int64_t P = 0, Pc = 0;
-  int head_conv = -1, avg_idx = -1, lin_idx = -1;
+  int64_t P = 0, Pc = 0, S = 0;
+  int head_conv = -1, avg_idx = -1, lin_idx = -1;  // head_conv: conv or norm feeding the head pooling
+  int norm_chunk_px = 256;
   bool head_maxpool = false;
   int Ch_head = 0;
   // The image layer's input is staged as im2col rows when its channel count
@@ -58,7 +68,7 @@ struct Plan {
   int schedule = GCPSL_SCHED_LOCKSTEP;
   size_t off_ids = 0, off_off = 0, off_coe = 0, off_fw = 0, off_hits = 0, off_idx = 0, off_y = 0,
          off_x = 0, off_dh = 0, off_grad = 0, off_part = 0, off_dbpart = 0, off_loss = 0, off_order = 0,
-         off_ident = 0;
+         off_ident = 0, off_npart = 0;
   size_t total = 0;
 };
 
@@ -109,16 +119,35 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
       if ((l.spec.flags & GCPSL_RESIDUAL) && l.spec.cin != l.spec.cout)
         return gcpsl_fail(GCPSL_EINVAL, "residual conv needs cin == cout");
       if (l.spec.flags & ~GCPSL_RESIDUAL) return gcpsl_fail(GCPSL_EINVAL, "unknown layer flag");
-      if (i > 0 && p.ly[i - 1].spec.kind != GCPSL_CONV3X3 && p.ly[i - 1].spec.kind != GCPSL_MAXPOOL2)
-        return gcpsl_fail(GCPSL_EUNSUPPORTED, "conv must follow a conv or a max pool");
+      if (i > 0 && !is_act(p.ly[i - 1].spec.kind) && p.ly[i - 1].spec.kind != GCPSL_MAXPOOL2)
+        return gcpsl_fail(GCPSL_EUNSUPPORTED, "conv must follow a conv, a norm or a max pool");
+      l.no_relu = i + 1 < n && is_norm(d->layers[i + 1].kind);
+      if (l.no_relu && (l.spec.flags & GCPSL_RESIDUAL))
+        return gcpsl_fail(GCPSL_EUNSUPPORTED, "a residual conv cannot feed a norm layer");
       l.Co = l.spec.cout; l.Ho = H; l.Wo = W;
       l.nw = (int64_t)l.Co * 9 * l.Ci;
       l.w_off = P; P += l.nw;
       l.b_off = P; P += l.Co;
       c = l.Co;
-    } else if (kind == GCPSL_MAXPOOL2) {
+    } else if (is_norm(kind)) {
       if (i == 0 || p.ly[i - 1].spec.kind != GCPSL_CONV3X3)
-        return gcpsl_fail(GCPSL_EUNSUPPORTED, "max pool must follow a conv");
+        return gcpsl_fail(GCPSL_EUNSUPPORTED, "a norm layer must follow a conv");
+      if (l.spec.cin != c || l.spec.cout != c) return gcpsl_fail(GCPSL_EINVAL, "norm channels must match the conv");
+      l.groups = kind == GCPSL_GROUPNORM ? l.spec.groups : 0;
+      if (kind == GCPSL_GROUPNORM && (l.groups < 1 || c % l.groups != 0))
+        return gcpsl_fail(GCPSL_EINVAL, "group norm needs groups >= 1 dividing the channels");
+      if (!norm_ok(d->dtype, c, l.groups)) return gcpsl_fail(GCPSL_EUNSUPPORTED, "norm layer channels");
+      l.Co = c; l.Ho = H; l.Wo = W;
+      l.w_off = P; P += c;  // gamma
+      l.b_off = P; P += c;  // beta
+      l.nstat = l.groups ? d->B * l.groups : c;
+      if (kind == GCPSL_BATCHNORM) {
+        l.st_off = p.S;
+        p.S += 2 * c + 1;  // running mean, running variance, counter
+      }
+    } else if (kind == GCPSL_MAXPOOL2) {
+      if (i == 0 || !is_act(p.ly[i - 1].spec.kind))
+        return gcpsl_fail(GCPSL_EUNSUPPORTED, "max pool must follow a conv or a norm layer");
       if (H % 2 || W % 2) return gcpsl_fail(GCPSL_EINVAL, "max pool needs even H and W");
       H /= 2; W /= 2;
       l.Co = c; l.Ho = H; l.Wo = W;
@@ -148,8 +177,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   } else {
     p.head_conv = n - 3;
   }
-  if (p.head_conv < 0 || p.ly[p.head_conv].spec.kind != GCPSL_CONV3X3)
-    return gcpsl_fail(GCPSL_EUNSUPPORTED, "avgpool must follow a conv or a conv + max pool");
+  if (p.head_conv < 0 || !is_act(p.ly[p.head_conv].spec.kind) || p.ly[p.head_conv].no_relu)
+    return gcpsl_fail(GCPSL_EUNSUPPORTED, "avgpool must follow a conv or norm layer, optionally + max pool");
   p.Ch_head = p.ly[p.head_conv].Co;
   if (linear_ce_lds_bytes(d->B, p.Ch_head, d->L) > kMaxLinearLds)
     return gcpsl_fail(GCPSL_EUNSUPPORTED, "classifier head too large for one workgroup (B * channels)");
@@ -179,10 +208,23 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   }
   p.x_rs = (int64_t)C * B * p.H * p.W * p.Kc;
   p.off_x = take((size_t)p.esz * p.max_window * p.x_rs);
-  size_t part = 0, dbpart = 0;
+  size_t part = 0, dbpart = 0, npart = 0;
   for (int i = 0; i < n; ++i) {
     LayerInfo &l = p.ly[i];
     const int kind = l.spec.kind;
+    if (is_norm(kind)) {
+      const int64_t rs = (int64_t)B * l.H * l.W;
+      l.stored = true;
+      l.act_rs = rs * l.Co;
+      l.act_off = take((size_t)p.esz * C * l.act_rs);
+      l.gpre_off = take((size_t)p.esz * C * l.act_rs);  // dL/du
+      l.mean_off = take(sizeof(float) * C * l.nstat);
+      l.rstd_off = take(sizeof(float) * C * l.nstat);
+      l.sums_off = take(sizeof(double) * 2 * C * l.nstat);
+      const int64_t chunks = (rs + p.norm_chunk_px - 1) / p.norm_chunk_px;
+      npart = std::max(npart, (size_t)(C * chunks * l.Co * 2));
+      continue;
+    }
     if (kind == GCPSL_CONV3X3 || (kind == GCPSL_MAXPOOL2 && !(p.head_maxpool && i == n - 3))) {
       l.stored = true;
       l.act_rs = (int64_t)B * l.Ho * l.Wo * l.Co;
@@ -253,6 +295,7 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   p.off_part = take(sizeof(float) * std::max<size_t>(part, 1));
   p.off_dbpart = take(sizeof(float) * std::max<size_t>(dbpart, 1));
   p.off_loss = take(sizeof(float) * C);
+  p.off_npart = take(sizeof(double) * std::max<size_t>(npart, 1));
   p.total = o;
   return GCPSL_OK;
 }
@@ -333,6 +376,16 @@ extern "C" int gcpsl_param_count(const gcpsl_desc *d, int64_t *P, int64_t *P_cli
   return GCPSL_OK;
 }
 
+extern "C" int gcpsl_state_count(const gcpsl_desc *d, int64_t *S) {
+  gcpsl_clear_error();
+  if (!S) return gcpsl_fail(GCPSL_EINVAL, "null output");
+  Plan p;
+  const int rc = build_plan(d, p);
+  if (rc) return rc;
+  *S = p.S;
+  return GCPSL_OK;
+}
+
 extern "C" int gcpsl_workspace_bytes(const gcpsl_desc *d, size_t *bytes) {
   gcpsl_clear_error();
   if (!bytes) return gcpsl_fail(GCPSL_EINVAL, "null output");
@@ -363,6 +416,7 @@ extern "C" int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out) {
     return gcpsl_fail(GCPSL_EINVAL, "workspace must be 256-byte aligned");
   if (reinterpret_cast<uintptr_t>(d->theta) % 16 || reinterpret_cast<uintptr_t>(d->momentum_buf) % 16)
     return gcpsl_fail(GCPSL_EINVAL, "theta and momentum must be 16-byte aligned");
+  if (p.S > 0 && !d->norm_state) return gcpsl_fail(GCPSL_EINVAL, "the model has batch norm layers: norm_state needed");
   if (d->workspace_bytes < p.total)
     return gcpsl_fail(GCPSL_EINVAL, "workspace too small: need " + std::to_string(p.total) + " bytes");
   if (!std::isfinite(d->lr) || !std::isfinite(d->momentum)) return gcpsl_fail(GCPSL_EINVAL, "lr and momentum must be finite");
@@ -503,6 +557,29 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
 
   // forward: client segment to the cut, server segment to the loss
   auto input_of = [&](int i) -> const void * { return i == 0 ? x_in : (const void *)(ws + p.ly[i - 1].act_off); };
+  auto norm_args = [&](int i) {
+    const LayerInfo &l = p.ly[i];
+    const LayerInfo &cv = p.ly[i - 1];
+    NormArgs na{};
+    na.z = ws + cv.act_off;
+    na.a = ws + l.act_off;
+    na.du = ws + l.gpre_off;
+    na.dz = ws + cv.gpre_off;
+    na.mean = ctx->at<float>(l.mean_off);
+    na.rstd = ctx->at<float>(l.rstd_off);
+    na.part = ctx->at<double>(p.off_npart);
+    na.sums = ctx->at<double>(l.sums_off);
+    na.theta = d.theta;
+    na.grad = grad;
+    na.state = d.norm_state;
+    na.P = p.P; na.g_off = l.w_off; na.b_off = l.b_off; na.S = p.S; na.st_off = l.st_off; na.z_rs = l.act_rs;
+    na.Bt = B; na.H = l.H; na.W = l.W; na.Ch = l.Co; na.groups = l.groups; na.nstat = l.nstat;
+    na.chunk_px = p.norm_chunk_px;
+    na.chunks = (int)(((int64_t)B * l.H * l.W + p.norm_chunk_px - 1) / p.norm_chunk_px);
+    na.C = C;
+    na.rmap = rmap;
+    return na;
+  };
   for (int i = 0; i < n; ++i) {
     const LayerInfo &l = p.ly[i];
     const int kind = l.spec.kind;
@@ -526,6 +603,7 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
       a.C = C;
       a.rmap = rmap;
       a.epi = EPI_FWD;
+      a.no_relu = l.no_relu ? 1 : 0;
       std::string lab;
       const double M = (double)B * l.H * l.W;
       const double fl = 2.0 * C * M * l.Co * 9.0 * l.Ci;
@@ -533,6 +611,9 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
       size_t t_ = tbegin(ctx, s);
       LAUNCH(launch_conv(p.dtype, a, s, &lab));
       tend(ctx, s, t_, lab, fl, by);
+    } else if (is_norm(kind)) {
+      const double by = (double)C * p.esz * B * l.H * l.W * l.Co * (l.groups ? 3.0 : 3.0);
+      LAUNCH_T(l.groups ? "groupnorm_fwd" : "batchnorm_fwd", 0.0, by, launch_norm_fwd(p.dtype, norm_args(i), s));
     } else if (kind == GCPSL_MAXPOOL2) {
       if (!l.stored) continue;  // fused into the head
       LAUNCH_T("maxpool_fwd", 0.0, 1.25 * p.esz * (double)C * B * l.H * l.W * l.Ci,
@@ -560,6 +641,13 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
   int i = p.head_conv;
   while (i >= 0) {
     const LayerInfo &l = p.ly[i];
+    if (is_norm(l.spec.kind)) {
+      // gamma, beta gradients and dL/dz of the conv below (which has no ReLU)
+      const double by = (double)C * p.esz * B * l.H * l.W * l.Co * 5.0;
+      LAUNCH_T(l.groups ? "groupnorm_bwd" : "batchnorm_bwd", 0.0, by, launch_norm_bwd(p.dtype, norm_args(i), s));
+      i -= 1;
+      continue;
+    }
     // weight and bias gradient
     WgradArgs w{};
     w.g = ws + l.gpre_off;
@@ -695,6 +783,10 @@ extern "C" int gcpsl_fuse(gcpsl_ctx *ctx, void *stream) {
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   LAUNCH_T("fuse", 2.0 * p.C * p.P, 8.0 * p.C * p.P,
            launch_fuse(ctx->desc.theta, ctx->at<double>(p.off_fw), W, p.C, p.P, s));
+  // the server normalisation state, with the same weights (Sec. IV-D)
+  if (p.S > 0)
+    LAUNCH_T("fuse", 2.0 * p.C * p.S, 8.0 * p.C * p.S,
+             launch_fuse(ctx->desc.norm_state, ctx->at<double>(p.off_fw), W, p.C, p.S, s));
   return GCPSL_OK;
 }
 
@@ -770,7 +862,7 @@ extern "C" int gcpsl_tensor(gcpsl_ctx *ctx, const char *name, void **ptr, int64_
     const LayerInfo &l = p.ly[i];
     const std::string k = std::to_string(i);
     if (nm == "act" + k && l.stored) return put(l.act_off, (int64_t)p.C * l.act_rs, p.dtype);
-    if (l.spec.kind == GCPSL_CONV3X3) {
+    if (l.spec.kind == GCPSL_CONV3X3 || is_norm(l.spec.kind)) {
       const int64_t rs = (int64_t)p.B * l.H * l.W;
       if (nm == "gpre" + k) return put(l.gpre_off, p.C * rs * l.Co, p.dtype);
       if (nm == "gin" + k && l.has_gin) return put(l.gin_off, p.C * rs * l.Ci, p.dtype);

@@ -296,7 +296,7 @@ conv_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT
           if constexpr (EPI == EPI_FWD) {
             v += bias;
             if (res) v += E::to_f(res[o]);
-            v = fmaxf(v, 0.f);
+            if (!a.no_relu) v = fmaxf(v, 0.f);
           } else {
             if (res) v += E::to_f(res[o]);
             if (msk && !(E::to_f(msk[o]) > 0.f)) v = 0.f;

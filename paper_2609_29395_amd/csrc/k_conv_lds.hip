@@ -378,7 +378,7 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
       }
       if constexpr (EPI == EPI_FWD) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = fmaxf(v[e] + bias[e], 0.f);
+        for (int e = 0; e < 8; ++e) v[e] = a.no_relu ? v[e] + bias[e] : fmaxf(v[e] + bias[e], 0.f);
       } else {
         // without a mask source every value passes (ones)
         const uint32_t mw[4] = {mv[i].x, mv[i].y, mv[i].z, mv[i].w};

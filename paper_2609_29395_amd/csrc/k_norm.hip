@@ -1,0 +1,324 @@
+// Normalisation layers of the split CNN (Sec. IV-B): GroupNorm in the client
+// segment, BatchNorm in the server segment, each followed by ReLU, over the
+// raw output z [Bt][H][W][Ch] (NHWC) of the conv before it:
+//
+//   x_hat = (z - mean) * rstd,  rstd = 1 / sqrt(var + 1e-5),  var biased,
+//   u = gamma_c x_hat + beta_c,  a = ReLU(u);
+//
+// batch norm takes mean and var per channel over (Bt, H, W), group norm per
+// example over (H, W, the channels of a group).  Backward, from du = dL/du:
+//
+//   dgamma_c = sum du x_hat,  dbeta_c = sum du        (over Bt, H, W)
+//   dz = rstd (du gamma_c - S1 / n - x_hat S2 / n),
+//   S1 = sum du gamma_c,  S2 = sum du gamma_c x_hat   (over the set of n values)
+//
+// Batch norm also updates its replica's running statistics (momentum 0.1,
+// unbiased variance for the running value) and batch counter.
+//
+// Every sum runs in fp64 in a fixed order (per-thread strides, then thread
+// order, then chunk order), so results do not depend on scheduling.  A
+// thread owns one 16-byte vector of VEC channels; a workgroup has 256 / (Ch /
+// VEC) pixel lanes.
+#include "runtime.h"
+
+namespace {
+
+constexpr double kEps = 1e-5;
+constexpr double kMomentum = 0.1;
+
+template <typename T> struct V16 {
+  T v[ElemT<T>::VEC];
+};
+template <typename T> __device__ __forceinline__ V16<T> load16(const T *p) {
+  return __builtin_bit_cast(V16<T>, *reinterpret_cast<const uint4 *>(p));
+}
+template <typename T> __device__ __forceinline__ void store16(T *p, const V16<T> &v) {
+  *reinterpret_cast<uint4 *>(p) = __builtin_bit_cast(uint4, v);
+}
+
+// statistics index of channel c of example b
+__device__ __forceinline__ int stat_index(const NormArgs &a, int b, int c) {
+  return a.groups ? b * a.groups + c / (a.Ch / a.groups) : c;
+}
+
+// Per-channel sums over one chunk of pixels: MODE 0 sum z and z^2 (batch
+// statistics), MODE 1 sum du and du x_hat (gradients of gamma and beta).
+// Partials part[rep][chunk][c][2].
+template <typename T, int MODE>
+__global__ void __launch_bounds__(256)
+chan_reduce_kernel(NormArgs a) {
+  constexpr int VEC = ElemT<T>::VEC;
+  __shared__ double red[256][2 * VEC];
+  const int rep = replica_of(a.rmap, blockIdx.y);
+  const int CV = a.Ch / VEC, PL = 256 / CV;
+  const int tid = threadIdx.x, cv = tid % CV, pl = tid / CV;
+  const int64_t M = (int64_t)a.Bt * a.H * a.W;
+  const int64_t p0 = (int64_t)blockIdx.x * a.chunk_px, p1 = min(M, p0 + a.chunk_px);
+  const T *z = reinterpret_cast<const T *>(a.z) + rep * a.z_rs;
+  const T *du = reinterpret_cast<const T *>(a.du) + rep * a.z_rs;
+  const float *mean = a.mean + (int64_t)rep * a.nstat, *rstd = a.rstd + (int64_t)rep * a.nstat;
+  double s0[VEC], s1[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) s0[e] = s1[e] = 0.0;
+  if (pl < PL) {
+    for (int64_t p = p0 + pl; p < p1; p += PL) {
+      const V16<T> zv = load16(z + p * a.Ch + cv * VEC);
+      if constexpr (MODE == 0) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const double v = ElemT<T>::to_f(zv.v[e]);
+          s0[e] += v;
+          s1[e] += v * v;
+        }
+      } else {
+        const V16<T> gv = load16(du + p * a.Ch + cv * VEC);
+        const int b = (int)(p / (a.H * a.W));
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const int si = stat_index(a, b, cv * VEC + e);
+          const float xh = (ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si];
+          const double g = ElemT<T>::to_f(gv.v[e]);
+          s0[e] += g;
+          s1[e] += g * (double)xh;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    red[tid][e] = s0[e];
+    red[tid][VEC + e] = s1[e];
+  }
+  __syncthreads();
+  if (tid < CV) {
+    double* out = a.part + (((int64_t)rep * a.chunks + blockIdx.x) * a.Ch + cv * VEC) * 2;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      double t0 = 0.0, t1 = 0.0;
+      for (int k = 0; k < PL; ++k) {
+        t0 += red[k * CV + cv][e];
+        t1 += red[k * CV + cv][VEC + e];
+      }
+      out[2 * e] = t0;
+      out[2 * e + 1] = t1;
+    }
+  }
+}
+
+// Chunk partials -> per-channel sums (chunk order).  MODE 0: batch-norm mean
+// and rstd, and the running statistics; MODE 1: dbeta, dgamma into grad and
+// (batch norm) the sums for the input gradient.
+template <int MODE>
+__global__ void __launch_bounds__(256)
+chan_finish_kernel(NormArgs a) {
+  const int rep = replica_of(a.rmap, blockIdx.y);
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= a.Ch) return;
+  double S0 = 0.0, S1 = 0.0;
+  for (int k = 0; k < a.chunks; ++k) {
+    const double *pp = a.part + (((int64_t)rep * a.chunks + k) * a.Ch + c) * 2;
+    S0 += pp[0];
+    S1 += pp[1];
+  }
+  const double n = (double)a.Bt * a.H * a.W;
+  if constexpr (MODE == 0) {
+    const double mean = S0 / n;
+    const double var = fmax(S1 / n - mean * mean, 0.0);
+    a.mean[(int64_t)rep * a.nstat + c] = (float)mean;
+    a.rstd[(int64_t)rep * a.nstat + c] = (float)(1.0 / sqrt(var + kEps));
+    float *st = a.state + rep * a.S + a.st_off;
+    st[c] = (float)((1.0 - kMomentum) * (double)st[c] + kMomentum * mean);
+    st[a.Ch + c] = (float)((1.0 - kMomentum) * (double)st[a.Ch + c] + kMomentum * var * n / (n - 1.0));
+    if (c == 0) st[2 * a.Ch] = (float)((double)st[2 * a.Ch] + 1.0);
+  } else {
+    a.grad[rep * a.P + a.b_off + c] = (float)S0;
+    a.grad[rep * a.P + a.g_off + c] = (float)S1;
+    if (!a.groups) {
+      a.sums[((int64_t)rep * a.nstat + c) * 2] = S0;
+      a.sums[((int64_t)rep * a.nstat + c) * 2 + 1] = S1;
+    }
+  }
+}
+
+// Group norm, one workgroup per example: MODE 0 mean and rstd per group;
+// MODE 1 the sums S1 = sum du gamma, S2 = sum du gamma x_hat per group.
+template <typename T, int MODE>
+__global__ void __launch_bounds__(256)
+group_reduce_kernel(NormArgs a) {
+  constexpr int VEC = ElemT<T>::VEC;
+  __shared__ double red[256][2 * VEC];
+  __shared__ double chs[2048][2];  // per-channel sums (Ch <= 2048)
+  const int rep = replica_of(a.rmap, blockIdx.y);
+  const int b = blockIdx.x;
+  const int CV = a.Ch / VEC, PL = 256 / CV;
+  const int tid = threadIdx.x, cv = tid % CV, pl = tid / CV;
+  const int HW = a.H * a.W, G = a.groups, CG = a.Ch / G;
+  const int64_t base = rep * a.z_rs + (int64_t)b * HW * a.Ch;
+  const T *z = reinterpret_cast<const T *>(a.z) + base;
+  const T *du = reinterpret_cast<const T *>(a.du) + base;
+  const float *mean = a.mean + (int64_t)rep * a.nstat, *rstd = a.rstd + (int64_t)rep * a.nstat;
+  const float *gamma = a.theta + rep * a.P + a.g_off;
+  double s0[VEC], s1[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) s0[e] = s1[e] = 0.0;
+  if (pl < PL) {
+    for (int p = pl; p < HW; p += PL) {
+      const V16<T> zv = load16(z + (int64_t)p * a.Ch + cv * VEC);
+      if constexpr (MODE == 0) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const double v = ElemT<T>::to_f(zv.v[e]);
+          s0[e] += v;
+          s1[e] += v * v;
+        }
+      } else {
+        const V16<T> gv = load16(du + (int64_t)p * a.Ch + cv * VEC);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const int c = cv * VEC + e, si = b * G + c / CG;
+          const float xh = (ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si];
+          const double dx = (double)ElemT<T>::to_f(gv.v[e]) * gamma[c];
+          s0[e] += dx;
+          s1[e] += dx * (double)xh;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    red[tid][e] = s0[e];
+    red[tid][VEC + e] = s1[e];
+  }
+  __syncthreads();
+  if (tid < CV) {
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      double t0 = 0.0, t1 = 0.0;
+      for (int k = 0; k < PL; ++k) {
+        t0 += red[k * CV + cv][e];
+        t1 += red[k * CV + cv][VEC + e];
+      }
+      chs[cv * VEC + e][0] = t0;
+      chs[cv * VEC + e][1] = t1;
+    }
+  }
+  __syncthreads();
+  for (int g = tid; g < G; g += blockDim.x) {
+    double S0 = 0.0, S1 = 0.0;
+    for (int c = g * CG; c < (g + 1) * CG; ++c) {
+      S0 += chs[c][0];
+      S1 += chs[c][1];
+    }
+    const int64_t si = (int64_t)rep * a.nstat + b * G + g;
+    if constexpr (MODE == 0) {
+      const double n = (double)HW * CG;
+      const double m = S0 / n;
+      const double var = fmax(S1 / n - m * m, 0.0);
+      a.mean[si] = (float)m;
+      a.rstd[si] = (float)(1.0 / sqrt(var + kEps));
+    } else {
+      a.sums[si * 2] = S0;
+      a.sums[si * 2 + 1] = S1;
+    }
+  }
+}
+
+// a = ReLU(gamma (z - mean) rstd + beta), one 16-byte vector per thread.
+template <typename T>
+__global__ void __launch_bounds__(256)
+norm_apply_fwd_kernel(NormArgs a, uint32_t total) {
+  constexpr int VEC = ElemT<T>::VEC;
+  const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+  if (i >= total) return;
+  const int rep = replica_of(a.rmap, blockIdx.y);
+  const int CV = a.Ch / VEC;
+  const uint32_t p = i / CV;
+  const int c0 = (int)(i - p * CV) * VEC, b = (int)(p / (a.H * a.W));
+  const T *z = reinterpret_cast<const T *>(a.z) + rep * a.z_rs;
+  T *out = reinterpret_cast<T *>(a.a) + rep * a.z_rs;
+  const float *mean = a.mean + (int64_t)rep * a.nstat, *rstd = a.rstd + (int64_t)rep * a.nstat;
+  const float *gamma = a.theta + rep * a.P + a.g_off, *beta = a.theta + rep * a.P + a.b_off;
+  const V16<T> zv = load16(z + (int64_t)i * VEC);
+  V16<T> o;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    const int c = c0 + e, si = stat_index(a, b, c);
+    const float u = gamma[c] * ((ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si]) + beta[c];
+    o.v[e] = ElemT<T>::from_f(fmaxf(u, 0.f));
+  }
+  store16(out + (int64_t)i * VEC, o);
+}
+
+// dz = rstd (du gamma - S1 / n - x_hat S2 / n), one 16-byte vector per thread;
+// batch norm's S1, S2 are gamma times the per-channel sums.
+template <typename T>
+__global__ void __launch_bounds__(256)
+norm_apply_bwd_kernel(NormArgs a, uint32_t total) {
+  constexpr int VEC = ElemT<T>::VEC;
+  const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+  if (i >= total) return;
+  const int rep = replica_of(a.rmap, blockIdx.y);
+  const int CV = a.Ch / VEC;
+  const uint32_t p = i / CV;
+  const int c0 = (int)(i - p * CV) * VEC, b = (int)(p / (a.H * a.W));
+  const T *z = reinterpret_cast<const T *>(a.z) + rep * a.z_rs;
+  const T *du = reinterpret_cast<const T *>(a.du) + rep * a.z_rs;
+  T *dz = reinterpret_cast<T *>(a.dz) + rep * a.z_rs;
+  const float *mean = a.mean + (int64_t)rep * a.nstat, *rstd = a.rstd + (int64_t)rep * a.nstat;
+  const float *gamma = a.theta + rep * a.P + a.g_off;
+  const double *sums = a.sums + (int64_t)rep * a.nstat * 2;
+  const double n = a.groups ? (double)a.H * a.W * (a.Ch / a.groups) : (double)a.Bt * a.H * a.W;
+  const V16<T> zv = load16(z + (int64_t)i * VEC), gv = load16(du + (int64_t)i * VEC);
+  V16<T> o;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    const int c = c0 + e, si = stat_index(a, b, c);
+    const float xh = (ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si];
+    const float s1 = (float)(sums[2 * si] / n), s2 = (float)(sums[2 * si + 1] / n);
+    const float g = gamma[c];
+    const float v = a.groups ? rstd[si] * (ElemT<T>::to_f(gv.v[e]) * g - s1 - xh * s2)
+                             : rstd[si] * g * (ElemT<T>::to_f(gv.v[e]) - s1 - xh * s2);
+    o.v[e] = ElemT<T>::from_f(v);
+  }
+  store16(dz + (int64_t)i * VEC, o);
+}
+
+template <typename T>
+hipError_t norm_fwd_t(const NormArgs &a, hipStream_t s) {
+  constexpr int VEC = ElemT<T>::VEC;
+  const uint32_t total = (uint32_t)((int64_t)a.Bt * a.H * a.W * (a.Ch / VEC));
+  if (a.groups) {
+    hipLaunchKernelGGL((group_reduce_kernel<T, 0>), dim3(a.Bt, a.C), dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((chan_reduce_kernel<T, 0>), dim3(a.chunks, a.C), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((chan_finish_kernel<0>), dim3((a.Ch + 255) / 256, a.C), dim3(256), 0, s, a);
+  }
+  hipLaunchKernelGGL((norm_apply_fwd_kernel<T>), dim3((total + 255) / 256, a.C), dim3(256), 0, s, a, total);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t norm_bwd_t(const NormArgs &a, hipStream_t s) {
+  constexpr int VEC = ElemT<T>::VEC;
+  const uint32_t total = (uint32_t)((int64_t)a.Bt * a.H * a.W * (a.Ch / VEC));
+  hipLaunchKernelGGL((chan_reduce_kernel<T, 1>), dim3(a.chunks, a.C), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((chan_finish_kernel<1>), dim3((a.Ch + 255) / 256, a.C), dim3(256), 0, s, a);
+  if (a.groups) hipLaunchKernelGGL((group_reduce_kernel<T, 1>), dim3(a.Bt, a.C), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((norm_apply_bwd_kernel<T>), dim3((total + 255) / 256, a.C), dim3(256), 0, s, a, total);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool norm_ok(int dtype, int Ch, int groups) {
+  const int vec = dtype == GCPSL_BF16 ? 8 : 4;
+  return Ch % vec == 0 && Ch / vec <= 256 && Ch <= 2048 && (groups == 0 || Ch % groups == 0);
+}
+
+hipError_t launch_norm_fwd(int dtype, const NormArgs &a, hipStream_t s) {
+  return dtype == GCPSL_BF16 ? norm_fwd_t<bf16_t>(a, s) : norm_fwd_t<float>(a, s);
+}
+
+hipError_t launch_norm_bwd(int dtype, const NormArgs &a, hipStream_t s) {
+  return dtype == GCPSL_BF16 ? norm_bwd_t<bf16_t>(a, s) : norm_bwd_t<float>(a, s);
+}

@@ -34,6 +34,7 @@ struct ConvArgs {
   int epi;
   int taps;  // 9: 3x3 implicit GEMM; 1: src already holds im2col rows, A[m][k] = src[m][k]
   int res_lds;  // set by the launcher: the residual (== src) is taken from the staged centre tap
+  int no_relu;  // fwd: store the raw output (a norm layer follows)
 };
 
 // Weight gradient: dW[co][kk] = sum_p G[p][co] X(p, kk), kk = (r, s, ci),
@@ -122,3 +123,26 @@ hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t P, in
                       float lr, float mu, hipStream_t s);
 hipError_t launch_fuse(float *theta, const double *weights, double W, int C, int64_t P,
                        hipStream_t s);
+
+// Normalisation layers (k_norm.hip): batch norm (groups == 0) or group norm
+// over a conv's raw output z, followed by ReLU.
+struct NormArgs {
+  const void *z;  // [C][Bt*H*W][Ch] raw conv output, replica stride z_rs
+  void *a;        // forward output a = ReLU(gamma x_hat + beta), stride z_rs
+  const void *du; // backward: dL/du (ReLU-masked), stride z_rs
+  void *dz;       // backward: dL/dz, stride z_rs
+  float *mean, *rstd;  // [C][nstat] statistics (per channel, or per example and group)
+  double *part;        // [C][chunks][Ch][2] per-chunk channel sums
+  double *sums;        // [C][nstat][2] sums for the input gradient
+  const float *theta;  // [C][P] parameters (gamma at g_off, beta at b_off)
+  float *grad;         // [C][P] gradient (dgamma, dbeta written)
+  float *state;        // [C][S] normalisation state (batch norm: running mean, var, counter at st_off)
+  int64_t P, g_off, b_off, S, st_off, z_rs;
+  int Bt, H, W, Ch, groups, nstat;
+  int chunks, chunk_px;  // pixel chunks of the channel reductions
+  int C;                 // replica slots
+  const int32_t *rmap;   // device [C]: replica of each slot, or null
+};
+bool norm_ok(int dtype, int Ch, int groups);
+hipError_t launch_norm_fwd(int dtype, const NormArgs &a, hipStream_t s);
+hipError_t launch_norm_bwd(int dtype, const NormArgs &a, hipStream_t s);

@@ -10,7 +10,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from gcpsl_inputs import client_stats, init_params, make_dataset
+from gcpsl_inputs import client_stats, init_norm_state, init_params, make_dataset
 
 from . import gcpsl
 
@@ -23,7 +23,8 @@ def setup(cfg, max_steps=None, max_window=1, device="cuda", schedule=None):
     counts, hist = client_stats(cfg, labels, coe)
     assignment = gcpsl.assign(cfg["rule"], cfg["K"], cfg["C"], cfg["seed"], counts, hist)
     ctx = gcpsl.Context(cfg, images, labels, coe, assignment, init_params(cfg),
-                        max_steps=max_steps, max_window=max_window, device=device, schedule=schedule)
+                        max_steps=max_steps, max_window=max_window, device=device, schedule=schedule,
+                        norm_state0=init_norm_state(cfg))
     return ctx, assignment
 
 

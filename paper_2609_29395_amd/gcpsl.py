@@ -18,11 +18,11 @@ LIB_PATH = os.path.join(_HERE, "libgcpsl.so")
 OK, EINVAL, ESTATE, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4
 RULES = {"random": 0, "size": 1, "label_l1": 2, "label_jsd": 3}
 DTYPES = {"f32": 0, "bf16": 1}
-CONV3X3, MAXPOOL2, AVGPOOL, LINEAR = 1, 2, 3, 4
+CONV3X3, MAXPOOL2, AVGPOOL, LINEAR, BATCHNORM, GROUPNORM = 1, 2, 3, 4, 5, 6
 RESIDUAL = 1
 SCHEDULES = {"lockstep": 0, "epoch": 1}
 
-EXPORTS = ["gcpsl_param_count", "gcpsl_workspace_bytes", "gcpsl_assign", "gcpsl_create",
+EXPORTS = ["gcpsl_param_count", "gcpsl_state_count", "gcpsl_workspace_bytes", "gcpsl_assign", "gcpsl_create",
            "gcpsl_sample", "gcpsl_step", "gcpsl_step_replica", "gcpsl_epoch_rounds", "gcpsl_fuse",
            "gcpsl_participation",
            "gcpsl_cluster_sizes", "gcpsl_tensor", "gcpsl_timing", "gcpsl_timing_read",
@@ -36,7 +36,8 @@ class GCPSLError(RuntimeError):
 
 
 class Layer(C.Structure):
-    _fields_ = [("kind", C.c_int32), ("cin", C.c_int32), ("cout", C.c_int32), ("flags", C.c_int32)]
+    _fields_ = [("kind", C.c_int32), ("cin", C.c_int32), ("cout", C.c_int32), ("flags", C.c_int32),
+                ("groups", C.c_int32)]
 
 
 class Desc(C.Structure):
@@ -48,7 +49,7 @@ class Desc(C.Structure):
         ("seed", C.c_uint64), ("max_steps", C.c_int64), ("max_window", C.c_int32),
         ("schedule", C.c_int32), ("client_of_example", C.POINTER(C.c_int32)),
         ("cluster_of_client", C.POINTER(C.c_int32)), ("images", C.c_void_p),
-        ("labels", C.c_void_p), ("theta", C.c_void_p), ("momentum_buf", C.c_void_p),
+        ("labels", C.c_void_p), ("theta", C.c_void_p), ("momentum_buf", C.c_void_p), ("norm_state", C.c_void_p),
         ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t),
     ]
 
@@ -72,6 +73,7 @@ def lib():
     vp, i32, i64, u64 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64
     P = C.POINTER
     L.gcpsl_param_count.argtypes = [P(Desc), P(i64), P(i64)]
+    L.gcpsl_state_count.argtypes = [P(Desc), P(i64)]
     L.gcpsl_workspace_bytes.argtypes = [P(Desc), P(C.c_size_t)]
     L.gcpsl_assign.argtypes = [i32, i32, i32, u64, P(i64), P(i64), i32, P(i32)]
     L.gcpsl_create.argtypes = [P(Desc), P(vp)]
@@ -113,13 +115,17 @@ def layers_struct(layers):
     for i, spec in enumerate(layers):
         kind = spec[0]
         if kind == "conv":
-            arr[i] = Layer(CONV3X3, spec[1], spec[2], RESIDUAL if spec[3] else 0)
+            arr[i] = Layer(CONV3X3, spec[1], spec[2], RESIDUAL if spec[3] else 0, 0)
         elif kind == "maxpool":
-            arr[i] = Layer(MAXPOOL2, 0, 0, 0)
+            arr[i] = Layer(MAXPOOL2, 0, 0, 0, 0)
         elif kind == "avgpool":
-            arr[i] = Layer(AVGPOOL, 0, 0, 0)
+            arr[i] = Layer(AVGPOOL, 0, 0, 0, 0)
         elif kind == "linear":
-            arr[i] = Layer(LINEAR, spec[1], spec[2], 0)
+            arr[i] = Layer(LINEAR, spec[1], spec[2], 0, 0)
+        elif kind == "bnorm":
+            arr[i] = Layer(BATCHNORM, spec[1], spec[1], 0, 0)
+        elif kind == "gnorm":
+            arr[i] = Layer(GROUPNORM, spec[1], spec[1], 0, spec[2])
         else:
             raise ValueError(kind)
     return arr
@@ -166,6 +172,12 @@ def param_count(desc):
     return P.value, Pc.value
 
 
+def state_count(desc):
+    S = C.c_int64()
+    _check(lib().gcpsl_state_count(C.byref(desc), C.byref(S)))
+    return S.value
+
+
 def workspace_bytes(desc):
     n = C.c_size_t()
     _check(lib().gcpsl_workspace_bytes(C.byref(desc), C.byref(n)))
@@ -182,7 +194,7 @@ class Context:
     """One gcpsl_ctx with the caller-owned device buffers it works in."""
 
     def __init__(self, cfg, images, labels, client_of_example, cluster_of_client, theta0,
-                 max_steps=None, max_window=1, device="cuda", schedule="lockstep"):
+                 max_steps=None, max_window=1, device="cuda", schedule="lockstep", norm_state0=None):
         import torch
         self.cfg = cfg
         self.schedule = schedule
@@ -195,6 +207,12 @@ class Context:
         self.labels = torch.from_numpy(np.array(labels, dtype=np.int32)).to(device)
         self.theta = t0.to(device).reshape(1, -1).repeat(cfg["C"], 1).contiguous()
         self.mom = torch.zeros_like(self.theta)
+        self.S = state_count(desc)
+        ns0 = np.zeros(self.S, dtype=np.float32) if norm_state0 is None else np.asarray(norm_state0, np.float32)
+        if ns0.size != self.S:
+            raise ValueError(f"norm_state0 has {ns0.size} entries, the model has {self.S}")
+        self.norm_state = (torch.as_tensor(ns0).to(device).reshape(1, -1).repeat(cfg["C"], 1).contiguous()
+                           if self.S else None)
         nbytes = workspace_bytes(desc)
         self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
         base = self.workspace.data_ptr()
@@ -203,6 +221,7 @@ class Context:
         desc.labels = self.labels.data_ptr()
         desc.theta = self.theta.data_ptr()
         desc.momentum_buf = self.mom.data_ptr()
+        desc.norm_state = self.norm_state.data_ptr() if self.S else None
         desc.workspace = base + self._ws_off
         desc.workspace_bytes = nbytes
         self.desc = desc

@@ -90,15 +90,43 @@ def test_assign_errors():
     assert e.value.code == g.EINVAL
 
 
-@pytest.mark.parametrize("name", ["tiny", "gpsl", "gcpsl16", "ragged"])
+@pytest.mark.parametrize("name", ["tiny", "gpsl", "gcpsl16", "ragged", "tiny_norm", "ragged_norm_bf16"])
 def test_param_count_matches_layout(name):
+    from gcpsl_inputs import norm_layout
     cfg = get_config(name)
     _, labels, coe = make_dataset(cfg)
     d, keep = g.make_desc(cfg, coe, np.zeros(cfg["K"], np.int32))
     P, Pc = g.param_count(d)
     pc, ps = param_counts(cfg)
     assert (P, Pc) == (pc + ps, pc)
+    nl = norm_layout(cfg)
+    assert g.state_count(d) == (nl[-1][3] + nl[-1][2][0] if nl else 0)
     assert g.workspace_bytes(d) > 0
+
+
+def test_norm_layer_shapes_are_checked():
+    base = get_config("tiny_norm")
+    _, labels, coe = make_dataset(base)
+    bad = [
+        # group norm groups must divide the channels
+        [("conv", 3, 8, False), ("gnorm", 8, 3), ("maxpool",), ("conv", 8, 16, False), ("bnorm", 16),
+         ("avgpool",), ("linear", 16, 4)],
+        # a norm layer needs a conv before it
+        [("conv", 3, 8, False), ("maxpool",), ("bnorm", 8), ("conv", 8, 16, False), ("avgpool",),
+         ("linear", 16, 4)],
+        # a residual conv cannot feed a norm layer
+        [("conv", 3, 8, False), ("maxpool",), ("conv", 8, 8, True), ("bnorm", 8), ("avgpool",),
+         ("linear", 8, 4)],
+        # norm channels must match the conv
+        [("conv", 3, 8, False), ("gnorm", 16, 2), ("maxpool",), ("conv", 8, 16, False), ("avgpool",),
+         ("linear", 16, 4)],
+    ]
+    for layers in bad:
+        cfg = get_config("tiny_norm", layers=layers)
+        d, keep = g.make_desc(cfg, coe, np.zeros(cfg["K"], np.int32))
+        with pytest.raises(g.GCPSLError) as e:
+            g.param_count(d)
+        assert e.value.code in (g.EINVAL, g.EUNSUPPORTED), layers
 
 
 def test_survey_parameter_counts():

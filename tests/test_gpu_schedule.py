@@ -71,7 +71,7 @@ def _run(cfg, T, serial):
     return ctx, losses.cpu().numpy()
 
 
-@pytest.mark.parametrize("name", ["tiny_epoch", "ragged_bf16_epoch", "ragged", "ragged_bf16"])
+@pytest.mark.parametrize("name", ["tiny_epoch", "ragged_bf16_epoch", "ragged", "ragged_bf16", "tiny_norm"])
 def test_sequential_equals_concurrent_bit_for_bit(name):
     # Eq. 6 compares running the cluster workloads one after another with
     # running them side by side: the same rounds, so the same results
@@ -82,6 +82,8 @@ def test_sequential_equals_concurrent_bit_for_bit(name):
     b, lb = _run(cfg, T, serial=True)
     assert np.array_equal(la, lb, equal_nan=True)
     assert torch.equal(a.theta, b.theta) and torch.equal(a.mom, b.mom)
+    if a.S:
+        assert torch.equal(a.norm_state, b.norm_state)
     assert np.array_equal(a.participation()[2], b.participation()[2])
 
 
