@@ -129,6 +129,24 @@ CONFIGS = {
                 ("conv", 24, 136, False), ("bnorm", 136),
                 ("conv", 136, 136, False), ("bnorm", 136), ("avgpool",), ("linear", 136, 7)],
         cut=4, dtype="bf16", lr=0.05, momentum=0.9, F=3, T=7, seed=0),
+    # The paper's training recipe (Sec. V-A) on the norm models: SGD with
+    # momentum 0.9, the Nesterov term and weight decay 5e-4, cross-entropy
+    # with label smoothing 0.1.
+    "tiny_recipe": dict(
+        K=16, C=2, B=8, L=4, N_ex=512, H=8, W=8, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="random",
+        layers=[("conv", 3, 8, False), ("gnorm", 8, 2), ("maxpool",),
+                ("conv", 8, 16, False), ("bnorm", 16), ("avgpool",), ("linear", 16, 4)],
+        cut=3, dtype="f32", lr=0.05, momentum=0.9, F=5, T=10, seed=0,
+        nesterov=True, weight_decay=5e-4, label_smoothing=0.1),
+    "ragged_recipe_bf16": dict(
+        K=24, C=3, B=20, L=7, N_ex=1400, H=12, W=12, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="size",
+        layers=[("conv", 3, 8, False), ("gnorm", 8, 4), ("conv", 8, 24, False), ("gnorm", 24, 3),
+                ("conv", 24, 136, False), ("bnorm", 136),
+                ("conv", 136, 136, False), ("bnorm", 136), ("avgpool",), ("linear", 136, 7)],
+        cut=4, dtype="bf16", lr=0.05, momentum=0.9, F=3, T=7, seed=0,
+        nesterov=True, weight_decay=5e-4, label_smoothing=0.1),
     # Epoch-barrier schedule (fusion after every system epoch) on unequal
     # clusters: tiny with B=32 (6 and 9 rounds per epoch), and the ragged
     # shapes under label-L1 clustering with B=100 (7, 4 and 2 rounds).
@@ -160,6 +178,9 @@ def get_config(name: str, **overrides) -> dict:
     cfg = copy.deepcopy(CONFIGS[name])
     cfg.update(overrides)
     cfg.setdefault("schedule", "lockstep")
+    cfg.setdefault("nesterov", False)
+    cfg.setdefault("weight_decay", 0.0)
+    cfg.setdefault("label_smoothing", 0.0)
     cfg["name"] = name
     return cfg
 

@@ -109,6 +109,12 @@ typedef struct gcpsl_desc {
   const gcpsl_layer *layers; /* host, copied at create                      */
   float lr;           /* SGD learning rate                                  */
   float momentum;     /* SGD momentum mu: v <- mu v + g, theta -= lr v      */
+  float weight_decay; /* L2 term wd >= 0 (Sec. V-A): the update uses
+                         g + wd theta in place of the gradient g           */
+  int32_t nesterov;   /* 1: Nesterov term (Sec. V-A), theta -= lr (g + mu v)
+                         with the new v; 0: theta -= lr v                   */
+  float label_smoothing; /* eps in [0, 1) (Sec. V-A): the cross-entropy
+                         target is (1 - eps) onehot(y) + eps / L            */
   uint64_t seed;      /* sampler seed                                       */
   int64_t max_steps;  /* rows of the participation table (steps recorded)   */
   int32_t max_window; /* largest nsteps accepted by gcpsl_sample, >= 1      */

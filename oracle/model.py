@@ -179,15 +179,21 @@ def bn_running_update(mean_run, var_run, count, mean, var_biased, n):
     return ((1.0 - m) * mean_run + m * mean, (1.0 - m) * var_run + m * var_biased * n / (n - 1), count + 1.0)
 
 
-def softmax_xent(logits, y):
-    """Mean softmax cross-entropy and its gradient with respect to the logits."""
-    Bt = logits.shape[0]
+def softmax_xent(logits, y, eps=0.0):
+    """Mean softmax cross-entropy and its gradient with respect to the logits.
+
+    With label smoothing eps (Sec. V-A) the target of an example with label
+    y is q = (1 - eps) onehot(y) + eps / L; the loss is -sum_j q_j log p_j
+    and its gradient p - q (eps = 0: plain cross-entropy)."""
+    Bt, L = logits.shape
     z = logits - logits.max(axis=1, keepdims=True)
     lse = np.log(np.exp(z).sum(axis=1))
     rows = np.arange(Bt)
-    loss = float(np.mean(lse - z[rows, y]))
-    d = np.exp(z - lse[:, None])
-    d[rows, y] -= 1.0
+    q = np.full((Bt, L), eps / L)
+    q[rows, y] += 1.0 - eps
+    logp = z - lse[:, None]
+    loss = float(np.mean(-(q * logp).sum(axis=1)))
+    d = np.exp(logp) - q
     return loss, d / Bt
 
 
@@ -249,7 +255,7 @@ def split_forward_backward(cfg, theta, x, y, keep=False):
         else:
             raise ValueError(kind)
         acts.append(out)
-    loss, g = softmax_xent(acts[-1], y)
+    loss, g = softmax_xent(acts[-1], y, cfg.get("label_smoothing", 0.0))
     if keep:
         rec["acts"] = acts
         rec["dlogits"] = g

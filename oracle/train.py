@@ -10,8 +10,11 @@ Readings:
   * Parameters and momentum are held as fp32 values (the workloads keep fp32
     master weights); each update is computed in fp64 and rounded once to
     fp32 when stored.
-  * SGD with momentum, PyTorch convention: v <- mu v + g, theta <- theta -
-    lr v, v starts at 0; no Nesterov term, no weight decay.
+  * SGD with momentum, PyTorch convention, v starts at 0: with weight decay
+    wd the step gradient is g + wd theta (L2 term, Sec. V-A); v <- mu v + g;
+    theta <- theta - lr v, or with the Nesterov term (Sec. V-A)
+    theta <- theta - lr (g + mu v).  wd = 0 and no Nesterov term unless the
+    workload asks for them.
   * Fusion happens after every F-th round (1-based: after rounds F, 2F, ...);
     all clusters advance in lockstep.  F = 0 disables fusion.
   * Fused value: (sum_n n_n theta_n) / W accumulated in fp64 in cluster
@@ -59,11 +62,21 @@ def ideal_schedule_speedup(rounds):
     return S, S / len(rounds)
 
 
-def sgd_update(theta, mom, grad, lr, mu):
-    """In place on fp32 state: v <- mu v + g; theta <- theta - lr v."""
-    v = mu * mom.astype(np.float64) + grad
+def sgd_update(theta, mom, grad, lr, mu, wd=0.0, nesterov=False):
+    """In place on fp32 state: g <- g + wd theta; v <- mu v + g;
+    theta <- theta - lr v (or theta - lr (g + mu v) with the Nesterov term).
+    Computed in fp64; the momentum is rounded to fp32 when stored, and the
+    stored value is the one the parameter step uses."""
+    g = np.asarray(grad, dtype=np.float64) + wd * theta.astype(np.float64)
+    v = mu * mom.astype(np.float64) + g
     mom[...] = v.astype(np.float32)
-    theta[...] = (theta.astype(np.float64) - lr * mom.astype(np.float64)).astype(np.float32)
+    step = g + mu * mom.astype(np.float64) if nesterov else mom.astype(np.float64)
+    theta[...] = (theta.astype(np.float64) - lr * step).astype(np.float32)
+
+
+def sgd_args(cfg):
+    """The workload's SGD settings as sgd_update arguments after theta, mom, grad."""
+    return (cfg["lr"], cfg["momentum"], cfg.get("weight_decay", 0.0), bool(cfg.get("nesterov", False)))
 
 
 def fuse(thetas, weights):
@@ -126,7 +139,7 @@ class GCPSLOracle:
             idx, x, y = self.batch(step, n)
             active[n] = active_clients(idx, self.coe)
             loss, g, rec = split_forward_backward(cfg, self.theta[n], x, y)
-            sgd_update(self.theta[n], self.mom[n], g, cfg["lr"], cfg["momentum"])
+            sgd_update(self.theta[n], self.mom[n], g, *sgd_args(cfg))
             self._update_norm_state(n, rec["bn_batch"])
             losses[n], grads[n] = loss, g
         if replicas is None:
@@ -155,7 +168,7 @@ class GCPSLOracle:
                 idx, x, y = self.batch(m * rounds[n] + t, n)
                 active.append(active_clients(idx, self.coe))
                 loss, g, rec = split_forward_backward(cfg, self.theta[n], x, y)
-                sgd_update(self.theta[n], self.mom[n], g, cfg["lr"], cfg["momentum"])
+                sgd_update(self.theta[n], self.mom[n], g, *sgd_args(cfg))
                 self._update_norm_state(n, rec["bn_batch"])
                 losses[n] = loss
             else:

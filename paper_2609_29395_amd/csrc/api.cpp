@@ -420,6 +420,11 @@ extern "C" int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out) {
   if (d->workspace_bytes < p.total)
     return gcpsl_fail(GCPSL_EINVAL, "workspace too small: need " + std::to_string(p.total) + " bytes");
   if (!std::isfinite(d->lr) || !std::isfinite(d->momentum)) return gcpsl_fail(GCPSL_EINVAL, "lr and momentum must be finite");
+  if (!(d->weight_decay >= 0.f) || !std::isfinite(d->weight_decay))
+    return gcpsl_fail(GCPSL_EINVAL, "weight_decay must be finite and >= 0");
+  if (d->nesterov != 0 && d->nesterov != 1) return gcpsl_fail(GCPSL_EINVAL, "nesterov must be 0 or 1");
+  if (!(d->label_smoothing >= 0.f && d->label_smoothing < 1.f))
+    return gcpsl_fail(GCPSL_EINVAL, "label_smoothing must lie in [0, 1)");
   for (int32_t k = 0; k < d->K; ++k)
     if (d->cluster_of_client[k] < 0 || d->cluster_of_client[k] >= d->C)
       return gcpsl_fail(GCPSL_EINVAL, "cluster_of_client out of range");
@@ -627,7 +632,7 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
       LAUNCH_T("linear_ce", 6.0 * C * B * l.Ci * l.Co,
                (double)C * (p.esz * B * l.Ci + 4.0 * (2.0 * l.nw + B * l.Ci + B)),
                launch_linear_ce(p.dtype, ws + p.ly[p.avg_idx].act_off, y, d.theta, p.P, l.w_off, l.b_off, grad,
-                                ctx->at<float>(p.off_dh), loss, C, rmap, B, l.Ci, l.Co, s));
+                                ctx->at<float>(p.off_dh), loss, C, rmap, B, l.Ci, l.Co, d.label_smoothing, s));
     }
   }
 
@@ -725,7 +730,8 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
   }
 
   LAUNCH_T("sgd", 3.0 * C * p.P, 20.0 * C * p.P,
-           launch_sgd(d.theta, d.momentum_buf, grad, p.P, C, rmap, d.lr, d.momentum, s));
+           launch_sgd(d.theta, d.momentum_buf, grad, p.P, C, rmap, d.lr, d.momentum, d.weight_decay,
+                      d.nesterov, s));
   ctx->horizon = std::max<int64_t>(ctx->horizon, std::min<int64_t>(step + 1, p.max_steps));
   return GCPSL_OK;
 }

@@ -436,8 +436,9 @@ head_pool_kernel(const T *__restrict__ a, T *__restrict__ h, const int32_t *__re
 }
 
 // Linear layer and mean softmax cross-entropy for one replica per workgroup:
-// logits = h W^T + b, loss = mean_b (logsumexp - logit_y),
-// dlogits = (softmax - onehot) / B, dW = dlogits^T h, db = sum_b dlogits,
+// logits = h W^T + b; with label smoothing eps (Sec. V-A) the target is
+// q = (1 - eps) onehot(y) + eps / L, loss = mean_b -sum_j q_j log softmax_j,
+// dlogits = (softmax - q) / B, dW = dlogits^T h, db = sum_b dlogits,
 // dh = dlogits W.  bf16 workloads use the bf16-rounded weight matrix.  The
 // pooled features, the weights and the logits are staged in LDS so every
 // global access is coalesced; each sum runs in a fixed order.
@@ -446,7 +447,7 @@ __global__ void __launch_bounds__(1024)
 linear_ce_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
                  const float *__restrict__ theta, int64_t P, int64_t w_off, int64_t b_off,
                  float *__restrict__ grad, float *__restrict__ dh, float *__restrict__ loss,
-                 const int32_t *__restrict__ rmap, int Bt, int Ch, int L) {
+                 const int32_t *__restrict__ rmap, int Bt, int Ch, int L, float eps) {
   extern __shared__ float sh[];
   // rows padded to Ch + 1 floats: threads of a wave that read the same
   // column of different rows hit different banks
@@ -477,10 +478,14 @@ linear_ce_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
     for (int j = 0; j < L; ++j) s += expf(lg[b * L + j] - m);
     const float lse = logf(s);
     const int yb = y[(int64_t)rep * Bt + b];
-    lossb[b] = lse - (lg[b * L + yb] - m);
+    // target q = (1 - eps) onehot(y) + eps / L; loss -sum_j q_j log p_j
+    const float qo = eps / (float)L, qy = 1.f - eps + qo;
+    float zs = 0.f;
+    for (int j = 0; j < L; ++j) zs += lg[b * L + j] - m;
+    lossb[b] = eps > 0.f ? lse - (1.f - eps) * (lg[b * L + yb] - m) - qo * zs : lse - (lg[b * L + yb] - m);
     for (int j = 0; j < L; ++j) {
       const float p = expf(lg[b * L + j] - m - lse);
-      lg[b * L + j] = (p - (j == yb ? 1.f : 0.f)) / (float)Bt;
+      lg[b * L + j] = (p - (j == yb ? qy : qo)) / (float)Bt;
     }
   }
   __syncthreads();
@@ -590,8 +595,10 @@ wgrad_reduce_kernel(const float *__restrict__ dw, const float *__restrict__ db, 
 }
 
 // ------------------------------------------------------------------- SGD
-// v <- mu v + g; theta <- theta - lr v on the P parameters of the replica of
-// slot blockIdx.y.  VEC divides P, so every replica row stays aligned.
+// g <- g + wd theta (weight decay); v <- mu v + g; theta <- theta - lr v, or
+// theta - lr (g + mu v) with the Nesterov term (Sec. V-A), on the P
+// parameters of the replica of slot blockIdx.y.  VEC divides P, so every
+// replica row stays aligned.
 template <int VEC> struct FVec;
 template <> struct FVec<1> { typedef float T; };
 template <> struct FVec<2> { typedef float2 T; };
@@ -600,7 +607,7 @@ template <> struct FVec<4> { typedef float4 T; };
 template <int VEC>
 __global__ void __launch_bounds__(256)
 sgd_kernel(float *__restrict__ theta, float *__restrict__ mom, const float *__restrict__ grad, int64_t P,
-           const int32_t *__restrict__ rmap, float lr, float mu) {
+           const int32_t *__restrict__ rmap, float lr, float mu, float wd, int nesterov) {
   typedef typename FVec<VEC>::T V;
   const int64_t base = (int64_t)replica_of(rmap, blockIdx.y) * P;
   V *t4 = reinterpret_cast<V *>(theta + base);
@@ -614,8 +621,9 @@ sgd_kernel(float *__restrict__ theta, float *__restrict__ mom, const float *__re
     const float *gf = reinterpret_cast<const float *>(&g);
 #pragma unroll
     for (int e = 0; e < VEC; ++e) {
-      vf[e] = mu * vf[e] + gf[e];
-      tf[e] -= lr * vf[e];
+      const float ge = gf[e] + wd * tf[e];
+      vf[e] = mu * vf[e] + ge;
+      tf[e] -= lr * (nesterov ? ge + mu * vf[e] : vf[e]);
     }
     m4[i] = v;
     t4[i] = t;
@@ -820,7 +828,7 @@ hipError_t launch_head_pool(int dtype, const void *a, void *h, int C, const int3
 
 hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const float *theta, int64_t P,
                             int64_t w_off, int64_t b_off, float *grad, float *dh, float *loss, int C,
-                            const int32_t *rmap, int Bt, int Ch, int L, hipStream_t s) {
+                            const int32_t *rmap, int Bt, int Ch, int L, float eps, hipStream_t s) {
   const size_t shm = linear_ce_lds_bytes(Bt, Ch, L);
   if (shm > kMaxLinearLds) return hipErrorInvalidValue;
   if (shm > 64 * 1024) {
@@ -833,10 +841,10 @@ hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const fl
   }
   if (dtype == GCPSL_BF16)
     hipLaunchKernelGGL(linear_ce_kernel<bf16_t>, dim3(C), dim3(1024), shm, s, (const bf16_t *)h, y,
-                       theta, P, w_off, b_off, grad, dh, loss, rmap, Bt, Ch, L);
+                       theta, P, w_off, b_off, grad, dh, loss, rmap, Bt, Ch, L, eps);
   else
     hipLaunchKernelGGL(linear_ce_kernel<float>, dim3(C), dim3(1024), shm, s, (const float *)h, y,
-                       theta, P, w_off, b_off, grad, dh, loss, rmap, Bt, Ch, L);
+                       theta, P, w_off, b_off, grad, dh, loss, rmap, Bt, Ch, L, eps);
   return hipGetLastError();
 }
 
@@ -857,18 +865,18 @@ hipError_t launch_wgrad_reduce(const float *dw, const float *db, int splits, int
 }
 
 hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t P, int C, const int32_t *rmap, float lr,
-                      float mu, hipStream_t s) {
+                      float mu, float wd, int nesterov, hipStream_t s) {
   const uintptr_t al = reinterpret_cast<uintptr_t>(theta) | reinterpret_cast<uintptr_t>(mom) |
                        reinterpret_cast<uintptr_t>(grad);
   if (P % 4 == 0 && al % 16 == 0)
     hipLaunchKernelGGL(sgd_kernel<4>, dim3(grid_for(P / 4, 256, 1024), C), dim3(256), 0, s, theta, mom, grad, P, rmap,
-                       lr, mu);
+                       lr, mu, wd, nesterov);
   else if (P % 2 == 0 && al % 8 == 0)
     hipLaunchKernelGGL(sgd_kernel<2>, dim3(grid_for(P / 2, 256, 1024), C), dim3(256), 0, s, theta, mom, grad, P, rmap,
-                       lr, mu);
+                       lr, mu, wd, nesterov);
   else
     hipLaunchKernelGGL(sgd_kernel<1>, dim3(grid_for(P, 256, 1024), C), dim3(256), 0, s, theta, mom, grad, P, rmap,
-                       lr, mu);
+                       lr, mu, wd, nesterov);
   return hipGetLastError();
 }
 

@@ -111,7 +111,8 @@ inline size_t linear_ce_lds_bytes(int Bt, int Ch, int L) {
 }
 hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const float *theta,
                             int64_t P, int64_t w_off, int64_t b_off, float *grad, float *dh,
-                            float *loss, int C, const int32_t *rmap, int Bt, int Ch, int L, hipStream_t s);
+                            float *loss, int C, const int32_t *rmap, int Bt, int Ch, int L, float eps,
+                            hipStream_t s);
 hipError_t launch_head_pool_bwd(int dtype, const void *a, const float *dh, void *gpre, int C, const int32_t *rmap,
                                 int Bt, int H, int W, int Ch, int maxpool, hipStream_t s);
 hipError_t launch_wgrad_reduce(const float *dw, const float *db, int splits, int64_t dw_ss,
@@ -120,7 +121,7 @@ hipError_t launch_wgrad_reduce(const float *dw, const float *db, int splits, int
                                int C, const int32_t *rmap, hipStream_t s);
 // SGD on the replicas of the launch's slots: P parameters each, row stride P.
 hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t P, int C, const int32_t *rmap,
-                      float lr, float mu, hipStream_t s);
+                      float lr, float mu, float wd, int nesterov, hipStream_t s);
 hipError_t launch_fuse(float *theta, const double *weights, double W, int C, int64_t P,
                        hipStream_t s);
 

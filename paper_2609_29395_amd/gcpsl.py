@@ -46,6 +46,7 @@ class Desc(C.Structure):
         ("H", C.c_int32), ("W", C.c_int32), ("Cin", C.c_int32), ("dtype", C.c_int32),
         ("n_examples", C.c_int64), ("n_layers", C.c_int32), ("cut", C.c_int32),
         ("layers", C.POINTER(Layer)), ("lr", C.c_float), ("momentum", C.c_float),
+        ("weight_decay", C.c_float), ("nesterov", C.c_int32), ("label_smoothing", C.c_float),
         ("seed", C.c_uint64), ("max_steps", C.c_int64), ("max_window", C.c_int32),
         ("schedule", C.c_int32), ("client_of_example", C.POINTER(C.c_int32)),
         ("cluster_of_client", C.POINTER(C.c_int32)), ("images", C.c_void_p),
@@ -157,6 +158,9 @@ def make_desc(cfg, client_of_example, cluster_of_client, max_steps=None, max_win
     d.cut = cfg["cut"]
     d.layers = C.cast(keep["layers"], C.POINTER(Layer))
     d.lr, d.momentum = cfg["lr"], cfg["momentum"]
+    d.weight_decay = cfg.get("weight_decay", 0.0)
+    d.nesterov = 1 if cfg.get("nesterov", False) else 0
+    d.label_smoothing = cfg.get("label_smoothing", 0.0)
     d.seed = cfg["seed"]
     d.max_steps = max_steps if max_steps is not None else cfg["T"]
     d.max_window = max_window

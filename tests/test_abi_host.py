@@ -90,7 +90,8 @@ def test_assign_errors():
     assert e.value.code == g.EINVAL
 
 
-@pytest.mark.parametrize("name", ["tiny", "gpsl", "gcpsl16", "ragged", "tiny_norm", "ragged_norm_bf16"])
+@pytest.mark.parametrize("name", ["tiny", "gpsl", "gcpsl16", "ragged", "tiny_norm", "ragged_norm_bf16",
+                                  "ragged_recipe_bf16"])
 def test_param_count_matches_layout(name):
     from gcpsl_inputs import norm_layout
     cfg = get_config(name)
@@ -169,6 +170,11 @@ def test_create_rejects_bad_descriptions_before_device_work():
     assert _create(d)[0] == g.EINVAL
     d, k = _desc(cfg, **dict(base, dtype=9))
     assert _create(d)[0] == g.EINVAL
+    for bad in (dict(weight_decay=-1e-4), dict(weight_decay=float("inf")), dict(nesterov=2),
+                dict(label_smoothing=1.0), dict(label_smoothing=-0.1), dict(label_smoothing=float("nan"))):
+        d, k = _desc(cfg, **dict(base, **bad))
+        rc, msg = _create(d)
+        assert rc == g.EINVAL, bad
 
 
 def test_unsupported_models_are_reported():

@@ -113,7 +113,7 @@ def test_sample_and_gather_bit_exact(name, window, starts):
 # ------------------------------------------------------- multi-step runs
 
 @pytest.mark.parametrize("name", ["tiny", "tiny_jsd", "ragged", "ragged_bf16", "ragged_res_bf16", "tiny_norm",
-                                  "ragged_norm_bf16"])
+                                  "ragged_norm_bf16", "tiny_recipe", "ragged_recipe_bf16"])
 def test_run_parity_with_fusion(name):
     cfg = get_config(name)
     T = cfg["T"]
@@ -140,7 +140,8 @@ def test_run_parity_with_fusion(name):
     assert np.array_equal(per, np.array(ref.active)) and a == int(np.sum(ref.active))
 
 
-@pytest.mark.parametrize("name", ["ragged", "ragged_bf16", "ragged_res_bf16", "tiny", "tiny_norm", "ragged_norm_bf16"])
+@pytest.mark.parametrize("name", ["ragged", "ragged_bf16", "ragged_res_bf16", "tiny", "tiny_norm", "ragged_norm_bf16",
+                                  "tiny_recipe", "ragged_recipe_bf16"])
 def test_intermediates_one_round(name):
     cfg = get_config(name)
     ctx, assignment = driver.setup(cfg)
@@ -177,6 +178,32 @@ def test_intermediates_one_round(name):
                     assert ok, (f"gin{i}", n, e)
         ok, e = close(grads[n], g, tol)
         assert ok, ("grad", n, e)
+
+
+@pytest.mark.parametrize("term", [dict(weight_decay=0.05), dict(nesterov=True), dict(label_smoothing=0.3),
+                                  dict(weight_decay=0.05, nesterov=True, label_smoothing=0.3)])
+def test_recipe_terms_each_change_the_run(term):
+    """Each term of the training recipe (Sec. V-A) on its own, at a strength
+    that moves the parameters well beyond the parity bar: the GPU run matches
+    the oracle run with the term, and differs from the GPU run without it."""
+    base = dict(momentum=0.9, nesterov=False, weight_decay=0.0, label_smoothing=0.0)
+    runs = {}
+    for key, over in (("with", dict(base, **term)), ("without", base)):
+        cfg = get_config("tiny", **over)
+        ctx, assignment = driver.setup(cfg)
+        losses = torch.zeros(cfg["T"], cfg["C"], device="cuda")
+        driver.train(ctx, cfg["T"], losses=losses)
+        torch.cuda.synchronize()
+        runs[key] = (ctx.theta.cpu().numpy(), losses.cpu().numpy(), cfg, assignment)
+    th, lo, cfg, assignment = runs["with"]
+    ref = GCPSLOracle(cfg, cluster_of_client=assignment).run(cfg["T"])
+    tol = TOL["f32"]
+    assert np.all(np.abs(lo - np.array(ref.losses)) <= tol * np.abs(np.array(ref.losses)))
+    for n in range(cfg["C"]):
+        ok, e = close(th[n], ref.theta[n], tol)
+        assert ok, ("theta", n, e)
+        ok, e = close(runs["without"][0][n], ref.theta[n], tol)
+        assert not ok, ("the term left theta unchanged", n, e)
 
 
 # ------------------------------------------------------------------ fusion

@@ -129,6 +129,41 @@ def test_softmax_xent_matches_torch():
     assert np.allclose(d, t.grad.numpy(), atol=1e-15)
 
 
+@pytest.mark.parametrize("eps", [0.1, 0.3, 0.95])
+def test_softmax_xent_label_smoothing_matches_torch(eps):
+    rng = np.random.default_rng(4)
+    logits = rng.standard_normal((11, 7)) * 3
+    y = rng.integers(0, 7, size=11)
+    loss, d = softmax_xent(logits, y, eps)
+    t = torch.tensor(logits, requires_grad=True)
+    tl = tF.cross_entropy(t, torch.tensor(y), label_smoothing=eps)
+    tl.backward()
+    assert loss == pytest.approx(tl.item(), rel=1e-13)
+    assert np.allclose(d, t.grad.numpy(), atol=1e-15)
+
+
+def test_softmax_xent_label_smoothing_closed_forms():
+    # equal logits: p = 1/L for every class, so the loss is log L whatever eps
+    # is, and the gradient (p - q)/B is (1 - eps)/(L B) off the label and
+    # -(1 - eps)(L - 1)/(L B) on it
+    L, B = 5, 3
+    for eps in (0.0, 0.1, 0.5):
+        loss, d = softmax_xent(np.zeros((B, L)), np.array([0, 2, 4]), eps)
+        assert loss == pytest.approx(np.log(L), rel=1e-14)
+        assert np.allclose(d.sum(axis=1), 0.0, atol=1e-16)
+        off = np.ones((B, L), bool)
+        off[[0, 1, 2], [0, 2, 4]] = False
+        assert np.allclose(d[off], (1 - eps) / (L * B), rtol=1e-14)
+        assert np.allclose(d[~off], -(1 - eps) * (L - 1) / (L * B), rtol=1e-14)
+    # a confident correct prediction: with eps = 0 the loss tends to 0, with
+    # eps > 0 it tends to eps (L-1)/L times the logit gap
+    gap = 40.0
+    lg = np.array([[gap, 0.0, 0.0, 0.0]])
+    assert softmax_xent(lg, np.array([0]), 0.0)[0] < 1e-15
+    want = 0.2 * 3 / 4 * gap
+    assert softmax_xent(lg, np.array([0]), 0.2)[0] == pytest.approx(want, rel=1e-12)
+
+
 # ------------------------------------------------- whole-step pins (fp64)
 
 def _batch(cfg, B=None, seed=0):
@@ -205,14 +240,15 @@ def torch_split_model_loss(cfg, theta, x, y, with_running=False):
             a = rf(a.mean(dim=(2, 3)))
         elif spec[0] == "linear":
             a = a @ rf(views[i]["w"]).T + views[i]["b"]
-    loss = tF.cross_entropy(a, torch.tensor(y))
+    loss = tF.cross_entropy(a, torch.tensor(y), label_smoothing=cfg.get("label_smoothing", 0.0))
     loss.backward()
     if with_running:
         return loss.item(), th.grad.numpy(), {i: (m.numpy(), v.numpy()) for i, (m, v) in running.items()}
     return loss.item(), th.grad.numpy()
 
 
-@pytest.mark.parametrize("name", ["tiny", "ragged", "ragged_bf16", "tiny_norm", "ragged_norm_bf16"])
+@pytest.mark.parametrize("name", ["tiny", "ragged", "ragged_bf16", "tiny_norm", "ragged_norm_bf16", "tiny_recipe",
+                                  "ragged_recipe_bf16"])
 def test_split_step_matches_torch_autograd(name):
     cfg = get_config(name)
     theta = init_params(cfg)

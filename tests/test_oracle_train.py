@@ -34,6 +34,61 @@ def test_sgd_matches_torch_optimizer():
     assert np.allclose(theta, p.detach().numpy(), rtol=1e-6, atol=1e-7)
 
 
+@pytest.mark.parametrize("mu,wd,nesterov", [(0.9, 5e-4, True), (0.9, 5e-4, False), (0.9, 0.0, True),
+                                             (0.0, 5e-4, False), (0.5, 0.1, True)])
+def test_sgd_weight_decay_and_nesterov_match_torch_optimizer(mu, wd, nesterov):
+    """The paper's recipe (Sec. V-A): momentum 0.9 with the Nesterov term and
+    weight decay 5e-4, against torch.optim.SGD in fp64 over several steps."""
+    rng = np.random.default_rng(11)
+    t0 = rng.standard_normal(64).astype(np.float32)
+    grads = [rng.standard_normal(64) for _ in range(5)]
+    theta, mom = t0.copy(), np.zeros(64, dtype=np.float32)
+    p = torch.nn.Parameter(torch.tensor(t0, dtype=torch.float64))
+    opt = torch.optim.SGD([p], lr=0.01, momentum=mu, weight_decay=wd, nesterov=nesterov and mu > 0)
+    for g in grads:
+        sgd_update(theta, mom, g, 0.01, mu, wd, nesterov)
+        p.grad = torch.tensor(g)
+        opt.step()
+    assert np.allclose(theta, p.detach().numpy(), rtol=1e-6, atol=1e-7)
+
+
+def test_sgd_nesterov_weight_decay_closed_form():
+    # theta0 = 2, wd = 0.5, mu = 0.5, lr = 0.1, g = 1:
+    # g' = 1 + 0.5*2 = 2; v1 = 2; step = g' + mu v1 = 3; theta1 = 2 - 0.3 = 1.7
+    # g' = 1 + 0.85 = 1.85; v2 = 1 + 1.85 = 2.85; step = 1.85 + 1.425 = 3.275; theta2 = 1.3725
+    theta = np.array([2.0], dtype=np.float32)
+    mom = np.zeros(1, dtype=np.float32)
+    sgd_update(theta, mom, np.array([1.0]), 0.1, 0.5, 0.5, True)
+    assert theta[0] == pytest.approx(1.7, rel=1e-7) and mom[0] == 2.0
+    sgd_update(theta, mom, np.array([1.0]), 0.1, 0.5, 0.5, True)
+    assert mom[0] == pytest.approx(2.85, rel=1e-7)
+    assert theta[0] == pytest.approx(1.3725, rel=1e-7)
+    # without the extra terms the update is the plain momentum step
+    t1, m1 = np.array([2.0], np.float32), np.zeros(1, np.float32)
+    sgd_update(t1, m1, np.array([1.0]), 0.1, 0.5, 0.0, False)
+    assert t1[0] == pytest.approx(1.9, rel=1e-7)
+
+
+def test_recipe_rounds_match_torch_training_loop():
+    """One cluster, three rounds of the paper's recipe (Nesterov, weight
+    decay, label smoothing) against torch autograd + torch.optim.SGD in fp64
+    on the same batches."""
+    from test_oracle_model import torch_split_model_loss
+    cfg = get_config("tiny_recipe", C=1, F=0, dtype="f32")
+    o = GCPSLOracle(cfg)
+    p = torch.nn.Parameter(torch.tensor(o.theta[0], dtype=torch.float64))
+    opt = torch.optim.SGD([p], lr=cfg["lr"], momentum=cfg["momentum"], weight_decay=cfg["weight_decay"],
+                          nesterov=True)
+    for step in range(3):
+        _, x, y = o.batch(step, 0)
+        want_loss, g = torch_split_model_loss(cfg, p.detach().numpy(), x, y)
+        losses, _ = o.round(step)
+        assert losses[0] == pytest.approx(want_loss, rel=1e-6)
+        p.grad = torch.tensor(g)
+        opt.step()
+        assert np.allclose(o.theta[0], p.detach().numpy(), rtol=1e-5, atol=1e-7), step
+
+
 def test_fusion_worked_example():
     # tests/golden: weights 1, 2, 5 (W = 8): (1*[8,0] + 2*[0,4] + 5*[0.8,-1.6]) / 8 = [1.5, 0]
     g = load_golden("fusion_eq5_worked.txt")
