@@ -115,6 +115,57 @@ def schedule_control(cfg, ctx, start, steps):
     return out
 
 
+def hbm_probes(cfg, F, ctx_sizes):
+    """The HBM-bound kernels at sizes where launch ramps and the 256 MB MALL
+    do not decide the rate: the fusion kernel on 16 replicas of 16M + 2
+    parameters (2.1 GB read, 2.1 GB written; weights = the workload's cluster
+    sizes) through gcpsl_fuse_replicas, and the gather of an F-step sample
+    window (gcpsl_sample with nsteps = F).  Rates are algorithmic bytes over
+    hipEvent time on the launching stream."""
+    import numpy as np
+    import torch
+    from paper_2609_29395_amd import driver, gcpsl
+
+    out = {}
+    Cf, Pf = 16, 16 * 1024 * 1024 + 2
+    w = np.resize(np.asarray(ctx_sizes, dtype=np.int64), Cf)
+    theta = torch.randn(Cf, Pf, device="cuda", generator=torch.Generator(device="cuda").manual_seed(0))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(2):
+        gcpsl.fuse_replicas(theta, w)
+    reps = 5
+    e0.record()
+    for _ in range(reps):
+        gcpsl.fuse_replicas(theta, w)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    fb = 8.0 * Cf * Pf
+    out["fusion_16x16M"] = {"replicas": Cf, "params": Pf, "bytes": fb, "us": round(us, 1),
+                            "gbs": round(fb / (us * 1e-6) / 1e9, 1),
+                            "frac": round(fb / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+    del theta
+    torch.cuda.empty_cache()
+
+    ctxw, _ = driver.setup(cfg, max_steps=4 * F, max_window=F)
+    ctxw.sample(0, F)
+    torch.cuda.synchronize()
+    ctxw.timing(True)
+    for k in range(1, 4):
+        ctxw.sample(k * F, F)
+    st = ctxw.timing_read()
+    ctxw.timing(False)
+    g = {k: v for k, v in st.items() if k.startswith("gather")}
+    name, v = max(g.items(), key=lambda kv: kv[1]["bytes"])
+    gbs = v["bytes"] / (v["ms"] * 1e-3) / 1e9
+    out["gather_window"] = {"kernel": name, "steps": F, "examples": F * cfg["C"] * cfg["B"],
+                            "bytes": v["bytes"] / v["launches"], "us": round(v["ms"] * 1e3 / v["launches"], 1),
+                            "gbs": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    del ctxw
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -127,6 +178,8 @@ def main():
     ap.add_argument("--no-schedule-control", action="store_true",
                     help="skip the concurrent-vs-sequential cluster execution control")
     ap.add_argument("--control-steps", type=int, default=10)
+    ap.add_argument("--no-hbm-probes", action="store_true",
+                    help="skip the large fusion and windowed gather measurements")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -218,6 +271,11 @@ def main():
         out["schedule_control"] = schedule_control(cfg, ctx, args.warmup + args.steps + args.timing_steps,
                                                    args.control_steps)
         print(f"bench: schedule control {out['schedule_control']}", file=sys.stderr, flush=True)
+    if not args.no_hbm_probes:
+        out["hbm"] = hbm_probes(cfg, max(F, 1), ctx.cluster_sizes())
+        if fusion_gbs is not None:
+            out["hbm"]["fusion_in_step"] = {"gbs": round(fusion_gbs, 1), "frac": round(fusion_gbs / PEAK_HBM_GBS, 4)}
+        print(f"bench: hbm {out['hbm']}", file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, assignment, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -259,6 +259,23 @@ int gcpsl_epoch_rounds(gcpsl_ctx *ctx, int64_t *rounds, int64_t *slots);
 int gcpsl_fuse(gcpsl_ctx *ctx, void *stream);
 
 /*
+ * The same sample-weighted fusion (Eq. 5, Sec. IV-D) on caller-owned
+ * replicas, without a context: theta_bar[p] = (sum_n weights[n] theta[n][p])
+ * / W, W = sum_n weights[n], accumulated in fp64 in replica order, rounded
+ * once to fp32 and written to all C rows.
+ * theta: device [C][P] fp32, row n = replica n, 4-byte aligned, in/out,
+ * caller-owned; weights: host [C] int64 in [0, 2^29] with W > 0 (e.g. the
+ * replicas' example counts n_n), read before the call returns; 1 <= C <= 64
+ * (the weights travel in the kernel arguments); P >= 1.  Each product and,
+ * when W <= 2^29, each partial sum is exact in fp64, so identical replicas
+ * come back unchanged.  Asynchronous on stream; EINVAL on a bad argument,
+ * EHIP on a failed launch.  This is the operation a sharded run applies to
+ * the all-reduced partial sums, and the form a benchmark times at arbitrary
+ * sizes.
+ */
+int gcpsl_fuse_replicas(float *theta, int32_t C, int64_t P, const int64_t *weights, void *stream);
+
+/*
  * Direct data participation (Sec. V-E): over the recorded horizon
  * [0, T_h), T_h = 1 + the largest step run by gcpsl_step (capped at
  * max_steps), active_slots = sum_t sum_n |A_{n,t}| and total_slots = K T_h;

@@ -785,14 +785,32 @@ extern "C" int gcpsl_fuse(gcpsl_ctx *ctx, void *stream) {
   if (!ctx) return gcpsl_fail(GCPSL_EINVAL, "null context");
   const Plan &p = ctx->plan;
   double W = 0.0;
-  for (int64_t v : ctx->sizes) W += (double)v;
+  std::vector<double> wh(ctx->sizes.size());
+  for (size_t n = 0; n < wh.size(); ++n) W += (wh[n] = (double)ctx->sizes[n]);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   LAUNCH_T("fuse", 2.0 * p.C * p.P, 8.0 * p.C * p.P,
-           launch_fuse(ctx->desc.theta, ctx->at<double>(p.off_fw), W, p.C, p.P, s));
+           launch_fuse(ctx->desc.theta, ctx->at<double>(p.off_fw), wh.data(), W, p.C, p.P, s));
   // the server normalisation state, with the same weights (Sec. IV-D)
   if (p.S > 0)
     LAUNCH_T("fuse", 2.0 * p.C * p.S, 8.0 * p.C * p.S,
-             launch_fuse(ctx->desc.norm_state, ctx->at<double>(p.off_fw), W, p.C, p.S, s));
+             launch_fuse(ctx->desc.norm_state, ctx->at<double>(p.off_fw), wh.data(), W, p.C, p.S, s));
+  return GCPSL_OK;
+}
+
+extern "C" int gcpsl_fuse_replicas(float *theta, int32_t C, int64_t P, const int64_t *weights, void *stream) {
+  gcpsl_clear_error();
+  if (!theta || !weights) return gcpsl_fail(GCPSL_EINVAL, "null argument");
+  if (C < 1 || C > kMaxArgWeights) return gcpsl_fail(GCPSL_EINVAL, "C must lie in [1, 64]");
+  if (P < 1) return gcpsl_fail(GCPSL_EINVAL, "P must be >= 1");
+  if (reinterpret_cast<uintptr_t>(theta) % 4) return gcpsl_fail(GCPSL_EINVAL, "theta must be 4-byte aligned");
+  double wh[kMaxArgWeights];
+  double W = 0.0;
+  for (int n = 0; n < C; ++n) {
+    if (weights[n] < 0 || weights[n] > (int64_t)1 << 29) return gcpsl_fail(GCPSL_EINVAL, "weights must lie in [0, 2^29]");
+    W += (wh[n] = (double)weights[n]);
+  }
+  if (!(W > 0.0)) return gcpsl_fail(GCPSL_EINVAL, "the weights sum to zero");
+  HIP_TRY(launch_fuse(theta, nullptr, wh, W, C, P, reinterpret_cast<hipStream_t>(stream)));
   return GCPSL_OK;
 }
 

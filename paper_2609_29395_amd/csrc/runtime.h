@@ -122,7 +122,10 @@ hipError_t launch_wgrad_reduce(const float *dw, const float *db, int splits, int
 // SGD on the replicas of the launch's slots: P parameters each, row stride P.
 hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t P, int C, const int32_t *rmap,
                       float lr, float mu, float wd, int nesterov, hipStream_t s);
-hipError_t launch_fuse(float *theta, const double *weights, double W, int C, int64_t P,
+// Eq. 5 over C replicas of P parameters: weights from w_host through the
+// kernel arguments when C <= kMaxArgWeights, else from w_dev (device).
+constexpr int kMaxArgWeights = 64;
+hipError_t launch_fuse(float *theta, const double *w_dev, const double *w_host, double W, int C, int64_t P,
                        hipStream_t s);
 
 // Normalisation layers (k_norm.hip): batch norm (groups == 0) or group norm

@@ -24,6 +24,7 @@ SCHEDULES = {"lockstep": 0, "epoch": 1}
 
 EXPORTS = ["gcpsl_param_count", "gcpsl_state_count", "gcpsl_workspace_bytes", "gcpsl_assign", "gcpsl_create",
            "gcpsl_sample", "gcpsl_step", "gcpsl_step_replica", "gcpsl_epoch_rounds", "gcpsl_fuse",
+           "gcpsl_fuse_replicas",
            "gcpsl_participation",
            "gcpsl_cluster_sizes", "gcpsl_tensor", "gcpsl_timing", "gcpsl_timing_read",
            "gcpsl_destroy", "gcpsl_last_error"]
@@ -83,6 +84,7 @@ def lib():
     L.gcpsl_step_replica.argtypes = [vp, i64, i32, vp, vp]
     L.gcpsl_epoch_rounds.argtypes = [vp, P(i64), P(i64)]
     L.gcpsl_fuse.argtypes = [vp, vp]
+    L.gcpsl_fuse_replicas.argtypes = [vp, i32, i64, P(i64), vp]
     L.gcpsl_participation.argtypes = [vp, P(i64), P(i64), P(i32)]
     L.gcpsl_cluster_sizes.argtypes = [vp, P(i64)]
     L.gcpsl_tensor.argtypes = [vp, C.c_char_p, P(vp), P(i64), P(i32)]
@@ -142,6 +144,20 @@ def assign(rule, K, C_, seed, counts=None, hist=None):
                               None if cnt is None else _i64p(cnt), None if h is None else _i64p(h),
                               L, _i32p(out)))
     return out
+
+
+def fuse_replicas(theta, weights, stream=None):
+    """gcpsl_fuse_replicas: Eq. 5 in place on a [C][P] fp32 torch tensor on
+    the GPU with host weights [C]."""
+    if theta.dim() != 2 or theta.dtype.is_floating_point is False or theta.element_size() != 4:
+        raise ValueError("theta must be a [C][P] fp32 tensor")
+    if not theta.is_contiguous():
+        raise ValueError("theta must be contiguous")
+    w = np.ascontiguousarray(weights, dtype=np.int64)
+    if w.shape != (theta.shape[0],):
+        raise ValueError("weights must have one entry per replica")
+    _check(lib().gcpsl_fuse_replicas(C.c_void_p(theta.data_ptr()), theta.shape[0], theta.shape[1], _i64p(w),
+                                     _stream(stream)))
 
 
 def make_desc(cfg, client_of_example, cluster_of_client, max_steps=None, max_window=1, schedule="lockstep"):

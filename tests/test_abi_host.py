@@ -227,3 +227,19 @@ def test_assign_label_jsd_random_instances():
     with pytest.raises(g.GCPSLError) as e:
         g.assign("label_jsd", 4, 2, 0, np.zeros(4, np.int64), np.zeros((4, 3), np.int64))
     assert e.value.code == g.EINVAL
+
+
+def test_fuse_replicas_rejects_bad_arguments_before_device_work():
+    lib = g.lib()
+    fake = C.c_void_p(1 << 20)  # never dereferenced: every case fails validation first
+    w = np.array([3, 4, 5], dtype=np.int64)
+    wp = w.ctypes.data_as(C.POINTER(C.c_int64))
+    cases = [(None, 3, 10, wp), (fake, 0, 10, wp), (fake, 65, 10, wp), (fake, 3, 0, wp), (fake, 3, 10, None),
+             (C.c_void_p((1 << 20) + 2), 3, 10, wp)]
+    for th, Cc, P, ww in cases:
+        assert lib.gcpsl_fuse_replicas(th, Cc, P, ww, None) == g.EINVAL, (Cc, P)
+    for bad in ([3, -1, 5], [0, 0, 0], [1, 1 << 30, 1]):
+        b = np.array(bad, dtype=np.int64)
+        rc = lib.gcpsl_fuse_replicas(fake, 3, 10, b.ctypes.data_as(C.POINTER(C.c_int64)), None)
+        assert rc == g.EINVAL, bad
+        assert "weights" in lib.gcpsl_last_error().decode()

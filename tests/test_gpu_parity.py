@@ -233,6 +233,49 @@ def test_fusion_of_identical_replicas_is_identity():
     assert torch.equal(ctx.theta, before)
 
 
+@pytest.mark.parametrize("C,P", [(1, 1), (3, 7), (5, 1001), (4, 1002), (7, 1024), (16, 65538), (64, 333)])
+def test_fuse_replicas_bit_exact_against_oracle(C, P):
+    """gcpsl_fuse_replicas on caller-given replicas (every kernel width: P
+    odd, P = 2 mod 4, P = 0 mod 4) and weights with zeros among them."""
+    rng = np.random.default_rng(C * 1000 + P)
+    th = (rng.standard_normal((C, P)) * np.exp(rng.uniform(-8, 8, (C, P)))).astype(np.float32)
+    w = rng.integers(0, 60000, size=C)
+    w[rng.random(C) < 0.2] = 0
+    if w.sum() == 0:
+        w[0] = 1
+    t = torch.tensor(th, device="cuda")
+    gcpsl.fuse_replicas(t, w)
+    torch.cuda.synchronize()
+    want = oracle_fuse(list(th), w.tolist())
+    got = t.cpu().numpy()
+    for n in range(C):
+        assert np.array_equal(got[n], want), n
+
+
+def test_fuse_replicas_large_sampled_and_identity():
+    """The 16-replica, 16M-parameter fusion timed by the benchmark: sampled
+    columns against the oracle (fusion is column by column), and identical
+    replicas come back unchanged."""
+    C, P = 16, 16 * 1024 * 1024 + 2
+    g = torch.Generator(device="cuda").manual_seed(5)
+    t = torch.randn(C, P, device="cuda", generator=g)
+    w = np.arange(1, C + 1, dtype=np.int64) * 3001
+    cols = np.sort(np.random.default_rng(6).choice(P, size=4096, replace=False))
+    cols = np.concatenate([[0, 1, P - 2, P - 1], cols])
+    before = t[:, torch.tensor(cols, device="cuda")].cpu().numpy()
+    gcpsl.fuse_replicas(t, w)
+    torch.cuda.synchronize()
+    after = t[:, torch.tensor(cols, device="cuda")].cpu().numpy()
+    want = oracle_fuse(list(before), w.tolist())
+    for n in range(C):
+        assert np.array_equal(after[n], want), n
+    same = t[:1].expand(C, -1).contiguous()
+    ref = same[0].clone()
+    gcpsl.fuse_replicas(same, w)
+    torch.cuda.synchronize()
+    assert torch.equal(same, ref.expand(C, -1))
+
+
 # ------------------------------------------------ full sizes, sampled outputs
 
 def _windows(a, shape):
