@@ -71,6 +71,27 @@ template <int BM_, int BN, int WM, int WN> struct Cfg {
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 };
 
+// Halo mode (16 x 16 images, 256-pixel tiles: one image per tile, 64-channel
+// multiples): per 64-channel block the image is staged once with a one-pixel
+// zero border, 18 x 18 rows of 128 bytes, and the 9 taps read their pixel
+// fragments from it at shifted rows, so a tile's pixels are copied once per
+// channel block instead of once per tap.  Row R = 18 h' + w' stores its
+// 16-byte chunk c at c ^ hswz(w'), hswz(w') = (w' >> 1) & 7: a fragment (16
+// pixels of one image row, rows R0 .. R0 + 15 for any tap) then hits every
+// bank once per row parity, and fragments of successive image rows sit a
+// constant 18 rows (2304 bytes) apart.  Two halo buffers (by channel block)
+// and two weight stages (by k tile).
+namespace halo {
+constexpr int IMG = 16, HP = IMG + 2, ROWS = HP * HP;    // 18 x 18 rows
+constexpr int BYTES = ((ROWS * 128 + 1023) / 1024) * 1024;  // padded to whole 1 KB wave copies
+constexpr int FSTRIDE = HP * 128;                         // bytes between image-row fragments
+constexpr int PIECES = (ROWS * 128 + 16383) / 16384;      // 16-byte copies per thread (1024 threads)
+constexpr int B_BYTES = 256 * 128;
+constexpr int LDS_BYTES = 2 * BYTES + 2 * B_BYTES;
+static_assert(PIECES == 3 && LDS_BYTES <= 160 * 1024, "halo layout");
+}  // namespace halo
+__device__ __forceinline__ int hswz(int wp) { return (wp >> 1) & 7; }
+
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 __device__ __forceinline__ int wn_of(int wave, int WN) { return wave % WN; }
 
@@ -93,14 +114,15 @@ template <int OFF>
 __device__ __forceinline__ void read_frag(u32x4 &f, uint32_t addr) {
   asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(f) : "v"(addr), "n"(OFF));
 }
-template <int T, int START, int... I>
+template <int T, int START, int STRIDE, int... I>
 __device__ __forceinline__ void read_frags_seq(u32x4 (&f)[T], uint32_t addr, std::integer_sequence<int, I...>) {
-  (read_frag<(START + I) * 2048>(f[I], addr), ...);
+  (read_frag<(START + I) * STRIDE>(f[I], addr), ...);
 }
-// fragments START .. START+T-1 of a 16-row-block column
-template <int T, int START = 0>
+// fragments START .. START+T-1 of a column of fragments STRIDE bytes apart
+// (2048: 16-row blocks)
+template <int T, int START = 0, int STRIDE = 2048>
 __device__ __forceinline__ void read_frags(u32x4 (&f)[T], uint32_t addr) {
-  read_frags_seq<T, START>(f, addr, std::make_integer_sequence<int, T>{});
+  read_frags_seq<T, START, STRIDE>(f, addr, std::make_integer_sequence<int, T>{});
 }
 
 // Wait for every outstanding LDS read, then mark the fragments as produced
@@ -176,10 +198,39 @@ __device__ __forceinline__ void issue_tile(int kt, char *stage0, int wave, const
                                                boff[q] == kOob ? kOob : boff[q] + kb, 0, 0, 0);
 }
 
-template <int BM, int BN, int WM, int WN, int EPI, bool TAPS1>
+// Halo mode: piece q of channel block cb's halo image into buffer cb % 2
+// (hoff: this thread's source offset within the image, -1 for the zero
+// border); the last piece covers only the first waves.
+__device__ __forceinline__ void issue_halo_piece(int q, int cb, char *smem, int wave, const ConvArgs &a,
+                                                 const void *src, int img_off, int hoff) {
+  const __amdgpu_buffer_rsrc_t rsa = rsrc(src, (uint32_t)(a.src_rs * 2));
+  if (q * 16384 + wave * 1024 < halo::BYTES) {
+    const uint32_t off = hoff >= 0 ? (uint32_t)(img_off + hoff + cb * BK) * 2u : kOob;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(smem + (cb & 1) * halo::BYTES + q * 16384 + wave * 1024),
+                                             16, off, 0, 0, 0);
+  }
+}
+
+// Halo mode: the weight rows of k tile kt (channel block kt / 9, tap kt % 9)
+// into weight stage kt % 2.
+template <typename CF>
+__device__ __forceinline__ void issue_weights(int kt, char *smem, int wave, const ConvArgs &a, const void *wt,
+                                              const uint32_t *boff) {
+  const __amdgpu_buffer_rsrc_t rsb = rsrc(wt, (uint32_t)((int64_t)a.N * a.Kp * 2));
+  const int cb = kt / 9, rs = kt - 9 * cb;
+  const uint32_t kb = (uint32_t)((rs * a.Csrc + cb * BK) * 2);
+  char *sb = smem + 2 * halo::BYTES + (kt & 1) * halo::B_BYTES + wave * 1024;
+#pragma unroll
+  for (int q = 0; q < CF::SB; ++q)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, LDS_PTR(sb + q * CF::NTHR * 16), 16,
+                                             boff[q] == kOob ? kOob : boff[q] + kb, 0, 0, 0);
+}
+
+template <int BM, int BN, int WM, int WN, int EPI, bool TAPS1, bool HALO = false>
 __global__ void __launch_bounds__(64 * WM * WN)
 conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
   using CF = Cfg<BM, BN, WM, WN>;
+  static_assert(!HALO || (BM == 256 && BN == 256 && WM == 4 && WN == 4 && !TAPS1), "halo mode tile");
   constexpr int SA = CF::SA, SB = CF::SB, TM = CF::TM, TN = CF::TN, NTHR = CF::NTHR, PF = CF::PF;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -199,27 +250,42 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   // the k tile advances.
   int achunk[SA], arowoff[SA];
   uint32_t amask[SA];  // kernel taps (bit r*3+s) whose source pixel is inside the image
+  // halo mode: source offset (pixel of the image x Csrc + chunk column) of
+  // this thread's piece q of a halo image, -1 on the zero border
+  int hoff[halo::PIECES];
+  if constexpr (HALO) {
 #pragma unroll
-  for (int q = 0; q < SA; ++q) {
-    const int byte = q * NTHR * 16 + wave * 1024 + lane * 16;
-    const int row = byte / ROW;
-    achunk[q] = ((byte % ROW) / 16) ^ swz(row);
-    const int m = m0 + row;
-    const uint32_t mm = m < M ? (uint32_t)m : 0u;
-    arowoff[q] = (int)mm * a.Csrc;
-    if constexpr (TAPS1) {
-      amask[q] = m < M ? 1u : 0u;
-    } else {
-      const uint32_t q1 = fdiv(mm, fd_w);
-      const int w = (int)(mm - q1 * (uint32_t)a.W);
-      const int h = (int)(q1 - fdiv(q1, fd_h) * (uint32_t)a.H);
-      uint32_t mk = 0;
+    for (int q = 0; q < halo::PIECES; ++q) {
+      const int g = q * 1024 + tid;  // 16-byte piece: row g / 8, physical chunk g % 8
+      const int R = g >> 3, hp = R / halo::HP, wp = R - hp * halo::HP;
+      const int c = (g & 7) ^ hswz(wp);
+      const bool in = R < halo::ROWS && hp >= 1 && hp <= halo::IMG && wp >= 1 && wp <= halo::IMG;
+      hoff[q] = in ? ((hp - 1) * halo::IMG + (wp - 1)) * a.Csrc + 8 * c : -1;
+    }
+  }
+  if constexpr (!HALO) {
 #pragma unroll
-      for (int rs = 0; rs < 9; ++rs) {
-        const int hh = h + rs / 3 - 1, ww = w + rs % 3 - 1;
-        if ((unsigned)hh < (unsigned)a.H && (unsigned)ww < (unsigned)a.W) mk |= 1u << rs;
+    for (int q = 0; q < SA; ++q) {
+      const int byte = q * NTHR * 16 + wave * 1024 + lane * 16;
+      const int row = byte / ROW;
+      achunk[q] = ((byte % ROW) / 16) ^ swz(row);
+      const int m = m0 + row;
+      const uint32_t mm = m < M ? (uint32_t)m : 0u;
+      arowoff[q] = (int)mm * a.Csrc;
+      if constexpr (TAPS1) {
+        amask[q] = m < M ? 1u : 0u;
+      } else {
+        const uint32_t q1 = fdiv(mm, fd_w);
+        const int w = (int)(mm - q1 * (uint32_t)a.W);
+        const int h = (int)(q1 - fdiv(q1, fd_h) * (uint32_t)a.H);
+        uint32_t mk = 0;
+#pragma unroll
+        for (int rs = 0; rs < 9; ++rs) {
+          const int hh = h + rs / 3 - 1, ww = w + rs % 3 - 1;
+          if ((unsigned)hh < (unsigned)a.H && (unsigned)ww < (unsigned)a.W) mk |= 1u << rs;
+        }
+        amask[q] = m < M ? mk : 0u;
       }
-      amask[q] = m < M ? mk : 0u;
     }
   }
   uint32_t boff[SB];
@@ -251,8 +317,13 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   for (int kg = 0; kg < 2; ++kg) {
     const int ph = ((4 * kg + lg) ^ swz(li)) * 16;
     xa[kg] = (uint32_t)((wm * TM * 16 + li) * ROW + ph);
-    wa[kg] = (uint32_t)(CF::A_BYTES + (wn * TN * 16 + li) * ROW + ph);
+    wa[kg] = (uint32_t)((HALO ? 0 : CF::A_BYTES) + (wn * TN * 16 + li) * ROW + ph);
   }
+  // halo mode: the tile is image m0 / 256; its channel block cb sits in halo
+  // buffer cb % 2, k tile kt's weights in weight stage kt % 2
+  const int img_off = m0 * a.Csrc;
+  const int ncb = a.Csrc / BK;
+  constexpr int XS = HALO ? halo::FSTRIDE : 2048;  // bytes between pixel fragments
 
   f32x4_t acc[TM][TN];
 #pragma unroll
@@ -260,14 +331,39 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
 #pragma unroll
     for (int k = 0; k < TN; ++k) acc[i][k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  issue(0);
+  if constexpr (HALO) {
+#pragma unroll
+    for (int q = 0; q < halo::PIECES; ++q) issue_halo_piece(q, 0, smem, wave, a, src, img_off, hoff[q]);
+    issue_weights<CF>(0, smem, wave, a, wt, boff);
+  } else {
+    issue(0);
+  }
   for (int kt = 0; kt < nk; ++kt) {
     // own copies of tile kt have landed; after the barrier every wave's
     // have, and every wave is done with tile kt-1, whose stage is refilled
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     asm volatile("s_barrier" ::: "memory");
-    if (kt + 1 < nk) issue(kt + 1);
-    const uint32_t st = lds0 + (uint32_t)((kt & 1) * CF::STAGE);
+    uint32_t xb[2], wb;  // pixel fragment bases of the two k groups, weight stage
+    uint32_t xst = 0;    // halo mode: the halo buffer of this channel block
+    if constexpr (HALO) {
+      const int cb = kt / 9, rs = kt - 9 * cb;
+      if (kt + 1 < nk) issue_weights<CF>(kt + 1, smem, wave, a, wt, boff);
+      // the next channel block's halo in three pieces over the first three
+      // taps (the buffer was last read by channel block cb - 1)
+      if (rs < halo::PIECES && cb + 1 < ncb)
+        issue_halo_piece(rs, cb + 1, smem, wave, a, src, img_off, rs == 0 ? hoff[0] : rs == 1 ? hoff[1] : hoff[2]);
+      xst = lds0 + (uint32_t)((cb & 1) * halo::BYTES);
+      wb = lds0 + (uint32_t)(2 * halo::BYTES + (kt & 1) * halo::B_BYTES);
+      const int r = (rs * 11) >> 5, sc = rs - 3 * r;  // tap (r, sc)
+#pragma unroll
+      for (int kg = 0; kg < 2; ++kg)
+        xb[kg] = xst + (uint32_t)(((wm * TM + r) * halo::HP + sc + li) * 128 + (((4 * kg + lg) ^ hswz(li + sc)) * 16));
+    } else {
+      if (kt + 1 < nk) issue(kt + 1);
+      wb = lds0 + (uint32_t)((kt & 1) * CF::STAGE);
+#pragma unroll
+      for (int kg = 0; kg < 2; ++kg) xb[kg] = wb + xa[kg];
+    }
     const bool add_res = a.res_lds && kt == res_kt;
     // per k group: the second half of the pixel fragments is read while the
     // first half is multiplied
@@ -275,10 +371,10 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
     for (int kg = 0; kg < 2; ++kg) {
       constexpr int H = TM / 2;
       u32x4 w[TN], x0[H], x1[H];
-      read_frags<TN>(w, st + wa[kg]);
-      read_frags<H>(x0, st + xa[kg]);
+      read_frags<TN>(w, wb + wa[kg]);
+      read_frags<H, 0, XS>(x0, xb[kg]);
       wait_frags<H, TN>(x0, w);
-      read_frags<H, H>(x1, st + xa[kg]);
+      read_frags<H, H, XS>(x1, xb[kg]);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int tm = 0; tm < H; ++tm)
@@ -294,14 +390,17 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
     if (add_res) {
       // residual of fragment (tm, tn): 4 channels tn*16 + lg*4 .. +3 of the
       // block at pixel row wm*TM*16 + tm*16 + li of the centre-tap A tile
+      // (halo mode: image row wm*TM + tm, column li, at halo row + 1, + 1)
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm) {
         u32x2 rv[TN];
         const int row = wm * TM * 16 + tm * 16 + li;
+        const int hrow = (wm * TM + tm + 1) * halo::HP + li + 1;
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) {
           const int ch = tn * 2 + (lg >> 1);  // 16-byte chunk of the row
-          const uint32_t ad = st + (uint32_t)(row * ROW + ((ch ^ swz(row)) * 16) + (lg & 1) * 8);
+          const uint32_t ad = HALO ? xst + (uint32_t)(hrow * 128 + ((ch ^ hswz(li + 1)) * 16) + (lg & 1) * 8)
+                                   : wb + (uint32_t)(row * ROW + ((ch ^ swz(row)) * 16) + (lg & 1) * 8);
           asm volatile("ds_read_b64 %0, %1" : "=v"(rv[tn]) : "v"(ad));
         }
         // the values are produced at the wait: keep every use after it
@@ -429,6 +528,13 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   }
   static bool attr = false;
   if (!attr) {
+    constexpr int halo_lds = halo::LDS_BYTES > Cfg<256, 256, 4, 4>::EP_BYTES ? halo::LDS_BYTES
+                                                                             : Cfg<256, 256, 4, 4>::EP_BYTES;
+    for (const void *f : {reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, 4, 4, EPI_FWD, false, true>),
+                          reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, 4, 4, EPI_DGRAD, false, true>)}) {
+      const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, halo_lds);
+      if (e != hipSuccess) return e;
+    }
     CONV_LDS_ATTR(256, 256, 4, 4)
     CONV_LDS_ATTR(256, 128, 4, 2)
     CONV_LDS_ATTR(128, 64, 2, 4)
@@ -455,9 +561,22 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   ConvArgs b = a;
   b.res_lds = (a.res != nullptr && a.res == a.src && a.taps == 9 && a.Csrc % BK == 0 && a.Csrc == a.N &&
                (bn == 256 || bn == 128)) ? 1 : 0;
+  // halo mode: one 16 x 16 image per 256-pixel tile, 64-channel blocks
+  const bool use_halo = bn == 256 && a.taps == 9 && a.Csrc % BK == 0 && a.H == halo::IMG && a.W == halo::IMG;
   if (label)
     *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16," + std::to_string(bm) + "x" +
-             std::to_string(bn) + "x64,w" + (bn == 256 ? "16" : "8") + ",lds>";
+             std::to_string(bn) + "x64,w" + (bn == 256 ? "16" : "8") + (use_halo ? ",halo>" : ",lds>");
+  if (use_halo) {
+    constexpr int halo_lds = halo::LDS_BYTES > Cfg<256, 256, 4, 4>::EP_BYTES ? halo::LDS_BYTES
+                                                                             : Cfg<256, 256, 4, 4>::EP_BYTES;
+    if (a.epi == EPI_FWD)
+      hipLaunchKernelGGL((conv_lds_kernel<256, 256, 4, 4, EPI_FWD, false, true>), g, dim3(1024), halo_lds, s, b, fw,
+                         fh, fc, MT, NT);
+    else
+      hipLaunchKernelGGL((conv_lds_kernel<256, 256, 4, 4, EPI_DGRAD, false, true>), g, dim3(1024), halo_lds, s, b,
+                         fw, fh, fc, MT, NT);
+    return hipGetLastError();
+  }
 #define CONV_LDS_GO(BM, BN, WM, WN, E, T)                                                                  \
   hipLaunchKernelGGL((CONV_LDS_K(BM, BN, WM, WN, E, T)), g, dim3(Cfg<BM, BN, WM, WN>::NTHR),                 \
                      (Cfg<BM, BN, WM, WN>::LDS_BYTES), s, b, fw, fh, fc, MT, NT)

@@ -42,8 +42,14 @@ def kink_sensitive(cfg):
     parameters, normalisation state, forward activations and the parameter
     gradient stay within the bf16 bar; the per-element backward tensors and
     the momentum (the accumulated gradients) are held to the flip check
-    below instead."""
-    return cfg["dtype"] == "bf16" and any(sp[0] in ("bnorm", "gnorm") for sp in cfg["layers"])
+    below instead.  The same holds for the 16 x 16 residual workload without
+    a max pool: its top conv feeds the average pool, which hands every pixel
+    of a channel the same gradient, and one ReLU decision at a pre-activation
+    within bf16 rounding of zero moves a full-size entry of that layer's
+    gradient (0.4 % in norm, 52 % of the maximum at one element of one
+    replica, propagating with shrinking size into the layers below)."""
+    norm = any(sp[0] in ("bnorm", "gnorm") for sp in cfg["layers"])
+    return cfg["dtype"] == "bf16" and (norm or cfg["name"] == "halo_res_bf16")
 
 
 def relu_flips_are_near_kinks(act_gpu, act_ref, pre_ref, rel=1e-2):
@@ -113,7 +119,7 @@ def test_sample_and_gather_bit_exact(name, window, starts):
 # ------------------------------------------------------- multi-step runs
 
 @pytest.mark.parametrize("name", ["tiny", "tiny_jsd", "ragged", "ragged_bf16", "ragged_res_bf16", "tiny_norm",
-                                  "ragged_norm_bf16", "tiny_recipe", "ragged_recipe_bf16"])
+                                  "ragged_norm_bf16", "tiny_recipe", "ragged_recipe_bf16", "halo_res_bf16"])
 def test_run_parity_with_fusion(name):
     cfg = get_config(name)
     T = cfg["T"]
@@ -141,7 +147,7 @@ def test_run_parity_with_fusion(name):
 
 
 @pytest.mark.parametrize("name", ["ragged", "ragged_bf16", "ragged_res_bf16", "tiny", "tiny_norm", "ragged_norm_bf16",
-                                  "tiny_recipe", "ragged_recipe_bf16"])
+                                  "tiny_recipe", "ragged_recipe_bf16", "halo_res_bf16"])
 def test_intermediates_one_round(name):
     cfg = get_config(name)
     ctx, assignment = driver.setup(cfg)
@@ -167,7 +173,9 @@ def test_intermediates_one_round(name):
                 ok, e = close(t, rec["acts"][i + 1], tol)
                 assert ok, (name_i, n, e)
             if kink_sensitive(cfg):
-                if spec[0] in ("bnorm", "gnorm"):
+                relu_after = spec[0] in ("bnorm", "gnorm") or (
+                    spec[0] == "conv" and not (i + 1 < len(cfg["layers"]) and cfg["layers"][i + 1][0] in ("bnorm", "gnorm")))
+                if relu_after and t is not None:
                     relu_flips_are_near_kinks(t, rec["acts"][i + 1], rec[f"pre{i}"])
                 continue
             if spec[0] in ("conv", "bnorm", "gnorm"):
