@@ -264,7 +264,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
         // workgroups) x (k tiles per workgroup + the cost of writing and
         // re-reading a partial tile, about 16 k tiles)
         int tile_bk, per_cu;
-        wgrad_lds_tile(l.Co, &bm, &bn, &tile_bk, &per_cu);
+        wgrad_lds_tile(l.Co, (i == 0 && p.col0) ? p.Kc : l.Ci, l.H, l.W, (i == 0 && p.col0) ? 1 : 9, &bm, &bn,
+                       &tile_bk, &per_cu);
         const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
         const int64_t slots = 256 * (int64_t)per_cu;
         int64_t best = -1;

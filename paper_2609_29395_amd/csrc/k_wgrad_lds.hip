@@ -304,6 +304,220 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
   }
 }
 
+// ------------------------------------------------------------- halo mode
+// 16 x 16 images, output channels a multiple of 128, input channels a
+// multiple of 64 (the wide server layers).  A workgroup owns 128 output
+// channels x one 64-channel input block x all nine taps (128 x 576 outputs).
+// A k tile of 64 pixels is four image rows; what every tap needs of the
+// input is the six image rows around them with a one-pixel zero border,
+// 6 x 18 pixel rows of 128 bytes, copied once; the nine taps read their
+// fragments from it at shifted rows.  A k tile then copies 16 KB of g and
+// 13.5 KB of input for 9.4 MFLOP, against 64 KB for 8.4 MFLOP with one tap
+// per 256 x 256 tile.
+// Halo row R = 18 h' + w' stores its 16-byte chunk c at c ^ 2 whsw(w'),
+// whsw(w') = bit 1 of w' | (bit 3 of w') << 1: the eight rows a half-wave's
+// transposing read touches (w' in {a .. a+3, a+8 .. a+11} for one image row)
+// then use every bank exactly once, and the rows of successive image rows and
+// of the three kernel-tap rows sit a constant 18 rows (2,304 bytes) apart.
+namespace wh {
+constexpr int IMG = 16, HP = 18, TR = 4;   // image side, halo row width, image rows per k tile
+constexpr int BK = IMG * TR;               // 64 pixels per k tile
+constexpr int HROWS = (TR + 2) * HP;       // 108 halo rows
+constexpr int ROWB = 128;                  // bytes per halo row (64 channels)
+constexpr int BM = 128, ROWA = BM * 2;     // output channels per workgroup, bytes per g row
+constexpr int NTHR = 512, TM = 4;          // 8 waves (2 x 4); g fragments per wave
+constexpr int A_BYTES = BK * ROWA;         // 16 KB
+constexpr int B_BYTES = 16384;             // 108 halo rows, the rest takes the zero copies of idle lanes
+constexpr int STAGE = A_BYTES + B_BYTES;
+constexpr int SA = A_BYTES / (NTHR * 16), SB = B_BYTES / (NTHR * 16), CPT = SA + SB;
+constexpr int QROWA = NTHR * 16 / ROWA;    // g rows between a thread's copies
+constexpr int FROW = HP * ROWB;            // bytes between halo image rows
+static_assert(HROWS * ROWB <= B_BYTES && SA == 2 && SB == 2 && QROWA % 16 == 0, "halo weight-gradient layout");
+}  // namespace wh
+__device__ __forceinline__ int whsw(int wp) { return ((wp >> 1) & 1) | ((wp >> 2) & 2); }
+
+// One operand fragment from two transposing reads at separate addresses (the
+// halo's swizzle differs between the two 4-pixel halves).
+template <int OFF>
+__device__ __forceinline__ void read_frag2(u32x4 &f, uint32_t a0, uint32_t a1) {
+  u32x2 lo, hi;
+  asm volatile("ds_read_b64_tr_b16 %0, %2 offset:%4\n\tds_read_b64_tr_b16 %1, %3 offset:%4"
+               : "=&v"(lo), "=&v"(hi)
+               : "v"(a0), "v"(a1), "n"(OFF));
+  f = __builtin_shufflevector(lo, hi, 0, 1, 2, 3);
+}
+
+// Copies of k tile kt into stage kt % NST: g rows (pixels) at this thread's
+// column, and this thread's halo rows (hh = h' of the row, -1 for the zero
+// border and padding; hrel = its source offset from the tile's first pixel).
+template <int NST>
+__device__ __forceinline__ void wh_issue(int kt, char *stage0, const void *G, const void *X, uint32_t gbytes,
+                                         uint32_t xbytes, int Co, int Ci, int p_begin, int arow, int acol,
+                                         const int (&hrel)[wh::SB], const int (&hh)[wh::SB]) {
+  const __amdgpu_buffer_rsrc_t rsg = rsrc(G, gbytes);
+  const __amdgpu_buffer_rsrc_t rsx = rsrc(X, xbytes);
+  char *sa = stage0 + (kt % NST) * wh::STAGE;
+  const int pt = p_begin + kt * wh::BK;
+#pragma unroll
+  for (int q = 0; q < wh::SA; ++q) {
+    const uint32_t off = ((uint32_t)(pt + arow + q * wh::QROWA) * (uint32_t)Co + (uint32_t)acol) * 2u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsg, LDS_PTR(sa + q * wh::NTHR * 16), 16, off, 0, 0, 0);
+  }
+  const int h0 = (pt >> 4) & (wh::IMG - 1);  // first image row of the tile
+#pragma unroll
+  for (int q = 0; q < wh::SB; ++q) {
+    const bool ok = hh[q] >= 0 && (unsigned)(h0 - 1 + hh[q]) < (unsigned)wh::IMG;
+    const uint32_t off = ok ? (uint32_t)(pt * Ci + hrel[q]) * 2u : kOob;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, LDS_PTR(sa + wh::A_BYTES + q * wh::NTHR * 16), 16, off, 0, 0, 0);
+  }
+}
+
+// k group KG (two image rows) of the stage at st: 4 g fragments, one input
+// fragment per tap, 36 MFMAs (+1 against ones for the bias gradient).
+template <int KG>
+__device__ __forceinline__ void wh_kgroup(f32x4_t (&acc)[wh::TM][9], f32x4_t &bacc, const uint32_t (&ra)[wh::TM],
+                                          const uint32_t (&hb)[3][2], uint32_t st, bool bias, int wn) {
+  u32x4 a[wh::TM], b[9];
+#pragma unroll
+  for (int i = 0; i < wh::TM; ++i) read_frag<KG * 32 * wh::ROWA, wh::ROWA>(a[i], st + ra[i]);
+  constexpr int O = wh::A_BYTES + KG * 2 * wh::FROW;
+  read_frag2<O + 0 * wh::FROW>(b[0], st + hb[0][0], st + hb[0][1]);
+  read_frag2<O + 0 * wh::FROW>(b[1], st + hb[1][0], st + hb[1][1]);
+  read_frag2<O + 0 * wh::FROW>(b[2], st + hb[2][0], st + hb[2][1]);
+  read_frag2<O + 1 * wh::FROW>(b[3], st + hb[0][0], st + hb[0][1]);
+  read_frag2<O + 1 * wh::FROW>(b[4], st + hb[1][0], st + hb[1][1]);
+  read_frag2<O + 1 * wh::FROW>(b[5], st + hb[2][0], st + hb[2][1]);
+  read_frag2<O + 2 * wh::FROW>(b[6], st + hb[0][0], st + hb[0][1]);
+  read_frag2<O + 2 * wh::FROW>(b[7], st + hb[1][0], st + hb[1][1]);
+  read_frag2<O + 2 * wh::FROW>(b[8], st + hb[2][0], st + hb[2][1]);
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < wh::TM; ++i) asm volatile("" : "+v"(a[i]));
+#pragma unroll
+  for (int i = 0; i < 9; ++i) asm volatile("" : "+v"(b[i]));
+#pragma unroll
+  for (int tm = 0; tm < wh::TM; ++tm)
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap) mma(acc[tm][tap], a[tm], b[tap]);
+  if (bias) {
+    const uint32_t one2 = 0x3F803F80u;  // two bf16 ones
+    const u32x4 ones = u32x4{one2, one2, one2, one2};
+#pragma unroll
+    for (int tm = 0; tm < wh::TM; ++tm)
+      if (tm == wn) mma(bacc, a[tm], ones);
+  }
+}
+
+template <int NST>
+__global__ void __launch_bounds__(wh::NTHR)
+wgrad_halo_kernel(WgradArgs a, int MT, int NT) {
+  constexpr int TM = wh::TM;
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t total = (uint32_t)(MT * NT * a.splits * a.C);
+  const uint32_t t = xcd_swizzle(blockIdx.x, total);
+  const int cb = __builtin_amdgcn_readfirstlane((int)(t % (uint32_t)NT));  // input-channel block
+  uint32_t rest = t / (uint32_t)NT;
+  const int mt = __builtin_amdgcn_readfirstlane((int)(rest % (uint32_t)MT));
+  rest /= (uint32_t)MT;
+  const int split = __builtin_amdgcn_readfirstlane((int)(rest % (uint32_t)a.splits));
+  const int rep = replica_of(a.rmap, __builtin_amdgcn_readfirstlane((int)(rest / (uint32_t)a.splits)));
+  const int M = a.Bt * wh::IMG * wh::IMG;
+  const int p_begin = split * a.chunk;
+  const int p_end = min(M, p_begin + a.chunk);
+  const int nk = (p_end - p_begin) / wh::BK;
+  const int m0 = mt * wh::BM;
+  const bf16_t *G = reinterpret_cast<const bf16_t *>(a.g) + rep * a.g_rs;
+  const bf16_t *X = reinterpret_cast<const bf16_t *>(a.x) + rep * a.x_rs;
+  const uint32_t gbytes = (uint32_t)((int64_t)M * a.Co * 2), xbytes = (uint32_t)((int64_t)M * a.Ci * 2);
+  const bool do_bias = (cb == 0) && a.db != nullptr;
+
+  // this thread's copies: bytes q*8192 + wave*1024 + lane*16 of each region
+  const int byte0 = wave * 1024 + lane * 16;
+  const int arow = byte0 / wh::ROWA;
+  const int acol = m0 + 8 * (((byte0 % wh::ROWA) / 16) ^ swz<wh::ROWA / 16>(arow));
+  int hrel[wh::SB], hh[wh::SB];
+#pragma unroll
+  for (int q = 0; q < wh::SB; ++q) {
+    const int R = (q * wh::NTHR * 16 + byte0) / wh::ROWB, cs = (byte0 / 16) & 7;
+    const int hp = R / wh::HP, wp = R - wh::HP * hp;
+    const int c = cs ^ (2 * whsw(wp));
+    const bool in = R < wh::HROWS && wp >= 1 && wp <= wh::IMG;
+    hh[q] = in ? hp : -1;
+    hrel[q] = ((hp - 1) * wh::IMG + (wp - 1)) * a.Ci + cb * 64 + 8 * c;
+  }
+  char *stage0 = smem + wave * 1024;
+
+  // fragment read addresses (relative to a stage)
+  const int j = lane & 15, lg = lane >> 4;
+  const int wm = wave >> 2, wn = wave & 3;
+  const int frow = 8 * lg + (j >> 2);
+  const int half = (j & 3) >> 1;
+  uint32_t ra[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+    ra[i] = (uint32_t)(frow * wh::ROWA + (((2 * (wm * TM + i) + half) ^ swz<wh::ROWA / 16>(frow)) * 16) + (j & 1) * 8);
+  // input fragments of tap column s, halves rd: pixel 8 lg + 4 rd + j / 4 of
+  // the k group is image row lg / 2, column 8 (lg & 1) + 4 rd + j / 4
+  uint32_t hb[3][2];
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+#pragma unroll
+    for (int rd = 0; rd < 2; ++rd) {
+      const int wp = (lg & 1) * 8 + 4 * rd + (j >> 2) + s;
+      const int R = (lg >> 1) * wh::HP + wp;
+      hb[s][rd] = (uint32_t)(R * wh::ROWB + (((2 * wn + half) ^ (2 * whsw(wp))) * 16) + (j & 1) * 8);
+    }
+  const uint32_t lds0 = (uint32_t)(size_t)LDS_PTR(smem);
+
+  f32x4_t acc[TM][9];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int k = 0; k < 9; ++k) acc[i][k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  f32x4_t bacc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int q = 0; q < NST - 1; ++q)
+    if (q < nk)
+      wh_issue<NST>(q, stage0, G, X, gbytes, xbytes, a.Co, a.Ci, p_begin, arow, acol, hrel, hh);
+  for (int kt = 0; kt < nk; ++kt) {
+    // as in the generic kernel: own copies of tile kt have landed once only
+    // those of tiles kt+1 .. kt+NST-2 are outstanding; after the barrier all
+    // waves' copies have landed and tile kt-1's stage is free
+    if (kt + NST - 2 < nk) wait_vm<(NST - 2) * wh::CPT>();
+    else wait_vm<0>();
+    asm volatile("s_barrier" ::: "memory");
+    if (kt + NST - 1 < nk)
+      wh_issue<NST>(kt + NST - 1, stage0, G, X, gbytes, xbytes, a.Co, a.Ci, p_begin, arow, acol, hrel, hh);
+    const uint32_t st = lds0 + (uint32_t)((kt % NST) * wh::STAGE);
+    wh_kgroup<0>(acc, bacc, ra, hb, st, do_bias, wn);
+    wh_kgroup<1>(acc, bacc, ra, hb, st, do_bias, wn);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  float *dw = a.dw + split * a.dw_ss + rep * a.dw_rs;
+#pragma unroll
+  for (int tap = 0; tap < 9; ++tap) {
+    const int n = tap * a.Ci + cb * 64 + wn * 16 + j;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + (wm * TM + tm) * 16 + lg * 4 + r;
+        dw[(int64_t)m * a.nw + n] = acc[tm][tap][r];
+      }
+  }
+  if (do_bias && j == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int co = m0 + (wm * TM + wn) * 16 + lg * 4 + r;
+      a.db[split * a.db_ss + rep * a.db_rs + co] = bacc[r];
+    }
+  }
+}
+
 }  // namespace
 
 bool wgrad_lds_ok(int dtype, int Co, int Ci) {
@@ -318,10 +532,20 @@ using WgBig = Cfg<256, 256, 2, 4, 64, 2>;
 using WgMid = Cfg<128, 256, 2, 4, 64, 2>;
 using WgSmall = Cfg<64, 128, 1, 8, 64, 2>;
 
+// Halo mode applies to 16 x 16 images with output channels a multiple of 128
+// and input channels a multiple of 64 (taps from the layer input).
+constexpr int kHaloStages = 3;
+bool wgrad_halo_ok(int Co, int Ci, int H, int W, int taps) {
+  return taps == 9 && H == wh::IMG && W == wh::IMG && Co % wh::BM == 0 && Ci % 64 == 0;
+}
+
 // Tile of a layer (rows = output channels, columns of the im2col operand)
-// and how many such workgroups one CU holds (LDS-limited).
-void wgrad_lds_tile(int Co, int *bm, int *bn, int *bk, int *per_cu) {
-  if (Co > 128) {
+// and how many such workgroups one CU holds (LDS-limited; halo mode: one,
+// its 8 waves hold 144 accumulator registers per lane).
+void wgrad_lds_tile(int Co, int Ci, int H, int W, int taps, int *bm, int *bn, int *bk, int *per_cu) {
+  if (wgrad_halo_ok(Co, Ci, H, W, taps)) {
+    *bm = wh::BM; *bn = 9 * 64; *bk = wh::BK; *per_cu = 1;
+  } else if (Co > 128) {
     *bm = 256; *bn = 256; *bk = WgBig::BK; *per_cu = 160 * 1024 / WgBig::LDS_BYTES;
   } else if (Co > 64) {
     *bm = 128; *bn = 256; *bk = WgMid::BK; *per_cu = 160 * 1024 / WgMid::LDS_BYTES;
@@ -347,8 +571,23 @@ hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *labe
     attr = true;
   }
   int BM, BN, bk, per_cu;
-  wgrad_lds_tile(a.Co, &BM, &BN, &bk, &per_cu);
+  wgrad_lds_tile(a.Co, a.Ci, a.H, a.W, a.taps, &BM, &BN, &bk, &per_cu);
   if (a.chunk % bk) return hipErrorInvalidValue;
+  if (wgrad_halo_ok(a.Co, a.Ci, a.H, a.W, a.taps)) {
+    constexpr int lds = kHaloStages * wh::STAGE;
+    static bool hattr = false;
+    if (!hattr) {
+      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&wgrad_halo_kernel<kHaloStages>),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+      if (e != hipSuccess) return e;
+      hattr = true;
+    }
+    const int MT = a.Co / wh::BM, NT = a.Ci / 64;
+    if (label) *label = "conv_wgrad<bf16,128x576,w8,halo>";
+    hipLaunchKernelGGL((wgrad_halo_kernel<kHaloStages>), dim3((uint32_t)MT * NT * a.splits * a.C), dim3(wh::NTHR),
+                       lds, s, a, MT, NT);
+    return hipGetLastError();
+  }
   const int NW = a.taps == 1 ? a.Ci : 9 * a.Ci;
   const int MT = (a.Co + BM - 1) / BM, NT = (NW + BN - 1) / BN;
   const FastDiv fw = make_fastdiv(a.W), fh = make_fastdiv(a.H), fc = make_fastdiv(a.Ci);

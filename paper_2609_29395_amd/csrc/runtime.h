@@ -60,7 +60,7 @@ int wgrad_k_tile(int dtype);
 // bf16 weight gradient with LDS-direct tile copies and transposing LDS reads
 // (k_wgrad_lds.hip): usable when wgrad_lds_ok; needs chunk % 64 == 0.
 bool wgrad_lds_ok(int dtype, int Co, int Ci);
-void wgrad_lds_tile(int Co, int *bm, int *bn, int *bk, int *per_cu);
+void wgrad_lds_tile(int Co, int Ci, int H, int W, int taps, int *bm, int *bn, int *bk, int *per_cu);
 hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *label);
 // bf16 forward / dgrad with LDS-direct tile copies (k_conv_lds.hip).
 bool conv_lds_ok(int dtype, const ConvArgs &a);

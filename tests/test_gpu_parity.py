@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 import torch
 
-from gcpsl_inputs import client_stats, get_config, init_params, make_dataset
+from gcpsl_inputs import param_layout, client_stats, get_config, init_params, make_dataset
 from oracle.model import im2col3x3, round_bf16, split_forward_backward
 from oracle.sampler import active_clients, batch_indices, cluster_examples
 from oracle.train import GCPSLOracle, fuse as oracle_fuse
@@ -357,6 +357,12 @@ def test_full_size_round_sampled_replicas(name):
         gtol = tol if (flips == 0 or cfg["dtype"] == "bf16") else 5e-3
         ok, e = close(grads[n], g, gtol)
         assert ok, ("grad", n, flips, e)
+        # and each layer's weight and bias gradient on its own (a mistake in
+        # one layer's kernel cannot hide behind the others' magnitudes)
+        for li, tag, shp, off in param_layout(cfg):
+            size = int(np.prod(shp))
+            ok, e = close(grads[n][off:off + size], g[off:off + size], gtol)
+            assert ok, ("grad", li, tag, n, flips, e)
         want = o.theta[n].astype(np.float64) - cfg["lr"] * g
         ok, e = close(th[n], want, tol)
         assert ok, ("theta", n, e)
