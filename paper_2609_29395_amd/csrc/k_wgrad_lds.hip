@@ -390,15 +390,34 @@ __device__ __forceinline__ void wh_kgroup(f32x4_t (&acc)[wh::TM][9], f32x4_t &ba
   read_frag2<O + 2 * wh::FROW>(b[6], st + hb[0][0], st + hb[0][1]);
   read_frag2<O + 2 * wh::FROW>(b[7], st + hb[1][0], st + hb[1][1]);
   read_frag2<O + 2 * wh::FROW>(b[8], st + hb[2][0], st + hb[2][1]);
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  // LDS reads complete in order: the g fragments and tap row 0 are in after
+  // all but the last 12 of the 26 reads, tap row 1 after all but 6
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_waitcnt lgkmcnt(12)" ::: "memory");
 #pragma unroll
   for (int i = 0; i < wh::TM; ++i) asm volatile("" : "+v"(a[i]));
 #pragma unroll
-  for (int i = 0; i < 9; ++i) asm volatile("" : "+v"(b[i]));
+  for (int i = 0; i < 3; ++i) asm volatile("" : "+v"(b[i]));
 #pragma unroll
   for (int tm = 0; tm < wh::TM; ++tm)
 #pragma unroll
-    for (int tap = 0; tap < 9; ++tap) mma(acc[tm][tap], a[tm], b[tap]);
+    for (int tap = 0; tap < 3; ++tap) mma(acc[tm][tap], a[tm], b[tap]);
+  __builtin_amdgcn_sched_barrier(0);  // keep these MFMAs ahead of the next wait
+  asm volatile("s_waitcnt lgkmcnt(6)" ::: "memory");
+#pragma unroll
+  for (int i = 3; i < 6; ++i) asm volatile("" : "+v"(b[i]));
+#pragma unroll
+  for (int tm = 0; tm < wh::TM; ++tm)
+#pragma unroll
+    for (int tap = 3; tap < 6; ++tap) mma(acc[tm][tap], a[tm], b[tap]);
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 6; i < 9; ++i) asm volatile("" : "+v"(b[i]));
+#pragma unroll
+  for (int tm = 0; tm < wh::TM; ++tm)
+#pragma unroll
+    for (int tap = 6; tap < 9; ++tap) mma(acc[tm][tap], a[tm], b[tap]);
   if (bias) {
     const uint32_t one2 = 0x3F803F80u;  // two bf16 ones
     const u32x4 ones = u32x4{one2, one2, one2, one2};
@@ -534,7 +553,7 @@ using WgSmall = Cfg<64, 128, 1, 8, 64, 2>;
 
 // Halo mode applies to 16 x 16 images with output channels a multiple of 128
 // and input channels a multiple of 64 (taps from the layer input).
-constexpr int kHaloStages = 3;
+constexpr int kHaloStages = 2;
 bool wgrad_halo_ok(int Co, int Ci, int H, int W, int taps) {
   return taps == 9 && H == wh::IMG && W == wh::IMG && Co % wh::BM == 0 && Ci % 64 == 0;
 }

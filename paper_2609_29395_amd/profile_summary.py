@@ -45,11 +45,14 @@ def kernel_label(name: str) -> str:
         t = "bf16" if m.group(1) == "unsigned short" else "f32"
         w = int(m.group(4)) * int(m.group(5))
         return f"conv_wgrad<{t},{m.group(2)}x{m.group(3)},w{w},{'vec' if m.group(6) == 'true' else 'gather'}>"
-    m = re.search(r"conv_lds_kernel<(\d+), (\d+), (\d+), (\d+), (\d), (true|false)>", name)
+    m = re.search(r"conv_lds_kernel<(\d+), (\d+), (\d+), (\d+), (\d), (true|false)(, (true|false))?>", name)
     if m:
         kind = "conv_fwd" if m.group(5) == "0" else "conv_dgrad"
         w = int(m.group(3)) * int(m.group(4))
-        return f"{kind}<bf16,{m.group(1)}x{m.group(2)}x64,w{w},lds>"
+        mode = "halo" if m.group(8) == "true" else "lds"
+        return f"{kind}<bf16,{m.group(1)}x{m.group(2)}x64,w{w},{mode}>"
+    if re.search(r"wgrad_halo_kernel<", name):
+        return "conv_wgrad<bf16,128x576,w8,halo>"
     m = re.search(r"wgrad_lds_kernel<(\d+), (\d+), (\d+), (\d+), (?:\d+, \d+, )?(true|false)>", name)
     if m:
         w = int(m.group(3)) * int(m.group(4))
@@ -64,9 +67,9 @@ SHARED_HEADERS = ("common.h",)  # device helpers every kernel source includes
 
 def kernel_source(label: str) -> str:
     """The source file that holds the kernel a timing label names."""
-    if label.startswith("conv_wgrad<") and label.endswith(",lds>"):
+    if label.startswith("conv_wgrad<") and label.endswith((",lds>", ",halo>")):
         return "k_wgrad_lds.hip"
-    if label.startswith("conv_") and label.endswith(",lds>"):
+    if label.startswith("conv_") and label.endswith((",lds>", ",halo>")):
         return "k_conv_lds.hip"
     if label.startswith("conv_"):
         return "k_conv.hip"
@@ -150,7 +153,7 @@ def traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload, out_
     md = os.path.join(os.path.dirname(out_json), f"{workload}_traffic.md")
     lines = [f"# HBM traffic per launch, {workload}", "",
              "Commands (R = repository root; B = `python $R/bench.py --steps 5 --warmup 2 --timing-steps 2 "
-             "--no-cpu-baseline --no-schedule-control`):", "",
+             "--no-cpu-baseline --no-schedule-control --no-hbm-probes`):", "",
              "* `rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/pfetch -o run -- $B`",
              "* `rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/pwrite -o run -- $B`",
              "* `rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/cfetch -o run -- python "
