@@ -215,7 +215,10 @@ gather_im2col_fixed_kernel(const float *__restrict__ images, const int32_t *__re
           const float v = base[off[e]];
           pk.v[e] = ElemT<T>::from_f(((live >> e) & 1u) ? v : 0.f);
         }
-        *reinterpret_cast<uint4 *>(dst + (int64_t)p * KC) = __builtin_bit_cast(uint4, pk);
+        // streaming store: the rows are written once and read by the next
+        // kernel, they need no cache allocation on the way out
+        typedef unsigned U4 __attribute__((ext_vector_type(4)));
+        __builtin_nontemporal_store(__builtin_bit_cast(U4, pk), reinterpret_cast<U4 *>(dst + (int64_t)p * KC));
       }
     }
   }
