@@ -62,7 +62,12 @@ template <int BM_, int BN, int WM, int WN> struct Cfg {
   static constexpr int WNW = BN / WN;                          // wave tile width
   // epilogue: PF pixel fragments (16 * PF rows) per pass through LDS
   static constexpr int PF = NW > 8 ? 2 : 4;
-  static constexpr int EP_LD = WNW + 4;  // floats per staged epilogue row
+  // floats per staged epilogue row: 64-wide wave tiles use unpadded rows
+  // whose 16-byte chunks are XOR-ed with the row's low 3 bits (measured free
+  // of LDS bank conflicts for both the fragment writes and the 8-channel
+  // reads); narrower tiles pad rows by 4 floats
+  static constexpr bool EP_SWZ = WNW == 64;
+  static constexpr int EP_LD = EP_SWZ ? WNW : WNW + 4;
   static constexpr int EP_BYTES = NW * 16 * PF * EP_LD * 4;
   static constexpr int LDS_BYTES = 2 * STAGE > EP_BYTES ? 2 * STAGE : EP_BYTES;
   static_assert(NW == 8 || NW == 16, "8 or 16 waves");
@@ -76,10 +81,12 @@ template <int BM_, int BN, int WM, int WN> struct Cfg {
 // zero border, 18 x 18 rows of 128 bytes, and the 9 taps read their pixel
 // fragments from it at shifted rows, so a tile's pixels are copied once per
 // channel block instead of once per tap.  Row R = 18 h' + w' stores its
-// 16-byte chunk c at c ^ hswz(w'), hswz(w') = (w' >> 1) & 7: a fragment (16
-// pixels of one image row, rows R0 .. R0 + 15 for any tap) then hits every
-// bank once per row parity, and fragments of successive image rows sit a
-// constant 18 rows (2304 bytes) apart.  Two halo buffers (by channel block)
+// 16-byte chunk c at c ^ hswz(w'), hswz(w') = w' & 7: the 16-row fragment
+// reads of all three tap columns (rows R0 .. R0 + 15, R0 = 18 h' + s) are
+// then free of LDS bank conflicts (measured with the hardware counter; the
+// (w' >> 1) & 7 key cost 4 conflict cycles per read at s = 1, 2), and
+// fragments of successive image rows sit a constant 18 rows (2304 bytes)
+// apart.  Two halo buffers (by channel block)
 // and two weight stages (by k tile).
 namespace halo {
 constexpr int IMG = 16, HP = IMG + 2, ROWS = HP * HP;    // 18 x 18 rows
@@ -90,7 +97,7 @@ constexpr int B_BYTES = 256 * 128;
 constexpr int LDS_BYTES = 2 * BYTES + 2 * B_BYTES;
 static_assert(PIECES == 3 && LDS_BYTES <= 160 * 1024, "halo layout");
 }  // namespace halo
-__device__ __forceinline__ int hswz(int wp) { return (wp >> 1) & 7; }
+__device__ __forceinline__ int hswz(int wp) { return wp & 7; }
 
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 __device__ __forceinline__ int wn_of(int wave, int WN) { return wave % WN; }
@@ -443,7 +450,8 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
     for (int tm = 0; tm < PF; ++tm)
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn)
-        *reinterpret_cast<f32x4_t *>(ep + (tm * 16 + li) * CF::EP_LD + tn * 16 + lg * 4) = acc[pass * PF + tm][tn];
+        *reinterpret_cast<f32x4_t *>(ep + (tm * 16 + li) * CF::EP_LD + 4 * ((tn * 4 + lg) ^ (CF::EP_SWZ ? li & 7 : 0))) =
+            acc[pass * PF + tm][tn];
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -464,8 +472,9 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
     for (int i = 0; i < ITS; ++i) {
       const int r = lane / SEGS + RSTEP * i;  // pixel row of this pass
       const int m = m0 + wm * TM * 16 + pass * PR + r;
-      const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(ep + r * CF::EP_LD + 8 * seg);
-      const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(ep + r * CF::EP_LD + 8 * seg + 4);
+      const int esw = CF::EP_SWZ ? r & 7 : 0;
+      const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(ep + r * CF::EP_LD + 4 * ((2 * seg) ^ esw));
+      const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(ep + r * CF::EP_LD + 4 * ((2 * seg + 1) ^ esw));
       float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
       if (res) {
         const uint32_t rw[4] = {rv[i].x, rv[i].y, rv[i].z, rv[i].w};
