@@ -92,10 +92,11 @@ namespace halo {
 constexpr int IMG = 16, HP = IMG + 2, ROWS = HP * HP;    // 18 x 18 rows
 constexpr int BYTES = ((ROWS * 128 + 1023) / 1024) * 1024;  // padded to whole 1 KB wave copies
 constexpr int FSTRIDE = HP * 128;                         // bytes between image-row fragments
-constexpr int PIECES = (ROWS * 128 + 16383) / 16384;      // 16-byte copies per thread (1024 threads)
+// 16-byte copies per thread for a workgroup of NTHR threads
+template <int NTHR> constexpr int pieces() { return (ROWS * 128 + NTHR * 16 - 1) / (NTHR * 16); }
 constexpr int B_BYTES = 256 * 128;
 constexpr int LDS_BYTES = 2 * BYTES + 2 * B_BYTES;
-static_assert(PIECES == 3 && LDS_BYTES <= 160 * 1024, "halo layout");
+static_assert(pieces<1024>() == 3 && pieces<512>() == 6 && LDS_BYTES <= 160 * 1024, "halo layout");
 }  // namespace halo
 __device__ __forceinline__ int hswz(int wp) { return wp & 7; }
 
@@ -208,12 +209,13 @@ __device__ __forceinline__ void issue_tile(int kt, char *stage0, int wave, const
 // Halo mode: piece q of channel block cb's halo image into buffer cb % 2
 // (hoff: this thread's source offset within the image, -1 for the zero
 // border); the last piece covers only the first waves.
+template <int NTHR>
 __device__ __forceinline__ void issue_halo_piece(int q, int cb, char *smem, int wave, const ConvArgs &a,
                                                  const void *src, int img_off, int hoff) {
   const __amdgpu_buffer_rsrc_t rsa = rsrc(src, (uint32_t)(a.src_rs * 2));
-  if (q * 16384 + wave * 1024 < halo::BYTES) {
+  if (q * NTHR * 16 + wave * 1024 < halo::BYTES) {
     const uint32_t off = hoff >= 0 ? (uint32_t)(img_off + hoff + cb * BK) * 2u : kOob;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(smem + (cb & 1) * halo::BYTES + q * 16384 + wave * 1024),
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(smem + (cb & 1) * halo::BYTES + q * NTHR * 16 + wave * 1024),
                                              16, off, 0, 0, 0);
   }
 }
@@ -237,7 +239,7 @@ template <int BM, int BN, int WM, int WN, int EPI, bool TAPS1, bool HALO = false
 __global__ void __launch_bounds__(64 * WM * WN)
 conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
   using CF = Cfg<BM, BN, WM, WN>;
-  static_assert(!HALO || (BM == 256 && BN == 256 && WM == 4 && WN == 4 && !TAPS1), "halo mode tile");
+  static_assert(!HALO || (BM == 256 && BN == 256 && (WM == 4 || WM == 2) && WN == 4 && !TAPS1), "halo mode tile");
   constexpr int SA = CF::SA, SB = CF::SB, TM = CF::TM, TN = CF::TN, NTHR = CF::NTHR, PF = CF::PF;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -259,11 +261,12 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   uint32_t amask[SA];  // kernel taps (bit r*3+s) whose source pixel is inside the image
   // halo mode: source offset (pixel of the image x Csrc + chunk column) of
   // this thread's piece q of a halo image, -1 on the zero border
-  int hoff[halo::PIECES];
+  constexpr int PIECES = halo::pieces<NTHR>();
+  int hoff[PIECES];
   if constexpr (HALO) {
 #pragma unroll
-    for (int q = 0; q < halo::PIECES; ++q) {
-      const int g = q * 1024 + tid;  // 16-byte piece: row g / 8, physical chunk g % 8
+    for (int q = 0; q < PIECES; ++q) {
+      const int g = q * NTHR + tid;  // 16-byte piece: row g / 8, physical chunk g % 8
       const int R = g >> 3, hp = R / halo::HP, wp = R - hp * halo::HP;
       const int c = (g & 7) ^ hswz(wp);
       const bool in = R < halo::ROWS && hp >= 1 && hp <= halo::IMG && wp >= 1 && wp <= halo::IMG;
@@ -340,7 +343,7 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
 
   if constexpr (HALO) {
 #pragma unroll
-    for (int q = 0; q < halo::PIECES; ++q) issue_halo_piece(q, 0, smem, wave, a, src, img_off, hoff[q]);
+    for (int q = 0; q < PIECES; ++q) issue_halo_piece<NTHR>(q, 0, smem, wave, a, src, img_off, hoff[q]);
     issue_weights<CF>(0, smem, wave, a, wt, boff);
   } else {
     issue(0);
@@ -357,8 +360,11 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
       if (kt + 1 < nk) issue_weights<CF>(kt + 1, smem, wave, a, wt, boff);
       // the next channel block's halo in three pieces over the first three
       // taps (the buffer was last read by channel block cb - 1)
-      if (rs < halo::PIECES && cb + 1 < ncb)
-        issue_halo_piece(rs, cb + 1, smem, wave, a, src, img_off, rs == 0 ? hoff[0] : rs == 1 ? hoff[1] : hoff[2]);
+      if (rs < PIECES && cb + 1 < ncb) {
+#pragma unroll
+        for (int q = 0; q < PIECES; ++q)
+          if (q == rs) issue_halo_piece<NTHR>(q, cb + 1, smem, wave, a, src, img_off, hoff[q]);
+      }
       xst = lds0 + (uint32_t)((cb & 1) * halo::BYTES);
       wb = lds0 + (uint32_t)(2 * halo::BYTES + (kt & 1) * halo::B_BYTES);
       const int r = (rs * 11) >> 5, sc = rs - 3 * r;  // tap (r, sc)
@@ -522,6 +528,10 @@ bool conv_lds_ok(int dtype, const ConvArgs &a) {
   return dtype == GCPSL_BF16 && a.N % 8 == 0 && a.Csrc % 8 == 0 && a.Kp % BK == 0;
 }
 
+// Halo mode wave layout: kHaloWM x 4 waves on the 256 x 256 tile.
+constexpr int kHaloWM = 4;
+using HaloCfg = Cfg<256, 256, kHaloWM, 4>;
+
 // Every instantiation is named in this (non-template) function, which is
 // what makes the compiler emit the host-side launch stubs.
 hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label) {
@@ -537,10 +547,9 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   }
   static bool attr = false;
   if (!attr) {
-    constexpr int halo_lds = halo::LDS_BYTES > Cfg<256, 256, 4, 4>::EP_BYTES ? halo::LDS_BYTES
-                                                                             : Cfg<256, 256, 4, 4>::EP_BYTES;
-    for (const void *f : {reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, 4, 4, EPI_FWD, false, true>),
-                          reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, 4, 4, EPI_DGRAD, false, true>)}) {
+    constexpr int halo_lds = halo::LDS_BYTES > HaloCfg::EP_BYTES ? halo::LDS_BYTES : HaloCfg::EP_BYTES;
+    for (const void *f : {reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, kHaloWM, 4, EPI_FWD, false, true>),
+                          reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, kHaloWM, 4, EPI_DGRAD, false, true>)}) {
       const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, halo_lds);
       if (e != hipSuccess) return e;
     }
@@ -574,16 +583,16 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   const bool use_halo = bn == 256 && a.taps == 9 && a.Csrc % BK == 0 && a.H == halo::IMG && a.W == halo::IMG;
   if (label)
     *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16," + std::to_string(bm) + "x" +
-             std::to_string(bn) + "x64,w" + (bn == 256 ? "16" : "8") + (use_halo ? ",halo>" : ",lds>");
+             std::to_string(bn) + "x64,w" + (use_halo ? std::to_string(HaloCfg::NW) : bn == 256 ? "16" : "8") +
+             (use_halo ? ",halo>" : ",lds>");
   if (use_halo) {
-    constexpr int halo_lds = halo::LDS_BYTES > Cfg<256, 256, 4, 4>::EP_BYTES ? halo::LDS_BYTES
-                                                                             : Cfg<256, 256, 4, 4>::EP_BYTES;
+    constexpr int halo_lds = halo::LDS_BYTES > HaloCfg::EP_BYTES ? halo::LDS_BYTES : HaloCfg::EP_BYTES;
     if (a.epi == EPI_FWD)
-      hipLaunchKernelGGL((conv_lds_kernel<256, 256, 4, 4, EPI_FWD, false, true>), g, dim3(1024), halo_lds, s, b, fw,
-                         fh, fc, MT, NT);
+      hipLaunchKernelGGL((conv_lds_kernel<256, 256, kHaloWM, 4, EPI_FWD, false, true>), g, dim3(HaloCfg::NTHR),
+                         halo_lds, s, b, fw, fh, fc, MT, NT);
     else
-      hipLaunchKernelGGL((conv_lds_kernel<256, 256, 4, 4, EPI_DGRAD, false, true>), g, dim3(1024), halo_lds, s, b,
-                         fw, fh, fc, MT, NT);
+      hipLaunchKernelGGL((conv_lds_kernel<256, 256, kHaloWM, 4, EPI_DGRAD, false, true>), g, dim3(HaloCfg::NTHR),
+                         halo_lds, s, b, fw, fh, fc, MT, NT);
     return hipGetLastError();
   }
 #define CONV_LDS_GO(BM, BN, WM, WN, E, T)                                                                  \

@@ -249,7 +249,26 @@ prep_weights_kernel(const float *__restrict__ theta, const int32_t *__restrict__
     // forward copy: output row lb
     T *dst = reinterpret_cast<T *>(J.dst) + ((int64_t)rep * co + lb) * J.kpad;
     const float *src = w + (int64_t)lb * K;
-    for (int k = threadIdx.x; k < J.kpad; k += blockDim.x) dst[k] = ElemT<T>::from_f(k < K ? src[k] : 0.f);
+    // 8 consecutive outputs per thread: 8 independent loads (the source row
+    // need not be vector-aligned), one 16-byte store per 16 output bytes
+    // (kpad is a multiple of the 32- or 64-wide k tile, so every run is
+    // aligned and inside the row)
+    for (int k0 = threadIdx.x * 8; k0 < J.kpad; k0 += blockDim.x * 8) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = k0 + e < K ? src[k0 + e] : 0.f;
+      if constexpr (sizeof(T) == 2) {
+        uint4 o;
+        o.x = pack2_bf16(v[0], v[1]);
+        o.y = pack2_bf16(v[2], v[3]);
+        o.z = pack2_bf16(v[4], v[5]);
+        o.w = pack2_bf16(v[6], v[7]);
+        *reinterpret_cast<uint4 *>(dst + k0) = o;
+      } else {
+        *reinterpret_cast<float4 *>(dst + k0) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4 *>(dst + k0 + 4) = make_float4(v[4], v[5], v[6], v[7]);
+      }
+    }
     return;
   }
   // input-gradient copy: block (cb, ib) of tap `tap` of the flipped kernel
@@ -473,18 +492,44 @@ linear_ce_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
   float *ws = hs + (int64_t)Bt * CP;   // [L][CP]
   float *lg = ws + (int64_t)L * CP;    // [Bt][L] logits, then dlogits
   float *lossb = lg + Bt * L;          // [Bt]
+  float *bs = lossb + Bt;              // [L] bias
   const int rep = replica_of(rmap, blockIdx.x), tid = threadIdx.x, nt = blockDim.x;
   const T *hr = h + (int64_t)rep * Bt * Ch;
   const float *Wl = theta + rep * P + w_off;
   const float *bl = theta + rep * P + b_off;
-  for (int i = tid; i < Bt * Ch; i += nt) hs[(i / Ch) * CP + i % Ch] = ElemT<T>::to_f(hr[i]);
+  // staging: whole 16-byte vectors when rows hold them, several loads in
+  // flight per thread (the loop is latency-bound otherwise)
+  constexpr int V = ElemT<T>::VEC;
+  if (Ch % V == 0) {
+    const int nv = Bt * Ch / V;
+#pragma unroll 4
+    for (int i = tid; i < nv; i += nt) {
+      const uint4 u = reinterpret_cast<const uint4 *>(hr)[i];
+      const T *e = reinterpret_cast<const T *>(&u);
+      const int b = (i * V) / Ch, c = (i * V) % Ch;
+#pragma unroll
+      for (int k = 0; k < V; ++k) hs[b * CP + c + k] = ElemT<T>::to_f(e[k]);
+    }
+  } else {
+    for (int i = tid; i < Bt * Ch; i += nt) hs[(i / Ch) * CP + i % Ch] = ElemT<T>::to_f(hr[i]);
+  }
+#pragma unroll 4
   for (int i = tid; i < L * Ch; i += nt) ws[(i / Ch) * CP + i % Ch] = ElemT<T>::to_f(ElemT<T>::from_f(Wl[i]));
+  for (int j = tid; j < L; j += nt) bs[j] = bl[j];
   __syncthreads();
   for (int i = tid; i < Bt * L; i += nt) {
     const int b = i / L, j = i % L;
     const float *hb = hs + (int64_t)b * CP, *wj = ws + (int64_t)j * CP;
-    float s = bl[j];
-    for (int c = 0; c < Ch; ++c) s += hb[c] * wj[c];
+    // two partial sums over unrolled runs keep several LDS reads in flight
+    float s0 = 0.f, s1 = 0.f;
+    int c = 0;
+#pragma unroll 4
+    for (; c + 1 < Ch; c += 2) {
+      s0 += hb[c] * wj[c];
+      s1 += hb[c + 1] * wj[c + 1];
+    }
+    if (c < Ch) s0 += hb[c] * wj[c];
+    float s = bs[j] + (s0 + s1);
     lg[i] = s;
   }
   __syncthreads();
@@ -514,9 +559,15 @@ linear_ce_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
   float *g = grad + rep * P;
   for (int i = tid; i < L * Ch; i += nt) {
     const int j = i / Ch, c = i % Ch;
-    float s = 0.f;
-    for (int b = 0; b < Bt; ++b) s += lg[b * L + j] * hs[(int64_t)b * CP + c];
-    g[w_off + i] = s;
+    float s0 = 0.f, s1 = 0.f;
+    int b = 0;
+#pragma unroll 4
+    for (; b + 1 < Bt; b += 2) {
+      s0 += lg[b * L + j] * hs[(int64_t)b * CP + c];
+      s1 += lg[(b + 1) * L + j] * hs[(int64_t)(b + 1) * CP + c];
+    }
+    if (b < Bt) s0 += lg[b * L + j] * hs[(int64_t)b * CP + c];
+    g[w_off + i] = s0 + s1;
   }
   for (int j = tid; j < L; j += nt) {
     float s = 0.f;
@@ -527,6 +578,7 @@ linear_ce_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
   for (int i = tid; i < Bt * Ch; i += nt) {
     const int b = i / Ch, c = i % Ch;
     float s = 0.f;
+#pragma unroll 4
     for (int j = 0; j < L; ++j) s += lg[b * L + j] * ws[(int64_t)j * CP + c];
     dhr[i] = s;
   }

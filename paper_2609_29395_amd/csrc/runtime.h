@@ -107,7 +107,7 @@ hipError_t launch_head_pool(int dtype, const void *a, void *h, int C, const int3
 // LDS the classifier-head kernel stages (pooled features, weights, logits).
 constexpr size_t kMaxLinearLds = 160 * 1024;
 inline size_t linear_ce_lds_bytes(int Bt, int Ch, int L) {
-  return sizeof(float) * ((size_t)Bt * (Ch + 1) + (size_t)L * (Ch + 1) + (size_t)Bt * L + Bt);
+  return sizeof(float) * ((size_t)Bt * (Ch + 1) + (size_t)L * (Ch + 1) + (size_t)Bt * L + Bt + L);
 }
 hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const float *theta,
                             int64_t P, int64_t w_off, int64_t b_off, float *grad, float *dh,
