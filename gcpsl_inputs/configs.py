@@ -121,6 +121,16 @@ CONFIGS = {
                 ("conv", 64, 256, False), ("conv", 256, 256, True), ("conv", 256, 256, True),
                 ("avgpool",), ("linear", 256, 7)],
         cut=2, dtype="bf16", lr=0.05, momentum=0.9, F=2, T=4, seed=0),
+    # The same 16 x 16 residual model at a batch whose weight-gradient plan
+    # splits the pixels of each replica into many chunks (chunk boundaries
+    # inside images, a shorter last chunk).
+    "halo_split_bf16": dict(
+        K=24, C=2, B=11, L=7, N_ex=1400, H=16, W=16, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="label_l1",
+        layers=[("conv", 3, 16, False), ("conv", 16, 64, False),
+                ("conv", 64, 256, False), ("conv", 256, 256, True), ("conv", 256, 256, True),
+                ("avgpool",), ("linear", 256, 7)],
+        cut=2, dtype="bf16", lr=0.05, momentum=0.9, F=2, T=3, seed=0),
     # GroupNorm in the client segment, BatchNorm in the server segment
     # (Sec. IV-B), whose running statistics are fused with the parameters.
     "tiny_norm": dict(

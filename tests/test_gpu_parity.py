@@ -49,7 +49,7 @@ def kink_sensitive(cfg):
     gradient (0.4 % in norm, 52 % of the maximum at one element of one
     replica, propagating with shrinking size into the layers below)."""
     norm = any(sp[0] in ("bnorm", "gnorm") for sp in cfg["layers"])
-    return cfg["dtype"] == "bf16" and (norm or cfg["name"] == "halo_res_bf16")
+    return cfg["dtype"] == "bf16" and (norm or cfg["name"] in ("halo_res_bf16", "halo_split_bf16"))
 
 
 def relu_flips_are_near_kinks(act_gpu, act_ref, pre_ref, rel=1e-2):
@@ -119,7 +119,8 @@ def test_sample_and_gather_bit_exact(name, window, starts):
 # ------------------------------------------------------- multi-step runs
 
 @pytest.mark.parametrize("name", ["tiny", "tiny_jsd", "ragged", "ragged_bf16", "ragged_res_bf16", "tiny_norm",
-                                  "ragged_norm_bf16", "tiny_recipe", "ragged_recipe_bf16", "halo_res_bf16"])
+                                  "ragged_norm_bf16", "tiny_recipe", "ragged_recipe_bf16", "halo_res_bf16",
+                                  "halo_split_bf16"])
 def test_run_parity_with_fusion(name):
     cfg = get_config(name)
     T = cfg["T"]
@@ -147,7 +148,7 @@ def test_run_parity_with_fusion(name):
 
 
 @pytest.mark.parametrize("name", ["ragged", "ragged_bf16", "ragged_res_bf16", "tiny", "tiny_norm", "ragged_norm_bf16",
-                                  "tiny_recipe", "ragged_recipe_bf16", "halo_res_bf16"])
+                                  "tiny_recipe", "ragged_recipe_bf16", "halo_res_bf16", "halo_split_bf16"])
 def test_intermediates_one_round(name):
     cfg = get_config(name)
     ctx, assignment = driver.setup(cfg)
