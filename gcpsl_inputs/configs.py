@@ -131,6 +131,14 @@ CONFIGS = {
                 ("conv", 64, 256, False), ("conv", 256, 256, True), ("conv", 256, 256, True),
                 ("avgpool",), ("linear", 256, 7)],
         cut=2, dtype="bf16", lr=0.05, momentum=0.9, F=2, T=3, seed=0),
+    # 32 x 32 images with the workloads' client layers (3 -> 32 -> 64, max
+    # pool), so the image-layer convolution kernels run at small size.
+    "img32_bf16": dict(
+        K=16, C=2, B=3, L=7, N_ex=602, H=32, W=32, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="label_l1",
+        layers=[("conv", 3, 32, False), ("conv", 32, 64, False), ("maxpool",),
+                ("conv", 64, 64, False), ("avgpool",), ("linear", 64, 7)],
+        cut=3, dtype="bf16", lr=0.05, momentum=0.9, F=2, T=3, seed=0),
     # GroupNorm in the client segment, BatchNorm in the server segment
     # (Sec. IV-B), whose running statistics are fused with the parameters.
     "tiny_norm": dict(

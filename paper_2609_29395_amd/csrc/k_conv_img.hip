@@ -1,0 +1,269 @@
+// Forward and input-gradient 3x3 convolution of the 32 x 32 image layers with
+// 32 or 64 input and output channels, bf16, on gfx950 (the layers between the
+// image layer and the cut in the workloads' client segment).
+//
+//   out[p][n] = epi( sum_{tap, c} src[p + tap][c] * wt[n][tap * Cs + c] )
+//
+// These layers are bound by HBM, not by the matrix cores: per pixel they read
+// Cs and write N channels for 2 * 9 * Cs * N FLOP.  A workgroup takes eight
+// full image rows (256 pixels) and every output channel; it copies the ten
+// image rows around them with a one-pixel zero border (10 x 34 pixel rows of
+// Cs channels) and the layer's whole weight matrix into LDS once, so every
+// input pixel crosses the copy path once per workgroup instead of once per
+// tap, and computes all nine taps from LDS.  LDS holds two such workgroups
+// per CU (42, 62 or 79 KB for 32/32, 32/64 and 64/32 channels), so one
+// workgroup's copies overlap the other's MFMAs and stores.
+//
+// The MFMA takes the weights as A (16 output channels x 32 k) and the pixels
+// as B (32 k x 16 pixels), so each lane ends with 4 consecutive channels of
+// one pixel; the epilogue regroups them through LDS into whole pixel rows.  Halo row R (pixel column w'
+// of its image row) keeps its 16-byte chunk c at c ^ (w' mod chunks per
+// row); weight row n keeps chunk kc at kc ^ (n & 7) (eight-chunk groups).
+#include "runtime.h"
+
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+#define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
+
+constexpr uint32_t kOob = 0x80000000u;
+constexpr int kBufferFlags = 0x00020000;
+
+constexpr int IMG = 32;                    // image side
+constexpr int TROWS = 8;                   // image rows per workgroup tile (256 pixels)
+constexpr int HP = IMG + 2, HR = TROWS + 2;  // halo row width, halo image rows
+constexpr int HPIX = HR * HP;              // 340 halo pixels
+constexpr int NTHR = 512;                  // 8 waves: wave w computes image row w of the tile
+
+template <int CS, int NO> struct ImgCfg {
+  static constexpr int RB = CS * 2;                              // bytes per halo pixel row
+  static constexpr int CPR = RB / 16;                            // 16-byte chunks per halo row
+  static constexpr int H_BYTES = ((HPIX * RB + 1023) / 1024) * 1024;
+  static constexpr int KP = ((9 * CS + 63) / 64) * 64;           // weight row length (elements)
+  static constexpr int WCH = KP / 8;                             // 16-byte chunks per weight row
+  static constexpr int W_BYTES = NO * KP * 2;
+  static constexpr int LDS = H_BYTES + W_BYTES;
+  static constexpr int HQ = (H_BYTES + NTHR * 16 - 1) / (NTHR * 16);  // halo copies per thread
+  static constexpr int WQ = (W_BYTES + NTHR * 16 - 1) / (NTHR * 16);  // weight copies per thread
+  static constexpr int TN = NO / 16;                             // output-channel fragments
+  static constexpr int KG = CS / 32;                             // 32-channel k groups per tap
+  static_assert(CS == 32 || CS == 64, "input channels");
+  static_assert(NO == 32 || NO == 64, "output channels");
+  static_assert(W_BYTES % 1024 == 0 && WCH % 8 == 0, "weight rows in whole 1 KB copies, 8-chunk groups");
+  static constexpr bool FITS2 = 2 * LDS <= 160 * 1024;  // two workgroups per CU
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) {
+  const uint64_t p = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)p);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
+  void *q = reinterpret_cast<void *>(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(q, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes), kBufferFlags);
+}
+
+__device__ __forceinline__ void mma(f32x4_t &acc, const u32x4 &a, const u32x4 &b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ float bf2f(uint32_t bits16) { return bf16_to_f32((bf16_t)bits16); }
+
+template <int CS, int NO, int EPI>
+__global__ void __launch_bounds__(NTHR)
+conv_img_kernel(ConvArgs a, int MT) {
+  using CF = ImgCfg<CS, NO>;
+  constexpr int TN = CF::TN, KG = CF::KG;
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t t = xcd_swizzle(blockIdx.x, (uint32_t)(MT * a.C));
+  const int mt = __builtin_amdgcn_readfirstlane((int)(t % (uint32_t)MT));
+  const int rep = replica_of(a.rmap, __builtin_amdgcn_readfirstlane((int)(t / (uint32_t)MT)));
+  const int M = a.Bt * IMG * IMG;
+  const int m0 = mt * (TROWS * IMG);         // first pixel of the tile
+  const int h0 = (m0 / IMG) % IMG;           // its image row (a multiple of 8)
+  const bf16_t *src = reinterpret_cast<const bf16_t *>(a.src) + rep * a.src_rs;
+  const bf16_t *wt = reinterpret_cast<const bf16_t *>(a.wt) + rep * a.wt_rs;
+
+  // ---- copies: halo image and weight matrix, 16 bytes per lane, LDS-direct
+  {
+    const __amdgpu_buffer_rsrc_t rss = rsrc(src, (uint32_t)((int64_t)M * CS * 2));
+    const __amdgpu_buffer_rsrc_t rsw = rsrc(wt, (uint32_t)CF::W_BYTES);
+#pragma unroll
+    for (int q = 0; q < CF::HQ; ++q) {
+      const int byte = q * NTHR * 16 + wave * 1024;  // this wave's 1 KB of the halo region
+      if (byte < CF::H_BYTES) {
+        const int j = byte / 16 + lane;  // 16-byte slot
+        const int R = j / CF::CPR, cs = j % CF::CPR;
+        const int hp = R / HP, wp = R - hp * HP;
+        const int c = cs ^ (wp & (CF::CPR - 1));
+        const int h = h0 - 1 + hp, w = wp - 1;
+        const bool ok = R < HPIX && (unsigned)h < (unsigned)IMG && (unsigned)w < (unsigned)IMG;
+        const uint32_t off = ok ? (uint32_t)((m0 + (hp - 1) * IMG + w) * CS + 8 * c) * 2u : kOob;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rss, LDS_PTR(smem + byte), 16, off, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < CF::WQ; ++q) {
+      const int byte = q * NTHR * 16 + wave * 1024;
+      if (byte < CF::W_BYTES) {
+        const int j = byte / 16 + lane;
+        const int row = j / CF::WCH, cs = j % CF::WCH;
+        const int kc = cs ^ (row & 7);
+        const uint32_t off = (uint32_t)(row * CF::KP + 8 * kc) * 2u;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsw, LDS_PTR(smem + CF::H_BYTES + byte), 16, off, 0, 0, 0);
+      }
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+
+  // ---- nine taps x KG k groups from LDS: wave = image row `wave` of the tile
+  const int li = lane & 15, lg = lane >> 4;
+  const uint32_t lds0 = (uint32_t)(size_t)LDS_PTR(smem);
+  f32x4_t acc[2][TN];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int k = 0; k < TN; ++k) acc[i][k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int tap = 0; tap < 9; ++tap) {
+    const int r = tap / 3, s = tap % 3;
+#pragma unroll
+    for (int g = 0; g < KG; ++g) {
+      u32x4 w[TN], x[2];
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const int row = tn * 16 + li;
+        const int kc = (tap * CS + g * 32) / 8 + lg;
+        const uint32_t ad = lds0 + (uint32_t)(CF::H_BYTES + row * CF::KP * 2 + ((kc ^ (row & 7)) * 16));
+        asm volatile("ds_read_b128 %0, %1" : "=v"(w[tn]) : "v"(ad));
+      }
+#pragma unroll
+      for (int tm = 0; tm < 2; ++tm) {
+        const int wp = tm * 16 + li + s;
+        const int R = (wave + r) * HP + wp;
+        const uint32_t ad = lds0 + (uint32_t)(R * CF::RB + (((4 * g + lg) ^ (wp & (CF::CPR - 1))) * 16));
+        asm volatile("ds_read_b128 %0, %1" : "=v"(x[tm]) : "v"(ad));
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+      for (int i = 0; i < TN; ++i) asm volatile("" : "+v"(w[i]));
+#pragma unroll
+      for (int i = 0; i < 2; ++i) asm volatile("" : "+v"(x[i]));
+#pragma unroll
+      for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) mma(acc[tm][tn], w[tn], x[tm]);
+    }
+  }
+
+  // ---- epilogue: lane holds channels tn*16 + 4*lg .. +3 of pixel tm*16 + li.
+  // The wave's 32 x NO bf16 results are staged in LDS (its own 32-row
+  // region, 16-byte chunk c of pixel row p at c ^ (p mod chunks per row)) and
+  // read back as 16-byte pieces, so every store instruction writes 8 (NO=64)
+  // or 16 (NO=32) whole pixel rows, 1 KB contiguous.
+  constexpr int OCH = NO / 8;             // 16-byte chunks per output pixel row
+  constexpr int OROW = NO * 2;            // bytes per output pixel row
+  bf16_t *out = reinterpret_cast<bf16_t *>(a.out) + rep * a.out_rs;
+  const int pbase = m0 + wave * IMG;      // first pixel of this wave's image row
+  const uint32_t stg = lds0 + (uint32_t)(wave * IMG * OROW);
+  float bias[TN][4];
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      bias[tn][e] = EPI == EPI_FWD ? a.bias[rep * a.bias_rs + tn * 16 + 4 * lg + e] : 0.f;
+  __syncthreads();  // every wave is done with the halo and weight tiles
+#pragma unroll
+  for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float y = acc[tm][tn][e] + bias[tn][e];
+        v[e] = (EPI == EPI_FWD && !a.no_relu) ? fmaxf(y, 0.f) : y;
+      }
+      u32x2 o;
+      o[0] = pack2_bf16(v[0], v[1]);
+      o[1] = pack2_bf16(v[2], v[3]);
+      const int px = tm * 16 + li, c = 2 * tn + (lg >> 1);
+      const uint32_t ad = stg + (uint32_t)(px * OROW + ((c ^ (px & (OCH - 1))) * 16) + (lg & 1) * 8);
+      asm volatile("ds_write_b64 %0, %1" ::"v"(ad), "v"(o) : "memory");
+    }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_wave_barrier();
+  // dgrad: ReLU mask of the layer below (value > 0), read in the same
+  // 16-byte pieces; without a mask source every value passes
+  const bf16_t *msk = (EPI == EPI_DGRAD && a.mask) ? reinterpret_cast<const bf16_t *>(a.mask) + rep * a.out_rs
+                                                   : nullptr;
+  constexpr int QN = IMG * OCH / 64;      // pieces per lane
+  u32x4 mv[QN];
+#pragma unroll
+  for (int q = 0; q < QN; ++q) {
+    const int i2 = q * 64 + lane, px = i2 / OCH, c = i2 % OCH;
+    mv[q] = msk ? *reinterpret_cast<const u32x4 *>(msk + (int64_t)(pbase + px) * NO + 8 * c)
+                : u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};
+  }
+#pragma unroll
+  for (int q = 0; q < QN; ++q) {
+    const int i2 = q * 64 + lane, px = i2 / OCH, c = i2 % OCH;
+    u32x4 v;
+    const uint32_t ad = stg + (uint32_t)(px * OROW + ((c ^ (px & (OCH - 1))) * 16));
+    asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(ad) : "memory");
+    if constexpr (EPI == EPI_DGRAD) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t mlo = mv[q][e] & 0xffffu, mhi = mv[q][e] >> 16;
+        const uint32_t keep = (bf2f(mlo) > 0.f ? 0x0000ffffu : 0u) | (bf2f(mhi) > 0.f ? 0xffff0000u : 0u);
+        v[e] &= keep;
+      }
+    }
+    *reinterpret_cast<u32x4 *>(out + (int64_t)(pbase + px) * NO + 8 * c) = v;
+  }
+}
+
+}  // namespace
+
+bool conv_img_ok(int dtype, const ConvArgs &a) {
+  return dtype == GCPSL_BF16 && a.taps == 9 && a.H == IMG && a.W == IMG && (a.Csrc == 32 || a.Csrc == 64) &&
+         (a.N == 32 || a.N == 64) && !(a.Csrc == 64 && a.N == 64) && a.res == nullptr &&
+         a.Kp == ((9 * a.Csrc + 63) / 64) * 64;
+}
+
+// Every instantiation is named in this (non-template) function.
+hipError_t launch_conv_img(const ConvArgs &a, hipStream_t s, std::string *label) {
+  if (!conv_img_ok(GCPSL_BF16, a)) return hipErrorInvalidValue;
+  const int MT = a.Bt * IMG / TROWS;  // tiles of 8 image rows per replica
+  const dim3 g((uint32_t)MT * a.C);
+  if (label)
+    *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16,256x" + std::to_string(a.N) +
+             "x" + std::to_string(9 * a.Csrc) + ",w8,img>";
+#define IMG_GO(CS, NO)                                                                                        \
+  do {                                                                                                        \
+    if (a.epi == EPI_FWD)                                                                                     \
+      hipLaunchKernelGGL((conv_img_kernel<CS, NO, EPI_FWD>), g, dim3(NTHR), (ImgCfg<CS, NO>::LDS), s, a, MT);   \
+    else                                                                                                      \
+      hipLaunchKernelGGL((conv_img_kernel<CS, NO, EPI_DGRAD>), g, dim3(NTHR), (ImgCfg<CS, NO>::LDS), s, a, MT); \
+  } while (0)
+  static_assert(ImgCfg<32, 32>::FITS2 && ImgCfg<32, 64>::FITS2 && ImgCfg<64, 32>::FITS2, "two per CU");
+  static bool attr = false;
+  if (!attr) {
+    for (const void *f : {reinterpret_cast<const void *>(&conv_img_kernel<64, 32, EPI_FWD>),
+                          reinterpret_cast<const void *>(&conv_img_kernel<64, 32, EPI_DGRAD>)}) {
+      const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, ImgCfg<64, 32>::LDS);
+      if (e != hipSuccess) return e;
+    }
+    attr = true;
+  }
+  if (a.Csrc == 32 && a.N == 32) IMG_GO(32, 32);
+  else if (a.Csrc == 32) IMG_GO(32, 64);
+  else IMG_GO(64, 32);
+#undef IMG_GO
+  return hipGetLastError();
+}

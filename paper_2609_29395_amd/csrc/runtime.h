@@ -62,6 +62,11 @@ int wgrad_k_tile(int dtype);
 bool wgrad_lds_ok(int dtype, int Co, int Ci);
 void wgrad_lds_tile(int Co, int Ci, int H, int W, int taps, int *bm, int *bn, int *bk, int *per_cu);
 hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *label);
+// bf16 forward / dgrad of 32 x 32 image layers with 32 or 64 channels
+// (k_conv_img.hip): one halo-staged 8-row tile and the whole weight matrix
+// per workgroup.
+bool conv_img_ok(int dtype, const ConvArgs &a);
+hipError_t launch_conv_img(const ConvArgs &a, hipStream_t s, std::string *label);
 // bf16 forward / dgrad with LDS-direct tile copies (k_conv_lds.hip).
 bool conv_lds_ok(int dtype, const ConvArgs &a);
 hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label);

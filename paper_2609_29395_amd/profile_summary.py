@@ -51,6 +51,10 @@ def kernel_label(name: str) -> str:
         w = int(m.group(3)) * int(m.group(4))
         mode = "halo" if m.group(8) == "true" else "lds"
         return f"{kind}<bf16,{m.group(1)}x{m.group(2)}x64,w{w},{mode}>"
+    m = re.search(r"conv_img_kernel<(\d+), (\d+), (\d)>", name)
+    if m:
+        kind = "conv_fwd" if m.group(3) == "0" else "conv_dgrad"
+        return f"{kind}<bf16,256x{m.group(2)}x{9 * int(m.group(1))},w8,img>"
     if re.search(r"wgrad_halo_kernel<", name):
         return "conv_wgrad<bf16,128x576,w8,halo>"
     m = re.search(r"wgrad_lds_kernel<(\d+), (\d+), (\d+), (\d+), (?:\d+, \d+, )?(true|false)>", name)
@@ -71,6 +75,8 @@ def kernel_source(label: str) -> str:
         return "k_wgrad_lds.hip"
     if label.startswith("conv_") and label.endswith((",lds>", ",halo>")):
         return "k_conv_lds.hip"
+    if label.startswith("conv_") and label.endswith(",img>"):
+        return "k_conv_img.hip"
     if label.startswith("conv_"):
         return "k_conv.hip"
     return "k_misc.hip"
