@@ -586,6 +586,7 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
     na.rmap = rmap;
     return na;
   };
+  bool pool_done = false;  // the max pool after the last conv was written by it
   for (int i = 0; i < n; ++i) {
     const LayerInfo &l = p.ly[i];
     const int kind = l.spec.kind;
@@ -610,10 +611,20 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
       a.rmap = rmap;
       a.epi = EPI_FWD;
       a.no_relu = l.no_relu ? 1 : 0;
+      // a stored 2 x 2 max pool right after this conv: written by the conv
+      // kernel itself where it supports that
+      pool_done = false;
+      if (i + 1 < n && p.ly[i + 1].spec.kind == GCPSL_MAXPOOL2 && p.ly[i + 1].stored && !l.no_relu) {
+        a.pool_out = ws + p.ly[i + 1].act_off;
+        a.pool_rs = p.ly[i + 1].act_rs;
+        pool_done = conv_fuses_pool(p.dtype, a);
+        if (!pool_done) a.pool_out = nullptr;
+      }
       std::string lab;
       const double M = (double)B * l.H * l.W;
       const double fl = 2.0 * C * M * l.Co * 9.0 * l.Ci;
-      const double by = (double)C * (p.esz * (M * l.Ci + (double)l.Co * 9 * l.Ci + M * l.Co * (a.res ? 2 : 1)) + 4.0 * l.Co);
+      const double by = (double)C * (p.esz * (M * l.Ci + (double)l.Co * 9 * l.Ci + M * l.Co * (a.res ? 2 : 1) +
+                                                (pool_done ? M / 4 * l.Co : 0.0)) + 4.0 * l.Co);
       size_t t_ = tbegin(ctx, s);
       LAUNCH(launch_conv(p.dtype, a, s, &lab));
       tend(ctx, s, t_, lab, fl, by);
@@ -622,6 +633,7 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
       LAUNCH_T(l.groups ? "groupnorm_fwd" : "batchnorm_fwd", 0.0, by, launch_norm_fwd(p.dtype, norm_args(i), s));
     } else if (kind == GCPSL_MAXPOOL2) {
       if (!l.stored) continue;  // fused into the head
+      if (pool_done) continue;  // written by the conv before it
       LAUNCH_T("maxpool_fwd", 0.0, 1.25 * p.esz * (double)C * B * l.H * l.W * l.Ci,
                launch_maxpool_fwd(p.dtype, input_of(i), ws + l.act_off, C, rmap, B, l.H, l.W, l.Ci, s));
     } else if (kind == GCPSL_AVGPOOL) {

@@ -16,7 +16,9 @@
 //
 // The MFMA takes the weights as A (16 output channels x 32 k) and the pixels
 // as B (32 k x 16 pixels), so each lane ends with 4 consecutive channels of
-// one pixel; the epilogue regroups them through LDS into whole pixel rows.  Halo row R (pixel column w'
+// one pixel; the epilogue regroups them through LDS into whole pixel rows
+// and, when the layer is followed by a 2 x 2 max pool, also writes the
+// pooled rows (a tile's eight image rows hold four whole pooling rows).  Halo row R (pixel column w'
 // of its image row) keeps its 16-byte chunk c at c ^ (w' mod chunks per
 // row); weight row n keeps chunk kc at kc ^ (n & 7) (eight-chunk groups).
 #include "runtime.h"
@@ -196,8 +198,8 @@ conv_img_kernel(ConvArgs a, int MT) {
       const uint32_t ad = stg + (uint32_t)(px * OROW + ((c ^ (px & (OCH - 1))) * 16) + (lg & 1) * 8);
       asm volatile("ds_write_b64 %0, %1" ::"v"(ad), "v"(o) : "memory");
     }
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  __builtin_amdgcn_wave_barrier();
+  // (the max pool reads the neighbouring wave's row too)
+  __syncthreads();
   // dgrad: ReLU mask of the layer below (value > 0), read in the same
   // 16-byte pieces; without a mask source every value passes
   const bf16_t *msk = (EPI == EPI_DGRAD && a.mask) ? reinterpret_cast<const bf16_t *>(a.mask) + rep * a.out_rs
@@ -226,9 +228,42 @@ conv_img_kernel(ConvArgs a, int MT) {
     }
     *reinterpret_cast<u32x4 *>(out + (int64_t)(pbase + px) * NO + 8 * c) = v;
   }
+  if (EPI == EPI_FWD && a.pool_out) {
+    // 2 x 2 max pool: waves 2k and 2k+1 hold image rows h0+2k, h0+2k+1; each
+    // takes 8 of the 16 pooled pixels of pooled row h0/2 + k, one 16-byte
+    // channel chunk per lane (the maximum of bf16 values is exact)
+    const int pw = (wave & 1) * 8 + lane / OCH, c = lane % OCH;
+    if (lane < 8 * OCH) {
+      const uint32_t r0 = lds0 + (uint32_t)((wave & ~1) * IMG * OROW), r1 = r0 + (uint32_t)(IMG * OROW);
+      u32x4 q4[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int px = 2 * pw + (e & 1);
+        const uint32_t ad = ((e >> 1) ? r1 : r0) + (uint32_t)(px * OROW + ((c ^ (px & (OCH - 1))) * 16));
+        asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(q4[e]) : "v"(ad) : "memory");
+      }
+      u32x4 z;
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        uint32_t lo = q4[0][d] & 0xffffu, hi = q4[0][d] >> 16;
+#pragma unroll
+        for (int e = 1; e < 4; ++e) {
+          const uint32_t l2 = q4[e][d] & 0xffffu, h2 = q4[e][d] >> 16;
+          if (bf2f(l2) > bf2f(lo)) lo = l2;
+          if (bf2f(h2) > bf2f(hi)) hi = h2;
+        }
+        z[d] = lo | (hi << 16);
+      }
+      bf16_t *zo = reinterpret_cast<bf16_t *>(a.pool_out) + rep * a.pool_rs;
+      const int b = m0 / (IMG * IMG), hz = h0 / 2 + (wave >> 1);
+      *reinterpret_cast<u32x4 *>(zo + ((int64_t)(b * (IMG / 2) + hz) * (IMG / 2) + pw) * NO + 8 * c) = z;
+    }
+  }
 }
 
 }  // namespace
+
+bool conv_fuses_pool(int dtype, const ConvArgs &a) { return a.epi == EPI_FWD && conv_img_ok(dtype, a); }
 
 bool conv_img_ok(int dtype, const ConvArgs &a) {
   return dtype == GCPSL_BF16 && a.taps == 9 && a.H == IMG && a.W == IMG && (a.Csrc == 32 || a.Csrc == 64) &&

@@ -35,6 +35,9 @@ struct ConvArgs {
   int taps;  // 9: 3x3 implicit GEMM; 1: src already holds im2col rows, A[m][k] = src[m][k]
   int res_lds;  // set by the launcher: the residual (== src) is taken from the staged centre tap
   int no_relu;  // fwd: store the raw output (a norm layer follows)
+  void *pool_out;      // fwd: also the 2x2 max pool of the output [C][Bt][H/2][W/2][N] (kernels that
+                       // report conv_fuses_pool), else null
+  int64_t pool_rs;     // its per-replica stride (elements)
 };
 
 // Weight gradient: dW[co][kk] = sum_p G[p][co] X(p, kk), kk = (r, s, ci),
@@ -66,6 +69,8 @@ hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *labe
 // (k_conv_img.hip): one halo-staged 8-row tile and the whole weight matrix
 // per workgroup.
 bool conv_img_ok(int dtype, const ConvArgs &a);
+// whether launch_conv also writes ConvArgs::pool_out for this layer
+bool conv_fuses_pool(int dtype, const ConvArgs &a);
 hipError_t launch_conv_img(const ConvArgs &a, hipStream_t s, std::string *label);
 // bf16 forward / dgrad with LDS-direct tile copies (k_conv_lds.hip).
 bool conv_lds_ok(int dtype, const ConvArgs &a);
