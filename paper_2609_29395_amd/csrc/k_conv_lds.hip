@@ -450,6 +450,20 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   const bf16_t *msk = a.mask ? reinterpret_cast<const bf16_t *>(a.mask) + rep * a.out_rs : nullptr;
   const __amdgpu_buffer_rsrc_t rsr = rsrc(res ? res : out, (uint32_t)(a.out_rs * 2));
   const __amdgpu_buffer_rsrc_t rsm = rsrc(msk ? msk : out, (uint32_t)(a.out_rs * 2));
+  // dgrad: the mask loads of every pass are issued up front, so their HBM
+  // latency is paid once per tile instead of once per pass
+  uint4 mvall[TM / PF][ITS];
+  if constexpr (EPI == EPI_DGRAD) {
+#pragma unroll
+    for (int pass = 0; pass < TM / PF; ++pass)
+#pragma unroll
+      for (int i = 0; i < ITS; ++i) {
+        const int m = m0 + wm * TM * 16 + pass * PR + lane / SEGS + RSTEP * i;
+        const uint32_t off = (nok && m < M) ? (uint32_t)((int64_t)m * a.N + n) * 2u : kOob;
+        mvall[pass][i] = msk ? __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsm, off, 0, 0))
+                             : make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
+      }
+  }
 #pragma unroll
   for (int pass = 0; pass < TM / PF; ++pass) {
 #pragma unroll
@@ -461,18 +475,15 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // every residual and mask load of the pass is issued before any is
-    // used; rows past M (and channels past N) read zero and store nothing
-    uint4 rv[ITS], mv[ITS];
+    // every residual load of the pass is issued before any is used; rows
+    // past M (and channels past N) read zero and store nothing
+    uint4 rv[ITS];
 #pragma unroll
     for (int i = 0; i < ITS; ++i) {
       const int m = m0 + wm * TM * 16 + pass * PR + lane / SEGS + RSTEP * i;
       const uint32_t off = (nok && m < M) ? (uint32_t)((int64_t)m * a.N + n) * 2u : kOob;
       rv[i] = res ? __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsr, off, 0, 0))
                   : make_uint4(0, 0, 0, 0);
-      if constexpr (EPI == EPI_DGRAD)
-        mv[i] = msk ? __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsm, off, 0, 0))
-                    : make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
     }
 #pragma unroll
     for (int i = 0; i < ITS; ++i) {
@@ -495,7 +506,7 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
         for (int e = 0; e < 8; ++e) v[e] = a.no_relu ? v[e] + bias[e] : fmaxf(v[e] + bias[e], 0.f);
       } else {
         // without a mask source every value passes (ones)
-        const uint32_t mw[4] = {mv[i].x, mv[i].y, mv[i].z, mv[i].w};
+        const uint32_t mw[4] = {mvall[pass][i].x, mvall[pass][i].y, mvall[pass][i].z, mvall[pass][i].w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           if (!(bf2f(mw[e] & 0xffffu) > 0.f)) v[2 * e] = 0.f;
