@@ -270,7 +270,7 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
         const int64_t slots = 256 * (int64_t)per_cu;
         int64_t best = -1;
         splits = 1;
-        for (int sp = 1; sp <= std::min(16, nkt); ++sp) {
+        for (int sp = 1; sp <= std::min(64, nkt); ++sp) {
           const int64_t rounds = (tiles * sp + slots - 1) / slots;
           const int64_t cost = rounds * ((nkt + sp - 1) / sp + (sp > 1 ? 16 : 0));
           if (best < 0 || cost < best) best = cost, splits = sp;

@@ -537,6 +537,181 @@ wgrad_halo_kernel(WgradArgs a, int MT, int NT) {
   }
 }
 
+// ------------------------------------------------- image-side client layer
+// 32 x 32 images, 64 output and 32 input channels (the layer between the
+// image layer and the cut).  A workgroup owns the whole 64 x 288 gradient
+// (nine taps x 32 input channels) for its pixel chunk: 8 waves, wave (wm, wn)
+// takes output channels 16 wm .. 16 wm + 15 and column fragments 9 wn ..
+// 9 wn + 8 (fragment f = tap * 2 + 16-channel block), 36 accumulator registers
+// per lane.  A k tile is 64 pixels = two image rows; the input rows all taps
+// need (four image rows with a zero border, 4 x 34 pixel rows of 64 bytes)
+// are copied once, next to the 64 x 64 g tile.  Halo row R (column w') keeps
+// its 16-byte chunk c at c ^ wisw(w').
+namespace wi {
+constexpr int IMG = 32, HP = 34, TR = 2;    // image side, halo row width, image rows per k tile
+constexpr int BK = IMG * TR;                // 64 pixels per k tile
+constexpr int HROWS = (TR + 2) * HP;        // 136 halo rows
+constexpr int CI = 32, CO = 64;             // input and output channels
+constexpr int ROWB = CI * 2;                // 64 bytes per halo row
+constexpr int ROWA = CO * 2;                // 128 bytes per g row
+constexpr int NTHR = 512;
+constexpr int A_BYTES = BK * ROWA;          // 8 KB
+constexpr int B_BYTES = 16384;              // 136 halo rows (8.5 KB); the rest takes idle lanes' zero copies
+constexpr int STAGE = A_BYTES + B_BYTES;
+constexpr int SA = A_BYTES / (NTHR * 16), SB = B_BYTES / (NTHR * 16), CPT = SA + SB;
+constexpr int QROWA = NTHR * 16 / ROWA;     // g rows between a thread's copies
+constexpr int FROW = HP * ROWB;             // bytes between halo image rows
+constexpr int NF = 9;                       // column fragments per wave
+static_assert(HROWS * ROWB <= B_BYTES && SA == 1 && SB == 2 && QROWA % 16 == 0, "image weight-gradient layout");
+}  // namespace wi
+__device__ __forceinline__ int wisw(int wp) { return (wp >> 1) & 3; }
+
+template <int NST>
+__device__ __forceinline__ void wi_issue(int kt, char *stage0, const void *G, const void *X, uint32_t gbytes,
+                                         uint32_t xbytes, int p_begin, int arow, int acol, const int (&hrel)[wi::SB],
+                                         const int (&hh)[wi::SB]) {
+  const __amdgpu_buffer_rsrc_t rsg = rsrc(G, gbytes);
+  const __amdgpu_buffer_rsrc_t rsx = rsrc(X, xbytes);
+  char *sa = stage0 + (kt % NST) * wi::STAGE;
+  const int pt = p_begin + kt * wi::BK;
+#pragma unroll
+  for (int q = 0; q < wi::SA; ++q) {
+    const uint32_t off = ((uint32_t)(pt + arow + q * wi::QROWA) * (uint32_t)wi::CO + (uint32_t)acol) * 2u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsg, LDS_PTR(sa + q * wi::NTHR * 16), 16, off, 0, 0, 0);
+  }
+  const int h0 = (pt / wi::IMG) % wi::IMG;  // first image row of the tile
+#pragma unroll
+  for (int q = 0; q < wi::SB; ++q) {
+    const bool ok = hh[q] >= 0 && (unsigned)(h0 - 1 + hh[q]) < (unsigned)wi::IMG;
+    const uint32_t off = ok ? (uint32_t)(pt * wi::CI + hrel[q]) * 2u : kOob;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, LDS_PTR(sa + wi::A_BYTES + q * wi::NTHR * 16), 16, off, 0, 0, 0);
+  }
+}
+
+// k group KG (image row KG of the tile): one g fragment, nine input
+// fragments, nine MFMAs (+1 against ones for the bias gradient).
+template <int KG>
+__device__ __forceinline__ void wi_kgroup(f32x4_t (&acc)[wi::NF], f32x4_t &bacc, uint32_t ra,
+                                          const uint32_t (&hb)[3][2][2], uint32_t st, bool bias, int wn) {
+  u32x4 a, b[wi::NF];
+  read_frag<KG * 32 * wi::ROWA, wi::ROWA>(a, st + ra);
+  // fragment f = 9 wn + i: tap t = f / 2 (r = t / 3, s = t % 3), block f % 2
+#pragma unroll
+  for (int i = 0; i < wi::NF; ++i) {
+    const int f0 = i, f1 = 9 + i;  // the wave's fragment for wn = 0 / 1
+    const int t0 = f0 / 2, t1 = f1 / 2;
+    // both choices are compile-time constants; wn selects one at run time
+    const uint32_t s0 = st + hb[t0 % 3][f0 % 2][0], s1 = st + hb[t1 % 3][f1 % 2][0];
+    const uint32_t e0 = st + hb[t0 % 3][f0 % 2][1], e1 = st + hb[t1 % 3][f1 % 2][1];
+    const uint32_t lo = wn ? s1 : s0, hi = wn ? e1 : e0;
+    const int r = wn ? t1 / 3 : t0 / 3;
+    const uint32_t ro = (uint32_t)(r * wi::FROW);
+    u32x2 l2, h2;
+    asm volatile("ds_read_b64_tr_b16 %0, %2 offset:%4\n\tds_read_b64_tr_b16 %1, %3 offset:%4"
+                 : "=&v"(l2), "=&v"(h2)
+                 : "v"(lo + ro), "v"(hi + ro), "n"(wi::A_BYTES + KG * wi::FROW));
+    b[i] = __builtin_shufflevector(l2, h2, 0, 1, 2, 3);
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  asm volatile("" : "+v"(a));
+#pragma unroll
+  for (int i = 0; i < wi::NF; ++i) asm volatile("" : "+v"(b[i]));
+#pragma unroll
+  for (int i = 0; i < wi::NF; ++i) mma(acc[i], a, b[i]);
+  if (bias) {
+    const uint32_t one2 = 0x3F803F80u;  // two bf16 ones
+    mma(bacc, a, u32x4{one2, one2, one2, one2});
+  }
+}
+
+template <int NST>
+__global__ void __launch_bounds__(wi::NTHR)
+wgrad_img_kernel(WgradArgs a) {
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t total = (uint32_t)(a.splits * a.C);
+  const uint32_t t = xcd_swizzle(blockIdx.x, total);
+  const int split = __builtin_amdgcn_readfirstlane((int)(t % (uint32_t)a.splits));
+  const int rep = replica_of(a.rmap, __builtin_amdgcn_readfirstlane((int)(t / (uint32_t)a.splits)));
+  const int M = a.Bt * wi::IMG * wi::IMG;
+  const int p_begin = split * a.chunk;
+  const int p_end = min(M, p_begin + a.chunk);
+  const int nk = (p_end - p_begin) / wi::BK;
+  const bf16_t *G = reinterpret_cast<const bf16_t *>(a.g) + rep * a.g_rs;
+  const bf16_t *X = reinterpret_cast<const bf16_t *>(a.x) + rep * a.x_rs;
+  const uint32_t gbytes = (uint32_t)((int64_t)M * wi::CO * 2), xbytes = (uint32_t)((int64_t)M * wi::CI * 2);
+  const int wm = wave >> 1, wn = wave & 1;
+  const bool do_bias = wn == 0 && a.db != nullptr;
+
+  // this thread's copies: bytes q*8192 + wave*1024 + lane*16 of each region
+  const int byte0 = wave * 1024 + lane * 16;
+  const int arow = byte0 / wi::ROWA;
+  const int acol = 8 * (((byte0 % wi::ROWA) / 16) ^ swz<wi::ROWA / 16>(arow));
+  int hrel[wi::SB], hh[wi::SB];
+#pragma unroll
+  for (int q = 0; q < wi::SB; ++q) {
+    const int R = (q * wi::NTHR * 16 + byte0) / wi::ROWB, cs = (byte0 / 16) & 3;
+    const int hp = R / wi::HP, wp = R - wi::HP * hp;
+    const int c = cs ^ wisw(wp);
+    const bool in = R < wi::HROWS && wp >= 1 && wp <= wi::IMG;
+    hh[q] = in ? hp : -1;
+    hrel[q] = ((hp - 1) * wi::IMG + (wp - 1)) * wi::CI + 8 * c;
+  }
+  char *stage0 = smem + wave * 1024;
+
+  // fragment read addresses (relative to a stage): g fragment of output
+  // channels 16 wm.., input fragment halves of tap column s, channel block cb
+  const int j = lane & 15, lg = lane >> 4;
+  const int frow = 8 * lg + (j >> 2);
+  const int half = (j & 3) >> 1;
+  const uint32_t ra = (uint32_t)(frow * wi::ROWA + (((2 * wm + half) ^ swz<wi::ROWA / 16>(frow)) * 16) + (j & 1) * 8);
+  uint32_t hb[3][2][2];
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+      for (int rd = 0; rd < 2; ++rd) {
+        const int wp = 8 * lg + 4 * rd + (j >> 2) + s;
+        hb[s][cb][rd] = (uint32_t)(wp * wi::ROWB + (((2 * cb + half) ^ wisw(wp)) * 16) + (j & 1) * 8);
+      }
+  const uint32_t lds0 = (uint32_t)(size_t)LDS_PTR(smem);
+
+  f32x4_t acc[wi::NF];
+#pragma unroll
+  for (int i = 0; i < wi::NF; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  f32x4_t bacc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int q = 0; q < NST - 1; ++q)
+    if (q < nk) wi_issue<NST>(q, stage0, G, X, gbytes, xbytes, p_begin, arow, acol, hrel, hh);
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + NST - 2 < nk) wait_vm<(NST - 2) * wi::CPT>();
+    else wait_vm<0>();
+    asm volatile("s_barrier" ::: "memory");
+    if (kt + NST - 1 < nk) wi_issue<NST>(kt + NST - 1, stage0, G, X, gbytes, xbytes, p_begin, arow, acol, hrel, hh);
+    const uint32_t st = lds0 + (uint32_t)((kt % NST) * wi::STAGE);
+    wi_kgroup<0>(acc, bacc, ra, hb, st, do_bias, wn);
+    wi_kgroup<1>(acc, bacc, ra, hb, st, do_bias, wn);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  // column of fragment f, lane j: (tap, channel) = (f / 2, 16 (f % 2) + j),
+  // i.e. 16 f + j of the 288
+  float *dw = a.dw + split * a.dw_ss + rep * a.dw_rs;
+#pragma unroll
+  for (int i = 0; i < wi::NF; ++i) {
+    const int n = 16 * (9 * wn + i) + j;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) dw[(int64_t)(wm * 16 + lg * 4 + r) * a.nw + n] = acc[i][r];
+  }
+  if (do_bias && j == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) a.db[split * a.db_ss + rep * a.db_rs + wm * 16 + lg * 4 + r] = bacc[r];
+  }
+}
+
 }  // namespace
 
 bool wgrad_lds_ok(int dtype, int Co, int Ci) {
@@ -554,6 +729,12 @@ using WgSmall = Cfg<64, 128, 1, 8, 64, 2>;
 // Halo mode applies to 16 x 16 images with output channels a multiple of 128
 // and input channels a multiple of 64 (taps from the layer input).
 constexpr int kHaloStages = 2;
+// The image-side client layer: 32 x 32 images, 64 output, 32 input channels.
+constexpr int kImgStages = 3;
+bool wgrad_img_ok(int Co, int Ci, int H, int W, int taps) {
+  return taps == 9 && H == wi::IMG && W == wi::IMG && Co == wi::CO && Ci == wi::CI;
+}
+
 bool wgrad_halo_ok(int Co, int Ci, int H, int W, int taps) {
   return taps == 9 && H == wh::IMG && W == wh::IMG && Co % wh::BM == 0 && Ci % 64 == 0;
 }
@@ -564,6 +745,8 @@ bool wgrad_halo_ok(int Co, int Ci, int H, int W, int taps) {
 void wgrad_lds_tile(int Co, int Ci, int H, int W, int taps, int *bm, int *bn, int *bk, int *per_cu) {
   if (wgrad_halo_ok(Co, Ci, H, W, taps)) {
     *bm = wh::BM; *bn = 9 * 64; *bk = wh::BK; *per_cu = 1;
+  } else if (wgrad_img_ok(Co, Ci, H, W, taps)) {
+    *bm = wi::CO; *bn = 9 * wi::CI; *bk = wi::BK; *per_cu = 160 * 1024 / (kImgStages * wi::STAGE);
   } else if (Co > 128) {
     *bm = 256; *bn = 256; *bk = WgBig::BK; *per_cu = 160 * 1024 / WgBig::LDS_BYTES;
   } else if (Co > 64) {
@@ -592,6 +775,19 @@ hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *labe
   int BM, BN, bk, per_cu;
   wgrad_lds_tile(a.Co, a.Ci, a.H, a.W, a.taps, &BM, &BN, &bk, &per_cu);
   if (a.chunk % bk) return hipErrorInvalidValue;
+  if (wgrad_img_ok(a.Co, a.Ci, a.H, a.W, a.taps)) {
+    constexpr int lds = kImgStages * wi::STAGE;
+    static bool iattr = false;
+    if (!iattr) {
+      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&wgrad_img_kernel<kImgStages>),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+      if (e != hipSuccess) return e;
+      iattr = true;
+    }
+    if (label) *label = "conv_wgrad<bf16,64x288,w8,img>";
+    hipLaunchKernelGGL((wgrad_img_kernel<kImgStages>), dim3((uint32_t)a.splits * a.C), dim3(wi::NTHR), lds, s, a);
+    return hipGetLastError();
+  }
   if (wgrad_halo_ok(a.Co, a.Ci, a.H, a.W, a.taps)) {
     constexpr int lds = kHaloStages * wh::STAGE;
     static bool hattr = false;
