@@ -646,6 +646,41 @@ __device__ __forceinline__ float ordered_sum(const float *__restrict__ p, int64_
   return s;
 }
 
+// Two consecutive weights per thread (every offset and stride even, so the
+// 8-byte accesses stay aligned); same order of additions as ordered_sum.
+__device__ __forceinline__ float2 ordered_sum2(const float *__restrict__ p, int64_t stride, int splits) {
+  float2 s = make_float2(0.f, 0.f);
+  int k = 0;
+  for (; k + 8 <= splits; k += 8) {
+    float2 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = *reinterpret_cast<const float2 *>(p + (k + u) * stride);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s.x += v[u].x, s.y += v[u].y;
+  }
+  for (; k < splits; ++k) {
+    const float2 v = *reinterpret_cast<const float2 *>(p + k * stride);
+    s.x += v.x, s.y += v.y;
+  }
+  return s;
+}
+
+__global__ void __launch_bounds__(256)
+wgrad_reduce2_kernel(const float *__restrict__ dw, const float *__restrict__ db, int splits, int64_t dw_ss,
+                     int64_t dw_rs, int64_t db_ss, int64_t db_rs, float *__restrict__ grad, int64_t P,
+                     int64_t w_off, int64_t b_off, int64_t nw, int co, const int32_t *__restrict__ rmap) {
+  const int rep = replica_of(rmap, blockIdx.y);
+  const int64_t n2 = (nw + co) / 2;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n2; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t j = 2 * i;
+    if (j < nw)
+      *reinterpret_cast<float2 *>(grad + rep * P + w_off + j) = ordered_sum2(dw + rep * dw_rs + j, dw_ss, splits);
+    else
+      *reinterpret_cast<float2 *>(grad + rep * P + b_off + (j - nw)) =
+          ordered_sum2(db + rep * db_rs + (j - nw), db_ss, splits);
+  }
+}
+
 __global__ void __launch_bounds__(256)
 wgrad_reduce_kernel(const float *__restrict__ dw, const float *__restrict__ db, int splits,
                     int64_t dw_ss, int64_t dw_rs, int64_t db_ss, int64_t db_rs,
@@ -934,8 +969,15 @@ hipError_t launch_wgrad_reduce(const float *dw, const float *db, int splits, int
                                int64_t dw_rs, int64_t db_ss, int64_t db_rs, float *grad, int64_t P,
                                int64_t w_off, int64_t b_off, int64_t nw, int co, int C, const int32_t *rmap,
                                hipStream_t s) {
-  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(grid_for(nw + co, 256, 4096), C), dim3(256), 0, s, dw,
-                     db, splits, dw_ss, dw_rs, db_ss, db_rs, grad, P, w_off, b_off, nw, co, rmap);
+  const bool even = ((P | w_off | b_off | nw | co | dw_ss | dw_rs | db_ss | db_rs) & 1) == 0 &&
+                    ((reinterpret_cast<uintptr_t>(dw) | reinterpret_cast<uintptr_t>(db) |
+                      reinterpret_cast<uintptr_t>(grad)) & 7) == 0;
+  if (even)
+    hipLaunchKernelGGL(wgrad_reduce2_kernel, dim3(grid_for((nw + co) / 2, 256, 4096), C), dim3(256), 0, s, dw,
+                       db, splits, dw_ss, dw_rs, db_ss, db_rs, grad, P, w_off, b_off, nw, co, rmap);
+  else
+    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(grid_for(nw + co, 256, 4096), C), dim3(256), 0, s, dw,
+                       db, splits, dw_ss, dw_rs, db_ss, db_rs, grad, P, w_off, b_off, nw, co, rmap);
   return hipGetLastError();
 }
 
