@@ -278,14 +278,20 @@ prep_weights_kernel(const float *__restrict__ theta, const int32_t *__restrict__
   const int cb = blk % nco, ib = blk / nco;
   const int rs_src = 8 - tap;  // (2 - r') * 3 + (2 - s')
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int r = ty; r < 64; r += 4) {
-    const int o = cb * 64 + r, c = ib * 64 + tx;
-    tile[r][tx] = (o < co && c < ci) ? w[(int64_t)o * K + rs_src * ci + c] : 0.f;
+  // 16 rows per thread with every load in flight (fixed trip counts)
+  float v[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int r = ty + 4 * i, o = cb * 64 + r, c = ib * 64 + tx;
+    v[i] = (o < co && c < ci) ? w[(int64_t)o * K + rs_src * ci + c] : 0.f;
   }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) tile[ty + 4 * i][tx] = v[i];
   __syncthreads();
   T *dst = reinterpret_cast<T *>(J.dst) + (int64_t)rep * ci * Kdp;
-  for (int r = ty; r < 64; r += 4) {
-    const int c = ib * 64 + r, o = cb * 64 + tx;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int r = ty + 4 * i, c = ib * 64 + r, o = cb * 64 + tx;
     if (c < ci && o < co) dst[(int64_t)c * Kdp + tap * co + o] = ElemT<T>::from_f(tile[tx][r]);
   }
   // zero the row padding once per row (by the first tap/co block)
