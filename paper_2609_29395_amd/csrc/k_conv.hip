@@ -696,6 +696,7 @@ void wgrad_tile(int dtype, int Co, int ncols, int *bm, int *bn) {
 
 hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s, std::string *label) {
   if (conv_img_ok(dtype, a)) return launch_conv_img(a, s, label);
+  if (a.epi == EPI_FWD && conv_col_ok(dtype, a)) return launch_conv_col(a, s, label);
   if (conv_lds_ok(dtype, a)) return launch_conv_lds(a, s, label);
   if (dtype == GCPSL_BF16)
     return (a.Csrc % 8 == 0) ? pick_conv<bf16_t, true>(a, s, label) : pick_conv<bf16_t, false>(a, s, label);

@@ -261,7 +261,95 @@ conv_img_kernel(ConvArgs a, int MT) {
   }
 }
 
+// The image layer on its im2col rows (taps == 1): out[p][n] = act(bias[n] +
+// sum_k A[p][k] W[n][k]) with 32 columns per row (9 x 3 taps and channels,
+// zero-padded) and 32 output channels.  A plain stream: each wave reads four
+// groups of 16 pixel rows (1 KB each, one 16-byte piece per lane), multiplies
+// them by the weight fragments it keeps in registers (two MFMAs per group) and
+// regroups the results through LDS into whole 64-byte output rows.
+constexpr int COL_K = 32, COL_N = 32, COL_PX = 256;  // k, n, pixels per workgroup
+
+__global__ void __launch_bounds__(256)
+conv_col_kernel(ConvArgs a, int MT) {
+  __shared__ __attribute__((aligned(16))) char stg_all[4 * 64 * COL_N * 2];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t t = xcd_swizzle(blockIdx.x, (uint32_t)(MT * a.C));
+  const int mt = __builtin_amdgcn_readfirstlane((int)(t % (uint32_t)MT));
+  const int rep = replica_of(a.rmap, __builtin_amdgcn_readfirstlane((int)(t / (uint32_t)MT)));
+  const int M = a.Bt * a.H * a.W;
+  const int p0 = mt * COL_PX + wave * 64;  // this wave's 64 pixels
+  const int li = lane & 15, lg = lane >> 4;
+  const bf16_t *src = reinterpret_cast<const bf16_t *>(a.src) + rep * a.src_rs;
+  const bf16_t *wt = reinterpret_cast<const bf16_t *>(a.wt) + rep * a.wt_rs;
+  // pixel rows (B operand: lane (li, lg) = pixel li, k 8 lg .. 8 lg + 7)
+  u32x4 x[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int p = p0 + g * 16 + li;
+    x[g] = p < M ? *reinterpret_cast<const u32x4 *>(src + (int64_t)p * COL_K + 8 * lg) : u32x4{0u, 0u, 0u, 0u};
+  }
+  // weights (A operand: lane (li, lg) = output channel tn*16 + li, k 8 lg ..)
+  u32x4 w[2];
+  float bias[2][4];
+#pragma unroll
+  for (int tn = 0; tn < 2; ++tn) {
+    w[tn] = *reinterpret_cast<const u32x4 *>(wt + (int64_t)(tn * 16 + li) * a.Kp + 8 * lg);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) bias[tn][e] = a.bias[rep * a.bias_rs + tn * 16 + 4 * lg + e];
+  }
+  f32x4_t acc[4][2];
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+#pragma unroll
+    for (int tn = 0; tn < 2; ++tn) {
+      acc[g][tn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      mma(acc[g][tn], w[tn], x[g]);
+    }
+  // lane holds channels tn*16 + 4 lg .. +3 of pixel g*16 + li; stage the
+  // wave's 64 x 32 bf16 block (row p, 16-byte chunk c at c ^ (p & 3))
+  char *stg = stg_all + wave * 64 * COL_N * 2;
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+#pragma unroll
+    for (int tn = 0; tn < 2; ++tn) {
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float y = acc[g][tn][e] + bias[tn][e];
+        v[e] = a.no_relu ? y : fmaxf(y, 0.f);
+      }
+      u32x2 o;
+      o[0] = pack2_bf16(v[0], v[1]);
+      o[1] = pack2_bf16(v[2], v[3]);
+      const int px = g * 16 + li, c = 2 * tn + (lg >> 1);
+      *reinterpret_cast<u32x2 *>(stg + px * 64 + ((c ^ (px & 3)) * 16) + (lg & 1) * 8) = o;
+    }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  bf16_t *out = reinterpret_cast<bf16_t *>(a.out) + rep * a.out_rs;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int i2 = q * 64 + lane, px = i2 >> 2, c = i2 & 3;
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(stg + px * 64 + ((c ^ (px & 3)) * 16));
+    if (p0 + px < M) *reinterpret_cast<u32x4 *>(out + (int64_t)(p0 + px) * COL_N + 8 * c) = v;
+  }
+}
+
 }  // namespace
+
+bool conv_col_ok(int dtype, const ConvArgs &a) {
+  return dtype == GCPSL_BF16 && a.taps == 1 && a.Csrc == COL_K && a.N == COL_N && a.res == nullptr &&
+         a.Kp >= COL_K && a.Kp % 8 == 0 && ((int64_t)a.Bt * a.H * a.W) % COL_PX == 0;
+}
+
+hipError_t launch_conv_col(const ConvArgs &a, hipStream_t s, std::string *label) {
+  if (!conv_col_ok(GCPSL_BF16, a) || a.epi != EPI_FWD) return hipErrorInvalidValue;
+  const int MT = a.Bt * a.H * a.W / COL_PX;
+  if (label) *label = "conv_fwd<bf16,256x32x32,w4,col>";
+  hipLaunchKernelGGL(conv_col_kernel, dim3((uint32_t)MT * a.C), dim3(256), 0, s, a, MT);
+  return hipGetLastError();
+}
 
 bool conv_fuses_pool(int dtype, const ConvArgs &a) { return a.epi == EPI_FWD && conv_img_ok(dtype, a); }
 

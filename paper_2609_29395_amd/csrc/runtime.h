@@ -69,6 +69,9 @@ hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *labe
 // (k_conv_img.hip): one halo-staged 8-row tile and the whole weight matrix
 // per workgroup.
 bool conv_img_ok(int dtype, const ConvArgs &a);
+// the image layer's forward on its im2col rows (32 columns, 32 channels)
+bool conv_col_ok(int dtype, const ConvArgs &a);
+hipError_t launch_conv_col(const ConvArgs &a, hipStream_t s, std::string *label);
 // whether launch_conv also writes ConvArgs::pool_out for this layer
 bool conv_fuses_pool(int dtype, const ConvArgs &a);
 hipError_t launch_conv_img(const ConvArgs &a, hipStream_t s, std::string *label);
