@@ -254,8 +254,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
       }
       // split-K over pixels for the weight gradient
       const int M = B * l.H * l.W;
-      const int kt = wgrad_k_tile(p.dtype);
-      const int nkt = (M + kt - 1) / kt;
+      int kt = wgrad_k_tile(p.dtype);
+      int nkt = (M + kt - 1) / kt;
       int bm, bn;
       const int nwc = (i == 0 && p.col0) ? p.Kc : 9 * l.Ci;
       int splits;
@@ -266,13 +266,15 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
         int tile_bk, per_cu;
         wgrad_lds_tile(l.Co, (i == 0 && p.col0) ? p.Kc : l.Ci, l.H, l.W, (i == 0 && p.col0) ? 1 : 9, &bm, &bn,
                        &tile_bk, &per_cu);
+        kt = tile_bk;  // chunks are whole k tiles of the kernel the layer runs
+        nkt = (M + kt - 1) / kt;
         const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
         const int64_t slots = 256 * (int64_t)per_cu;
         int64_t best = -1;
         splits = 1;
         for (int sp = 1; sp <= std::min(64, nkt); ++sp) {
           const int64_t rounds = (tiles * sp + slots - 1) / slots;
-          const int64_t cost = rounds * ((nkt + sp - 1) / sp + (sp > 1 ? 16 : 0));
+          const int64_t cost = rounds * ((nkt + sp - 1) / sp + (sp > 1 ? 16 * 64 / kt : 0));
           if (best < 0 || cost < best) best = cost, splits = sp;
         }
       } else {

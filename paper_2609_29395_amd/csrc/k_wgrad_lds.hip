@@ -308,31 +308,32 @@ wgrad_lds_kernel(WgradArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, 
 // 16 x 16 images, output channels a multiple of 128, input channels a
 // multiple of 64 (the wide server layers).  A workgroup owns 128 output
 // channels x one 64-channel input block x all nine taps (128 x 576 outputs).
-// A k tile of 64 pixels is four image rows; what every tap needs of the
-// input is the six image rows around them with a one-pixel zero border,
-// 6 x 18 pixel rows of 128 bytes, copied once; the nine taps read their
-// fragments from it at shifted rows.  A k tile then copies 16 KB of g and
-// 13.5 KB of input for 9.4 MFLOP, against 64 KB for 8.4 MFLOP with one tap
-// per 256 x 256 tile.
+// A k tile of 128 pixels is eight image rows (half an image); what every tap
+// needs of the input is the ten image rows around them with a one-pixel
+// zero border, 10 x 18 pixel rows of 128 bytes, copied once; the nine taps
+// read their fragments from it at shifted rows.  A k tile then copies 32 KB
+// of g and 22.5 KB of input for 18.9 MFLOP, against 128 KB for 16.8 MFLOP
+// with one tap per 256 x 256 tile; four k groups of two image rows share one
+// barrier.
 // Halo row R = 18 h' + w' stores its 16-byte chunk c at c ^ 2 whsw(w'),
 // whsw(w') = bit 1 of w' | (bit 3 of w') << 1: the eight rows a half-wave's
 // transposing read touches (w' in {a .. a+3, a+8 .. a+11} for one image row)
 // then use every bank exactly once, and the rows of successive image rows and
 // of the three kernel-tap rows sit a constant 18 rows (2,304 bytes) apart.
 namespace wh {
-constexpr int IMG = 16, HP = 18, TR = 4;   // image side, halo row width, image rows per k tile
-constexpr int BK = IMG * TR;               // 64 pixels per k tile
-constexpr int HROWS = (TR + 2) * HP;       // 108 halo rows
+constexpr int IMG = 16, HP = 18, TR = 8;   // image side, halo row width, image rows per k tile
+constexpr int BK = IMG * TR;               // 128 pixels per k tile
+constexpr int HROWS = (TR + 2) * HP;       // 180 halo rows
 constexpr int ROWB = 128;                  // bytes per halo row (64 channels)
 constexpr int BM = 128, ROWA = BM * 2;     // output channels per workgroup, bytes per g row
 constexpr int NTHR = 512, TM = 4;          // 8 waves (2 x 4); g fragments per wave
-constexpr int A_BYTES = BK * ROWA;         // 16 KB
-constexpr int B_BYTES = 16384;             // 108 halo rows, the rest takes the zero copies of idle lanes
+constexpr int A_BYTES = BK * ROWA;         // 32 KB
+constexpr int B_BYTES = 24576;             // 180 halo rows, the rest takes the zero copies of idle lanes
 constexpr int STAGE = A_BYTES + B_BYTES;
 constexpr int SA = A_BYTES / (NTHR * 16), SB = B_BYTES / (NTHR * 16), CPT = SA + SB;
 constexpr int QROWA = NTHR * 16 / ROWA;    // g rows between a thread's copies
 constexpr int FROW = HP * ROWB;            // bytes between halo image rows
-static_assert(HROWS * ROWB <= B_BYTES && SA == 2 && SB == 2 && QROWA % 16 == 0, "halo weight-gradient layout");
+static_assert(HROWS * ROWB <= B_BYTES && SA == 4 && SB == 3 && QROWA % 16 == 0, "halo weight-gradient layout");
 }  // namespace wh
 __device__ __forceinline__ int whsw(int wp) { return ((wp >> 1) & 1) | ((wp >> 2) & 2); }
 
@@ -372,7 +373,7 @@ __device__ __forceinline__ void wh_issue(int kt, char *stage0, const void *G, co
   }
 }
 
-// k group KG (two image rows) of the stage at st: 4 g fragments, one input
+// k group KG (image rows 2 KG, 2 KG + 1) of the stage at st: 4 g fragments, one input
 // fragment per tap, 36 MFMAs (+1 against ones for the bias gradient).
 template <int KG>
 __device__ __forceinline__ void wh_kgroup(f32x4_t (&acc)[wh::TM][9], f32x4_t &bacc, const uint32_t (&ra)[wh::TM],
@@ -513,6 +514,8 @@ wgrad_halo_kernel(WgradArgs a, int MT, int NT) {
     const uint32_t st = lds0 + (uint32_t)((kt % NST) * wh::STAGE);
     wh_kgroup<0>(acc, bacc, ra, hb, st, do_bias, wn);
     wh_kgroup<1>(acc, bacc, ra, hb, st, do_bias, wn);
+    wh_kgroup<2>(acc, bacc, ra, hb, st, do_bias, wn);
+    wh_kgroup<3>(acc, bacc, ra, hb, st, do_bias, wn);
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
