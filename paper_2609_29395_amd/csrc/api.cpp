@@ -259,7 +259,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
       int bm, bn;
       const int nwc = (i == 0 && p.col0) ? p.Kc : 9 * l.Ci;
       int splits;
-      if (wgrad_lds_ok(p.dtype, l.Co, (i == 0 && p.col0) ? p.Kc : l.Ci)) {
+      if (wgrad_lds_ok(p.dtype, l.Co, (i == 0 && p.col0) ? p.Kc : l.Ci) ||
+          wgrad_col_ok(p.dtype, l.Co, (i == 0 && p.col0) ? p.Kc : l.Ci, (i == 0 && p.col0) ? 1 : 9)) {
         // pick the split count that minimises (rounds of 256 x per_cu
         // workgroups) x (k tiles per workgroup + the cost of writing and
         // re-reading a partial tile, about 16 k tiles)

@@ -704,6 +704,7 @@ hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s, std::string 
 }
 
 hipError_t launch_wgrad(int dtype, const WgradArgs &a, hipStream_t s, std::string *label) {
+  if (wgrad_col_ok(dtype, a.Co, a.Ci, a.taps) && a.chunk % 128 == 0) return launch_wgrad_col(a, s, label);
   if (wgrad_lds_ok(dtype, a.Co, a.Ci) && a.chunk % 64 == 0) return launch_wgrad_lds(a, s, label);
   // vector path: whole 16-byte channel vectors and pixel blocks within one
   // image row (im2col rows need no image-row structure)

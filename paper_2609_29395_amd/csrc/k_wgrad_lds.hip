@@ -715,7 +715,144 @@ wgrad_img_kernel(WgradArgs a) {
   }
 }
 
+// ------------------------------------------------- image layer (im2col rows)
+// dW[co][k] = sum_p g[p][co] A[p][k] and db[co] = sum_p g[p][co] for the image
+// layer on its im2col rows: 32 output channels, 32 columns (9 x 3 taps and
+// channels, zero-padded; the first 27 are written).  A stream: each wave walks
+// groups of 32 pixels of the workgroup's chunk, copying the group's g rows and
+// im2col rows (2 KB each, contiguous) into its own double-buffered LDS region
+// (no workgroup barrier in the loop), and multiplies transposed fragments
+// (four MFMAs per group, two more against ones for the bias).  The four
+// waves' sums are added in wave order at the end.
+namespace wc {
+constexpr int CO = 32, KC = 32, PX = 32;  // output channels, columns, pixels per group
+constexpr int ROW = 64;                   // bytes per pixel row of either operand
+constexpr int OP = PX * ROW;              // 2 KB per operand and group
+constexpr int STAGE = 2 * OP;             // g rows, then im2col rows
+constexpr int WAVE_LDS = 2 * STAGE;       // two stages per wave
+constexpr int BK = 128;                   // chunks are multiples of this
+}  // namespace wc
+
+__device__ __forceinline__ void wc_issue(char *dst, const bf16_t *G, const bf16_t *X, uint32_t gbytes,
+                                         uint32_t xbytes, int p, int lane) {
+  const __amdgpu_buffer_rsrc_t rsg = rsrc(G, gbytes);
+  const __amdgpu_buffer_rsrc_t rsx = rsrc(X, xbytes);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const uint32_t off = (uint32_t)(p * wc::ROW + h * 1024 + lane * 16);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsg, LDS_PTR(dst + h * 1024), 16, off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, LDS_PTR(dst + wc::OP + h * 1024), 16, off, 0, 0, 0);
+  }
+}
+
+__global__ void __launch_bounds__(256)
+wgrad_col_kernel(WgradArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem[4 * wc::WAVE_LDS];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t t = xcd_swizzle(blockIdx.x, (uint32_t)(a.splits * a.C));
+  const int split = __builtin_amdgcn_readfirstlane((int)(t % (uint32_t)a.splits));
+  const int rep = replica_of(a.rmap, __builtin_amdgcn_readfirstlane((int)(t / (uint32_t)a.splits)));
+  const int M = a.Bt * a.H * a.W;
+  const int p_begin = split * a.chunk;
+  const int ng = (min(M, p_begin + a.chunk) - p_begin) / wc::PX;  // groups of the chunk
+  const bf16_t *G = reinterpret_cast<const bf16_t *>(a.g) + rep * a.g_rs;
+  const bf16_t *X = reinterpret_cast<const bf16_t *>(a.x) + rep * a.x_rs;
+  const uint32_t gbytes = (uint32_t)((int64_t)M * wc::CO * 2), xbytes = (uint32_t)((int64_t)M * wc::KC * 2);
+  char *mine = smem + wave * wc::WAVE_LDS;
+  const uint32_t base = (uint32_t)(size_t)LDS_PTR(mine);
+  // transposing reads: lane (lg, j) takes pixel rows 8 lg + j / 4 (+4), 16-byte
+  // chunk 2 c + half of channel block c, 8-byte half j & 1
+  const int j = lane & 15, lg = lane >> 4;
+  const int half = (j & 3) >> 1;
+  const uint32_t fr = (uint32_t)((8 * lg + (j >> 2)) * wc::ROW + half * 16 + (j & 1) * 8);
+  f32x4_t acc[2][2], bacc[2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    bacc[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int d = 0; d < 2; ++d) acc[c][d] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
+  // this wave's groups: wave, wave + 4, ...
+  int i = wave;
+  if (i < ng) wc_issue(mine, G, X, gbytes, xbytes, p_begin + i * wc::PX, lane);
+  for (int s = 0; i < ng; i += 4, s ^= 1) {
+    const bool next = i + 4 < ng;
+    if (next) wc_issue(mine + (s ^ 1) * wc::STAGE, G, X, gbytes, xbytes, p_begin + (i + 4) * wc::PX, lane);
+    // the group's own copies have landed once only the next group's are out
+    if (next) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    const uint32_t st = base + (uint32_t)(s * wc::STAGE);
+    u32x4 ga[2], xb[2];
+    read_frag<0, wc::ROW>(ga[0], st + fr);
+    read_frag<32, wc::ROW>(ga[1], st + fr);
+    read_frag<wc::OP, wc::ROW>(xb[0], st + fr);
+    read_frag<wc::OP + 32, wc::ROW>(xb[1], st + fr);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int c = 0; c < 2; ++c) asm volatile("" : "+v"(ga[c]), "+v"(xb[c]));
+    const uint32_t one2 = 0x3F803F80u;  // two bf16 ones
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+#pragma unroll
+      for (int d = 0; d < 2; ++d) mma(acc[c][d], ga[c], xb[d]);
+      mma(bacc[c], ga[c], u32x4{one2, one2, one2, one2});
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // add the four waves' sums in wave order: each wave stages its 16 + 8
+  // values per lane, wave 0 adds and writes the chunk's partial
+  __syncthreads();
+  float *red = reinterpret_cast<float *>(smem);
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+#pragma unroll
+    for (int d = 0; d < 2; ++d)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) red[((wave * 24 + (c * 2 + d) * 4 + r) * 64) + lane] = acc[c][d][r];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[((wave * 24 + 16 + c * 4 + r) * 64) + lane] = bacc[c][r];
+  }
+  __syncthreads();
+  if (wave == 0) {
+    float *dw = a.dw + split * a.dw_ss + rep * a.dw_rs;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int d = 0; d < 2; ++d)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float v = 0.f;
+          for (int w = 0; w < 4; ++w) v += red[((w * 24 + (c * 2 + d) * 4 + r) * 64) + lane];
+          const int co = c * 16 + lg * 4 + r, k = d * 16 + j;
+          if (k < a.nw) dw[(int64_t)co * a.nw + k] = v;
+        }
+    if (a.db != nullptr && j == 0) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float v = 0.f;
+          for (int w = 0; w < 4; ++w) v += red[((w * 24 + 16 + c * 4 + r) * 64) + lane];
+          a.db[split * a.db_ss + rep * a.db_rs + c * 16 + lg * 4 + r] = v;
+        }
+    }
+  }
+}
+
 }  // namespace
+
+bool wgrad_col_ok(int dtype, int Co, int Ci, int taps) {
+  return dtype == GCPSL_BF16 && taps == 1 && Co == wc::CO && Ci == wc::KC;
+}
+
+hipError_t launch_wgrad_col(const WgradArgs &a, hipStream_t s, std::string *label) {
+  if (!wgrad_col_ok(GCPSL_BF16, a.Co, a.Ci, a.taps) || a.chunk % wc::BK || a.nw > wc::KC)
+    return hipErrorInvalidValue;
+  if (label) *label = "conv_wgrad<bf16,32x32,w4,col>";
+  hipLaunchKernelGGL(wgrad_col_kernel, dim3((uint32_t)a.splits * a.C), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
 
 bool wgrad_lds_ok(int dtype, int Co, int Ci) {
   return dtype == GCPSL_BF16 && Co >= 64 && Co % 8 == 0 && Ci % 8 == 0;
@@ -746,7 +883,9 @@ bool wgrad_halo_ok(int Co, int Ci, int H, int W, int taps) {
 // and how many such workgroups one CU holds (LDS-limited; halo mode: one,
 // its 8 waves hold 144 accumulator registers per lane).
 void wgrad_lds_tile(int Co, int Ci, int H, int W, int taps, int *bm, int *bn, int *bk, int *per_cu) {
-  if (wgrad_halo_ok(Co, Ci, H, W, taps)) {
+  if (taps == 1 && Co == wc::CO && Ci == wc::KC) {
+    *bm = wc::CO; *bn = wc::KC; *bk = wc::BK; *per_cu = 4;
+  } else if (wgrad_halo_ok(Co, Ci, H, W, taps)) {
     *bm = wh::BM; *bn = 9 * 64; *bk = wh::BK; *per_cu = 1;
   } else if (wgrad_img_ok(Co, Ci, H, W, taps)) {
     *bm = wi::CO; *bn = 9 * wi::CI; *bk = wi::BK; *per_cu = 160 * 1024 / (kImgStages * wi::STAGE);

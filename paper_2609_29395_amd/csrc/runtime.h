@@ -63,6 +63,9 @@ int wgrad_k_tile(int dtype);
 // bf16 weight gradient with LDS-direct tile copies and transposing LDS reads
 // (k_wgrad_lds.hip): usable when wgrad_lds_ok; needs chunk % 64 == 0.
 bool wgrad_lds_ok(int dtype, int Co, int Ci);
+// the image layer's weight gradient on its im2col rows (32 channels, 32 columns)
+bool wgrad_col_ok(int dtype, int Co, int Ci, int taps);
+hipError_t launch_wgrad_col(const WgradArgs &a, hipStream_t s, std::string *label);
 void wgrad_lds_tile(int Co, int Ci, int H, int W, int taps, int *bm, int *bn, int *bk, int *per_cu);
 hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *label);
 // bf16 forward / dgrad of 32 x 32 image layers with 32 or 64 channels

@@ -55,6 +55,8 @@ def kernel_label(name: str) -> str:
     if m:
         kind = "conv_fwd" if m.group(3) == "0" else "conv_dgrad"
         return f"{kind}<bf16,256x{m.group(2)}x{9 * int(m.group(1))},w8,img>"
+    if re.search(r"wgrad_col_kernel", name):
+        return "conv_wgrad<bf16,32x32,w4,col>"
     if re.search(r"conv_col_kernel", name):
         return "conv_fwd<bf16,256x32x32,w4,col>"
     if re.search(r"wgrad_img_kernel<", name):
@@ -77,7 +79,7 @@ SHARED_HEADERS = ("common.h",)  # device helpers every kernel source includes
 
 def kernel_source(label: str) -> str:
     """The source file that holds the kernel a timing label names."""
-    if label.startswith("conv_wgrad<") and label.endswith((",lds>", ",halo>", ",img>")):
+    if label.startswith("conv_wgrad<") and label.endswith((",lds>", ",halo>", ",img>", ",col>")):
         return "k_wgrad_lds.hip"
     if label.startswith("conv_") and label.endswith((",lds>", ",halo>")):
         return "k_conv_lds.hip"
