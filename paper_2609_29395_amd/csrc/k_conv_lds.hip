@@ -51,7 +51,7 @@ constexpr uint32_t kOob = 0x80000000u;
 constexpr int kBufferFlags = 0x00020000;
 
 template <int BM_, int BN, int WM, int WN> struct Cfg {
-  static constexpr int BM = BM_;
+  static constexpr int BM = BM_, BN_ = BN;
   static constexpr int NW = WM * WN, NTHR = 64 * NW;  // waves, threads
   static constexpr int A_BYTES = BM * ROW, B_BYTES = BN * ROW;
   static constexpr int STAGE = A_BYTES + B_BYTES;
@@ -94,9 +94,10 @@ constexpr int BYTES = ((ROWS * 128 + 1023) / 1024) * 1024;  // padded to whole 1
 constexpr int FSTRIDE = HP * 128;                         // bytes between image-row fragments
 // 16-byte copies per thread for a workgroup of NTHR threads
 template <int NTHR> constexpr int pieces() { return (ROWS * 128 + NTHR * 16 - 1) / (NTHR * 16); }
-constexpr int B_BYTES = 256 * 128;
-constexpr int LDS_BYTES = 2 * BYTES + 2 * B_BYTES;
-static_assert(pieces<1024>() == 3 && pieces<512>() == 6 && LDS_BYTES <= 160 * 1024, "halo layout");
+// k tiles: TPK kernel taps of one 64-channel block (TPK = 1, or 3 for a whole
+// tap row); two halo buffers and two weight stages of TPK x BN rows
+template <int BN, int TPK> constexpr int lds_bytes() { return 2 * BYTES + 2 * TPK * BN * 128; }
+static_assert(pieces<1024>() == 3 && pieces<512>() == 6 && lds_bytes<256, 1>() <= 160 * 1024, "halo layout");
 }  // namespace halo
 __device__ __forceinline__ int hswz(int wp) { return wp & 7; }
 
@@ -220,26 +221,39 @@ __device__ __forceinline__ void issue_halo_piece(int q, int cb, char *smem, int 
   }
 }
 
-// Halo mode: the weight rows of k tile kt (channel block kt / 9, tap kt % 9)
-// into weight stage kt % 2.
-template <typename CF>
+// Halo mode: the weight rows of k tile kt into weight stage kt % 2: TPK
+// taps of channel block kt / (9 / TPK) (one tap kt % 9, or the taps of tap
+// row kt % 3), one BN-row sub-stage per tap.
+template <typename CF, int TPK>
 __device__ __forceinline__ void issue_weights(int kt, char *smem, int wave, const ConvArgs &a, const void *wt,
                                               const uint32_t *boff) {
   const __amdgpu_buffer_rsrc_t rsb = rsrc(wt, (uint32_t)((int64_t)a.N * a.Kp * 2));
-  const int cb = kt / 9, rs = kt - 9 * cb;
-  const uint32_t kb = (uint32_t)((rs * a.Csrc + cb * BK) * 2);
-  char *sb = smem + 2 * halo::BYTES + (kt & 1) * halo::B_BYTES + wave * 1024;
+  constexpr int KPB = 9 / TPK;  // k tiles per channel block
+  const int cb = kt / KPB, kr = kt - KPB * cb;
+  char *sb = smem + 2 * halo::BYTES + (kt & 1) * TPK * CF::B_BYTES + wave * 1024;
 #pragma unroll
-  for (int q = 0; q < CF::SB; ++q)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, LDS_PTR(sb + q * CF::NTHR * 16), 16,
-                                             boff[q] == kOob ? kOob : boff[q] + kb, 0, 0, 0);
+  for (int t = 0; t < TPK; ++t) {
+    const int rs = TPK == 1 ? kr : 3 * kr + t;  // kernel tap
+    const uint32_t kb = (uint32_t)((rs * a.Csrc + cb * BK) * 2);
+#pragma unroll
+    for (int q = 0; q < CF::SB; ++q)
+      // a narrow stage takes the first waves only
+      if (CF::B_BYTES % (CF::NTHR * 16) == 0 || q * CF::NTHR * 16 + wave * 1024 < CF::B_BYTES)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, LDS_PTR(sb + t * CF::B_BYTES + q * CF::NTHR * 16), 16,
+                                                 boff[q] == kOob ? kOob : boff[q] + kb, 0, 0, 0);
+  }
 }
 
 template <int BM, int BN, int WM, int WN, int EPI, bool TAPS1, bool HALO = false>
 __global__ void __launch_bounds__(64 * WM * WN)
 conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
   using CF = Cfg<BM, BN, WM, WN>;
-  static_assert(!HALO || (BM == 256 && BN == 256 && (WM == 4 || WM == 2) && WN == 4 && !TAPS1), "halo mode tile");
+  static_assert(!HALO || (BM == 256 && !TAPS1 &&
+                          ((BN == 256 && (WM == 4 || WM == 2) && WN == 4) || (BN == 64 && WM == 8 && WN == 2))),
+                "halo mode tile");
+  // halo mode, 64-wide weight tiles: a k tile is a whole tap row (three taps)
+  // so that each barrier covers three times the MFMAs of a one-tap tile
+  constexpr int TPK = (HALO && BN == 64) ? 3 : 1;
   constexpr int SA = CF::SA, SB = CF::SB, TM = CF::TM, TN = CF::TN, NTHR = CF::NTHR, PF = CF::PF;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -308,7 +322,7 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
                       : kOob;
   }
 
-  const int nk = a.Kp / BK;
+  const int nk = a.Kp / BK / TPK;
   // k tile of the centre tap of this wave's 64-channel block (tap-fastest
   // order: k tile kt is channel block kt / 9, tap kt % 9)
   const int res_kt = ((n0 + wn_of(wave, WN) * CF::WNW) / BK) * 9 + 4;
@@ -344,7 +358,7 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   if constexpr (HALO) {
 #pragma unroll
     for (int q = 0; q < PIECES; ++q) issue_halo_piece<NTHR>(q, 0, smem, wave, a, src, img_off, hoff[q]);
-    issue_weights<CF>(0, smem, wave, a, wt, boff);
+    issue_weights<CF, TPK>(0, smem, wave, a, wt, boff);
   } else {
     issue(0);
   }
@@ -355,22 +369,27 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
     asm volatile("s_barrier" ::: "memory");
     uint32_t xb[2], wb;  // pixel fragment bases of the two k groups, weight stage
     uint32_t xst = 0;    // halo mode: the halo buffer of this channel block
+    int kr = 0;          // halo mode: k tile within its channel block
     if constexpr (HALO) {
-      const int cb = kt / 9, rs = kt - 9 * cb;
-      if (kt + 1 < nk) issue_weights<CF>(kt + 1, smem, wave, a, wt, boff);
-      // the next channel block's halo in three pieces over the first three
-      // taps (the buffer was last read by channel block cb - 1)
-      if (rs < PIECES && cb + 1 < ncb) {
+      constexpr int KPB = 9 / TPK;
+      const int cb = kt / KPB;
+      kr = kt - KPB * cb;
+      if (kt + 1 < nk) issue_weights<CF, TPK>(kt + 1, smem, wave, a, wt, boff);
+      // the next channel block's halo in pieces over the first k tiles (the
+      // buffer was last read by channel block cb - 1)
+      if (kr < PIECES && cb + 1 < ncb) {
 #pragma unroll
         for (int q = 0; q < PIECES; ++q)
-          if (q == rs) issue_halo_piece<NTHR>(q, cb + 1, smem, wave, a, src, img_off, hoff[q]);
+          if (q == kr) issue_halo_piece<NTHR>(q, cb + 1, smem, wave, a, src, img_off, hoff[q]);
       }
       xst = lds0 + (uint32_t)((cb & 1) * halo::BYTES);
-      wb = lds0 + (uint32_t)(2 * halo::BYTES + (kt & 1) * halo::B_BYTES);
-      const int r = (rs * 11) >> 5, sc = rs - 3 * r;  // tap (r, sc)
+      wb = lds0 + (uint32_t)(2 * halo::BYTES + (kt & 1) * TPK * CF::B_BYTES);
+      if constexpr (TPK == 1) {
+        const int r = (kr * 11) >> 5, sc = kr - 3 * r;  // tap (r, sc)
 #pragma unroll
-      for (int kg = 0; kg < 2; ++kg)
-        xb[kg] = xst + (uint32_t)(((wm * TM + r) * halo::HP + sc + li) * 128 + (((4 * kg + lg) ^ hswz(li + sc)) * 16));
+        for (int kg = 0; kg < 2; ++kg)
+          xb[kg] = xst + (uint32_t)(((wm * TM + r) * halo::HP + sc + li) * 128 + (((4 * kg + lg) ^ hswz(li + sc)) * 16));
+      }
     } else {
       if (kt + 1 < nk) issue(kt + 1);
       wb = lds0 + (uint32_t)((kt & 1) * CF::STAGE);
@@ -378,13 +397,23 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
       for (int kg = 0; kg < 2; ++kg) xb[kg] = wb + xa[kg];
     }
     const bool add_res = a.res_lds && kt == res_kt;
+#pragma unroll
+    for (int t = 0; t < TPK; ++t) {
+      uint32_t wbt = wb;  // this tap's weight sub-stage
+      if constexpr (HALO && TPK > 1) {
+        // tap (kr, t) of the tap row
+        wbt = wb + (uint32_t)(t * CF::B_BYTES);
+#pragma unroll
+        for (int kg = 0; kg < 2; ++kg)
+          xb[kg] = xst + (uint32_t)(((wm * TM + kr) * halo::HP + t + li) * 128 + (((4 * kg + lg) ^ hswz(li + t)) * 16));
+      }
     // per k group: the second half of the pixel fragments is read while the
     // first half is multiplied
 #pragma unroll
     for (int kg = 0; kg < 2; ++kg) {
       constexpr int H = TM / 2;
       u32x4 w[TN], x0[H], x1[H];
-      read_frags<TN>(w, wb + wa[kg]);
+      read_frags<TN>(w, wbt + wa[kg]);
       read_frags<H, 0, XS>(x0, xb[kg]);
       wait_frags<H, TN>(x0, w);
       read_frags<H, H, XS>(x1, xb[kg]);
@@ -400,6 +429,7 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) mma(acc[H + tm][tn], w[tn], x1[tm]);
     }
+    }  // taps of the k tile
     if (add_res) {
       // residual of fragment (tm, tn): 4 channels tn*16 + lg*4 .. +3 of the
       // block at pixel row wm*TM*16 + tm*16 + li of the centre-tap A tile
@@ -542,6 +572,14 @@ bool conv_lds_ok(int dtype, const ConvArgs &a) {
 // Halo mode wave layout: kHaloWM x 4 waves on the 256 x 256 tile.
 constexpr int kHaloWM = 4;
 using HaloCfg = Cfg<256, 256, kHaloWM, 4>;
+// 64-wide weight tiles: 16 waves of 32 pixels x 32 channels, tap-row k tiles
+using Halo64Cfg = Cfg<256, 64, 8, 2>;
+// dynamic LDS of a halo-mode launch: the k loop's buffers or the epilogue's
+// staging, whichever is larger
+template <typename CF, int TPK> constexpr int halo_lds_of() {
+  return halo::lds_bytes<CF::BN_, TPK>() > CF::EP_BYTES ? halo::lds_bytes<CF::BN_, TPK>() : CF::EP_BYTES;
+}
+static_assert(halo_lds_of<HaloCfg, 1>() <= 160 * 1024 && halo_lds_of<Halo64Cfg, 3>() <= 160 * 1024, "halo LDS");
 
 // Every instantiation is named in this (non-template) function, which is
 // what makes the compiler emit the host-side launch stubs.
@@ -558,10 +596,15 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   }
   static bool attr = false;
   if (!attr) {
-    constexpr int halo_lds = halo::LDS_BYTES > HaloCfg::EP_BYTES ? halo::LDS_BYTES : HaloCfg::EP_BYTES;
     for (const void *f : {reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, kHaloWM, 4, EPI_FWD, false, true>),
                           reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, kHaloWM, 4, EPI_DGRAD, false, true>)}) {
-      const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, halo_lds);
+      const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, halo_lds_of<HaloCfg, 1>());
+      if (e != hipSuccess) return e;
+    }
+    for (const void *f : {reinterpret_cast<const void *>(&conv_lds_kernel<256, 64, 8, 2, EPI_FWD, false, true>),
+                          reinterpret_cast<const void *>(&conv_lds_kernel<256, 64, 8, 2, EPI_DGRAD, false, true>)}) {
+      const hipError_t e =
+          hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, halo_lds_of<Halo64Cfg, 3>());
       if (e != hipSuccess) return e;
     }
     CONV_LDS_ATTR(256, 256, 4, 4)
@@ -576,7 +619,13 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   // workgroups per CU hide more latency), over a short one 256 (less fixed
   // cost per output)
   const int bn = a.N > 128 ? 256 : a.N > 64 ? 128 : a.N > 32 ? 64 : 32;
-  const int bm = (bn == 64 && a.Kp >= 16 * BK) ? 128 : 256;
+  // halo mode: one 16 x 16 image per 256-pixel tile, 64-channel blocks, with
+  // 256-wide weight tiles or (input channels a multiple of 64, no residual)
+  // 64-wide ones
+  const bool img16 = a.taps == 9 && a.Csrc % BK == 0 && a.H == halo::IMG && a.W == halo::IMG;
+  const bool use_halo = img16 && bn == 256;
+  const bool use_halo64 = img16 && bn == 64 && a.res == nullptr;
+  const int bm = (bn == 64 && a.Kp >= 16 * BK && !use_halo64) ? 128 : 256;
   int MT, NT;
   if (bn == 256) grid<256, 256>(a, &MT, &NT);
   else if (bn == 128) grid<256, 128>(a, &MT, &NT);
@@ -590,20 +639,27 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   ConvArgs b = a;
   b.res_lds = (a.res != nullptr && a.res == a.src && a.taps == 9 && a.Csrc % BK == 0 && a.Csrc == a.N &&
                (bn == 256 || bn == 128)) ? 1 : 0;
-  // halo mode: one 16 x 16 image per 256-pixel tile, 64-channel blocks
-  const bool use_halo = bn == 256 && a.taps == 9 && a.Csrc % BK == 0 && a.H == halo::IMG && a.W == halo::IMG;
   if (label)
     *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16," + std::to_string(bm) + "x" +
-             std::to_string(bn) + "x64,w" + (use_halo ? std::to_string(HaloCfg::NW) : bn == 256 ? "16" : "8") +
-             (use_halo ? ",halo>" : ",lds>");
+             std::to_string(bn) + (use_halo64 ? "x192,w16" : "x64,w") +
+             (use_halo ? std::to_string(HaloCfg::NW) : use_halo64 ? "" : bn == 256 ? "16" : "8") +
+             ((use_halo || use_halo64) ? ",halo>" : ",lds>");
   if (use_halo) {
-    constexpr int halo_lds = halo::LDS_BYTES > HaloCfg::EP_BYTES ? halo::LDS_BYTES : HaloCfg::EP_BYTES;
     if (a.epi == EPI_FWD)
       hipLaunchKernelGGL((conv_lds_kernel<256, 256, kHaloWM, 4, EPI_FWD, false, true>), g, dim3(HaloCfg::NTHR),
-                         halo_lds, s, b, fw, fh, fc, MT, NT);
+                         (halo_lds_of<HaloCfg, 1>()), s, b, fw, fh, fc, MT, NT);
     else
       hipLaunchKernelGGL((conv_lds_kernel<256, 256, kHaloWM, 4, EPI_DGRAD, false, true>), g, dim3(HaloCfg::NTHR),
-                         halo_lds, s, b, fw, fh, fc, MT, NT);
+                         (halo_lds_of<HaloCfg, 1>()), s, b, fw, fh, fc, MT, NT);
+    return hipGetLastError();
+  }
+  if (use_halo64) {
+    if (a.epi == EPI_FWD)
+      hipLaunchKernelGGL((conv_lds_kernel<256, 64, 8, 2, EPI_FWD, false, true>), g, dim3(Halo64Cfg::NTHR),
+                         (halo_lds_of<Halo64Cfg, 3>()), s, b, fw, fh, fc, MT, NT);
+    else
+      hipLaunchKernelGGL((conv_lds_kernel<256, 64, 8, 2, EPI_DGRAD, false, true>), g, dim3(Halo64Cfg::NTHR),
+                         (halo_lds_of<Halo64Cfg, 3>()), s, b, fw, fh, fc, MT, NT);
     return hipGetLastError();
   }
 #define CONV_LDS_GO(BM, BN, WM, WN, E, T)                                                                  \

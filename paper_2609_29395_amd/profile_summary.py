@@ -50,7 +50,8 @@ def kernel_label(name: str) -> str:
         kind = "conv_fwd" if m.group(5) == "0" else "conv_dgrad"
         w = int(m.group(3)) * int(m.group(4))
         mode = "halo" if m.group(8) == "true" else "lds"
-        return f"{kind}<bf16,{m.group(1)}x{m.group(2)}x64,w{w},{mode}>"
+        kt = 192 if (mode == "halo" and m.group(2) == "64") else 64  # tap-row k tiles
+        return f"{kind}<bf16,{m.group(1)}x{m.group(2)}x{kt},w{w},{mode}>"
     m = re.search(r"conv_img_kernel<(\d+), (\d+), (\d)>", name)
     if m:
         kind = "conv_fwd" if m.group(3) == "0" else "conv_dgrad"
