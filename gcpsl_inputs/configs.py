@@ -139,6 +139,14 @@ CONFIGS = {
         layers=[("conv", 3, 32, False), ("conv", 32, 64, False), ("maxpool",),
                 ("conv", 64, 64, False), ("avgpool",), ("linear", 64, 7)],
         cut=3, dtype="bf16", lr=0.05, momentum=0.9, F=2, T=3, seed=0),
+    # The same client layers on 12 x 12 images: 432 pixels per replica, not
+    # a multiple of the image layer's 32-pixel weight-gradient groups.
+    "col_ragged_bf16": dict(
+        K=16, C=2, B=3, L=7, N_ex=602, H=12, W=12, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="label_l1",
+        layers=[("conv", 3, 32, False), ("conv", 32, 64, False), ("maxpool",),
+                ("conv", 64, 64, False), ("avgpool",), ("linear", 64, 7)],
+        cut=3, dtype="bf16", lr=0.05, momentum=0.9, F=2, T=3, seed=0),
     # GroupNorm in the client segment, BatchNorm in the server segment
     # (Sec. IV-B), whose running statistics are fused with the parameters.
     "tiny_norm": dict(

@@ -755,7 +755,9 @@ wgrad_col_kernel(WgradArgs a) {
   const int rep = replica_of(a.rmap, __builtin_amdgcn_readfirstlane((int)(t / (uint32_t)a.splits)));
   const int M = a.Bt * a.H * a.W;
   const int p_begin = split * a.chunk;
-  const int ng = (min(M, p_begin + a.chunk) - p_begin) / wc::PX;  // groups of the chunk
+  // groups of the chunk; a last partial group reads zeros past the last
+  // pixel (the copies' range check), which add nothing
+  const int ng = (min(M, p_begin + a.chunk) - p_begin + wc::PX - 1) / wc::PX;
   const bf16_t *G = reinterpret_cast<const bf16_t *>(a.g) + rep * a.g_rs;
   const bf16_t *X = reinterpret_cast<const bf16_t *>(a.x) + rep * a.x_rs;
   const uint32_t gbytes = (uint32_t)((int64_t)M * wc::CO * 2), xbytes = (uint32_t)((int64_t)M * wc::KC * 2);
