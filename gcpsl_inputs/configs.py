@@ -147,6 +147,14 @@ CONFIGS = {
         layers=[("conv", 3, 32, False), ("conv", 32, 64, False), ("maxpool",),
                 ("conv", 64, 64, False), ("avgpool",), ("linear", 64, 7)],
         cut=3, dtype="bf16", lr=0.05, momentum=0.9, F=2, T=3, seed=0),
+    # 20 classes: more than the register-resident classifier head holds, so
+    # the LDS-staged head runs (with label smoothing).
+    "wide_head_bf16": dict(
+        K=16, C=2, B=20, L=20, N_ex=600, H=8, W=8, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="label_l1",
+        layers=[("conv", 3, 16, False), ("maxpool",), ("conv", 16, 64, False), ("avgpool",),
+                ("linear", 64, 20)],
+        cut=2, dtype="bf16", lr=0.05, momentum=0.9, F=2, T=4, seed=0, label_smoothing=0.1),
     # GroupNorm in the client segment, BatchNorm in the server segment
     # (Sec. IV-B), whose running statistics are fused with the parameters.
     "tiny_norm": dict(

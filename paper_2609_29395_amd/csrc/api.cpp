@@ -180,7 +180,7 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   if (p.head_conv < 0 || !is_act(p.ly[p.head_conv].spec.kind) || p.ly[p.head_conv].no_relu)
     return gcpsl_fail(GCPSL_EUNSUPPORTED, "avgpool must follow a conv or norm layer, optionally + max pool");
   p.Ch_head = p.ly[p.head_conv].Co;
-  if (linear_ce_lds_bytes(d->B, p.Ch_head, d->L) > kMaxLinearLds)
+  if (!linear_ce_reg_ok(d->B, p.Ch_head, d->L) && linear_ce_lds_bytes(d->B, p.Ch_head, d->L) > kMaxLinearLds)
     return gcpsl_fail(GCPSL_EUNSUPPORTED, "classifier head too large for one workgroup (B * channels)");
 
   // workspace layout

@@ -590,6 +590,253 @@ linear_ce_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
   }
 }
 
+// The same head with the weights in registers, for heads of at most 256
+// channels and kHeadRegL classes: lane l of each wave holds channels
+// 4l..4l+3 of every weight row (bf16-rounded for bf16 workloads), and wave w
+// takes examples w, w + 8, ...  A lane forms its 4-channel share of every
+// logit of an example; a butterfly over the 64 lanes adds the shares.  The
+// input gradient of an example comes from the lane's own weights; the
+// weight gradient is summed per wave over its examples, then over the
+// waves in a fixed tree.  Every sum runs in a fixed order.  LM is L rounded
+// up to a multiple of 4 (classes past L have zero weights and gradients).
+// Loads never sit behind a branch: out-of-range lanes read a clamped,
+// valid address and select zero, so every load of a group is in flight
+// together.
+
+// Channels c..c+3 of one example as floats.
+template <typename T>
+__device__ __forceinline__ void head_load4(const T *p, float x[4]) {
+  if constexpr (sizeof(T) == 2) {
+    const uint2 u = *reinterpret_cast<const uint2 *>(p);
+    x[0] = __uint_as_float(u.x << 16);
+    x[1] = __uint_as_float(u.x & 0xffff0000u);
+    x[2] = __uint_as_float(u.y << 16);
+    x[3] = __uint_as_float(u.y & 0xffff0000u);
+  } else {
+    const float4 f = *reinterpret_cast<const float4 *>(p);
+    x[0] = f.x; x[1] = f.y; x[2] = f.z; x[3] = f.w;
+  }
+}
+
+// One halving exchange over lane bit 2 N, for each of NB vectors at once
+// (their exchanges are independent and overlap): a lane keeps half N / 2..
+// of its N entries if that bit is set, else half 0.., and adds its
+// partner's copy of the half it keeps.  A compile-time stage, so every
+// index is a register.
+template <int N, int NB>
+__device__ __forceinline__ void wave_halve(float (&v)[NB][kHeadRegL], int lane) {
+  const bool up = lane & (2 * N);
+  float keep[NB][N / 2], got[NB][N / 2];
+#pragma unroll
+  for (int u = 0; u < NB; ++u)
+#pragma unroll
+    for (int i = 0; i < N / 2; ++i) {
+      const float lo = v[u][i], hi = v[u][i + N / 2];  // both in registers, then a select
+      keep[u][i] = up ? hi : lo;
+      got[u][i] = __shfl_xor(up ? lo : hi, 2 * N, 64);
+    }
+#pragma unroll
+  for (int u = 0; u < NB; ++u)
+#pragma unroll
+    for (int i = 0; i < N / 2; ++i) v[u][i] = keep[u][i] + got[u][i];
+}
+
+// Sums each of NB vectors v[u][0..15] over the 64 lanes of a wave: four
+// halving exchanges leave entry (lane >> 2) & 15 in each lane, two more add
+// the four lanes that hold the same entry (all four get the same value).
+template <int NB>
+__device__ __forceinline__ void wave_sum16(float (&v)[NB][kHeadRegL], float (&sum)[NB]) {
+  static_assert(kHeadRegL == 16, "four halving stages");
+  const int lane = threadIdx.x & 63;
+  wave_halve<16>(v, lane);
+  wave_halve<8>(v, lane);
+  wave_halve<4>(v, lane);
+  wave_halve<2>(v, lane);
+  float t[NB];
+#pragma unroll
+  for (int u = 0; u < NB; ++u) t[u] = __shfl_xor(v[u][0], 2, 64);
+#pragma unroll
+  for (int u = 0; u < NB; ++u) sum[u] = v[u][0] + t[u];
+#pragma unroll
+  for (int u = 0; u < NB; ++u) t[u] = __shfl_xor(sum[u], 1, 64);
+#pragma unroll
+  for (int u = 0; u < NB; ++u) sum[u] += t[u];
+}
+
+template <typename T, int LM>
+__global__ void __launch_bounds__(kHeadRegWaves * 64)
+linear_ce_reg_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
+                     const float *__restrict__ theta, int64_t P, int64_t w_off, int64_t b_off,
+                     float *__restrict__ grad, float *__restrict__ dh, float *__restrict__ loss,
+                     const int32_t *__restrict__ rmap, int Bt, int Ch, int L, float eps) {
+  static_assert(LM % 4 == 0 && LM <= kHeadRegL, "class slots");
+  constexpr int NW = kHeadRegWaves, NB = 4;  // NB examples' loads in flight per wave
+  extern __shared__ float sh[];
+  float *lg = sh;               // [Bt][L] logits, then dlogits
+  float *lossb = lg + Bt * L;   // [Bt]
+  float4 *red = reinterpret_cast<float4 *>(sh + ((Bt * (L + 1) + 3) & ~3));  // [NW / 2][L][64]
+  const int rep = replica_of(rmap, blockIdx.x), tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int c0 = 4 * lane;
+  const bool live = c0 < Ch;
+  const int cl = live ? c0 : 0;  // a valid channel for every lane
+  const T *hr = h + (int64_t)rep * Bt * Ch + cl;
+  const float *Wl = theta + rep * P + w_off;
+  const float *bl = theta + rep * P + b_off;
+  float w[LM][4];
+#pragma unroll
+  for (int j = 0; j < LM; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float v = Wl[(int64_t)min(j, L - 1) * Ch + cl + e];
+      w[j][e] = (live && j < L) ? ElemT<T>::to_f(ElemT<T>::from_f(v)) : 0.f;
+    }
+  const int jl = (lane >> 2) & (kHeadRegL - 1);  // the logit this lane's sum ends as
+  const bool writer = (lane & 3) == 0 && jl < L;
+  const float bias = bl[min(jl, L - 1)];
+
+  // logits
+  for (int b0 = wave; b0 < Bt; b0 += NB * NW) {
+    float x[NB][4];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) head_load4(hr + (int64_t)min(b0 + u * NW, Bt - 1) * Ch, x[u]);
+    float v[NB][kHeadRegL], sum[NB];
+#pragma unroll
+    for (int u = 0; u < NB; ++u)
+#pragma unroll
+      for (int j = 0; j < kHeadRegL; ++j)
+        v[u][j] = j < LM ? fmaf(x[u][3], w[j][3], fmaf(x[u][2], w[j][2], fmaf(x[u][1], w[j][1], x[u][0] * w[j][0])))
+                         : 0.f;
+    wave_sum16(v, sum);
+    if (writer) {
+#pragma unroll
+      for (int u = 0; u < NB; ++u)
+        if (b0 + u * NW < Bt) lg[(b0 + u * NW) * L + jl] = bias + sum[u];
+    }
+  }
+  __syncthreads();
+  // softmax cross-entropy per example, as in linear_ce_kernel
+  for (int b = tid; b < Bt; b += NW * 64) {
+    float m = lg[b * L];
+    for (int j = 1; j < L; ++j) m = fmaxf(m, lg[b * L + j]);
+    float s = 0.f;
+    for (int j = 0; j < L; ++j) s += expf(lg[b * L + j] - m);
+    const float lse = logf(s);
+    const int yb = y[(int64_t)rep * Bt + b];
+    const float qo = eps / (float)L, qy = 1.f - eps + qo;
+    float zs = 0.f;
+    for (int j = 0; j < L; ++j) zs += lg[b * L + j] - m;
+    lossb[b] = eps > 0.f ? lse - (1.f - eps) * (lg[b * L + yb] - m) - qo * zs : lse - (lg[b * L + yb] - m);
+    for (int j = 0; j < L; ++j) {
+      const float p = expf(lg[b * L + j] - m - lse);
+      lg[b * L + j] = (p - (j == yb ? qy : qo)) / (float)Bt;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float s = 0.f;
+    for (int b = 0; b < Bt; ++b) s += lossb[b];
+    loss[rep] = s / (float)Bt;
+  }
+  float *g = grad + rep * P;
+  for (int j = tid; j < L; j += NW * 64) {
+    float s = 0.f;
+    for (int b = 0; b < Bt; ++b) s += lg[b * L + j];
+    g[b_off + j] = s;
+  }
+
+  // input gradient of each example, weight-gradient share of each wave
+  float acc[LM][4];
+#pragma unroll
+  for (int j = 0; j < LM; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[j][e] = 0.f;
+  float *dhr = dh + (int64_t)rep * Bt * Ch + cl;
+  for (int b0 = wave; b0 < Bt; b0 += NB * NW) {
+    float x[NB][4], d[NB][LM];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+      const int b = b0 + u * NW, bc = min(b, Bt - 1);
+      head_load4(hr + (int64_t)bc * Ch, x[u]);
+#pragma unroll
+      for (int j = 0; j < LM; ++j) {
+        const float v = lg[bc * L + min(j, L - 1)];
+        d[u][j] = (b < Bt && j < L) ? v : 0.f;
+      }
+    }
+    float o[NB][4];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[u][e] = 0.f;
+#pragma unroll
+      for (int j = 0; j < LM; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          o[u][e] = fmaf(d[u][j], w[j][e], o[u][e]);
+          acc[j][e] = fmaf(d[u][j], x[u][e], acc[j][e]);
+        }
+    }
+    if (live) {
+#pragma unroll
+      for (int u = 0; u < NB; ++u)
+        if (b0 + u * NW < Bt)
+          *reinterpret_cast<float4 *>(dhr + (int64_t)(b0 + u * NW) * Ch) = make_float4(o[u][0], o[u][1], o[u][2], o[u][3]);
+    }
+  }
+  // waves [half, 2 half) hand their sums to waves [0, half)
+#pragma unroll
+  for (int half = NW / 2; half >= 1; half >>= 1) {
+    if (wave >= half && wave < 2 * half) {
+#pragma unroll
+      for (int j = 0; j < LM; ++j)
+        if (j < L) red[((wave - half) * L + j) * 64 + lane] = make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+    }
+    __syncthreads();
+    if (wave < half) {
+#pragma unroll
+      for (int j = 0; j < LM; ++j) {
+        const float4 r = red[(wave * L + min(j, L - 1)) * 64 + lane];
+        acc[j][0] += r.x;
+        acc[j][1] += r.y;
+        acc[j][2] += r.z;
+        acc[j][3] += r.w;
+      }
+    }
+    __syncthreads();
+  }
+  if (wave == 0 && live) {
+#pragma unroll
+    for (int j = 0; j < LM; ++j)
+      if (j < L)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) g[w_off + (int64_t)j * Ch + c0 + e] = acc[j][e];
+  }
+}
+
+template <typename T>
+static hipError_t launch_linear_ce_reg(const T *h, const int32_t *y, const float *theta, int64_t P, int64_t w_off,
+                                       int64_t b_off, float *grad, float *dh, float *loss, int C,
+                                       const int32_t *rmap, int Bt, int Ch, int L, float eps, hipStream_t s) {
+  const size_t shm = linear_ce_reg_lds_bytes(Bt, L);
+  auto go = [&](auto kern) -> hipError_t {
+    if (shm > 64 * 1024) {
+      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kern, dim3(C), dim3(kHeadRegWaves * 64), shm, s, h, y, theta, P, w_off, b_off, grad, dh,
+                       loss, rmap, Bt, Ch, L, eps);
+    return hipGetLastError();
+  };
+  switch ((L + 3) / 4) {
+    case 1: return go(linear_ce_reg_kernel<T, 4>);
+    case 2: return go(linear_ce_reg_kernel<T, 8>);
+    case 3: return go(linear_ce_reg_kernel<T, 12>);
+    default: return go(linear_ce_reg_kernel<T, 16>);
+  }
+}
+
 // Gradient of the head pooling, with the last conv's ReLU mask:
 // gpre = mask * route(dh / npos) (route = first maximum if max pooled).  A
 // thread handles one 16-byte vector of channels of one window (max pooled)
@@ -945,6 +1192,11 @@ hipError_t launch_head_pool(int dtype, const void *a, void *h, int C, const int3
 hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const float *theta, int64_t P,
                             int64_t w_off, int64_t b_off, float *grad, float *dh, float *loss, int C,
                             const int32_t *rmap, int Bt, int Ch, int L, float eps, hipStream_t s) {
+  if (linear_ce_reg_ok(Bt, Ch, L))
+    return dtype == GCPSL_BF16 ? launch_linear_ce_reg((const bf16_t *)h, y, theta, P, w_off, b_off, grad, dh, loss,
+                                                      C, rmap, Bt, Ch, L, eps, s)
+                               : launch_linear_ce_reg((const float *)h, y, theta, P, w_off, b_off, grad, dh, loss,
+                                                      C, rmap, Bt, Ch, L, eps, s);
   const size_t shm = linear_ce_lds_bytes(Bt, Ch, L);
   if (shm > kMaxLinearLds) return hipErrorInvalidValue;
   if (shm > 64 * 1024) {

@@ -125,6 +125,20 @@ constexpr size_t kMaxLinearLds = 160 * 1024;
 inline size_t linear_ce_lds_bytes(int Bt, int Ch, int L) {
   return sizeof(float) * ((size_t)Bt * (Ch + 1) + (size_t)L * (Ch + 1) + (size_t)Bt * L + Bt + L);
 }
+// Register-resident head (weights in registers, one 4-channel slice per
+// lane): heads of at most 256 channels (a multiple of 4) and kHeadRegL
+// classes, on kHeadRegWaves waves; its LDS holds the logits, the per-example
+// losses and the weight-gradient hand-over of the reduction tree.
+constexpr int kHeadRegL = 16, kHeadRegWaves = 8;
+inline size_t linear_ce_reg_lds_bytes(int Bt, int L) {
+  return sizeof(float) * ((((size_t)Bt * (L + 1) + 3) & ~(size_t)3) + (size_t)(kHeadRegWaves / 2) * L * 64 * 4);
+}
+inline bool linear_ce_reg_ok(int Bt, int Ch, int L) {
+  return Ch % 4 == 0 && Ch <= 256 && L <= kHeadRegL && linear_ce_reg_lds_bytes(Bt, L) <= kMaxLinearLds;
+}
+// The classifier head (linear layer and softmax cross-entropy, one workgroup
+// per replica): the register-resident kernel where linear_ce_reg_ok holds,
+// else the LDS-staged one.
 hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const float *theta,
                             int64_t P, int64_t w_off, int64_t b_off, float *grad, float *dh,
                             float *loss, int C, const int32_t *rmap, int Bt, int Ch, int L, float eps,
