@@ -233,6 +233,87 @@ gather_im2col_fixed_kernel(const float *__restrict__ images, const int32_t *__re
 // tap, staged through LDS so both the reads and the writes are coalesced.
 // One launch covers every layer: workgroup b belongs to the job whose first
 // workgroup is the largest not above b.
+// Eight consecutive outputs from fp32 values: one 16-byte store for bf16,
+// two for fp32 (p is 8-element aligned).
+template <typename T>
+__device__ __forceinline__ void store8(T *p, const float (&v)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    uint4 o;
+    o.x = pack2_bf16(v[0], v[1]);
+    o.y = pack2_bf16(v[2], v[3]);
+    o.z = pack2_bf16(v[4], v[5]);
+    o.w = pack2_bf16(v[6], v[7]);
+    *reinterpret_cast<uint4 *>(p) = o;
+  } else {
+    *reinterpret_cast<float4 *>(p) = make_float4(v[0], v[1], v[2], v[3]);
+    *reinterpret_cast<float4 *>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
+// Both copies of one 64 x 64 (co, ci) block of source tap ts = (r, s): the
+// block is read once into LDS, written to wf at tap ts (rows co) and,
+// transposed, to wd at the flipped tap 8 - ts (rows ci).  co and ci are
+// multiples of 8, so every 8-element run is wholly inside or outside the
+// layer and 16-byte aligned (Kp, Kdp are multiples of 8 as well).  The
+// workgroups of tap 0 also zero the row padding of their blocks.
+template <typename T>
+__device__ __forceinline__ void prep_both_block(const float *w, int rep, const PrepJob &J, int lb,
+                                                float (&tile)[64][65]) {
+  const int co = J.co, ci = J.ci, K = 9 * ci, Kdp = J.kpad, Kp = J.kpad2;
+  const int nco = (co + 63) / 64;
+  const int ts = lb % 9, blk = lb / 9;
+  const int cb = blk % nco, ib = blk / nco;
+  const int tid = threadIdx.x, tx = tid & 63, ty = tid >> 6;
+  float v[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int o = cb * 64 + ty + 4 * i, c = ib * 64 + tx;
+    v[i] = (o < co && c < ci) ? w[(int64_t)o * K + ts * ci + c] : 0.f;
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) tile[ty + 4 * i][tx] = v[i];
+  __syncthreads();
+  T *wf = reinterpret_cast<T *>(J.dst2) + (int64_t)rep * co * Kp;
+  T *wd = reinterpret_cast<T *>(J.dst) + (int64_t)rep * ci * Kdp;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int q = tid + 256 * k, r = q >> 3, run = 8 * (q & 7);
+    // forward copy: row o = cb 64 + r, columns ts ci + ib 64 + run ..
+    const int o = cb * 64 + r, c = ib * 64 + run;
+    if (o < co && c < ci) {
+      float e[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) e[t] = tile[r][run + t];
+      store8(wf + (int64_t)o * Kp + ts * ci + c, e);
+    }
+    // input-gradient copy: row c = ib 64 + r, columns (8 - ts) co + cb 64 + run ..
+    const int c2 = ib * 64 + r, o2 = cb * 64 + run;
+    if (c2 < ci && o2 < co) {
+      float e[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) e[t] = tile[run + t][r];
+      store8(wd + (int64_t)c2 * Kdp + (8 - ts) * co + o2, e);
+    }
+  }
+  if (ts == 0) {
+    const float z[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (ib == 0) {  // wf columns 9 ci .. Kp of this block's rows
+      const int runs = (Kp - K) / 8;
+      for (int q = tid; q < 64 * runs; q += 256) {
+        const int o = cb * 64 + q / runs;
+        if (o < co) store8(wf + (int64_t)o * Kp + K + 8 * (q % runs), z);
+      }
+    }
+    if (cb == 0) {  // wd columns 9 co .. Kdp of this block's rows
+      const int runs = (Kdp - 9 * co) / 8;
+      for (int q = tid; q < 64 * runs; q += 256) {
+        const int c = ib * 64 + q / runs;
+        if (c < ci) store8(wd + (int64_t)c * Kdp + 9 * co + 8 * (q % runs), z);
+      }
+    }
+  }
+}
+
 template <typename T>
 __global__ void __launch_bounds__(256)
 prep_weights_kernel(const float *__restrict__ theta, const int32_t *__restrict__ rmap, int64_t P, PrepJobs jobs) {
@@ -269,6 +350,10 @@ prep_weights_kernel(const float *__restrict__ theta, const int32_t *__restrict__
         *reinterpret_cast<float4 *>(dst + k0 + 4) = make_float4(v[4], v[5], v[6], v[7]);
       }
     }
+    return;
+  }
+  if (J.kind == 2) {
+    prep_both_block<T>(w, rep, J, lb, tile);
     return;
   }
   // input-gradient copy: block (cb, ib) of tap `tap` of the flipped kernel
@@ -1102,6 +1187,12 @@ hipError_t launch_gather_im2col(const float *images, const int32_t *idx, void *x
 
 void prep_add_layer(PrepJobs &jobs, int64_t w_off, int co, int ci, void *wf, int Kp, void *wd, int Kdp) {
   if (jobs.n + 2 > kMaxPrepJobs) return;  // the plan checks the layer count
+  if (wd && co % 8 == 0 && ci % 8 == 0) {
+    // one read of the masters for both copies, 8-element (16-byte bf16) runs
+    jobs.j[jobs.n++] = PrepJob{w_off, wd, co, ci, Kdp, 2, jobs.total, wf, Kp};
+    jobs.total += ((co + 63) / 64) * ((ci + 63) / 64) * 9;
+    return;
+  }
   jobs.j[jobs.n++] = PrepJob{w_off, wf, co, ci, Kp, 0, jobs.total};
   jobs.total += co;
   if (wd) {

@@ -102,8 +102,10 @@ struct PrepJob {
   int64_t w_off;  // the layer's weights in a replica's parameter vector
   void *dst;      // wf or wd of replica 0 (replica r at r * co * kpad / r * ci * kpad)
   int co, ci, kpad;
-  int kind;   // 0 forward copy, 1 input-gradient copy
+  int kind;   // 0 forward copy, 1 input-gradient copy, 2 both (dst = wd, dst2 = wf)
   int first;  // first workgroup of the job
+  void *dst2 = nullptr;  // kind 2: wf
+  int kpad2 = 0;         // kind 2: Kp
 };
 constexpr int kMaxPrepJobs = 32;
 struct PrepJobs {
