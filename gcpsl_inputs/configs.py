@@ -131,6 +131,16 @@ CONFIGS = {
                 ("conv", 64, 256, False), ("conv", 256, 256, True), ("conv", 256, 256, True),
                 ("avgpool",), ("linear", 256, 7)],
         cut=2, dtype="bf16", lr=0.05, momentum=0.9, F=2, T=3, seed=0),
+    # 16 x 16 images into a 136-channel head conv (one 256-wide tile, 120
+    # channels unused) with a 2 x 2 max pool before the mean, the head of
+    # the wide 16-cluster workload at small size.
+    "halo_maxhead_bf16": dict(
+        K=24, C=2, B=5, L=7, N_ex=1400, H=16, W=16, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="label_l1",
+        layers=[("conv", 3, 16, False), ("conv", 16, 64, False),
+                ("conv", 64, 256, False), ("conv", 256, 136, False), ("maxpool",),
+                ("avgpool",), ("linear", 136, 7)],
+        cut=2, dtype="bf16", lr=0.05, momentum=0.9, F=2, T=3, seed=0),
     # 32 x 32 images with the workloads' client layers (3 -> 32 -> 64, max
     # pool), so the image-layer convolution kernels run at small size.
     "img32_bf16": dict(

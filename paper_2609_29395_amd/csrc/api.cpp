@@ -590,6 +590,7 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
     return na;
   };
   bool pool_done = false;  // the max pool after the last conv was written by it
+  bool avg_done = false;   // the head's mean pooling was written by the conv before it
   for (int i = 0; i < n; ++i) {
     const LayerInfo &l = p.ly[i];
     const int kind = l.spec.kind;
@@ -623,6 +624,16 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
         pool_done = conv_fuses_pool(p.dtype, a);
         if (!pool_done) a.pool_out = nullptr;
       }
+      // the head's mean pooling right after this conv: written by the conv
+      // kernel itself where it supports that
+      avg_done = false;
+      if (i == p.head_conv && i + (p.head_maxpool ? 2 : 1) == p.avg_idx) {
+        a.pool_out = ws + p.ly[p.avg_idx].act_off;
+        a.pool_rs = (int64_t)B * l.Co;
+        a.pool_max = p.head_maxpool ? 1 : 0;
+        avg_done = conv_fuses_avg(p.dtype, a);
+        if (!avg_done) a.pool_out = nullptr;
+      }
       std::string lab;
       const double M = (double)B * l.H * l.W;
       const double fl = 2.0 * C * M * l.Co * 9.0 * l.Ci;
@@ -640,6 +651,7 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
       LAUNCH_T("maxpool_fwd", 0.0, 1.25 * p.esz * (double)C * B * l.H * l.W * l.Ci,
                launch_maxpool_fwd(p.dtype, input_of(i), ws + l.act_off, C, rmap, B, l.H, l.W, l.Ci, s));
     } else if (kind == GCPSL_AVGPOOL) {
+      if (avg_done) continue;  // written by the conv before it
       const LayerInfo &hc = p.ly[p.head_conv];
       LAUNCH_T("head_pool", 0.0, (double)p.esz * C * B * hc.Co * ((double)hc.Ho * hc.Wo + 1),
                launch_head_pool(p.dtype, ws + hc.act_off, ws + l.act_off, C, rmap, B, hc.Ho, hc.Wo, hc.Co,

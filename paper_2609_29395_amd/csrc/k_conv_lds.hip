@@ -244,13 +244,16 @@ __device__ __forceinline__ void issue_weights(int kt, char *smem, int wave, cons
   }
 }
 
-template <int BM, int BN, int WM, int WN, int EPI, bool TAPS1, bool HALO = false>
+template <int BM, int BN, int WM, int WN, int EPI, bool TAPS1, bool HALO = false, bool AVG = false>
 __global__ void __launch_bounds__(64 * WM * WN)
 conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
   using CF = Cfg<BM, BN, WM, WN>;
   static_assert(!HALO || (BM == 256 && !TAPS1 &&
                           ((BN == 256 && (WM == 4 || WM == 2) && WN == 4) || (BN == 64 && WM == 8 && WN == 2))),
                 "halo mode tile");
+  // AVG: the tile is one whole image and every output channel (halo mode,
+  // 256-wide weight tile, forward)
+  static_assert(!AVG || (HALO && BN == 256 && EPI == EPI_FWD), "image mean in the epilogue");
   // halo mode, 64-wide weight tiles: a k tile is a whole tap row (three taps)
   // so that each barrier covers three times the MFMAs of a one-tap tile
   constexpr int TPK = (HALO && BN == 64) ? 3 : 1;
@@ -482,6 +485,10 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   const __amdgpu_buffer_rsrc_t rsm = rsrc(msk ? msk : out, (uint32_t)(a.out_rs * 2));
   // dgrad: the mask loads of every pass are issued up front, so their HBM
   // latency is paid once per tile instead of once per pass
+  float avs[8];  // AVG: this lane's sums of its 8 channels over its pixel rows (or windows)
+#pragma unroll
+  for (int e = 0; e < 8; ++e) avs[e] = 0.f;
+  float pv[AVG ? ITS : 1][8];  // AVG: the pass's stored values of this lane
   uint4 mvall[TM / PF][ITS];
   if constexpr (EPI == EPI_DGRAD) {
 #pragma unroll
@@ -549,10 +556,70 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
       ov.z = pack2_bf16(v[4], v[5]);
       ov.w = pack2_bf16(v[6], v[7]);
       if (nok && m < M) *reinterpret_cast<uint4 *>(out + (int64_t)m * a.N + n) = ov;
+      if constexpr (AVG) {
+        // the stored (bf16-rounded) values, as the pooling reads them back
+        const uint32_t ow[4] = {ov.x, ov.y, ov.z, ov.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          pv[i][2 * e] = bf2f(ow[e] & 0xffffu);
+          pv[i][2 * e + 1] = bf2f(ow[e] >> 16);
+        }
+      }
+    }
+    if constexpr (AVG) {
+      // a pass holds two whole image rows (one pooling row); lane step i
+      // is row i >> 1, column lane / 8 + 8 (i & 1)
+      static_assert(PR == 2 * halo::IMG && RSTEP == 8 && ITS == 4, "pass = one pooling row");
+      if (a.pool_max) {
+        // 2 x 2 windows: the other column of a window is in lane ^ 8; the
+        // even-column lane adds the window's maximum
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float c0 = fmaxf(pv[0][e], pv[2][e]), c1 = fmaxf(pv[1][e], pv[3][e]);
+          const float w0 = fmaxf(c0, __shfl_xor(c0, 8, 64)), w1 = fmaxf(c1, __shfl_xor(c1, 8, 64));
+          if ((lane & 8) == 0) {
+            avs[e] += w0;
+            avs[e] += w1;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < ITS; ++i)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) avs[e] += pv[i][e];
+      }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  if constexpr (AVG) {
+    // mean over the tile's image (or its 2 x 2 windows) per channel: the 8
+    // lanes of a channel segment add over lane bits 3..5 (each pair sum is symmetric, so all
+    // 8 hold the same total), then the WM waves of a channel range add in
+    // wave order through LDS
+    static_assert(SEGS == 8, "8 lanes per segment");
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      avs[e] += __shfl_xor(avs[e], 8, 64);
+      avs[e] += __shfl_xor(avs[e], 16, 64);
+      avs[e] += __shfl_xor(avs[e], 32, 64);
+    }
+    __syncthreads();  // every wave is done with its staging rows
+    float *ps = reinterpret_cast<float *>(smem);  // [WM][BN]
+    if (lane < SEGS) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ps[wm * BN + wn * CF::WNW + 8 * lane + e] = avs[e];
+    }
+    __syncthreads();
+    if (tid < BN && n0 + tid < a.N) {
+      float sm = 0.f;
+#pragma unroll
+      for (int w = 0; w < WM; ++w) sm += ps[w * BN + tid];
+      const int npos = a.pool_max ? (a.H / 2) * (a.W / 2) : a.H * a.W;
+      bf16_t *ho = reinterpret_cast<bf16_t *>(a.pool_out) + rep * a.pool_rs + (int64_t)(m0 / (a.H * a.W)) * a.N;
+      ho[n0 + tid] = f32_to_bf16(sm / (float)npos);
+    }
   }
 }
 
@@ -581,6 +648,14 @@ template <typename CF, int TPK> constexpr int halo_lds_of() {
 }
 static_assert(halo_lds_of<HaloCfg, 1>() <= 160 * 1024 && halo_lds_of<Halo64Cfg, 3>() <= 160 * 1024, "halo LDS");
 
+// The halo forward on a 256-wide weight tile writes the per-image channel
+// means to pool_out as well when that is set (launch_conv reaches
+// launch_conv_lds for these arguments: not an image-side or im2col layer).
+bool conv_fuses_avg(int dtype, const ConvArgs &a) {
+  return a.epi == EPI_FWD && !conv_img_ok(dtype, a) && conv_lds_ok(dtype, a) && a.taps == 9 && a.Csrc % BK == 0 &&
+         a.H == halo::IMG && a.W == halo::IMG && a.N > 128 && a.N <= 256;
+}
+
 // Every instantiation is named in this (non-template) function, which is
 // what makes the compiler emit the host-side launch stubs.
 hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label) {
@@ -597,6 +672,7 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   static bool attr = false;
   if (!attr) {
     for (const void *f : {reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, kHaloWM, 4, EPI_FWD, false, true>),
+                          reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, kHaloWM, 4, EPI_FWD, false, true, true>),
                           reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, kHaloWM, 4, EPI_DGRAD, false, true>)}) {
       const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, halo_lds_of<HaloCfg, 1>());
       if (e != hipSuccess) return e;
@@ -645,7 +721,10 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
              (use_halo ? std::to_string(HaloCfg::NW) : use_halo64 ? "" : bn == 256 ? "16" : "8") +
              ((use_halo || use_halo64) ? ",halo>" : ",lds>");
   if (use_halo) {
-    if (a.epi == EPI_FWD)
+    if (a.epi == EPI_FWD && a.pool_out != nullptr && NT == 1)
+      hipLaunchKernelGGL((conv_lds_kernel<256, 256, kHaloWM, 4, EPI_FWD, false, true, true>), g, dim3(HaloCfg::NTHR),
+                         (halo_lds_of<HaloCfg, 1>()), s, b, fw, fh, fc, MT, NT);
+    else if (a.epi == EPI_FWD)
       hipLaunchKernelGGL((conv_lds_kernel<256, 256, kHaloWM, 4, EPI_FWD, false, true>), g, dim3(HaloCfg::NTHR),
                          (halo_lds_of<HaloCfg, 1>()), s, b, fw, fh, fc, MT, NT);
     else

@@ -30,13 +30,17 @@ struct ConvArgs {
   int Bt, H, W, Csrc, N, K, Kp;
   int64_t src_rs, wt_rs, out_rs, bias_rs;  // per-replica strides (elements)
   int C;     // replica slots of the launch
+  int pool_max;  // with the per-image mean in pool_out: the mean of the 2x2 max pool (in the padding
+                 // after C, so no other field moves)
   const int32_t *rmap;  // device [C]: replica of each slot, or null (slot z = replica z)
   int epi;
   int taps;  // 9: 3x3 implicit GEMM; 1: src already holds im2col rows, A[m][k] = src[m][k]
   int res_lds;  // set by the launcher: the residual (== src) is taken from the staged centre tap
   int no_relu;  // fwd: store the raw output (a norm layer follows)
-  void *pool_out;      // fwd: also the 2x2 max pool of the output [C][Bt][H/2][W/2][N] (kernels that
-                       // report conv_fuses_pool), else null
+  void *pool_out;      // fwd: also a pooling of the output, else null: the 2x2 max pool
+                       // [C][Bt][H/2][W/2][N] (kernels that report conv_fuses_pool) or the mean over
+                       // each image's positions, of the 2x2 max pool if pool_max, [C][Bt][N] (kernels
+                       // that report conv_fuses_avg)
   int64_t pool_rs;     // its per-replica stride (elements)
 };
 
@@ -77,6 +81,10 @@ bool conv_col_ok(int dtype, const ConvArgs &a);
 hipError_t launch_conv_col(const ConvArgs &a, hipStream_t s, std::string *label);
 // whether launch_conv also writes ConvArgs::pool_out for this layer
 bool conv_fuses_pool(int dtype, const ConvArgs &a);
+// Whether launch_conv writes the per-image mean (of the 2x2 max pool if
+// pool_max) to pool_out for these arguments (16 x 16 bf16 images on the
+// 256-wide halo tile, every output channel in one tile).
+bool conv_fuses_avg(int dtype, const ConvArgs &a);
 hipError_t launch_conv_img(const ConvArgs &a, hipStream_t s, std::string *label);
 // bf16 forward / dgrad with LDS-direct tile copies (k_conv_lds.hip).
 bool conv_lds_ok(int dtype, const ConvArgs &a);

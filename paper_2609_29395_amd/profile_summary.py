@@ -45,7 +45,9 @@ def kernel_label(name: str) -> str:
         t = "bf16" if m.group(1) == "unsigned short" else "f32"
         w = int(m.group(4)) * int(m.group(5))
         return f"conv_wgrad<{t},{m.group(2)}x{m.group(3)},w{w},{'vec' if m.group(6) == 'true' else 'gather'}>"
-    m = re.search(r"conv_lds_kernel<(\d+), (\d+), (\d+), (\d+), (\d), (true|false)(, (true|false))?>", name)
+    # (an optional last flag marks the halo forward that also writes the image means)
+    m = re.search(r"conv_lds_kernel<(\d+), (\d+), (\d+), (\d+), (\d), (true|false)(, (true|false))?"
+                  r"(, (true|false))?>", name)
     if m:
         kind = "conv_fwd" if m.group(5) == "0" else "conv_dgrad"
         w = int(m.group(3)) * int(m.group(4))

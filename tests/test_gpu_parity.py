@@ -47,9 +47,14 @@ def kink_sensitive(cfg):
     of a channel the same gradient, and one ReLU decision at a pre-activation
     within bf16 rounding of zero moves a full-size entry of that layer's
     gradient (0.4 % in norm, 52 % of the maximum at one element of one
-    replica, propagating with shrinking size into the layers below)."""
+    replica, propagating with shrinking size into the layers below).  With a
+    2 x 2 max pool between the top conv and the average pool, a window whose
+    two largest values are within bf16 rounding of each other can also route
+    its gradient to the other pixel (measured: 0.6 % in norm, 2.9 % of the
+    maximum in the first layer's gradient of one replica)."""
     norm = any(sp[0] in ("bnorm", "gnorm") for sp in cfg["layers"])
-    return cfg["dtype"] == "bf16" and (norm or cfg["name"] in ("halo_res_bf16", "halo_split_bf16"))
+    return cfg["dtype"] == "bf16" and (norm or cfg["name"] in ("halo_res_bf16", "halo_split_bf16",
+                                                              "halo_maxhead_bf16"))
 
 
 def relu_flips_are_near_kinks(act_gpu, act_ref, pre_ref, rel=1e-2):
@@ -120,7 +125,8 @@ def test_sample_and_gather_bit_exact(name, window, starts):
 
 @pytest.mark.parametrize("name", ["tiny", "tiny_jsd", "ragged", "ragged_bf16", "ragged_res_bf16", "tiny_norm",
                                   "ragged_norm_bf16", "tiny_recipe", "ragged_recipe_bf16", "halo_res_bf16",
-                                  "halo_split_bf16", "img32_bf16", "col_ragged_bf16", "wide_head_bf16"])
+                                  "halo_split_bf16", "img32_bf16", "col_ragged_bf16", "wide_head_bf16",
+                                  "halo_maxhead_bf16"])
 def test_run_parity_with_fusion(name):
     cfg = get_config(name)
     T = cfg["T"]
@@ -149,7 +155,7 @@ def test_run_parity_with_fusion(name):
 
 @pytest.mark.parametrize("name", ["ragged", "ragged_bf16", "ragged_res_bf16", "tiny", "tiny_norm", "ragged_norm_bf16",
                                   "tiny_recipe", "ragged_recipe_bf16", "halo_res_bf16", "halo_split_bf16",
-                                  "img32_bf16", "col_ragged_bf16", "wide_head_bf16"])
+                                  "img32_bf16", "col_ragged_bf16", "wide_head_bf16", "halo_maxhead_bf16"])
 def test_intermediates_one_round(name):
     cfg = get_config(name)
     ctx, assignment = driver.setup(cfg)
