@@ -127,11 +127,17 @@ def _one(pattern):
 def stats(trace_dir, out_md, cmd):
     rows = list(csv.DictReader(open(_one(os.path.join(trace_dir, "**", "*kernel_stats.csv")))))
     total = sum(float(r["TotalDurationNs"]) for r in rows)
+    # instantiations that share a label (e.g. the head conv that also writes
+    # the pooled features) are one row, as in the library's own timing
+    by = collections.defaultdict(lambda: [0, 0.0])
+    for r in rows:
+        v = by[kernel_label(r["Name"])]
+        v[0] += int(r["Calls"])
+        v[1] += float(r["TotalDurationNs"])
     lines = [f"# Kernel time summary", "", f"Command: `{' '.join(cmd)}`", "",
              "| kernel (label) | calls | total ms | avg us | % |", "|---|---|---|---|---|"]
-    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
-        lines.append(f"| {kernel_label(r['Name'])} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.3f} | "
-                     f"{float(r['AverageNs']) / 1e3:.2f} | {100 * float(r['TotalDurationNs']) / total:.2f} |")
+    for lab, (calls, tot) in sorted(by.items(), key=lambda kv: -kv[1][1]):
+        lines.append(f"| {lab} | {calls} | {tot / 1e6:.3f} | {tot / calls / 1e3:.2f} | {100 * tot / total:.2f} |")
     lines += ["", f"Sum of kernel time: {total / 1e6:.3f} ms", ""]
     with open(out_md, "w") as fh:
         fh.write("\n".join(lines))
@@ -158,11 +164,17 @@ def traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload, out_
     w_fac = (sum(cw) / len(cw)) / expect_kib if cw else 1.0
     out = {"source_hashes": source_hashes(), "copy_mib": COPY_MIB, "fetch_factor": f_fac,
            "write_factor": w_fac, "kernels": {}}
-    for k in set(fetch) | set(write):
-        fv, wv = fetch.get(k, []), write.get(k, [])
+    # per label: the launches of every instantiation with that label
+    fl, wl = collections.defaultdict(list), collections.defaultdict(list)
+    for k, v in fetch.items():
+        fl[kernel_label(k)] += v
+    for k, v in write.items():
+        wl[kernel_label(k)] += v
+    for k in set(fl) | set(wl):
+        fv, wv = fl.get(k, []), wl.get(k, [])
         fk = sum(fv) / len(fv) if fv else 0.0
         wk = sum(wv) / len(wv) if wv else 0.0
-        out["kernels"][f"{workload}:{kernel_label(k)}"] = {
+        out["kernels"][f"{workload}:{k}"] = {
             "launches": max(len(fv), len(wv)), "fetch_kib": fk, "write_kib": wk,
             "bytes_per_launch": 1024.0 * (fk / f_fac + wk / w_fac)}
     with open(out_json, "w") as fh:
