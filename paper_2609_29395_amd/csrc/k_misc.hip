@@ -776,6 +776,7 @@ linear_ce_reg_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
       const float v = Wl[(int64_t)min(j, L - 1) * Ch + cl + e];
       w[j][e] = (live && j < L) ? ElemT<T>::to_f(ElemT<T>::from_f(v)) : 0.f;
     }
+  const int y0 = tid < Bt ? y[(int64_t)rep * Bt + tid] : 0;
   const int jl = (lane >> 2) & (kHeadRegL - 1);  // the logit this lane's sum ends as
   const bool writer = (lane & 3) == 0 && jl < L;
   const float bias = bl[min(jl, L - 1)];
@@ -800,14 +801,15 @@ linear_ce_reg_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
     }
   }
   __syncthreads();
-  // softmax cross-entropy per example, as in linear_ce_kernel
+  // softmax cross-entropy per example, as in linear_ce_kernel (the label of
+  // the first example of each thread was loaded at the start)
   for (int b = tid; b < Bt; b += NW * 64) {
     float m = lg[b * L];
     for (int j = 1; j < L; ++j) m = fmaxf(m, lg[b * L + j]);
     float s = 0.f;
     for (int j = 0; j < L; ++j) s += expf(lg[b * L + j] - m);
     const float lse = logf(s);
-    const int yb = y[(int64_t)rep * Bt + b];
+    const int yb = b == tid ? y0 : y[(int64_t)rep * Bt + b];
     const float qo = eps / (float)L, qy = 1.f - eps + qo;
     float zs = 0.f;
     for (int j = 0; j < L; ++j) zs += lg[b * L + j] - m;
@@ -818,16 +820,27 @@ linear_ce_reg_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
     }
   }
   __syncthreads();
-  if (tid == 0) {
-    float s = 0.f;
-    for (int b = 0; b < Bt; ++b) s += lossb[b];
-    loss[rep] = s / (float)Bt;
-  }
+  // the mean loss and the bias gradient: sums over the examples as 8
+  // interleaved partial sums added in a fixed order (8 LDS reads in flight
+  // instead of one), by the last wave, which has no more head work than
+  // the others
   float *g = grad + rep * P;
-  for (int j = tid; j < L; j += NW * 64) {
-    float s = 0.f;
-    for (int b = 0; b < Bt; ++b) s += lg[b * L + j];
-    g[b_off + j] = s;
+  if (wave == NW - 1 && lane <= L) {
+    const float *col = lane < L ? lg + lane : lossb;  // lane L: the losses
+    const int st = lane < L ? L : 1;
+    float p8[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) p8[k] = 0.f;
+    int b = 0;
+    for (; b + 8 <= Bt; b += 8)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) p8[k] += col[(b + k) * st];
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (b + k < Bt) p8[k] += col[(b + k) * st];
+    const float sm = ((p8[0] + p8[1]) + (p8[2] + p8[3])) + ((p8[4] + p8[5]) + (p8[6] + p8[7]));
+    if (lane < L) g[b_off + lane] = sm;
+    else loss[rep] = sm / (float)Bt;
   }
 
   // input gradient of each example, weight-gradient share of each wave
