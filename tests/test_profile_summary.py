@@ -1,0 +1,77 @@
+"""Host logic of the rocprofv3 summaries (no GPU): kernel names map to the
+labels the library's own timing reports, instantiations that share a label
+are merged, and the traffic figures are calibrated by the copy kernel's
+counters."""
+import csv
+import json
+import os
+
+import pytest
+
+from paper_2609_29395_amd import profile_summary as ps
+
+HALO = "void (anonymous namespace)::conv_lds_kernel<256, 256, 4, 4, 0, false, true{}>(ConvArgs, FastDiv, " \
+       "FastDiv, FastDiv, int, int)"
+
+
+@pytest.mark.parametrize("flag", ["", ", false", ", true"])
+def test_halo_forward_instantiations_share_a_label(flag):
+    # the head conv that also writes the pooled features is one more
+    # template flag on the same kernel
+    assert ps.kernel_label(HALO.format(flag)) == "conv_fwd<bf16,256x256x64,w16,halo>"
+
+
+def test_other_labels():
+    assert ps.kernel_label("void (anonymous namespace)::conv_lds_kernel<256, 64, 8, 2, 1, false, true>"
+                           "(ConvArgs, FastDiv, FastDiv, FastDiv, int, int)") == "conv_dgrad<bf16,256x64x192,w16,halo>"
+    assert ps.kernel_label("void (anonymous namespace)::conv_lds_kernel<128, 64, 2, 4, 0, false>"
+                           "(ConvArgs, FastDiv, FastDiv, FastDiv, int, int)") == "conv_fwd<bf16,128x64x64,w8,lds>"
+
+
+def _write(path, header, rows):
+    os.makedirs(os.path.dirname(path), exist_ok=True)
+    with open(path, "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(header)
+        w.writerows(rows)
+
+
+def test_stats_merges_rows_with_one_label(tmp_path):
+    d = tmp_path / "trace"
+    _write(str(d / "host" / "run_kernel_stats.csv"), ["Name", "Calls", "TotalDurationNs", "AverageNs"],
+           [[HALO.format(""), 3, 3000.0, 1000.0], [HALO.format(", true"), 1, 2000.0, 2000.0],
+            ["sgd_kernel<4>", 2, 1000.0, 500.0]])
+    out = tmp_path / "stats.md"
+    ps.stats(str(d), str(out), ["cmd"])
+    rows = [l for l in out.read_text().splitlines() if l.startswith("| conv_fwd")]
+    assert len(rows) == 1
+    cells = [c.strip() for c in rows[0].strip("|").split("|")]
+    # 4 calls, 5000 ns in all, 1250 ns = 1.25 us each, 5000 / 6000 of the time
+    assert cells[1:] == ["4", "0.005", "1.25", "83.33"]
+
+
+def _counters(path, counter, per_kernel):
+    rows = [[k, counter, v] for k, vs in per_kernel.items() for v in vs]
+    _write(path, ["Kernel_Name", "Counter_Name", "Counter_Value"], rows)
+
+
+def test_traffic_calibration_and_merge(tmp_path):
+    kib = ps.COPY_MIB * 1024.0
+    # the copy reads FETCH_SIZE = 0.5 x and writes WRITE_SIZE = 1.0 x its size
+    _counters(str(tmp_path / "cf" / "a" / "run_counter_collection.csv"), "FETCH_SIZE", {"copy": [0.5 * kib] * 3})
+    _counters(str(tmp_path / "cw" / "a" / "run_counter_collection.csv"), "WRITE_SIZE", {"copy": [kib] * 3})
+    # three plain halo forward launches and one that also writes the pooled
+    # features; counters in KiB per dispatch
+    _counters(str(tmp_path / "f" / "a" / "run_counter_collection.csv"), "FETCH_SIZE",
+              {HALO.format(""): [100.0, 100.0, 100.0], HALO.format(", true"): [140.0]})
+    _counters(str(tmp_path / "w" / "a" / "run_counter_collection.csv"), "WRITE_SIZE",
+              {HALO.format(""): [256.0, 256.0, 256.0], HALO.format(", true"): [260.0]})
+    out = tmp_path / "traffic.json"
+    ps.traffic(str(tmp_path / "f"), str(tmp_path / "w"), str(tmp_path / "cf"), str(tmp_path / "cw"), "wl", str(out))
+    t = json.loads(out.read_text())
+    assert t["fetch_factor"] == pytest.approx(0.5) and t["write_factor"] == pytest.approx(1.0)
+    k = t["kernels"]["wl:conv_fwd<bf16,256x256x64,w16,halo>"]
+    assert k["launches"] == 4
+    assert k["fetch_kib"] == pytest.approx(110.0) and k["write_kib"] == pytest.approx(257.0)
+    assert k["bytes_per_launch"] == pytest.approx(1024.0 * (110.0 / 0.5 + 257.0))
+    assert set(t["source_hashes"]) == {f for f in os.listdir(ps.CSRC) if f.endswith(".hip")}
