@@ -781,11 +781,19 @@ linear_ce_reg_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
   const bool writer = (lane & 3) == 0 && jl < L;
   const float bias = bl[min(jl, L - 1)];
 
-  // logits
+  // logits; each group of NB examples issues the next group's loads first
+  // (clamped to the last example past the end)
+  float xn[NB][4];
+#pragma unroll
+  for (int u = 0; u < NB; ++u) head_load4(hr + (int64_t)min(wave + u * NW, Bt - 1) * Ch, xn[u]);
   for (int b0 = wave; b0 < Bt; b0 += NB * NW) {
     float x[NB][4];
 #pragma unroll
-    for (int u = 0; u < NB; ++u) head_load4(hr + (int64_t)min(b0 + u * NW, Bt - 1) * Ch, x[u]);
+    for (int u = 0; u < NB; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[u][e] = xn[u][e];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) head_load4(hr + (int64_t)min(b0 + (NB + u) * NW, Bt - 1) * Ch, xn[u]);
     float v[NB][kHeadRegL], sum[NB];
 #pragma unroll
     for (int u = 0; u < NB; ++u)
@@ -850,12 +858,19 @@ linear_ce_reg_kernel(const T *__restrict__ h, const int32_t *__restrict__ y,
 #pragma unroll
     for (int e = 0; e < 4; ++e) acc[j][e] = 0.f;
   float *dhr = dh + (int64_t)rep * Bt * Ch + cl;
+#pragma unroll
+  for (int u = 0; u < NB; ++u) head_load4(hr + (int64_t)min(wave + u * NW, Bt - 1) * Ch, xn[u]);
   for (int b0 = wave; b0 < Bt; b0 += NB * NW) {
     float x[NB][4], d[NB][LM];
 #pragma unroll
+    for (int u = 0; u < NB; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[u][e] = xn[u][e];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) head_load4(hr + (int64_t)min(b0 + (NB + u) * NW, Bt - 1) * Ch, xn[u]);
+#pragma unroll
     for (int u = 0; u < NB; ++u) {
       const int b = b0 + u * NW, bc = min(b, Bt - 1);
-      head_load4(hr + (int64_t)bc * Ch, x[u]);
 #pragma unroll
       for (int j = 0; j < LM; ++j) {
         const float v = lg[bc * L + min(j, L - 1)];
