@@ -375,14 +375,14 @@ hipError_t launch_conv_img(const ConvArgs &a, hipStream_t s, std::string *label)
       hipLaunchKernelGGL((conv_img_kernel<CS, NO, EPI_DGRAD>), g, dim3(NTHR), (ImgCfg<CS, NO>::LDS), s, a, MT); \
   } while (0)
   static_assert(ImgCfg<32, 32>::FITS2 && ImgCfg<32, 64>::FITS2 && ImgCfg<64, 32>::FITS2, "two per CU");
-  static bool attr = false;
-  if (!attr) {
+  static PerDeviceOnce attr;
+  if (attr.needed()) {
     for (const void *f : {reinterpret_cast<const void *>(&conv_img_kernel<64, 32, EPI_FWD>),
                           reinterpret_cast<const void *>(&conv_img_kernel<64, 32, EPI_DGRAD>)}) {
       const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, ImgCfg<64, 32>::LDS);
       if (e != hipSuccess) return e;
     }
-    attr = true;
+    attr.mark();
   }
   if (a.Csrc == 32 && a.N == 32) IMG_GO(32, 32);
   else if (a.Csrc == 32) IMG_GO(32, 64);

@@ -669,8 +669,8 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
                                              Cfg<BM, BN, WM, WN>::LDS_BYTES);                             \
     if (e != hipSuccess) return e;                                                                        \
   }
-  static bool attr = false;
-  if (!attr) {
+  static PerDeviceOnce attr;
+  if (attr.needed()) {
     for (const void *f : {reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, kHaloWM, 4, EPI_FWD, false, true>),
                           reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, kHaloWM, 4, EPI_FWD, false, true, true>),
                           reinterpret_cast<const void *>(&conv_lds_kernel<256, 256, kHaloWM, 4, EPI_DGRAD, false, true>)}) {
@@ -688,7 +688,7 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
     CONV_LDS_ATTR(128, 64, 2, 4)
     CONV_LDS_ATTR(256, 64, 4, 2)
     CONV_LDS_ATTR(256, 32, 4, 2)
-    attr = true;
+    attr.mark();
   }
   // the narrowest weight tile that covers N (256 beyond 128); a 64-wide
   // tile over a long k loop takes 128 pixels (48 KB of LDS: three

@@ -909,24 +909,24 @@ hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *labe
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, CF::LDS_BYTES);  \
     if (e != hipSuccess) return e;                                                                           \
   }
-  static bool attr = false;
-  if (!attr) {
+  static PerDeviceOnce attr;
+  if (attr.needed()) {
     WG_ATTR(WgBig)
     WG_ATTR(WgMid)
     WG_ATTR(WgSmall)
-    attr = true;
+    attr.mark();
   }
   int BM, BN, bk, per_cu;
   wgrad_lds_tile(a.Co, a.Ci, a.H, a.W, a.taps, &BM, &BN, &bk, &per_cu);
   if (a.chunk % bk) return hipErrorInvalidValue;
   if (wgrad_img_ok(a.Co, a.Ci, a.H, a.W, a.taps)) {
     constexpr int lds = kImgStages * wi::STAGE;
-    static bool iattr = false;
-    if (!iattr) {
+    static PerDeviceOnce iattr;
+    if (iattr.needed()) {
       const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&wgrad_img_kernel<kImgStages>),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, lds);
       if (e != hipSuccess) return e;
-      iattr = true;
+      iattr.mark();
     }
     if (label) *label = "conv_wgrad<bf16,64x288,w8,img>";
     hipLaunchKernelGGL((wgrad_img_kernel<kImgStages>), dim3((uint32_t)a.splits * a.C), dim3(wi::NTHR), lds, s, a);
@@ -934,12 +934,12 @@ hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *labe
   }
   if (wgrad_halo_ok(a.Co, a.Ci, a.H, a.W, a.taps)) {
     constexpr int lds = kHaloStages * wh::STAGE;
-    static bool hattr = false;
-    if (!hattr) {
+    static PerDeviceOnce hattr;
+    if (hattr.needed()) {
       const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&wgrad_halo_kernel<kHaloStages>),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, lds);
       if (e != hipSuccess) return e;
-      hattr = true;
+      hattr.mark();
     }
     const int MT = a.Co / wh::BM, NT = a.Ci / 64;
     if (label) *label = "conv_wgrad<bf16,128x576,w8,halo>";

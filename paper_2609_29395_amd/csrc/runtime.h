@@ -4,11 +4,31 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <string>
 #include <vector>
 
 #include "../../include/gcpsl.h"
 #include "common.h"
+
+// One-time set-up that belongs to a device (kernel attributes such as the
+// dynamic LDS limit): bit d records device d; a device id past 31 (or a
+// failed query) repeats the set-up on every call, which is harmless.
+struct PerDeviceOnce {
+  std::atomic<uint32_t> done{0};
+  static int current() {
+    int d = -1;
+    return hipGetDevice(&d) == hipSuccess ? d : -1;
+  }
+  bool needed() const {
+    const int d = current();
+    return d < 0 || d >= 32 || (done.load(std::memory_order_acquire) & (1u << d)) == 0;
+  }
+  void mark() {
+    const int d = current();
+    if (d >= 0 && d < 32) done.fetch_or(1u << d, std::memory_order_acq_rel);
+  }
+};
 
 // ----------------------------------------------------------------- errors
 void gcpsl_clear_error();
