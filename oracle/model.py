@@ -48,6 +48,7 @@ gradient, and the textbook col2im scatter for the input gradient.
 from __future__ import annotations
 
 import numpy as np
+import torch
 
 from gcpsl_inputs import param_layout
 
@@ -55,14 +56,18 @@ from gcpsl_inputs import param_layout
 def round_bf16(x):
     """Round fp64 values to the nearest bf16 value, ties to even.
 
-    bf16 keeps 8 significant bits and the fp32 exponent range; below 2^-126
-    its values are multiples of 2^-133."""
-    x = np.asarray(x, dtype=np.float64)
-    m, e = np.frexp(x)
-    r = np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)
-    tiny = np.abs(x) < 2.0 ** -126
-    if np.any(tiny):
-        r = np.where(tiny, np.ldexp(np.rint(np.ldexp(x, 133)), -133), r)
+    bf16 keeps 8 significant bits and the fp32 exponent range.  For a normal
+    fp64 value that is the fp64 bit pattern with its 45 low mantissa bits
+    rounded away: add half a bf16 unit minus one plus the kept last bit (ties
+    go to the even neighbour) and clear the 45 bits; a carry out of the
+    mantissa correctly moves the value to the next binade.  Below 2^-126 bf16
+    values are multiples of 2^-133, which is rounded on its own."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    bits = torch.from_numpy(x).view(torch.int64)  # two's complement add == unsigned add
+    r = ((bits + (((bits >> 45) & 1) + ((1 << 44) - 1))) & ~((1 << 45) - 1)).view(torch.float64).numpy()
+    tiny = np.flatnonzero(np.abs(x) < 2.0 ** -126)
+    if tiny.size:
+        r.reshape(-1)[tiny] = np.ldexp(np.rint(np.ldexp(x.reshape(-1)[tiny], 133)), -133)
     return r
 
 
@@ -77,15 +82,18 @@ def rounder(dtype: str):
 # ----------------------------------------------------------------- layers
 
 def im2col3x3(x):
-    """[Bt,H,W,Ci] -> [Bt*H*W, 9*Ci], column order (kernel row, kernel col, ci)."""
+    """[Bt,H,W,Ci] -> [Bt*H*W, 9*Ci], column order (kernel row, kernel col, ci):
+    column (r, s, i) of pixel (h, w) is x[h + r - 1, w + s - 1, i], zero
+    outside the image.  (The nine shifted copies are plain element copies;
+    torch's CPU copy only spreads them over the host threads.)"""
     Bt, H, W, Ci = x.shape
-    xp = np.zeros((Bt, H + 2, W + 2, Ci))
-    xp[:, 1:-1, 1:-1, :] = x
-    cols = np.empty((Bt, H, W, 3, 3, Ci))
+    xp = torch.zeros((Bt, H + 2, W + 2, Ci), dtype=torch.float64)
+    xp[:, 1:-1, 1:-1, :] = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float64))
+    cols = torch.empty((Bt, H, W, 3, 3, Ci), dtype=torch.float64)
     for r in range(3):
         for s in range(3):
             cols[:, :, :, r, s, :] = xp[:, r:r + H, s:s + W, :]
-    return cols.reshape(Bt * H * W, 9 * Ci)
+    return cols.numpy().reshape(Bt * H * W, 9 * Ci)
 
 
 def conv3x3_forward(x, w, b):
@@ -102,12 +110,14 @@ def conv3x3_backward(x, w, gp):
     gf = gp.reshape(-1, Co)
     dw = (gf.T @ im2col3x3(x)).reshape(w.shape)
     db = gf.sum(axis=0)
-    dcols = (gf @ w.reshape(Co, -1)).reshape(Bt, H, W, 3, 3, Ci)
-    dxp = np.zeros((Bt, H + 2, W + 2, Ci))
+    dcols = torch.from_numpy((gf @ w.reshape(Co, -1)).reshape(Bt, H, W, 3, 3, Ci))
+    # col2im: each column's value added back to the input pixel it was read
+    # from, taps in (r, s) order
+    dxp = torch.zeros((Bt, H + 2, W + 2, Ci), dtype=torch.float64)
     for r in range(3):
         for s in range(3):
             dxp[:, r:r + H, s:s + W, :] += dcols[:, :, :, r, s, :]
-    return dxp[:, 1:-1, 1:-1, :], dw, db
+    return dxp[:, 1:-1, 1:-1, :].numpy(), dw, db
 
 
 def _windows(x):
@@ -121,6 +131,11 @@ def maxpool2_forward(x):
     win = _windows(x)
     arg = np.argmax(win, axis=3)
     return np.take_along_axis(win, arg[:, :, :, None, :], axis=3)[:, :, :, 0, :], arg
+
+
+def maxpool2_select(x, arg):
+    """Pooled values of x at the given window positions arg."""
+    return np.take_along_axis(_windows(x), arg[:, :, :, None, :], axis=3)[:, :, :, 0, :]
 
 
 def maxpool2_backward(gz, arg):
@@ -210,14 +225,24 @@ def unflatten(cfg, theta):
 
 # ------------------------------------------------------------- split step
 
-def split_forward_backward(cfg, theta, x, y, keep=False):
+def split_forward_backward(cfg, theta, x, y, keep=False, choose=None):
     """One cluster-local round's loss and flat gradient for one replica.
 
     theta: flat parameters (fp64 view of the fp32 master); x: [B,H,W,Cin]
     gathered images; y: [B] labels.  Returns (loss, grad[P], record) where
     record holds each bnorm layer's batch mean, biased variance and value
     count under "bn_batch" and (if keep) every intermediate tensor, keyed by
-    name."""
+    name.
+
+    The pass takes two kinds of discrete decisions: whether a ReLU passes a
+    value (its output is > 0) and which pixel of a 2 x 2 window the max pool
+    takes (the first maximum in row-major order).  Where two candidates are
+    within rounding of each other at the working precision, either decision
+    is a correct result.  choose, if given, is called at every decision as
+    choose(kind, layer, own, values) with kind "relu" (own: boolean mask of
+    the layer's output, values: its pre-activation) or "pool" (own: window
+    index per pooled value, values: the windows [Bt, H/2, W/2, 4, C]) and
+    returns the decision the pass then follows."""
     rnd = rounder(cfg["dtype"])
     layers = cfg["layers"]
     p = unflatten(cfg, np.asarray(theta, dtype=np.float64))
@@ -225,7 +250,14 @@ def split_forward_backward(cfg, theta, x, y, keep=False):
     acts = [rnd(x)]
     args = {}
     norm = {}
+    mask = {}
     rec["bn_batch"] = {}
+
+    def relu(i, v):
+        own = rnd(np.maximum(v, 0.0)) > 0
+        mask[i] = own if choose is None else np.asarray(choose("relu", i, own, v), dtype=bool)
+        return rnd(np.where(mask[i], v, 0.0))
+
     for i, spec in enumerate(layers):
         a = acts[-1]
         kind = spec[0]
@@ -236,7 +268,7 @@ def split_forward_backward(cfg, theta, x, y, keep=False):
             if keep:
                 rec[f"pre{i}"] = pre
             normed = i + 1 < len(layers) and layers[i + 1][0] in ("bnorm", "gnorm")
-            out = rnd(pre) if normed else rnd(np.maximum(pre, 0.0))
+            out = rnd(pre) if normed else relu(i, pre)
         elif kind in ("bnorm", "gnorm"):
             groups = spec[2] if kind == "gnorm" else None
             u, x_hat, rstd, mean, var = norm_forward(a, p[i]["w"], p[i]["b"], groups)
@@ -245,9 +277,12 @@ def split_forward_backward(cfg, theta, x, y, keep=False):
                 rec["bn_batch"][i] = (mean, var, a.shape[0] * a.shape[1] * a.shape[2])
             if keep:
                 rec[f"pre{i}"] = u
-            out = rnd(np.maximum(u, 0.0))
+            out = relu(i, u)
         elif kind == "maxpool":
             out, args[i] = maxpool2_forward(a)
+            if choose is not None:
+                args[i] = np.asarray(choose("pool", i, args[i], _windows(a)))
+                out = maxpool2_select(a, args[i])
         elif kind == "avgpool":
             out = rnd(a.mean(axis=(1, 2)))
         elif kind == "linear":
@@ -259,6 +294,8 @@ def split_forward_backward(cfg, theta, x, y, keep=False):
     if keep:
         rec["acts"] = acts
         rec["dlogits"] = g
+        rec["relu_mask"] = mask
+        rec["pool_arg"] = args
     grad = np.zeros(len(theta))
     gview = unflatten(cfg, grad)
     for i in range(len(layers) - 1, -1, -1):
@@ -275,7 +312,7 @@ def split_forward_backward(cfg, theta, x, y, keep=False):
         elif kind == "maxpool":
             g = maxpool2_backward(g, args[i])
         elif kind in ("bnorm", "gnorm"):
-            du = rnd(g * (a_out > 0))
+            du = rnd(g * mask[i])
             if keep:
                 rec[f"gpre{i}"] = du
             x_hat, rstd, groups = norm[i]
@@ -285,7 +322,7 @@ def split_forward_backward(cfg, theta, x, y, keep=False):
             g = rnd(dz)
         elif kind == "conv":
             normed = i + 1 < len(layers) and layers[i + 1][0] in ("bnorm", "gnorm")
-            gp = g if normed else rnd(g * (a_out > 0))
+            gp = g if normed else rnd(g * mask[i])
             if keep:
                 rec[f"gpre{i}"] = gp
             dx, dw, db = conv3x3_backward(a_in, rnd(p[i]["w"]), gp)

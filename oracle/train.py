@@ -127,18 +127,21 @@ class GCPSLOracle:
             st[off + ch:off + 2 * ch] = rv.astype(np.float32)
             st[off + 2 * ch] = np.float32(cnt)
 
-    def round(self, step, replicas=None):
+    def round(self, step, replicas=None, choose=None):
         """One local round for the given replicas (default: all).
 
         Returns (losses, grads) per replica; updates theta / momentum and
-        records |A_{n,t}| for every cluster when all replicas ran."""
+        records |A_{n,t}| for every cluster when all replicas ran.
+        choose: optional {replica: decision callback} handed to
+        split_forward_backward (the discrete decisions at near-ties)."""
         cfg = self.cfg
         reps = range(cfg["C"]) if replicas is None else replicas
         losses, grads, active = {}, {}, {}
         for n in reps:
             idx, x, y = self.batch(step, n)
             active[n] = active_clients(idx, self.coe)
-            loss, g, rec = split_forward_backward(cfg, self.theta[n], x, y)
+            loss, g, rec = split_forward_backward(cfg, self.theta[n], x, y,
+                                                  choose=None if choose is None else choose.get(n))
             sgd_update(self.theta[n], self.mom[n], g, *sgd_args(cfg))
             self._update_norm_state(n, rec["bn_batch"])
             losses[n], grads[n] = loss, g
@@ -156,9 +159,10 @@ class GCPSLOracle:
             for n in range(self.cfg["C"]):
                 self.norm[n] = fused_norm.copy()
 
-    def slot(self, s):
+    def slot(self, s, choose=None):
         """Slot s of the epoch-barrier schedule; fuses after the epoch's last
-        slot.  Returns {cluster: loss} of the clusters that took a round."""
+        slot.  Returns {cluster: loss} of the clusters that took a round.
+        choose: as for round()."""
         cfg = self.cfg
         rounds, R = epoch_rounds(self.weights, cfg["B"])
         m, t = divmod(s, R)
@@ -167,7 +171,8 @@ class GCPSLOracle:
             if t < rounds[n]:
                 idx, x, y = self.batch(m * rounds[n] + t, n)
                 active.append(active_clients(idx, self.coe))
-                loss, g, rec = split_forward_backward(cfg, self.theta[n], x, y)
+                loss, g, rec = split_forward_backward(cfg, self.theta[n], x, y,
+                                                      choose=None if choose is None else choose.get(n))
                 sgd_update(self.theta[n], self.mom[n], g, *sgd_args(cfg))
                 self._update_norm_state(n, rec["bn_batch"])
                 losses[n] = loss

@@ -4,7 +4,10 @@ Bar: bit-exact on sampled indices, labels, gathered inputs (as values),
 cluster assignments, participation counts and fusion of given replicas;
 floating point within tol = 1e-4 (fp32 workloads) or 2e-2 (bf16 workloads),
 tested per tensor as ||a - b||_2 <= tol ||b||_2 and max|a - b| <= tol max|b|,
-and elementwise relative for the per-cluster losses.
+and elementwise relative for the per-cluster losses.  Every round's oracle
+runs under the GPU's ReLU and max-pool decisions, each one that differs from
+the oracle's own first checked to be a near-tie of the oracle's values
+(gpu_match); no tensor is exempt from the comparison.
 """
 import numpy as np
 import pytest
@@ -15,63 +18,12 @@ from oracle.model import im2col3x3, round_bf16, split_forward_backward
 from oracle.sampler import active_clients, batch_indices, cluster_examples
 from oracle.train import GCPSLOracle, fuse as oracle_fuse
 
+from gpu_match import TOL, GpuChoices, LazyChoices, close, compare_params, layer_shapes, master_ulp, replica_tensor
+from gpu_match import to_np as _np
+
 pytestmark = pytest.mark.gpu
 
 from paper_2609_29395_amd import driver, gcpsl  # noqa: E402
-
-TOL = {"f32": 1e-4, "bf16": 2e-2}
-
-
-def close(a, b, tol):
-    a = np.asarray(a, dtype=np.float64).ravel()
-    b = np.asarray(b, dtype=np.float64).ravel()
-    assert a.shape == b.shape, (a.shape, b.shape)
-    nb = np.linalg.norm(b)
-    err = np.linalg.norm(a - b)
-    mx = np.abs(b).max() if b.size else 0.0
-    ok = err <= tol * nb + 1e-30 and np.abs(a - b).max() <= tol * mx + 1e-30
-    return ok, (err / (nb + 1e-30), np.abs(a - b).max() / (mx + 1e-30))
-
-
-def kink_sensitive(cfg):
-    """bf16 workloads with norm layers: a norm centres its output at zero, so
-    the ReLU after it cuts at the mode of the distribution and a one-ulp
-    difference upstream (fp32 kernels against the fp64 oracle) flips its
-    decision for ~0.1 % of the values; each flip changes that gradient entry
-    completely and the norm's backward spreads it over the channel.  Losses,
-    parameters, normalisation state, forward activations and the parameter
-    gradient stay within the bf16 bar; the per-element backward tensors and
-    the momentum (the accumulated gradients) are held to the flip check
-    below instead.  The same holds for the 16 x 16 residual workload without
-    a max pool: its top conv feeds the average pool, which hands every pixel
-    of a channel the same gradient, and one ReLU decision at a pre-activation
-    within bf16 rounding of zero moves a full-size entry of that layer's
-    gradient (0.4 % in norm, 52 % of the maximum at one element of one
-    replica, propagating with shrinking size into the layers below).  With a
-    2 x 2 max pool between the top conv and the average pool, a window whose
-    two largest values are within bf16 rounding of each other can also route
-    its gradient to the other pixel (measured: 0.6 % in norm, 2.9 % of the
-    maximum in the first layer's gradient of one replica)."""
-    norm = any(sp[0] in ("bnorm", "gnorm") for sp in cfg["layers"])
-    return cfg["dtype"] == "bf16" and (norm or cfg["name"] in ("halo_res_bf16", "halo_split_bf16",
-                                                              "halo_maxhead_bf16"))
-
-
-def relu_flips_are_near_kinks(act_gpu, act_ref, pre_ref, rel=1e-2):
-    """Every ReLU decision where GPU and oracle differ is at a pre-activation
-    within rel of the tensor's largest magnitude of zero; returns the count."""
-    diff = (np.asarray(act_gpu).ravel() > 0) != (np.asarray(act_ref).ravel() > 0)
-    pre = np.asarray(pre_ref).ravel()
-    bad = np.abs(pre[diff.ravel()]) > rel * np.abs(pre).max()
-    assert not bad.any(), (int(bad.sum()), pre[diff.ravel()][bad][:5])
-    return int(diff.sum())
-
-
-def _np(t):
-    if t.dtype == torch.bfloat16:
-        t = t.float()
-    return t.cpu().numpy()
-
 
 # ---------------------------------------------------------------- sampling
 
@@ -123,34 +75,66 @@ def test_sample_and_gather_bit_exact(name, window, starts):
 
 # ------------------------------------------------------- multi-step runs
 
+def matched_run(cfg, T, F=None, log=None):
+    """T rounds on the GPU, one at a time, fusing after every F-th; the oracle
+    runs the same rounds under the GPU's validated decisions.  Returns the
+    context, the oracle, the initial parameters, the GPU losses [T][C] and
+    the number of decisions that differed."""
+    F = cfg["F"] if F is None else F
+    C = cfg["C"]
+    ctx, assignment = driver.setup(cfg, max_steps=T)
+    o = GCPSLOracle(cfg, cluster_of_client=assignment)
+    theta0 = ctx.theta[0].cpu().numpy().astype(np.float64)
+    losses = torch.zeros(T, C, device="cuda")
+    flips, worst = 0, 0.0
+    for s in range(T):
+        ctx.sample(s)
+        ctx.step(s, losses[s])
+        torch.cuda.synchronize()
+        ch = LazyChoices(ctx, cfg)
+        o.round(s, choose=ch)
+        flips += sum(sum(c.flips.values()) for c in ch.values())
+        worst = max([worst] + [c.worst for c in ch.values()])
+        if F and (s + 1) % F == 0:
+            ctx.fuse()
+            o.fuse()
+        if log:
+            log(f"round {s + 1}/{T} done, {flips} decisions at near-ties so far "
+                f"(largest distance {worst:.2e} of the tensor's scale)")
+    torch.cuda.synchronize()
+    return ctx, o, theta0, losses.cpu().numpy(), flips
+
+
+def check_run(ctx, o, theta0, losses, cfg):
+    """Losses of every round (elementwise), then per replica the parameters,
+    the update theta_T - theta_0 and the momentum, each layer's weight and bias
+    on its own; the normalisation state; participation bit-exact."""
+    tol = TOL[cfg["dtype"]]
+    want_l = np.array(o.losses)
+    assert np.all(np.abs(losses - want_l) <= tol * np.abs(want_l)), (losses, want_l)
+    th, mo = ctx.theta.cpu().numpy(), ctx.mom.cpu().numpy()
+    for n in range(cfg["C"]):
+        ok, e = close(th[n], o.theta[n], tol)
+        assert ok, ("theta", n, e)
+        compare_params(th[n] - theta0, o.theta[n] - theta0, cfg, tol, ("update", n), ulp=master_ulp(o.theta[n]))
+        compare_params(mo[n], o.mom[n], cfg, tol, ("momentum", n))
+        if ctx.S:  # batch-norm running statistics, fused with the parameters
+            ok, e = close(ctx.norm_state[n].cpu().numpy(), o.norm[n], tol)
+            assert ok, ("norm state", n, e)
+    a, t, per = ctx.participation()
+    assert t == cfg["K"] * len(losses)
+    assert np.array_equal(per, np.array(o.active)) and a == int(np.sum(o.active))
+
+
 @pytest.mark.parametrize("name", ["tiny", "tiny_jsd", "ragged", "ragged_bf16", "ragged_res_bf16", "tiny_norm",
                                   "ragged_norm_bf16", "tiny_recipe", "ragged_recipe_bf16", "halo_res_bf16",
                                   "halo_split_bf16", "img32_bf16", "col_ragged_bf16", "wide_head_bf16",
                                   "halo_maxhead_bf16"])
 def test_run_parity_with_fusion(name):
     cfg = get_config(name)
-    T = cfg["T"]
-    ctx, assignment = driver.setup(cfg)
-    losses = torch.zeros(T, cfg["C"], device="cuda")
-    driver.train(ctx, T, losses=losses)
-    torch.cuda.synchronize()
-    ref = GCPSLOracle(cfg, cluster_of_client=assignment).run(T)
-    tol = TOL[cfg["dtype"]]
-    got_l, want_l = losses.cpu().numpy(), np.array(ref.losses)
-    assert np.all(np.abs(got_l - want_l) <= tol * np.abs(want_l)), (got_l, want_l)
-    th, mo = ctx.theta.cpu().numpy(), ctx.mom.cpu().numpy()
-    for n in range(cfg["C"]):
-        ok, e = close(th[n], ref.theta[n], tol)
-        assert ok, ("theta", n, e)
-        if not kink_sensitive(cfg):
-            ok, e = close(mo[n], ref.mom[n], tol)
-            assert ok, ("momentum", n, e)
-        if ctx.S:  # batch-norm running statistics, fused with the parameters
-            ok, e = close(ctx.norm_state[n].cpu().numpy(), ref.norm[n], tol)
-            assert ok, ("norm state", n, e)
-    a, t, per = ctx.participation()
-    assert t == cfg["K"] * T
-    assert np.array_equal(per, np.array(ref.active)) and a == int(np.sum(ref.active))
+    ctx, o, theta0, losses, flips = matched_run(cfg, cfg["T"])
+    print(f"{name}: {flips} decisions at near-ties", flush=True)
+    check_run(ctx, o, theta0, losses, cfg)
 
 
 @pytest.mark.parametrize("name", ["ragged", "ragged_bf16", "ragged_res_bf16", "tiny", "tiny_norm", "ragged_norm_bf16",
@@ -166,34 +150,30 @@ def test_intermediates_one_round(name):
     o = GCPSLOracle(cfg, cluster_of_client=assignment)
     tol = TOL[cfg["dtype"]]
     C = cfg["C"]
+    layers = cfg["layers"]
+    shapes = layer_shapes(cfg)
     grads = _np(ctx.tensor("grad")).reshape(C, -1)
     for n in range(C):
         idx, x, y = o.batch(0, n)
-        l, g, rec = split_forward_backward(cfg, o.theta[n], x, y, keep=True)
+        ch = GpuChoices(ctx, cfg, n)
+        l, g, rec = split_forward_backward(cfg, o.theta[n], x, y, keep=True, choose=ch)
         assert abs(loss[n].item() - l) <= tol * abs(l)
-        for i, spec in enumerate(cfg["layers"]):
-            name_i = f"act{i}"
-            try:
-                t = _np(ctx.tensor(name_i)).reshape(C, -1)[n]
-            except gcpsl.GCPSLError:
-                t = None
-            if t is not None and spec[0] != "linear":
-                ok, e = close(t, rec["acts"][i + 1], tol)
-                assert ok, (name_i, n, e)
-            if kink_sensitive(cfg):
-                relu_after = spec[0] in ("bnorm", "gnorm") or (
-                    spec[0] == "conv" and not (i + 1 < len(cfg["layers"]) and cfg["layers"][i + 1][0] in ("bnorm", "gnorm")))
-                if relu_after and t is not None:
-                    relu_flips_are_near_kinks(t, rec["acts"][i + 1], rec[f"pre{i}"])
-                continue
+        for i, spec in enumerate(layers):
+            if spec[0] != "linear":
+                t = replica_tensor(ctx, f"act{i}", n, shapes[i])
+                if t is not None:
+                    ok, e = close(t, rec["acts"][i + 1], tol)
+                    assert ok, (f"act{i}", n, e)
             if spec[0] in ("conv", "bnorm", "gnorm"):
                 ok, e = close(_np(ctx.tensor(f"gpre{i}")).reshape(C, -1)[n], rec[f"gpre{i}"], tol)
                 assert ok, (f"gpre{i}", n, e)
-                if i > 0 and cfg["layers"][i - 1][0] == "maxpool":
+                if i > 0 and layers[i - 1][0] == "maxpool":
                     ok, e = close(_np(ctx.tensor(f"gin{i}")).reshape(C, -1)[n], rec[f"gin{i}"], tol)
                     assert ok, (f"gin{i}", n, e)
         ok, e = close(grads[n], g, tol)
         assert ok, ("grad", n, e)
+        compare_params(grads[n], g, cfg, tol, ("grad", n))
+        print(f"{name} replica {n}: decisions at near-ties {ch.flips}, largest distance {ch.worst:.2e}", flush=True)
 
 
 @pytest.mark.parametrize("term", [dict(weight_decay=0.05), dict(nesterov=True), dict(label_smoothing=0.3),
@@ -294,86 +274,44 @@ def test_fuse_replicas_large_sampled_and_identity():
 
 # ------------------------------------------------ full sizes, sampled outputs
 
-def _windows(a, shape):
-    Bt, H, W, Ch = shape
-    return (np.asarray(a).reshape(Bt, H // 2, 2, W // 2, 2, Ch).transpose(0, 1, 3, 5, 2, 4)
-            .reshape(-1, 4))
-
-
-def routing_flips(act_ref, gpre_gpu, gpre_ref, shape, tie):
-    """Windows where the GPU routes a max-pool gradient to another pixel than
-    the oracle.  Where rounding decides between two pixels whose values are
-    within (rel, abs) = tie of each other -- rel of the window maximum, abs of
-    the tensor's largest value, since a one-ulp difference in an upstream
-    input moves every later value by an amount set by that scale -- both
-    choices are correct; any other difference is a bug.  Returns the number
-    of (valid) flips."""
-    rel, absolute = tie
-    A = _windows(act_ref, shape)
-    G = _windows(gpre_gpu, shape) != 0
-    R = _windows(gpre_ref, shape) != 0
-    bad = np.flatnonzero((G != R).any(axis=1))
-    scale = np.abs(A).max()
-    for w in bad:
-        top = A[w].max()
-        chosen = np.flatnonzero(G[w] | R[w])
-        # every pixel either side picked is (within rounding) a maximum of its
-        # window, or a ReLU-clamped value near zero
-        assert np.all(top - A[w][chosen] <= rel * abs(top) + absolute * scale), \
-            (w, A[w], G[w], R[w])
-    return len(bad)
-
-
 @pytest.mark.parametrize("name", ["gpsl", "gcpsl4", "gcpsl8", "gcpsl16"])
 def test_full_size_round_sampled_replicas(name):
     """One round at the workload's real size; replicas 0 and C-1 recomputed by
-    the oracle.  Forward activations, loss and the updated parameters are held
-    to the parity bar.  Gradients are held to it too unless a max-pool routing
-    decision flipped at a near-tie (checked valid above); one such flip moves
-    |dL/dz| / npos to a neighbouring pixel and was measured at 2e-4 relative on
-    the 64-example gradient, so the gradient bound then widens to 5e-3 (fp32)."""
+    the oracle under the GPU's validated decisions: forward activations of
+    every conv, loss, each layer's weight and bias gradient and the update."""
     cfg = get_config(name)
     ctx, assignment = driver.setup(cfg)
     C = cfg["C"]
+    theta0 = ctx.theta[0].cpu().numpy().astype(np.float64)
     ctx.sample(0)
     loss = torch.zeros(C, device="cuda")
     ctx.step(0, loss)
     torch.cuda.synchronize()
     tol = TOL[cfg["dtype"]]
-    # fp32: a few ulp (2^-23) of the window max plus 1e-6 of the scale;
-    # bf16: one ulp is 2^-8 = 3.9e-3, so 2e-2 of the max and 1e-3 of the scale
-    tie = (1e-5, 1e-6) if cfg["dtype"] == "f32" else (2e-2, 1e-3)
     o = GCPSLOracle(cfg, cluster_of_client=assignment)
     grads = _np(ctx.tensor("grad")).reshape(C, -1)
     th = ctx.theta.cpu().numpy()
     layers = cfg["layers"]
+    shapes = layer_shapes(cfg)
     for n in sorted({0, C - 1}):
         idx, x, y = o.batch(0, n)
-        l, g, rec = split_forward_backward(cfg, o.theta[n], x, y, keep=True)
+        ch = GpuChoices(ctx, cfg, n)
+        l, g, rec = split_forward_backward(cfg, o.theta[n], x, y, keep=True, choose=ch)
         assert abs(loss[n].item() - l) <= tol * abs(l), (n, loss[n].item(), l)
-        flips = 0
         for i, spec in enumerate(layers):
             if spec[0] != "conv":
                 continue
-            act = _np(ctx.tensor(f"act{i}")).reshape(C, -1)[n]
+            act = replica_tensor(ctx, f"act{i}", n, shapes[i])
             ok, e = close(act, rec["acts"][i + 1], tol)
             assert ok, (f"act{i}", n, e)
-            if i + 1 < len(layers) and layers[i + 1][0] == "maxpool":
-                shape = rec["acts"][i + 1].shape
-                gp = _np(ctx.tensor(f"gpre{i}")).reshape(C, -1)[n]
-                flips += routing_flips(rec["acts"][i + 1], gp, rec[f"gpre{i}"], shape, tie)
-        gtol = tol if (flips == 0 or cfg["dtype"] == "bf16") else 5e-3
-        ok, e = close(grads[n], g, gtol)
-        assert ok, ("grad", n, flips, e)
-        # and each layer's weight and bias gradient on its own (a mistake in
-        # one layer's kernel cannot hide behind the others' magnitudes)
-        for li, tag, shp, off in param_layout(cfg):
-            size = int(np.prod(shp))
-            ok, e = close(grads[n][off:off + size], g[off:off + size], gtol)
-            assert ok, ("grad", li, tag, n, flips, e)
-        want = o.theta[n].astype(np.float64) - cfg["lr"] * g
-        ok, e = close(th[n], want, tol)
-        assert ok, ("theta", n, e)
+        ok, e = close(grads[n], g, tol)
+        assert ok, ("grad", n, ch.flips, e)
+        compare_params(grads[n], g, cfg, tol, ("grad", n))
+        # v = g after one round from v = 0, so theta_1 = theta_0 - lr g, stored
+        # as an fp32 master on both sides
+        want = (theta0 - cfg["lr"] * g).astype(np.float32).astype(np.float64)
+        compare_params(th[n] - theta0, want - theta0, cfg, tol, ("update", n), ulp=master_ulp(want))
+        print(f"{name} replica {n}: decisions at near-ties {ch.flips}, largest distance {ch.worst:.2e}", flush=True)
     # participation of the round, every cluster
     a, t, per = ctx.participation()
     coe = make_dataset(cfg)[2]

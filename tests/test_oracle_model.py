@@ -369,3 +369,69 @@ def test_split_step_finite_differences_with_norm_layers():
         tm[j] -= h
         fd = (split_forward_backward(cfg, tp, x, y)[0] - split_forward_backward(cfg, tm, x, y)[0]) / (2 * h)
         assert abs(fd - grad[j]) <= 1e-8 + 1e-6 * abs(grad[j]), (j, fd, grad[j])
+
+
+def test_choose_with_own_decisions_changes_nothing():
+    # a decision callback that returns the oracle's own decisions reproduces
+    # the plain pass bit for bit (every ReLU and max-pool decision consulted)
+    for name in ("ragged_bf16", "tiny_norm"):
+        cfg = get_config(name)
+        theta = init_params(cfg)
+        x, y = _batch(cfg)
+        seen = []
+
+        def own(kind, i, decision, values):
+            seen.append((kind, i))
+            return decision
+
+        l0, g0, r0 = split_forward_backward(cfg, theta, x, y, keep=True)
+        l1, g1, r1 = split_forward_backward(cfg, theta, x, y, keep=True, choose=own)
+        assert l0 == l1 and np.array_equal(g0, g1)
+        for a, b in zip(r0["acts"], r1["acts"]):
+            assert np.array_equal(a, b)
+        relus = [i for i, sp in enumerate(cfg["layers"])
+                 if sp[0] in ("bnorm", "gnorm") or (sp[0] == "conv" and not (
+                     i + 1 < len(cfg["layers"]) and cfg["layers"][i + 1][0] in ("bnorm", "gnorm")))]
+        pools = [i for i, sp in enumerate(cfg["layers"]) if sp[0] == "maxpool"]
+        assert sorted(seen) == sorted([("relu", i) for i in relus] + [("pool", i) for i in pools])
+
+
+def test_forced_decisions_give_the_gradient_of_the_fixed_decision_network():
+    # With every ReLU mask and max-pool index fixed (here: the pass's own
+    # decisions at theta with about 5 % of them overturned at random), the
+    # pass is a smooth function of theta, and its gradient must be the
+    # derivative of that function: central finite differences in fp64, with
+    # the same fixed decisions at theta +- h.
+    cfg = get_config("tiny")
+    theta = init_params(cfg).astype(np.float64)
+    x, y = _batch(cfg, seed=5)
+    rng = np.random.default_rng(11)
+    fixed = {}
+
+    def record(kind, i, decision, values):
+        d = decision.copy()
+        flip = rng.random(d.shape) < 0.05
+        if kind == "relu":
+            d[flip] = ~d[flip]
+        else:
+            d[flip] = (d[flip] + 1 + rng.integers(0, 3, size=int(flip.sum()))) % 4
+        fixed[(kind, i)] = d
+        return d
+
+    loss, grad, _ = split_forward_backward(cfg, theta, x, y, choose=record)
+
+    def replay(kind, i, decision, values):
+        return fixed[(kind, i)]
+
+    assert split_forward_backward(cfg, theta, x, y, choose=replay)[0] == loss
+    plain = split_forward_backward(cfg, theta, x, y)[1]
+    assert not np.allclose(plain, grad, rtol=1e-3)  # the overturned decisions matter
+    coords = rng.choice(len(theta), size=60, replace=False)
+    h = 1e-6
+    for j in coords:
+        tp, tm = theta.copy(), theta.copy()
+        tp[j] += h
+        tm[j] -= h
+        fd = (split_forward_backward(cfg, tp, x, y, choose=replay)[0]
+              - split_forward_backward(cfg, tm, x, y, choose=replay)[0]) / (2 * h)
+        assert abs(fd - grad[j]) <= 1e-8 + 1e-6 * abs(grad[j]), (j, fd, grad[j])
