@@ -59,6 +59,14 @@ extern "C" {
 #define GCPSL_SCHED_EPOCH 1    /* epoch barrier: a cluster takes floor(n_n/B)
                                   rounds per system epoch, then waits          */
 
+/* Categories of the logical application payload (gcpsl_payload, Sec. V-E). */
+#define GCPSL_PAYLOAD_ACTIVATIONS 0  /* cut activations and labels, client -> server */
+#define GCPSL_PAYLOAD_CUT_GRADS 1    /* cut gradients, server -> client             */
+#define GCPSL_PAYLOAD_CLIENT_GRADS 2 /* active clients' client-segment gradients    */
+#define GCPSL_PAYLOAD_CLIENT_MODEL 3 /* averaged client segment to every replica    */
+#define GCPSL_PAYLOAD_FUSION 4       /* fusion: states up, fused state down         */
+#define GCPSL_PAYLOAD_COUNT 5
+
 /* Layer kinds of the split CNN. */
 #define GCPSL_CONV3X3 1 /* 3x3, stride 1, zero pad 1, bias, ReLU            */
 #define GCPSL_MAXPOOL2 2 /* 2x2 max pool, stride 2                           */
@@ -182,12 +190,14 @@ int gcpsl_assign(int32_t K, int32_t C, int32_t rule, uint64_t seed, const int64_
 /*
  * Create a context: validates the description, builds each cluster's example
  * list (ascending global id) and its fusion weight n_n = |D_{C_n}| (Eq. 5),
- * and uploads them into the workspace (synchronous copies).  Replicas are not
+ * reads the labels back to count the data set's examples per class (the
+ * global distribution of the batch deviation, Sec. V-E), and uploads these
+ * into the workspace (synchronous copies).  Replicas are not
  * initialised here: the caller fills theta with C equal copies (Alg. 2,
  * "initialize all split-model replicas equally") and zeroes momentum_buf.
  * EINVAL if any cluster holds fewer than B examples, on null pointers,
- * out-of-range ids or a too-small workspace; EUNSUPPORTED on an unsupported
- * model shape; EHIP on a failed copy.
+ * out-of-range ids or labels or a too-small workspace; EUNSUPPORTED on an
+ * unsupported model shape or L > 4096; EHIP on a failed copy.
  */
 int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out);
 
@@ -259,6 +269,27 @@ int gcpsl_epoch_rounds(gcpsl_ctx *ctx, int64_t *rounds, int64_t *slots);
 int gcpsl_fuse(gcpsl_ctx *ctx, void *stream);
 
 /*
+ * The fusion of gcpsl_fuse in two halves (Eq. 5, Sec. IV-D), for a run whose
+ * replicas are spread over several devices: every device reduces its own
+ * replicas, the caller sums the devices' partials (e.g. an all-reduce), and
+ * every device divides by the global W and broadcasts to its replicas.
+ *   gcpsl_fuse_partial:  partial[p] = sum_n n_n theta_n[p] over this
+ *     context's replicas, in fp64, in cluster order; entries [0, P) are the
+ *     parameters, [P, P + S) the normalisation state (S = gcpsl_state_count).
+ *   gcpsl_fuse_finalise: theta_n[p] = fp32(partial[p] / W) (one division, one
+ *     rounding to nearest even) for every replica n, and the same for the
+ *     normalisation state.  W is the sum of n_n over every replica of the run
+ *     (on one device: the sum of gcpsl_cluster_sizes).
+ * partial: device [P + S] fp64, 8-byte aligned, caller-owned (written by
+ * partial, read by finalise).  On one device, partial then finalise with that
+ * device's W gives gcpsl_fuse's result bit for bit.  Asynchronous on stream;
+ * EINVAL on a null or misaligned partial or W outside [1, 2^53]; EHIP on a
+ * failed launch.
+ */
+int gcpsl_fuse_partial(gcpsl_ctx *ctx, double *partial, void *stream);
+int gcpsl_fuse_finalise(gcpsl_ctx *ctx, const double *partial, int64_t W, void *stream);
+
+/*
  * The same sample-weighted fusion (Eq. 5, Sec. IV-D) on caller-owned
  * replicas, without a context: theta_bar[p] = (sum_n weights[n] theta[n][p])
  * / W, W = sum_n weights[n], accumulated in fp64 in replica order, rounded
@@ -284,6 +315,39 @@ int gcpsl_fuse_replicas(float *theta, int32_t C, int64_t P, const int64_t *weigh
  */
 int gcpsl_participation(gcpsl_ctx *ctx, int64_t *active_slots, int64_t *total_slots,
                         int32_t *per_step);
+
+/*
+ * Batch deviation (Sec. V-E): the l1 distance sum_c |h_c / B - g_c / |D||
+ * between a batch's class distribution (h_c of its B examples in class c)
+ * and the data set's (g_c of |D|), recorded by gcpsl_sample for every batch,
+ * as the exact integer numerator sum_c |h_c |D| - B g_c| over the common
+ * denominator denom = B |D|.  Over the recorded horizon [0, T_h) (as for
+ * gcpsl_participation): sum_num = the numerators summed over every batch
+ * drawn, batches = their number (waiting clusters draw none), so the mean
+ * deviation is sum_num / (batches denom).  per_step: host [T_h][C] int64
+ * numerators, -1 where a cluster drew no batch, or NULL (caller-owned, at
+ * least max_steps * C entries).  Synchronises the device.
+ */
+int gcpsl_batch_deviation(gcpsl_ctx *ctx, int64_t *sum_num, int64_t *batches, int64_t *denom,
+                          int64_t *per_step);
+
+/*
+ * Logical application payload (Sec. V-E): bytes of the tensors handed between
+ * application endpoints over the recorded horizon [0, T_h) and the fusions
+ * so far, by category (bytes: host [GCPSL_PAYLOAD_COUNT] int64, caller-owned):
+ *   ACTIVATIONS  per local round, B cut activations (the client segment's
+ *                output, in the compute precision) and B int32 labels;
+ *   CUT_GRADS    per local round, B cut gradients (same size);
+ *   CLIENT_GRADS per local round, |A_{n,t}| client-segment gradients
+ *                (P_client fp32 entries each, Sec. III-B averaging);
+ *   CLIENT_MODEL per local round, the averaged client segment to each of
+ *                the cluster's |C_n| client replicas (P_client fp32 each);
+ *   FUSION       per fusion, every replica's P + S fp32 entries up and the
+ *                fused state down (gcpsl_fuse_partial counts the first half,
+ *                gcpsl_fuse_finalise the second).
+ * A cluster waiting at the epoch barrier adds nothing.  Synchronises.
+ */
+int gcpsl_payload(gcpsl_ctx *ctx, int64_t *bytes);
 
 /* Host copy of the per-cluster example counts n_n: sizes host [C] int64. */
 int gcpsl_cluster_sizes(gcpsl_ctx *ctx, int64_t *sizes);

@@ -42,9 +42,10 @@ from __future__ import annotations
 
 import numpy as np
 
-from gcpsl_inputs import client_stats, init_norm_state, init_params, make_dataset, norm_layout
+from gcpsl_inputs import client_stats, init_norm_state, init_params, make_dataset, norm_layout, param_counts
 
 from .assign import assign
+from .metrics import CATEGORIES, batch_deviation_numerator, class_histogram, fusion_payload, round_payload
 from .model import bn_running_update, split_forward_backward
 from .sampler import active_clients, batch_indices, cluster_examples
 
@@ -106,6 +107,20 @@ class GCPSLOracle:
         self.norm = [init_norm_state(cfg) for _ in range(cfg["C"])]
         self.active = []
         self.losses = []
+        # Sec. V-E metrics: batch deviation numerators per round and cluster
+        # (-1: no batch) over the denominator B |D|, and logical payload bytes
+        self.global_hist = class_histogram(self.labels, cfg["L"])
+        self.deviation = []
+        self.payload = {k: 0 for k in CATEGORIES}
+        self.clients_in = [int(np.sum(self.assignment == n)) for n in range(cfg["C"])]
+        self.P_client = param_counts(cfg)[0]
+
+    def _account(self, n, idx, active):
+        """Sec. V-E records of cluster n's round: its batch deviation
+        numerator (returned) and its payload (added)."""
+        for k, v in round_payload(self.cfg, active, self.clients_in[n], self.P_client).items():
+            self.payload[k] += v
+        return batch_deviation_numerator(self.labels[idx], self.global_hist)
 
     def batch(self, step, n):
         idx = batch_indices(self.ids[n], self.cfg["B"], self.cfg["seed"], n, step)
@@ -136,10 +151,12 @@ class GCPSLOracle:
         split_forward_backward (the discrete decisions at near-ties)."""
         cfg = self.cfg
         reps = range(cfg["C"]) if replicas is None else replicas
-        losses, grads, active = {}, {}, {}
+        losses, grads, active, dev = {}, {}, {}, {}
         for n in reps:
             idx, x, y = self.batch(step, n)
             active[n] = active_clients(idx, self.coe)
+            if replicas is None:
+                dev[n] = self._account(n, idx, active[n])
             loss, g, rec = split_forward_backward(cfg, self.theta[n], x, y,
                                                   choose=None if choose is None else choose.get(n))
             sgd_update(self.theta[n], self.mom[n], g, *sgd_args(cfg))
@@ -148,9 +165,12 @@ class GCPSLOracle:
         if replicas is None:
             self.active.append([active[n] for n in range(cfg["C"])])
             self.losses.append([losses[n] for n in range(cfg["C"])])
+            self.deviation.append([dev[n] for n in range(cfg["C"])])
         return losses, grads
 
     def fuse(self):
+        for k, v in fusion_payload(self.cfg["C"], len(self.theta[0]), len(self.norm[0])).items():
+            self.payload[k] += v
         fused = fuse(self.theta, self.weights)
         for n in range(self.cfg["C"]):
             self.theta[n] = fused.copy()
@@ -166,11 +186,12 @@ class GCPSLOracle:
         cfg = self.cfg
         rounds, R = epoch_rounds(self.weights, cfg["B"])
         m, t = divmod(s, R)
-        losses, active = {}, []
+        losses, active, dev = {}, [], []
         for n in range(cfg["C"]):
             if t < rounds[n]:
                 idx, x, y = self.batch(m * rounds[n] + t, n)
                 active.append(active_clients(idx, self.coe))
+                dev.append(self._account(n, idx, active[-1]))
                 loss, g, rec = split_forward_backward(cfg, self.theta[n], x, y,
                                                       choose=None if choose is None else choose.get(n))
                 sgd_update(self.theta[n], self.mom[n], g, *sgd_args(cfg))
@@ -178,7 +199,9 @@ class GCPSLOracle:
                 losses[n] = loss
             else:
                 active.append(0)  # waits at the barrier: no batch, no update
+                dev.append(-1)
         self.active.append(active)
+        self.deviation.append(dev)
         self.losses.append([losses.get(n, float("nan")) for n in range(cfg["C"])])
         if t == R - 1:
             self.fuse()

@@ -66,9 +66,10 @@ struct Plan {
   int Kc = 0;
   int64_t x_rs = 0;  // elements of one staged step: C * B * H * W * (Kc or Cin)
   int schedule = GCPSL_SCHED_LOCKSTEP;
+  int cut = 0;
   size_t off_ids = 0, off_off = 0, off_coe = 0, off_fw = 0, off_hits = 0, off_idx = 0, off_y = 0,
          off_x = 0, off_dh = 0, off_grad = 0, off_part = 0, off_dbpart = 0, off_loss = 0, off_order = 0,
-         off_ident = 0, off_npart = 0;
+         off_ident = 0, off_npart = 0, off_dev = 0, off_ghist = 0;
   size_t total = 0;
 };
 
@@ -80,6 +81,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   if (d->C > d->K) return gcpsl_fail(GCPSL_EINVAL, "C must not exceed K");
   if (d->B < 1 || d->L < 2 || d->H < 1 || d->W < 1 || d->Cin < 1)
     return gcpsl_fail(GCPSL_EINVAL, "B, L, H, W, Cin out of range");
+  if (d->L > kMaxDevClasses) return gcpsl_fail(GCPSL_EUNSUPPORTED, "L must not exceed 4096");
+  if (d->B >= (1 << 29)) return gcpsl_fail(GCPSL_EUNSUPPORTED, "B must be below 2^29");
   if (d->n_examples < 1 || d->n_examples > INT32_MAX)
     return gcpsl_fail(GCPSL_EINVAL, "n_examples must be in [1, 2^31)");
   if (d->max_steps < 1 || d->max_window < 1) return gcpsl_fail(GCPSL_EINVAL, "max_steps and max_window must be >= 1");
@@ -101,6 +104,7 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   p.schedule = d->schedule;
   p.max_steps = d->max_steps;
   p.max_window = d->max_window;
+  p.cut = d->cut;
   const int n = d->n_layers;
   p.ly.assign(n, LayerInfo());
   int H = d->H, W = d->W, c = d->Cin;
@@ -199,6 +203,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   p.off_order = take(sizeof(int32_t) * C);  // clusters by epoch rounds, descending
   p.off_ident = take(sizeof(int32_t) * C);  // 0, 1, ..., C-1
   p.off_hits = take(sizeof(int32_t) * p.max_steps * C);
+  p.off_dev = take(sizeof(int64_t) * p.max_steps * C);  // batch deviation numerators (Sec. V-E)
+  p.off_ghist = take(sizeof(int64_t) * p.L);           // examples per class in the data set
   p.off_idx = take(sizeof(int32_t) * (size_t)p.max_window * C * B);
   p.off_y = take(sizeof(int32_t) * (size_t)p.max_window * C * B);
   {
@@ -327,6 +333,8 @@ struct gcpsl_ctx {
   int64_t staged_lo = -1;
   int staged_n = 0;
   int64_t horizon = 0;
+  std::vector<int64_t> clients_in;  // |C_n|: clients of each cluster
+  int64_t fusion_bytes = 0;         // logical payload of the fusions so far (Sec. V-E)
   bool timing = false;
   std::vector<hipEvent_t> events;
   size_t next_event = 0;
@@ -454,7 +462,20 @@ extern "C" int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out) {
     sizes[n] = off[n + 1] - off[n];
     fw[n] = (double)sizes[n];
   }
+  // class histogram of the data set (batch deviation, Sec. V-E); the labels
+  // are checked here because the sampler counts them in LDS
+  std::vector<int32_t> lab(d->n_examples);
+  HIP_TRY(hipMemcpy(lab.data(), d->labels, sizeof(int32_t) * lab.size(), hipMemcpyDeviceToHost));
+  std::vector<int64_t> ghist(p.L, 0);
+  for (int64_t e = 0; e < d->n_examples; ++e) {
+    if (lab[e] < 0 || lab[e] >= p.L) return gcpsl_fail(GCPSL_EINVAL, "labels must lie in [0, L)");
+    ghist[lab[e]] += 1;
+  }
+  std::vector<int64_t> clients_in(p.C, 0);
+  for (int32_t k = 0; k < d->K; ++k) clients_in[d->cluster_of_client[k]] += 1;
   char *ws = reinterpret_cast<char *>(d->workspace);
+  HIP_TRY(hipMemcpy(ws + p.off_ghist, ghist.data(), sizeof(int64_t) * ghist.size(), hipMemcpyHostToDevice));
+  HIP_TRY(hipMemset(ws + p.off_dev, 0xff, sizeof(int64_t) * p.max_steps * p.C));  // -1: no batch recorded
   HIP_TRY(hipMemcpy(ws + p.off_ids, ids.data(), sizeof(int32_t) * ids.size(), hipMemcpyHostToDevice));
   HIP_TRY(hipMemcpy(ws + p.off_off, off.data(), sizeof(int64_t) * off.size(), hipMemcpyHostToDevice));
   HIP_TRY(hipMemcpy(ws + p.off_coe, d->client_of_example, sizeof(int32_t) * d->n_examples, hipMemcpyHostToDevice));
@@ -478,6 +499,7 @@ extern "C" int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out) {
   ctx->desc.client_of_example = nullptr;
   ctx->desc.cluster_of_client = nullptr;
   ctx->sizes = std::move(sizes);
+  ctx->clients_in = std::move(clients_in);
   ctx->R = rounds[order[0]];
   ctx->rounds = std::move(rounds);
   ctx->order = std::move(order);
@@ -517,8 +539,9 @@ extern "C" int gcpsl_sample(gcpsl_ctx *ctx, int64_t step, int32_t nsteps, int32_
   const double rows = (double)nsteps * p.C * p.B, row_elems = (double)p.H * p.W * p.Cin;
   LAUNCH_T("sample", 0.0, rows * 20.0,
            launch_sample(ctx->at<int32_t>(p.off_ids), ctx->at<int64_t>(p.off_off), ctx->at<int32_t>(p.off_coe),
-                         ctx->desc.labels, idx, ctx->at<int32_t>(p.off_y), ctx->at<int32_t>(p.off_hits), p.C, p.B,
-                         p.K, ctx->desc.seed, step, nsteps, p.max_steps,
+                         ctx->desc.labels, ctx->at<int64_t>(p.off_ghist), idx, ctx->at<int32_t>(p.off_y),
+                         ctx->at<int32_t>(p.off_hits), ctx->at<int64_t>(p.off_dev), p.C, p.B, p.K, p.L,
+                         p.n_examples, ctx->desc.seed, step, nsteps, p.max_steps,
                          p.schedule == GCPSL_SCHED_EPOCH ? ctx->R : 0, s));
   if (p.col0)
     LAUNCH_T(p.dtype == GCPSL_BF16 ? "gather_im2col<bf16>" : "gather_im2col<f32>", 0.0,
@@ -822,6 +845,41 @@ extern "C" int gcpsl_fuse(gcpsl_ctx *ctx, void *stream) {
   if (p.S > 0)
     LAUNCH_T("fuse", 2.0 * p.C * p.S, 8.0 * p.C * p.S,
              launch_fuse(ctx->desc.norm_state, ctx->at<double>(p.off_fw), wh.data(), W, p.C, p.S, s));
+  ctx->fusion_bytes += 2 * 4 * (int64_t)p.C * (p.P + p.S);
+  return GCPSL_OK;
+}
+
+extern "C" int gcpsl_fuse_partial(gcpsl_ctx *ctx, double *partial, void *stream) {
+  gcpsl_clear_error();
+  if (!ctx || !partial) return gcpsl_fail(GCPSL_EINVAL, "null argument");
+  if (reinterpret_cast<uintptr_t>(partial) % 8) return gcpsl_fail(GCPSL_EINVAL, "partial must be 8-byte aligned");
+  const Plan &p = ctx->plan;
+  std::vector<double> wh(ctx->sizes.size());
+  for (size_t n = 0; n < wh.size(); ++n) wh[n] = (double)ctx->sizes[n];
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  LAUNCH_T("fuse_partial", 2.0 * p.C * p.P, (4.0 * p.C + 8.0) * p.P,
+           launch_fuse_partial(ctx->desc.theta, partial, ctx->at<double>(p.off_fw), wh.data(), p.C, p.P, s));
+  if (p.S > 0)
+    LAUNCH_T("fuse_partial", 2.0 * p.C * p.S, (4.0 * p.C + 8.0) * p.S,
+             launch_fuse_partial(ctx->desc.norm_state, partial + p.P, ctx->at<double>(p.off_fw), wh.data(), p.C,
+                                 p.S, s));
+  ctx->fusion_bytes += 4 * (int64_t)p.C * (p.P + p.S);  // every replica's state to the fusion point
+  return GCPSL_OK;
+}
+
+extern "C" int gcpsl_fuse_finalise(gcpsl_ctx *ctx, const double *partial, int64_t W, void *stream) {
+  gcpsl_clear_error();
+  if (!ctx || !partial) return gcpsl_fail(GCPSL_EINVAL, "null argument");
+  if (reinterpret_cast<uintptr_t>(partial) % 8) return gcpsl_fail(GCPSL_EINVAL, "partial must be 8-byte aligned");
+  if (W < 1 || W > ((int64_t)1 << 53)) return gcpsl_fail(GCPSL_EINVAL, "W must lie in [1, 2^53]");
+  const Plan &p = ctx->plan;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  LAUNCH_T("fuse_finalise", (double)p.P, (8.0 + 4.0 * p.C) * p.P,
+           launch_fuse_finalise(ctx->desc.theta, partial, (double)W, p.C, p.P, s));
+  if (p.S > 0)
+    LAUNCH_T("fuse_finalise", (double)p.S, (8.0 + 4.0 * p.C) * p.S,
+             launch_fuse_finalise(ctx->desc.norm_state, partial + p.P, (double)W, p.C, p.S, s));
+  ctx->fusion_bytes += 4 * (int64_t)p.C * (p.P + p.S);  // the fused state back to every replica
   return GCPSL_OK;
 }
 
@@ -889,6 +947,55 @@ extern "C" int gcpsl_participation(gcpsl_ctx *ctx, int64_t *active_slots, int64_
   *active_slots = act;
   *total_slots = (int64_t)p.K * T;
   if (per_step && T > 0) std::copy(hits.begin(), hits.begin() + T * p.C, per_step);
+  return GCPSL_OK;
+}
+
+extern "C" int gcpsl_batch_deviation(gcpsl_ctx *ctx, int64_t *sum_num, int64_t *batches, int64_t *denom,
+                                     int64_t *per_step) {
+  gcpsl_clear_error();
+  if (!ctx || !sum_num || !batches || !denom) return gcpsl_fail(GCPSL_EINVAL, "null argument");
+  const Plan &p = ctx->plan;
+  HIP_TRY(hipDeviceSynchronize());
+  const int64_t T = ctx->horizon;
+  std::vector<int64_t> dev((size_t)std::max<int64_t>(T, 1) * p.C, -1);
+  if (T > 0) HIP_TRY(hipMemcpy(dev.data(), ctx->ws + p.off_dev, sizeof(int64_t) * T * p.C, hipMemcpyDeviceToHost));
+  int64_t sum = 0, cnt = 0;
+  for (int64_t i = 0; i < T * p.C; ++i)
+    if (dev[i] >= 0) {
+      sum += dev[i];
+      cnt += 1;
+    }
+  *sum_num = sum;
+  *batches = cnt;
+  *denom = (int64_t)p.B * p.n_examples;
+  if (per_step && T > 0) std::copy(dev.begin(), dev.begin() + T * p.C, per_step);
+  return GCPSL_OK;
+}
+
+extern "C" int gcpsl_payload(gcpsl_ctx *ctx, int64_t *bytes) {
+  gcpsl_clear_error();
+  if (!ctx || !bytes) return gcpsl_fail(GCPSL_EINVAL, "null argument");
+  const Plan &p = ctx->plan;
+  HIP_TRY(hipDeviceSynchronize());
+  const int64_t T = ctx->horizon;
+  std::vector<int32_t> hits((size_t)std::max<int64_t>(T, 1) * p.C, 0);
+  if (T > 0) HIP_TRY(hipMemcpy(hits.data(), ctx->ws + p.off_hits, sizeof(int32_t) * T * p.C, hipMemcpyDeviceToHost));
+  const LayerInfo &cl = p.ly[p.cut - 1];
+  const int64_t cut_bytes = (int64_t)cl.Ho * cl.Wo * cl.Co * p.esz;  // one example's cut activation
+  int64_t act = 0, cg = 0, up = 0, down = 0;
+  for (int64_t t = 0; t < T; ++t)
+    for (int n = 0; n < p.C; ++n) {
+      if (!takes_round(ctx, t, n)) continue;
+      act += (int64_t)p.B * (cut_bytes + 4);  // activations and labels, client -> server
+      cg += (int64_t)p.B * cut_bytes;         // cut gradients, server -> client
+      up += (int64_t)hits[t * p.C + n] * p.Pc * 4;
+      down += ctx->clients_in[n] * p.Pc * 4;
+    }
+  bytes[GCPSL_PAYLOAD_ACTIVATIONS] = act;
+  bytes[GCPSL_PAYLOAD_CUT_GRADS] = cg;
+  bytes[GCPSL_PAYLOAD_CLIENT_GRADS] = up;
+  bytes[GCPSL_PAYLOAD_CLIENT_MODEL] = down;
+  bytes[GCPSL_PAYLOAD_FUSION] = ctx->fusion_bytes;
   return GCPSL_OK;
 }
 

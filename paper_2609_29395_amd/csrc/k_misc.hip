@@ -12,7 +12,11 @@ constexpr int kMaxBitmapWords = 2048;  // clients tracked per cluster: K <= 6553
 // Eq. 1 / Eq. 3: cluster n's batch at its local round s is B distinct
 // examples of its own pool: positions [tB, (t+1)B) of the keyed permutation
 // of epoch e = s / S_n, t = s mod S_n, S_n = floor(n_n / B).  Also counts the
-// distinct clients of the batch, |A_{n,t}| (Sec. III-A).
+// distinct clients of the batch, |A_{n,t}| (Sec. III-A), and the batch
+// deviation of Sec. V-E, the l1 distance between the batch's class
+// distribution and the global one, as the exact integer numerator
+// sum_c |h_c |D| - B g_c| (over B |D|; h_c: the batch's examples of class c,
+// g_c: the data set's).
 // Lockstep schedule (R = 0): every cluster takes its round s = step at every
 // step.  Epoch-barrier schedule (R = max_n S_n slots per system epoch,
 // Sec. III-A, Sec. IV-D): step = m R + t is slot t of system epoch m; cluster
@@ -21,10 +25,13 @@ constexpr int kMaxBitmapWords = 2048;  // clients tracked per cluster: K <= 6553
 __global__ void __launch_bounds__(256)
 sample_kernel(const int32_t *__restrict__ ids, const int64_t *__restrict__ off,
               const int32_t *__restrict__ coe, const int32_t *__restrict__ labels,
-              int32_t *__restrict__ idx, int32_t *__restrict__ y, int32_t *__restrict__ hits,
-              int C, int B, int K, uint64_t seed, int64_t step0, int64_t max_steps, int64_t R) {
+              const int64_t *__restrict__ ghist, int32_t *__restrict__ idx, int32_t *__restrict__ y,
+              int32_t *__restrict__ hits, int64_t *__restrict__ dev, int C, int B, int K, int L, int64_t nex,
+              uint64_t seed, int64_t step0, int64_t max_steps, int64_t R) {
   __shared__ uint32_t bitmap[kMaxBitmapWords];
+  __shared__ int32_t hist[kMaxDevClasses];
   __shared__ int count;
+  __shared__ unsigned long long dsum;
   const int n = blockIdx.x, j = blockIdx.y, tid = threadIdx.x;
   const int64_t step = step0 + j;
   const int64_t lo = off[n];
@@ -37,20 +44,29 @@ sample_kernel(const int32_t *__restrict__ ids, const int64_t *__restrict__ off,
       idx[o] = -1;
       y[o] = -1;
     }
-    if (tid == 0 && step < max_steps) hits[step * C + n] = 0;
+    if (tid == 0 && step < max_steps) {
+      hits[step * C + n] = 0;
+      dev[step * C + n] = -1;  // no batch
+    }
     return;
   }
   const uint64_t key = gc_sample_key(seed, (uint64_t)n, (uint64_t)e);
   const int words = (K + 31) >> 5;
   for (int w = tid; w < words; w += blockDim.x) bitmap[w] = 0u;
-  if (tid == 0) count = 0;
+  for (int c = tid; c < L; c += blockDim.x) hist[c] = 0;
+  if (tid == 0) {
+    count = 0;
+    dsum = 0ull;
+  }
   __syncthreads();
   for (int i = tid; i < B; i += blockDim.x) {
     const uint32_t p = (uint32_t)(t * B + i);
     const int32_t ex = ids[lo + gc_permute(p, nn, key)];
     const int64_t o = ((int64_t)j * C + n) * B + i;
+    const int32_t lab = labels[ex];
     idx[o] = ex;
-    y[o] = labels[ex];
+    y[o] = lab;
+    if ((uint32_t)lab < (uint32_t)L) atomicAdd(&hist[lab], 1);  // labels checked at create
     const int32_t c = coe[ex];
     atomicOr(&bitmap[c >> 5], 1u << (c & 31));
   }
@@ -58,8 +74,18 @@ sample_kernel(const int32_t *__restrict__ ids, const int64_t *__restrict__ off,
   int local = 0;
   for (int w = tid; w < words; w += blockDim.x) local += __popc(bitmap[w]);
   atomicAdd(&count, local);
+  // |h_c |D| - B g_c| < 2^62 and their sum < 2^63: B |D| < 2^62 (B < 2^29, |D| < 2^31)
+  unsigned long long dl = 0ull;
+  for (int c = tid; c < L; c += blockDim.x) {
+    const int64_t d = (int64_t)hist[c] * nex - (int64_t)B * ghist[c];
+    dl += (unsigned long long)(d < 0 ? -d : d);
+  }
+  atomicAdd(&dsum, dl);
   __syncthreads();
-  if (tid == 0 && step < max_steps) hits[step * C + n] = count;
+  if (tid == 0 && step < max_steps) {
+    hits[step * C + n] = count;
+    dev[step * C + n] = (int64_t)dsum;
+  }
 }
 
 template <typename T>
@@ -1145,6 +1171,59 @@ fuse_kernel(float *__restrict__ theta, const double *__restrict__ w, FuseWeights
   }
 }
 
+// The two halves of the same fusion, for a run whose replicas are spread
+// over several devices: partial[p] = sum_n w_n theta_n[p] in fp64 in cluster
+// order (the same operations as fuse_kernel), then theta_n[p] =
+// fp32(partial[p] / W) for every replica.  A sharded run sums the devices'
+// partials in between; on one device the two halves give fuse_kernel's
+// result bit for bit.
+template <int VEC, bool KW>
+__global__ void __launch_bounds__(256)
+fuse_partial_kernel(const float *__restrict__ theta, double *__restrict__ partial, const double *__restrict__ w,
+                    FuseWeights kw, int C, int64_t P) {
+  typedef typename FVec<VEC>::T V;
+  constexpr int U = 16;
+  const int64_t nv = P / VEC;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nv;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    double acc[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] = 0.0;
+    for (int n0 = 0; n0 < C; n0 += U) {
+      V v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (n0 + u < C) v[u] = reinterpret_cast<const V *>(theta + (int64_t)(n0 + u) * P)[i];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (n0 + u < C) {
+          const double wn = KW ? kw.w[n0 + u] : w[n0 + u];
+          const float *f = reinterpret_cast<const float *>(&v[u]);
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) acc[e] += wn * (double)f[e];
+        }
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) partial[i * VEC + e] = acc[e];
+  }
+}
+
+template <int VEC>
+__global__ void __launch_bounds__(256)
+fuse_finalise_kernel(float *__restrict__ theta, const double *__restrict__ partial, double W, int C, int64_t P) {
+  typedef typename FVec<VEC>::T V;
+  const int64_t nv = P / VEC;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nv;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    V out;
+    float *o = reinterpret_cast<float *>(&out);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) o[e] = (float)(partial[i * VEC + e] / W);
+    for (int n = 0; n < C; ++n) reinterpret_cast<V *>(theta + (int64_t)n * P)[i] = out;
+  }
+}
+
 inline unsigned grid_for(int64_t n, int per = 256, unsigned cap = 65535u * 8u) {
   const int64_t g = (n + per - 1) / per;
   return (unsigned)(g < 1 ? 1 : (g > cap ? cap : g));
@@ -1153,11 +1232,12 @@ inline unsigned grid_for(int64_t n, int per = 256, unsigned cap = 65535u * 8u) {
 }  // namespace
 
 hipError_t launch_sample(const int32_t *ids, const int64_t *off, const int32_t *coe,
-                         const int32_t *labels, int32_t *idx, int32_t *y, int32_t *hits, int C,
-                         int B, int K, uint64_t seed, int64_t step0, int nsteps, int64_t max_steps,
-                         int64_t R, hipStream_t s) {
-  hipLaunchKernelGGL(sample_kernel, dim3(C, nsteps), dim3(256), 0, s, ids, off, coe, labels, idx, y,
-                     hits, C, B, K, seed, step0, max_steps, R);
+                         const int32_t *labels, const int64_t *ghist, int32_t *idx, int32_t *y, int32_t *hits,
+                         int64_t *dev, int C, int B, int K, int L, int64_t nex, uint64_t seed, int64_t step0,
+                         int nsteps, int64_t max_steps, int64_t R, hipStream_t s) {
+  if (L < 1 || L > kMaxDevClasses || K > 32 * kMaxBitmapWords) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(sample_kernel, dim3(C, nsteps), dim3(256), 0, s, ids, off, coe, labels, ghist, idx, y,
+                     hits, dev, C, B, K, L, nex, seed, step0, max_steps, R);
   return hipGetLastError();
 }
 
@@ -1376,6 +1456,48 @@ hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t P, in
 
 // One thread per VEC parameters up to 65536 workgroups (a fully resident
 // grid streams ~2 % faster than 16384 workgroups looping over the rows).
+hipError_t launch_fuse_partial(const float *theta, double *partial, const double *w_dev, const double *w_host,
+                               int C, int64_t P, hipStream_t s) {
+  const uintptr_t a = reinterpret_cast<uintptr_t>(theta);
+  FuseWeights kw{};
+  const bool by_arg = w_host && C <= kMaxArgWeights;
+  if (by_arg)
+    for (int n = 0; n < C; ++n) kw.w[n] = w_host[n];
+  else if (!w_dev)
+    return hipErrorInvalidValue;
+#define FUSE_GO(VEC)                                                                                        \
+  do {                                                                                                      \
+    const dim3 g(grid_for(P / VEC, 256, 65536));                                                           \
+    if (by_arg)                                                                                             \
+      hipLaunchKernelGGL((fuse_partial_kernel<VEC, true>), g, dim3(256), 0, s, theta, partial, w_dev, kw, C, P); \
+    else                                                                                                    \
+      hipLaunchKernelGGL((fuse_partial_kernel<VEC, false>), g, dim3(256), 0, s, theta, partial, w_dev, kw, C, P); \
+  } while (0)
+  if (P % 4 == 0 && a % 16 == 0)
+    FUSE_GO(4);
+  else if (P % 2 == 0 && a % 8 == 0)
+    FUSE_GO(2);
+  else
+    FUSE_GO(1);
+#undef FUSE_GO
+  return hipGetLastError();
+}
+
+hipError_t launch_fuse_finalise(float *theta, const double *partial, double W, int C, int64_t P, hipStream_t s) {
+  const uintptr_t a = reinterpret_cast<uintptr_t>(theta);
+#define FUSE_GO(VEC)                                                                                     \
+  hipLaunchKernelGGL((fuse_finalise_kernel<VEC>), dim3(grid_for(P / VEC, 256, 65536)), dim3(256), 0, s, \
+                     theta, partial, W, C, P)
+  if (P % 4 == 0 && a % 16 == 0)
+    FUSE_GO(4);
+  else if (P % 2 == 0 && a % 8 == 0)
+    FUSE_GO(2);
+  else
+    FUSE_GO(1);
+#undef FUSE_GO
+  return hipGetLastError();
+}
+
 hipError_t launch_fuse(float *theta, const double *w_dev, const double *w_host, double W, int C, int64_t P,
                        hipStream_t s) {
   const uintptr_t a = reinterpret_cast<uintptr_t>(theta);

@@ -113,10 +113,12 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
 // weight-gradient launcher uses for a layer; the split-K plan depends on it.
 void wgrad_tile(int dtype, int Co, int ncols, int *bm, int *bn);
 
+// Largest L the sampler's batch-deviation histogram holds (LDS, Sec. V-E).
+constexpr int kMaxDevClasses = 4096;
 hipError_t launch_sample(const int32_t *ids, const int64_t *off, const int32_t *coe,
-                         const int32_t *labels, int32_t *idx, int32_t *y, int32_t *hits,
-                         int C, int B, int K, uint64_t seed, int64_t step0, int nsteps,
-                         int64_t max_steps, int64_t R, hipStream_t s);
+                         const int32_t *labels, const int64_t *ghist, int32_t *idx, int32_t *y, int32_t *hits,
+                         int64_t *dev, int C, int B, int K, int L, int64_t nex, uint64_t seed, int64_t step0,
+                         int nsteps, int64_t max_steps, int64_t R, hipStream_t s);
 hipError_t launch_gather(const float *images, const int32_t *idx, void *x, int dtype,
                          int64_t rows, int64_t row_elems, hipStream_t s);
 // Gather with im2col: x[row][pixel][k], k = (r, s, c) < 9 Cin, zero to Kc.
@@ -187,6 +189,11 @@ hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t P, in
 constexpr int kMaxArgWeights = 64;
 hipError_t launch_fuse(float *theta, const double *w_dev, const double *w_host, double W, int C, int64_t P,
                        hipStream_t s);
+// The fusion in two halves (fp64 partial sum to a buffer, then division,
+// rounding and broadcast); the same result as launch_fuse bit for bit.
+hipError_t launch_fuse_partial(const float *theta, double *partial, const double *w_dev, const double *w_host,
+                               int C, int64_t P, hipStream_t s);
+hipError_t launch_fuse_finalise(float *theta, const double *partial, double W, int C, int64_t P, hipStream_t s);
 
 // Normalisation layers (k_norm.hip): batch norm (groups == 0) or group norm
 // over a conv's raw output z, followed by ReLU.

@@ -21,11 +21,12 @@ DTYPES = {"f32": 0, "bf16": 1}
 CONV3X3, MAXPOOL2, AVGPOOL, LINEAR, BATCHNORM, GROUPNORM = 1, 2, 3, 4, 5, 6
 RESIDUAL = 1
 SCHEDULES = {"lockstep": 0, "epoch": 1}
+PAYLOAD = ("activations", "cut_grads", "client_grads", "client_model", "fusion")  # GCPSL_PAYLOAD_* order
 
 EXPORTS = ["gcpsl_param_count", "gcpsl_state_count", "gcpsl_workspace_bytes", "gcpsl_assign", "gcpsl_create",
            "gcpsl_sample", "gcpsl_step", "gcpsl_step_replica", "gcpsl_epoch_rounds", "gcpsl_fuse",
-           "gcpsl_fuse_replicas",
-           "gcpsl_participation",
+           "gcpsl_fuse_replicas", "gcpsl_fuse_partial", "gcpsl_fuse_finalise",
+           "gcpsl_participation", "gcpsl_batch_deviation", "gcpsl_payload",
            "gcpsl_cluster_sizes", "gcpsl_tensor", "gcpsl_timing", "gcpsl_timing_read",
            "gcpsl_destroy", "gcpsl_last_error"]
 
@@ -85,7 +86,11 @@ def lib():
     L.gcpsl_epoch_rounds.argtypes = [vp, P(i64), P(i64)]
     L.gcpsl_fuse.argtypes = [vp, vp]
     L.gcpsl_fuse_replicas.argtypes = [vp, i32, i64, P(i64), vp]
+    L.gcpsl_fuse_partial.argtypes = [vp, vp, vp]
+    L.gcpsl_fuse_finalise.argtypes = [vp, vp, i64, vp]
     L.gcpsl_participation.argtypes = [vp, P(i64), P(i64), P(i32)]
+    L.gcpsl_batch_deviation.argtypes = [vp, P(i64), P(i64), P(i64), P(i64)]
+    L.gcpsl_payload.argtypes = [vp, P(i64)]
     L.gcpsl_cluster_sizes.argtypes = [vp, P(i64)]
     L.gcpsl_tensor.argtypes = [vp, C.c_char_p, P(vp), P(i64), P(i32)]
     L.gcpsl_timing.argtypes = [vp, i32]
@@ -281,6 +286,34 @@ class Context:
 
     def fuse(self, stream=None):
         _check(lib().gcpsl_fuse(self._h, _stream(stream)))
+
+    def fuse_partial(self, partial, stream=None):
+        """gcpsl_fuse_partial into a device fp64 tensor of P + S entries."""
+        if partial.numel() != self.P + self.S or partial.element_size() != 8 or not partial.is_contiguous():
+            raise ValueError("partial must be a contiguous fp64 tensor of P + S entries")
+        _check(lib().gcpsl_fuse_partial(self._h, C.c_void_p(partial.data_ptr()), _stream(stream)))
+
+    def fuse_finalise(self, partial, W, stream=None):
+        """gcpsl_fuse_finalise from a device fp64 tensor of P + S entries."""
+        if partial.numel() != self.P + self.S or partial.element_size() != 8 or not partial.is_contiguous():
+            raise ValueError("partial must be a contiguous fp64 tensor of P + S entries")
+        _check(lib().gcpsl_fuse_finalise(self._h, C.c_void_p(partial.data_ptr()), int(W), _stream(stream)))
+
+    def batch_deviation(self):
+        """(sum of numerators, batches, denominator B |D|, per-step numerators
+        [T_h][C] with -1 where no batch was drawn) of Sec. V-E's batch
+        deviation (synchronises)."""
+        sn, nb, den = C.c_int64(), C.c_int64(), C.c_int64()
+        per = np.zeros((self.desc.max_steps, self.cfg["C"]), dtype=np.int64)
+        _check(lib().gcpsl_batch_deviation(self._h, C.byref(sn), C.byref(nb), C.byref(den), _i64p(per)))
+        T = self.participation()[1] // self.cfg["K"]
+        return sn.value, nb.value, den.value, per[:T]
+
+    def payload(self):
+        """{category: bytes} of Sec. V-E's logical payload (synchronises)."""
+        out = np.zeros(len(PAYLOAD), dtype=np.int64)
+        _check(lib().gcpsl_payload(self._h, _i64p(out)))
+        return {k: int(v) for k, v in zip(PAYLOAD, out)}
 
     def participation(self):
         a, t = C.c_int64(), C.c_int64()

@@ -124,6 +124,18 @@ def check_run(ctx, o, theta0, losses, cfg):
     a, t, per = ctx.participation()
     assert t == cfg["K"] * len(losses)
     assert np.array_equal(per, np.array(o.active)) and a == int(np.sum(o.active))
+    check_metrics(ctx, o, cfg)
+
+
+def check_metrics(ctx, o, cfg):
+    """Sec. V-E metrics bit-exact: every batch's deviation numerator (-1 where
+    a cluster drew none) and the logical payload by category."""
+    sn, nb, den, per = ctx.batch_deviation()
+    want = np.array(o.deviation, dtype=np.int64)
+    assert np.array_equal(per, want), (per, want)
+    assert den == cfg["B"] * sum(o.global_hist)
+    assert sn == int(want[want >= 0].sum()) and nb == int((want >= 0).sum())
+    assert ctx.payload() == o.payload, (ctx.payload(), o.payload)
 
 
 @pytest.mark.parametrize("name", ["tiny", "tiny_jsd", "ragged", "ragged_bf16", "ragged_res_bf16", "tiny_norm",
@@ -218,6 +230,61 @@ def test_fusion_bit_exact_against_oracle_on_given_replicas():
     for n in range(cfg["C"]):
         assert np.array_equal(after[n], want)
     assert not np.array_equal(ctx.mom[0].cpu().numpy(), ctx.mom[1].cpu().numpy())
+
+
+@pytest.mark.parametrize("name", ["ragged", "tiny_norm", "gcpsl4"])
+def test_fusion_in_two_halves_equals_fusion(name):
+    """gcpsl_fuse_partial then gcpsl_fuse_finalise (the halves a sharded run
+    puts an all-reduce between) against gcpsl_fuse on the same trained
+    replicas: the fp64 partial equals the oracle's sum_n n_n theta_n bit for
+    bit, the result equals gcpsl_fuse's bit for bit (parameters and
+    normalisation state), and both count the same fusion payload."""
+    cfg = get_config(name)
+    ctx, assignment = driver.setup(cfg)
+    driver.train(ctx, 3, F=0)
+    torch.cuda.synchronize()
+    before = ctx.theta.clone()
+    ns_before = ctx.norm_state.clone() if ctx.S else None
+    assert not torch.equal(before[0], before[1])
+    sizes = ctx.cluster_sizes()
+    partial = torch.zeros(ctx.P + ctx.S, dtype=torch.float64, device="cuda")
+    ctx.fuse_partial(partial)
+    torch.cuda.synchronize()
+    got = partial.cpu().numpy()
+    th = before.cpu().numpy()
+    want = np.zeros(ctx.P)
+    for n in range(cfg["C"]):
+        want += float(sizes[n]) * th[n].astype(np.float64)
+    assert np.array_equal(got[:ctx.P], want)
+    if ctx.S:
+        ns = ns_before.cpu().numpy()
+        want_s = np.zeros(ctx.S)
+        for n in range(cfg["C"]):
+            want_s += float(sizes[n]) * ns[n].astype(np.float64)
+        assert np.array_equal(got[ctx.P:], want_s)
+    ctx.fuse_finalise(partial, int(sizes.sum()))
+    torch.cuda.synchronize()
+    halves = ctx.theta.clone()
+    halves_ns = ctx.norm_state.clone() if ctx.S else None
+    pay_halves = ctx.payload()["fusion"]
+    ctx.theta.copy_(before)
+    if ctx.S:
+        ctx.norm_state.copy_(ns_before)
+    ctx.fuse()
+    torch.cuda.synchronize()
+    assert torch.equal(ctx.theta, halves)
+    if ctx.S:
+        assert torch.equal(ctx.norm_state, halves_ns)
+    assert ctx.payload()["fusion"] == 2 * pay_halves == 4 * 4 * cfg["C"] * (ctx.P + ctx.S)
+    # a run whose replicas span other devices divides by the global W
+    ctx.fuse_finalise(partial, 2 * int(sizes.sum()))
+    torch.cuda.synchronize()
+    half = (got[:ctx.P] / (2.0 * sizes.sum())).astype(np.float32)
+    for n in range(cfg["C"]):
+        assert np.array_equal(ctx.theta[n].cpu().numpy(), half)
+    with pytest.raises(gcpsl.GCPSLError) as e:
+        ctx.fuse_finalise(partial, 0)
+    assert e.value.code == gcpsl.EINVAL
 
 
 def test_fusion_of_identical_replicas_is_identity():
@@ -352,3 +419,18 @@ def test_state_errors():
     torch.cuda.synchronize()
     with pytest.raises(gcpsl.GCPSLError):
         ctx.tensor("nope")
+
+
+def test_create_rejects_labels_outside_the_classes():
+    # the sampler counts labels per class for the batch deviation (Sec. V-E):
+    # gcpsl_create reads them back and refuses any outside [0, L)
+    from gcpsl_inputs import client_stats, init_params
+    cfg = get_config("tiny")
+    images, labels, coe = make_dataset(cfg)
+    counts, hist = client_stats(cfg, labels, coe)
+    assignment = gcpsl.assign(cfg["rule"], cfg["K"], cfg["C"], cfg["seed"], counts, hist)
+    bad = labels.copy()
+    bad[17] = cfg["L"]
+    with pytest.raises(gcpsl.GCPSLError) as e:
+        gcpsl.Context(cfg, images, bad, coe, assignment, init_params(cfg))
+    assert e.value.code == gcpsl.EINVAL and "labels" in str(e.value)

@@ -14,6 +14,7 @@ pytestmark = pytest.mark.gpu
 
 from paper_2609_29395_amd import driver, gcpsl  # noqa: E402
 from gpu_match import TOL, LazyChoices, close, compare_params, master_ulp  # noqa: E402
+from test_gpu_parity import check_metrics  # noqa: E402
 
 
 @pytest.mark.parametrize("name", ["tiny_epoch", "ragged_epoch", "ragged_bf16_epoch"])
@@ -50,6 +51,7 @@ def test_epoch_schedule_parity(name):
     a, t, per = ctx.participation()
     assert t == cfg["K"] * T
     assert np.array_equal(per, np.array(ref.active)) and a == int(np.sum(ref.active))
+    check_metrics(ctx, ref, cfg)  # waiting clusters: no batch deviation, no payload
 
 
 def test_epoch_sample_marks_waiting_clusters():
