@@ -202,6 +202,25 @@ int gcpsl_assign(int32_t K, int32_t C, int32_t rule, uint64_t seed, const int64_
 int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out);
 
 /*
+ * gcpsl_create for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same context, whose workspace is a static device array of the library
+ * (GCPSL_STATIC_WORKSPACE_BYTES per device, held from the library's load
+ * until the process ends) instead of d->workspace, which is ignored (may be
+ * NULL).  Allocates no device memory.  The caller still owns images, labels,
+ * theta, momentum_buf and norm_state.  Every later call works on the
+ * returned context as on any other.
+ * One such context per device at a time: the array is shared by every call
+ * on that device and keeps the previous context's contents (the tables that
+ * must start at zero are cleared here), so a second one would race with the
+ * first; it is refused with ESTATE until gcpsl_destroy releases the first.
+ * EINVAL when gcpsl_workspace_bytes of the description exceeds
+ * GCPSL_STATIC_WORKSPACE_BYTES; otherwise the errors of gcpsl_create.
+ */
+#define GCPSL_STATIC_WORKSPACE_BYTES (32u << 20)
+int gcpsl_create_static(const gcpsl_desc *d, gcpsl_ctx **out);
+
+/*
  * Steps.  A step is one slot of the round schedule.
  *   LOCKSTEP: at step s every cluster takes its local round s.
  *   EPOCH (the system epoch of Sec. III-A and Eq. 6 of Sec. IV-D): with
@@ -392,7 +411,8 @@ typedef struct gcpsl_kernel_stat {
 int gcpsl_timing(gcpsl_ctx *ctx, int32_t on);
 int gcpsl_timing_read(gcpsl_ctx *ctx, gcpsl_kernel_stat *out, int32_t cap, int32_t *n);
 
-/* Release the context (host metadata only; device memory is the caller's). */
+/* Release the context (host metadata only; device memory is the caller's;
+ * a context of gcpsl_create_static releases its device's static workspace). */
 void gcpsl_destroy(gcpsl_ctx *ctx);
 
 /* Thread-local description of the last error, "" if none. */

@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -334,6 +335,7 @@ struct gcpsl_ctx {
   int staged_n = 0;
   int64_t horizon = 0;
   std::vector<int64_t> clients_in;  // |C_n|: clients of each cluster
+  int static_dev = -1;              // device whose static workspace this context holds, or -1
   int64_t fusion_bytes = 0;         // logical payload of the fusions so far (Sec. V-E)
   bool timing = false;
   std::vector<hipEvent_t> events;
@@ -414,22 +416,96 @@ extern "C" int gcpsl_workspace_bytes(const gcpsl_desc *d, size_t *bytes) {
     if (e_ != hipSuccess) return gcpsl_fail(GCPSL_EHIP, std::string(#expr ": ") + hipGetErrorString(e_)); \
   } while (0)
 
+// The workspace of the allocation-free context (gcpsl_create_static): one
+// array per device, held from the library's load until the process ends.  In
+// host code `scratch` only names the symbol; its device address comes from
+// hipGetSymbolAddress, once per device with that device current.
+static __device__ __align__(256) char scratch[GCPSL_STATIC_WORKSPACE_BYTES];
+
+namespace {
+constexpr int kMaxStaticDevices = 64;
+struct StaticWorkspaces {
+  std::mutex mu;
+  char *ptr[kMaxStaticDevices] = {};   // device address of `scratch` per device
+  bool busy[kMaxStaticDevices] = {};   // a static context lives on the device
+};
+StaticWorkspaces g_static;
+
+// Claims the current device's array for one context: its address, or an
+// error (no device, lookup failed, already claimed).
+int claim_static(int *dev_out, char **ptr_out) {
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxStaticDevices) return gcpsl_fail(GCPSL_EUNSUPPORTED, "device id beyond 63");
+  std::lock_guard<std::mutex> lock(g_static.mu);
+  if (g_static.busy[dev])
+    return gcpsl_fail(GCPSL_ESTATE, "a static context already lives on device " + std::to_string(dev));
+  if (!g_static.ptr[dev]) {
+    void *a = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&a, HIP_SYMBOL(scratch)));
+    if (!a || reinterpret_cast<uintptr_t>(a) % kAlign) return gcpsl_fail(GCPSL_EHIP, "static workspace address");
+    g_static.ptr[dev] = reinterpret_cast<char *>(a);
+  }
+  g_static.busy[dev] = true;
+  *dev_out = dev;
+  *ptr_out = g_static.ptr[dev];
+  return GCPSL_OK;
+}
+
+void release_static(int dev) {
+  if (dev < 0 || dev >= kMaxStaticDevices) return;
+  std::lock_guard<std::mutex> lock(g_static.mu);
+  g_static.busy[dev] = false;
+}
+
+int create_ctx(const gcpsl_desc *d, char *ws, size_t ws_bytes, gcpsl_ctx **out);
+}  // namespace
+
 extern "C" int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out) {
   gcpsl_clear_error();
   if (!out) return gcpsl_fail(GCPSL_EINVAL, "null output");
   *out = nullptr;
+  if (!d) return gcpsl_fail(GCPSL_EINVAL, "null description");
+  if (!d->workspace) return gcpsl_fail(GCPSL_EINVAL, "null pointer in description");
+  return create_ctx(d, reinterpret_cast<char *>(d->workspace), d->workspace_bytes, out);
+}
+
+extern "C" int gcpsl_create_static(const gcpsl_desc *d, gcpsl_ctx **out) {
+  gcpsl_clear_error();
+  if (!out) return gcpsl_fail(GCPSL_EINVAL, "null output");
+  *out = nullptr;
+  Plan p;
+  if (int rc = build_plan(d, p)) return rc;
+  if (p.total > GCPSL_STATIC_WORKSPACE_BYTES)
+    return gcpsl_fail(GCPSL_EINVAL, "the description needs " + std::to_string(p.total) +
+                                        " workspace bytes, more than the static workspace's " +
+                                        std::to_string((size_t)GCPSL_STATIC_WORKSPACE_BYTES));
+  int dev = -1;
+  char *ws = nullptr;
+  if (int rc = claim_static(&dev, &ws)) return rc;
+  const int rc = create_ctx(d, ws, GCPSL_STATIC_WORKSPACE_BYTES, out);
+  if (rc) {
+    release_static(dev);
+    return rc;
+  }
+  (*out)->static_dev = dev;
+  return GCPSL_OK;
+}
+
+namespace {
+int create_ctx(const gcpsl_desc *d, char *ws, size_t ws_bytes, gcpsl_ctx **out) {
   Plan p;
   int rc = build_plan(d, p);
   if (rc) return rc;
   if (!d->client_of_example || !d->cluster_of_client || !d->images || !d->labels || !d->theta ||
-      !d->momentum_buf || !d->workspace)
+      !d->momentum_buf)
     return gcpsl_fail(GCPSL_EINVAL, "null pointer in description");
-  if (reinterpret_cast<uintptr_t>(d->workspace) % kAlign)
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign)
     return gcpsl_fail(GCPSL_EINVAL, "workspace must be 256-byte aligned");
   if (reinterpret_cast<uintptr_t>(d->theta) % 16 || reinterpret_cast<uintptr_t>(d->momentum_buf) % 16)
     return gcpsl_fail(GCPSL_EINVAL, "theta and momentum must be 16-byte aligned");
   if (p.S > 0 && !d->norm_state) return gcpsl_fail(GCPSL_EINVAL, "the model has batch norm layers: norm_state needed");
-  if (d->workspace_bytes < p.total)
+  if (ws_bytes < p.total)
     return gcpsl_fail(GCPSL_EINVAL, "workspace too small: need " + std::to_string(p.total) + " bytes");
   if (!std::isfinite(d->lr) || !std::isfinite(d->momentum)) return gcpsl_fail(GCPSL_EINVAL, "lr and momentum must be finite");
   if (!(d->weight_decay >= 0.f) || !std::isfinite(d->weight_decay))
@@ -473,7 +549,6 @@ extern "C" int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out) {
   }
   std::vector<int64_t> clients_in(p.C, 0);
   for (int32_t k = 0; k < d->K; ++k) clients_in[d->cluster_of_client[k]] += 1;
-  char *ws = reinterpret_cast<char *>(d->workspace);
   HIP_TRY(hipMemcpy(ws + p.off_ghist, ghist.data(), sizeof(int64_t) * ghist.size(), hipMemcpyHostToDevice));
   HIP_TRY(hipMemset(ws + p.off_dev, 0xff, sizeof(int64_t) * p.max_steps * p.C));  // -1: no batch recorded
   HIP_TRY(hipMemcpy(ws + p.off_ids, ids.data(), sizeof(int32_t) * ids.size(), hipMemcpyHostToDevice));
@@ -512,8 +587,13 @@ extern "C" int gcpsl_create(const gcpsl_desc *d, gcpsl_ctx **out) {
   *out = ctx;
   return GCPSL_OK;
 }
+}  // namespace
 
-extern "C" void gcpsl_destroy(gcpsl_ctx *ctx) { delete ctx; }
+extern "C" void gcpsl_destroy(gcpsl_ctx *ctx) {
+  if (!ctx) return;
+  release_static(ctx->static_dev);
+  delete ctx;
+}
 
 extern "C" int gcpsl_cluster_sizes(gcpsl_ctx *ctx, int64_t *sizes) {
   gcpsl_clear_error();

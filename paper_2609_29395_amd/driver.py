@@ -15,16 +15,16 @@ from gcpsl_inputs import client_stats, init_norm_state, init_params, make_datase
 from . import gcpsl
 
 
-def setup(cfg, max_steps=None, max_window=1, device="cuda", schedule=None):
+def setup(cfg, max_steps=None, max_window=1, device="cuda", schedule=None, static=False):
     """Inputs, Alg. 1 assignment and a Context for a workload (schedule:
-    the workload's own unless given)."""
+    the workload's own unless given; static: gcpsl_create_static)."""
     schedule = cfg.get("schedule", "lockstep") if schedule is None else schedule
     images, labels, coe = make_dataset(cfg)
     counts, hist = client_stats(cfg, labels, coe)
     assignment = gcpsl.assign(cfg["rule"], cfg["K"], cfg["C"], cfg["seed"], counts, hist)
     ctx = gcpsl.Context(cfg, images, labels, coe, assignment, init_params(cfg),
                         max_steps=max_steps, max_window=max_window, device=device, schedule=schedule,
-                        norm_state0=init_norm_state(cfg))
+                        norm_state0=init_norm_state(cfg), static=static)
     return ctx, assignment
 
 

@@ -24,6 +24,7 @@ SCHEDULES = {"lockstep": 0, "epoch": 1}
 PAYLOAD = ("activations", "cut_grads", "client_grads", "client_model", "fusion")  # GCPSL_PAYLOAD_* order
 
 EXPORTS = ["gcpsl_param_count", "gcpsl_state_count", "gcpsl_workspace_bytes", "gcpsl_assign", "gcpsl_create",
+           "gcpsl_create_static",
            "gcpsl_sample", "gcpsl_step", "gcpsl_step_replica", "gcpsl_epoch_rounds", "gcpsl_fuse",
            "gcpsl_fuse_replicas", "gcpsl_fuse_partial", "gcpsl_fuse_finalise",
            "gcpsl_participation", "gcpsl_batch_deviation", "gcpsl_payload",
@@ -80,6 +81,7 @@ def lib():
     L.gcpsl_workspace_bytes.argtypes = [P(Desc), P(C.c_size_t)]
     L.gcpsl_assign.argtypes = [i32, i32, i32, u64, P(i64), P(i64), i32, P(i32)]
     L.gcpsl_create.argtypes = [P(Desc), P(vp)]
+    L.gcpsl_create_static.argtypes = [P(Desc), P(vp)]
     L.gcpsl_sample.argtypes = [vp, i64, i32, vp, vp]
     L.gcpsl_step.argtypes = [vp, i64, vp, vp]
     L.gcpsl_step_replica.argtypes = [vp, i64, i32, vp, vp]
@@ -219,7 +221,10 @@ class Context:
     """One gcpsl_ctx with the caller-owned device buffers it works in."""
 
     def __init__(self, cfg, images, labels, client_of_example, cluster_of_client, theta0,
-                 max_steps=None, max_window=1, device="cuda", schedule="lockstep", norm_state0=None):
+                 max_steps=None, max_window=1, device="cuda", schedule="lockstep", norm_state0=None,
+                 static=False):
+        """static: gcpsl_create_static (the library's own workspace, no
+        workspace tensor here; `tensor` is then unavailable)."""
         import torch
         self.cfg = cfg
         self.schedule = schedule
@@ -238,20 +243,25 @@ class Context:
             raise ValueError(f"norm_state0 has {ns0.size} entries, the model has {self.S}")
         self.norm_state = (torch.as_tensor(ns0).to(device).reshape(1, -1).repeat(cfg["C"], 1).contiguous()
                            if self.S else None)
-        nbytes = workspace_bytes(desc)
-        self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
-        base = self.workspace.data_ptr()
-        self._ws_off = (-base) % 256
         desc.images = self.images.data_ptr()
         desc.labels = self.labels.data_ptr()
         desc.theta = self.theta.data_ptr()
         desc.momentum_buf = self.mom.data_ptr()
         desc.norm_state = self.norm_state.data_ptr() if self.S else None
-        desc.workspace = base + self._ws_off
-        desc.workspace_bytes = nbytes
+        self.static = static
+        if static:
+            self.workspace = None
+            desc.workspace, desc.workspace_bytes = None, 0
+        else:
+            nbytes = workspace_bytes(desc)
+            self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+            base = self.workspace.data_ptr()
+            desc.workspace = base + (-base) % 256
+            desc.workspace_bytes = nbytes
         self.desc = desc
         h = C.c_void_p()
-        _check(lib().gcpsl_create(C.byref(desc), C.byref(h)))
+        create = lib().gcpsl_create_static if static else lib().gcpsl_create
+        _check(create(C.byref(desc), C.byref(h)))
         self._h = h
 
     def close(self):
@@ -343,6 +353,8 @@ class Context:
     def tensor(self, name):
         """torch view of a named workspace tensor (gcpsl_tensor)."""
         import torch
+        if self.workspace is None:
+            raise ValueError("a static context's workspace is the library's own; it has no tensor view")
         ptr, n, dt = C.c_void_p(), C.c_int64(), C.c_int32()
         _check(lib().gcpsl_tensor(self._h, name.encode(), C.byref(ptr), C.byref(n), C.byref(dt)))
         tdt = {0: torch.float32, 1: torch.bfloat16, -1: torch.int32}[dt.value]
