@@ -7,13 +7,20 @@ SGD update, plus the fusion of all replicas every F rounds -- the whole path,
 on inputs already resident in HBM.  The default workload is the 16-cluster
 one: K=256 clients, C=16 label-L1 clusters, B=128 per cluster (2048 examples
 per step), bf16 activations/weights with fp32 masters, wide residual server,
-fusion every 50 rounds, synthetic CIFAR-10-shaped data.
+fusion every 50 rounds, synthetic CIFAR-10-shaped data.  The 8-cluster (bf16)
+and 4-cluster (fp32) workloads are measured the same way as sub-results.
 
 Prints one JSON line.  `value` is examples/s summed over the C clusters,
-wall clock over exactly --steps rounds bracketed by device synchronisation.
-A second, separately timed pass records hipEvents around every kernel launch
-(on the stream the kernels run on) to report the dominant kernel's roofline
-fraction.  The CPU oracle is timed on a bounded sample on the host cores.
+wall clock over exactly --steps rounds bracketed by device synchronisation;
+the window is placed so that it ends right after a fusion, so it always holds
+at least its share of fusions (exactly its share when F divides --steps).
+A second pass right after it records hipEvents around every kernel launch
+(on the stream the kernels run on) for per-kernel time; `roofline` gives the
+dominant kernel's algorithmic work over that time against the MI355X peak,
+and next to it the same fraction from the committed rocprofv3 kernel trace
+(profiles/profile.json) with the MFMA busy counters, when the kernel's source
+is unchanged since they were taken.  The CPU oracle is timed on a bounded
+sample on the host cores.
 """
 from __future__ import annotations
 
@@ -41,20 +48,11 @@ DESCRIPTIONS = {
 }
 
 
-def load_traffic(workload, kernel):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when it is absent or the kernel's source changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", "traffic.json")
-    if not os.path.exists(path):
-        return None
-    from paper_2609_29395_amd.profile_summary import file_hash, kernel_source
-    with open(path) as fh:
-        rec = json.load(fh)
-    src = kernel_source(kernel)
-    if rec.get("source_hashes", {}).get(src) != file_hash(src):
-        return None
-    entry = rec.get("kernels", {}).get(f"{workload}:{kernel}")
-    return None if entry is None else entry.get("bytes_per_launch")
+def profile(workload, kernel, kind):
+    """Figures of the committed rocprofv3 summaries, or None (absent, or the
+    kernel's source changed since)."""
+    from paper_2609_29395_amd.profile_summary import profile_entry
+    return profile_entry(workload, kernel, kind)
 
 
 def cpu_baseline(cfg, assignment, budget_s):
@@ -157,13 +155,141 @@ def hbm_probes(cfg, F, ctx_sizes):
     ctxw.timing(False)
     g = {k: v for k, v in st.items() if k.startswith("gather")}
     name, v = max(g.items(), key=lambda kv: kv[1]["bytes"])
-    gbs = v["bytes"] / (v["ms"] * 1e-3) / 1e9
-    out["gather_window"] = {"kernel": name, "steps": F, "examples": F * cfg["C"] * cfg["B"],
-                            "bytes": v["bytes"] / v["launches"], "us": round(v["ms"] * 1e3 / v["launches"], 1),
-                            "gbs": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    us = v["ms"] * 1e3 / v["launches"]
+    examples = F * cfg["C"] * cfg["B"]
+    # the gather's own work: each example's image read (fp32) and written
+    # once in the compute precision, its id and label (4 B each); what the
+    # kernel writes beyond that is staging for the first conv layer
+    px = cfg["H"] * cfg["W"] * cfg["Cin"]
+    alg = examples * (4.0 * px + (2.0 if cfg["dtype"] == "bf16" else 4.0) * px + 8.0)
+    impl = v["bytes"] / v["launches"]
+    out["gather_window"] = {"kernel": name, "steps": F, "examples": examples, "us": round(us, 1),
+                            "algorithmic_bytes": alg, "gbs": round(alg / (us * 1e-6) / 1e9, 1),
+                            "frac": round(alg / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                            "implementation_bytes": impl, "implementation_gbs": round(impl / (us * 1e-6) / 1e9, 1),
+                            "implementation_frac": round(impl / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
     del ctxw
     torch.cuda.empty_cache()
     return out
+
+
+def fusion_aligned_start(warmup, steps, F):
+    """First step index >= warmup of a window of `steps` rounds that ends
+    right after a fusion (the sampler is stateless in the step index)."""
+    if not F:
+        return warmup
+    return warmup + (-(warmup + steps)) % F
+
+
+def measure(name, steps, warmup, timing_steps, cpu_seconds, with_cpu=True, with_extras=False, args=None):
+    import torch
+    from gcpsl_inputs import get_config
+    from paper_2609_29395_amd import driver
+
+    cfg = get_config(name)
+    C, B, F = cfg["C"], cfg["B"], cfg["F"]
+    x0 = fusion_aligned_start(warmup, steps, F)
+    total = x0 + steps + timing_steps + (2 * args.control_steps if with_extras else 0)
+    print(f"bench: workload {name} C={C} B={B} F={F} warmup={warmup} steps={steps} (timed rounds "
+          f"[{x0}, {x0 + steps}))", file=sys.stderr, flush=True)
+    ctx, assignment = driver.setup(cfg, max_steps=total)
+    driver.train(ctx, warmup, start=x0 - warmup)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    driver.train(ctx, steps, start=x0)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    fusions = (x0 + steps) // F - x0 // F if F else 0
+    value = C * B * steps / dt
+    print(f"bench: timed {steps} steps ({fusions} fusions) in {dt:.3f} s", file=sys.stderr, flush=True)
+
+    # per-kernel event timing pass, right after the timed window
+    ctx.timing(True)
+    driver.train(ctx, timing_steps, start=x0 + steps)
+    ctx.fuse()  # one fusion inside the per-kernel record
+    stats = ctx.timing_read()
+    ctx.timing(False)
+    dom = max(stats, key=lambda k: stats[k]["ms"])
+    st = stats[dom]
+    peak_tf = PEAK_TFLOPS[cfg["dtype"]]
+    ridge = peak_tf * 1e12 / (PEAK_HBM_GBS * 1e9)
+    per_launch_flops = st["flops"] / st["launches"]
+    per_launch_bytes = st["bytes"] / st["launches"]
+    avg_us = st["ms"] * 1e3 / st["launches"]
+    mfma_bound = st["flops"] > 0 and st["flops"] / max(st["bytes"], 1.0) >= ridge
+    if mfma_bound:
+        achieved = per_launch_flops / (avg_us * 1e-6) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak_tf, "unit": "TFLOP/s",
+                "frac": round(achieved / peak_tf, 4)}
+    else:
+        achieved = per_launch_bytes / (avg_us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    tr = profile(name, dom, "traffic")
+    roof["traffic"] = None if tr is None else round(tr["bytes_per_launch"], 0)
+    roof["kernel"] = dom
+    roof["launches"] = st["launches"]
+    roof["avg_launch_us"] = round(avg_us, 2)
+    roof["work_per_launch"] = per_launch_flops if mfma_bound else per_launch_bytes
+    roof["timing"] = (f"hipEvent pair around every launch on the library's stream, {timing_steps} steps run "
+                      f"right after the timed window")
+    prof_t, prof_m = profile(name, dom, "trace"), profile(name, dom, "mfma")
+    if prof_t is not None:
+        rate = roof["work_per_launch"] / (prof_t["avg_us"] * 1e-6) / (1e12 if mfma_bound else 1e9)
+        roof["profile"] = {"avg_launch_us": round(prof_t["avg_us"], 2), "achieved": round(rate, 2),
+                           "frac": round(rate / roof["peak"], 4),
+                           "mfma_busy_pct": None if prof_m is None else round(prof_m["mfma_busy_pct"], 2),
+                           "counted_mfma_flops_per_launch": None if prof_m is None else
+                           prof_m["counted_flops_per_launch"],
+                           "source": f"profiles/profile.json [{name}] (rocprofv3 kernel trace and counters)"}
+    else:
+        roof["profile"] = None
+    conv = {k: v for k, v in stats.items() if k.startswith("conv_")}
+    conv_ms = sum(v["ms"] for v in conv.values())
+    conv_tf = sum(v["flops"] for v in conv.values()) / (conv_ms * 1e-3) / 1e12 if conv_ms else 0.0
+    # MFMA busy of the conv kernels from the counters, weighted by their time
+    busy = [(profile(name, k, "mfma"), v["ms"]) for k, v in conv.items()]
+    mfma_util = (round(sum(b["mfma_busy_pct"] * ms for b, ms in busy) / sum(ms for _, ms in busy), 2)
+                 if busy and all(b is not None for b, _ in busy) else None)
+    fuse = stats.get("fuse")
+    fusion_gbs = fuse["bytes"] / (fuse["ms"] * 1e-3) / 1e9 if fuse else None
+    kernel_ms = sum(v["ms"] for v in stats.values())
+    for k, v in sorted(stats.items(), key=lambda kv: -kv[1]["ms"]):
+        rate = f"{v['flops'] / (v['ms'] * 1e-3) / 1e12:8.1f} TFLOP/s" if v["flops"] > 0 else ""
+        print(f"  {k:34s} {v['launches']:5d} launches {v['ms'] / timing_steps:8.3f} ms/step "
+              f"{v['bytes'] / (v['ms'] * 1e-3) / 1e9:8.1f} GB/s {rate}", file=sys.stderr)
+    out = {
+        "value": round(value, 1), "ms_per_step": round(dt * 1e3 / steps, 4), "fusions_in_window": fusions,
+        "dtype": cfg["dtype"],
+        "config": {"workload": name, "description": DESCRIPTIONS[name], "clients": cfg["K"], "clusters": C,
+                   "batch_per_cluster": B, "global_batch": C * B, "fusion_every": F, "rule": cfg["rule"],
+                   "parallelism": "C replicas batched in every kernel, 1 GPU"},
+        "mfma_util_pct": mfma_util,
+        "conv_flops_frac_pct": round(100.0 * conv_tf / peak_tf, 2),
+        "conv_tflops": round(conv_tf, 2),
+        "fusion_gbs": None if fusion_gbs is None else round(fusion_gbs, 1),
+        "kernel_ms_per_step": round(kernel_ms / timing_steps, 4),
+        "roofline": roof,
+    }
+    if with_extras and not args.no_schedule_control:
+        out["schedule_control"] = schedule_control(cfg, ctx, x0 + steps + timing_steps, args.control_steps)
+        print(f"bench: schedule control {out['schedule_control']}", file=sys.stderr, flush=True)
+    if with_extras and not args.no_hbm_probes:
+        out["hbm"] = hbm_probes(cfg, max(F, 1), ctx.cluster_sizes())
+        if fusion_gbs is not None:
+            out["hbm"]["fusion_in_step"] = {"gbs": round(fusion_gbs, 1),
+                                            "frac": round(fusion_gbs / PEAK_HBM_GBS, 4)}
+        print(f"bench: hbm {out['hbm']}", file=sys.stderr, flush=True)
+    ctx.close()
+    del ctx
+    torch.cuda.empty_cache()
+    if with_cpu:
+        out["cpu_baseline"] = cpu_baseline(cfg, assignment, cpu_seconds)
+        print(f"bench: cpu baseline {out['cpu_baseline']}", file=sys.stderr, flush=True)
+    return out
+
+
+SUB_RESULTS = ("gcpsl8", "gcpsl4")
 
 
 def main():
@@ -180,6 +306,8 @@ def main():
     ap.add_argument("--control-steps", type=int, default=10)
     ap.add_argument("--no-hbm-probes", action="store_true",
                     help="skip the large fusion and windowed gather measurements")
+    ap.add_argument("--no-sub-results", action="store_true",
+                    help="measure only --workload (not also the 8- and 4-cluster workloads)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -188,96 +316,33 @@ def main():
         sys.exit(2)
 
     import torch
-    from gcpsl_inputs import get_config
-    from paper_2609_29395_amd import driver
-
-    cfg = get_config(args.workload)
-    C, B, F = cfg["C"], cfg["B"], cfg["F"]
-    total = args.warmup + args.steps + args.timing_steps + 2 * args.control_steps
-    print(f"bench: workload {args.workload} C={C} B={B} F={F} warmup={args.warmup} steps={args.steps}",
-          file=sys.stderr, flush=True)
     torch.cuda.set_device(0)
-    ctx, assignment = driver.setup(cfg, max_steps=total)
-    stream = torch.cuda.current_stream()
-
-    driver.train(ctx, args.warmup, start=0)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    driver.train(ctx, args.steps, start=args.warmup)
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t0
-    value = C * B * args.steps / dt
-    print(f"bench: timed {args.steps} steps in {dt:.3f} s", file=sys.stderr, flush=True)
-
-    # per-kernel event timing pass (separate from the timed region)
-    ctx.timing(True)
-    driver.train(ctx, args.timing_steps, start=args.warmup + args.steps)
-    ctx.fuse()  # one fusion inside the timed-kernel record
-    stats = ctx.timing_read()
-    ctx.timing(False)
-    nsteps = args.timing_steps
-    dom = max(stats, key=lambda k: stats[k]["ms"])
-    st = stats[dom]
-    ridge = PEAK_TFLOPS[cfg["dtype"]] * 1e12 / (PEAK_HBM_GBS * 1e9)
-    intensity = st["flops"] / max(st["bytes"], 1.0)
-    if st["flops"] > 0 and intensity >= ridge:
-        achieved = st["flops"] / (st["ms"] * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS[cfg["dtype"]],
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[cfg["dtype"]], 4)}
-    else:
-        achieved = st["bytes"] / (st["ms"] * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    traffic = load_traffic(args.workload, dom)
-    roof["traffic"] = traffic
-    roof["kernel"] = dom
-    roof["launches"] = st["launches"]
-    roof["avg_launch_us"] = round(st["ms"] * 1e3 / st["launches"], 2)
-    conv = [v for k, v in stats.items() if k.startswith("conv_")]
-    conv_ms = sum(v["ms"] for v in conv)
-    conv_tf = sum(v["flops"] for v in conv) / (conv_ms * 1e-3) / 1e12 if conv_ms else 0.0
-    fuse = stats.get("fuse")
-    fusion_gbs = fuse["bytes"] / (fuse["ms"] * 1e-3) / 1e9 if fuse else None
-    kernel_ms = sum(v["ms"] for v in stats.values())
-    breakdown = sorted(((k, v) for k, v in stats.items()), key=lambda kv: -kv[1]["ms"])
-    for k, v in breakdown:
-        rate = (f"{v['flops'] / (v['ms'] * 1e-3) / 1e12:8.1f} TFLOP/s" if v["flops"] > 0 else "")
-        print(f"  {k:34s} {v['launches']:5d} launches {v['ms'] / nsteps:8.3f} ms/step "
-              f"{v['bytes'] / (v['ms'] * 1e-3) / 1e9:8.1f} GB/s {rate}", file=sys.stderr)
-
+    head = measure(args.workload, args.steps, args.warmup, args.timing_steps, args.cpu_seconds,
+                   with_cpu=not args.no_cpu_baseline, with_extras=True, args=args)
     out = {
         "metric": "examples/s summed over C clusters on 1 GPU; MFMA util %; fusion GB/s",
-        "value": round(value, 1),
+        "value": head.pop("value"),
         "unit": "examples/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(dt * 1e3 / args.steps, 4),
+        "ms_per_step": head.pop("ms_per_step"),
         "higher_is_better": True,
         "scaling": "strong",
         "vs_baseline": None,
-        "dtype": cfg["dtype"],
+        "dtype": head.pop("dtype"),
         "data": "synthetic",
-        "config": {"workload": args.workload, "description": DESCRIPTIONS[args.workload], "clients": cfg["K"],
-                   "clusters": C, "batch_per_cluster": B, "global_batch": C * B, "fusion_every": F,
-                   "rule": cfg["rule"], "parallelism": "C replicas batched in every kernel, 1 GPU"},
-        "mfma_util_pct": round(100.0 * conv_tf / PEAK_TFLOPS[cfg["dtype"]], 2),
-        "conv_tflops": round(conv_tf, 2),
-        "fusion_gbs": None if fusion_gbs is None else round(fusion_gbs, 1),
-        "kernel_ms_per_step": round(kernel_ms / nsteps, 4),
-        "roofline": roof,
+        "config": head.pop("config"),
     }
-    if not args.no_schedule_control:
-        out["schedule_control"] = schedule_control(cfg, ctx, args.warmup + args.steps + args.timing_steps,
-                                                   args.control_steps)
-        print(f"bench: schedule control {out['schedule_control']}", file=sys.stderr, flush=True)
-    if not args.no_hbm_probes:
-        out["hbm"] = hbm_probes(cfg, max(F, 1), ctx.cluster_sizes())
-        if fusion_gbs is not None:
-            out["hbm"]["fusion_in_step"] = {"gbs": round(fusion_gbs, 1), "frac": round(fusion_gbs / PEAK_HBM_GBS, 4)}
-        print(f"bench: hbm {out['hbm']}", file=sys.stderr, flush=True)
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, assignment, args.cpu_seconds)
+    out.update(head)
+    if not args.no_sub_results:
+        out["sub_results"] = {}
+        for name in SUB_RESULTS:
+            if name == args.workload:
+                continue
+            r = measure(name, args.steps, args.warmup, args.timing_steps, args.cpu_seconds / 2,
+                        with_cpu=not args.no_cpu_baseline, args=args)
+            out["sub_results"][name] = r
     print(json.dumps(out), flush=True)
 
 

@@ -1,18 +1,29 @@
 """Summaries of rocprofv3 output for the kernels of this library.
 
+Every figure lands in profiles/profile.json, per workload and kernel label,
+with the hash of each kernel source file at the time it was taken (bench.py
+reports a figure only while the kernel's source still has that hash), and in
+a Markdown summary per workload and kind:
+
   python -m paper_2609_29395_amd.profile_summary copy [--mib N] [--reps R]
       Run a plain device copy of a known size (the calibration kernel for the
       FETCH_SIZE / WRITE_SIZE counters).
-  python -m paper_2609_29395_amd.profile_summary stats TRACE_DIR OUT.md CMD...
-      Write a Markdown summary of `rocprofv3 --kernel-trace --stats` CSV output.
-  python -m paper_2609_29395_amd.profile_summary traffic FETCH_DIR WRITE_DIR COPY_FETCH_DIR COPY_WRITE_DIR WORKLOAD OUT.json
+  python -m paper_2609_29395_amd.profile_summary stats TRACE_DIR WORKLOAD OUT.md CMD...
+      `rocprofv3 --kernel-trace --stats` CSV output: calls, total and average
+      duration per kernel.
+  python -m paper_2609_29395_amd.profile_summary mfma PMC_DIR WORKLOAD OUT.md CMD...
+      `rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16
+      SQ_INSTS_VALU_MFMA_MOPS_F32 GRBM_GUI_ACTIVE` CSV output: MFMA busy
+      fraction (busy cycles over GUI-active cycles times the 1024 SIMDs) and
+      MFMA FLOPs counted per launch (512 per MOPS count).
+  python -m paper_2609_29395_amd.profile_summary traffic FETCH_DIR WRITE_DIR COPY_FETCH_DIR COPY_WRITE_DIR WORKLOAD OUT.md
+      Two counter runs of the workload (FETCH_SIZE, then WRITE_SIZE) combined
+      into HBM bytes per launch for every kernel, each counter scaled by what
+      it reads for the copy of known size (runs COPY_FETCH_DIR, COPY_WRITE_DIR).
   python -m paper_2609_29395_amd.profile_summary layers TRACE_DIR OUT.md CMD...
       Per-dispatch table of one step from `rocprofv3 --kernel-trace` CSV output.
   python -m paper_2609_29395_amd.profile_summary gemm-ref OUT.md
       hipBLASLt bf16 GEMMs of the convolution shapes, for comparison.
-      Combine two counter runs of the workload (FETCH_SIZE, then WRITE_SIZE)
-      into HBM bytes per launch for every kernel, each counter scaled by what
-      it reads for the copy of known size (runs COPY_FETCH_DIR, COPY_WRITE_DIR).
 """
 from __future__ import annotations
 
@@ -27,6 +38,8 @@ import sys
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 COPY_MIB = 256
+PROFILE_JSON = os.path.join(ROOT, "profiles", "profile.json")
+SIMDS = 256 * 4  # MI355X: 256 compute units of 4 SIMDs
 
 
 def kernel_label(name: str) -> str:
@@ -124,7 +137,35 @@ def _one(pattern):
     return files[0]
 
 
-def stats(trace_dir, out_md, cmd):
+def _update_profile(workload, kind, entries):
+    """Merge {label: {field: value}} of one kind (trace, mfma, traffic) into
+    profiles/profile.json, with the current source hash of each label's file."""
+    rec = {}
+    if os.path.exists(PROFILE_JSON):
+        with open(PROFILE_JSON) as fh:
+            rec = json.load(fh)
+    w = rec.setdefault(workload, {})
+    for lab, fields in entries.items():
+        e = w.setdefault(lab, {})
+        e[kind] = dict(fields, source_hash=file_hash(kernel_source(lab)))
+    with open(PROFILE_JSON, "w") as fh:
+        json.dump(rec, fh, indent=1, sort_keys=True)
+
+
+def profile_entry(workload, label, kind):
+    """One kind of profile figures for a kernel, or None when absent or taken
+    on a source file that has changed since."""
+    if not os.path.exists(PROFILE_JSON):
+        return None
+    with open(PROFILE_JSON) as fh:
+        rec = json.load(fh)
+    e = rec.get(workload, {}).get(label, {}).get(kind)
+    if e is None or e.get("source_hash") != file_hash(kernel_source(label)):
+        return None
+    return e
+
+
+def stats(trace_dir, workload, out_md, cmd):
     rows = list(csv.DictReader(open(_one(os.path.join(trace_dir, "**", "*kernel_stats.csv")))))
     total = sum(float(r["TotalDurationNs"]) for r in rows)
     # instantiations that share a label (e.g. the head conv that also writes
@@ -134,7 +175,7 @@ def stats(trace_dir, out_md, cmd):
         v = by[kernel_label(r["Name"])]
         v[0] += int(r["Calls"])
         v[1] += float(r["TotalDurationNs"])
-    lines = [f"# Kernel time summary", "", f"Command: `{' '.join(cmd)}`", "",
+    lines = [f"# Kernel time summary, {workload}", "", f"Command: `{' '.join(cmd)}`", "",
              "| kernel (label) | calls | total ms | avg us | % |", "|---|---|---|---|---|"]
     for lab, (calls, tot) in sorted(by.items(), key=lambda kv: -kv[1][1]):
         lines.append(f"| {lab} | {calls} | {tot / 1e6:.3f} | {tot / calls / 1e3:.2f} | {100 * tot / total:.2f} |")
@@ -142,6 +183,53 @@ def stats(trace_dir, out_md, cmd):
     with open(out_md, "w") as fh:
         fh.write("\n".join(lines))
     print("\n".join(lines))
+    _update_profile(workload, "trace", {lab: {"calls": c, "avg_us": t / c / 1e3} for lab, (c, t) in by.items()
+                                        if not lab.startswith(("elementwise", "vectorized", "__amd"))})
+
+
+def mfma(pmc_dir, workload, out_md, cmd):
+    """MFMA busy fraction and counted MFMA FLOPs per launch, per kernel label."""
+    rows = list(csv.DictReader(open(_one(os.path.join(pmc_dir, "**", "*counter_collection.csv")))))
+    disp = collections.defaultdict(dict)  # dispatch id -> {counter: value, name, ns}
+    for r in rows:
+        d = disp[r["Dispatch_Id"]]
+        d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        d["name"] = r["Kernel_Name"]
+        d["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    by = collections.defaultdict(list)
+    for d in disp.values():
+        lab = kernel_label(d["name"])
+        if not lab.startswith(("elementwise", "vectorized", "__amd")):
+            by[lab].append(d)
+
+    def gui_per_xcd(d):
+        g = d.get("GRBM_GUI_ACTIVE", 0.0)
+        return g / 8.0 if d["ns"] > 0 and g > 3.0 * d["ns"] else g  # the CSV sums the 8 XCDs
+
+    out = {}
+    lines = [f"# MFMA counters per launch, {workload}", "", f"Command: `{' '.join(cmd)}`", "",
+             "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x 1024 SIMDs), with GRBM_GUI_ACTIVE per "
+             "XCD (the CSV value over 8 when it sums the 8 XCDs, i.e. when it exceeds the launch's duration "
+             "times 3 GHz); counted FLOPs = 512 x SQ_INSTS_VALU_MFMA_MOPS_{BF16,F32}; GUI-active MHz = "
+             "GRBM_GUI_ACTIVE per XCD over the launch's duration.", "",
+             "| kernel (label) | launches | MFMA busy % | counted MFMA GFLOP/launch | GUI-active MHz |",
+             "|---|---|---|---|---|"]
+    for lab, ds in by.items():
+        busy = sum(d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) for d in ds)
+        gui = sum(gui_per_xcd(d) for d in ds)
+        flops = 512.0 * sum(d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) + d.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0.0)
+                            for d in ds) / len(ds)
+        ns = sum(d["ns"] for d in ds)
+        out[lab] = {"launches": len(ds), "mfma_busy_pct": 100.0 * busy / (gui * SIMDS) if gui > 0 else 0.0,
+                    "counted_flops_per_launch": flops, "gui_mhz": 1e3 * gui / ns if ns > 0 else 0.0}
+    for lab, v in sorted(out.items(), key=lambda kv: -kv[1]["counted_flops_per_launch"]):
+        lines.append(f"| {lab} | {v['launches']} | {v['mfma_busy_pct']:.1f} | "
+                     f"{v['counted_flops_per_launch'] / 1e9:.2f} | {v['gui_mhz']:.0f} |")
+    lines.append("")
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
+    _update_profile(workload, "mfma", out)
 
 
 def _counter_per_dispatch(d, counter):
@@ -153,7 +241,7 @@ def _counter_per_dispatch(d, counter):
     return per
 
 
-def traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload, out_json):
+def traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload, out_md):
     fetch = _counter_per_dispatch(fetch_dir, "FETCH_SIZE")
     write = _counter_per_dispatch(write_dir, "WRITE_SIZE")
     expect_kib = COPY_MIB * 1024.0
@@ -162,27 +250,25 @@ def traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload, out_
     cw = samples(_counter_per_dispatch(copy_write_dir, "WRITE_SIZE"))
     f_fac = (sum(cf) / len(cf)) / expect_kib if cf else 1.0
     w_fac = (sum(cw) / len(cw)) / expect_kib if cw else 1.0
-    out = {"source_hashes": source_hashes(), "copy_mib": COPY_MIB, "fetch_factor": f_fac,
-           "write_factor": w_fac, "kernels": {}}
     # per label: the launches of every instantiation with that label
     fl, wl = collections.defaultdict(list), collections.defaultdict(list)
     for k, v in fetch.items():
         fl[kernel_label(k)] += v
     for k, v in write.items():
         wl[kernel_label(k)] += v
+    out = {}
     for k in set(fl) | set(wl):
+        if k.startswith(("elementwise", "vectorized", "__amd")):
+            continue
         fv, wv = fl.get(k, []), wl.get(k, [])
         fk = sum(fv) / len(fv) if fv else 0.0
         wk = sum(wv) / len(wv) if wv else 0.0
-        out["kernels"][f"{workload}:{k}"] = {
-            "launches": max(len(fv), len(wv)), "fetch_kib": fk, "write_kib": wk,
-            "bytes_per_launch": 1024.0 * (fk / f_fac + wk / w_fac)}
-    with open(out_json, "w") as fh:
-        json.dump(out, fh, indent=1, sort_keys=True)
-    md = os.path.join(os.path.dirname(out_json), f"{workload}_traffic.md")
+        out[k] = {"launches": max(len(fv), len(wv)), "fetch_kib": fk, "write_kib": wk,
+                  "fetch_factor": f_fac, "write_factor": w_fac,
+                  "bytes_per_launch": 1024.0 * (fk / f_fac + wk / w_fac)}
     lines = [f"# HBM traffic per launch, {workload}", "",
-             "Commands (R = repository root; B = `python $R/bench.py --steps 5 --warmup 2 --timing-steps 2 "
-             "--no-cpu-baseline --no-schedule-control --no-hbm-probes`):", "",
+             "Commands (R = repository root; B = the bench.py command of the kernel-trace summary of this "
+             "workload):", "",
              "* `rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/pfetch -o run -- $B`",
              "* `rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/pwrite -o run -- $B`",
              "* `rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/cfetch -o run -- python "
@@ -190,20 +276,21 @@ def traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload, out_
              "* `rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/cwrite -o run -- python "
              "$R/paper_2609_29395_amd/profile_summary.py copy`",
              f"* `python -m paper_2609_29395_amd.profile_summary traffic gpurun_out/pfetch gpurun_out/pwrite "
-             f"gpurun_out/cfetch gpurun_out/cwrite {workload} {out_json}`", "",
+             f"gpurun_out/cfetch gpurun_out/cwrite {workload} {os.path.relpath(out_md, ROOT)}`", "",
              f"Calibration: a {COPY_MIB} MiB device copy reads FETCH_SIZE = {f_fac:.4f} x and WRITE_SIZE = "
              f"{w_fac:.4f} x its size; counters are divided by these factors.",
-             "Kernel source hashes when taken: per kernel source file in `traffic.json` (`source_hashes`); "
-             "bench.py reports traffic = null for a kernel whose source file changed since.", "",
+             "The figures also sit in `profile.json` with the hash of each kernel's source file when taken; "
+             "bench.py reports traffic = null for a kernel whose source changed since.", "",
              "| kernel | launches | FETCH KiB/launch | WRITE KiB/launch | HBM MB/launch (calibrated) |",
              "|---|---|---|---|---|"]
-    for k, v in sorted(out["kernels"].items(), key=lambda kv: -kv[1]["bytes_per_launch"]):
-        lines.append(f"| {k.split(':', 1)[1]} | {v['launches']} | {v['fetch_kib']:.0f} | {v['write_kib']:.0f} | "
+    for k, v in sorted(out.items(), key=lambda kv: -kv[1]["bytes_per_launch"]):
+        lines.append(f"| {k} | {v['launches']} | {v['fetch_kib']:.0f} | {v['write_kib']:.0f} | "
                      f"{v['bytes_per_launch'] / 1e6:.1f} |")
     lines.append("")
-    with open(md, "w") as fh:
+    with open(out_md, "w") as fh:
         fh.write("\n".join(lines))
     print("\n".join(lines))
+    _update_profile(workload, "traffic", out)
 
 
 def gemm_reference(out_md):
@@ -268,7 +355,9 @@ if __name__ == "__main__":
     elif what == "layers":
         layer_table(sys.argv[2], sys.argv[3], sys.argv[4:])
     elif what == "stats":
-        stats(sys.argv[2], sys.argv[3], sys.argv[4:])
+        stats(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5:])
+    elif what == "mfma":
+        mfma(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5:])
     elif what == "traffic":
         traffic(*sys.argv[2:8])
     else:

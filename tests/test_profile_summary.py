@@ -42,12 +42,46 @@ def test_stats_merges_rows_with_one_label(tmp_path):
            [[HALO.format(""), 3, 3000.0, 1000.0], [HALO.format(", true"), 1, 2000.0, 2000.0],
             ["sgd_kernel<4>", 2, 1000.0, 500.0]])
     out = tmp_path / "stats.md"
-    ps.stats(str(d), str(out), ["cmd"])
+    ps.stats(str(d), "wl", str(out), ["cmd"])
     rows = [l for l in out.read_text().splitlines() if l.startswith("| conv_fwd")]
     assert len(rows) == 1
     cells = [c.strip() for c in rows[0].strip("|").split("|")]
     # 4 calls, 5000 ns in all, 1250 ns = 1.25 us each, 5000 / 6000 of the time
     assert cells[1:] == ["4", "0.005", "1.25", "83.33"]
+    e = ps.profile_entry("wl", "conv_fwd<bf16,256x256x64,w16,halo>", "trace")
+    assert e["calls"] == 4 and e["avg_us"] == pytest.approx(1.25)
+
+
+@pytest.fixture(autouse=True)
+def _private_profile(tmp_path, monkeypatch):
+    # every summary writes profile.json: keep the committed one untouched
+    monkeypatch.setattr(ps, "PROFILE_JSON", str(tmp_path / "profile.json"))
+
+
+def test_profile_entry_goes_stale_with_its_source(tmp_path, monkeypatch):
+    ps._update_profile("wl", "trace", {"sgd": {"calls": 1, "avg_us": 2.0}})
+    assert ps.profile_entry("wl", "sgd", "trace")["avg_us"] == 2.0
+    monkeypatch.setattr(ps, "file_hash", lambda name: "changed")
+    assert ps.profile_entry("wl", "sgd", "trace") is None
+
+
+def test_mfma_busy_and_counted_flops(tmp_path):
+    # two launches of one kernel: 800 ns each at 2.0 GHz per XCD (the CSV sums
+    # the 8 XCDs: 8 x 1600 cycles), MFMA busy 512 x 1600 of 1024 x 1600
+    # SIMD-cycles = 50 %, 1000 MOPS = 512,000 FLOPs each
+    hdr = ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp", "End_Timestamp"]
+    rows = []
+    for disp in (1, 2):
+        for c, v in (("SQ_VALU_MFMA_BUSY_CYCLES", 512 * 1600.0), ("GRBM_GUI_ACTIVE", 8 * 1600.0),
+                     ("SQ_INSTS_VALU_MFMA_MOPS_BF16", 1000.0), ("SQ_INSTS_VALU_MFMA_MOPS_F32", 0.0)):
+            rows.append([disp, HALO.format(""), c, v, 1000, 1800])
+    _write(str(tmp_path / "m" / "a" / "run_counter_collection.csv"), hdr, rows)
+    ps.mfma(str(tmp_path / "m"), "wl", str(tmp_path / "m.md"), ["cmd"])
+    e = ps.profile_entry("wl", "conv_fwd<bf16,256x256x64,w16,halo>", "mfma")
+    assert e["launches"] == 2
+    assert e["mfma_busy_pct"] == pytest.approx(50.0)
+    assert e["counted_flops_per_launch"] == pytest.approx(512000.0)
+    assert e["gui_mhz"] == pytest.approx(2000.0)
 
 
 def _counters(path, counter, per_kernel):
@@ -66,12 +100,11 @@ def test_traffic_calibration_and_merge(tmp_path):
               {HALO.format(""): [100.0, 100.0, 100.0], HALO.format(", true"): [140.0]})
     _counters(str(tmp_path / "w" / "a" / "run_counter_collection.csv"), "WRITE_SIZE",
               {HALO.format(""): [256.0, 256.0, 256.0], HALO.format(", true"): [260.0]})
-    out = tmp_path / "traffic.json"
+    out = tmp_path / "traffic.md"
     ps.traffic(str(tmp_path / "f"), str(tmp_path / "w"), str(tmp_path / "cf"), str(tmp_path / "cw"), "wl", str(out))
-    t = json.loads(out.read_text())
-    assert t["fetch_factor"] == pytest.approx(0.5) and t["write_factor"] == pytest.approx(1.0)
-    k = t["kernels"]["wl:conv_fwd<bf16,256x256x64,w16,halo>"]
+    k = ps.profile_entry("wl", "conv_fwd<bf16,256x256x64,w16,halo>", "traffic")
+    assert k["fetch_factor"] == pytest.approx(0.5) and k["write_factor"] == pytest.approx(1.0)
     assert k["launches"] == 4
     assert k["fetch_kib"] == pytest.approx(110.0) and k["write_kib"] == pytest.approx(257.0)
     assert k["bytes_per_launch"] == pytest.approx(1024.0 * (110.0 / 0.5 + 257.0))
-    assert set(t["source_hashes"]) == {f for f in os.listdir(ps.CSRC) if f.endswith(".hip")}
+    assert "conv_fwd<bf16,256x256x64,w16,halo>" in out.read_text()
