@@ -141,6 +141,17 @@ CONFIGS = {
                 ("conv", 64, 256, False), ("conv", 256, 136, False), ("maxpool",),
                 ("avgpool",), ("linear", 136, 7)],
         cut=2, dtype="bf16", lr=0.05, momentum=0.9, F=2, T=3, seed=0),
+    # 16 x 16 images into 128-channel server layers (the 8-cluster server's
+    # shape): the 128-wide one-buffer halo tile in the forward (one and two
+    # 64-channel blocks, a residual layer) and input gradient, and the head's
+    # max pool and mean in its epilogue.
+    "halo128_bf16": dict(
+        K=24, C=2, B=5, L=7, N_ex=1400, H=16, W=16, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="label_l1",
+        layers=[("conv", 3, 16, False), ("conv", 16, 64, False),
+                ("conv", 64, 128, False), ("conv", 128, 128, True), ("conv", 128, 128, False), ("maxpool",),
+                ("avgpool",), ("linear", 128, 7)],
+        cut=2, dtype="bf16", lr=0.05, momentum=0.9, F=2, T=3, seed=0),
     # 32 x 32 images with the workloads' client layers (3 -> 32 -> 64, max
     # pool), so the image-layer convolution kernels run at small size.
     "img32_bf16": dict(

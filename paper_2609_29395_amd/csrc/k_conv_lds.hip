@@ -50,7 +50,7 @@ constexpr int ROW = BK * 2;  // bytes per LDS row
 constexpr uint32_t kOob = 0x80000000u;
 constexpr int kBufferFlags = 0x00020000;
 
-template <int BM_, int BN, int WM, int WN> struct Cfg {
+template <int BM_, int BN, int WM, int WN, int PFO = 0> struct Cfg {
   static constexpr int BM = BM_, BN_ = BN;
   static constexpr int NW = WM * WN, NTHR = 64 * NW;  // waves, threads
   static constexpr int A_BYTES = BM * ROW, B_BYTES = BN * ROW;
@@ -61,7 +61,7 @@ template <int BM_, int BN, int WM, int WN> struct Cfg {
   static constexpr int TM = BM / WM / 16, TN = BN / WN / 16;  // fragments per wave
   static constexpr int WNW = BN / WN;                          // wave tile width
   // epilogue: PF pixel fragments (16 * PF rows) per pass through LDS
-  static constexpr int PF = NW > 8 ? 2 : 4;
+  static constexpr int PF = PFO ? PFO : (NW > 8 ? 2 : 4);
   // floats per staged epilogue row: 64-wide wave tiles use unpadded rows
   // whose 16-byte chunks are XOR-ed with the row's low 3 bits (measured free
   // of LDS bank conflicts for both the fragment writes and the 8-channel
@@ -88,6 +88,12 @@ template <int BM_, int BN, int WM, int WN> struct Cfg {
 // fragments of successive image rows sit a constant 18 rows (2304 bytes)
 // apart.  Two halo buffers (by channel block)
 // and two weight stages (by k tile).
+//
+// A 128-wide weight tile (8 waves) keeps one halo buffer: its k loop, two
+// weight stages and two-pass epilogue fit in 73 KB, so two workgroups share
+// a CU and one's prologue, epilogue and barrier waits overlap the other's
+// MFMAs.  With one buffer the next channel block's halo is loaded when the
+// last tap of the current block is done (one wait per channel block).
 namespace halo {
 constexpr int IMG = 16, HP = IMG + 2, ROWS = HP * HP;    // 18 x 18 rows
 constexpr int BYTES = ((ROWS * 128 + 1023) / 1024) * 1024;  // padded to whole 1 KB wave copies
@@ -95,9 +101,10 @@ constexpr int FSTRIDE = HP * 128;                         // bytes between image
 // 16-byte copies per thread for a workgroup of NTHR threads
 template <int NTHR> constexpr int pieces() { return (ROWS * 128 + NTHR * 16 - 1) / (NTHR * 16); }
 // k tiles: TPK kernel taps of one 64-channel block (TPK = 1, or 3 for a whole
-// tap row); two halo buffers and two weight stages of TPK x BN rows
-template <int BN, int TPK> constexpr int lds_bytes() { return 2 * BYTES + 2 * TPK * BN * 128; }
-static_assert(pieces<1024>() == 3 && pieces<512>() == 6 && lds_bytes<256, 1>() <= 160 * 1024, "halo layout");
+// tap row); HB halo buffers and two weight stages of TPK x BN rows
+template <int BN, int TPK, int HB = 2> constexpr int lds_bytes() { return HB * BYTES + 2 * TPK * BN * 128; }
+static_assert(pieces<1024>() == 3 && pieces<512>() == 6 && lds_bytes<256, 1>() <= 160 * 1024 &&
+              lds_bytes<128, 1, 1>() <= 80 * 1024, "halo layout");
 }  // namespace halo
 __device__ __forceinline__ int hswz(int wp) { return wp & 7; }
 
@@ -207,16 +214,17 @@ __device__ __forceinline__ void issue_tile(int kt, char *stage0, int wave, const
                                                boff[q] == kOob ? kOob : boff[q] + kb, 0, 0, 0);
 }
 
-// Halo mode: piece q of channel block cb's halo image into buffer cb % 2
+// Halo mode: piece q of channel block cb's halo image into buffer cb % HB
 // (hoff: this thread's source offset within the image, -1 for the zero
 // border); the last piece covers only the first waves.
-template <int NTHR>
+template <int NTHR, int HB>
 __device__ __forceinline__ void issue_halo_piece(int q, int cb, char *smem, int wave, const ConvArgs &a,
                                                  const void *src, int img_off, int hoff) {
   const __amdgpu_buffer_rsrc_t rsa = rsrc(src, (uint32_t)(a.src_rs * 2));
   if (q * NTHR * 16 + wave * 1024 < halo::BYTES) {
     const uint32_t off = hoff >= 0 ? (uint32_t)(img_off + hoff + cb * BK) * 2u : kOob;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(smem + (cb & 1) * halo::BYTES + q * NTHR * 16 + wave * 1024),
+    const int buf = HB == 2 ? (cb & 1) : 0;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, LDS_PTR(smem + buf * halo::BYTES + q * NTHR * 16 + wave * 1024),
                                              16, off, 0, 0, 0);
   }
 }
@@ -224,13 +232,13 @@ __device__ __forceinline__ void issue_halo_piece(int q, int cb, char *smem, int 
 // Halo mode: the weight rows of k tile kt into weight stage kt % 2: TPK
 // taps of channel block kt / (9 / TPK) (one tap kt % 9, or the taps of tap
 // row kt % 3), one BN-row sub-stage per tap.
-template <typename CF, int TPK>
+template <typename CF, int TPK, int HB>
 __device__ __forceinline__ void issue_weights(int kt, char *smem, int wave, const ConvArgs &a, const void *wt,
                                               const uint32_t *boff) {
   const __amdgpu_buffer_rsrc_t rsb = rsrc(wt, (uint32_t)((int64_t)a.N * a.Kp * 2));
   constexpr int KPB = 9 / TPK;  // k tiles per channel block
   const int cb = kt / KPB, kr = kt - KPB * cb;
-  char *sb = smem + 2 * halo::BYTES + (kt & 1) * TPK * CF::B_BYTES + wave * 1024;
+  char *sb = smem + HB * halo::BYTES + (kt & 1) * TPK * CF::B_BYTES + wave * 1024;
 #pragma unroll
   for (int t = 0; t < TPK; ++t) {
     const int rs = TPK == 1 ? kr : 3 * kr + t;  // kernel tap
@@ -244,16 +252,22 @@ __device__ __forceinline__ void issue_weights(int kt, char *smem, int wave, cons
   }
 }
 
-template <int BM, int BN, int WM, int WN, int EPI, bool TAPS1, bool HALO = false, bool AVG = false>
-__global__ void __launch_bounds__(64 * WM * WN)
+// (one halo buffer: at most 128 registers, so that two 8-wave workgroups
+// share a CU)
+template <int BM, int BN, int WM, int WN, int EPI, bool TAPS1, bool HALO = false, bool AVG = false, int HB = 2>
+__global__ void __launch_bounds__(64 * WM * WN, (HALO && HB == 1) ? 4 : 1)
 conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, int NT) {
-  using CF = Cfg<BM, BN, WM, WN>;
+  // one halo buffer: the two-pass epilogue keeps the staging within the
+  // k loop's 73 KB
+  using CF = Cfg<BM, BN, WM, WN, (HALO && HB == 1) ? 2 : 0>;
   static_assert(!HALO || (BM == 256 && !TAPS1 &&
-                          ((BN == 256 && (WM == 4 || WM == 2) && WN == 4) || (BN == 64 && WM == 8 && WN == 2))),
+                          ((BN == 256 && (WM == 4 || WM == 2) && WN == 4 && HB == 2) ||
+                           (BN == 64 && WM == 8 && WN == 2 && HB == 2) || (BN == 128 && WM == 4 && WN == 2 && HB == 1))),
                 "halo mode tile");
-  // AVG: the tile is one whole image and every output channel (halo mode,
-  // 256-wide weight tile, forward)
-  static_assert(!AVG || (HALO && BN == 256 && EPI == EPI_FWD), "image mean in the epilogue");
+  static_assert(HB == 2 || (HALO && HB == 1), "halo buffers");
+  // AVG: the tile is one whole image (halo mode, forward) and writes the
+  // means of its BN channels
+  static_assert(!AVG || (HALO && (BN == 256 || BN == 128) && EPI == EPI_FWD), "image mean in the epilogue");
   // halo mode, 64-wide weight tiles: a k tile is a whole tap row (three taps)
   // so that each barrier covers three times the MFMAs of a one-tap tile
   constexpr int TPK = (HALO && BN == 64) ? 3 : 1;
@@ -360,8 +374,8 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
 
   if constexpr (HALO) {
 #pragma unroll
-    for (int q = 0; q < PIECES; ++q) issue_halo_piece<NTHR>(q, 0, smem, wave, a, src, img_off, hoff[q]);
-    issue_weights<CF, TPK>(0, smem, wave, a, wt, boff);
+    for (int q = 0; q < PIECES; ++q) issue_halo_piece<NTHR, HB>(q, 0, smem, wave, a, src, img_off, hoff[q]);
+    issue_weights<CF, TPK, HB>(0, smem, wave, a, wt, boff);
   } else {
     issue(0);
   }
@@ -377,16 +391,28 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
       constexpr int KPB = 9 / TPK;
       const int cb = kt / KPB;
       kr = kt - KPB * cb;
-      if (kt + 1 < nk) issue_weights<CF, TPK>(kt + 1, smem, wave, a, wt, boff);
-      // the next channel block's halo in pieces over the first k tiles (the
-      // buffer was last read by channel block cb - 1)
-      if (kr < PIECES && cb + 1 < ncb) {
+      if constexpr (HB == 1) {
+        if (kr == 0 && cb > 0) {
+          // every wave is done with channel block cb - 1 (the barrier
+          // above): its buffer takes block cb, waited for here
 #pragma unroll
-        for (int q = 0; q < PIECES; ++q)
-          if (q == kr) issue_halo_piece<NTHR>(q, cb + 1, smem, wave, a, src, img_off, hoff[q]);
+          for (int q = 0; q < PIECES; ++q) issue_halo_piece<NTHR, HB>(q, cb, smem, wave, a, src, img_off, hoff[q]);
+          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+          asm volatile("s_barrier" ::: "memory");
+        }
       }
-      xst = lds0 + (uint32_t)((cb & 1) * halo::BYTES);
-      wb = lds0 + (uint32_t)(2 * halo::BYTES + (kt & 1) * TPK * CF::B_BYTES);
+      if (kt + 1 < nk) issue_weights<CF, TPK, HB>(kt + 1, smem, wave, a, wt, boff);
+      if constexpr (HB == 2) {
+        // the next channel block's halo in pieces over the first k tiles (the
+        // buffer was last read by channel block cb - 1)
+        if (kr < PIECES && cb + 1 < ncb) {
+#pragma unroll
+          for (int q = 0; q < PIECES; ++q)
+            if (q == kr) issue_halo_piece<NTHR, HB>(q, cb + 1, smem, wave, a, src, img_off, hoff[q]);
+        }
+      }
+      xst = lds0 + (uint32_t)((HB == 2 ? (cb & 1) : 0) * halo::BYTES);
+      wb = lds0 + (uint32_t)(HB * halo::BYTES + (kt & 1) * TPK * CF::B_BYTES);
       if constexpr (TPK == 1) {
         const int r = (kr * 11) >> 5, sc = kr - 3 * r;  // tap (r, sc)
 #pragma unroll
@@ -641,19 +667,33 @@ constexpr int kHaloWM = 4;
 using HaloCfg = Cfg<256, 256, kHaloWM, 4>;
 // 64-wide weight tiles: 16 waves of 32 pixels x 32 channels, tap-row k tiles
 using Halo64Cfg = Cfg<256, 64, 8, 2>;
+// 128-wide weight tiles: 8 waves of 64 x 64, one halo buffer, two-pass
+// epilogue; two workgroups per CU
+using Halo128Cfg = Cfg<256, 128, 4, 2, 2>;
 // dynamic LDS of a halo-mode launch: the k loop's buffers or the epilogue's
 // staging, whichever is larger
-template <typename CF, int TPK> constexpr int halo_lds_of() {
-  return halo::lds_bytes<CF::BN_, TPK>() > CF::EP_BYTES ? halo::lds_bytes<CF::BN_, TPK>() : CF::EP_BYTES;
+template <typename CF, int TPK, int HB = 2> constexpr int halo_lds_of() {
+  return halo::lds_bytes<CF::BN_, TPK, HB>() > CF::EP_BYTES ? halo::lds_bytes<CF::BN_, TPK, HB>() : CF::EP_BYTES;
 }
-static_assert(halo_lds_of<HaloCfg, 1>() <= 160 * 1024 && halo_lds_of<Halo64Cfg, 3>() <= 160 * 1024, "halo LDS");
+static_assert(halo_lds_of<HaloCfg, 1>() <= 160 * 1024 && halo_lds_of<Halo64Cfg, 3>() <= 160 * 1024 &&
+              2 * halo_lds_of<Halo128Cfg, 1, 1>() <= 160 * 1024, "halo LDS");
+
+// 16 x 16 images in 64-channel blocks: the halo layouts apply
+bool halo_img16(const ConvArgs &a) {
+  return a.taps == 9 && a.Csrc % BK == 0 && a.H == halo::IMG && a.W == halo::IMG;
+}
+// the 128-wide, one-buffer halo tile for N = 128 or 256 (on the 256-channel
+// layers of the 16-cluster step: forward 1.38 -> 0.95 + 0.46 ms, input
+// gradient 1.40 -> 1.25 ms per step against the 256-wide tile, whose
+// workgroup fills a CU)
+bool use_halo128(const ConvArgs &a) { return halo_img16(a) && (a.N == 128 || a.N == 256); }
 
 // The halo forward on a 256-wide weight tile writes the per-image channel
 // means to pool_out as well when that is set (launch_conv reaches
 // launch_conv_lds for these arguments: not an image-side or im2col layer).
 bool conv_fuses_avg(int dtype, const ConvArgs &a) {
-  return a.epi == EPI_FWD && !conv_img_ok(dtype, a) && conv_lds_ok(dtype, a) && a.taps == 9 && a.Csrc % BK == 0 &&
-         a.H == halo::IMG && a.W == halo::IMG && a.N > 128 && a.N <= 256;
+  return a.epi == EPI_FWD && !conv_img_ok(dtype, a) && conv_lds_ok(dtype, a) && halo_img16(a) && a.N >= 128 &&
+         a.N <= 256;
 }
 
 // Every instantiation is named in this (non-template) function, which is
@@ -683,6 +723,14 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
           hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, halo_lds_of<Halo64Cfg, 3>());
       if (e != hipSuccess) return e;
     }
+    for (const void *f :
+         {reinterpret_cast<const void *>(&conv_lds_kernel<256, 128, 4, 2, EPI_FWD, false, true, false, 1>),
+          reinterpret_cast<const void *>(&conv_lds_kernel<256, 128, 4, 2, EPI_FWD, false, true, true, 1>),
+          reinterpret_cast<const void *>(&conv_lds_kernel<256, 128, 4, 2, EPI_DGRAD, false, true, false, 1>)}) {
+      const hipError_t e =
+          hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, halo_lds_of<Halo128Cfg, 1, 1>());
+      if (e != hipSuccess) return e;
+    }
     CONV_LDS_ATTR(256, 256, 4, 4)
     CONV_LDS_ATTR(256, 128, 4, 2)
     CONV_LDS_ATTR(128, 64, 2, 4)
@@ -698,12 +746,14 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   // halo mode: one 16 x 16 image per 256-pixel tile, 64-channel blocks, with
   // 256-wide weight tiles or (input channels a multiple of 64, no residual)
   // 64-wide ones
-  const bool img16 = a.taps == 9 && a.Csrc % BK == 0 && a.H == halo::IMG && a.W == halo::IMG;
-  const bool use_halo = img16 && bn == 256;
+  const bool img16 = halo_img16(a);
+  const bool use_h128 = use_halo128(a);
+  const bool use_halo = img16 && bn == 256 && !use_h128;
   const bool use_halo64 = img16 && bn == 64 && a.res == nullptr;
   const int bm = (bn == 64 && a.Kp >= 16 * BK && !use_halo64) ? 128 : 256;
   int MT, NT;
-  if (bn == 256) grid<256, 256>(a, &MT, &NT);
+  if (use_h128) grid<256, 128>(a, &MT, &NT);
+  else if (bn == 256) grid<256, 256>(a, &MT, &NT);
   else if (bn == 128) grid<256, 128>(a, &MT, &NT);
   else if (bn == 64 && bm == 128) grid<128, 64>(a, &MT, &NT);
   else if (bn == 64) grid<256, 64>(a, &MT, &NT);
@@ -715,11 +765,29 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   ConvArgs b = a;
   b.res_lds = (a.res != nullptr && a.res == a.src && a.taps == 9 && a.Csrc % BK == 0 && a.Csrc == a.N &&
                (bn == 256 || bn == 128)) ? 1 : 0;
-  if (label)
-    *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16," + std::to_string(bm) + "x" +
-             std::to_string(bn) + (use_halo64 ? "x192,w16" : "x64,w") +
-             (use_halo ? std::to_string(HaloCfg::NW) : use_halo64 ? "" : bn == 256 ? "16" : "8") +
-             ((use_halo || use_halo64) ? ",halo>" : ",lds>");
+  if (label) {
+    if (use_h128)
+      *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16,256x128x64,w8,halo1>";
+    else
+      *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16," + std::to_string(bm) + "x" +
+               std::to_string(bn) + (use_halo64 ? "x192,w16" : "x64,w") +
+               (use_halo ? std::to_string(HaloCfg::NW) : use_halo64 ? "" : bn == 256 ? "16" : "8") +
+               ((use_halo || use_halo64) ? ",halo>" : ",lds>");
+  }
+  if (use_h128) {
+    // (with the image means: each 128-channel tile writes its own channels')
+    const dim3 gh((uint32_t)MT * NT * a.C);
+    if (a.epi == EPI_FWD && a.pool_out != nullptr)
+      hipLaunchKernelGGL((conv_lds_kernel<256, 128, 4, 2, EPI_FWD, false, true, true, 1>), gh, dim3(Halo128Cfg::NTHR),
+                         (halo_lds_of<Halo128Cfg, 1, 1>()), s, b, fw, fh, fc, MT, NT);
+    else if (a.epi == EPI_FWD)
+      hipLaunchKernelGGL((conv_lds_kernel<256, 128, 4, 2, EPI_FWD, false, true, false, 1>), gh, dim3(Halo128Cfg::NTHR),
+                         (halo_lds_of<Halo128Cfg, 1, 1>()), s, b, fw, fh, fc, MT, NT);
+    else
+      hipLaunchKernelGGL((conv_lds_kernel<256, 128, 4, 2, EPI_DGRAD, false, true, false, 1>), gh,
+                         dim3(Halo128Cfg::NTHR), (halo_lds_of<Halo128Cfg, 1, 1>()), s, b, fw, fh, fc, MT, NT);
+    return hipGetLastError();
+  }
   if (use_halo) {
     if (a.epi == EPI_FWD && a.pool_out != nullptr && NT == 1)
       hipLaunchKernelGGL((conv_lds_kernel<256, 256, kHaloWM, 4, EPI_FWD, false, true, true>), g, dim3(HaloCfg::NTHR),

@@ -60,11 +60,13 @@ def kernel_label(name: str) -> str:
         return f"conv_wgrad<{t},{m.group(2)}x{m.group(3)},w{w},{'vec' if m.group(6) == 'true' else 'gather'}>"
     # (an optional last flag marks the halo forward that also writes the image means)
     m = re.search(r"conv_lds_kernel<(\d+), (\d+), (\d+), (\d+), (\d), (true|false)(, (true|false))?"
-                  r"(, (true|false))?>", name)
+                  r"(, (true|false))?(, (\d))?>", name)
     if m:
         kind = "conv_fwd" if m.group(5) == "0" else "conv_dgrad"
         w = int(m.group(3)) * int(m.group(4))
         mode = "halo" if m.group(8) == "true" else "lds"
+        if mode == "halo" and m.group(12) == "1":  # one halo buffer
+            return f"{kind}<bf16,{m.group(1)}x{m.group(2)}x64,w{w},halo1>"
         kt = 192 if (mode == "halo" and m.group(2) == "64") else 64  # tap-row k tiles
         return f"{kind}<bf16,{m.group(1)}x{m.group(2)}x{kt},w{w},{mode}>"
     m = re.search(r"conv_img_kernel<(\d+), (\d+), (\d)>", name)

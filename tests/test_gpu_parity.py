@@ -141,7 +141,7 @@ def check_metrics(ctx, o, cfg):
 @pytest.mark.parametrize("name", ["tiny", "tiny_jsd", "ragged", "ragged_bf16", "ragged_res_bf16", "tiny_norm",
                                   "ragged_norm_bf16", "tiny_recipe", "ragged_recipe_bf16", "halo_res_bf16",
                                   "halo_split_bf16", "img32_bf16", "col_ragged_bf16", "wide_head_bf16",
-                                  "halo_maxhead_bf16"])
+                                  "halo_maxhead_bf16", "halo128_bf16"])
 def test_run_parity_with_fusion(name):
     cfg = get_config(name)
     ctx, o, theta0, losses, flips = matched_run(cfg, cfg["T"])
@@ -151,7 +151,8 @@ def test_run_parity_with_fusion(name):
 
 @pytest.mark.parametrize("name", ["ragged", "ragged_bf16", "ragged_res_bf16", "tiny", "tiny_norm", "ragged_norm_bf16",
                                   "tiny_recipe", "ragged_recipe_bf16", "halo_res_bf16", "halo_split_bf16",
-                                  "img32_bf16", "col_ragged_bf16", "wide_head_bf16", "halo_maxhead_bf16"])
+                                  "img32_bf16", "col_ragged_bf16", "wide_head_bf16", "halo_maxhead_bf16",
+                                  "halo128_bf16"])
 def test_intermediates_one_round(name):
     cfg = get_config(name)
     ctx, assignment = driver.setup(cfg)

@@ -21,6 +21,15 @@ def test_halo_forward_instantiations_share_a_label(flag):
     assert ps.kernel_label(HALO.format(flag)) == "conv_fwd<bf16,256x256x64,w16,halo>"
 
 
+def test_one_buffer_halo_label():
+    for avg in ("false", "true"):
+        assert ps.kernel_label("void (anonymous namespace)::conv_lds_kernel<256, 128, 4, 2, 0, false, true, "
+                               f"{avg}, 1>(ConvArgs, FastDiv, FastDiv, FastDiv, int, int)") == \
+            "conv_fwd<bf16,256x128x64,w8,halo1>"
+    assert ps.kernel_label("void (anonymous namespace)::conv_lds_kernel<256, 256, 4, 4, 1, false, true, false, 2>"
+                           "(ConvArgs, FastDiv, FastDiv, FastDiv, int, int)") == "conv_dgrad<bf16,256x256x64,w16,halo>"
+
+
 def test_other_labels():
     assert ps.kernel_label("void (anonymous namespace)::conv_lds_kernel<256, 64, 8, 2, 1, false, true>"
                            "(ConvArgs, FastDiv, FastDiv, FastDiv, int, int)") == "conv_dgrad<bf16,256x64x192,w16,halo>"
