@@ -18,6 +18,14 @@ Layer tuples:
                                     output it normalises
     ("gnorm", ch, groups)           group normalisation over (H, W, channels
                                     of a group) per example, affine, then ReLU
+    ("block", cin, cout, stride, groups)
+                                    ResNet basic block: conv3x3 (stride,
+                                    pad 1) -> norm -> ReLU -> conv3x3 -> norm,
+                                    plus the shortcut (the input itself, or
+                                    conv1x1 (stride, no pad) -> norm when
+                                    stride > 1 or cin != cout), added before
+                                    the final ReLU; norm = batch norm
+                                    (groups 0) or group norm (groups)
 
 The client segment is layers[:cut]; the server segment is layers[cut:].
 
@@ -48,6 +56,23 @@ _SERVER_WIDE = [("conv", 64, 256, False), ("conv", 256, 256, True), ("conv", 256
                 ("conv", 256, 256, True), ("maxpool",), ("avgpool",), ("linear", 256, 10)]
 
 _CIFAR_DATA = dict(N_ex=50000, H=32, W=32, Cin=3, L=10, noise_std=0.5)
+
+
+def _resnet(widths, client_groups, blocks=2, classes=10):
+    """ResNet-18 for 32 x 32 inputs split after its second stage (Sec. V-A):
+    a 3x3 stem conv with group norm, then four stages of `blocks` basic
+    blocks of the given widths (stride 2 at the first block of stages 2-4),
+    group norm in the client segment (stem and stages 1-2) and batch norm in
+    the server segment (stages 3-4), global average pool, linear head."""
+    layers = [("conv", 3, widths[0], False), ("gnorm", widths[0], client_groups)]
+    cin = widths[0]
+    for st, w in enumerate(widths):
+        for b in range(blocks):
+            stride = 2 if (st > 0 and b == 0) else 1
+            layers.append(("block", cin, w, stride, client_groups if st < 2 else 0))
+            cin = w
+    layers += [("avgpool",), ("linear", cin, classes)]
+    return layers, 2 + 2 * blocks  # cut after stage 2
 
 CONFIGS = {
     # Tiny reference workload: 16 clients in 2 random clusters of 8.
@@ -85,6 +110,31 @@ CONFIGS = {
         K=256, C=16, B=128, alpha=0.1, rule="label_l1", **_CIFAR_DATA,
         layers=_CIFAR_CLIENT + _SERVER_WIDE, cut=3,
         dtype="bf16", lr=0.05, momentum=0.9, F=50, T=1000, seed=0),
+    # The paper's model (Sec. V-A): ResNet-18 split after its second stage,
+    # group norm in the client segment (32 groups), batch norm in the server
+    # segment, on the CIFAR-shaped data: K = 256 clients in N = 4 clusters of
+    # the paper's label-aware rule (Eq. 4), B = 64 per cluster, its training
+    # recipe (SGD lr 0.01, momentum 0.9, Nesterov, weight decay 5e-4, label
+    # smoothing 0.1) and fusion after every epoch (the epoch-barrier
+    # schedule).  Precision fp32 (the paper states none).
+    "resnet18": dict(
+        K=256, C=4, B=64, alpha=0.3, rule="label_jsd", **_CIFAR_DATA,
+        layers=_resnet((64, 128, 256, 512), 32)[0], cut=_resnet((64, 128, 256, 512), 32)[1],
+        dtype="f32", lr=0.01, momentum=0.9, nesterov=True, weight_decay=5e-4, label_smoothing=0.1,
+        F=0, T=3, seed=0, schedule="epoch"),
+    # The same topology at small size (16 x 16 images, widths 8-64), fp32 and
+    # bf16: every block kind (identity and projection shortcut, stride 1 and
+    # 2, group and batch norm), stage 4 on 2 x 2 maps (batch norm over 64
+    # values per channel).
+    "resnet_tiny": dict(
+        K=16, C=2, B=16, L=4, N_ex=512, H=16, W=16, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="random", layers=_resnet((8, 16, 32, 64), 4, classes=4)[0], cut=_resnet((8, 16, 32, 64), 4)[1],
+        dtype="f32", lr=0.05, momentum=0.9, F=2, T=4, seed=0),
+    "resnet_tiny_bf16": dict(
+        K=16, C=2, B=16, L=4, N_ex=512, H=16, W=16, Cin=3, noise_std=0.5, alpha=0.5,
+        rule="random", layers=_resnet((8, 16, 32, 64), 4, classes=4)[0], cut=_resnet((8, 16, 32, 64), 4)[1],
+        dtype="bf16", lr=0.05, momentum=0.9, F=2, T=4, seed=0, nesterov=True, weight_decay=5e-4,
+        label_smoothing=0.1),
     # Small parity workloads whose GEMM sizes are ragged against every tile
     # size (M, N and K tails; more than one N tile; a residual layer).
     "ragged": dict(
@@ -238,6 +288,22 @@ CONFIGS = {
 }
 
 
+def block_has_projection(spec) -> bool:
+    """A block whose shortcut is a strided 1x1 conv + norm (shape change)."""
+    return spec[3] != 1 or spec[1] != spec[2]
+
+
+# Parameters of a block, in order: (tag, shape) for cin, cout; conv weights
+# [cout][r][s][cin], then bias, then the norm's gamma and beta.
+def block_params(spec) -> list:
+    _, cin, cout, _, _ = spec
+    out = [("w1", (cout, 3, 3, cin)), ("b1", (cout,)), ("n1w", (cout,)), ("n1b", (cout,)),
+           ("w2", (cout, 3, 3, cout)), ("b2", (cout,)), ("n2w", (cout,)), ("n2b", (cout,))]
+    if block_has_projection(spec):
+        out += [("wp", (cout, 1, 1, cin)), ("bp", (cout,)), ("npw", (cout,)), ("npb", (cout,))]
+    return out
+
+
 def get_config(name: str, **overrides) -> dict:
     """Return a deep copy of a named workload with optional field overrides."""
     cfg = copy.deepcopy(CONFIGS[name])
@@ -258,6 +324,10 @@ def model_layers(cfg: dict) -> list:
         out.append((spec, h, w, c))
         kind = spec[0]
         if kind in ("bnorm", "gnorm"):
+            continue
+        if kind == "block":
+            c = spec[2]
+            h, w = (h - 1) // spec[3] + 1, (w - 1) // spec[3] + 1
             continue
         if kind == "conv":
             c = spec[2]
@@ -280,6 +350,8 @@ def param_layout(cfg: dict) -> list:
             shapes = [("w", (spec[2], spec[1])), ("b", (spec[2],))]
         elif spec[0] in ("bnorm", "gnorm"):
             shapes = [("w", (spec[1],)), ("b", (spec[1],))]
+        elif spec[0] == "block":
+            shapes = block_params(spec)
         else:
             continue
         for tag, shp in shapes:
@@ -306,13 +378,22 @@ def param_counts(cfg: dict) -> tuple:
 
 
 def norm_layout(cfg: dict) -> list:
-    """[(layer_index, 'mean'|'var'|'count', shape, offset)] of the
-    normalisation state (bnorm layers only)."""
+    """[(key, 'mean'|'var'|'count', shape, offset)] of the normalisation
+    state: every batch norm in layer order, key = its layer index, or
+    (layer index, 'n1' | 'n2' | 'np') for the norms of a block (its first,
+    second and shortcut norm, in that order)."""
     out, off = [], 0
     for i, spec in enumerate(cfg["layers"]):
-        if spec[0] != "bnorm":
+        if spec[0] == "bnorm":
+            keys = [(i, spec[1])]
+        elif spec[0] == "block" and spec[4] == 0:
+            keys = [((i, "n1"), spec[2]), ((i, "n2"), spec[2])]
+            if block_has_projection(spec):
+                keys.append(((i, "np"), spec[2]))
+        else:
             continue
-        for tag, shp in (("mean", (spec[1],)), ("var", (spec[1],)), ("count", (1,))):
-            out.append((i, tag, shp, off))
-            off += int(shp[0])
+        for key, ch in keys:
+            for tag, shp in (("mean", (ch,)), ("var", (ch,)), ("count", (1,))):
+                out.append((key, tag, shp, off))
+                off += int(shp[0])
     return out

@@ -69,10 +69,13 @@ def init_params(cfg: dict) -> np.ndarray:
     theta = np.empty(total, dtype=np.float32)
     for i, tag, shp, off in layout:
         spec = cfg["layers"][i]
-        if spec[0] in ("bnorm", "gnorm"):  # gamma = 1, beta = 0 (the PyTorch default)
-            theta[off:off + int(np.prod(shp))] = 1.0 if tag == "w" else 0.0
+        if spec[0] in ("bnorm", "gnorm") or tag.startswith("n"):  # gamma = 1, beta = 0 (PyTorch default)
+            theta[off:off + int(np.prod(shp))] = 1.0 if tag[-1] == "w" else 0.0
             continue
-        fan_in = 9 * spec[1] if spec[0] == "conv" else spec[1]
+        if spec[0] == "block":  # fan-in of the block's conv the tag names
+            fan_in = {"1": 9 * spec[1], "2": 9 * spec[2], "p": spec[1]}[tag[1]]
+        else:
+            fan_in = 9 * spec[1] if spec[0] == "conv" else spec[1]
         bound = 1.0 / np.sqrt(fan_in)
         n = int(np.prod(shp))
         theta[off:off + n] = rng.uniform(-bound, bound, size=n).astype(np.float32)

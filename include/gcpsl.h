@@ -74,24 +74,42 @@ extern "C" {
 #define GCPSL_LINEAR 4   /* fully connected layer producing the logits       */
 #define GCPSL_BATCHNORM 5 /* batch norm of the conv before it, then ReLU     */
 #define GCPSL_GROUPNORM 6 /* group norm of the conv before it, then ReLU     */
+#define GCPSL_BLOCK 7     /* ResNet basic block (Sec. V-A), see below        */
 
 /* Layer flags. */
 #define GCPSL_RESIDUAL 1 /* conv output is ReLU(conv(x) + b + x); cin == cout */
+#define GCPSL_STRIDE2 2  /* GCPSL_BLOCK: stride 2 (first conv, shortcut)     */
 
 typedef struct gcpsl_layer {
-  int32_t kind;   /* GCPSL_CONV3X3 ... GCPSL_GROUPNORM                     */
-  int32_t cin;    /* input channels (conv, linear, norm); ignored for pools */
-  int32_t cout;   /* output channels (conv, linear; norm: = cin)           */
-  int32_t flags;  /* GCPSL_RESIDUAL or 0                                   */
-  int32_t groups; /* GCPSL_GROUPNORM: groups (dividing the channels); else 0 */
+  int32_t kind;   /* GCPSL_CONV3X3 ... GCPSL_BLOCK                        */
+  int32_t cin;    /* input channels (conv, linear, norm, block); ignored for pools */
+  int32_t cout;   /* output channels (conv, linear, block; norm: = cin)    */
+  int32_t flags;  /* GCPSL_RESIDUAL (conv), GCPSL_STRIDE2 (block) or 0     */
+  int32_t groups; /* GCPSL_GROUPNORM, GCPSL_BLOCK: groups (dividing the
+                     channels; block: 0 = batch norm); else 0              */
 } gcpsl_layer;
 
 /*
- * Supported model shapes: layer 0 is a conv; every max pool follows a conv or
- * norm layer and sees an even H and W; the last two layers are GCPSL_AVGPOOL
- * then GCPSL_LINEAR (cout = L), optionally preceded by one max pool; conv
- * channel counts are either 3 (the image layer) or multiples of 8; at most 16
- * conv layers.  Other shapes return GCPSL_EUNSUPPORTED.
+ * Supported model shapes: layer 0 is a conv; every max pool follows a conv,
+ * norm or block layer and sees an even H and W; the last two layers are
+ * GCPSL_AVGPOOL then GCPSL_LINEAR (cout = L), optionally preceded by one max
+ * pool; conv channel counts are either 3 (the image layer) or multiples of 8;
+ * at most 48 weight-copy jobs (two per conv: 24 convs, a block counting its
+ * two or three).  Other shapes return GCPSL_EUNSUPPORTED.
+ *
+ * GCPSL_BLOCK, the basic block of the paper's ResNet-18 (Sec. V-A): y =
+ * ReLU(norm2(conv2(ReLU(norm1(conv1(x))))) + shortcut(x)), conv1 3x3 with
+ * the block's stride (1, or 2 with GCPSL_STRIDE2; pad 1), conv2 3x3 stride 1,
+ * shortcut = x when stride 1 and cin == cout, else norm(conv 1x1 with the
+ * stride, no pad) (no ReLU on that norm); every norm is batch norm (groups
+ * 0) or group norm with `groups` groups, applied as for GCPSL_BATCHNORM /
+ * GCPSL_GROUPNORM below.  cin, cout multiples of 8; a block follows a conv
+ * with ReLU, a norm or a block.  Its parameters, in the parameter vector:
+ * conv1 weight [cout][3][3][cin] and bias, norm1 gamma and beta, conv2
+ * weight [cout][3][3][cout] and bias, norm2 gamma and beta, then (with a
+ * projection) the 1x1 weight [cout][1][1][cin] and bias, its norm's gamma
+ * and beta.  With batch norm its running statistics (norm1, norm2, the
+ * projection's) follow in norm_state in that order.
  *
  * Normalisation layers (Sec. IV-B: GroupNorm in the client segment,
  * BatchNorm in the server segment) follow a conv without GCPSL_RESIDUAL; that

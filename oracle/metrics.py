@@ -64,6 +64,9 @@ def cut_elements(cfg):
     for spec in cfg["layers"][:cfg["cut"]]:
         if spec[0] == "conv":
             c = spec[2]
+        elif spec[0] == "block":  # 3x3 conv with pad 1 and the block's stride
+            c = spec[2]
+            h, w = (h - 1) // spec[3] + 1, (w - 1) // spec[3] + 1
         elif spec[0] == "maxpool":
             h, w = h // 2, w // 2
     return h * w * c

@@ -26,6 +26,12 @@ workloads' plain CNNs):
   gnorm      group normalisation (Wu and He 2018): the same with mean and
              variance per example over (H, W, the channels of a group).  The
              client segment's normalisation (Sec. IV-B).
+  block      ResNet basic block (He et al. 2016; the paper's ResNet-18,
+             Sec. V-A): conv3x3 with the block's stride (pad 1) -> norm ->
+             ReLU -> conv3x3 -> norm; the shortcut is the block input, or a
+             1x1 conv with the stride (no pad) -> norm when the shape
+             changes; the output is ReLU(second norm + shortcut).  Batch norm
+             (groups 0, server) or group norm (client), as above.
 
 BatchNorm's running statistics (Sec. IV-B: running mean, running variance
 and batch counter, the server normalisation state) follow the PyTorch
@@ -39,8 +45,12 @@ matrices (biases stay at the master's precision); every conv output after
 its ReLU, or its raw output when a norm layer follows; every norm output
 after its ReLU; the average-pool output; the gradient with respect to each
 conv's pre-activation and each norm's pre-ReLU value; and each input
-gradient a conv returns (including the cut gradient).  Norm statistics and
-parameters stay unrounded.  Logits, loss, logit gradients, parameter gradients stay unrounded.
+gradient a conv returns (including the cut gradient).  Inside a block the
+same holds for each of its convs and norms (the shortcut norm's output is
+rounded; the block output after its ReLU; the gradient at the sum before
+that ReLU; the block's input gradient = the rounded sum of its first conv's
+input gradient and the shortcut's).  Norm statistics and parameters stay
+unrounded.  Logits, loss, logit gradients, parameter gradients stay unrounded.
 
 Conv uses im2col with a library matmul for the forward pass and the weight
 gradient, and the textbook col2im scatter for the input gradient.
@@ -51,6 +61,7 @@ import numpy as np
 import torch
 
 from gcpsl_inputs import param_layout
+from gcpsl_inputs.configs import block_has_projection
 
 
 def round_bf16(x):
@@ -81,43 +92,67 @@ def rounder(dtype: str):
 
 # ----------------------------------------------------------------- layers
 
-def im2col3x3(x):
-    """[Bt,H,W,Ci] -> [Bt*H*W, 9*Ci], column order (kernel row, kernel col, ci):
-    column (r, s, i) of pixel (h, w) is x[h + r - 1, w + s - 1, i], zero
-    outside the image.  (The nine shifted copies are plain element copies;
-    torch's CPU copy only spreads them over the host threads.)"""
+def conv_out_size(n, k, stride, pad):
+    return (n + 2 * pad - k) // stride + 1
+
+
+def im2col(x, R, S, stride, pad):
+    """[Bt,H,W,Ci] -> [Bt*Ho*Wo, R*S*Ci], column order (kernel row, kernel
+    col, ci): column (r, s, i) of output pixel (ho, wo) is
+    x[ho*stride + r - pad, wo*stride + s - pad, i], zero outside the image.
+    (The shifted copies are plain element copies; torch's CPU copy only
+    spreads them over the host threads.)"""
     Bt, H, W, Ci = x.shape
-    xp = torch.zeros((Bt, H + 2, W + 2, Ci), dtype=torch.float64)
-    xp[:, 1:-1, 1:-1, :] = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float64))
-    cols = torch.empty((Bt, H, W, 3, 3, Ci), dtype=torch.float64)
-    for r in range(3):
-        for s in range(3):
-            cols[:, :, :, r, s, :] = xp[:, r:r + H, s:s + W, :]
-    return cols.numpy().reshape(Bt * H * W, 9 * Ci)
+    Ho, Wo = conv_out_size(H, R, stride, pad), conv_out_size(W, S, stride, pad)
+    xp = torch.zeros((Bt, H + 2 * pad, W + 2 * pad, Ci), dtype=torch.float64)
+    xp[:, pad:pad + H, pad:pad + W, :] = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float64))
+    cols = torch.empty((Bt, Ho, Wo, R, S, Ci), dtype=torch.float64)
+    for r in range(R):
+        for s in range(S):
+            cols[:, :, :, r, s, :] = xp[:, r:r + stride * (Ho - 1) + 1:stride, s:s + stride * (Wo - 1) + 1:stride, :]
+    return cols.numpy().reshape(Bt * Ho * Wo, R * S * Ci)
+
+
+def im2col3x3(x):
+    """The 3x3, stride 1, pad 1 columns."""
+    return im2col(x, 3, 3, 1, 1)
+
+
+def conv_forward(x, w, b, stride=1, pad=1):
+    """Pre-activation y[b,ho,wo,o] = b[o] + sum_{r,s,i} x[b, ho*stride+r-pad,
+    wo*stride+s-pad, i] w[o,r,s,i] (cross-correlation, zero padding)."""
+    Bt, H, W, _ = x.shape
+    Co, R, S, _ = w.shape
+    Ho, Wo = conv_out_size(H, R, stride, pad), conv_out_size(W, S, stride, pad)
+    return (im2col(x, R, S, stride, pad) @ w.reshape(Co, -1).T + b).reshape(Bt, Ho, Wo, Co)
+
+
+def conv_backward(x, w, gp, stride=1, pad=1):
+    """Given dL/dpre gp [Bt,Ho,Wo,Co]: (dL/dx, dL/dw, dL/db)."""
+    Bt, H, W, Ci = x.shape
+    Co, R, S, _ = w.shape
+    _, Ho, Wo, _ = gp.shape
+    gf = gp.reshape(-1, Co)
+    dw = (gf.T @ im2col(x, R, S, stride, pad)).reshape(w.shape)
+    db = gf.sum(axis=0)
+    dcols = torch.from_numpy((gf @ w.reshape(Co, -1)).reshape(Bt, Ho, Wo, R, S, Ci))
+    # col2im: each column's value added back to the input pixel it was read
+    # from, taps in (r, s) order
+    dxp = torch.zeros((Bt, H + 2 * pad, W + 2 * pad, Ci), dtype=torch.float64)
+    for r in range(R):
+        for s in range(S):
+            dxp[:, r:r + stride * (Ho - 1) + 1:stride, s:s + stride * (Wo - 1) + 1:stride, :] += dcols[:, :, :, r, s, :]
+    return dxp[:, pad:pad + H, pad:pad + W, :].numpy(), dw, db
 
 
 def conv3x3_forward(x, w, b):
     """Pre-activation y[b,h,w,o] = b[o] + sum_{r,s,i} x[b,h+r-1,w+s-1,i] w[o,r,s,i]."""
-    Bt, H, W, _ = x.shape
-    Co = w.shape[0]
-    return (im2col3x3(x) @ w.reshape(Co, -1).T + b).reshape(Bt, H, W, Co)
+    return conv_forward(x, w, b, 1, 1)
 
 
 def conv3x3_backward(x, w, gp):
     """Given dL/dpre gp [Bt,H,W,Co]: (dL/dx, dL/dw, dL/db)."""
-    Bt, H, W, Ci = x.shape
-    Co = w.shape[0]
-    gf = gp.reshape(-1, Co)
-    dw = (gf.T @ im2col3x3(x)).reshape(w.shape)
-    db = gf.sum(axis=0)
-    dcols = torch.from_numpy((gf @ w.reshape(Co, -1)).reshape(Bt, H, W, 3, 3, Ci))
-    # col2im: each column's value added back to the input pixel it was read
-    # from, taps in (r, s) order
-    dxp = torch.zeros((Bt, H + 2, W + 2, Ci), dtype=torch.float64)
-    for r in range(3):
-        for s in range(3):
-            dxp[:, r:r + H, s:s + W, :] += dcols[:, :, :, r, s, :]
-    return dxp[:, 1:-1, 1:-1, :].numpy(), dw, db
+    return conv_backward(x, w, gp, 1, 1)
 
 
 def _windows(x):
@@ -278,6 +313,35 @@ def split_forward_backward(cfg, theta, x, y, keep=False, choose=None):
             if keep:
                 rec[f"pre{i}"] = u
             out = relu(i, u)
+        elif kind == "block":
+            _, cin, cout, stride, groups = spec
+            gr, q = groups or None, p[i]
+            z1 = rnd(conv_forward(a, rnd(q["w1"]), q["b1"], stride, 1))
+            u1, xh1, rs1, m1, v1 = norm_forward(z1, q["n1w"], q["n1b"], gr)
+            a1 = relu((i, "n1"), u1)
+            z2 = rnd(conv_forward(a1, rnd(q["w2"]), q["b2"], 1, 1))
+            u2, xh2, rs2, m2, v2 = norm_forward(z2, q["n2w"], q["n2b"], gr)
+            st = {"n1": (z1, xh1, rs1, m1, v1), "n2": (z2, xh2, rs2, m2, v2), "a1": a1}
+            if block_has_projection(spec):
+                zp = rnd(conv_forward(a, rnd(q["wp"]), q["bp"], stride, 0))
+                up, xhp, rsp, mp, vp = norm_forward(zp, q["npw"], q["npb"], gr)
+                st["np"] = (zp, xhp, rsp, mp, vp)
+                sc = rnd(up)
+            else:
+                sc = a
+            norm[i] = st
+            if gr is None:
+                for sub in ("n1", "n2", "np"):
+                    if sub in st:
+                        z_, _, _, mean_, var_ = st[sub]
+                        rec["bn_batch"][(i, sub)] = (mean_, var_, z_.shape[0] * z_.shape[1] * z_.shape[2])
+            if keep:
+                rec[f"pre{i}"] = u2 + sc
+                rec[f"pre{i}.n1"] = u1
+                rec[f"z{i}.1"], rec[f"z{i}.2"], rec[f"act{i}.n1"] = z1, z2, a1
+                if "np" in st:
+                    rec[f"z{i}.p"], rec[f"sc{i}"] = st["np"][0], sc
+            out = relu(i, u2 + sc)
         elif kind == "maxpool":
             out, args[i] = maxpool2_forward(a)
             if choose is not None:
@@ -320,6 +384,32 @@ def split_forward_backward(cfg, theta, x, y, keep=False, choose=None):
             gview[i]["w"][...] = dgamma
             gview[i]["b"][...] = dbeta
             g = rnd(dz)
+        elif kind == "block":
+            _, cin, cout, stride, groups = spec
+            gr, q, st = groups or None, p[i], norm[i]
+            du2 = rnd(g * mask[i])  # at the sum before the block's last ReLU
+            z2, xh2, rs2, _, _ = st["n2"]
+            dz2, gview[i]["n2w"][...], gview[i]["n2b"][...] = norm_backward(du2, xh2, rs2, q["n2w"], gr)
+            dz2 = rnd(dz2)
+            da1, gview[i]["w2"][...], gview[i]["b2"][...] = conv_backward(st["a1"], rnd(q["w2"]), dz2, 1, 1)
+            du1 = rnd(da1 * mask[(i, "n1")])
+            z1, xh1, rs1, _, _ = st["n1"]
+            dz1, gview[i]["n1w"][...], gview[i]["n1b"][...] = norm_backward(du1, xh1, rs1, q["n1w"], gr)
+            dz1 = rnd(dz1)
+            dx, gview[i]["w1"][...], gview[i]["b1"][...] = conv_backward(a_in, rnd(q["w1"]), dz1, stride, 1)
+            if "np" in st:
+                zp, xhp, rsp, _, _ = st["np"]
+                dzp, gview[i]["npw"][...], gview[i]["npb"][...] = norm_backward(du2, xhp, rsp, q["npw"], gr)
+                dzp = rnd(dzp)
+                dxs, gview[i]["wp"][...], gview[i]["bp"][...] = conv_backward(a_in, rnd(q["wp"]), dzp, stride, 0)
+                dxs = rnd(dxs)
+            else:
+                dxs = du2
+            if keep:
+                rec[f"gpre{i}"], rec[f"gpre{i}.n1"], rec[f"dz{i}.1"], rec[f"dz{i}.2"] = du2, du1, dz1, dz2
+                if "np" in st:
+                    rec[f"dz{i}.p"], rec[f"gsc{i}"] = dzp, dxs
+            g = rnd(dx + dxs)
         elif kind == "conv":
             normed = i + 1 < len(layers) and layers[i + 1][0] in ("bnorm", "gnorm")
             gp = g if normed else rnd(g * mask[i])

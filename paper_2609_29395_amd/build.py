@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OBJDIR = os.path.join(os.path.dirname(HERE), "_build", "gcpsl")
 LIB = os.path.join(HERE, "libgcpsl.so")
-SOURCES = ["api.cpp", "assign.cpp", "k_conv.hip", "k_misc.hip", "k_wgrad_lds.hip", "k_conv_lds.hip", "k_conv_img.hip", "k_norm.hip"]
+SOURCES = ["api.cpp", "assign.cpp", "k_conv.hip", "k_misc.hip", "k_wgrad_lds.hip", "k_conv_lds.hip", "k_conv_img.hip", "k_norm.hip", "k_block.hip"]
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wshadow", "-Wno-unused-function",

@@ -44,11 +44,28 @@ struct LayerInfo {
   int nstat = 0;              // norm statistics per replica
   int64_t st_off = 0;         // batch norm: running statistics in the state vector
   size_t mean_off = 0, rstd_off = 0, sums_off = 0;
+  int blk = -1;               // GCPSL_BLOCK: its entry in Plan::blocks
+};
+
+// A ResNet basic block (GCPSL_BLOCK) as internal layers, each with its own
+// parameters, buffers and split-K plan in the LayerInfo fields the other
+// layers use: c1 (3 x 3, the block's stride; at stride 2 on im2col rows of
+// Kc1 = 9 cin columns) -> n1 (norm, ReLU) -> c2 (3 x 3) -> n2 (norm, + the
+// shortcut, ReLU: its output and gradient are the block's); with a
+// projection, cp (1 x 1, stride, on rows of the strided input) -> np (norm,
+// no ReLU) is the shortcut.  At stride 2 the input gradients of c1 and cp
+// take their output gradients spread back to the input grid (gup).
+struct BlockInfo {
+  int stride = 1;
+  bool proj = false;
+  int Kc1 = 0, Kcp = 0;
+  LayerInfo c1, n1, c2, n2, cp, np;
+  size_t cols1_off = 0, xs_off = 0, gup_off = 0, gsc_off = 0;
 };
 
 bool is_norm(int kind) { return kind == GCPSL_BATCHNORM || kind == GCPSL_GROUPNORM; }
-// layers whose output is followed by ReLU and stored: conv or norm
-bool is_act(int kind) { return kind == GCPSL_CONV3X3 || is_norm(kind); }
+// layers whose output is followed by ReLU and stored: conv, norm or block
+bool is_act(int kind) { return kind == GCPSL_CONV3X3 || is_norm(kind) || kind == GCPSL_BLOCK; }
 
 struct Plan {
   int dtype = 0, esz = 4;
@@ -56,6 +73,7 @@ struct Plan {
   int64_t n_examples = 0, max_steps = 0;
   int max_window = 1;
   std::vector<LayerInfo> ly;
+  std::vector<BlockInfo> blocks;
   int64_t P = 0, Pc = 0, S = 0;
   int head_conv = -1, avg_idx = -1, lin_idx = -1;  // head_conv: conv or norm feeding the head pooling
   int norm_chunk_px = 256;
@@ -91,9 +109,14 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
     return gcpsl_fail(GCPSL_EINVAL, "unknown schedule");
   if (!d->layers || d->n_layers < 3) return gcpsl_fail(GCPSL_EINVAL, "need at least conv, avgpool, linear");
   {
-    int convs = 0;
-    for (int i = 0; i < d->n_layers; ++i) convs += d->layers[i].kind == GCPSL_CONV3X3;
-    if (2 * convs > kMaxPrepJobs) return gcpsl_fail(GCPSL_EUNSUPPORTED, "more than 16 conv layers");
+    // weight-copy jobs (prep_add_layer): two per conv, at most
+    int jobs = 0;
+    for (int i = 0; i < d->n_layers; ++i) {
+      jobs += d->layers[i].kind == GCPSL_CONV3X3 ? 2 : 0;
+      if (d->layers[i].kind == GCPSL_BLOCK)
+        jobs += 4 + ((d->layers[i].flags & GCPSL_STRIDE2) || d->layers[i].cin != d->layers[i].cout ? 2 : 0);
+    }
+    if (jobs > kMaxPrepJobs) return gcpsl_fail(GCPSL_EUNSUPPORTED, "too many conv layers (weight-copy jobs)");
   }
   if (d->cut < 1 || d->cut > d->n_layers - 2) return gcpsl_fail(GCPSL_EINVAL, "cut outside the model");
   if ((int64_t)d->B * d->H * d->W > INT32_MAX / 4) return gcpsl_fail(GCPSL_EUNSUPPORTED, "batch too large");
@@ -150,6 +173,57 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
         l.st_off = p.S;
         p.S += 2 * c + 1;  // running mean, running variance, counter
       }
+    } else if (kind == GCPSL_BLOCK) {
+      const int cout = l.spec.cout;
+      if (i == 0 || !is_act(p.ly[i - 1].spec.kind) || p.ly[i - 1].no_relu)
+        return gcpsl_fail(GCPSL_EUNSUPPORTED, "a block must follow a conv, norm or block");
+      if (l.spec.cin != c) return gcpsl_fail(GCPSL_EINVAL, "block cin does not match its input");
+      if (c % 8 != 0 || cout < 8 || cout % 8 != 0)
+        return gcpsl_fail(GCPSL_EUNSUPPORTED, "block channels must be multiples of 8");
+      if (l.spec.flags & ~GCPSL_STRIDE2) return gcpsl_fail(GCPSL_EINVAL, "unknown block flag");
+      const int st = (l.spec.flags & GCPSL_STRIDE2) ? 2 : 1;
+      if (st == 2 && (H % 2 || W % 2)) return gcpsl_fail(GCPSL_EINVAL, "a stride-2 block needs even H and W");
+      l.groups = l.spec.groups;
+      if (l.groups < 0 || (l.groups && cout % l.groups) || !norm_ok(d->dtype, cout, l.groups))
+        return gcpsl_fail(GCPSL_EUNSUPPORTED, "block norm channels / groups");
+      BlockInfo bk;
+      bk.stride = st;
+      bk.proj = st != 1 || c != cout;
+      l.blk = (int)p.blocks.size();
+      l.Co = cout; l.Ho = H / st; l.Wo = W / st;
+      // internal layers: input geometry, parameters (w, b, gamma, beta in the
+      // order of the layer description), batch-norm state
+      auto conv = [&](LayerInfo &cv, int ci, int co, int hh, int ww, int taps) {
+        cv.spec = gcpsl_layer{GCPSL_CONV3X3, ci, co, 0, 0};
+        cv.H = hh; cv.W = ww; cv.Ci = ci; cv.Co = co; cv.Ho = l.Ho; cv.Wo = l.Wo;
+        cv.nw = (int64_t)co * taps * ci;
+        cv.w_off = P; P += cv.nw;
+        cv.b_off = P; P += co;
+        cv.no_relu = true;
+      };
+      auto nrm = [&](LayerInfo &nl) {
+        nl.spec = gcpsl_layer{l.groups ? GCPSL_GROUPNORM : GCPSL_BATCHNORM, cout, cout, 0, l.groups};
+        nl.H = l.Ho; nl.W = l.Wo; nl.Ci = nl.Co = cout; nl.Ho = l.Ho; nl.Wo = l.Wo;
+        nl.groups = l.groups;
+        nl.w_off = P; P += cout;
+        nl.b_off = P; P += cout;
+        nl.nstat = l.groups ? d->B * l.groups : cout;
+        if (!l.groups) {
+          nl.st_off = p.S;
+          p.S += 2 * cout + 1;
+        }
+      };
+      conv(bk.c1, c, cout, H, W, 9);
+      nrm(bk.n1);
+      conv(bk.c2, cout, cout, l.Ho, l.Wo, 9);
+      nrm(bk.n2);
+      if (bk.proj) {
+        conv(bk.cp, c, cout, H, W, 1);
+        nrm(bk.np);
+      }
+      p.blocks.push_back(bk);
+      H = l.Ho; W = l.Wo;
+      c = cout;
     } else if (kind == GCPSL_MAXPOOL2) {
       if (i == 0 || !is_act(p.ly[i - 1].spec.kind))
         return gcpsl_fail(GCPSL_EUNSUPPORTED, "max pool must follow a conv or a norm layer");
@@ -190,7 +264,7 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
 
   // workspace layout
   const int C = p.C, B = p.B;
-  const int bk = p.dtype == GCPSL_BF16 ? 64 : 32;
+  const int bk_tile = p.dtype == GCPSL_BF16 ? 64 : 32;
   size_t o = 0;
   auto take = [&](size_t bytes) {
     const size_t at = o;
@@ -216,20 +290,122 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   p.x_rs = (int64_t)C * B * p.H * p.W * p.Kc;
   p.off_x = take((size_t)p.esz * p.max_window * p.x_rs);
   size_t part = 0, dbpart = 0, npart = 0;
+  // split-K over pixels for a weight gradient of M pixels per replica with
+  // Ci_eff columns per tap (taps 9, or 1 on im2col rows)
+  auto plan_wgrad = [&](LayerInfo &l, int M, int Ci_eff, int taps, int Hh, int Ww) {
+    int kt = wgrad_k_tile(p.dtype);
+    int nkt = (M + kt - 1) / kt;
+    int bm, bn;
+    const int nwc = taps == 1 ? Ci_eff : 9 * Ci_eff;
+    int splits;
+    if (wgrad_lds_ok(p.dtype, l.Co, Ci_eff) || wgrad_col_ok(p.dtype, l.Co, Ci_eff, taps)) {
+      // pick the split count that minimises (rounds of 256 x per_cu
+      // workgroups) x (k tiles per workgroup + the cost of writing and
+      // re-reading a partial tile, about 16 k tiles)
+      int tile_bk, per_cu;
+      wgrad_lds_tile(l.Co, Ci_eff, Hh, Ww, taps, &bm, &bn, &tile_bk, &per_cu);
+      kt = tile_bk;  // chunks are whole k tiles of the kernel the layer runs
+      nkt = (M + kt - 1) / kt;
+      const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
+      const int64_t slots = 256 * (int64_t)per_cu;
+      int64_t best = -1;
+      splits = 1;
+      for (int sp = 1; sp <= std::min(64, nkt); ++sp) {
+        const int64_t rounds = (tiles * sp + slots - 1) / slots;
+        const int64_t cost = rounds * ((nkt + sp - 1) / sp + (sp > 1 ? 16 * 64 / kt : 0));
+        if (best < 0 || cost < best) best = cost, splits = sp;
+      }
+    } else {
+      wgrad_tile(p.dtype, l.Co, nwc, &bm, &bn);
+      const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
+      const int64_t target = bm * bn >= 256 * 128 ? 512 : 1024;  // workgroups to fill 256 CUs
+      splits = (int)std::min<int64_t>(std::max(1, nkt / 4), (target + tiles - 1) / tiles);
+      splits = std::max(1, splits);
+    }
+    const int per = (nkt + splits - 1) / splits;
+    l.chunk = per * kt;
+    l.splits = (M + l.chunk - 1) / l.chunk;
+    if (l.splits > 1) {
+      part = std::max(part, (size_t)l.splits * C * l.nw);
+      dbpart = std::max(dbpart, (size_t)l.splits * C * l.Co);
+    }
+  };
+  // kernels address one replica's tensors with 32-bit byte offsets and mark
+  // invalid lanes with offset 2^31
+  auto small_enough = [&](int64_t px, int ci, int co, int taps) {
+    return (int64_t)p.esz * px * std::max(ci, co) < (1ll << 31) &&
+           (int64_t)p.esz * std::max(co, ci) * ((int64_t)taps * std::max(ci, co) + 64) < (1ll << 31);
+  };
+  // a norm layer's statistics buffers (output and gradient set by the caller)
+  auto norm_buffers = [&](LayerInfo &l) {
+    const int64_t rs = (int64_t)B * l.H * l.W;
+    l.mean_off = take(sizeof(float) * C * l.nstat);
+    l.rstd_off = take(sizeof(float) * C * l.nstat);
+    l.sums_off = take(sizeof(double) * 2 * C * l.nstat);
+    const int64_t chunks = (rs + p.norm_chunk_px - 1) / p.norm_chunk_px;
+    npart = std::max(npart, (size_t)(C * chunks * l.Co * 2));
+  };
   for (int i = 0; i < n; ++i) {
     LayerInfo &l = p.ly[i];
     const int kind = l.spec.kind;
+    if (kind == GCPSL_BLOCK) {
+      BlockInfo &bk = p.blocks[l.blk];
+      const int64_t px_in = (int64_t)B * l.H * l.W, px = (int64_t)B * l.Ho * l.Wo;
+      if (!small_enough(px_in, l.Ci, l.Co, 9) || !small_enough(px, 9 * l.Ci, l.Co, 1))
+        return gcpsl_fail(GCPSL_EUNSUPPORTED, "per-replica layer tensors must stay below 2 GiB");
+      auto out_buffers = [&](LayerInfo &x) {  // output and its gradient, [B][Ho][Wo][Co]
+        x.stored = true;
+        x.act_rs = px * x.Co;
+        x.act_off = take((size_t)p.esz * C * x.act_rs);
+        x.gpre_off = take((size_t)p.esz * C * x.act_rs);
+      };
+      auto weights = [&](LayerInfo &cv, int taps) {  // compute copies: forward rows, input-gradient rows
+        cv.Kp = round_up(taps * cv.Ci, bk_tile);
+        cv.wf_off = take((size_t)p.esz * C * cv.Co * cv.Kp);
+        cv.Kdp = round_up(taps * cv.Co, bk_tile);
+        cv.wd_off = take((size_t)p.esz * C * cv.Ci * cv.Kdp);
+      };
+      out_buffers(bk.c1);
+      weights(bk.c1, 9);
+      if (bk.stride == 2) {
+        bk.Kc1 = 9 * l.Ci;
+        bk.cols1_off = take((size_t)p.esz * C * px * bk.Kc1);
+        plan_wgrad(bk.c1, (int)px, bk.Kc1, 1, l.Ho, l.Wo);
+      } else {
+        plan_wgrad(bk.c1, (int)px, l.Ci, 9, l.H, l.W);
+      }
+      out_buffers(bk.n1);
+      norm_buffers(bk.n1);
+      out_buffers(bk.c2);
+      weights(bk.c2, 9);
+      plan_wgrad(bk.c2, (int)px, l.Co, 9, l.Ho, l.Wo);
+      // n2 writes the block's output; its gradient is the block's
+      out_buffers(l);
+      bk.n2.stored = true;
+      bk.n2.act_rs = l.act_rs;
+      bk.n2.act_off = l.act_off;
+      bk.n2.gpre_off = l.gpre_off;
+      norm_buffers(bk.n2);
+      if (bk.proj) {
+        bk.Kcp = l.Ci;
+        bk.xs_off = take((size_t)p.esz * C * px * bk.Kcp);
+        out_buffers(bk.cp);
+        weights(bk.cp, 1);
+        plan_wgrad(bk.cp, (int)px, bk.Kcp, 1, l.Ho, l.Wo);
+        out_buffers(bk.np);  // (its gradient buffer is unused: np's gradient is the block's)
+        norm_buffers(bk.np);
+        bk.gsc_off = take((size_t)p.esz * C * px_in * l.Ci);
+      }
+      if (bk.stride == 2) bk.gup_off = take((size_t)p.esz * C * px_in * l.Co);
+      continue;
+    }
     if (is_norm(kind)) {
       const int64_t rs = (int64_t)B * l.H * l.W;
       l.stored = true;
       l.act_rs = rs * l.Co;
       l.act_off = take((size_t)p.esz * C * l.act_rs);
       l.gpre_off = take((size_t)p.esz * C * l.act_rs);  // dL/du
-      l.mean_off = take(sizeof(float) * C * l.nstat);
-      l.rstd_off = take(sizeof(float) * C * l.nstat);
-      l.sums_off = take(sizeof(double) * 2 * C * l.nstat);
-      const int64_t chunks = (rs + p.norm_chunk_px - 1) / p.norm_chunk_px;
-      npart = std::max(npart, (size_t)(C * chunks * l.Co * 2));
+      norm_buffers(l);
       continue;
     }
     if (kind == GCPSL_CONV3X3 || (kind == GCPSL_MAXPOOL2 && !(p.head_maxpool && i == n - 3))) {
@@ -243,62 +419,21 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
     }
     if (kind == GCPSL_CONV3X3) {
       const int64_t rs = (int64_t)B * l.H * l.W;
-      // kernels address one replica's tensors with 32-bit byte offsets and
-      // mark invalid lanes with offset 2^31
-      if ((int64_t)p.esz * rs * std::max(l.Ci, l.Co) >= (1ll << 31) ||
-          (int64_t)p.esz * std::max(l.Co, l.Ci) * (9 * (int64_t)std::max(l.Ci, l.Co) + 64) >= (1ll << 31))
+      if (!small_enough(rs, l.Ci, l.Co, 9))
         return gcpsl_fail(GCPSL_EUNSUPPORTED, "per-replica layer tensors must stay below 2 GiB");
       l.gpre_off = take((size_t)p.esz * C * rs * l.Co);
       if (i > 0 && p.ly[i - 1].spec.kind == GCPSL_MAXPOOL2) {
         l.has_gin = true;
         l.gin_off = take((size_t)p.esz * C * rs * l.Ci);
       }
-      l.Kp = round_up(9 * l.Ci, bk);
+      l.Kp = round_up(9 * l.Ci, bk_tile);
       l.wf_off = take((size_t)p.esz * C * l.Co * l.Kp);
       if (i > 0) {
-        l.Kdp = round_up(9 * l.Co, bk);
+        l.Kdp = round_up(9 * l.Co, bk_tile);
         l.wd_off = take((size_t)p.esz * C * l.Ci * l.Kdp);
       }
-      // split-K over pixels for the weight gradient
-      const int M = B * l.H * l.W;
-      int kt = wgrad_k_tile(p.dtype);
-      int nkt = (M + kt - 1) / kt;
-      int bm, bn;
-      const int nwc = (i == 0 && p.col0) ? p.Kc : 9 * l.Ci;
-      int splits;
-      if (wgrad_lds_ok(p.dtype, l.Co, (i == 0 && p.col0) ? p.Kc : l.Ci) ||
-          wgrad_col_ok(p.dtype, l.Co, (i == 0 && p.col0) ? p.Kc : l.Ci, (i == 0 && p.col0) ? 1 : 9)) {
-        // pick the split count that minimises (rounds of 256 x per_cu
-        // workgroups) x (k tiles per workgroup + the cost of writing and
-        // re-reading a partial tile, about 16 k tiles)
-        int tile_bk, per_cu;
-        wgrad_lds_tile(l.Co, (i == 0 && p.col0) ? p.Kc : l.Ci, l.H, l.W, (i == 0 && p.col0) ? 1 : 9, &bm, &bn,
-                       &tile_bk, &per_cu);
-        kt = tile_bk;  // chunks are whole k tiles of the kernel the layer runs
-        nkt = (M + kt - 1) / kt;
-        const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
-        const int64_t slots = 256 * (int64_t)per_cu;
-        int64_t best = -1;
-        splits = 1;
-        for (int sp = 1; sp <= std::min(64, nkt); ++sp) {
-          const int64_t rounds = (tiles * sp + slots - 1) / slots;
-          const int64_t cost = rounds * ((nkt + sp - 1) / sp + (sp > 1 ? 16 * 64 / kt : 0));
-          if (best < 0 || cost < best) best = cost, splits = sp;
-        }
-      } else {
-        wgrad_tile(p.dtype, l.Co, nwc, &bm, &bn);
-        const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
-        const int64_t target = bm * bn >= 256 * 128 ? 512 : 1024;  // workgroups to fill 256 CUs
-        splits = (int)std::min<int64_t>(std::max(1, nkt / 4), (target + tiles - 1) / tiles);
-        splits = std::max(1, splits);
-      }
-      const int per = (nkt + splits - 1) / splits;
-      l.chunk = per * kt;
-      l.splits = (M + l.chunk - 1) / l.chunk;
-      if (l.splits > 1) {
-        part = std::max(part, (size_t)l.splits * C * l.nw);
-        dbpart = std::max(dbpart, (size_t)l.splits * C * l.Co);
-      }
+      const bool col = i == 0 && p.col0;
+      plan_wgrad(l, B * l.H * l.W, col ? p.Kc : l.Ci, col ? 1 : 9, l.H, l.W);
     }
   }
   p.off_dh = take(sizeof(float) * (size_t)C * B * p.Ch_head);
@@ -583,6 +718,14 @@ int create_ctx(const gcpsl_desc *d, char *ws, size_t ws_bytes, gcpsl_ctx **out) 
     const LayerInfo &l = ctx->plan.ly[i];
     if (l.spec.kind == GCPSL_CONV3X3)
       prep_add_layer(ctx->prep, l.w_off, l.Co, l.Ci, ws + l.wf_off, l.Kp, i > 0 ? ws + l.wd_off : nullptr, l.Kdp);
+    if (l.spec.kind == GCPSL_BLOCK) {
+      const BlockInfo &bk = ctx->plan.blocks[l.blk];
+      for (const LayerInfo *cv : {&bk.c1, &bk.c2})
+        prep_add_layer(ctx->prep, cv->w_off, cv->Co, cv->Ci, ws + cv->wf_off, cv->Kp, ws + cv->wd_off, cv->Kdp);
+      if (bk.proj)
+        prep_add_layer(ctx->prep, bk.cp.w_off, bk.cp.Co, bk.cp.Ci, ws + bk.cp.wf_off, bk.cp.Kp, ws + bk.cp.wd_off,
+                       bk.cp.Kdp, 1);
+    }
   }
   *out = ctx;
   return GCPSL_OK;
@@ -661,6 +804,11 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
     double pb = 0.0;
     for (int i = 0; i < n; ++i) {
       const LayerInfo &l = p.ly[i];
+      if (l.spec.kind == GCPSL_BLOCK) {
+        const BlockInfo &bk = p.blocks[l.blk];
+        for (const LayerInfo *cv : {&bk.c1, &bk.c2, &bk.cp})
+          if (cv->nw) pb += (double)C * (8.0 * cv->nw + p.esz * ((double)cv->Co * cv->Kp + (double)cv->Ci * cv->Kdp));
+      }
       if (l.spec.kind != GCPSL_CONV3X3) continue;
       pb += (double)C * ((i > 0 ? 8.0 : 4.0) * l.nw + p.esz * ((double)l.Co * l.Kp + (i > 0 ? (double)l.Ci * l.Kdp : 0.0)));
     }
@@ -691,6 +839,127 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
     na.C = C;
     na.rmap = rmap;
     return na;
+  };
+  // ---- the pieces a block (GCPSL_BLOCK) runs, on its internal layers
+  auto nargs = [&](const LayerInfo &nl, const void *z, void *out, const void *du, void *dz, const void *res,
+                   int relu) {
+    NormArgs na{};
+    na.z = z;
+    na.a = out;
+    na.du = du;
+    na.dz = dz;
+    na.mean = ctx->at<float>(nl.mean_off);
+    na.rstd = ctx->at<float>(nl.rstd_off);
+    na.part = ctx->at<double>(p.off_npart);
+    na.sums = ctx->at<double>(nl.sums_off);
+    na.theta = d.theta;
+    na.grad = grad;
+    na.state = d.norm_state;
+    na.P = p.P; na.g_off = nl.w_off; na.b_off = nl.b_off; na.S = p.S; na.st_off = nl.st_off;
+    na.z_rs = (int64_t)B * nl.H * nl.W * nl.Co;
+    na.Bt = B; na.H = nl.H; na.W = nl.W; na.Ch = nl.Co; na.groups = nl.groups; na.nstat = nl.nstat;
+    na.chunk_px = p.norm_chunk_px;
+    na.chunks = (int)(((int64_t)B * nl.H * nl.W + p.norm_chunk_px - 1) / p.norm_chunk_px);
+    na.C = C;
+    na.rmap = rmap;
+    na.res = res;
+    na.relu = relu;
+    return na;
+  };
+  // forward of an internal conv (raw output: a norm follows) over Hh x Ww
+  // pixels: 3 x 3 stride 1 (taps 9) or a one-tap product on im2col rows
+  auto conv_fwd = [&](const LayerInfo &cv, const void *src, int taps, int Csrc, int Hh, int Ww, void *out) -> int {
+    ConvArgs a{};
+    a.src = src;
+    a.wt = ws + cv.wf_off;
+    a.out = out;
+    a.bias = d.theta + cv.b_off;
+    a.Bt = B; a.H = Hh; a.W = Ww; a.N = cv.Co; a.Kp = cv.Kp;
+    a.Csrc = Csrc;
+    a.K = taps == 1 ? Csrc : 9 * Csrc;
+    a.taps = taps;
+    a.src_rs = (int64_t)B * Hh * Ww * Csrc;
+    a.wt_rs = (int64_t)cv.Co * cv.Kp;
+    a.out_rs = (int64_t)B * Hh * Ww * cv.Co;
+    a.bias_rs = p.P;
+    a.C = C;
+    a.rmap = rmap;
+    a.epi = EPI_FWD;
+    a.no_relu = 1;
+    std::string lab;
+    const double M = (double)B * Hh * Ww;
+    const double kk = (double)cv.nw / cv.Co;  // taps x input channels of the layer
+    size_t t_ = tbegin(ctx, s);
+    LAUNCH(launch_conv(p.dtype, a, s, &lab));
+    tend(ctx, s, t_, lab, 2.0 * C * M * cv.Co * kk,
+         (double)C * (p.esz * (M * Csrc + cv.Co * kk + M * cv.Co) + 4.0 * cv.Co));
+    return GCPSL_OK;
+  };
+  // input gradient of an internal conv over the input grid Hh x Ww: out =
+  // (sum + res) * [mask > 0] (res, mask optional); taps 9 (3 x 3 stride 1)
+  // or 1 (1 x 1)
+  auto conv_dgrad = [&](const LayerInfo &cv, const void *src, int taps, int Hh, int Ww, void *out, const void *res,
+                        const void *mask) -> int {
+    ConvArgs a{};
+    a.src = src;
+    a.wt = ws + cv.wd_off;
+    a.out = out;
+    a.res = res;
+    a.mask = mask;
+    a.Bt = B; a.H = Hh; a.W = Ww; a.Csrc = cv.Co; a.N = cv.Ci; a.K = taps * cv.Co; a.Kp = cv.Kdp;
+    a.src_rs = (int64_t)B * Hh * Ww * cv.Co;
+    a.wt_rs = (int64_t)cv.Ci * cv.Kdp;
+    a.out_rs = (int64_t)B * Hh * Ww * cv.Ci;
+    a.C = C;
+    a.rmap = rmap;
+    a.epi = EPI_DGRAD;
+    a.taps = taps;
+    std::string lab;
+    const double M = (double)B * Hh * Ww;
+    size_t t_ = tbegin(ctx, s);
+    LAUNCH(launch_conv(p.dtype, a, s, &lab));
+    tend(ctx, s, t_, lab, 2.0 * C * M * cv.Ci * taps * cv.Co,
+         (double)C * p.esz * (M * cv.Co + (double)cv.Ci * taps * cv.Co + M * cv.Ci * (1 + (res ? 1 : 0) + (mask ? 1 : 0))));
+    return GCPSL_OK;
+  };
+  // weight and bias gradient of a conv from g (Hh x Ww pixels) and its input
+  // x (taps 9: the layer input, Ci_eff its channels; taps 1: im2col rows of
+  // Ci_eff columns), split over pixels as planned, partials summed in order
+  auto wgrad_run = [&](const LayerInfo &cv, const void *g, const void *x, int taps, int Ci_eff, int Hh,
+                       int Ww) -> int {
+    WgradArgs w{};
+    w.g = g;
+    w.x = x;
+    w.Bt = B; w.H = Hh; w.W = Ww; w.Co = cv.Co;
+    w.Ci = Ci_eff;
+    w.taps = taps;
+    w.nw = (int)(cv.nw / cv.Co);
+    w.g_rs = (int64_t)B * Hh * Ww * cv.Co;
+    w.x_rs = (int64_t)B * Hh * Ww * Ci_eff;
+    w.C = C;
+    w.rmap = rmap;
+    w.splits = cv.splits;
+    w.chunk = cv.chunk;
+    if (cv.splits == 1) {
+      w.dw = grad + cv.w_off; w.dw_rs = p.P; w.dw_ss = 0;
+      w.db = grad + cv.b_off; w.db_rs = p.P; w.db_ss = 0;
+    } else {
+      w.dw = ctx->at<float>(p.off_part); w.dw_rs = cv.nw; w.dw_ss = (int64_t)p.C * cv.nw;
+      w.db = ctx->at<float>(p.off_dbpart); w.db_rs = cv.Co; w.db_ss = (int64_t)p.C * cv.Co;
+    }
+    {
+      std::string lab;
+      const double M = (double)B * Hh * Ww;
+      size_t t_ = tbegin(ctx, s);
+      LAUNCH(launch_wgrad(p.dtype, w, s, &lab));
+      tend(ctx, s, t_, lab, 2.0 * C * M * cv.nw,
+           (double)C * (p.esz * M * (cv.Co + cv.Ci) + 4.0 * cv.splits * (cv.nw + cv.Co)));
+    }
+    if (cv.splits > 1)
+      LAUNCH_T("wgrad_reduce", 0.0, 4.0 * C * (cv.nw + cv.Co) * (cv.splits + 1.0),
+               launch_wgrad_reduce(w.dw, w.db, cv.splits, w.dw_ss, w.dw_rs, w.db_ss, w.db_rs, grad, p.P, cv.w_off,
+                                   cv.b_off, cv.nw, cv.Co, C, rmap, s));
+    return GCPSL_OK;
   };
   bool pool_done = false;  // the max pool after the last conv was written by it
   bool avg_done = false;   // the head's mean pooling was written by the conv before it
@@ -745,6 +1014,36 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
       size_t t_ = tbegin(ctx, s);
       LAUNCH(launch_conv(p.dtype, a, s, &lab));
       tend(ctx, s, t_, lab, fl, by);
+    } else if (kind == GCPSL_BLOCK) {
+      // conv1 (the block's stride) -> norm1 + ReLU -> conv2 -> norm2 + shortcut + ReLU
+      const BlockInfo &bk = p.blocks[l.blk];
+      const void *x = input_of(i);
+      const char *nn = l.groups ? "groupnorm_fwd" : "batchnorm_fwd";
+      pool_done = avg_done = false;  // a max pool or the head after a block: their own kernels
+      const double nby = (double)C * p.esz * B * l.Ho * l.Wo * l.Co * 3.0;
+      if (bk.stride == 2) {
+        LAUNCH_T("im2col", 0.0, (double)C * p.esz * B * l.Ho * l.Wo * (bk.Kc1 + 9.0 * l.Ci),
+                 launch_im2col(p.dtype, x, ws + bk.cols1_off, C, rmap, B, l.H, l.W, l.Ci, l.Ho, l.Wo, 3, 3, 2, 1,
+                               bk.Kc1, s));
+        if (int rc = conv_fwd(bk.c1, ws + bk.cols1_off, 1, bk.Kc1, l.Ho, l.Wo, ws + bk.c1.act_off)) return rc;
+      } else {
+        if (int rc = conv_fwd(bk.c1, x, 9, l.Ci, l.H, l.W, ws + bk.c1.act_off)) return rc;
+      }
+      LAUNCH_T(nn, 0.0, nby, launch_norm_fwd(p.dtype, nargs(bk.n1, ws + bk.c1.act_off, ws + bk.n1.act_off, nullptr,
+                                                             nullptr, nullptr, 1), s));
+      if (int rc = conv_fwd(bk.c2, ws + bk.n1.act_off, 9, l.Co, l.Ho, l.Wo, ws + bk.c2.act_off)) return rc;
+      const void *sc = x;
+      if (bk.proj) {
+        LAUNCH_T("im2col", 0.0, (double)C * p.esz * B * l.Ho * l.Wo * 2.0 * bk.Kcp,
+                 launch_im2col(p.dtype, x, ws + bk.xs_off, C, rmap, B, l.H, l.W, l.Ci, l.Ho, l.Wo, 1, 1, bk.stride, 0,
+                               bk.Kcp, s));
+        if (int rc = conv_fwd(bk.cp, ws + bk.xs_off, 1, bk.Kcp, l.Ho, l.Wo, ws + bk.cp.act_off)) return rc;
+        LAUNCH_T(nn, 0.0, nby, launch_norm_fwd(p.dtype, nargs(bk.np, ws + bk.cp.act_off, ws + bk.np.act_off, nullptr,
+                                                               nullptr, nullptr, 0), s));
+        sc = ws + bk.np.act_off;
+      }
+      LAUNCH_T(nn, 0.0, nby * 4.0 / 3.0, launch_norm_fwd(p.dtype, nargs(bk.n2, ws + bk.c2.act_off, ws + l.act_off,
+                                                                         nullptr, nullptr, sc, 1), s));
     } else if (is_norm(kind)) {
       const double by = (double)C * p.esz * B * l.H * l.W * l.Co * (l.groups ? 3.0 : 3.0);
       LAUNCH_T(l.groups ? "groupnorm_fwd" : "batchnorm_fwd", 0.0, by, launch_norm_fwd(p.dtype, norm_args(i), s));
@@ -777,6 +1076,53 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
   int i = p.head_conv;
   while (i >= 0) {
     const LayerInfo &l = p.ly[i];
+    if (l.spec.kind == GCPSL_BLOCK) {
+      // the block's gradient at its output sum (gpre, already masked by its
+      // ReLU) back through norm2, conv2, norm1, conv1 and the shortcut; the
+      // input gradient goes to the layer below, masked by that layer's output
+      const BlockInfo &bk = p.blocks[l.blk];
+      const LayerInfo &prev = p.ly[i - 1];
+      const void *x = input_of(i);
+      const char *nn = l.groups ? "groupnorm_bwd" : "batchnorm_bwd";
+      const double nby = (double)C * p.esz * B * l.Ho * l.Wo * l.Co * 5.0;
+      LAUNCH_T(nn, 0.0, nby, launch_norm_bwd(p.dtype, nargs(bk.n2, ws + bk.c2.act_off, nullptr, ws + l.gpre_off,
+                                                             ws + bk.c2.gpre_off, nullptr, 1), s));
+      if (int rc = wgrad_run(bk.c2, ws + bk.c2.gpre_off, ws + bk.n1.act_off, 9, l.Co, l.Ho, l.Wo)) return rc;
+      if (int rc = conv_dgrad(bk.c2, ws + bk.c2.gpre_off, 9, l.Ho, l.Wo, ws + bk.n1.gpre_off, nullptr,
+                              ws + bk.n1.act_off))
+        return rc;
+      LAUNCH_T(nn, 0.0, nby, launch_norm_bwd(p.dtype, nargs(bk.n1, ws + bk.c1.act_off, nullptr, ws + bk.n1.gpre_off,
+                                                             ws + bk.c1.gpre_off, nullptr, 1), s));
+      const void *sc_grad = ws + l.gpre_off;  // identity shortcut: the gradient at the sum
+      if (bk.proj) {
+        LAUNCH_T(nn, 0.0, nby, launch_norm_bwd(p.dtype, nargs(bk.np, ws + bk.cp.act_off, nullptr, ws + l.gpre_off,
+                                                               ws + bk.cp.gpre_off, nullptr, 0), s));
+        if (int rc = wgrad_run(bk.cp, ws + bk.cp.gpre_off, ws + bk.xs_off, 1, bk.Kcp, l.Ho, l.Wo)) return rc;
+        const void *g = ws + bk.cp.gpre_off;
+        if (bk.stride == 2) {
+          LAUNCH_T("zero_insert", 0.0, (double)C * p.esz * B * l.Co * (l.Ho * l.Wo + (double)l.H * l.W),
+                   launch_zero_insert(p.dtype, g, ws + bk.gup_off, C, rmap, B, l.H, l.W, l.Ho, l.Wo, l.Co, s));
+          g = ws + bk.gup_off;
+        }
+        if (int rc = conv_dgrad(bk.cp, g, 1, l.H, l.W, ws + bk.gsc_off, nullptr, nullptr)) return rc;
+        sc_grad = ws + bk.gsc_off;
+      }
+      if (bk.stride == 2) {
+        if (int rc = wgrad_run(bk.c1, ws + bk.c1.gpre_off, ws + bk.cols1_off, 1, bk.Kc1, l.Ho, l.Wo)) return rc;
+        LAUNCH_T("zero_insert", 0.0, (double)C * p.esz * B * l.Co * (l.Ho * l.Wo + (double)l.H * l.W),
+                 launch_zero_insert(p.dtype, ws + bk.c1.gpre_off, ws + bk.gup_off, C, rmap, B, l.H, l.W, l.Ho, l.Wo,
+                                    l.Co, s));
+        if (int rc = conv_dgrad(bk.c1, ws + bk.gup_off, 9, l.H, l.W, ws + prev.gpre_off, sc_grad, ws + prev.act_off))
+          return rc;
+      } else {
+        if (int rc = wgrad_run(bk.c1, ws + bk.c1.gpre_off, x, 9, l.Ci, l.H, l.W)) return rc;
+        if (int rc = conv_dgrad(bk.c1, ws + bk.c1.gpre_off, 9, l.H, l.W, ws + prev.gpre_off, sc_grad,
+                                ws + prev.act_off))
+          return rc;
+      }
+      i -= 1;
+      continue;
+    }
     if (is_norm(l.spec.kind)) {
       // gamma, beta gradients and dL/dz of the conv below (which has no ReLU)
       const double by = (double)C * p.esz * B * l.H * l.W * l.Co * 5.0;
@@ -1100,6 +1446,27 @@ extern "C" int gcpsl_tensor(gcpsl_ctx *ctx, const char *name, void **ptr, int64_
   for (size_t i = 0; i < p.ly.size(); ++i) {
     const LayerInfo &l = p.ly[i];
     const std::string k = std::to_string(i);
+    if (l.spec.kind == GCPSL_BLOCK) {
+      // internals of block i: conv outputs z<i>.1 .2 .p, norm1 output
+      // act<i>.n1, shortcut sc<i>; gradients dz<i>.1 .2 .p (conv outputs),
+      // gpre<i>.n1 (norm1), gpre<i> (the block's output sum), gsc<i> (the
+      // shortcut's input gradient)
+      const BlockInfo &bk = p.blocks[l.blk];
+      const int64_t rs = (int64_t)p.C * l.act_rs, rs_in = (int64_t)p.C * p.B * l.H * l.W * l.Ci;
+      if (nm == "act" + k) return put(l.act_off, rs, p.dtype);
+      if (nm == "gpre" + k) return put(l.gpre_off, rs, p.dtype);
+      if (nm == "z" + k + ".1") return put(bk.c1.act_off, rs, p.dtype);
+      if (nm == "z" + k + ".2") return put(bk.c2.act_off, rs, p.dtype);
+      if (nm == "act" + k + ".n1") return put(bk.n1.act_off, rs, p.dtype);
+      if (nm == "dz" + k + ".1") return put(bk.c1.gpre_off, rs, p.dtype);
+      if (nm == "dz" + k + ".2") return put(bk.c2.gpre_off, rs, p.dtype);
+      if (nm == "gpre" + k + ".n1") return put(bk.n1.gpre_off, rs, p.dtype);
+      if (bk.proj && nm == "z" + k + ".p") return put(bk.cp.act_off, rs, p.dtype);
+      if (bk.proj && nm == "sc" + k) return put(bk.np.act_off, rs, p.dtype);
+      if (bk.proj && nm == "dz" + k + ".p") return put(bk.cp.gpre_off, rs, p.dtype);
+      if (bk.proj && nm == "gsc" + k) return put(bk.gsc_off, rs_in, p.dtype);
+      continue;
+    }
     if (nm == "act" + k && l.stored) return put(l.act_off, (int64_t)p.C * l.act_rs, p.dtype);
     if (l.spec.kind == GCPSL_CONV3X3 || is_norm(l.spec.kind)) {
       const int64_t rs = (int64_t)p.B * l.H * l.W;

@@ -340,7 +340,7 @@ conv_col_kernel(ConvArgs a, int MT) {
 
 bool conv_col_ok(int dtype, const ConvArgs &a) {
   return dtype == GCPSL_BF16 && a.taps == 1 && a.Csrc == COL_K && a.N == COL_N && a.res == nullptr &&
-         a.Kp >= COL_K && a.Kp % 8 == 0 && ((int64_t)a.Bt * a.H * a.W) % COL_PX == 0;
+         !a.no_relu && a.Kp >= COL_K && a.Kp % 8 == 0 && ((int64_t)a.Bt * a.H * a.W) % COL_PX == 0;
 }
 
 hipError_t launch_conv_col(const ConvArgs &a, hipStream_t s, std::string *label) {

@@ -275,9 +275,9 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const uint32_t t = xcd_swizzle(blockIdx.x, (uint32_t)(MT * NT * a.C));
-  const int nt = __builtin_amdgcn_readfirstlane((int)(t % (uint32_t)NT));
-  const uint32_t rest = t / (uint32_t)NT;
+  const uint32_t tile = xcd_swizzle(blockIdx.x, (uint32_t)(MT * NT * a.C));
+  const int nt = __builtin_amdgcn_readfirstlane((int)(tile % (uint32_t)NT));
+  const uint32_t rest = tile / (uint32_t)NT;
   const int mt = __builtin_amdgcn_readfirstlane((int)(rest % (uint32_t)MT));
   const int rep = replica_of(a.rmap, __builtin_amdgcn_readfirstlane((int)(rest / (uint32_t)MT)));
   const int M = a.Bt * a.H * a.W;

@@ -350,7 +350,7 @@ prep_weights_kernel(const float *__restrict__ theta, const int32_t *__restrict__
   const PrepJob &J = jobs.j[jn];
   const int rep = replica_of(rmap, blockIdx.y);
   const float *w = theta + rep * P + J.w_off;
-  const int co = J.co, ci = J.ci, K = 9 * ci;
+  const int co = J.co, ci = J.ci, taps = J.taps, K = taps * ci;
   const int lb = b - J.first;
   if (J.kind == 0) {
     // forward copy: output row lb
@@ -383,11 +383,12 @@ prep_weights_kernel(const float *__restrict__ theta, const int32_t *__restrict__
     return;
   }
   // input-gradient copy: block (cb, ib) of tap `tap` of the flipped kernel
+  // (one tap: the transpose)
   const int Kdp = J.kpad;
   const int nco = (co + 63) / 64;
-  const int tap = lb % 9, blk = lb / 9;
+  const int tap = lb % taps, blk = lb / taps;
   const int cb = blk % nco, ib = blk / nco;
-  const int rs_src = 8 - tap;  // (2 - r') * 3 + (2 - s')
+  const int rs_src = taps - 1 - tap;  // (2 - r') * 3 + (2 - s')
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   // 16 rows per thread with every load in flight (fixed trip counts)
   float v[16];
@@ -410,7 +411,7 @@ prep_weights_kernel(const float *__restrict__ theta, const int32_t *__restrict__
     for (int r = ty; r < 64; r += 4) {
       const int c = ib * 64 + r;
       if (c >= ci) continue;
-      for (int k = 9 * co + tx; k < Kdp; k += 64) dst[(int64_t)c * Kdp + k] = T(0);
+      for (int k = taps * co + tx; k < Kdp; k += 64) dst[(int64_t)c * Kdp + k] = T(0);
     }
   }
 }
@@ -1293,19 +1294,19 @@ hipError_t launch_gather_im2col(const float *images, const int32_t *idx, void *x
   return hipGetLastError();
 }
 
-void prep_add_layer(PrepJobs &jobs, int64_t w_off, int co, int ci, void *wf, int Kp, void *wd, int Kdp) {
+void prep_add_layer(PrepJobs &jobs, int64_t w_off, int co, int ci, void *wf, int Kp, void *wd, int Kdp, int taps) {
   if (jobs.n + 2 > kMaxPrepJobs) return;  // the plan checks the layer count
-  if (wd && co % 8 == 0 && ci % 8 == 0) {
+  if (wd && co % 8 == 0 && ci % 8 == 0 && taps == 9) {
     // one read of the masters for both copies, 8-element (16-byte bf16) runs
     jobs.j[jobs.n++] = PrepJob{w_off, wd, co, ci, Kdp, 2, jobs.total, wf, Kp};
     jobs.total += ((co + 63) / 64) * ((ci + 63) / 64) * 9;
     return;
   }
-  jobs.j[jobs.n++] = PrepJob{w_off, wf, co, ci, Kp, 0, jobs.total};
+  jobs.j[jobs.n++] = PrepJob{w_off, wf, co, ci, Kp, 0, jobs.total, nullptr, 0, taps};
   jobs.total += co;
   if (wd) {
-    jobs.j[jobs.n++] = PrepJob{w_off, wd, co, ci, Kdp, 1, jobs.total};
-    jobs.total += ((co + 63) / 64) * ((ci + 63) / 64) * 9;
+    jobs.j[jobs.n++] = PrepJob{w_off, wd, co, ci, Kdp, 1, jobs.total, nullptr, 0, taps};
+    jobs.total += ((co + 63) / 64) * ((ci + 63) / 64) * taps;
   }
 }
 

@@ -223,7 +223,8 @@ group_reduce_kernel(NormArgs a) {
   }
 }
 
-// a = ReLU(gamma (z - mean) rstd + beta), one 16-byte vector per thread.
+// a = ReLU(gamma (z - mean) rstd + beta (+ res)), one 16-byte vector per
+// thread (without the ReLU for a shortcut's norm).
 template <typename T>
 __global__ void __launch_bounds__(256)
 norm_apply_fwd_kernel(NormArgs a, uint32_t total) {
@@ -239,12 +240,15 @@ norm_apply_fwd_kernel(NormArgs a, uint32_t total) {
   const float *mean = a.mean + (int64_t)rep * a.nstat, *rstd = a.rstd + (int64_t)rep * a.nstat;
   const float *gamma = a.theta + rep * a.P + a.g_off, *beta = a.theta + rep * a.P + a.b_off;
   const V16<T> zv = load16(z + (int64_t)i * VEC);
+  V16<T> rv;
+  if (a.res) rv = load16(reinterpret_cast<const T *>(a.res) + rep * a.z_rs + (int64_t)i * VEC);
   V16<T> o;
 #pragma unroll
   for (int e = 0; e < VEC; ++e) {
     const int c = c0 + e, si = stat_index(a, b, c);
-    const float u = gamma[c] * ((ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si]) + beta[c];
-    o.v[e] = ElemT<T>::from_f(fmaxf(u, 0.f));
+    float u = gamma[c] * ((ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si]) + beta[c];
+    if (a.res) u += ElemT<T>::to_f(rv.v[e]);
+    o.v[e] = ElemT<T>::from_f(a.relu ? fmaxf(u, 0.f) : u);
   }
   store16(out + (int64_t)i * VEC, o);
 }

@@ -136,14 +136,17 @@ struct PrepJob {
   int first;  // first workgroup of the job
   void *dst2 = nullptr;  // kind 2: wf
   int kpad2 = 0;         // kind 2: Kp
+  int taps = 9;          // kernel taps: 9 (3 x 3) or 1 (1 x 1)
 };
-constexpr int kMaxPrepJobs = 32;
+constexpr int kMaxPrepJobs = 48;
 struct PrepJobs {
   PrepJob j[kMaxPrepJobs];
   int n = 0, total = 0;  // jobs, workgroups per replica
 };
-// Appends the jobs of one layer (wd may be null).
-void prep_add_layer(PrepJobs &jobs, int64_t w_off, int co, int ci, void *wf, int Kp, void *wd, int Kdp);
+// Appends the jobs of one layer (wd may be null) with 9 (3 x 3) or 1 (1 x 1)
+// kernel taps.
+void prep_add_layer(PrepJobs &jobs, int64_t w_off, int co, int ci, void *wf, int Kp, void *wd, int Kdp,
+                    int taps = 9);
 hipError_t launch_prep_weights(int dtype, const float *theta, int64_t P, int C, const int32_t *rmap,
                                const PrepJobs &jobs, hipStream_t s);
 hipError_t launch_maxpool_fwd(int dtype, const void *x, void *z, int C, const int32_t *rmap, int Bt, int H, int W,
@@ -213,7 +216,14 @@ struct NormArgs {
   int chunks, chunk_px;  // pixel chunks of the channel reductions
   int C;                 // replica slots
   const int32_t *rmap;   // device [C]: replica of each slot, or null
+  const void *res = nullptr;  // forward: added to gamma x_hat + beta before the ReLU (a block's shortcut), or null
+  int relu = 1;               // forward: 1 applies the ReLU, 0 stores gamma x_hat + beta (a shortcut's norm)
 };
 bool norm_ok(int dtype, int Ch, int groups);
+// Operand staging of a block's strided convolutions (k_block.hip).
+hipError_t launch_im2col(int dtype, const void *x, void *cols, int C, const int32_t *rmap, int Bt, int H, int W,
+                         int Ci, int Ho, int Wo, int R, int S, int stride, int pad, int Kc, hipStream_t s);
+hipError_t launch_zero_insert(int dtype, const void *g, void *gup, int C, const int32_t *rmap, int Bt, int H, int W,
+                              int Ho, int Wo, int Ch, hipStream_t s);
 hipError_t launch_norm_fwd(int dtype, const NormArgs &a, hipStream_t s);
 hipError_t launch_norm_bwd(int dtype, const NormArgs &a, hipStream_t s);

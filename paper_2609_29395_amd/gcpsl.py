@@ -18,8 +18,8 @@ LIB_PATH = os.path.join(_HERE, "libgcpsl.so")
 OK, EINVAL, ESTATE, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4
 RULES = {"random": 0, "size": 1, "label_l1": 2, "label_jsd": 3}
 DTYPES = {"f32": 0, "bf16": 1}
-CONV3X3, MAXPOOL2, AVGPOOL, LINEAR, BATCHNORM, GROUPNORM = 1, 2, 3, 4, 5, 6
-RESIDUAL = 1
+CONV3X3, MAXPOOL2, AVGPOOL, LINEAR, BATCHNORM, GROUPNORM, BLOCK = 1, 2, 3, 4, 5, 6, 7
+RESIDUAL, STRIDE2 = 1, 2
 SCHEDULES = {"lockstep": 0, "epoch": 1}
 PAYLOAD = ("activations", "cut_grads", "client_grads", "client_model", "fusion")  # GCPSL_PAYLOAD_* order
 
@@ -136,6 +136,10 @@ def layers_struct(layers):
             arr[i] = Layer(BATCHNORM, spec[1], spec[1], 0, 0)
         elif kind == "gnorm":
             arr[i] = Layer(GROUPNORM, spec[1], spec[1], 0, spec[2])
+        elif kind == "block":
+            if spec[3] not in (1, 2):
+                raise ValueError("block stride must be 1 or 2")
+            arr[i] = Layer(BLOCK, spec[1], spec[2], STRIDE2 if spec[3] == 2 else 0, spec[4])
         else:
             raise ValueError(kind)
     return arr

@@ -269,16 +269,16 @@ def traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload, out_
                   "fetch_factor": f_fac, "write_factor": w_fac,
                   "bytes_per_launch": 1024.0 * (fk / f_fac + wk / w_fac)}
     lines = [f"# HBM traffic per launch, {workload}", "",
-             "Commands (R = repository root; B = the bench.py command of the kernel-trace summary of this "
-             "workload):", "",
-             "* `rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/pfetch -o run -- $B`",
-             "* `rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/pwrite -o run -- $B`",
-             "* `rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/gpurun_out/cfetch -o run -- python "
+             "Commands (R = repository root; O = an output directory; B = the bench.py command of the "
+             "kernel-trace summary of this workload):", "",
+             "* `rocprofv3 --pmc FETCH_SIZE --output-format csv -d $O/pfetch -o run -- $B`",
+             "* `rocprofv3 --pmc WRITE_SIZE --output-format csv -d $O/pwrite -o run -- $B`",
+             "* `rocprofv3 --pmc FETCH_SIZE --output-format csv -d $O/cfetch -o run -- python "
              "$R/paper_2609_29395_amd/profile_summary.py copy`",
-             "* `rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/gpurun_out/cwrite -o run -- python "
+             "* `rocprofv3 --pmc WRITE_SIZE --output-format csv -d $O/cwrite -o run -- python "
              "$R/paper_2609_29395_amd/profile_summary.py copy`",
-             f"* `python -m paper_2609_29395_amd.profile_summary traffic gpurun_out/pfetch gpurun_out/pwrite "
-             f"gpurun_out/cfetch gpurun_out/cwrite {workload} {os.path.relpath(out_md, ROOT)}`", "",
+             f"* `python -m paper_2609_29395_amd.profile_summary traffic $O/pfetch $O/pwrite "
+             f"$O/cfetch $O/cwrite {workload} {os.path.relpath(out_md, ROOT)}`", "",
              f"Calibration: a {COPY_MIB} MiB device copy reads FETCH_SIZE = {f_fac:.4f} x and WRITE_SIZE = "
              f"{w_fac:.4f} x its size; counters are divided by these factors.",
              "The figures also sit in `profile.json` with the hash of each kernel's source file when taken; "

@@ -30,15 +30,64 @@ TOL = {"f32": 1e-4, "bf16": 2e-2}
 
 # Near-tie bounds, relative to the tensor's largest magnitude (ReLU: the
 # pre-activation is within this of zero) or (relative to the window maximum,
-# relative to the tensor's largest magnitude) for a max-pool window.  fp32:
-# a few ulps (2^-23) of accumulation-order difference against fp64.  bf16:
-# one ulp is 2^-8 = 3.9e-3 relative, and one-ulp differences upstream move the
-# values of deeper layers by several ulps of their scale; the bound is the
+# relative to the tensor's largest magnitude) for a max-pool window: the
 # per-element bar of the tensor comparison itself (tol of the largest
 # magnitude), so a decision counts as a near-tie exactly when the two
-# candidates are within what the activation comparison accepts.
-KINK = {"f32": 1e-5, "bf16": 2e-2}
-TIE = {"f32": (1e-5, 1e-6), "bf16": (2e-2, 2e-2)}
+# candidates are within what the activation comparison accepts.  (fp32
+# differences start at a few ulps, 2^-23, of accumulation order against fp64;
+# bf16 ones at one ulp, 2^-8; normalisations over few values and deeper layers
+# enlarge both.)
+KINK = {"f32": 1e-4, "bf16": 2e-2}
+TIE = {"f32": (1e-4, 1e-4), "bf16": (2e-2, 2e-2)}
+
+# bf16 networks of residual blocks (ten normalised 3x3 convs and more between
+# input and loss) sit at the edge of the bf16 bar on their own: noise of the
+# size of fp32 accumulation order before each bf16 rounding moves the oracle's
+# own first-round gradients by up to 3.5 % of a tensor's largest entry
+# (test_parity_bar pins this), so the GPU, which differs from the oracle by
+# exactly such noise, is held to 5e-2 there, for tensors and near-ties alike.
+# Over several rounds the per-tensor updates and momenta of such a network
+# drift further apart under that noise alone (up to 5e-2 and 9e-2 after two
+# to four rounds), so those comparisons take a bar calibrated by a twin
+# oracle run under the noise (noisy_rounding, twin_bar).
+BF16_DEEP = 5e-2
+
+# relative standard deviation of the calibration noise: 8 fp32 ulps
+NOISE_REL = 8 * 2.0 ** -24
+
+
+def deep_bf16(cfg):
+    return cfg["dtype"] == "bf16" and any(spec[0] == "block" for spec in cfg["layers"])
+
+
+def bar(cfg):
+    """The workload's comparison bar (TOL, KINK and TIE in one figure)."""
+    return BF16_DEEP if deep_bf16(cfg) else TOL[cfg["dtype"]]
+
+
+class noisy_rounding:
+    """Within the block, the oracle's bf16 rounding first multiplies each
+    value by (1 + NOISE_REL z), z standard normal (seeded): the oracle
+    then differs from itself the way the GPU differs from it, by
+    accumulation-order noise ahead of the same rounding points."""
+
+    def __init__(self, seed):
+        self.rng = np.random.default_rng(seed)
+
+    def __enter__(self):
+        import oracle.model as om
+        self.om, self.exact = om, om.round_bf16
+        rng, exact = self.rng, self.exact
+
+        def rnd(x):
+            x = np.asarray(x, dtype=np.float64)
+            return exact(x * (1.0 + rng.standard_normal(x.shape) * NOISE_REL))
+        om.round_bf16 = rnd
+        return self
+
+    def __exit__(self, *exc):
+        self.om.round_bf16 = self.exact
+        return False
 
 
 def close(a, b, tol):
@@ -74,6 +123,9 @@ def layer_shapes(cfg):
         kind = spec[0]
         if kind == "conv":
             c = spec[2]
+        elif kind == "block":
+            c = spec[2]
+            h, w = (h - 1) // spec[3] + 1, (w - 1) // spec[3] + 1
         elif kind == "maxpool":
             h, w = h // 2, w // 2
         elif kind == "avgpool":
@@ -101,8 +153,8 @@ class GpuChoices:
     docstring).  flips[(kind, layer)] counts the decisions that differed."""
 
     def __init__(self, ctx, cfg, n):
-        self.kink = KINK[cfg["dtype"]]
-        self.tie = TIE[cfg["dtype"]]
+        self.kink = bar(cfg)
+        self.tie = (bar(cfg), bar(cfg))
         shapes = layer_shapes(cfg)
         layers = cfg["layers"]
         self.relu, self.pool, self.flips = {}, {}, {}
@@ -110,12 +162,16 @@ class GpuChoices:
         for i, spec in enumerate(layers):
             kind = spec[0]
             normed = i + 1 < len(layers) and layers[i + 1][0] in ("bnorm", "gnorm")
-            if (kind == "conv" and not normed) or kind in ("bnorm", "gnorm"):
+            if (kind == "conv" and not normed) or kind in ("bnorm", "gnorm", "block"):
                 a = replica_tensor(ctx, f"act{i}", n, shapes[i])
                 if a is not None:
                     self.relu[i] = a > 0
                     if i + 1 < len(layers) and layers[i + 1][0] == "maxpool":
                         self.pool[i + 1] = np.argmax(pool_windows(a), axis=3)
+            if kind == "block":  # the block's inner ReLU, after its first norm
+                a1 = replica_tensor(ctx, f"act{i}.n1", n, shapes[i])
+                if a1 is not None:
+                    self.relu[(i, "n1")] = a1 > 0
 
     def __call__(self, kind, i, own, values):
         if kind == "relu":
@@ -164,30 +220,47 @@ class LazyChoices(dict):
         return self[n]
 
 
+def replayed(choices):
+    """The GPU's decisions of a round whose LazyChoices the exact oracle has
+    already validated, handed on unchecked (for the twin oracle of twin_bar,
+    whose noisy values sit further from the GPU's than the exact oracle's)."""
+    def one(c):
+        return lambda kind, i, own, values: c.relu[i] if kind == "relu" else c.pool[i]
+    return {n: one(c) for n, c in choices.items()}
+
+
 def vanishing_biases(cfg):
-    """Layers whose bias has an exactly zero loss gradient in exact
-    arithmetic: a conv followed by batch norm (the batch mean subtracts any
-    per-channel constant).  Both sides then hold rounding noise of their own
+    """{(layer, bias tag): weight tag} of the biases with an exactly zero
+    loss gradient in exact arithmetic: a conv followed by batch norm (the
+    batch mean subtracts any per-channel constant), in a block with batch
+    norm every conv's.  Both sides then hold rounding noise of their own
     precision in its gradient, momentum and update."""
     layers = cfg["layers"]
-    return {i for i, sp in enumerate(layers)
-            if sp[0] == "conv" and i + 1 < len(layers) and layers[i + 1][0] == "bnorm"}
+    out = {}
+    for i, sp in enumerate(layers):
+        if sp[0] == "conv" and i + 1 < len(layers) and layers[i + 1][0] == "bnorm":
+            out[(i, "b")] = "w"
+        if sp[0] == "block" and sp[4] == 0:
+            out.update({(i, "b1"): "w1", (i, "b2"): "w2", (i, "bp"): "wp"})
+    return out
 
 
-def master_ulp(theta):
-    """Spacing of the fp32 masters at theta: two updates of the same master
-    that round differently differ by at least this much."""
-    return np.spacing(np.abs(np.asarray(theta, dtype=np.float32))).astype(np.float64)
+def master_ulp(theta, roundings=1):
+    """Resolution of fp32 masters at theta after `roundings` stored updates
+    and fusions: each one rounds the master to fp32, so two runs whose
+    arithmetic differs in the last bits can end up to one spacing apart per
+    rounding."""
+    return roundings * np.spacing(np.abs(np.asarray(theta, dtype=np.float32))).astype(np.float64)
 
 
-def compare_params(got, want, cfg, tol, what, ulp=None):
-    """Every layer's weight and bias of a flat parameter-shaped vector on its
-    own, so an error in one layer cannot hide behind another's magnitude.  A
-    bias whose gradient vanishes exactly (vanishing_biases) is compared
-    elementwise on the scale of its layer's weight: max|a - b| <= tol
-    max|weight entries of b|.  ulp (for differences of fp32 masters, e.g. an
-    update theta_T - theta_0): per-element resolution of the stored values,
-    allowed on top of the max-element bound (a gradient that differs in its
+def param_distances(got, want, cfg, ulp=None):
+    """Per layer weight and bias of two flat parameter-shaped vectors:
+    yields (layer, tag, l2, mx), the relative L2 and max distances.  A bias
+    whose gradient vanishes exactly (vanishing_biases) has l2 = 0 and mx on
+    the scale of its layer's weight: max|a - b| / max|weight entries of b|.
+    ulp (for differences of fp32 masters, e.g. an update theta_T - theta_0):
+    per-element resolution of the stored values (master_ulp), subtracted
+    from each element's difference first (a gradient that differs in its
     last bits can round a master to the neighbouring fp32 value)."""
     from gcpsl_inputs import param_layout
     zero = vanishing_biases(cfg)
@@ -197,14 +270,34 @@ def compare_params(got, want, cfg, tol, what, ulp=None):
         a = np.asarray(got[off:off + size], dtype=np.float64)
         b = np.asarray(want[off:off + size], dtype=np.float64)
         res = 0.0 if ulp is None else ulp[off:off + size]
-        if tag == "w":
-            wmax[li] = np.abs(b).max()
-        if tag == "b" and li in zero:
-            err = (np.abs(a - b) - res).max()
-            assert err <= tol * wmax[li], (what, li, tag, "vanishing", err, wmax[li])
+        beyond = np.maximum(np.abs(a - b) - res, 0.0)
+        if tag.startswith("w"):
+            wmax[(li, tag)] = np.abs(b).max()
+        if (li, tag) in zero:
+            yield li, tag, 0.0, beyond.max() / (wmax[(li, zero[(li, tag)])] + 1e-30)
             continue
-        nb = np.linalg.norm(b)
-        err = np.linalg.norm(a - b)
-        worst = (np.abs(a - b) - res).max()
-        ok = err <= tol * nb + 1e-30 and worst <= tol * np.abs(b).max() + 1e-30
-        assert ok, (what, li, tag, err / (nb + 1e-30), worst / (np.abs(b).max() + 1e-30))
+        yield (li, tag, np.linalg.norm(beyond) / (np.linalg.norm(b) + 1e-30),
+               beyond.max() / (np.abs(b).max() + 1e-30))
+
+
+def compare_params(got, want, cfg, tol, what, ulp=None):
+    """Every layer's weight and bias on its own (param_distances), so an
+    error in one layer cannot hide behind another's magnitude: both relative
+    distances within tol."""
+    for li, tag, l2, mx in param_distances(got, want, cfg, ulp):
+        assert l2 <= tol and mx <= tol, (what, li, tag, l2, mx)
+
+
+def twin_bar(tol, cfg, pairs):
+    """The bar for a deep bf16 network's per-tensor comparisons after
+    several rounds: max(tol, twice the largest distance, over every tensor
+    of every (twin, want, ulp) pair, of a twin oracle run under
+    noisy_rounding from the exact oracle).  One figure for the whole run:
+    a single tensor's distance under the noise varies several-fold from
+    one noise sample to the next, the largest over all tensors by less than
+    2x (test_parity_bar)."""
+    worst = 0.0
+    for twin, want, ulp in pairs:
+        for _, _, l2, mx in param_distances(twin, want, cfg, ulp):
+            worst = max(worst, l2, mx)
+    return max(tol, 2.0 * worst)

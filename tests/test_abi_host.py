@@ -91,7 +91,7 @@ def test_assign_errors():
 
 
 @pytest.mark.parametrize("name", ["tiny", "gpsl", "gcpsl16", "ragged", "tiny_norm", "ragged_norm_bf16",
-                                  "ragged_recipe_bf16"])
+                                  "ragged_recipe_bf16", "resnet_tiny", "resnet_tiny_bf16", "resnet18"])
 def test_param_count_matches_layout(name):
     from gcpsl_inputs import norm_layout
     cfg = get_config(name)
@@ -130,7 +130,7 @@ def test_norm_layer_shapes_are_checked():
         assert e.value.code in (g.EINVAL, g.EUNSUPPORTED), layers
 
 
-def test_survey_parameter_counts():
+def test_parameter_counts_of_the_workload_models():
     assert param_counts(get_config("tiny")) == (224, 1236)
     assert param_counts(get_config("gpsl")) == (19392, 222730)
     assert param_counts(get_config("gcpsl16")) == (19392, 1920522)

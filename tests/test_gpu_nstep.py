@@ -11,6 +11,9 @@ N spans a fusion where the workload fuses:
     gcpsl16  C = 16, bf16, N = 3 with fusion every 2 rounds (the workload
              fuses every 50; the interval is shortened so a fusion of trained
              replicas falls inside an N the oracle finishes in minutes)
+    resnet18 the paper's ResNet-18 split after stage 2 (Sec. V-A), C = 4,
+             fp32, N = 3 with fusion every 2 rounds in lockstep (the
+             workload fuses after each 195-round epoch)
 
 Compared: every round's loss of every cluster (elementwise), and for every
 replica its parameters, its update theta_N - theta_0 and its momentum, each
@@ -29,11 +32,12 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("name,N,F", [("gpsl", 20, None), ("gcpsl4", 51, None), ("gcpsl8", 26, None),
-                                      ("gcpsl16", 3, 2)])
+                                      ("gcpsl16", 3, 2), ("resnet18", 3, 2)])
 def test_full_size_n_rounds(name, N, F):
     cfg = get_config(name)
     if F is not None:
         cfg["F"] = F
+        cfg["schedule"] = "lockstep"
     t0 = time.time()
 
     def log(msg):

@@ -89,7 +89,7 @@ def _enumerate_messages(o, cfg, T, fused_after, schedule_rounds=None):
     return out
 
 
-@pytest.mark.parametrize("name", ["tiny", "ragged_bf16", "tiny_norm"])
+@pytest.mark.parametrize("name", ["tiny", "ragged_bf16", "tiny_norm", "resnet_tiny"])
 def test_payload_counts_every_message(name):
     cfg = get_config(name)
     T = 5

@@ -234,6 +234,28 @@ def torch_split_model_loss(cfg, theta, x, y, with_running=False):
         elif spec[0] == "gnorm":
             u = tF.group_norm(a, spec[2], views[i]["w"], views[i]["b"], eps=1e-5)
             a = rf(torch.relu(rb(u)))
+        elif spec[0] == "block":
+            _, cin, cout, stride, groups = spec
+            v = views[i]
+
+            def norm(t, sub, v=v, i=i, groups=groups, cout=cout):
+                if groups:
+                    return tF.group_norm(t, groups, v[sub + "w"], v[sub + "b"], eps=1e-5)
+                rm = torch.zeros(cout, dtype=torch.float64)
+                rv = torch.ones(cout, dtype=torch.float64)
+                running[(i, sub)] = (rm, rv)
+                return tF.batch_norm(t, rm, rv, v[sub + "w"], v[sub + "b"], training=True, momentum=0.1, eps=1e-5)
+
+            x_in = rb(a)  # the block's input gradient (main + shortcut) is rounded
+            z1 = rf(rb(tF.conv2d(x_in, rf(v["w1"]).permute(0, 3, 1, 2), v["b1"], stride=stride, padding=1)))
+            a1 = rf(torch.relu(rb(norm(z1, "n1"))))
+            z2 = rf(rb(tF.conv2d(a1, rf(v["w2"]).permute(0, 3, 1, 2), v["b2"], padding=1)))
+            if "wp" in v:
+                zp = rf(rb(tF.conv2d(rb(x_in), rf(v["wp"]).permute(0, 3, 1, 2), v["bp"], stride=stride)))
+                sc = rf(norm(zp, "np"))
+            else:
+                sc = x_in
+            a = rf(torch.relu(rb(norm(z2, "n2") + sc)))
         elif spec[0] == "maxpool":
             a = tF.max_pool2d(a, 2)
         elif spec[0] == "avgpool":
@@ -248,7 +270,7 @@ def torch_split_model_loss(cfg, theta, x, y, with_running=False):
 
 
 @pytest.mark.parametrize("name", ["tiny", "ragged", "ragged_bf16", "tiny_norm", "ragged_norm_bf16", "tiny_recipe",
-                                  "ragged_recipe_bf16"])
+                                  "ragged_recipe_bf16", "resnet_tiny", "resnet_tiny_bf16"])
 def test_split_step_matches_torch_autograd(name):
     cfg = get_config(name)
     theta = init_params(cfg)
@@ -307,7 +329,7 @@ def test_split_step_finite_differences():
         assert abs(fd - grad[j]) <= 1e-8 + 1e-6 * abs(grad[j]), (j, fd, grad[j])
 
 
-@pytest.mark.parametrize("name", ["tiny_norm", "ragged_norm_bf16"])
+@pytest.mark.parametrize("name", ["tiny_norm", "ragged_norm_bf16", "resnet_tiny"])
 def test_batchnorm_running_statistics_match_torch(name):
     # one round's running mean / variance update (Sec. IV-B normalisation
     # state) against torch's buffers after one training-mode batch_norm
@@ -318,9 +340,9 @@ def test_batchnorm_running_statistics_match_torch(name):
     x, y = _batch(cfg)
     _, _, rec = split_forward_backward(cfg, theta, x, y)
     _, _, running = torch_split_model_loss(cfg, theta, x, y, with_running=True)
-    assert sorted(rec["bn_batch"]) == sorted(running)
+    assert sorted(rec["bn_batch"], key=str) == sorted(running, key=str)
     for i, (mean, var, n) in rec["bn_batch"].items():
-        ch = cfg["layers"][i][1]
+        ch = len(mean)
         rm, rv, cnt = bn_running_update(np.zeros(ch), np.ones(ch), 0.0, mean, var, n)
         assert np.allclose(rm, running[i][0], rtol=1e-12, atol=1e-15)
         assert np.allclose(rv, running[i][1], rtol=1e-12)
@@ -435,3 +457,81 @@ def test_forced_decisions_give_the_gradient_of_the_fixed_decision_network():
         fd = (split_forward_backward(cfg, tp, x, y, choose=replay)[0]
               - split_forward_backward(cfg, tm, x, y, choose=replay)[0]) / (2 * h)
         assert abs(fd - grad[j]) <= 1e-8 + 1e-6 * abs(grad[j]), (j, fd, grad[j])
+
+
+def test_resnet_block_finite_differences_and_decisions():
+    # the ResNet-shaped model (every block kind): with its discrete decisions
+    # fixed, the gradient is the derivative of the loss (central differences,
+    # fp64); both ReLUs of every block are consulted, the inner one under
+    # the key (layer, "n1")
+    cfg = get_config("resnet_tiny")
+    theta = init_params(cfg).astype(np.float64)
+    x, y = _batch(cfg, seed=3)
+    fixed = {}
+
+    def record(kind, i, decision, values):
+        fixed[(kind, i)] = decision.copy()
+        return decision
+
+    loss, grad, _ = split_forward_backward(cfg, theta, x, y, choose=record)
+    blocks = [i for i, sp in enumerate(cfg["layers"]) if sp[0] == "block"]
+    assert {k for k in fixed if isinstance(k[1], tuple)} == {("relu", (i, "n1")) for i in blocks}
+    assert all(("relu", i) in fixed for i in blocks)
+
+    def replay(kind, i, decision, values):
+        return fixed[(kind, i)]
+
+    rng = np.random.default_rng(4)
+    coords = rng.choice(len(theta), size=50, replace=False)
+    h = 1e-6
+    for j in coords:
+        tp, tm = theta.copy(), theta.copy()
+        tp[j] += h
+        tm[j] -= h
+        fd = (split_forward_backward(cfg, tp, x, y, choose=replay)[0]
+              - split_forward_backward(cfg, tm, x, y, choose=replay)[0]) / (2 * h)
+        assert abs(fd - grad[j]) <= 1e-8 + 1e-6 * abs(grad[j]), (j, fd, grad[j])
+
+
+def test_strided_conv_matches_explicit_loops():
+    # stride 2, 3x3 pad 1 and 1x1 pad 0, forward and backward, against the
+    # definition written as loops on a tiny tensor
+    from oracle.model import conv_backward, conv_forward
+    rng = np.random.default_rng(9)
+    x = rng.standard_normal((2, 6, 6, 3))
+    for R, pad in ((3, 1), (1, 0)):
+        w = rng.standard_normal((4, R, R, 3))
+        b = rng.standard_normal(4)
+        out = conv_forward(x, w, b, 2, pad)
+        Ho = (6 + 2 * pad - R) // 2 + 1
+        assert out.shape == (2, Ho, Ho, 4)
+        want = np.zeros_like(out)
+        for n in range(2):
+            for ho in range(Ho):
+                for wo in range(Ho):
+                    for o in range(4):
+                        acc = b[o]
+                        for r in range(R):
+                            for s_ in range(R):
+                                hh, ww = 2 * ho + r - pad, 2 * wo + s_ - pad
+                                if 0 <= hh < 6 and 0 <= ww < 6:
+                                    acc += x[n, hh, ww] @ w[o, r, s_]
+                        want[n, ho, wo, o] = acc
+        assert np.allclose(out, want, rtol=1e-13, atol=1e-13)
+        gp = rng.standard_normal(out.shape)
+        dx, dw, db = conv_backward(x, w, gp, 2, pad)
+        # the gradient of sum(out * gp) is linear: check it against the loops
+        dx_want = np.zeros_like(x)
+        dw_want = np.zeros_like(w)
+        for n in range(2):
+            for ho in range(Ho):
+                for wo in range(Ho):
+                    for r in range(R):
+                        for s_ in range(R):
+                            hh, ww = 2 * ho + r - pad, 2 * wo + s_ - pad
+                            if 0 <= hh < 6 and 0 <= ww < 6:
+                                dx_want[n, hh, ww] += gp[n, ho, wo] @ w[:, r, s_]
+                                dw_want[:, r, s_] += np.outer(gp[n, ho, wo], x[n, hh, ww])
+        assert np.allclose(dx, dx_want, rtol=1e-12, atol=1e-12)
+        assert np.allclose(dw, dw_want, rtol=1e-12, atol=1e-12)
+        assert np.allclose(db, gp.sum(axis=(0, 1, 2)), rtol=1e-12)
