@@ -8,9 +8,12 @@ on inputs already resident in HBM.  The default workload is the 16-cluster
 one: K=256 clients, C=16 label-L1 clusters, B=128 per cluster (2048 examples
 per step), bf16 activations/weights with fp32 masters, wide residual server,
 fusion every 50 rounds, synthetic CIFAR-10-shaped data.  The 8-cluster (bf16)
-and 4-cluster (fp32) workloads are measured the same way as sub-results.
+and 4-cluster (fp32) workloads and the paper's ResNet-18 model (4 clusters,
+fp32, epoch-barrier schedule) are measured the same way as sub-results.
 
-Prints one JSON line.  `value` is examples/s summed over the C clusters,
+Prints one JSON line.  `value` is examples/s summed over the C clusters
+(the examples the clusters that take a round process: under the epoch
+schedule a cluster whose rounds are done waits at the barrier),
 wall clock over exactly --steps rounds bracketed by device synchronisation;
 the window is placed so that it ends right after a fusion, so it always holds
 at least its share of fusions (exactly its share when F divides --steps).
@@ -45,6 +48,10 @@ DESCRIPTIONS = {
     "gcpsl4": "GCPSL C=4 random clusters of K=256 clients, B=64/cluster, fp32, "
               "split CNN 3-32-64|64-128-128, fusion every 50 rounds, synthetic 32x32x3 10-class",
     "gpsl": "GPSL C=1, K=256 clients, B=64, fp32, split CNN 3-32-64|64-128-128, synthetic 32x32x3",
+    "resnet18": "GCPSL C=4 label-aware (Eq. 4) clusters of K=256 clients, B=64/cluster, fp32, ResNet-18 split "
+                "after stage 2 (group norm client / batch norm server), Nesterov SGD with weight decay and "
+                "label smoothing, epoch-barrier schedule with fusion after every epoch, synthetic 32x32x3 "
+                "10-class",
 }
 
 
@@ -187,12 +194,19 @@ def measure(name, steps, warmup, timing_steps, cpu_seconds, with_cpu=True, with_
     from paper_2609_29395_amd import driver
 
     cfg = get_config(name)
-    C, B, F = cfg["C"], cfg["B"], cfg["F"]
+    C, B = cfg["C"], cfg["B"]
+    # the participation table records steps below max_steps; the epoch
+    # schedule's fusion interval (slots per epoch) is only known once the
+    # context has the assignment, so the table is sized with room for it
+    extra = 2 * args.control_steps if with_extras else 0
+    ctx, assignment = driver.setup(cfg, max_steps=warmup + steps + timing_steps + extra + 4096)
+    if ctx.schedule == "epoch":
+        rounds, F = ctx.epoch_rounds()
+    else:
+        rounds, F = None, cfg["F"]
     x0 = fusion_aligned_start(warmup, steps, F)
-    total = x0 + steps + timing_steps + (2 * args.control_steps if with_extras else 0)
-    print(f"bench: workload {name} C={C} B={B} F={F} warmup={warmup} steps={steps} (timed rounds "
-          f"[{x0}, {x0 + steps}))", file=sys.stderr, flush=True)
-    ctx, assignment = driver.setup(cfg, max_steps=total)
+    print(f"bench: workload {name} C={C} B={B} F={F} ({ctx.schedule}) warmup={warmup} steps={steps} (timed "
+          f"rounds [{x0}, {x0 + steps}))", file=sys.stderr, flush=True)
     driver.train(ctx, warmup, start=x0 - warmup)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -200,8 +214,13 @@ def measure(name, steps, warmup, timing_steps, cpu_seconds, with_cpu=True, with_
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     fusions = (x0 + steps) // F - x0 // F if F else 0
-    value = C * B * steps / dt
-    print(f"bench: timed {steps} steps ({fusions} fusions) in {dt:.3f} s", file=sys.stderr, flush=True)
+    if rounds is None:
+        examples = C * B * steps
+    else:  # a cluster whose rounds of the epoch are done waits at the barrier
+        examples = B * sum(int((rounds > s % F).sum()) for s in range(x0, x0 + steps))
+    value = examples / dt
+    print(f"bench: timed {steps} steps ({fusions} fusions, {examples} examples) in {dt:.3f} s", file=sys.stderr,
+          flush=True)
 
     # per-kernel event timing pass, right after the timed window
     ctx.timing(True)
@@ -260,9 +279,11 @@ def measure(name, steps, warmup, timing_steps, cpu_seconds, with_cpu=True, with_
               f"{v['bytes'] / (v['ms'] * 1e-3) / 1e9:8.1f} GB/s {rate}", file=sys.stderr)
     out = {
         "value": round(value, 1), "ms_per_step": round(dt * 1e3 / steps, 4), "fusions_in_window": fusions,
+        "examples_in_window": examples,
         "dtype": cfg["dtype"],
         "config": {"workload": name, "description": DESCRIPTIONS[name], "clients": cfg["K"], "clusters": C,
-                   "batch_per_cluster": B, "global_batch": C * B, "fusion_every": F, "rule": cfg["rule"],
+                   "batch_per_cluster": B, "global_batch": C * B, "fusion_every": F, "schedule": ctx.schedule,
+                   "rule": cfg["rule"],
                    "parallelism": "C replicas batched in every kernel, 1 GPU"},
         "mfma_util_pct": mfma_util,
         "conv_flops_frac_pct": round(100.0 * conv_tf / peak_tf, 2),
@@ -289,7 +310,7 @@ def measure(name, steps, warmup, timing_steps, cpu_seconds, with_cpu=True, with_
     return out
 
 
-SUB_RESULTS = ("gcpsl8", "gcpsl4")
+SUB_RESULTS = ("gcpsl8", "gcpsl4", "resnet18")
 
 
 def main():
@@ -307,7 +328,7 @@ def main():
     ap.add_argument("--no-hbm-probes", action="store_true",
                     help="skip the large fusion and windowed gather measurements")
     ap.add_argument("--no-sub-results", action="store_true",
-                    help="measure only --workload (not also the 8- and 4-cluster workloads)")
+                    help="measure only --workload (not also the 8- and 4-cluster and ResNet-18 workloads)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
