@@ -116,9 +116,11 @@ CONFIGS = {
     # the paper's label-aware rule (Eq. 4), B = 64 per cluster, its training
     # recipe (SGD lr 0.01, momentum 0.9, Nesterov, weight decay 5e-4, label
     # smoothing 0.1) and fusion after every epoch (the epoch-barrier
-    # schedule).  Precision fp32 (the paper states none).
+    # schedule).  Precision fp32 (the paper states none).  45,000 training
+    # examples: the real-execution study holds 5,000 of CIFAR-10's 50,000 out
+    # for validation before partitioning (Sec. V-B).
     "resnet18": dict(
-        K=256, C=4, B=64, alpha=0.3, rule="label_jsd", **_CIFAR_DATA,
+        K=256, C=4, B=64, alpha=0.3, rule="label_jsd", **dict(_CIFAR_DATA, N_ex=45000),
         layers=_resnet((64, 128, 256, 512), 32)[0], cut=_resnet((64, 128, 256, 512), 32)[1],
         dtype="f32", lr=0.01, momentum=0.9, nesterov=True, weight_decay=5e-4, label_smoothing=0.1,
         F=0, T=3, seed=0, schedule="epoch"),

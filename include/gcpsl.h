@@ -297,16 +297,16 @@ int gcpsl_step_replica(gcpsl_ctx *ctx, int64_t step, int32_t replica, float *los
 int gcpsl_epoch_rounds(gcpsl_ctx *ctx, int64_t *rounds, int64_t *slots);
 
 /*
- * Fusion and broadcast, Eq. 5 (Sec. IV-D): theta_bar = sum_n (n_n / W)
+ * Fusion and broadcast, Eq. 5 (Sec. IV-C): theta_bar = sum_n (n_n / W)
  * theta_n over both segments, accumulated in fp64 in cluster order, divided
  * once by W = sum_n n_n and rounded once to fp32, then written to every
  * replica.  The server normalisation state (norm_state) is fused the same way
- * (Sec. IV-B, IV-D).  Momentum is not touched (optimizer state stays local).
+ * (Sec. IV-B, IV-C).  Momentum is not touched (optimizer state stays local).
  */
 int gcpsl_fuse(gcpsl_ctx *ctx, void *stream);
 
 /*
- * The fusion of gcpsl_fuse in two halves (Eq. 5, Sec. IV-D), for a run whose
+ * The fusion of gcpsl_fuse in two halves (Eq. 5, Sec. IV-C), for a run whose
  * replicas are spread over several devices: every device reduces its own
  * replicas, the caller sums the devices' partials (e.g. an all-reduce), and
  * every device divides by the global W and broadcasts to its replicas.
@@ -327,19 +327,18 @@ int gcpsl_fuse_partial(gcpsl_ctx *ctx, double *partial, void *stream);
 int gcpsl_fuse_finalise(gcpsl_ctx *ctx, const double *partial, int64_t W, void *stream);
 
 /*
- * The same sample-weighted fusion (Eq. 5, Sec. IV-D) on caller-owned
+ * The same sample-weighted fusion (Eq. 5, Sec. IV-C) on caller-owned
  * replicas, without a context: theta_bar[p] = (sum_n weights[n] theta[n][p])
  * / W, W = sum_n weights[n], accumulated in fp64 in replica order, rounded
  * once to fp32 and written to all C rows.
  * theta: device [C][P] fp32, row n = replica n, 4-byte aligned, in/out,
  * caller-owned; weights: host [C] int64 in [0, 2^29] with W > 0 (e.g. the
  * replicas' example counts n_n), read before the call returns; 1 <= C <= 64
- * (the weights travel in the kernel arguments); P >= 1.  Each product and,
- * when W <= 2^29, each partial sum is exact in fp64, so identical replicas
- * come back unchanged.  Asynchronous on stream; EINVAL on a bad argument,
- * EHIP on a failed launch.  This is the operation a sharded run applies to
- * the all-reduced partial sums, and the form a benchmark times at arbitrary
- * sizes.
+ * (the weights travel in the kernel arguments); P >= 1.  Each product is
+ * exact in fp64, and for identical replicas so is each partial sum (W <=
+ * 2^29), so identical replicas come back unchanged.  Asynchronous on stream;
+ * EINVAL on a bad argument, EHIP on a failed launch.  The form a benchmark
+ * times at arbitrary sizes.
  */
 int gcpsl_fuse_replicas(float *theta, int32_t C, int64_t P, const int64_t *weights, void *stream);
 

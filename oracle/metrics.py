@@ -26,7 +26,7 @@ one endpoint to another, in the precision the workload stores it) is:
     "client_model" the averaged client segment to every client replica of
                    the cluster, P_c fp32 entries each, including replicas whose
                    owners supplied no data (Sec. IV-B);
-  per fusion (Sec. IV-D, Eq. 5):
+  per fusion (Sec. IV-C, Eq. 5):
     "fusion"       every replica's parameters and server normalisation state
                    to the fusion point and the fused state back, 2 (P + S)
                    fp32 entries per replica.

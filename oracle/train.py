@@ -3,8 +3,8 @@
 Alg. 2: build the fixed clusters (Alg. 1), start every split-model replica
 from the same parameters, run the clusters' GPSL rounds side by side, and at
 the synchronisation points fuse client and server parameters with the weights
-q_n = |D_{C_n}| / |D| and give the fused model to every replica (Sec. IV-D).
-Optimiser state stays local to each cluster and is never fused (Sec. IV-D).
+q_n = |D_{C_n}| / |D| and give the fused model to every replica (Sec. IV-C).
+Optimiser state stays local to each cluster and is never fused (Sec. IV-C).
 
 Readings:
   * Parameters and momentum are held as fp32 values (the workloads keep fp32
@@ -27,7 +27,7 @@ Readings:
   * The server normalisation state (each BatchNorm layer's running mean,
     running variance and batch counter, Sec. IV-B) is updated by every round
     of its replica and fused with the same weights as the parameters
-    (Sec. IV-D), in fp64 and rounded once to fp32 like them.
+    (Sec. IV-C), in fp64 and rounded once to fp32 like them.
 
 Epoch-barrier schedule (Sec. III-A, Sec. IV-D "Schedule and Cost", Eq. 6):
 cluster n takes r_n = floor(n_n / B) local rounds per epoch (the sampler's

@@ -1267,7 +1267,7 @@ extern "C" int gcpsl_fuse(gcpsl_ctx *ctx, void *stream) {
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   LAUNCH_T("fuse", 2.0 * p.C * p.P, 8.0 * p.C * p.P,
            launch_fuse(ctx->desc.theta, ctx->at<double>(p.off_fw), wh.data(), W, p.C, p.P, s));
-  // the server normalisation state, with the same weights (Sec. IV-D)
+  // the server normalisation state, with the same weights (Sec. IV-C)
   if (p.S > 0)
     LAUNCH_T("fuse", 2.0 * p.C * p.S, 8.0 * p.C * p.S,
              launch_fuse(ctx->desc.norm_state, ctx->at<double>(p.off_fw), wh.data(), W, p.C, p.S, s));

@@ -153,7 +153,7 @@ def test_tiny_workload_learns():
 
 
 def test_normalisation_state_is_fused_with_the_parameter_weights():
-    # Sec. IV-B / IV-D: each server replica's BatchNorm running mean, variance
+    # Sec. IV-B / IV-C: each server replica's BatchNorm running mean, variance
     # and counter evolve locally and are fused with the weights n_n / W
     cfg = get_config("tiny_norm", F=0)
     o = GCPSLOracle(cfg)
