@@ -283,8 +283,13 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   p.off_idx = take(sizeof(int32_t) * (size_t)p.max_window * C * B);
   p.off_y = take(sizeof(int32_t) * (size_t)p.max_window * C * B);
   {
+    // a first layer with few channels runs on im2col rows that the gather
+    // writes (col0), unless its kernels build those rows from the gathered
+    // images themselves (3 -> 32 channels, bf16, 32-pixel-wide images)
     const int vec = 16 / p.esz;
-    p.col0 = p.Cin % vec != 0;
+    const LayerInfo &l0 = p.ly[0];
+    const bool img3 = !(l0.spec.flags & GCPSL_RESIDUAL) && conv_im3_ok(p.dtype, p.Cin, l0.Co, p.H, p.W);
+    p.col0 = p.Cin % vec != 0 && !img3;
     p.Kc = p.col0 ? round_up(9 * p.Cin, vec) : p.Cin;
   }
   p.x_rs = (int64_t)C * B * p.H * p.W * p.Kc;
@@ -298,7 +303,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
     int bm, bn;
     const int nwc = taps == 1 ? Ci_eff : 9 * Ci_eff;
     int splits;
-    if (wgrad_lds_ok(p.dtype, l.Co, Ci_eff) || wgrad_col_ok(p.dtype, l.Co, Ci_eff, taps)) {
+    if (wgrad_lds_ok(p.dtype, l.Co, Ci_eff) || wgrad_col_ok(p.dtype, l.Co, Ci_eff, taps) ||
+        (taps == 9 && conv_im3_ok(p.dtype, Ci_eff, l.Co, Hh, Ww))) {
       // pick the split count that minimises (rounds of 256 x per_cu
       // workgroups) x (k tiles per workgroup + the cost of writing and
       // re-reading a partial tile, about 16 k tiles)

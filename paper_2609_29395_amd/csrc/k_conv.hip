@@ -695,6 +695,8 @@ void wgrad_tile(int dtype, int Co, int ncols, int *bm, int *bn) {
 }
 
 hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s, std::string *label) {
+  if (a.taps == 9 && a.epi == EPI_FWD && a.res == nullptr && conv_im3_ok(dtype, a.Csrc, a.N, a.H, a.W))
+    return launch_conv_col(a, s, label);
   if (conv_img_ok(dtype, a)) return launch_conv_img(a, s, label);
   if (a.epi == EPI_FWD && conv_col_ok(dtype, a)) return launch_conv_col(a, s, label);
   if (conv_lds_ok(dtype, a)) return launch_conv_lds(a, s, label);
@@ -704,7 +706,9 @@ hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s, std::string 
 }
 
 hipError_t launch_wgrad(int dtype, const WgradArgs &a, hipStream_t s, std::string *label) {
-  if (wgrad_col_ok(dtype, a.Co, a.Ci, a.taps) && a.chunk % 128 == 0) return launch_wgrad_col(a, s, label);
+  if ((wgrad_col_ok(dtype, a.Co, a.Ci, a.taps) ||
+       (a.taps == 9 && conv_im3_ok(dtype, a.Ci, a.Co, a.H, a.W))) && a.chunk % 128 == 0)
+    return launch_wgrad_col(a, s, label);
   if (wgrad_lds_ok(dtype, a.Co, a.Ci) && a.chunk % 64 == 0) return launch_wgrad_lds(a, s, label);
   // vector path: whole 16-byte channel vectors and pixel blocks within one
   // image row (im2col rows need no image-row structure)

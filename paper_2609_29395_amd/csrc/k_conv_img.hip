@@ -261,17 +261,30 @@ conv_img_kernel(ConvArgs a, int MT) {
   }
 }
 
-// The image layer on its im2col rows (taps == 1): out[p][n] = act(bias[n] +
-// sum_k A[p][k] W[n][k]) with 32 columns per row (9 x 3 taps and channels,
-// zero-padded) and 32 output channels.  A plain stream: each wave reads four
-// groups of 16 pixel rows (1 KB each, one 16-byte piece per lane), multiplies
-// them by the weight fragments it keeps in registers (two MFMAs per group) and
-// regroups the results through LDS into whole 64-byte output rows.
+// The image layer: out[p][n] = act(bias[n] + sum_k A[p][k] W[n][k]) with k =
+// (r, s, c) over the 3 x 3 taps of the 3 image channels (27 columns,
+// zero-padded to 32) and 32 output channels.  A plain stream: each wave takes
+// four groups of 16 pixels, multiplies their rows by the weight fragments it
+// keeps in registers (two MFMAs per group) and regroups the results through
+// LDS into whole 64-byte output rows.  The rows come either from the
+// gathered im2col rows (IMG3 false: one 16-byte piece per lane), or (IMG3)
+// from the bf16 NHWC images themselves: a workgroup's 256 pixels are 8 rows
+// of one 32-pixel-wide image, whose 10 input rows (one above, one below)
+// are staged once in LDS with a zero border, and lane (li, lg) collects its
+// 8 values k = 8 lg .. 8 lg + 7 of pixel li from there.
 constexpr int COL_K = 32, COL_N = 32, COL_PX = 256;  // k, n, pixels per workgroup
+namespace im3 {
+constexpr int CIN = 3, W = 32, ROWS = COL_PX / W;   // image channels, width, output rows per workgroup
+constexpr int RS = (W + 2) * CIN;                   // bf16 values per staged row (zero pixel either side)
+constexpr int LROWS = ROWS + 2;                     // staged rows: one above and one below
+constexpr int VROW = W * CIN * 2 / 16;              // 16-byte vectors per image row (12)
+}  // namespace im3
 
+template <bool IMG3>
 __global__ void __launch_bounds__(256)
 conv_col_kernel(ConvArgs a, int MT) {
   __shared__ __attribute__((aligned(16))) char stg_all[4 * 64 * COL_N * 2];
+  __shared__ __attribute__((aligned(16))) uint16_t img[IMG3 ? im3::LROWS * im3::RS : 2];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t t = xcd_swizzle(blockIdx.x, (uint32_t)(MT * a.C));
   const int mt = __builtin_amdgcn_readfirstlane((int)(t % (uint32_t)MT));
@@ -283,10 +296,49 @@ conv_col_kernel(ConvArgs a, int MT) {
   const bf16_t *wt = reinterpret_cast<const bf16_t *>(a.wt) + rep * a.wt_rs;
   // pixel rows (B operand: lane (li, lg) = pixel li, k 8 lg .. 8 lg + 7)
   u32x4 x[4];
+  if constexpr (IMG3) {
+    // staged rows h0 - 1 .. h0 + 8 of the tile's image, pixels -1 .. 32
+    const int tpi = a.H / im3::ROWS;  // tiles per image
+    const int b = mt / tpi, h0 = (mt - b * tpi) * im3::ROWS;
+    for (int e = threadIdx.x; e < im3::LROWS * im3::RS / 2; e += 256) reinterpret_cast<uint32_t *>(img)[e] = 0u;
+    __syncthreads();
+    if (threadIdx.x < im3::LROWS * im3::VROW) {
+      const int lr = threadIdx.x / im3::VROW, v = threadIdx.x - lr * im3::VROW, h = h0 - 1 + lr;
+      if ((unsigned)h < (unsigned)a.H) {
+        const u32x4 q = *reinterpret_cast<const u32x4 *>(src + ((int64_t)b * a.H + h) * im3::W * im3::CIN + 8 * v);
+        uint16_t *d = img + lr * im3::RS + im3::CIN + 8 * v;
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    const int p = p0 + g * 16 + li;
-    x[g] = p < M ? *reinterpret_cast<const u32x4 *>(src + (int64_t)p * COL_K + 8 * lg) : u32x4{0u, 0u, 0u, 0u};
+        for (int e = 0; e < 4; ++e) {
+          d[2 * e] = (uint16_t)(q[e] & 0xffffu);
+          d[2 * e + 1] = (uint16_t)(q[e] >> 16);
+        }
+      }
+    }
+    __syncthreads();
+    // k = 9 r + 3 s + c sits at (row + r) * RS + (pixel + s) * 3 + c =
+    // base + k + (RS - 9) r; k >= 27 is padding
+    int off[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int k = 8 * lg + e;
+      off[e] = k < 27 ? k + (im3::RS - 9) * (k / 9) : -1;
+    }
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int pl = wave * 64 + g * 16 + li;  // pixel of the tile: row pl / 32, column pl % 32
+      const int base = (pl / im3::W) * im3::RS + (pl % im3::W) * im3::CIN;
+      uint32_t h16[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) h16[e] = off[e] >= 0 ? (uint32_t)img[base + off[e]] : 0u;
+      x[g] = u32x4{h16[0] | (h16[1] << 16), h16[2] | (h16[3] << 16), h16[4] | (h16[5] << 16),
+                   h16[6] | (h16[7] << 16)};
+    }
+  } else {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int p = p0 + g * 16 + li;
+      x[g] = p < M ? *reinterpret_cast<const u32x4 *>(src + (int64_t)p * COL_K + 8 * lg) : u32x4{0u, 0u, 0u, 0u};
+    }
   }
   // weights (A operand: lane (li, lg) = output channel tn*16 + li, k 8 lg ..)
   u32x4 w[2];
@@ -343,11 +395,21 @@ bool conv_col_ok(int dtype, const ConvArgs &a) {
          !a.no_relu && a.Kp >= COL_K && a.Kp % 8 == 0 && ((int64_t)a.Bt * a.H * a.W) % COL_PX == 0;
 }
 
+bool conv_im3_ok(int dtype, int Ci, int Co, int H, int W) {
+  return dtype == GCPSL_BF16 && Ci == im3::CIN && Co == COL_N && W == im3::W && H % im3::ROWS == 0;
+}
+
 hipError_t launch_conv_col(const ConvArgs &a, hipStream_t s, std::string *label) {
-  if (!conv_col_ok(GCPSL_BF16, a) || a.epi != EPI_FWD) return hipErrorInvalidValue;
+  const bool img3 = a.taps == 9 && conv_im3_ok(GCPSL_BF16, a.Csrc, a.N, a.H, a.W);
+  if (a.epi != EPI_FWD || a.res != nullptr || a.Kp < COL_K || a.Kp % 8 != 0 ||
+      !(img3 || conv_col_ok(GCPSL_BF16, a)))
+    return hipErrorInvalidValue;
   const int MT = a.Bt * a.H * a.W / COL_PX;
-  if (label) *label = "conv_fwd<bf16,256x32x32,w4,col>";
-  hipLaunchKernelGGL(conv_col_kernel, dim3((uint32_t)MT * a.C), dim3(256), 0, s, a, MT);
+  if (label) *label = img3 ? "conv_fwd<bf16,256x32x27,w4,img3>" : "conv_fwd<bf16,256x32x32,w4,col>";
+  if (img3)
+    hipLaunchKernelGGL(conv_col_kernel<true>, dim3((uint32_t)MT * a.C), dim3(256), 0, s, a, MT);
+  else
+    hipLaunchKernelGGL(conv_col_kernel<false>, dim3((uint32_t)MT * a.C), dim3(256), 0, s, a, MT);
   return hipGetLastError();
 }
 

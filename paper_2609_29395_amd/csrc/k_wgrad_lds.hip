@@ -715,22 +715,29 @@ wgrad_img_kernel(WgradArgs a) {
   }
 }
 
-// ------------------------------------------------- image layer (im2col rows)
+// ------------------------------------------------------------ image layer
 // dW[co][k] = sum_p g[p][co] A[p][k] and db[co] = sum_p g[p][co] for the image
-// layer on its im2col rows: 32 output channels, 32 columns (9 x 3 taps and
-// channels, zero-padded; the first 27 are written).  A stream: each wave walks
-// groups of 32 pixels of the workgroup's chunk, copying the group's g rows and
-// im2col rows (2 KB each, contiguous) into its own double-buffered LDS region
+// layer: 32 output channels, k = (r, s, c) over the 3 x 3 taps of the 3 image
+// channels (27 columns, zero-padded to 32; the first 27 are written).  A
+// stream: each wave walks groups of 32 pixels of the workgroup's chunk,
+// copying the group's g rows (2 KB) into its own double-buffered LDS region
 // (no workgroup barrier in the loop), and multiplies transposed fragments
-// (four MFMAs per group, two more against ones for the bias).  The four
-// waves' sums are added in wave order at the end.
+// (four MFMAs per group, two more against ones for the bias).  The group's
+// im2col rows (2 KB) are either copied from the gathered rows (IMG3 false),
+// or (IMG3: bf16 NHWC images 32 pixels wide, so a group is one image row)
+// built in the stage by the wave from the image rows above, at and below
+// the group's row (576 bytes, copied with the g rows; zero outside the
+// image).  The four waves' sums are added in wave order at the end.
 namespace wc {
 constexpr int CO = 32, KC = 32, PX = 32;  // output channels, columns, pixels per group
 constexpr int ROW = 64;                   // bytes per pixel row of either operand
 constexpr int OP = PX * ROW;              // 2 KB per operand and group
-constexpr int STAGE = 2 * OP;             // g rows, then im2col rows
-constexpr int WAVE_LDS = 2 * STAGE;       // two stages per wave
+constexpr int RAW = 1024;                 // IMG3: three image rows of 192 bytes
+template <bool IMG3> constexpr int stage() { return 2 * OP + (IMG3 ? RAW : 0); }  // g rows, im2col rows (, image rows)
+template <bool IMG3> constexpr int wave_lds() { return 2 * stage<IMG3>(); }      // two stages per wave
 constexpr int BK = 128;                   // chunks are multiples of this
+constexpr int IMG_W = 32, IMG_C = 3;      // IMG3: image width and channels
+constexpr int VROW = IMG_W * IMG_C * 2 / 16;  // 16-byte pieces per image row (12)
 }  // namespace wc
 
 __device__ __forceinline__ void wc_issue(char *dst, const bf16_t *G, const bf16_t *X, uint32_t gbytes,
@@ -745,9 +752,30 @@ __device__ __forceinline__ void wc_issue(char *dst, const bf16_t *G, const bf16_
   }
 }
 
+// IMG3: the group's g rows, and image rows h - 1, h, h + 1 of the group's
+// image row (b, h) into the stage's raw region (lane 12 r + v: piece v of row
+// h + r - 1; lanes past 36 and rows outside the image read zero)
+__device__ __forceinline__ void wc_issue_img3(char *dst, const bf16_t *G, const bf16_t *X, uint32_t gbytes,
+                                              uint32_t xbytes, int p, int H, int lane) {
+  const __amdgpu_buffer_rsrc_t rsg = rsrc(G, gbytes);
+  const __amdgpu_buffer_rsrc_t rsx = rsrc(X, xbytes);
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsg, LDS_PTR(dst + h * 1024), 16,
+                                             (uint32_t)(p * wc::ROW + h * 1024 + lane * 16), 0, 0, 0);
+  const int q = p / wc::IMG_W, b = q / H, h = q - b * H;  // the group's image row
+  const int r = lane / wc::VROW, v = lane - r * wc::VROW, hh = h + r - 1;
+  const uint32_t off = (lane < 3 * wc::VROW && (unsigned)hh < (unsigned)H)
+                           ? (uint32_t)((((int64_t)b * H + hh) * wc::IMG_W * wc::IMG_C + 8 * v) * 2)
+                           : kOob;
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, LDS_PTR(dst + 2 * wc::OP), 16, off, 0, 0, 0);
+}
+
+template <bool IMG3>
 __global__ void __launch_bounds__(256)
 wgrad_col_kernel(WgradArgs a) {
-  __shared__ __attribute__((aligned(1024))) char smem[4 * wc::WAVE_LDS];
+  constexpr int STAGE = wc::stage<IMG3>();
+  __shared__ __attribute__((aligned(1024))) char smem[4 * wc::wave_lds<IMG3>()];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t t = xcd_swizzle(blockIdx.x, (uint32_t)(a.splits * a.C));
@@ -760,8 +788,18 @@ wgrad_col_kernel(WgradArgs a) {
   const int ng = (min(M, p_begin + a.chunk) - p_begin + wc::PX - 1) / wc::PX;
   const bf16_t *G = reinterpret_cast<const bf16_t *>(a.g) + rep * a.g_rs;
   const bf16_t *X = reinterpret_cast<const bf16_t *>(a.x) + rep * a.x_rs;
-  const uint32_t gbytes = (uint32_t)((int64_t)M * wc::CO * 2), xbytes = (uint32_t)((int64_t)M * wc::KC * 2);
-  char *mine = smem + wave * wc::WAVE_LDS;
+  const uint32_t gbytes = (uint32_t)((int64_t)M * wc::CO * 2),
+                 xbytes = (uint32_t)((int64_t)M * (IMG3 ? wc::IMG_C : wc::KC) * 2);
+  char *mine = smem + wave * wc::wave_lds<IMG3>();
+  auto issue = [&](char *dst, int p) {
+    if constexpr (IMG3)
+      wc_issue_img3(dst, G, X, gbytes, xbytes, p, a.H, lane);
+    else
+      wc_issue(dst, G, X, gbytes, xbytes, p, lane);
+  };
+  // IMG3: lane (px, kh) builds k = 16 kh .. 16 kh + 15 of pixel px's row;
+  // (r, s, c) of k sits at raw row r, pixel px + s - 1, channel c
+  const int bpx = lane & 31, bkh = lane >> 5;
   const uint32_t base = (uint32_t)(size_t)LDS_PTR(mine);
   // transposing reads: lane (lg, j) takes pixel rows 8 lg + j / 4 (+4), 16-byte
   // chunk 2 c + half of channel block c, 8-byte half j & 1
@@ -777,14 +815,35 @@ wgrad_col_kernel(WgradArgs a) {
   }
   // this wave's groups: wave, wave + 4, ...
   int i = wave;
-  if (i < ng) wc_issue(mine, G, X, gbytes, xbytes, p_begin + i * wc::PX, lane);
+  if (i < ng) issue(mine, p_begin + i * wc::PX);
   for (int s = 0; i < ng; i += 4, s ^= 1) {
     const bool next = i + 4 < ng;
-    if (next) wc_issue(mine + (s ^ 1) * wc::STAGE, G, X, gbytes, xbytes, p_begin + (i + 4) * wc::PX, lane);
+    if (next) issue(mine + (s ^ 1) * STAGE, p_begin + (i + 4) * wc::PX);
     // the group's own copies have landed once only the next group's are out
-    if (next) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    const uint32_t st = base + (uint32_t)(s * wc::STAGE);
+    if (next) {
+      if constexpr (IMG3)
+        asm volatile("s_waitcnt vmcnt(3)" ::: "memory");
+      else
+        asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    if constexpr (IMG3) {
+      const uint16_t *raw = reinterpret_cast<const uint16_t *>(mine + s * STAGE + 2 * wc::OP);
+      uint32_t h16[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int k = 16 * bkh + e, r = k / 9, sc = (k % 9) / 3, c = k % 3, w = bpx + sc - 1;
+        h16[e] = (k < 27 && (unsigned)w < (unsigned)wc::IMG_W) ? (uint32_t)raw[r * wc::IMG_W * wc::IMG_C + w * 3 + c]
+                                                                : 0u;
+      }
+      u32x4 *row = reinterpret_cast<u32x4 *>(mine + s * STAGE + wc::OP + bpx * wc::ROW + bkh * 32);
+      row[0] = u32x4{h16[0] | (h16[1] << 16), h16[2] | (h16[3] << 16), h16[4] | (h16[5] << 16),
+                     h16[6] | (h16[7] << 16)};
+      row[1] = u32x4{h16[8] | (h16[9] << 16), h16[10] | (h16[11] << 16), h16[12] | (h16[13] << 16),
+                     h16[14] | (h16[15] << 16)};
+    }
+    const uint32_t st = base + (uint32_t)(s * STAGE);
     u32x4 ga[2], xb[2];
     read_frag<0, wc::ROW>(ga[0], st + fr);
     read_frag<32, wc::ROW>(ga[1], st + fr);
@@ -849,10 +908,14 @@ bool wgrad_col_ok(int dtype, int Co, int Ci, int taps) {
 }
 
 hipError_t launch_wgrad_col(const WgradArgs &a, hipStream_t s, std::string *label) {
-  if (!wgrad_col_ok(GCPSL_BF16, a.Co, a.Ci, a.taps) || a.chunk % wc::BK || a.nw > wc::KC)
+  const bool img3 = a.taps == 9 && conv_im3_ok(GCPSL_BF16, a.Ci, a.Co, a.H, a.W);
+  if (!(img3 || wgrad_col_ok(GCPSL_BF16, a.Co, a.Ci, a.taps)) || a.chunk % wc::BK || a.nw > wc::KC)
     return hipErrorInvalidValue;
-  if (label) *label = "conv_wgrad<bf16,32x32,w4,col>";
-  hipLaunchKernelGGL(wgrad_col_kernel, dim3((uint32_t)a.splits * a.C), dim3(256), 0, s, a);
+  if (label) *label = img3 ? "conv_wgrad<bf16,32x27,w4,img3>" : "conv_wgrad<bf16,32x32,w4,col>";
+  if (img3)
+    hipLaunchKernelGGL(wgrad_col_kernel<true>, dim3((uint32_t)a.splits * a.C), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(wgrad_col_kernel<false>, dim3((uint32_t)a.splits * a.C), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -885,7 +948,7 @@ bool wgrad_halo_ok(int Co, int Ci, int H, int W, int taps) {
 // and how many such workgroups one CU holds (LDS-limited; halo mode: one,
 // its 8 waves hold 144 accumulator registers per lane).
 void wgrad_lds_tile(int Co, int Ci, int H, int W, int taps, int *bm, int *bn, int *bk, int *per_cu) {
-  if (taps == 1 && Co == wc::CO && Ci == wc::KC) {
+  if ((taps == 1 && Co == wc::CO && Ci == wc::KC) || (taps == 9 && conv_im3_ok(GCPSL_BF16, Ci, Co, H, W))) {
     *bm = wc::CO; *bn = wc::KC; *bk = wc::BK; *per_cu = 4;
   } else if (wgrad_halo_ok(Co, Ci, H, W, taps)) {
     *bm = wh::BM; *bn = 9 * 64; *bk = wh::BK; *per_cu = 1;

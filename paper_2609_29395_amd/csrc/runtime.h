@@ -98,6 +98,10 @@ hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *labe
 bool conv_img_ok(int dtype, const ConvArgs &a);
 // the image layer's forward on its im2col rows (32 columns, 32 channels)
 bool conv_col_ok(int dtype, const ConvArgs &a);
+// the image layer on the bf16 NHWC images themselves (3 -> 32 channels,
+// 32-pixel-wide images, a multiple of 8 rows): forward and weight gradient
+// build its im2col rows in LDS
+bool conv_im3_ok(int dtype, int Ci, int Co, int H, int W);
 hipError_t launch_conv_col(const ConvArgs &a, hipStream_t s, std::string *label);
 // whether launch_conv also writes ConvArgs::pool_out for this layer
 bool conv_fuses_pool(int dtype, const ConvArgs &a);

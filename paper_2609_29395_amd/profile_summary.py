@@ -73,10 +73,12 @@ def kernel_label(name: str) -> str:
     if m:
         kind = "conv_fwd" if m.group(3) == "0" else "conv_dgrad"
         return f"{kind}<bf16,256x{m.group(2)}x{9 * int(m.group(1))},w8,img>"
-    if re.search(r"wgrad_col_kernel", name):
-        return "conv_wgrad<bf16,32x32,w4,col>"
-    if re.search(r"conv_col_kernel", name):
-        return "conv_fwd<bf16,256x32x32,w4,col>"
+    m = re.search(r"wgrad_col_kernel(<(true|false)>)?", name)
+    if m:
+        return "conv_wgrad<bf16,32x27,w4,img3>" if m.group(2) == "true" else "conv_wgrad<bf16,32x32,w4,col>"
+    m = re.search(r"conv_col_kernel(<(true|false)>)?", name)
+    if m:
+        return "conv_fwd<bf16,256x32x27,w4,img3>" if m.group(2) == "true" else "conv_fwd<bf16,256x32x32,w4,col>"
     if re.search(r"wgrad_img_kernel<", name):
         return "conv_wgrad<bf16,64x288,w8,img>"
     if re.search(r"wgrad_halo_kernel<", name):
@@ -97,14 +99,19 @@ SHARED_HEADERS = ("common.h",)  # device helpers every kernel source includes
 
 def kernel_source(label: str) -> str:
     """The source file that holds the kernel a timing label names."""
-    if label.startswith("conv_wgrad<") and label.endswith((",lds>", ",halo>", ",img>", ",col>")):
+    if label.startswith("conv_wgrad<") and label.endswith((",lds>", ",halo>", ",img>", ",col>", ",img3>")):
         return "k_wgrad_lds.hip"
-    if label.startswith("conv_") and label.endswith((",lds>", ",halo>")):
+    if label.startswith("conv_") and label.endswith((",lds>", ",halo>", ",halo1>")):
         return "k_conv_lds.hip"
-    if label.startswith("conv_") and label.endswith((",img>", ",col>")):
+    if label.startswith("conv_") and label.endswith((",img>", ",col>", ",img3>")):
         return "k_conv_img.hip"
     if label.startswith("conv_"):
         return "k_conv.hip"
+    if label in ("chan_reduce", "chan_finish", "group_reduce", "norm_apply_fwd", "norm_apply_bwd") or \
+            label.startswith(("batchnorm", "groupnorm")):
+        return "k_norm.hip"
+    if label in ("im2col", "zero_insert"):
+        return "k_block.hip"
     return "k_misc.hip"
 
 

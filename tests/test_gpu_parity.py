@@ -47,9 +47,13 @@ def test_sample_and_gather_bit_exact(name, window, starts):
         got = out.cpu().numpy()
         ys = _np(ctx.tensor("y")).reshape(-1, C, B)
         H, W, Cin = cfg["H"], cfg["W"], cfg["Cin"]
+        # staged as the images themselves (kc = Cin) or as the image layer's
+        # im2col rows (kc = 9 Cin rounded up to the vector width)
+        xt = _np(ctx.tensor("x"))
+        kc = xt.size // (window * C * B * H * W)
         vec = 8 if cfg["dtype"] == "bf16" else 4
-        kc = Cin if Cin % vec == 0 else -(-9 * Cin // vec) * vec
-        xs = _np(ctx.tensor("x")).reshape(-1, C, B, H, W, kc)
+        assert kc in (Cin, -(-9 * Cin // vec) * vec), kc
+        xs = xt.reshape(-1, C, B, H, W, kc)
         for j in range(window):
             for n in range(C):
                 want = batch_indices(ids[n], B, cfg["seed"], n, s0 + j)

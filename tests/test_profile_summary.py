@@ -37,6 +37,37 @@ def test_other_labels():
                            "(ConvArgs, FastDiv, FastDiv, FastDiv, int, int)") == "conv_fwd<bf16,128x64x64,w8,lds>"
 
 
+def test_image_layer_labels():
+    ns = "void (anonymous namespace)::"
+    assert ps.kernel_label(ns + "conv_col_kernel<true>(ConvArgs, int)") == "conv_fwd<bf16,256x32x27,w4,img3>"
+    assert ps.kernel_label(ns + "conv_col_kernel<false>(ConvArgs, int)") == "conv_fwd<bf16,256x32x32,w4,col>"
+    assert ps.kernel_label(ns + "wgrad_col_kernel<true>(WgradArgs)") == "conv_wgrad<bf16,32x27,w4,img3>"
+    assert ps.kernel_label(ns + "wgrad_col_kernel<false>(WgradArgs)") == "conv_wgrad<bf16,32x32,w4,col>"
+
+
+@pytest.mark.parametrize("label,source", [
+    ("conv_fwd<bf16,256x128x64,w8,halo1>", "k_conv_lds.hip"),
+    ("conv_dgrad<bf16,256x128x64,w8,halo1>", "k_conv_lds.hip"),
+    ("conv_dgrad<bf16,256x64x192,w16,halo>", "k_conv_lds.hip"),
+    ("conv_wgrad<bf16,128x576,w8,halo>", "k_wgrad_lds.hip"),
+    ("conv_fwd<bf16,256x32x27,w4,img3>", "k_conv_img.hip"),
+    ("conv_wgrad<bf16,32x27,w4,img3>", "k_wgrad_lds.hip"),
+    ("conv_fwd<bf16,256x64x288,w8,img>", "k_conv_img.hip"),
+    ("conv_fwd<f32,128x128x32,w4,vec>", "k_conv.hip"),
+    ("sgd", "k_misc.hip"),
+    ("fuse", "k_misc.hip"),
+    ("chan_reduce", "k_norm.hip"),
+    ("norm_apply_bwd", "k_norm.hip"),
+    ("group_reduce", "k_norm.hip"),
+    ("im2col", "k_block.hip"),
+    ("zero_insert", "k_block.hip"),
+])
+def test_kernel_source_of_every_label_kind(label, source):
+    # the file whose hash decides whether a kernel's committed counters are
+    # still current
+    assert ps.kernel_source(label) == source
+
+
 def _write(path, header, rows):
     os.makedirs(os.path.dirname(path), exist_ok=True)
     with open(path, "w", newline="") as fh:
