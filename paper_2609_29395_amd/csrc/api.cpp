@@ -27,6 +27,15 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
+// Pixels per chunk of a channel reduction over px pixels of each of C
+// replicas: halved from 256 down to 16 until there are about 2048 chunks in
+// all, so that small late-stage tensors still spread over the chip.
+int norm_chunk(int64_t px, int C) {
+  int ch = 256;
+  while (ch > 16 && (px + ch - 1) / ch * C < 2048) ch >>= 1;
+  return ch;
+}
+
 struct LayerInfo {
   gcpsl_layer spec{};
   int H = 0, W = 0, Ci = 0;   // input geometry (per example)
@@ -76,7 +85,6 @@ struct Plan {
   std::vector<BlockInfo> blocks;
   int64_t P = 0, Pc = 0, S = 0;
   int head_conv = -1, avg_idx = -1, lin_idx = -1;  // head_conv: conv or norm feeding the head pooling
-  int norm_chunk_px = 256;
   bool head_maxpool = false;
   int Ch_head = 0;
   // The image layer's input is staged as im2col rows when its channel count
@@ -348,7 +356,7 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
     l.mean_off = take(sizeof(float) * C * l.nstat);
     l.rstd_off = take(sizeof(float) * C * l.nstat);
     l.sums_off = take(sizeof(double) * 2 * C * l.nstat);
-    const int64_t chunks = (rs + p.norm_chunk_px - 1) / p.norm_chunk_px;
+    const int64_t chunks = (rs + norm_chunk(rs, C) - 1) / norm_chunk(rs, C);
     npart = std::max(npart, (size_t)(C * chunks * l.Co * 2));
   };
   for (int i = 0; i < n; ++i) {
@@ -840,8 +848,8 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
     na.state = d.norm_state;
     na.P = p.P; na.g_off = l.w_off; na.b_off = l.b_off; na.S = p.S; na.st_off = l.st_off; na.z_rs = l.act_rs;
     na.Bt = B; na.H = l.H; na.W = l.W; na.Ch = l.Co; na.groups = l.groups; na.nstat = l.nstat;
-    na.chunk_px = p.norm_chunk_px;
-    na.chunks = (int)(((int64_t)B * l.H * l.W + p.norm_chunk_px - 1) / p.norm_chunk_px);
+    na.chunk_px = norm_chunk((int64_t)B * l.H * l.W, C);
+    na.chunks = (int)(((int64_t)B * l.H * l.W + na.chunk_px - 1) / na.chunk_px);
     na.C = C;
     na.rmap = rmap;
     return na;
@@ -864,8 +872,8 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
     na.P = p.P; na.g_off = nl.w_off; na.b_off = nl.b_off; na.S = p.S; na.st_off = nl.st_off;
     na.z_rs = (int64_t)B * nl.H * nl.W * nl.Co;
     na.Bt = B; na.H = nl.H; na.W = nl.W; na.Ch = nl.Co; na.groups = nl.groups; na.nstat = nl.nstat;
-    na.chunk_px = p.norm_chunk_px;
-    na.chunks = (int)(((int64_t)B * nl.H * nl.W + p.norm_chunk_px - 1) / p.norm_chunk_px);
+    na.chunk_px = norm_chunk((int64_t)B * nl.H * nl.W, C);
+    na.chunks = (int)(((int64_t)B * nl.H * nl.W + na.chunk_px - 1) / na.chunk_px);
     na.C = C;
     na.rmap = rmap;
     na.res = res;

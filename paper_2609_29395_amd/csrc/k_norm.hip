@@ -60,28 +60,43 @@ chan_reduce_kernel(NormArgs a) {
   double s0[VEC], s1[VEC];
 #pragma unroll
   for (int e = 0; e < VEC; ++e) s0[e] = s1[e] = 0.0;
-  if (pl < PL) {
-    for (int64_t p = p0 + pl; p < p1; p += PL) {
-      const V16<T> zv = load16(z + p * a.Ch + cv * VEC);
-      if constexpr (MODE == 0) {
+  auto add = [&](const V16<T> &zv, const V16<T> &gv, int64_t p) {
+    if constexpr (MODE == 0) {
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          const double v = ElemT<T>::to_f(zv.v[e]);
-          s0[e] += v;
-          s1[e] += v * v;
-        }
-      } else {
-        const V16<T> gv = load16(du + p * a.Ch + cv * VEC);
-        const int b = (int)(p / (a.H * a.W));
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          const int si = stat_index(a, b, cv * VEC + e);
-          const float xh = (ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si];
-          const double g = ElemT<T>::to_f(gv.v[e]);
-          s0[e] += g;
-          s1[e] += g * (double)xh;
-        }
+      for (int e = 0; e < VEC; ++e) {
+        const double v = ElemT<T>::to_f(zv.v[e]);
+        s0[e] += v;
+        s1[e] += v * v;
       }
+    } else {
+      const int b = (int)(p / (a.H * a.W));
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const int si = stat_index(a, b, cv * VEC + e);
+        const float xh = (ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si];
+        const double g = ElemT<T>::to_f(gv.v[e]);
+        s0[e] += g;
+        s1[e] += g * (double)xh;
+      }
+    }
+  };
+  if (pl < PL) {
+    // four pixels' loads in flight, added in pixel order
+    int64_t p = p0 + pl;
+    for (; p + 3 * PL < p1; p += 4 * PL) {
+      V16<T> zv[4], gv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        zv[u] = load16(z + (p + u * PL) * a.Ch + cv * VEC);
+        if constexpr (MODE == 1) gv[u] = load16(du + (p + u * PL) * a.Ch + cv * VEC);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) add(zv[u], gv[u], p + u * PL);
+    }
+    for (; p < p1; p += PL) {
+      V16<T> zv = load16(z + p * a.Ch + cv * VEC), gv{};
+      if constexpr (MODE == 1) gv = load16(du + p * a.Ch + cv * VEC);
+      add(zv, gv, p);
     }
   }
 #pragma unroll
@@ -105,20 +120,53 @@ chan_reduce_kernel(NormArgs a) {
   }
 }
 
-// Chunk partials -> per-channel sums (chunk order).  MODE 0: batch-norm mean
-// and rstd, and the running statistics; MODE 1: dbeta, dgamma into grad and
-// (batch norm) the sums for the input gradient.
+// Chunk partials -> per-channel sums.  A workgroup takes 32 channels: lane j
+// of a channel adds chunks j, j + 8, j + 16, ... in order (four loads in
+// flight), and the 8 lanes' sums are added in lane order.  MODE 0:
+// batch-norm mean and rstd, and the running statistics; MODE 1: dbeta,
+// dgamma into grad and (batch norm) the sums for the input gradient.
+constexpr int kFinishCh = 32, kFinishLanes = 8;
+
 template <int MODE>
 __global__ void __launch_bounds__(256)
 chan_finish_kernel(NormArgs a) {
+  __shared__ double red[kFinishLanes][kFinishCh][2];
   const int rep = replica_of(a.rmap, blockIdx.y);
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= a.Ch) return;
+  const int cl = threadIdx.x % kFinishCh, j = threadIdx.x / kFinishCh;
+  const int c = blockIdx.x * kFinishCh + cl;
   double S0 = 0.0, S1 = 0.0;
-  for (int k = 0; k < a.chunks; ++k) {
-    const double *pp = a.part + (((int64_t)rep * a.chunks + k) * a.Ch + c) * 2;
-    S0 += pp[0];
-    S1 += pp[1];
+  if (c < a.Ch) {
+    const double *pp = a.part + ((int64_t)rep * a.chunks * a.Ch + c) * 2;
+    const int64_t step = (int64_t)a.Ch * 2;
+    int k = j;
+    for (; k + 3 * kFinishLanes < a.chunks; k += 4 * kFinishLanes) {
+      double v[4][2];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        v[u][0] = pp[(k + u * kFinishLanes) * step];
+        v[u][1] = pp[(k + u * kFinishLanes) * step + 1];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        S0 += v[u][0];
+        S1 += v[u][1];
+      }
+    }
+    for (; k < a.chunks; k += kFinishLanes) {
+      S0 += pp[k * step];
+      S1 += pp[k * step + 1];
+    }
+  }
+  red[j][cl][0] = S0;
+  red[j][cl][1] = S1;
+  __syncthreads();
+  if (j != 0 || c >= a.Ch) return;
+  S0 = red[0][cl][0];
+  S1 = red[0][cl][1];
+#pragma unroll
+  for (int l = 1; l < kFinishLanes; ++l) {
+    S0 += red[l][cl][0];
+    S1 += red[l][cl][1];
   }
   const double n = (double)a.Bt * a.H * a.W;
   if constexpr (MODE == 0) {
@@ -161,27 +209,42 @@ group_reduce_kernel(NormArgs a) {
   double s0[VEC], s1[VEC];
 #pragma unroll
   for (int e = 0; e < VEC; ++e) s0[e] = s1[e] = 0.0;
-  if (pl < PL) {
-    for (int p = pl; p < HW; p += PL) {
-      const V16<T> zv = load16(z + (int64_t)p * a.Ch + cv * VEC);
-      if constexpr (MODE == 0) {
+  auto add = [&](const V16<T> &zv, const V16<T> &gv) {
+    if constexpr (MODE == 0) {
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          const double v = ElemT<T>::to_f(zv.v[e]);
-          s0[e] += v;
-          s1[e] += v * v;
-        }
-      } else {
-        const V16<T> gv = load16(du + (int64_t)p * a.Ch + cv * VEC);
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          const int c = cv * VEC + e, si = b * G + c / CG;
-          const float xh = (ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si];
-          const double dx = (double)ElemT<T>::to_f(gv.v[e]) * gamma[c];
-          s0[e] += dx;
-          s1[e] += dx * (double)xh;
-        }
+      for (int e = 0; e < VEC; ++e) {
+        const double v = ElemT<T>::to_f(zv.v[e]);
+        s0[e] += v;
+        s1[e] += v * v;
       }
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const int c = cv * VEC + e, si = b * G + c / CG;
+        const float xh = (ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si];
+        const double dx = (double)ElemT<T>::to_f(gv.v[e]) * gamma[c];
+        s0[e] += dx;
+        s1[e] += dx * (double)xh;
+      }
+    }
+  };
+  if (pl < PL) {
+    // four pixels' loads in flight, added in pixel order
+    int p = pl;
+    for (; p + 3 * PL < HW; p += 4 * PL) {
+      V16<T> zv[4], gv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        zv[u] = load16(z + (int64_t)(p + u * PL) * a.Ch + cv * VEC);
+        if constexpr (MODE == 1) gv[u] = load16(du + (int64_t)(p + u * PL) * a.Ch + cv * VEC);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) add(zv[u], gv[u]);
+    }
+    for (; p < HW; p += PL) {
+      V16<T> zv = load16(z + (int64_t)p * a.Ch + cv * VEC), gv{};
+      if constexpr (MODE == 1) gv = load16(du + (int64_t)p * a.Ch + cv * VEC);
+      add(zv, gv);
     }
   }
 #pragma unroll
@@ -295,7 +358,7 @@ hipError_t norm_fwd_t(const NormArgs &a, hipStream_t s) {
     hipLaunchKernelGGL((group_reduce_kernel<T, 0>), dim3(a.Bt, a.C), dim3(256), 0, s, a);
   } else {
     hipLaunchKernelGGL((chan_reduce_kernel<T, 0>), dim3(a.chunks, a.C), dim3(256), 0, s, a);
-    hipLaunchKernelGGL((chan_finish_kernel<0>), dim3((a.Ch + 255) / 256, a.C), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((chan_finish_kernel<0>), dim3((a.Ch + kFinishCh - 1) / kFinishCh, a.C), dim3(256), 0, s, a);
   }
   hipLaunchKernelGGL((norm_apply_fwd_kernel<T>), dim3((total + 255) / 256, a.C), dim3(256), 0, s, a, total);
   return hipGetLastError();
@@ -306,7 +369,7 @@ hipError_t norm_bwd_t(const NormArgs &a, hipStream_t s) {
   constexpr int VEC = ElemT<T>::VEC;
   const uint32_t total = (uint32_t)((int64_t)a.Bt * a.H * a.W * (a.Ch / VEC));
   hipLaunchKernelGGL((chan_reduce_kernel<T, 1>), dim3(a.chunks, a.C), dim3(256), 0, s, a);
-  hipLaunchKernelGGL((chan_finish_kernel<1>), dim3((a.Ch + 255) / 256, a.C), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((chan_finish_kernel<1>), dim3((a.Ch + kFinishCh - 1) / kFinishCh, a.C), dim3(256), 0, s, a);
   if (a.groups) hipLaunchKernelGGL((group_reduce_kernel<T, 1>), dim3(a.Bt, a.C), dim3(256), 0, s, a);
   hipLaunchKernelGGL((norm_apply_bwd_kernel<T>), dim3((total + 255) / 256, a.C), dim3(256), 0, s, a, total);
   return hipGetLastError();
