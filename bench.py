@@ -9,7 +9,8 @@ one: K=256 clients, C=16 label-L1 clusters, B=128 per cluster (2048 examples
 per step), bf16 activations/weights with fp32 masters, wide residual server,
 fusion every 50 rounds, synthetic CIFAR-10-shaped data.  The 8-cluster (bf16)
 and 4-cluster (fp32) workloads and the paper's ResNet-18 model (4 clusters,
-fp32, epoch-barrier schedule) are measured the same way as sub-results.
+epoch-barrier schedule, fp32 and bf16) are measured the same way as
+sub-results.
 
 Prints one JSON line.  `value` is examples/s summed over the C clusters
 (the examples the clusters that take a round process: under the epoch
@@ -52,6 +53,7 @@ DESCRIPTIONS = {
                 "after stage 2 (group norm client / batch norm server), Nesterov SGD with weight decay and "
                 "label smoothing, epoch-barrier schedule with fusion after every epoch, synthetic 32x32x3 "
                 "10-class",
+    "resnet18_bf16": "the same ResNet-18 workload in bf16 (fp32 masters)",
 }
 
 
@@ -310,7 +312,7 @@ def measure(name, steps, warmup, timing_steps, cpu_seconds, with_cpu=True, with_
     return out
 
 
-SUB_RESULTS = ("gcpsl8", "gcpsl4", "resnet18")
+SUB_RESULTS = ("gcpsl8", "gcpsl4", "resnet18", "resnet18_bf16")
 
 
 def main():

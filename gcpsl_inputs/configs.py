@@ -124,6 +124,13 @@ CONFIGS = {
         layers=_resnet((64, 128, 256, 512), 32)[0], cut=_resnet((64, 128, 256, 512), 32)[1],
         dtype="f32", lr=0.01, momentum=0.9, nesterov=True, weight_decay=5e-4, label_smoothing=0.1,
         F=0, T=3, seed=0, schedule="epoch"),
+    # The same model and recipe in bf16 (fp32 masters): the paper states no
+    # precision, and this is the one the MFMA peak is quoted for.
+    "resnet18_bf16": dict(
+        K=256, C=4, B=64, alpha=0.3, rule="label_jsd", **dict(_CIFAR_DATA, N_ex=45000),
+        layers=_resnet((64, 128, 256, 512), 32)[0], cut=_resnet((64, 128, 256, 512), 32)[1],
+        dtype="bf16", lr=0.01, momentum=0.9, nesterov=True, weight_decay=5e-4, label_smoothing=0.1,
+        F=0, T=3, seed=0, schedule="epoch"),
     # The same topology at small size (16 x 16 images, widths 8-64), fp32 and
     # bf16: every block kind (identity and projection shortcut, stride 1 and
     # 2, group and batch norm), stage 4 on 2 x 2 maps (batch norm over 64

@@ -372,7 +372,7 @@ def test_fuse_replicas_large_sampled_and_identity():
 
 # ------------------------------------------------ full sizes, sampled outputs
 
-@pytest.mark.parametrize("name", ["gpsl", "gcpsl4", "gcpsl8", "gcpsl16", "resnet18"])
+@pytest.mark.parametrize("name", ["gpsl", "gcpsl4", "gcpsl8", "gcpsl16", "resnet18", "resnet18_bf16"])
 def test_full_size_round_sampled_replicas(name):
     """One round at the workload's real size; replicas 0 and C-1 recomputed by
     the oracle under the GPU's validated decisions: forward activations of
