@@ -742,7 +742,7 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   // tile over a long k loop takes 128 pixels (48 KB of LDS: three
   // workgroups per CU hide more latency), over a short one 256 (less fixed
   // cost per output)
-  const int bn = a.N > 128 ? 256 : a.N > 64 ? 128 : a.N > 32 ? 64 : 32;
+  int bn = a.N > 128 ? 256 : a.N > 64 ? 128 : a.N > 32 ? 64 : 32;
   // halo mode: one 16 x 16 image per 256-pixel tile, 64-channel blocks, with
   // 256-wide weight tiles or (input channels a multiple of 64, no residual)
   // 64-wide ones
@@ -750,7 +750,16 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   const bool use_h128 = use_halo128(a);
   const bool use_halo = img16 && bn == 256 && !use_h128;
   const bool use_halo64 = img16 && bn == 64 && a.res == nullptr;
-  const int bm = (bn == 64 && a.Kp >= 16 * BK && !use_halo64) ? 128 : 256;
+  int bm = (bn == 64 && a.Kp >= 16 * BK && !use_halo64) ? 128 : 256;
+  if (!img16) {
+    // a small grid (low-resolution layers of a few replicas: 8 x 8 or 4 x 4
+    // maps of 64 examples fill 64 or fewer 256 x 256 tiles) takes narrower
+    // tiles, 256 x 128 and then 128 x 64, until about two workgroups per CU
+    const int64_t Mr = (int64_t)a.Bt * a.H * a.W;
+    auto wgs = [&](int m, int n) { return ((Mr + m - 1) / m) * ((a.N + n - 1) / n) * a.C; };
+    if (bn == 256 && wgs(256, 256) < 512) bn = 128;
+    if (bn == 128 && wgs(256, 128) < 512) bn = 64, bm = 128;
+  }
   int MT, NT;
   if (use_h128) grid<256, 128>(a, &MT, &NT);
   else if (bn == 256) grid<256, 256>(a, &MT, &NT);

@@ -60,6 +60,10 @@ chan_reduce_kernel(NormArgs a) {
   double s0[VEC], s1[VEC];
 #pragma unroll
   for (int e = 0; e < VEC; ++e) s0[e] = s1[e] = 0.0;
+  // MODE 1: the statistics of this thread's channels, loaded when its example
+  // changes (group norm) or once (batch norm)
+  int kb = -1;
+  float km[VEC], kr[VEC];
   auto add = [&](const V16<T> &zv, const V16<T> &gv, int64_t p) {
     if constexpr (MODE == 0) {
 #pragma unroll
@@ -70,10 +74,17 @@ chan_reduce_kernel(NormArgs a) {
       }
     } else {
       const int b = (int)(p / (a.H * a.W));
+      if (kb < 0 || (a.groups && b != kb)) {
+        kb = b;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const int si = stat_index(a, b, cv * VEC + e);
+          km[e] = mean[si], kr[e] = rstd[si];
+        }
+      }
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        const int si = stat_index(a, b, cv * VEC + e);
-        const float xh = (ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si];
+        const float xh = (ElemT<T>::to_f(zv.v[e]) - km[e]) * kr[e];
         const double g = ElemT<T>::to_f(gv.v[e]);
         s0[e] += g;
         s1[e] += g * (double)xh;
@@ -209,6 +220,17 @@ group_reduce_kernel(NormArgs a) {
   double s0[VEC], s1[VEC];
 #pragma unroll
   for (int e = 0; e < VEC; ++e) s0[e] = s1[e] = 0.0;
+  // MODE 1: this thread's channels' statistics of example b and gamma
+  float km[VEC], kr[VEC], kg[VEC];
+  if constexpr (MODE == 1) {
+    if (pl < PL) {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const int c = cv * VEC + e, si = b * G + c / CG;
+        km[e] = mean[si], kr[e] = rstd[si], kg[e] = gamma[c];
+      }
+    }
+  }
   auto add = [&](const V16<T> &zv, const V16<T> &gv) {
     if constexpr (MODE == 0) {
 #pragma unroll
@@ -220,9 +242,8 @@ group_reduce_kernel(NormArgs a) {
     } else {
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        const int c = cv * VEC + e, si = b * G + c / CG;
-        const float xh = (ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si];
-        const double dx = (double)ElemT<T>::to_f(gv.v[e]) * gamma[c];
+        const float xh = (ElemT<T>::to_f(zv.v[e]) - km[e]) * kr[e];
+        const double dx = (double)ElemT<T>::to_f(gv.v[e]) * kg[e];
         s0[e] += dx;
         s1[e] += dx * (double)xh;
       }
@@ -286,48 +307,75 @@ group_reduce_kernel(NormArgs a) {
   }
 }
 
-// a = ReLU(gamma (z - mean) rstd + beta (+ res)), one 16-byte vector per
-// thread (without the ReLU for a shortcut's norm).
+// The elementwise passes: a thread keeps one 16-byte vector of VEC channels
+// and walks pixels at a stride that is a multiple of the channel vectors per
+// pixel (so its channels stay the same unless Ch / VEC does not divide the
+// stride), four pixels' loads in flight.  The per-channel values it needs
+// (gamma, beta; the statistics of its example for group norm) are loaded when
+// its channels or its example change, not per element; every value and
+// expression is the same as per element, so the results are too.
+constexpr int kApplyUnroll = 4;
+
+// a = ReLU(gamma (z - mean) rstd + beta (+ res)) (without the ReLU for a
+// shortcut's norm).
 template <typename T>
 __global__ void __launch_bounds__(256)
 norm_apply_fwd_kernel(NormArgs a, uint32_t total) {
   constexpr int VEC = ElemT<T>::VEC;
-  const uint32_t i = blockIdx.x * 256u + threadIdx.x;
-  if (i >= total) return;
   const int rep = replica_of(a.rmap, blockIdx.y);
-  const int CV = a.Ch / VEC;
-  const uint32_t p = i / CV;
-  const int c0 = (int)(i - p * CV) * VEC, b = (int)(p / (a.H * a.W));
+  const int CV = a.Ch / VEC, HW = a.H * a.W;
   const T *z = reinterpret_cast<const T *>(a.z) + rep * a.z_rs;
+  const T *res = a.res ? reinterpret_cast<const T *>(a.res) + rep * a.z_rs : nullptr;
   T *out = reinterpret_cast<T *>(a.a) + rep * a.z_rs;
   const float *mean = a.mean + (int64_t)rep * a.nstat, *rstd = a.rstd + (int64_t)rep * a.nstat;
   const float *gamma = a.theta + rep * a.P + a.g_off, *beta = a.theta + rep * a.P + a.b_off;
-  const V16<T> zv = load16(z + (int64_t)i * VEC);
-  V16<T> rv;
-  if (a.res) rv = load16(reinterpret_cast<const T *>(a.res) + rep * a.z_rs + (int64_t)i * VEC);
-  V16<T> o;
+  const uint32_t stride = gridDim.x * 256u;
+  int kc = -1, kb = -1;  // channel vector and example of the cached values
+  float km[VEC], kr[VEC], kg[VEC], kbt[VEC];
+  for (uint32_t i0 = blockIdx.x * 256u + threadIdx.x; i0 < total; i0 += kApplyUnroll * stride) {
+    V16<T> zv[kApplyUnroll], rv[kApplyUnroll];
 #pragma unroll
-  for (int e = 0; e < VEC; ++e) {
-    const int c = c0 + e, si = stat_index(a, b, c);
-    float u = gamma[c] * ((ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si]) + beta[c];
-    if (a.res) u += ElemT<T>::to_f(rv.v[e]);
-    o.v[e] = ElemT<T>::from_f(a.relu ? fmaxf(u, 0.f) : u);
+    for (int u = 0; u < kApplyUnroll; ++u) {
+      const uint32_t i = i0 + u * stride;
+      if (i < total) {
+        zv[u] = load16(z + (int64_t)i * VEC);
+        if (res) rv[u] = load16(res + (int64_t)i * VEC);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kApplyUnroll; ++u) {
+      const uint32_t i = i0 + u * stride;
+      if (i >= total) break;
+      const uint32_t p = i / CV;
+      const int cv = (int)(i - p * CV), b = (int)(p / HW);
+      if (cv != kc || (a.groups && b != kb)) {
+        kc = cv, kb = b;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const int c = cv * VEC + e, si = stat_index(a, b, c);
+          km[e] = mean[si], kr[e] = rstd[si], kg[e] = gamma[c], kbt[e] = beta[c];
+        }
+      }
+      V16<T> o;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        float uu = kg[e] * ((ElemT<T>::to_f(zv[u].v[e]) - km[e]) * kr[e]) + kbt[e];
+        if (res) uu += ElemT<T>::to_f(rv[u].v[e]);
+        o.v[e] = ElemT<T>::from_f(a.relu ? fmaxf(uu, 0.f) : uu);
+      }
+      store16(out + (int64_t)i * VEC, o);
+    }
   }
-  store16(out + (int64_t)i * VEC, o);
 }
 
-// dz = rstd (du gamma - S1 / n - x_hat S2 / n), one 16-byte vector per thread;
-// batch norm's S1, S2 are gamma times the per-channel sums.
+// dz = rstd (du gamma - S1 / n - x_hat S2 / n); batch norm's S1, S2 are gamma
+// times the per-channel sums.
 template <typename T>
 __global__ void __launch_bounds__(256)
 norm_apply_bwd_kernel(NormArgs a, uint32_t total) {
   constexpr int VEC = ElemT<T>::VEC;
-  const uint32_t i = blockIdx.x * 256u + threadIdx.x;
-  if (i >= total) return;
   const int rep = replica_of(a.rmap, blockIdx.y);
-  const int CV = a.Ch / VEC;
-  const uint32_t p = i / CV;
-  const int c0 = (int)(i - p * CV) * VEC, b = (int)(p / (a.H * a.W));
+  const int CV = a.Ch / VEC, HW = a.H * a.W;
   const T *z = reinterpret_cast<const T *>(a.z) + rep * a.z_rs;
   const T *du = reinterpret_cast<const T *>(a.du) + rep * a.z_rs;
   T *dz = reinterpret_cast<T *>(a.dz) + rep * a.z_rs;
@@ -335,19 +383,51 @@ norm_apply_bwd_kernel(NormArgs a, uint32_t total) {
   const float *gamma = a.theta + rep * a.P + a.g_off;
   const double *sums = a.sums + (int64_t)rep * a.nstat * 2;
   const double n = a.groups ? (double)a.H * a.W * (a.Ch / a.groups) : (double)a.Bt * a.H * a.W;
-  const V16<T> zv = load16(z + (int64_t)i * VEC), gv = load16(du + (int64_t)i * VEC);
-  V16<T> o;
+  const uint32_t stride = gridDim.x * 256u;
+  int kc = -1, kb = -1;
+  float km[VEC], kr[VEC], kg[VEC], k1[VEC], k2[VEC];
+  for (uint32_t i0 = blockIdx.x * 256u + threadIdx.x; i0 < total; i0 += kApplyUnroll * stride) {
+    V16<T> zv[kApplyUnroll], gv[kApplyUnroll];
 #pragma unroll
-  for (int e = 0; e < VEC; ++e) {
-    const int c = c0 + e, si = stat_index(a, b, c);
-    const float xh = (ElemT<T>::to_f(zv.v[e]) - mean[si]) * rstd[si];
-    const float s1 = (float)(sums[2 * si] / n), s2 = (float)(sums[2 * si + 1] / n);
-    const float g = gamma[c];
-    const float v = a.groups ? rstd[si] * (ElemT<T>::to_f(gv.v[e]) * g - s1 - xh * s2)
-                             : rstd[si] * g * (ElemT<T>::to_f(gv.v[e]) - s1 - xh * s2);
-    o.v[e] = ElemT<T>::from_f(v);
+    for (int u = 0; u < kApplyUnroll; ++u) {
+      const uint32_t i = i0 + u * stride;
+      if (i < total) {
+        zv[u] = load16(z + (int64_t)i * VEC);
+        gv[u] = load16(du + (int64_t)i * VEC);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kApplyUnroll; ++u) {
+      const uint32_t i = i0 + u * stride;
+      if (i >= total) break;
+      const uint32_t p = i / CV;
+      const int cv = (int)(i - p * CV), b = (int)(p / HW);
+      if (cv != kc || (a.groups && b != kb)) {
+        kc = cv, kb = b;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const int c = cv * VEC + e, si = stat_index(a, b, c);
+          km[e] = mean[si], kr[e] = rstd[si], kg[e] = gamma[c];
+          k1[e] = (float)(sums[2 * si] / n), k2[e] = (float)(sums[2 * si + 1] / n);
+        }
+      }
+      V16<T> o;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const float xh = (ElemT<T>::to_f(zv[u].v[e]) - km[e]) * kr[e];
+        const float v = a.groups ? kr[e] * (ElemT<T>::to_f(gv[u].v[e]) * kg[e] - k1[e] - xh * k2[e])
+                                 : kr[e] * kg[e] * (ElemT<T>::to_f(gv[u].v[e]) - k1[e] - xh * k2[e]);
+        o.v[e] = ElemT<T>::from_f(v);
+      }
+      store16(dz + (int64_t)i * VEC, o);
+    }
   }
-  store16(dz + (int64_t)i * VEC, o);
+}
+
+// workgroups of an elementwise pass over `total` vectors of one replica:
+// about kApplyUnroll vectors per thread
+uint32_t apply_blocks(uint32_t total) {
+  return std::max<uint32_t>(1u, (total + 256u * kApplyUnroll - 1) / (256u * kApplyUnroll));
 }
 
 template <typename T>
@@ -360,7 +440,7 @@ hipError_t norm_fwd_t(const NormArgs &a, hipStream_t s) {
     hipLaunchKernelGGL((chan_reduce_kernel<T, 0>), dim3(a.chunks, a.C), dim3(256), 0, s, a);
     hipLaunchKernelGGL((chan_finish_kernel<0>), dim3((a.Ch + kFinishCh - 1) / kFinishCh, a.C), dim3(256), 0, s, a);
   }
-  hipLaunchKernelGGL((norm_apply_fwd_kernel<T>), dim3((total + 255) / 256, a.C), dim3(256), 0, s, a, total);
+  hipLaunchKernelGGL((norm_apply_fwd_kernel<T>), dim3(apply_blocks(total), a.C), dim3(256), 0, s, a, total);
   return hipGetLastError();
 }
 
@@ -371,7 +451,7 @@ hipError_t norm_bwd_t(const NormArgs &a, hipStream_t s) {
   hipLaunchKernelGGL((chan_reduce_kernel<T, 1>), dim3(a.chunks, a.C), dim3(256), 0, s, a);
   hipLaunchKernelGGL((chan_finish_kernel<1>), dim3((a.Ch + kFinishCh - 1) / kFinishCh, a.C), dim3(256), 0, s, a);
   if (a.groups) hipLaunchKernelGGL((group_reduce_kernel<T, 1>), dim3(a.Bt, a.C), dim3(256), 0, s, a);
-  hipLaunchKernelGGL((norm_apply_bwd_kernel<T>), dim3((total + 255) / 256, a.C), dim3(256), 0, s, a, total);
+  hipLaunchKernelGGL((norm_apply_bwd_kernel<T>), dim3(apply_blocks(total), a.C), dim3(256), 0, s, a, total);
   return hipGetLastError();
 }
 
