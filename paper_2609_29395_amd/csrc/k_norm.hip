@@ -46,7 +46,7 @@ __device__ __forceinline__ int stat_index(const NormArgs &a, int b, int c) {
 // Partials part[rep][chunk][c][2].
 template <typename T, int MODE>
 __global__ void __launch_bounds__(256)
-chan_reduce_kernel(NormArgs a) {
+chan_reduce_kernel(NormArgs a, FastDiv fhw) {
   constexpr int VEC = ElemT<T>::VEC;
   __shared__ double red[256][2 * VEC];
   const int rep = replica_of(a.rmap, blockIdx.y);
@@ -73,7 +73,7 @@ chan_reduce_kernel(NormArgs a) {
         s1[e] += v * v;
       }
     } else {
-      const int b = (int)(p / (a.H * a.W));
+      const int b = (int)fdiv((uint32_t)p, fhw);
       if (kb < 0 || (a.groups && b != kb)) {
         kb = b;
 #pragma unroll
@@ -116,18 +116,14 @@ chan_reduce_kernel(NormArgs a) {
     red[tid][VEC + e] = s1[e];
   }
   __syncthreads();
-  if (tid < CV) {
-    double* out = a.part + (((int64_t)rep * a.chunks + blockIdx.x) * a.Ch + cv * VEC) * 2;
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      double t0 = 0.0, t1 = 0.0;
-      for (int k = 0; k < PL; ++k) {
-        t0 += red[k * CV + cv][e];
-        t1 += red[k * CV + cv][VEC + e];
-      }
-      out[2 * e] = t0;
-      out[2 * e + 1] = t1;
-    }
+  // the chunk's sums: one (channel, sum) per thread, over the pixel lanes in
+  // lane order
+  double *out = a.part + ((int64_t)rep * a.chunks + blockIdx.x) * a.Ch * 2;
+  for (int o = tid; o < 2 * a.Ch; o += 256) {
+    const int c = o >> 1, k = o & 1, ocv = c / VEC, e = c - ocv * VEC;
+    double t = 0.0;
+    for (int l = 0; l < PL; ++l) t += red[l * CV + ocv][k * VEC + e];
+    out[o] = t;
   }
 }
 
@@ -274,17 +270,13 @@ group_reduce_kernel(NormArgs a) {
     red[tid][VEC + e] = s1[e];
   }
   __syncthreads();
-  if (tid < CV) {
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      double t0 = 0.0, t1 = 0.0;
-      for (int k = 0; k < PL; ++k) {
-        t0 += red[k * CV + cv][e];
-        t1 += red[k * CV + cv][VEC + e];
-      }
-      chs[cv * VEC + e][0] = t0;
-      chs[cv * VEC + e][1] = t1;
-    }
+  // per-channel sums: one (channel, sum) per thread, over the pixel lanes in
+  // lane order
+  for (int o = tid; o < 2 * a.Ch; o += 256) {
+    const int c = o >> 1, k = o & 1, ocv = c / VEC, e = c - ocv * VEC;
+    double t = 0.0;
+    for (int l = 0; l < PL; ++l) t += red[l * CV + ocv][k * VEC + e];
+    chs[c][k] = t;
   }
   __syncthreads();
   for (int g = tid; g < G; g += blockDim.x) {
@@ -307,32 +299,33 @@ group_reduce_kernel(NormArgs a) {
   }
 }
 
-// The elementwise passes: a thread keeps one 16-byte vector of VEC channels
-// and walks pixels at a stride that is a multiple of the channel vectors per
-// pixel (so its channels stay the same unless Ch / VEC does not divide the
-// stride), four pixels' loads in flight.  The per-channel values it needs
-// (gamma, beta; the statistics of its example for group norm) are loaded when
-// its channels or its example change, not per element; every value and
-// expression is the same as per element, so the results are too.
+// The elementwise passes: a workgroup takes kApplyUnroll consecutive runs of
+// 256 16-byte vectors (four loads in flight per thread), so a thread keeps
+// the same VEC channels (256 is a multiple of the vectors per pixel) and
+// stays within one example over neighbouring pixels.  The per-channel values
+// it needs (gamma, beta; the statistics of its example for group norm) are
+// loaded when its channels or its example change, not per element; every
+// value and expression is the same as per element, so the results are too.
 constexpr int kApplyUnroll = 4;
 
 // a = ReLU(gamma (z - mean) rstd + beta (+ res)) (without the ReLU for a
 // shortcut's norm).
 template <typename T>
 __global__ void __launch_bounds__(256)
-norm_apply_fwd_kernel(NormArgs a, uint32_t total) {
+norm_apply_fwd_kernel(NormArgs a, uint32_t total, FastDiv fcv, FastDiv fhw) {
   constexpr int VEC = ElemT<T>::VEC;
   const int rep = replica_of(a.rmap, blockIdx.y);
-  const int CV = a.Ch / VEC, HW = a.H * a.W;
+  const int CV = a.Ch / VEC;
   const T *z = reinterpret_cast<const T *>(a.z) + rep * a.z_rs;
   const T *res = a.res ? reinterpret_cast<const T *>(a.res) + rep * a.z_rs : nullptr;
   T *out = reinterpret_cast<T *>(a.a) + rep * a.z_rs;
   const float *mean = a.mean + (int64_t)rep * a.nstat, *rstd = a.rstd + (int64_t)rep * a.nstat;
   const float *gamma = a.theta + rep * a.P + a.g_off, *beta = a.theta + rep * a.P + a.b_off;
-  const uint32_t stride = gridDim.x * 256u;
+  constexpr uint32_t stride = 256u;
   int kc = -1, kb = -1;  // channel vector and example of the cached values
   float km[VEC], kr[VEC], kg[VEC], kbt[VEC];
-  for (uint32_t i0 = blockIdx.x * 256u + threadIdx.x; i0 < total; i0 += kApplyUnroll * stride) {
+  {
+    const uint32_t i0 = blockIdx.x * (256u * kApplyUnroll) + threadIdx.x;
     V16<T> zv[kApplyUnroll], rv[kApplyUnroll];
 #pragma unroll
     for (int u = 0; u < kApplyUnroll; ++u) {
@@ -346,8 +339,8 @@ norm_apply_fwd_kernel(NormArgs a, uint32_t total) {
     for (int u = 0; u < kApplyUnroll; ++u) {
       const uint32_t i = i0 + u * stride;
       if (i >= total) break;
-      const uint32_t p = i / CV;
-      const int cv = (int)(i - p * CV), b = (int)(p / HW);
+      const uint32_t p = fdiv(i, fcv);  // pixel, then its example
+      const int cv = (int)(i - p * CV), b = (int)fdiv(p, fhw);
       if (cv != kc || (a.groups && b != kb)) {
         kc = cv, kb = b;
 #pragma unroll
@@ -372,10 +365,10 @@ norm_apply_fwd_kernel(NormArgs a, uint32_t total) {
 // times the per-channel sums.
 template <typename T>
 __global__ void __launch_bounds__(256)
-norm_apply_bwd_kernel(NormArgs a, uint32_t total) {
+norm_apply_bwd_kernel(NormArgs a, uint32_t total, FastDiv fcv, FastDiv fhw) {
   constexpr int VEC = ElemT<T>::VEC;
   const int rep = replica_of(a.rmap, blockIdx.y);
-  const int CV = a.Ch / VEC, HW = a.H * a.W;
+  const int CV = a.Ch / VEC;
   const T *z = reinterpret_cast<const T *>(a.z) + rep * a.z_rs;
   const T *du = reinterpret_cast<const T *>(a.du) + rep * a.z_rs;
   T *dz = reinterpret_cast<T *>(a.dz) + rep * a.z_rs;
@@ -383,10 +376,11 @@ norm_apply_bwd_kernel(NormArgs a, uint32_t total) {
   const float *gamma = a.theta + rep * a.P + a.g_off;
   const double *sums = a.sums + (int64_t)rep * a.nstat * 2;
   const double n = a.groups ? (double)a.H * a.W * (a.Ch / a.groups) : (double)a.Bt * a.H * a.W;
-  const uint32_t stride = gridDim.x * 256u;
+  constexpr uint32_t stride = 256u;
   int kc = -1, kb = -1;
   float km[VEC], kr[VEC], kg[VEC], k1[VEC], k2[VEC];
-  for (uint32_t i0 = blockIdx.x * 256u + threadIdx.x; i0 < total; i0 += kApplyUnroll * stride) {
+  {
+    const uint32_t i0 = blockIdx.x * (256u * kApplyUnroll) + threadIdx.x;
     V16<T> zv[kApplyUnroll], gv[kApplyUnroll];
 #pragma unroll
     for (int u = 0; u < kApplyUnroll; ++u) {
@@ -400,8 +394,8 @@ norm_apply_bwd_kernel(NormArgs a, uint32_t total) {
     for (int u = 0; u < kApplyUnroll; ++u) {
       const uint32_t i = i0 + u * stride;
       if (i >= total) break;
-      const uint32_t p = i / CV;
-      const int cv = (int)(i - p * CV), b = (int)(p / HW);
+      const uint32_t p = fdiv(i, fcv);  // pixel, then its example
+      const int cv = (int)(i - p * CV), b = (int)fdiv(p, fhw);
       if (cv != kc || (a.groups && b != kb)) {
         kc = cv, kb = b;
 #pragma unroll
@@ -434,13 +428,14 @@ template <typename T>
 hipError_t norm_fwd_t(const NormArgs &a, hipStream_t s) {
   constexpr int VEC = ElemT<T>::VEC;
   const uint32_t total = (uint32_t)((int64_t)a.Bt * a.H * a.W * (a.Ch / VEC));
+  const FastDiv fcv = make_fastdiv((uint32_t)(a.Ch / VEC)), fhw = make_fastdiv((uint32_t)(a.H * a.W));
   if (a.groups) {
     hipLaunchKernelGGL((group_reduce_kernel<T, 0>), dim3(a.Bt, a.C), dim3(256), 0, s, a);
   } else {
-    hipLaunchKernelGGL((chan_reduce_kernel<T, 0>), dim3(a.chunks, a.C), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((chan_reduce_kernel<T, 0>), dim3(a.chunks, a.C), dim3(256), 0, s, a, fhw);
     hipLaunchKernelGGL((chan_finish_kernel<0>), dim3((a.Ch + kFinishCh - 1) / kFinishCh, a.C), dim3(256), 0, s, a);
   }
-  hipLaunchKernelGGL((norm_apply_fwd_kernel<T>), dim3(apply_blocks(total), a.C), dim3(256), 0, s, a, total);
+  hipLaunchKernelGGL((norm_apply_fwd_kernel<T>), dim3(apply_blocks(total), a.C), dim3(256), 0, s, a, total, fcv, fhw);
   return hipGetLastError();
 }
 
@@ -448,10 +443,11 @@ template <typename T>
 hipError_t norm_bwd_t(const NormArgs &a, hipStream_t s) {
   constexpr int VEC = ElemT<T>::VEC;
   const uint32_t total = (uint32_t)((int64_t)a.Bt * a.H * a.W * (a.Ch / VEC));
-  hipLaunchKernelGGL((chan_reduce_kernel<T, 1>), dim3(a.chunks, a.C), dim3(256), 0, s, a);
+  const FastDiv fcv = make_fastdiv((uint32_t)(a.Ch / VEC)), fhw = make_fastdiv((uint32_t)(a.H * a.W));
+  hipLaunchKernelGGL((chan_reduce_kernel<T, 1>), dim3(a.chunks, a.C), dim3(256), 0, s, a, fhw);
   hipLaunchKernelGGL((chan_finish_kernel<1>), dim3((a.Ch + kFinishCh - 1) / kFinishCh, a.C), dim3(256), 0, s, a);
   if (a.groups) hipLaunchKernelGGL((group_reduce_kernel<T, 1>), dim3(a.Bt, a.C), dim3(256), 0, s, a);
-  hipLaunchKernelGGL((norm_apply_bwd_kernel<T>), dim3(apply_blocks(total), a.C), dim3(256), 0, s, a, total);
+  hipLaunchKernelGGL((norm_apply_bwd_kernel<T>), dim3(apply_blocks(total), a.C), dim3(256), 0, s, a, total, fcv, fhw);
   return hipGetLastError();
 }
 
