@@ -23,7 +23,9 @@ A second pass right after it records hipEvents around every kernel launch
 dominant kernel's algorithmic work over that time against the MI355X peak,
 and next to it the same fraction from the committed rocprofv3 kernel trace
 (profiles/profile.json) with the MFMA busy counters, when the kernel's source
-is unchanged since they were taken.  The CPU oracle is timed on a bounded
+is unchanged since they were taken; `step_roofline` puts the whole step
+against the roofline (every kernel's algorithmic work at the peak that bounds
+it, over the measured time per step).  The CPU oracle is timed on a bounded
 sample on the host cores.
 """
 from __future__ import annotations
@@ -274,6 +276,18 @@ def measure(name, steps, warmup, timing_steps, cpu_seconds, with_cpu=True, with_
                  if busy and all(b is not None for b, _ in busy) else None)
     fuse = stats.get("fuse")
     fusion_gbs = fuse["bytes"] / (fuse["ms"] * 1e-3) / 1e9 if fuse else None
+    # the whole step against the roofline: every kernel's algorithmic work at
+    # the peak that bounds it (MFMA FLOPs or HBM bytes, whichever takes
+    # longer), per step (the fusion at its share of the timed window), over
+    # the measured wall time per step
+    def ideal_ms(v):
+        return 1e3 * max(v["flops"] / (peak_tf * 1e12), v["bytes"] / (PEAK_HBM_GBS * 1e9))
+    ideal = sum(ideal_ms(v) for k, v in stats.items() if k != "fuse") / timing_steps
+    if fuse:
+        ideal += ideal_ms(fuse) / fuse["launches"] * fusions / steps
+    step_roof = {"ideal_ms_per_step": round(ideal, 4), "frac": round(ideal / (dt * 1e3 / steps), 4),
+                 "definition": "sum over kernels of max(algorithmic FLOPs / MFMA peak, algorithmic bytes / HBM "
+                               "peak) per step, over the measured wall time per step"}
     kernel_ms = sum(v["ms"] for v in stats.values())
     for k, v in sorted(stats.items(), key=lambda kv: -kv[1]["ms"]):
         rate = f"{v['flops'] / (v['ms'] * 1e-3) / 1e12:8.1f} TFLOP/s" if v["flops"] > 0 else ""
@@ -292,6 +306,7 @@ def measure(name, steps, warmup, timing_steps, cpu_seconds, with_cpu=True, with_
         "conv_tflops": round(conv_tf, 2),
         "fusion_gbs": None if fusion_gbs is None else round(fusion_gbs, 1),
         "kernel_ms_per_step": round(kernel_ms / timing_steps, 4),
+        "step_roofline": step_roof,
         "roofline": roof,
     }
     if with_extras and not args.no_schedule_control:

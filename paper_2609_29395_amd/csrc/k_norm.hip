@@ -15,10 +15,13 @@
 // Batch norm also updates its replica's running statistics (momentum 0.1,
 // unbiased variance for the running value) and batch counter.
 //
-// Every sum runs in fp64 in a fixed order (per-thread strides, then thread
-// order, then chunk order), so results do not depend on scheduling.  A
-// thread owns one 16-byte vector of VEC channels; a workgroup has 256 / (Ch /
-// VEC) pixel lanes.
+// Every sum runs in fp64 in a fixed order (per-thread pixel strides, then
+// pixel-lane order within a workgroup; across the chunks of a channel
+// reduction, eight strided chunk lanes, then lane order), so results do not
+// depend on scheduling or on which replicas share a launch.  A thread owns
+// one 16-byte vector of VEC channels; a workgroup has 256 / (Ch / VEC) pixel
+// lanes.  Chunks shrink for small tensors (16 to 256 pixels) so that late,
+// low-resolution layers still spread over the chip.
 #include "runtime.h"
 
 namespace {
