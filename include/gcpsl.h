@@ -399,9 +399,16 @@ int gcpsl_cluster_sizes(gcpsl_ctx *ctx, int64_t *sizes);
  * every sampled step), "act<i>" (output of layer i, [C][B][...]),
  * "gpre<i>" (gradient w.r.t. conv layer i's pre-activation), "gin<i>"
  * (gradient w.r.t. the input of conv layer i when layer i-1 is a max pool),
- * "dh" ([C][B][channels] fp32 gradient of the pooled feature), "grad"
- * ([C][P] fp32 last gradient).  dtype receives GCPSL_F32, GCPSL_BF16 or -1
- * for int32.  EINVAL on an unknown name.
+ * "route<j>" (routing codes of max-pool layer j, [C][B][H/2][W/2][channels]
+ * uint8: the row-major window position 0..3 of the first maximum, 4 where
+ * the maximum is not positive and no gradient passes), "dh" ([C][B][channels]
+ * fp32 gradient of the pooled feature), "grad" ([C][P] fp32 last gradient).
+ * A bf16 conv whose ReLU output feeds a stored 2 x 2 max pool and then
+ * another conv (the 32 x 32, 32 -> 64 image-side layer) keeps only the pool's
+ * output and "route<j>": its "act<i>" and "gpre<i>" are not stored (its
+ * gradient is "gin<j+1>" routed through the codes).  dtype receives
+ * GCPSL_F32, GCPSL_BF16, -1 for int32 or -2 for uint8.  EINVAL on an unknown
+ * or unstored name.
  */
 int gcpsl_tensor(gcpsl_ctx *ctx, const char *name, void **ptr, int64_t *numel, int32_t *dtype);
 

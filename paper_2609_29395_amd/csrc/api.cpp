@@ -54,6 +54,12 @@ struct LayerInfo {
   int64_t st_off = 0;         // batch norm: running statistics in the state vector
   size_t mean_off = 0, rstd_off = 0, sums_off = 0;
   int blk = -1;               // GCPSL_BLOCK: its entry in Plan::blocks
+  // conv followed by a stored 2 x 2 max pool and another conv: the forward
+  // writes the pool's routing codes (one byte per pooled element) instead of
+  // the unpooled output, and the layer's gradients take the next conv's
+  // input gradient routed through them (no unpooled output or gradient)
+  bool pcode = false;
+  size_t code_off = 0;
 };
 
 // A ResNet basic block (GCPSL_BLOCK) as internal layers, each with its own
@@ -359,6 +365,30 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
     const int64_t chunks = (rs + norm_chunk(rs, C) - 1) / norm_chunk(rs, C);
     npart = std::max(npart, (size_t)(C * chunks * l.Co * 2));
   };
+  // routing codes for conv i (LayerInfo::pcode): bf16, ReLU, a stored max
+  // pool then a conv after it, and forward, input- and weight-gradient
+  // kernels that take the codes for the layer's shape
+  auto pool_codes = [&](int i) {
+    const LayerInfo &l = p.ly[i];
+    if (p.dtype != GCPSL_BF16 || l.spec.kind != GCPSL_CONV3X3 || l.no_relu || (l.spec.flags & GCPSL_RESIDUAL) ||
+        i + 2 >= n || (i == 0 && p.col0))
+      return false;
+    if (p.ly[i + 1].spec.kind != GCPSL_MAXPOOL2 || (p.head_maxpool && i + 1 == n - 3) ||
+        p.ly[i + 2].spec.kind != GCPSL_CONV3X3)
+      return false;
+    ConvArgs f{};
+    f.epi = EPI_FWD;
+    f.taps = 9;
+    f.H = l.H; f.W = l.W; f.Csrc = l.Ci; f.N = l.Co; f.K = 9 * l.Ci; f.Kp = round_up(9 * l.Ci, bk_tile);
+    if (!conv_fuses_pool(p.dtype, f) || !conv_pool_codes(p.dtype, f)) return false;
+    if (i > 0) {
+      ConvArgs g = f;
+      g.epi = EPI_DGRAD;
+      g.Csrc = l.Co; g.N = l.Ci; g.K = 9 * l.Co; g.Kp = round_up(9 * l.Co, bk_tile);
+      if (!conv_pool_codes(p.dtype, g)) return false;
+    }
+    return wgrad_pool_codes(p.dtype, l.Co, l.Ci, l.H, l.W, 9);
+  };
   for (int i = 0; i < n; ++i) {
     LayerInfo &l = p.ly[i];
     const int kind = l.spec.kind;
@@ -422,7 +452,11 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
       norm_buffers(l);
       continue;
     }
-    if (kind == GCPSL_CONV3X3 || (kind == GCPSL_MAXPOOL2 && !(p.head_maxpool && i == n - 3))) {
+    l.pcode = pool_codes(i);
+    if (l.pcode) {
+      l.act_rs = (int64_t)B * l.Ho * l.Wo * l.Co;
+      l.code_off = take((size_t)C * l.act_rs / 4);
+    } else if (kind == GCPSL_CONV3X3 || (kind == GCPSL_MAXPOOL2 && !(p.head_maxpool && i == n - 3))) {
       l.stored = true;
       l.act_rs = (int64_t)B * l.Ho * l.Wo * l.Co;
       l.act_off = take((size_t)p.esz * C * l.act_rs);
@@ -435,7 +469,7 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
       const int64_t rs = (int64_t)B * l.H * l.W;
       if (!small_enough(rs, l.Ci, l.Co, 9))
         return gcpsl_fail(GCPSL_EUNSUPPORTED, "per-replica layer tensors must stay below 2 GiB");
-      l.gpre_off = take((size_t)p.esz * C * rs * l.Co);
+      if (!l.pcode) l.gpre_off = take((size_t)p.esz * C * rs * l.Co);
       if (i > 0 && p.ly[i - 1].spec.kind == GCPSL_MAXPOOL2) {
         l.has_gin = true;
         l.gin_off = take((size_t)p.esz * C * rs * l.Ci);
@@ -1009,6 +1043,11 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
         a.pool_rs = p.ly[i + 1].act_rs;
         pool_done = conv_fuses_pool(p.dtype, a);
         if (!pool_done) a.pool_out = nullptr;
+        if (l.pcode) {  // the pool and its routing codes only
+          if (!pool_done) return gcpsl_fail(GCPSL_EUNSUPPORTED, "routing codes without the fused pool");
+          a.pool_code = reinterpret_cast<uint8_t *>(ws + l.code_off);
+          a.out = nullptr;
+        }
       }
       // the head's mean pooling right after this conv: written by the conv
       // kernel itself where it supports that
@@ -1023,8 +1062,10 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
       std::string lab;
       const double M = (double)B * l.H * l.W;
       const double fl = 2.0 * C * M * l.Co * 9.0 * l.Ci;
-      const double by = (double)C * (p.esz * (M * l.Ci + (double)l.Co * 9 * l.Ci + M * l.Co * (a.res ? 2 : 1) +
-                                                (pool_done ? M / 4 * l.Co : 0.0)) + 4.0 * l.Co);
+      const double by = (double)C * (p.esz * (M * l.Ci + (double)l.Co * 9 * l.Ci +
+                                                (l.pcode ? 0.0 : M * l.Co * (a.res ? 2 : 1)) +
+                                                (pool_done ? M / 4 * l.Co : 0.0)) +
+                                     (l.pcode ? M / 4 * l.Co : 0.0) + 4.0 * l.Co);
       size_t t_ = tbegin(ctx, s);
       LAUNCH(launch_conv(p.dtype, a, s, &lab));
       tend(ctx, s, t_, lab, fl, by);
@@ -1145,15 +1186,21 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
       continue;
     }
     // weight and bias gradient
+    // the layer's output gradient: gpre, or (routing codes) the next conv's
+    // input gradient at the pool's output with the codes
+    const void *gsrc = l.pcode ? (const void *)(ws + p.ly[i + 2].gin_off) : (const void *)(ws + l.gpre_off);
+    const uint8_t *gcode = l.pcode ? reinterpret_cast<const uint8_t *>(ws + l.code_off) : nullptr;
+    const int64_t g_rs = (int64_t)B * l.H * l.W * l.Co / (l.pcode ? 4 : 1);
     WgradArgs w{};
-    w.g = ws + l.gpre_off;
+    w.g = gsrc;
+    w.gcode = gcode;
     w.x = input_of(i);
     const bool col = i == 0 && p.col0;
     w.Bt = B; w.H = l.H; w.W = l.W; w.Co = l.Co;
     w.Ci = col ? p.Kc : l.Ci;
     w.taps = col ? 1 : 9;
     w.nw = 9 * l.Ci;
-    w.g_rs = (int64_t)B * l.H * l.W * l.Co;
+    w.g_rs = g_rs;
     w.x_rs = (int64_t)B * l.H * l.W * w.Ci;
     w.C = C;
     w.rmap = rmap;
@@ -1170,7 +1217,8 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
       std::string lab;
       const double M = (double)B * l.H * l.W;
       const double fl = 2.0 * C * M * l.Co * 9.0 * l.Ci;
-      const double by = (double)C * (p.esz * M * (l.Co + l.Ci) + 4.0 * l.splits * (l.nw + l.Co));
+      const double gby = l.pcode ? (p.esz + 1.0) * M / 4 * l.Co : p.esz * M * l.Co;
+      const double by = (double)C * (gby + p.esz * M * l.Ci + 4.0 * l.splits * (l.nw + l.Co));
       size_t t_ = tbegin(ctx, s);
       LAUNCH(launch_wgrad(p.dtype, w, s, &lab));
       tend(ctx, s, t_, lab, fl, by);
@@ -1184,14 +1232,15 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
     const LayerInfo &prev = p.ly[i - 1];
     const bool through_pool = prev.spec.kind == GCPSL_MAXPOOL2;
     ConvArgs a{};
-    a.src = ws + l.gpre_off;
+    a.src = gsrc;
+    a.pool_code = const_cast<uint8_t *>(gcode);
     a.wt = ws + l.wd_off;
     a.out = through_pool ? ws + l.gin_off : ws + prev.gpre_off;
     a.bias = nullptr;
     a.res = (l.spec.flags & GCPSL_RESIDUAL) ? a.src : nullptr;
     a.mask = through_pool ? nullptr : (const void *)(ws + prev.act_off);
     a.Bt = B; a.H = l.H; a.W = l.W; a.Csrc = l.Co; a.N = l.Ci; a.K = 9 * l.Co; a.Kp = l.Kdp;
-    a.src_rs = (int64_t)B * l.H * l.W * l.Co;
+    a.src_rs = g_rs;
     a.wt_rs = (int64_t)l.Ci * l.Kdp;
     a.out_rs = (int64_t)B * l.H * l.W * l.Ci;
     a.bias_rs = 0;
@@ -1203,14 +1252,16 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
       std::string lab;
       const double M = (double)B * l.H * l.W;
       const double fl = 2.0 * C * M * l.Ci * 9.0 * l.Co;
-      const double by = (double)C * p.esz *
-                        (M * l.Co + (double)l.Ci * 9 * l.Co + M * l.Ci * (1 + (a.res ? 1 : 0) + (a.mask ? 1 : 0)));
+      const double gby = l.pcode ? (p.esz + 1.0) * M / 4 * l.Co : p.esz * M * l.Co;
+      const double by = (double)C * (gby + p.esz * ((double)l.Ci * 9 * l.Co +
+                                                   M * l.Ci * (1 + (a.res ? 1 : 0) + (a.mask ? 1 : 0))));
       size_t t_ = tbegin(ctx, s);
       LAUNCH(launch_conv(p.dtype, a, s, &lab));
       tend(ctx, s, t_, lab, fl, by);
     }
     if (through_pool) {
       const LayerInfo &pc = p.ly[i - 2];
+      if (!pc.pcode)  // (with routing codes the layer below reads gin itself)
       LAUNCH_T("maxpool_bwd", 0.0, 2.25 * p.esz * (double)C * B * pc.Ho * pc.Wo * pc.Co,
                launch_maxpool_bwd(p.dtype, ws + pc.act_off, ws + l.gin_off, ws + pc.gpre_off, C, rmap, B, pc.Ho, pc.Wo,
                                   pc.Co, s));
@@ -1482,9 +1533,10 @@ extern "C" int gcpsl_tensor(gcpsl_ctx *ctx, const char *name, void **ptr, int64_
       continue;
     }
     if (nm == "act" + k && l.stored) return put(l.act_off, (int64_t)p.C * l.act_rs, p.dtype);
+    if (l.pcode && nm == "route" + std::to_string(i + 1)) return put(l.code_off, (int64_t)p.C * l.act_rs / 4, -2);
     if (l.spec.kind == GCPSL_CONV3X3 || is_norm(l.spec.kind)) {
       const int64_t rs = (int64_t)p.B * l.H * l.W;
-      if (nm == "gpre" + k) return put(l.gpre_off, p.C * rs * l.Co, p.dtype);
+      if (nm == "gpre" + k && !l.pcode) return put(l.gpre_off, p.C * rs * l.Co, p.dtype);
       if (nm == "gin" + k && l.has_gin) return put(l.gin_off, p.C * rs * l.Ci, p.dtype);
     }
   }

@@ -695,6 +695,10 @@ void wgrad_tile(int dtype, int Co, int ncols, int *bm, int *bn) {
 }
 
 hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s, std::string *label) {
+  // routing codes: only the image-side kernels take them
+  if (a.pool_code)
+    return (conv_pool_codes(dtype, a) && (a.epi == EPI_DGRAD || a.pool_out)) ? launch_conv_img(a, s, label)
+                                                                              : hipErrorInvalidValue;
   if (a.taps == 9 && a.epi == EPI_FWD && a.res == nullptr && conv_im3_ok(dtype, a.Csrc, a.N, a.H, a.W))
     return launch_conv_col(a, s, label);
   if (conv_img_ok(dtype, a)) return launch_conv_img(a, s, label);
@@ -706,6 +710,11 @@ hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s, std::string 
 }
 
 hipError_t launch_wgrad(int dtype, const WgradArgs &a, hipStream_t s, std::string *label) {
+  if (a.gcode)
+    return (wgrad_pool_codes(dtype, a.Co, a.Ci, a.H, a.W, a.taps) && wgrad_lds_ok(dtype, a.Co, a.Ci) &&
+            a.chunk % 64 == 0)
+               ? launch_wgrad_lds(a, s, label)
+               : hipErrorInvalidValue;
   if ((wgrad_col_ok(dtype, a.Co, a.Ci, a.taps) ||
        (a.taps == 9 && conv_im3_ok(dtype, a.Ci, a.Co, a.H, a.W))) && a.chunk % 128 == 0)
     return launch_wgrad_col(a, s, label);

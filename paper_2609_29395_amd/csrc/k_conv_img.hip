@@ -18,7 +18,12 @@
 // as B (32 k x 16 pixels), so each lane ends with 4 consecutive channels of
 // one pixel; the epilogue regroups them through LDS into whole pixel rows
 // and, when the layer is followed by a 2 x 2 max pool, also writes the
-// pooled rows (a tile's eight image rows hold four whole pooling rows).  Halo row R (pixel column w'
+// pooled rows (a tile's eight image rows hold four whole pooling rows), and
+// then, given a code buffer, the pool's routing codes in place of the
+// unpooled rows.  The input gradient of such a layer starts from the pooled
+// gradient: its halo pieces are loaded with their codes into registers and
+// written to LDS routed (the gradient where the code names the pixel's
+// window position, zero elsewhere).  Halo row R (pixel column w'
 // of its image row) keeps its 16-byte chunk c at c ^ (w' mod chunks per
 // row); weight row n keeps chunk kc at kc ^ (n & 7) (eight-chunk groups).
 #include "runtime.h"
@@ -91,13 +96,22 @@ conv_img_kernel(ConvArgs a, int MT) {
   const bf16_t *src = reinterpret_cast<const bf16_t *>(a.src) + rep * a.src_rs;
   const bf16_t *wt = reinterpret_cast<const bf16_t *>(a.wt) + rep * a.wt_rs;
 
-  // ---- copies: halo image and weight matrix, 16 bytes per lane, LDS-direct
+  // ---- copies: halo image and weight matrix, 16 bytes per lane, LDS-direct;
+  // dgrad from a pooled gradient: the halo pieces are routed through the
+  // pool's codes in registers and written to the same LDS slots
+  const bool pooled = EPI == EPI_DGRAD && a.pool_code != nullptr;
+  u32x4 gv[CF::HQ];  // pooled: gradient piece, its 8 codes, window position
+  u32x2 cv[CF::HQ];
+  int kw[CF::HQ];
   {
     const __amdgpu_buffer_rsrc_t rss = rsrc(src, (uint32_t)((int64_t)M * CS * 2));
     const __amdgpu_buffer_rsrc_t rsw = rsrc(wt, (uint32_t)CF::W_BYTES);
+    const uint8_t *cd = pooled ? a.pool_code + rep * a.src_rs : nullptr;
+    const int img0 = m0 / (IMG * IMG) * (IMG / 2) * (IMG / 2);  // first pooled pixel of the tile's image
 #pragma unroll
     for (int q = 0; q < CF::HQ; ++q) {
       const int byte = q * NTHR * 16 + wave * 1024;  // this wave's 1 KB of the halo region
+      kw[q] = -1;
       if (byte < CF::H_BYTES) {
         const int j = byte / 16 + lane;  // 16-byte slot
         const int R = j / CF::CPR, cs = j % CF::CPR;
@@ -105,8 +119,19 @@ conv_img_kernel(ConvArgs a, int MT) {
         const int c = cs ^ (wp & (CF::CPR - 1));
         const int h = h0 - 1 + hp, w = wp - 1;
         const bool ok = R < HPIX && (unsigned)h < (unsigned)IMG && (unsigned)w < (unsigned)IMG;
-        const uint32_t off = ok ? (uint32_t)((m0 + (hp - 1) * IMG + w) * CS + 8 * c) * 2u : kOob;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rss, LDS_PTR(smem + byte), 16, off, 0, 0, 0);
+        if (pooled) {
+          gv[q] = u32x4{0u, 0u, 0u, 0u};
+          cv[q] = u32x2{0u, 0u};
+          if (ok) {
+            const int pp = (img0 + (h >> 1) * (IMG / 2) + (w >> 1)) * CS + 8 * c;
+            gv[q] = *reinterpret_cast<const u32x4 *>(src + pp);
+            cv[q] = *reinterpret_cast<const u32x2 *>(cd + pp);
+            kw[q] = ((h & 1) << 1) | (w & 1);
+          }
+        } else {
+          const uint32_t off = ok ? (uint32_t)((m0 + (hp - 1) * IMG + w) * CS + 8 * c) * 2u : kOob;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rss, LDS_PTR(smem + byte), 16, off, 0, 0, 0);
+        }
       }
     }
 #pragma unroll
@@ -118,6 +143,25 @@ conv_img_kernel(ConvArgs a, int MT) {
         const int kc = cs ^ (row & 7);
         const uint32_t off = (uint32_t)(row * CF::KP + 8 * kc) * 2u;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsw, LDS_PTR(smem + CF::H_BYTES + byte), 16, off, 0, 0, 0);
+      }
+    }
+  }
+  if (pooled) {
+    // value e of a piece passes where its code names this pixel's window
+    // position (a zero-border or out-of-image slot keeps kw = -1: zeros)
+#pragma unroll
+    for (int q = 0; q < CF::HQ; ++q) {
+      const int byte = q * NTHR * 16 + wave * 1024;
+      if (byte < CF::H_BYTES) {
+        const uint32_t k = (uint32_t)kw[q];
+        u32x4 v;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const uint32_t cb = cv[q][d >> 1] >> (16 * (d & 1));  // codes of channels 2d, 2d + 1
+          const uint32_t keep = ((cb & 0xffu) == k ? 0x0000ffffu : 0u) | (((cb >> 8) & 0xffu) == k ? 0xffff0000u : 0u);
+          v[d] = gv[q][d] & keep;
+        }
+        *reinterpret_cast<u32x4 *>(smem + byte + lane * 16) = v;
       }
     }
   }
@@ -212,8 +256,11 @@ conv_img_kernel(ConvArgs a, int MT) {
     mv[q] = msk ? *reinterpret_cast<const u32x4 *>(msk + (int64_t)(pbase + px) * NO + 8 * c)
                 : u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u};
   }
+  // forward with pool codes: only the pool and its codes are written
+  const bool unpooled = !(EPI == EPI_FWD && a.pool_out && a.pool_code);
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
+    if (!unpooled) break;
     const int i2 = q * 64 + lane, px = i2 / OCH, c = i2 % OCH;
     u32x4 v;
     const uint32_t ad = stg + (uint32_t)(px * OROW + ((c ^ (px & (OCH - 1))) * 16));
@@ -242,21 +289,29 @@ conv_img_kernel(ConvArgs a, int MT) {
         const uint32_t ad = ((e >> 1) ? r1 : r0) + (uint32_t)(px * OROW + ((c ^ (px & (OCH - 1))) * 16));
         asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(q4[e]) : "v"(ad) : "memory");
       }
+      // window position e = 2 dh + dw (row-major); the first maximum under
+      // strict comparison, code 4 where it is not positive
       u32x4 z;
+      u32x2 code = u32x2{0u, 0u};
 #pragma unroll
       for (int d = 0; d < 4; ++d) {
-        uint32_t lo = q4[0][d] & 0xffffu, hi = q4[0][d] >> 16;
+        uint32_t lo = q4[0][d] & 0xffffu, hi = q4[0][d] >> 16, alo = 0u, ahi = 0u;
 #pragma unroll
         for (int e = 1; e < 4; ++e) {
           const uint32_t l2 = q4[e][d] & 0xffffu, h2 = q4[e][d] >> 16;
-          if (bf2f(l2) > bf2f(lo)) lo = l2;
-          if (bf2f(h2) > bf2f(hi)) hi = h2;
+          if (bf2f(l2) > bf2f(lo)) lo = l2, alo = (uint32_t)e;
+          if (bf2f(h2) > bf2f(hi)) hi = h2, ahi = (uint32_t)e;
         }
         z[d] = lo | (hi << 16);
+        if (!(bf2f(lo) > 0.f)) alo = 4u;
+        if (!(bf2f(hi) > 0.f)) ahi = 4u;
+        code[d >> 1] |= (alo | (ahi << 8)) << (16 * (d & 1));
       }
       bf16_t *zo = reinterpret_cast<bf16_t *>(a.pool_out) + rep * a.pool_rs;
       const int b = m0 / (IMG * IMG), hz = h0 / 2 + (wave >> 1);
-      *reinterpret_cast<u32x4 *>(zo + ((int64_t)(b * (IMG / 2) + hz) * (IMG / 2) + pw) * NO + 8 * c) = z;
+      const int64_t zi = ((int64_t)(b * (IMG / 2) + hz) * (IMG / 2) + pw) * NO + 8 * c;
+      *reinterpret_cast<u32x4 *>(zo + zi) = z;
+      if (a.pool_code) *reinterpret_cast<u32x2 *>(a.pool_code + rep * a.pool_rs + zi) = code;
     }
   }
 }
@@ -414,6 +469,8 @@ hipError_t launch_conv_col(const ConvArgs &a, hipStream_t s, std::string *label)
 }
 
 bool conv_fuses_pool(int dtype, const ConvArgs &a) { return a.epi == EPI_FWD && conv_img_ok(dtype, a); }
+
+bool conv_pool_codes(int dtype, const ConvArgs &a) { return conv_img_ok(dtype, a); }
 
 bool conv_img_ok(int dtype, const ConvArgs &a) {
   return dtype == GCPSL_BF16 && a.taps == 9 && a.H == IMG && a.W == IMG && (a.Csrc == 32 || a.Csrc == 64) &&

@@ -565,30 +565,100 @@ constexpr int SA = A_BYTES / (NTHR * 16), SB = B_BYTES / (NTHR * 16), CPT = SA +
 constexpr int QROWA = NTHR * 16 / ROWA;     // g rows between a thread's copies
 constexpr int FROW = HP * ROWB;             // bytes between halo image rows
 constexpr int NF = 9;                       // column fragments per wave
+// routed g tile (POOL): the pooled gradient row and its codes in the B
+// region's tail, after the halo rows and 32 zero pieces
+constexpr int PROW_G = (IMG / 2) * CO * 2;  // 2 KB: one pooled row of gradient
+constexpr int PROW_C = (IMG / 2) * CO;      // 1 KB: its codes
+constexpr int RAW_G = NTHR * 16 + 1024, RAW_C = RAW_G + PROW_G, IDLE = RAW_C + PROW_C;
 static_assert(HROWS * ROWB <= B_BYTES && SA == 1 && SB == 2 && QROWA % 16 == 0, "image weight-gradient layout");
+static_assert(HROWS * ROWB <= RAW_G && IDLE + 4 * 1024 <= B_BYTES && PROW_G == 2048 && PROW_C == 1024,
+              "routed g tile in the B region's tail");
 }  // namespace wi
 __device__ __forceinline__ int wisw(int wp) { return (wp >> 1) & 3; }
 
-template <int NST>
-__device__ __forceinline__ void wi_issue(int kt, char *stage0, const void *G, const void *X, uint32_t gbytes,
-                                         uint32_t xbytes, int p_begin, int arow, int acol, const int (&hrel)[wi::SB],
-                                         const int (&hh)[wi::SB]) {
+// Copies of k tile kt into stage kt % NST.  Plain: the g tile (A region)
+// and the input halo rows (B region, two copies per thread).  POOL: the g
+// tile is routed in LDS (wi_route) from the pooled gradient and its codes,
+// which the second copy brings into the B region's idle tail: waves 0 and 1
+// the tile's pooled gradient row (2 KB at RAW_G), wave 2 its codes (1 KB at
+// RAW_C), wave 7 the last 32 halo pieces (and 32 zero pieces after them),
+// waves 3 .. 6 zero copies into the rest of the tail.  Each copy instruction
+// stays with one source buffer per wave.  The second copy is issued first,
+// so that the routed tile can be waited for ahead of the halo copies.
+template <int NST, bool POOL>
+__device__ __forceinline__ void wi_issue(int kt, char *smem, int wave, int lane, const void *G, const void *X,
+                                         const void *code, uint32_t gbytes, uint32_t xbytes, int p_begin, int arow,
+                                         int acol, const int (&hrel)[wi::SB], const int (&hh)[wi::SB]) {
   const __amdgpu_buffer_rsrc_t rsg = rsrc(G, gbytes);
   const __amdgpu_buffer_rsrc_t rsx = rsrc(X, xbytes);
-  char *sa = stage0 + (kt % NST) * wi::STAGE;
+  char *st = smem + (kt % NST) * wi::STAGE;
   const int pt = p_begin + kt * wi::BK;
-#pragma unroll
-  for (int q = 0; q < wi::SA; ++q) {
-    const uint32_t off = ((uint32_t)(pt + arow + q * wi::QROWA) * (uint32_t)wi::CO + (uint32_t)acol) * 2u;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsg, LDS_PTR(sa + q * wi::NTHR * 16), 16, off, 0, 0, 0);
-  }
   const int h0 = (pt / wi::IMG) % wi::IMG;  // first image row of the tile
-#pragma unroll
-  for (int q = 0; q < wi::SB; ++q) {
+  auto halo_off = [&](int q) {
     const bool ok = hh[q] >= 0 && (unsigned)(h0 - 1 + hh[q]) < (unsigned)wi::IMG;
-    const uint32_t off = ok ? (uint32_t)(pt * wi::CI + hrel[q]) * 2u : kOob;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, LDS_PTR(sa + wi::A_BYTES + q * wi::NTHR * 16), 16, off, 0, 0, 0);
+    return ok ? (uint32_t)(pt * wi::CI + hrel[q]) * 2u : kOob;
+  };
+  if constexpr (!POOL) {
+#pragma unroll
+    for (int q = 0; q < wi::SA; ++q) {
+      const uint32_t off = ((uint32_t)(pt + arow + q * wi::QROWA) * (uint32_t)wi::CO + (uint32_t)acol) * 2u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsg, LDS_PTR(st + wave * 1024 + q * wi::NTHR * 16), 16, off, 0, 0, 0);
+    }
+#pragma unroll
+    for (int q = 0; q < wi::SB; ++q)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, LDS_PTR(st + wi::A_BYTES + wave * 1024 + q * wi::NTHR * 16), 16,
+                                               halo_off(q), 0, 0, 0);
+  } else {
+    static_assert(wi::SB == 2 && wi::NTHR == 512 && wi::HROWS * wi::ROWB == wi::NTHR * 16 + 32 * 16,
+                  "the second copy holds 32 halo pieces");
+    const int prow = pt / wi::BK;  // pooled row of the replica (a tile is two image rows)
+    char *sb = st + wi::A_BYTES;
+    // (offsets from an opaque copy of the thread index, recomputed at each
+    // issue rather than held in registers across the k loop)
+    int t16 = (int)threadIdx.x * 16;
+    asm volatile("" : "+v"(t16));
+    if (wave == 7) {
+      // halo pieces 512 + lane = halo rows 128 + lane / 4: halo image row 3
+      // (image row h0 + 2), columns 26 + lane / 4, inside the image for
+      // lanes 0 .. 27; the rest are the right border and zero pieces
+      static_assert(wi::NTHR * 16 / wi::ROWB == 3 * wi::HP + 26 && wi::HROWS == 4 * wi::HP, "halo tail");
+      const int ln = (t16 >> 4) & 63, wp = 26 + (ln >> 2), c = (ln & 3) ^ wisw(wp);
+      const bool ok = ln < 28 && (unsigned)(h0 + 2) < (unsigned)wi::IMG;
+      const uint32_t off = ok ? (uint32_t)(pt * wi::CI + (2 * wi::IMG + wp - 1) * wi::CI + 8 * c) * 2u : kOob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, LDS_PTR(sb + wi::NTHR * 16), 16, off, 0, 0, 0);
+    } else if (wave < 2) {
+      const uint32_t off = (uint32_t)(prow * wi::PROW_G + t16);  // wave * 1024 + lane * 16
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsg, LDS_PTR(sb + wi::RAW_G + wave * 1024), 16, off, 0, 0, 0);
+    } else if (wave == 2) {
+      const __amdgpu_buffer_rsrc_t rsc = rsrc(code, gbytes / 2);
+      const uint32_t off = (uint32_t)(prow * wi::PROW_C + t16 - 2048);  // lane * 16
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsc, LDS_PTR(sb + wi::RAW_C), 16, off, 0, 0, 0);
+    } else {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, LDS_PTR(sb + wi::IDLE + (wave - 3) * 1024), 16, kOob, 0, 0, 0);
+    }
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, LDS_PTR(sb + wave * 1024), 16, halo_off(0), 0, 0, 0);
   }
+}
+
+// POOL: this thread's piece of the g tile in the stage (pixel row arow,
+// channels acol .. acol + 7, at byte 16 tid as a copy would put it) is the
+// pooled gradient of its 2 x 2 window where the window's routing code names
+// the pixel's position, zero elsewhere.  A tile is two image rows from an
+// even row, so the pixel's window is pooled column (arow mod 32) / 2 of the
+// tile's pooled row and its position is fixed by arow.
+__device__ __forceinline__ void wi_route(char *st, int tid, int arow, int acol) {
+  const int pc = (arow % wi::IMG) >> 1;
+  const uint32_t pos = (uint32_t)((((arow / wi::IMG) & 1) << 1) | (arow & 1));
+  const u32x4 g = *reinterpret_cast<const u32x4 *>(st + wi::A_BYTES + wi::RAW_G + pc * wi::ROWA + acol * 2);
+  const u32x2 code = *reinterpret_cast<const u32x2 *>(st + wi::A_BYTES + wi::RAW_C + pc * wi::CO + acol);
+  u32x4 v;
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const uint32_t cb = code[d >> 1] >> (16 * (d & 1));  // codes of channels 2d, 2d + 1
+    const uint32_t keep = ((cb & 0xffu) == pos ? 0x0000ffffu : 0u) | (((cb >> 8) & 0xffu) == pos ? 0xffff0000u : 0u);
+    v[d] = g[d] & keep;
+  }
+  *reinterpret_cast<u32x4 *>(st + tid * 16) = v;
 }
 
 // k group KG (image row KG of the tile): one g fragment, nine input
@@ -627,8 +697,10 @@ __device__ __forceinline__ void wi_kgroup(f32x4_t (&acc)[wi::NF], f32x4_t &bacc,
   }
 }
 
-template <int NST>
-__global__ void __launch_bounds__(wi::NTHR)
+// (at least four waves per SIMD: at most 128 registers, so that two
+// workgroups share a CU)
+template <int NST, bool POOL>
+__global__ void __launch_bounds__(wi::NTHR, 4)
 wgrad_img_kernel(WgradArgs a) {
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -643,7 +715,10 @@ wgrad_img_kernel(WgradArgs a) {
   const int nk = (p_end - p_begin) / wi::BK;
   const bf16_t *G = reinterpret_cast<const bf16_t *>(a.g) + rep * a.g_rs;
   const bf16_t *X = reinterpret_cast<const bf16_t *>(a.x) + rep * a.x_rs;
-  const uint32_t gbytes = (uint32_t)((int64_t)M * wi::CO * 2), xbytes = (uint32_t)((int64_t)M * wi::CI * 2);
+  const uint8_t *gc = POOL ? a.gcode + rep * a.g_rs : nullptr;
+  // (POOL: g and gc are the pooled gradient and its codes, a quarter of the pixels)
+  const uint32_t gbytes = (uint32_t)((int64_t)M * wi::CO * 2 / (POOL ? 4 : 1)),
+                 xbytes = (uint32_t)((int64_t)M * wi::CI * 2);
   const int wm = wave >> 1, wn = wave & 1;
   const bool do_bias = wn == 0 && a.db != nullptr;
 
@@ -653,15 +728,15 @@ wgrad_img_kernel(WgradArgs a) {
   const int acol = 8 * (((byte0 % wi::ROWA) / 16) ^ swz<wi::ROWA / 16>(arow));
   int hrel[wi::SB], hh[wi::SB];
 #pragma unroll
-  for (int q = 0; q < wi::SB; ++q) {
-    const int R = (q * wi::NTHR * 16 + byte0) / wi::ROWB, cs = (byte0 / 16) & 3;
+  for (int q = 0; q < wi::SB; ++q) {  // (POOL: piece 0 only)
+    const int b0 = byte0;
+    const int R = (q * wi::NTHR * 16 + b0) / wi::ROWB, cs = (b0 / 16) & 3;
     const int hp = R / wi::HP, wp = R - wi::HP * hp;
     const int c = cs ^ wisw(wp);
     const bool in = R < wi::HROWS && wp >= 1 && wp <= wi::IMG;
     hh[q] = in ? hp : -1;
     hrel[q] = ((hp - 1) * wi::IMG + (wp - 1)) * wi::CI + 8 * c;
   }
-  char *stage0 = smem + wave * 1024;
 
   // fragment read addresses (relative to a stage): g fragment of output
   // channels 16 wm.., input fragment halves of tap column s, channel block cb
@@ -686,17 +761,52 @@ wgrad_img_kernel(WgradArgs a) {
   for (int i = 0; i < wi::NF; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   f32x4_t bacc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  if constexpr (!POOL) {
 #pragma unroll
-  for (int q = 0; q < NST - 1; ++q)
-    if (q < nk) wi_issue<NST>(q, stage0, G, X, gbytes, xbytes, p_begin, arow, acol, hrel, hh);
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + NST - 2 < nk) wait_vm<(NST - 2) * wi::CPT>();
-    else wait_vm<0>();
+    for (int q = 0; q < NST - 1; ++q)
+      if (q < nk) wi_issue<NST, false>(q, smem, wave, lane, G, X, gc, gbytes, xbytes, p_begin, arow, acol, hrel, hh);
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt + NST - 2 < nk) wait_vm<(NST - 2) * wi::CPT>();
+      else wait_vm<0>();
+      asm volatile("s_barrier" ::: "memory");
+      if (kt + NST - 1 < nk)
+        wi_issue<NST, false>(kt + NST - 1, smem, wave, lane, G, X, gc, gbytes, xbytes, p_begin, arow, acol, hrel, hh);
+      const uint32_t st = lds0 + (uint32_t)((kt % NST) * wi::STAGE);
+      wi_kgroup<0>(acc, bacc, ra, hb, st, do_bias, wn);
+      wi_kgroup<1>(acc, bacc, ra, hb, st, do_bias, wn);
+    }
+  } else {
+    // copies NST - 1 = 2 k tiles ahead; g tile kt + 1 routed in LDS during
+    // iteration kt, so its pooled row and codes (each thread's first copy of
+    // the tile) are waited for one tile ahead and the halo rows (its second,
+    // last copy) two tiles ahead.  Loads complete in issue order.
+    static_assert(NST == 3 && wi::BK == 2 * wi::IMG, "two halo tiles ahead; a tile is two image rows");
+    wi_issue<NST, true>(0, smem, wave, lane, G, X, gc, gbytes, xbytes, p_begin, arow, acol, hrel, hh);
+    if (1 < nk) {
+      wi_issue<NST, true>(1, smem, wave, lane, G, X, gc, gbytes, xbytes, p_begin, arow, acol, hrel, hh);
+      wait_vm<wi::SB>();
+    } else {
+      wait_vm<0>();
+    }
     asm volatile("s_barrier" ::: "memory");
-    if (kt + NST - 1 < nk) wi_issue<NST>(kt + NST - 1, stage0, G, X, gbytes, xbytes, p_begin, arow, acol, hrel, hh);
-    const uint32_t st = lds0 + (uint32_t)((kt % NST) * wi::STAGE);
-    wi_kgroup<0>(acc, bacc, ra, hb, st, do_bias, wn);
-    wi_kgroup<1>(acc, bacc, ra, hb, st, do_bias, wn);
+    wi_route(smem, tid, arow, acol);
+    for (int kt = 0; kt < nk; ++kt) {
+      // tile kt's copies and routed g have landed, and tile kt + 1's pooled
+      // row and codes (only its halo copy may still be in flight); every
+      // wave is done with tile kt - 1 and with routing tile kt
+      if (kt + 1 < nk) wait_vm<1>();
+      else wait_vm<0>();
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      asm volatile("s_barrier" ::: "memory");
+      // stage (kt + 2) % NST was last read by tile kt - 1 and (its pooled
+      // row) by the routing of tile kt - 1
+      if (kt + 2 < nk) wi_issue<NST, true>(kt + 2, smem, wave, lane, G, X, gc, gbytes, xbytes, p_begin, arow, acol, hrel, hh);
+      // stage (kt + 1) % NST's g tile was last read by tile kt - 2
+      if (kt + 1 < nk) wi_route(smem + ((kt + 1) % NST) * wi::STAGE, tid, arow, acol);
+      const uint32_t st = lds0 + (uint32_t)((kt % NST) * wi::STAGE);
+      wi_kgroup<0>(acc, bacc, ra, hb, st, do_bias, wn);
+      wi_kgroup<1>(acc, bacc, ra, hb, st, do_bias, wn);
+    }
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
@@ -940,6 +1050,10 @@ bool wgrad_img_ok(int Co, int Ci, int H, int W, int taps) {
   return taps == 9 && H == wi::IMG && W == wi::IMG && Co == wi::CO && Ci == wi::CI;
 }
 
+bool wgrad_pool_codes(int dtype, int Co, int Ci, int H, int W, int taps) {
+  return dtype == GCPSL_BF16 && wgrad_img_ok(Co, Ci, H, W, taps);
+}
+
 bool wgrad_halo_ok(int Co, int Ci, int H, int W, int taps) {
   return taps == 9 && H == wh::IMG && W == wh::IMG && Co % wh::BM == 0 && Ci % 64 == 0;
 }
@@ -986,13 +1100,20 @@ hipError_t launch_wgrad_lds(const WgradArgs &a, hipStream_t s, std::string *labe
     constexpr int lds = kImgStages * wi::STAGE;
     static PerDeviceOnce iattr;
     if (iattr.needed()) {
-      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&wgrad_img_kernel<kImgStages>),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-      if (e != hipSuccess) return e;
+      for (const void *f : {reinterpret_cast<const void *>(&wgrad_img_kernel<kImgStages, false>),
+                            reinterpret_cast<const void *>(&wgrad_img_kernel<kImgStages, true>)}) {
+        const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        if (e != hipSuccess) return e;
+      }
       iattr.mark();
     }
-    if (label) *label = "conv_wgrad<bf16,64x288,w8,img>";
-    hipLaunchKernelGGL((wgrad_img_kernel<kImgStages>), dim3((uint32_t)a.splits * a.C), dim3(wi::NTHR), lds, s, a);
+    if (label) *label = a.gcode ? "conv_wgrad<bf16,64x288,w8,img,pool>" : "conv_wgrad<bf16,64x288,w8,img>";
+    if (a.gcode)
+      hipLaunchKernelGGL((wgrad_img_kernel<kImgStages, true>), dim3((uint32_t)a.splits * a.C), dim3(wi::NTHR), lds,
+                         s, a);
+    else
+      hipLaunchKernelGGL((wgrad_img_kernel<kImgStages, false>), dim3((uint32_t)a.splits * a.C), dim3(wi::NTHR), lds,
+                         s, a);
     return hipGetLastError();
   }
   if (wgrad_halo_ok(a.Co, a.Ci, a.H, a.W, a.taps)) {

@@ -62,6 +62,14 @@ struct ConvArgs {
                        // each image's positions, of the 2x2 max pool if pool_max, [C][Bt][N] (kernels
                        // that report conv_fuses_avg)
   int64_t pool_rs;     // its per-replica stride (elements)
+  // Routing codes of a 2 x 2 max pool, one byte per pooled element: 0..3 =
+  // the window position (row-major) of the first maximum, 4 = no gradient
+  // (the maximum is not positive, so the ReLU below it is off).  fwd (with
+  // the max pool in pool_out, kernels that report conv_pool_codes): written
+  // beside pool_out in its layout, and `out` is then not written.  dgrad: src
+  // holds the pooled gradient [C][Bt][H/2][W/2][Csrc] (stride src_rs) and the
+  // kernel routes it to the unpooled grid through these codes (same layout).
+  uint8_t *pool_code;
 };
 
 // Weight gradient: dW[co][kk] = sum_p G[p][co] X(p, kk), kk = (r, s, ci),
@@ -77,6 +85,11 @@ struct WgradArgs {
   const int32_t *rmap;   // device [C]: replica of each slot, or null (slot z = replica z)
   int taps;  // 9: x is the layer input; 1: x holds im2col rows of Ci columns
   int nw;    // weight-gradient row length written (9 * input channels)
+  // or null; else g holds the gradient at the output of the 2 x 2 max pool
+  // after this layer, [C][Bt][H/2][W/2][Co] (stride g_rs), and gcode its
+  // routing codes (ConvArgs::pool_code): the pre-activation gradient is
+  // g routed through them (kernels that report wgrad_pool_codes)
+  const uint8_t *gcode;
 };
 
 // ---------------------------------------------------------------- launchers
@@ -105,6 +118,12 @@ bool conv_im3_ok(int dtype, int Ci, int Co, int H, int W);
 hipError_t launch_conv_col(const ConvArgs &a, hipStream_t s, std::string *label);
 // whether launch_conv also writes ConvArgs::pool_out for this layer
 bool conv_fuses_pool(int dtype, const ConvArgs &a);
+// whether launch_conv takes ConvArgs::pool_code for these arguments (fwd:
+// writes the codes with the pool instead of the unpooled output; dgrad: a
+// pooled source routed through them)
+bool conv_pool_codes(int dtype, const ConvArgs &a);
+// whether launch_wgrad takes WgradArgs::gcode for this layer shape
+bool wgrad_pool_codes(int dtype, int Co, int Ci, int H, int W, int taps);
 // Whether launch_conv writes the per-image mean (of the 2x2 max pool if
 // pool_max) to pool_out for these arguments (16 x 16 bf16 images on the
 // 256-wide halo tile, every output channel in one tile).

@@ -361,7 +361,7 @@ class Context:
             raise ValueError("a static context's workspace is the library's own; it has no tensor view")
         ptr, n, dt = C.c_void_p(), C.c_int64(), C.c_int32()
         _check(lib().gcpsl_tensor(self._h, name.encode(), C.byref(ptr), C.byref(n), C.byref(dt)))
-        tdt = {0: torch.float32, 1: torch.bfloat16, -1: torch.int32}[dt.value]
+        tdt = {0: torch.float32, 1: torch.bfloat16, -1: torch.int32, -2: torch.uint8}[dt.value]
         esz = torch.tensor([], dtype=tdt).element_size()
         off = ptr.value - self.workspace.data_ptr()
         return self.workspace[off:off + n.value * esz].view(tdt)

@@ -79,8 +79,9 @@ def kernel_label(name: str) -> str:
     m = re.search(r"conv_col_kernel(<(true|false)>)?", name)
     if m:
         return "conv_fwd<bf16,256x32x27,w4,img3>" if m.group(2) == "true" else "conv_fwd<bf16,256x32x32,w4,col>"
-    if re.search(r"wgrad_img_kernel<", name):
-        return "conv_wgrad<bf16,64x288,w8,img>"
+    m = re.search(r"wgrad_img_kernel<\d+(, (true|false))?>", name)
+    if m:  # (true: the output gradient routed from a max pool's codes)
+        return "conv_wgrad<bf16,64x288,w8,img,pool>" if m.group(2) == "true" else "conv_wgrad<bf16,64x288,w8,img>"
     if re.search(r"wgrad_halo_kernel<", name):
         return "conv_wgrad<bf16,128x576,w8,halo>"
     m = re.search(r"wgrad_lds_kernel<(\d+), (\d+), (\d+), (\d+), (?:\d+, \d+, )?(true|false)>", name)
@@ -99,7 +100,7 @@ SHARED_HEADERS = ("common.h",)  # device helpers every kernel source includes
 
 def kernel_source(label: str) -> str:
     """The source file that holds the kernel a timing label names."""
-    if label.startswith("conv_wgrad<") and label.endswith((",lds>", ",halo>", ",img>", ",col>", ",img3>")):
+    if label.startswith("conv_wgrad<") and label.endswith((",lds>", ",halo>", ",img>", ",col>", ",img3>", ",pool>")):
         return "k_wgrad_lds.hip"
     if label.startswith("conv_") and label.endswith((",lds>", ",halo>", ",halo1>")):
         return "k_conv_lds.hip"

@@ -13,7 +13,10 @@ then report as a kernel error.
 
 `GpuChoices` reads the decisions the GPU took from its stored activations
 (the mask is act > 0, the routing the first maximum of the stored window,
-exactly as the GPU's backward kernels take them), checks every one that
+exactly as the GPU's backward kernels take them), or, for a conv whose
+max pool keeps routing codes instead of the unpooled output, from the codes
+(the routed position of each window, or none; the ReLU decisions at a
+window's other positions change nothing and stay the oracle's), checks every one that
 differs from the oracle's own decision to be such a near-tie of the
 oracle's values (an assertion otherwise), and hands the GPU's decision to
 the oracle through `split_forward_backward(choose=...)`.  The oracle then
@@ -115,6 +118,24 @@ def pool_windows(x):
             .reshape(Bt, H // 2, W // 2, 4, C))
 
 
+def unpool_windows(w):
+    """Inverse of pool_windows: [Bt,H/2,W/2,4,C] -> [Bt,H,W,C]."""
+    Bt, Hp, Wp, _, C = w.shape
+    return (w.reshape(Bt, Hp, Wp, 2, 2, C).transpose(0, 1, 3, 2, 4, 5)
+            .reshape(Bt, 2 * Hp, 2 * Wp, C))
+
+
+def routed_gradient(g, route):
+    """The pre-activation gradient of a conv whose 2 x 2 max pool keeps
+    routing codes (route [Bt,H/2,W/2,C]: window position 0..3 of the
+    gradient g [Bt,H/2,W/2,C], 4 for none): g at the routed position of each
+    window, zero elsewhere, [Bt,H,W,C]."""
+    w = np.zeros(g.shape[:3] + (4,) + g.shape[3:], dtype=g.dtype)
+    for k in range(4):
+        w[:, :, :, k, :] = np.where(route == k, g, 0)
+    return unpool_windows(w)
+
+
 def layer_shapes(cfg):
     """Output shape [B, ...] of every layer of the workload's model."""
     h, w, c = cfg["H"], cfg["W"], cfg["Cin"]
@@ -158,6 +179,7 @@ class GpuChoices:
         shapes = layer_shapes(cfg)
         layers = cfg["layers"]
         self.relu, self.pool, self.flips = {}, {}, {}
+        self.route = {}  # conv i -> routing codes of its max pool (no unpooled output stored)
         self.worst = 0.0  # largest near-tie distance seen, as a fraction of its tensor's scale
         for i, spec in enumerate(layers):
             kind = spec[0]
@@ -168,12 +190,28 @@ class GpuChoices:
                     self.relu[i] = a > 0
                     if i + 1 < len(layers) and layers[i + 1][0] == "maxpool":
                         self.pool[i + 1] = np.argmax(pool_windows(a), axis=3)
+                elif i + 1 < len(layers) and layers[i + 1][0] == "maxpool":
+                    r = replica_tensor(ctx, f"route{i + 1}", n, shapes[i + 1])
+                    if r is not None:
+                        r = r.astype(np.int64)
+                        assert r.max() <= 4, ("routing code out of range", i + 1)
+                        self.route[i] = r
+                        # an all-zero window routes nothing; its first maximum is position 0
+                        self.pool[i + 1] = np.where(r < 4, r, 0)
             if kind == "block":  # the block's inner ReLU, after its first norm
                 a1 = replica_tensor(ctx, f"act{i}.n1", n, shapes[i])
                 if a1 is not None:
                     self.relu[(i, "n1")] = a1 > 0
 
     def __call__(self, kind, i, own, values):
+        if kind == "relu" and i in self.route:
+            # on at each window's routed position, off at all four where
+            # nothing is routed, the oracle's own elsewhere
+            r = self.route[i]
+            w = pool_windows(own).copy()
+            for k in range(4):
+                w[:, :, :, k, :] = np.where(r == 4, False, np.where(r == k, True, w[:, :, :, k, :]))
+            self.relu[i] = unpool_windows(w)
         if kind == "relu":
             gpu = self.relu.get(i)
             assert gpu is not None, f"layer {i}: the GPU's activation is not stored"

@@ -18,7 +18,7 @@ from oracle.model import im2col3x3, round_bf16, split_forward_backward
 from oracle.sampler import active_clients, batch_indices, cluster_examples
 from oracle.train import GCPSLOracle, fuse as oracle_fuse, sgd_args, sgd_update
 
-from gpu_match import TOL, bar, deep_bf16, noisy_rounding, GpuChoices, LazyChoices, close, compare_params, layer_shapes, master_ulp, replayed, replica_tensor, twin_bar
+from gpu_match import TOL, bar, deep_bf16, noisy_rounding, GpuChoices, LazyChoices, close, compare_params, layer_shapes, master_ulp, replayed, replica_tensor, routed_gradient, twin_bar
 from gpu_match import to_np as _np
 
 pytestmark = pytest.mark.gpu
@@ -200,9 +200,21 @@ def test_intermediates_one_round(name):
                 if t is not None:
                     ok, e = close(t, rec["acts"][i + 1], tol)
                     assert ok, (f"act{i}", n, e)
+                else:  # a conv whose max pool keeps routing codes: its pool's output is stored
+                    assert i in ch.route and replica_tensor(ctx, f"act{i + 1}", n, shapes[i + 1]) is not None, i
             if spec[0] in ("conv", "bnorm", "gnorm", "block"):
-                ok, e = close(_np(ctx.tensor(f"gpre{i}")).reshape(C, -1)[n], rec[f"gpre{i}"], tol)
+                if i in ch.route:
+                    # the gradient the layer's kernels route from the next
+                    # conv's input gradient through the codes
+                    gin = replica_tensor(ctx, f"gin{i + 2}", n, shapes[i + 1])
+                    got = routed_gradient(gin, ch.route[i]).reshape(-1)
+                else:
+                    got = _np(ctx.tensor(f"gpre{i}")).reshape(C, -1)[n]
+                ok, e = close(got, rec[f"gpre{i}"], tol)
                 assert ok, (f"gpre{i}", n, e)
+            if spec[0] == "conv" and i > 0 and layers[i - 1][0] == "maxpool":
+                ok, e = close(_np(ctx.tensor(f"gin{i}")).reshape(C, -1)[n], rec[f"gin{i}"], tol)
+                assert ok, (f"gin{i}", n, e)
             if spec[0] == "block":  # every stored tensor inside the block
                 names = [f"z{i}.1", f"act{i}.n1", f"z{i}.2", f"dz{i}.1", f"gpre{i}.n1", f"dz{i}.2"]
                 if f"sc{i}" in rec:
@@ -400,6 +412,9 @@ def test_full_size_round_sampled_replicas(name):
             if spec[0] not in ("conv", "block"):
                 continue
             act = replica_tensor(ctx, f"act{i}", n, shapes[i])
+            if act is None:  # routing codes: the conv's stored output is its max pool's
+                assert i in ch.route, i
+                i, act = i + 1, replica_tensor(ctx, f"act{i + 1}", n, shapes[i + 1])
             ok, e = close(act, rec["acts"][i + 1], tol)
             assert ok, (f"act{i}", n, e)
         ok, e = close(grads[n], g, tol)
