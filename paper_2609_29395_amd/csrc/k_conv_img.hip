@@ -242,7 +242,10 @@ conv_img_kernel(ConvArgs a, int MT) {
       const uint32_t ad = stg + (uint32_t)(px * OROW + ((c ^ (px & (OCH - 1))) * 16) + (lg & 1) * 8);
       asm volatile("ds_write_b64 %0, %1" ::"v"(ad), "v"(o) : "memory");
     }
-  // (the max pool reads the neighbouring wave's row too)
+  // The max pool reads the neighbouring wave's row too: every wave's staged
+  // rows must have landed before the barrier (the compiler does not count
+  // the asm writes, so the barrier alone does not wait for them).
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   __syncthreads();
   // dgrad: ReLU mask of the layer below (value > 0), read in the same
   // 16-byte pieces; without a mask source every value passes
