@@ -406,7 +406,9 @@ int gcpsl_cluster_sizes(gcpsl_ctx *ctx, int64_t *sizes);
  * A bf16 conv whose ReLU output feeds a stored 2 x 2 max pool and then
  * another conv (the 32 x 32, 32 -> 64 image-side layer) keeps only the pool's
  * output and "route<j>": its "act<i>" and "gpre<i>" are not stored (its
- * gradient is "gin<j+1>" routed through the codes).  dtype receives
+ * gradient is "gin<j+1>" routed through the codes).  A bf16 head conv whose
+ * max pool and mean are fused into it keeps "route<j>" of that pool and its
+ * "gpre<i>", not its "act<i>".  dtype receives
  * GCPSL_F32, GCPSL_BF16, -1 for int32 or -2 for uint8.  EINVAL on an unknown
  * or unstored name.
  */

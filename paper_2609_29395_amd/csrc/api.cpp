@@ -59,6 +59,10 @@ struct LayerInfo {
   // the unpooled output, and the layer's gradients take the next conv's
   // input gradient routed through them (no unpooled output or gradient)
   bool pcode = false;
+  // the head conv (bf16, head of a max pool then the mean): its pooling
+  // epilogue writes the max pool's routing codes and the head's pooling
+  // backward routes through them, so its output is not kept (gpre is)
+  bool hcode = false;
   size_t code_off = 0;
 };
 
@@ -389,6 +393,19 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
     }
     return wgrad_pool_codes(p.dtype, l.Co, l.Ci, l.H, l.W, 9);
   };
+  // routing codes for the head conv (LayerInfo::hcode): bf16, the head's
+  // mean of a 2 x 2 max pool written by the conv's own epilogue
+  auto head_codes = [&](int i) {
+    const LayerInfo &l = p.ly[i];
+    if (p.dtype != GCPSL_BF16 || i != p.head_conv || !p.head_maxpool || l.spec.kind != GCPSL_CONV3X3 ||
+        i + 2 != p.avg_idx)
+      return false;
+    ConvArgs f{};
+    f.epi = EPI_FWD;
+    f.taps = 9;
+    f.H = l.H; f.W = l.W; f.Csrc = l.Ci; f.N = l.Co; f.K = 9 * l.Ci; f.Kp = round_up(9 * l.Ci, bk_tile);
+    return conv_fuses_avg(p.dtype, f);
+  };
   for (int i = 0; i < n; ++i) {
     LayerInfo &l = p.ly[i];
     const int kind = l.spec.kind;
@@ -453,7 +470,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
       continue;
     }
     l.pcode = pool_codes(i);
-    if (l.pcode) {
+    l.hcode = head_codes(i);
+    if (l.pcode || l.hcode) {
       l.act_rs = (int64_t)B * l.Ho * l.Wo * l.Co;
       l.code_off = take((size_t)C * l.act_rs / 4);
     } else if (kind == GCPSL_CONV3X3 || (kind == GCPSL_MAXPOOL2 && !(p.head_maxpool && i == n - 3))) {
@@ -1058,14 +1076,21 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
         a.pool_max = p.head_maxpool ? 1 : 0;
         avg_done = conv_fuses_avg(p.dtype, a);
         if (!avg_done) a.pool_out = nullptr;
+        if (l.hcode) {  // the mean and the max pool's routing codes only
+          if (!avg_done) return gcpsl_fail(GCPSL_EUNSUPPORTED, "head routing codes without the fused pooling");
+          a.pool_code = reinterpret_cast<uint8_t *>(ws + l.code_off);
+          a.code_rs = l.act_rs / 4;
+          a.out = nullptr;
+        }
       }
       std::string lab;
       const double M = (double)B * l.H * l.W;
       const double fl = 2.0 * C * M * l.Co * 9.0 * l.Ci;
+      const bool codes = l.pcode || l.hcode;
       const double by = (double)C * (p.esz * (M * l.Ci + (double)l.Co * 9 * l.Ci +
-                                                (l.pcode ? 0.0 : M * l.Co * (a.res ? 2 : 1)) +
-                                                (pool_done ? M / 4 * l.Co : 0.0)) +
-                                     (l.pcode ? M / 4 * l.Co : 0.0) + 4.0 * l.Co);
+                                                (codes ? 0.0 : M * l.Co) + (a.res ? M * l.Co : 0.0) +
+                                                (pool_done ? M / 4 * l.Co : 0.0) + (avg_done ? (double)B * l.Co : 0.0)) +
+                                     (codes ? M / 4 * l.Co : 0.0) + 4.0 * l.Co);
       size_t t_ = tbegin(ctx, s);
       LAUNCH(launch_conv(p.dtype, a, s, &lab));
       tend(ctx, s, t_, lab, fl, by);
@@ -1124,9 +1149,13 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
   // backward: head pooling, then every conv from the top down
   {
     const LayerInfo &hc = p.ly[p.head_conv];
-    LAUNCH_T("head_pool_bwd", 0.0, (double)C * B * hc.Co * (2.0 * p.esz * hc.Ho * hc.Wo + 4.0),
+    // (with routing codes the head conv's output is not read)
+    const double rd = hc.hcode ? 0.25 * hc.Ho * hc.Wo : p.esz * hc.Ho * hc.Wo;
+    LAUNCH_T("head_pool_bwd", 0.0, (double)C * B * hc.Co * (rd + p.esz * hc.Ho * hc.Wo + 4.0),
              launch_head_pool_bwd(p.dtype, ws + hc.act_off, ctx->at<float>(p.off_dh), ws + hc.gpre_off, C, rmap, B,
-                                  hc.Ho, hc.Wo, hc.Co, p.head_maxpool ? 1 : 0, s));
+                                  hc.Ho, hc.Wo, hc.Co, p.head_maxpool ? 1 : 0, s,
+                                  hc.hcode ? reinterpret_cast<const uint8_t *>(ws + hc.code_off) : nullptr,
+                                  hc.act_rs / 4));
   }
   int i = p.head_conv;
   while (i >= 0) {
@@ -1533,7 +1562,8 @@ extern "C" int gcpsl_tensor(gcpsl_ctx *ctx, const char *name, void **ptr, int64_
       continue;
     }
     if (nm == "act" + k && l.stored) return put(l.act_off, (int64_t)p.C * l.act_rs, p.dtype);
-    if (l.pcode && nm == "route" + std::to_string(i + 1)) return put(l.code_off, (int64_t)p.C * l.act_rs / 4, -2);
+    if ((l.pcode || l.hcode) && nm == "route" + std::to_string(i + 1))
+      return put(l.code_off, (int64_t)p.C * l.act_rs / 4, -2);
     if (l.spec.kind == GCPSL_CONV3X3 || is_norm(l.spec.kind)) {
       const int64_t rs = (int64_t)p.B * l.H * l.W;
       if (nm == "gpre" + k && !l.pcode) return put(l.gpre_off, p.C * rs * l.Co, p.dtype);

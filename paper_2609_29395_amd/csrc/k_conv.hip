@@ -695,10 +695,13 @@ void wgrad_tile(int dtype, int Co, int ncols, int *bm, int *bn) {
 }
 
 hipError_t launch_conv(int dtype, const ConvArgs &a, hipStream_t s, std::string *label) {
-  // routing codes: only the image-side kernels take them
-  if (a.pool_code)
+  // routing codes: the head's pooling epilogue (halo tile) and the
+  // image-side kernels take them
+  if (a.pool_code) {
+    if (a.epi == EPI_FWD && a.pool_max && a.pool_out && conv_fuses_avg(dtype, a)) return launch_conv_lds(a, s, label);
     return (conv_pool_codes(dtype, a) && (a.epi == EPI_DGRAD || a.pool_out)) ? launch_conv_img(a, s, label)
                                                                               : hipErrorInvalidValue;
+  }
   if (a.taps == 9 && a.epi == EPI_FWD && a.res == nullptr && conv_im3_ok(dtype, a.Csrc, a.N, a.H, a.W))
     return launch_conv_col(a, s, label);
   if (conv_img_ok(dtype, a)) return launch_conv_img(a, s, label);

@@ -581,7 +581,8 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
       ov.y = pack2_bf16(v[2], v[3]);
       ov.z = pack2_bf16(v[4], v[5]);
       ov.w = pack2_bf16(v[6], v[7]);
-      if (nok && m < M) *reinterpret_cast<uint4 *>(out + (int64_t)m * a.N + n) = ov;
+      // (with the pool's routing codes the output itself is not kept)
+      if (nok && m < M && !(AVG && a.pool_code)) *reinterpret_cast<uint4 *>(out + (int64_t)m * a.N + n) = ov;
       if constexpr (AVG) {
         // the stored (bf16-rounded) values, as the pooling reads them back
         const uint32_t ow[4] = {ov.x, ov.y, ov.z, ov.w};
@@ -596,7 +597,41 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
       // a pass holds two whole image rows (one pooling row); lane step i
       // is row i >> 1, column lane / 8 + 8 (i & 1)
       static_assert(PR == 2 * halo::IMG && RSTEP == 8 && ITS == 4, "pass = one pooling row");
-      if (a.pool_max) {
+      if (a.pool_max && a.pool_code) {
+        // 2 x 2 windows with routing codes: the even-column lane takes its
+        // partner's (lane ^ 8) two values and finds the first maximum in
+        // row-major window order (strict comparison), adds it and stores its
+        // position, 4 where it is not positive.  Window h of the lane: pooled
+        // column (lane / 8) / 2 + 4 h of pooled row 2 wm + pass.
+        uint32_t cw[2][2] = {{0u, 0u}, {0u, 0u}};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const float t0 = pv[h][e], b0 = pv[2 + h][e];
+            const float t1 = __shfl_xor(t0, 8, 64), b1 = __shfl_xor(b0, 8, 64);
+            float best = t0;
+            uint32_t arg = 0u;
+            if (t1 > best) best = t1, arg = 1u;
+            if (b0 > best) best = b0, arg = 2u;
+            if (b1 > best) best = b1, arg = 3u;
+            if (!(best > 0.f)) arg = 4u;
+            if ((lane & 8) == 0) avs[e] += best;
+            cw[h][e >> 2] |= arg << (8 * (e & 3));
+          }
+        }
+        if ((lane & 8) == 0 && nok) {
+          constexpr int PH = halo::IMG / 2;  // pooled side
+          const int img = m0 / (halo::IMG * halo::IMG), prow = 2 * wm + pass;
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int pcol = (lane >> 4) + 4 * h;
+            *reinterpret_cast<uint2 *>(a.pool_code + rep * a.code_rs +
+                                       ((int64_t)(img * PH + prow) * PH + pcol) * a.N + n) =
+                make_uint2(cw[h][0], cw[h][1]);
+          }
+        }
+      } else if (a.pool_max) {
         // 2 x 2 windows: the other column of a window is in lane ^ 8; the
         // even-column lane adds the window's maximum
 #pragma unroll

@@ -981,11 +981,14 @@ static hipError_t launch_linear_ce_reg(const T *h, const int32_t *y, const float
 // gpre = mask * route(dh / npos) (route = first maximum if max pooled).  A
 // thread handles one 16-byte vector of channels of one window (max pooled)
 // or one position.
+// With routing codes (code, one byte per pooled element in the pooled
+// layout: the window position of the first maximum, 4 for none) the head
+// conv's output is not read.
 template <typename T>
 __global__ void __launch_bounds__(256)
 head_pool_bwd_kernel(const T *__restrict__ a, const float *__restrict__ dh, T *__restrict__ gpre,
                      const int32_t *__restrict__ rmap, int64_t a_rs, int64_t dh_rs, uint32_t total, PoolIdx d, int W,
-                     int Ch, int maxpool) {
+                     int Ch, int maxpool, const uint8_t *__restrict__ code, int64_t code_rs) {
   constexpr int VEC = ElemT<T>::VEC;
   const uint32_t i = blockIdx.x * 256u + threadIdx.x;
   if (i >= total) return;
@@ -1002,7 +1005,28 @@ head_pool_bwd_kernel(const T *__restrict__ a, const float *__restrict__ dh, T *_
     Vec16<T> g;
 #pragma unroll
     for (int e = 0; e < VEC; ++e) g.v[e] = ElemT<T>::from_f(dr[e] / npos);
-    route_window(a, gpre, base, W, Ch, g);
+    if (code) {
+      uint8_t k8[VEC];
+      const uint8_t *cp = code + rep * code_rs + (int64_t)i * VEC;
+      if constexpr (VEC == 8) {
+        const uint2 cw = *reinterpret_cast<const uint2 *>(cp);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) k8[e] = (uint8_t)(((e < 4 ? cw.x : cw.y) >> (8 * (e & 3))) & 0xffu);
+      } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) k8[e] = cp[e];
+      }
+      const int64_t o[4] = {base, base + Ch, base + (int64_t)W * Ch, base + (int64_t)W * Ch + Ch};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        Vec16<T> out;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) out.v[e] = k8[e] == k ? g.v[e] : T(0);
+        st16(gpre + o[k], out);
+      }
+    } else {
+      route_window(a, gpre, base, W, Ch, g);
+    }
   } else {
     // d.wo = W, d.ho = H: i = ((bi * H + h) * W + w) * CV + cv
     const uint32_t r = fdiv(i, d.cv);
@@ -1360,13 +1384,16 @@ static hipError_t head_pool_t(const T *a, T *h, int C, const int32_t *rmap, int 
 
 template <typename T>
 static hipError_t head_pool_bwd_t(const T *a, const float *dh, T *gpre, int C, const int32_t *rmap, int Bt, int H,
-                                  int W, int Ch, int maxpool, hipStream_t s) {
+                                  int W, int Ch, int maxpool, hipStream_t s, const uint8_t *code, int64_t code_rs) {
   constexpr int VEC = ElemT<T>::VEC;
   const int CV = Ch / VEC;
   const int Ho = maxpool ? H / 2 : H, Wo = maxpool ? W / 2 : W;
   const uint32_t tot = (uint32_t)((int64_t)Bt * Ho * Wo * CV);
+  if (code && (!maxpool || (reinterpret_cast<uintptr_t>(code) | (uintptr_t)code_rs) % VEC != 0))
+    return hipErrorInvalidValue;
   hipLaunchKernelGGL(head_pool_bwd_kernel<T>, dim3((tot + 255) / 256, C), dim3(256), 0, s, a, dh, gpre, rmap,
-                     (int64_t)Bt * H * W * Ch, (int64_t)Bt * Ch, tot, pool_idx(CV, Wo, Ho), W, Ch, maxpool);
+                     (int64_t)Bt * H * W * Ch, (int64_t)Bt * Ch, tot, pool_idx(CV, Wo, Ho), W, Ch, maxpool, code,
+                     code_rs);
   return hipGetLastError();
 }
 
@@ -1417,10 +1444,11 @@ hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const fl
 }
 
 hipError_t launch_head_pool_bwd(int dtype, const void *a, const float *dh, void *gpre, int C, const int32_t *rmap,
-                                int Bt, int H, int W, int Ch, int maxpool, hipStream_t s) {
+                                int Bt, int H, int W, int Ch, int maxpool, hipStream_t s, const uint8_t *code,
+                                int64_t code_rs) {
   if (dtype == GCPSL_BF16)
-    return head_pool_bwd_t((const bf16_t *)a, dh, (bf16_t *)gpre, C, rmap, Bt, H, W, Ch, maxpool, s);
-  return head_pool_bwd_t((const float *)a, dh, (float *)gpre, C, rmap, Bt, H, W, Ch, maxpool, s);
+    return head_pool_bwd_t((const bf16_t *)a, dh, (bf16_t *)gpre, C, rmap, Bt, H, W, Ch, maxpool, s, code, code_rs);
+  return head_pool_bwd_t((const float *)a, dh, (float *)gpre, C, rmap, Bt, H, W, Ch, maxpool, s, code, code_rs);
 }
 
 hipError_t launch_wgrad_reduce(const float *dw, const float *db, int splits, int64_t dw_ss,

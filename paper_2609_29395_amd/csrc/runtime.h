@@ -70,6 +70,9 @@ struct ConvArgs {
   // holds the pooled gradient [C][Bt][H/2][W/2][Csrc] (stride src_rs) and the
   // kernel routes it to the unpooled grid through these codes (same layout).
   uint8_t *pool_code;
+  int64_t code_rs;  // fwd with the head's mean of a max pool in pool_out (kernels that report
+                    // conv_fuses_avg): the pool's routing codes [C][Bt][H/2][W/2][N] go to
+                    // pool_code, this its per-replica stride, and `out` is not written
 };
 
 // Weight gradient: dW[co][kk] = sum_p G[p][co] X(p, kk), kk = (r, s, ci),
@@ -201,8 +204,12 @@ hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const fl
                             int64_t P, int64_t w_off, int64_t b_off, float *grad, float *dh,
                             float *loss, int C, const int32_t *rmap, int Bt, int Ch, int L, float eps,
                             hipStream_t s);
+// maxpool with code (bf16, the head conv's routing codes [C][Bt][H/2][W/2][Ch],
+// per-replica stride code_rs): the gradient is routed through the codes and
+// `a` is not read
 hipError_t launch_head_pool_bwd(int dtype, const void *a, const float *dh, void *gpre, int C, const int32_t *rmap,
-                                int Bt, int H, int W, int Ch, int maxpool, hipStream_t s);
+                                int Bt, int H, int W, int Ch, int maxpool, hipStream_t s,
+                                const uint8_t *code = nullptr, int64_t code_rs = 0);
 hipError_t launch_wgrad_reduce(const float *dw, const float *db, int splits, int64_t dw_ss,
                                int64_t dw_rs, int64_t db_ss, int64_t db_rs, float *grad,
                                int64_t P, int64_t w_off, int64_t b_off, int64_t nw, int co,

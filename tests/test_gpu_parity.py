@@ -200,16 +200,17 @@ def test_intermediates_one_round(name):
                 if t is not None:
                     ok, e = close(t, rec["acts"][i + 1], tol)
                     assert ok, (f"act{i}", n, e)
-                elif i in ch.route:  # a conv whose max pool keeps routing codes: its pool's output is stored
-                    assert replica_tensor(ctx, f"act{i + 1}", n, shapes[i + 1]) is not None, i
+                else:  # unstored: a conv whose max pool keeps routing codes, or a pool fused into the head
+                    assert i in ch.route or spec[0] == "maxpool", (i, spec)
             if spec[0] in ("conv", "bnorm", "gnorm", "block"):
-                if i in ch.route:
+                got = replica_tensor(ctx, f"gpre{i}", n, rec[f"gpre{i}"].shape)
+                if got is None:
                     # the gradient the layer's kernels route from the next
                     # conv's input gradient through the codes
+                    assert i in ch.route, i
                     gin = replica_tensor(ctx, f"gin{i + 2}", n, shapes[i + 1])
-                    got = routed_gradient(gin, ch.route[i]).reshape(-1)
-                else:
-                    got = _np(ctx.tensor(f"gpre{i}")).reshape(C, -1)[n]
+                    got = routed_gradient(gin, ch.route[i])
+                got = got.reshape(-1)
                 ok, e = close(got, rec[f"gpre{i}"], tol)
                 assert ok, (f"gpre{i}", n, e)
             if spec[0] == "conv" and i > 0 and layers[i - 1][0] == "maxpool":
@@ -412,9 +413,13 @@ def test_full_size_round_sampled_replicas(name):
             if spec[0] not in ("conv", "block"):
                 continue
             act = replica_tensor(ctx, f"act{i}", n, shapes[i])
-            if act is None:  # routing codes: the conv's stored output is its max pool's
+            if act is None:
+                # routing codes: the next stored output is the conv's max pool
+                # (or, at the head, the mean over the pool)
                 assert i in ch.route, i
-                i, act = i + 1, replica_tensor(ctx, f"act{i + 1}", n, shapes[i + 1])
+                while act is None:
+                    i += 1
+                    act = replica_tensor(ctx, f"act{i}", n, shapes[i])
             ok, e = close(act, rec["acts"][i + 1], tol)
             assert ok, (f"act{i}", n, e)
         ok, e = close(grads[n], g, tol)
