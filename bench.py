@@ -258,9 +258,15 @@ def measure(name, steps, warmup, timing_steps, cpu_seconds, with_cpu=True, with_
                       f"right after the timed window")
     prof_t, prof_m = profile(name, dom, "trace"), profile(name, dom, "mfma")
     if prof_t is not None:
-        rate = roof["work_per_launch"] / (prof_t["avg_us"] * 1e-6) / (1e12 if mfma_bound else 1e9)
-        roof["profile"] = {"avg_launch_us": round(prof_t["avg_us"], 2), "achieved": round(rate, 2),
+        # the profiled run's launches after its warm-up steps (the steady
+        # state this run times), else every launch
+        steady = prof_t.get("avg_us_steady")
+        prof_us = steady if steady else prof_t["avg_us"]
+        rate = roof["work_per_launch"] / (prof_us * 1e-6) / (1e12 if mfma_bound else 1e9)
+        roof["profile"] = {"avg_launch_us": round(prof_us, 2), "achieved": round(rate, 2),
                            "frac": round(rate / roof["peak"], 4),
+                           "launches": "after the profiled run's warm-up steps" if steady else "every launch",
+                           "avg_launch_us_every_launch": round(prof_t["avg_us"], 2),
                            "mfma_busy_pct": None if prof_m is None else round(prof_m["mfma_busy_pct"], 2),
                            "counted_mfma_flops_per_launch": None if prof_m is None else
                            prof_m["counted_flops_per_launch"],

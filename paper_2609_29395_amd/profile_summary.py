@@ -175,6 +175,23 @@ def profile_entry(workload, label, kind):
     return e
 
 
+def steady_averages(trace_dir, warmup):
+    """Per label, the mean launch duration (us) over the launches that start
+    after the warm-up steps of the bench run: the sampler runs once per step,
+    so its (warmup + 1)-th launch starts the first step after the warm-up."""
+    try:
+        rows = list(csv.DictReader(open(_one(os.path.join(trace_dir, "**", "*kernel_trace.csv")))))
+    except FileNotFoundError:
+        return {}
+    starts = sorted(int(r["Start_Timestamp"]) for r in rows if "sample_kernel" in r["Kernel_Name"])
+    t0 = starts[warmup] if 0 < warmup < len(starts) else 0
+    by = collections.defaultdict(list)
+    for r in rows:
+        if int(r["Start_Timestamp"]) >= t0:
+            by[kernel_label(r["Kernel_Name"])].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    return {lab: sum(v) / len(v) for lab, v in by.items()}
+
+
 def stats(trace_dir, workload, out_md, cmd):
     rows = list(csv.DictReader(open(_one(os.path.join(trace_dir, "**", "*kernel_stats.csv")))))
     total = sum(float(r["TotalDurationNs"]) for r in rows)
@@ -185,15 +202,22 @@ def stats(trace_dir, workload, out_md, cmd):
         v = by[kernel_label(r["Name"])]
         v[0] += int(r["Calls"])
         v[1] += float(r["TotalDurationNs"])
+    m = re.search(r"--warmup (\d+)", " ".join(cmd))
+    warmup = int(m.group(1)) if m else 0
+    steady = steady_averages(trace_dir, warmup)
     lines = [f"# Kernel time summary, {workload}", "", f"Command: `{' '.join(cmd)}`", "",
-             "| kernel (label) | calls | total ms | avg us | % |", "|---|---|---|---|---|"]
+             f"avg us: every launch of the run (rocprofv3 --stats); after warm-up: the launches of the steps "
+             f"after the run's {warmup} warm-up steps (kernel trace), the steady state the bench times.", "",
+             "| kernel (label) | calls | total ms | avg us | avg us after warm-up | % |", "|---|---|---|---|---|---|"]
     for lab, (calls, tot) in sorted(by.items(), key=lambda kv: -kv[1][1]):
-        lines.append(f"| {lab} | {calls} | {tot / 1e6:.3f} | {tot / calls / 1e3:.2f} | {100 * tot / total:.2f} |")
+        st = f"{steady[lab]:.2f}" if lab in steady else "-"
+        lines.append(f"| {lab} | {calls} | {tot / 1e6:.3f} | {tot / calls / 1e3:.2f} | {st} | {100 * tot / total:.2f} |")
     lines += ["", f"Sum of kernel time: {total / 1e6:.3f} ms", ""]
     with open(out_md, "w") as fh:
         fh.write("\n".join(lines))
     print("\n".join(lines))
-    _update_profile(workload, "trace", {lab: {"calls": c, "avg_us": t / c / 1e3} for lab, (c, t) in by.items()
+    _update_profile(workload, "trace", {lab: {"calls": c, "avg_us": t / c / 1e3, "avg_us_steady": steady.get(lab)}
+                                        for lab, (c, t) in by.items()
                                         if not lab.startswith(("elementwise", "vectorized", "__amd"))})
 
 

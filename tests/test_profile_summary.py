@@ -84,15 +84,24 @@ def test_stats_merges_rows_with_one_label(tmp_path):
     _write(str(d / "host" / "run_kernel_stats.csv"), ["Name", "Calls", "TotalDurationNs", "AverageNs"],
            [[HALO.format(""), 3, 3000.0, 1000.0], [HALO.format(", true"), 1, 2000.0, 2000.0],
             ["sgd_kernel<4>", 2, 1000.0, 500.0]])
+    # the trace: one sampler launch per step (steps at 0, 10000, 20000 ns);
+    # with one warm-up step only the launches from 10000 ns on count for the
+    # steady-state column: (1000 + 2000 + 2000) / 3 ns
+    _write(str(d / "host" / "run_kernel_trace.csv"), ["Kernel_Name", "Start_Timestamp", "End_Timestamp"],
+           [["sample_kernel(int const*)", 0, 100], ["sample_kernel(int const*)", 10000, 10100],
+            ["sample_kernel(int const*)", 20000, 20100],
+            [HALO.format(""), 200, 200 + 0], [HALO.format(""), 10200, 11200], [HALO.format(""), 20200, 22200],
+            [HALO.format(", true"), 21000, 23000], ["sgd_kernel<4>", 500, 1000], ["sgd_kernel<4>", 20500, 21000]])
     out = tmp_path / "stats.md"
-    ps.stats(str(d), "wl", str(out), ["cmd"])
+    ps.stats(str(d), "wl", str(out), ["bench.py --warmup 1"])
     rows = [l for l in out.read_text().splitlines() if l.startswith("| conv_fwd")]
     assert len(rows) == 1
     cells = [c.strip() for c in rows[0].strip("|").split("|")]
     # 4 calls, 5000 ns in all, 1250 ns = 1.25 us each, 5000 / 6000 of the time
-    assert cells[1:] == ["4", "0.005", "1.25", "83.33"]
+    assert cells[1:] == ["4", "0.005", "1.25", "1.67", "83.33"]
     e = ps.profile_entry("wl", "conv_fwd<bf16,256x256x64,w16,halo>", "trace")
     assert e["calls"] == 4 and e["avg_us"] == pytest.approx(1.25)
+    assert e["avg_us_steady"] == pytest.approx(5000 / 3 / 1e3)
 
 
 @pytest.fixture(autouse=True)
