@@ -41,12 +41,13 @@ constexpr uint32_t kOob = 0x80000000u;
 constexpr int kBufferFlags = 0x00020000;
 
 constexpr int IMG = 32;                    // image side
-constexpr int TROWS = 8;                   // image rows per workgroup tile (256 pixels)
-constexpr int HP = IMG + 2, HR = TROWS + 2;  // halo row width, halo image rows
-constexpr int HPIX = HR * HP;              // 340 halo pixels
-constexpr int NTHR = 512;                  // 8 waves: wave w computes image row w of the tile
+constexpr int HP = IMG + 2;                // halo row width
+constexpr int NTHR = 512;                  // 8 waves: wave w computes image rows RPW w .. RPW w + RPW - 1
 
-template <int CS, int NO> struct ImgCfg {
+// RPW image rows per wave: a tile of 8 RPW image rows (256 RPW pixels)
+template <int CS, int NO, int RPW = 1> struct ImgCfg {
+  static constexpr int TROWS = 8 * RPW;                          // image rows per workgroup tile
+  static constexpr int HR = TROWS + 2, HPIX = HR * HP;           // halo image rows, halo pixels
   static constexpr int RB = CS * 2;                              // bytes per halo pixel row
   static constexpr int CPR = RB / 16;                            // 16-byte chunks per halo row
   static constexpr int H_BYTES = ((HPIX * RB + 1023) / 1024) * 1024;
@@ -79,10 +80,13 @@ __device__ __forceinline__ void mma(f32x4_t &acc, const u32x4 &a, const u32x4 &b
 
 __device__ __forceinline__ float bf2f(uint32_t bits16) { return bf16_to_f32((bf16_t)bits16); }
 
-template <int CS, int NO, int EPI>
-__global__ void __launch_bounds__(NTHR)
+// (two rows per wave: at least four waves per SIMD, i.e. at most 128
+// registers, so that two workgroups share a CU)
+template <int CS, int NO, int EPI, int RPW = 1>
+__global__ void __launch_bounds__(NTHR, RPW == 2 ? 4 : 1)
 conv_img_kernel(ConvArgs a, int MT) {
-  using CF = ImgCfg<CS, NO>;
+  using CF = ImgCfg<CS, NO, RPW>;
+  constexpr int TROWS = CF::TROWS, HPIX = CF::HPIX;
   constexpr int TN = CF::TN, KG = CF::KG;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -168,12 +172,15 @@ conv_img_kernel(ConvArgs a, int MT) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
-  // ---- nine taps x KG k groups from LDS: wave = image row `wave` of the tile
+  // ---- nine taps x KG k groups from LDS: wave = image rows RPW wave ..
+  // RPW wave + RPW - 1 of the tile; pixel fragment tm = 2 rr + half is
+  // pixels 16 half .. 16 half + 15 of row rr
+  constexpr int TMW = 2 * RPW;  // pixel fragments per wave
   const int li = lane & 15, lg = lane >> 4;
   const uint32_t lds0 = (uint32_t)(size_t)LDS_PTR(smem);
-  f32x4_t acc[2][TN];
+  f32x4_t acc[TMW][TN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TMW; ++i)
 #pragma unroll
     for (int k = 0; k < TN; ++k) acc[i][k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -181,7 +188,7 @@ conv_img_kernel(ConvArgs a, int MT) {
     const int r = tap / 3, s = tap % 3;
 #pragma unroll
     for (int g = 0; g < KG; ++g) {
-      u32x4 w[TN], x[2];
+      u32x4 w[TN], x[TMW];
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
         const int row = tn * 16 + li;
@@ -190,9 +197,9 @@ conv_img_kernel(ConvArgs a, int MT) {
         asm volatile("ds_read_b128 %0, %1" : "=v"(w[tn]) : "v"(ad));
       }
 #pragma unroll
-      for (int tm = 0; tm < 2; ++tm) {
-        const int wp = tm * 16 + li + s;
-        const int R = (wave + r) * HP + wp;
+      for (int tm = 0; tm < TMW; ++tm) {
+        const int wp = (tm & 1) * 16 + li + s;
+        const int R = (RPW * wave + (tm >> 1) + r) * HP + wp;
         const uint32_t ad = lds0 + (uint32_t)(R * CF::RB + (((4 * g + lg) ^ (wp & (CF::CPR - 1))) * 16));
         asm volatile("ds_read_b128 %0, %1" : "=v"(x[tm]) : "v"(ad));
       }
@@ -200,24 +207,25 @@ conv_img_kernel(ConvArgs a, int MT) {
 #pragma unroll
       for (int i = 0; i < TN; ++i) asm volatile("" : "+v"(w[i]));
 #pragma unroll
-      for (int i = 0; i < 2; ++i) asm volatile("" : "+v"(x[i]));
+      for (int i = 0; i < TMW; ++i) asm volatile("" : "+v"(x[i]));
 #pragma unroll
-      for (int tm = 0; tm < 2; ++tm)
+      for (int tm = 0; tm < TMW; ++tm)
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) mma(acc[tm][tn], w[tn], x[tm]);
     }
   }
 
-  // ---- epilogue: lane holds channels tn*16 + 4*lg .. +3 of pixel tm*16 + li.
-  // The wave's 32 x NO bf16 results are staged in LDS (its own 32-row
-  // region, 16-byte chunk c of pixel row p at c ^ (p mod chunks per row)) and
-  // read back as 16-byte pieces, so every store instruction writes 8 (NO=64)
-  // or 16 (NO=32) whole pixel rows, 1 KB contiguous.
+  // ---- epilogue: lane holds channels tn*16 + 4*lg .. +3 of pixel tm*16 + li
+  // of the wave's rows.  The wave's 32 RPW x NO bf16 results are staged in LDS
+  // (its own 32 RPW-row region, 16-byte chunk c of pixel row p at c ^ (p mod
+  // chunks per row)) and read back as 16-byte pieces, so every store
+  // instruction writes 8 (NO=64) or 16 (NO=32) whole pixel rows, 1 KB
+  // contiguous.
   constexpr int OCH = NO / 8;             // 16-byte chunks per output pixel row
   constexpr int OROW = NO * 2;            // bytes per output pixel row
   bf16_t *out = reinterpret_cast<bf16_t *>(a.out) + rep * a.out_rs;
-  const int pbase = m0 + wave * IMG;      // first pixel of this wave's image row
-  const uint32_t stg = lds0 + (uint32_t)(wave * IMG * OROW);
+  const int pbase = m0 + wave * RPW * IMG;  // first pixel of this wave's image rows
+  const uint32_t stg = lds0 + (uint32_t)(wave * RPW * IMG * OROW);
   float bias[TN][4];
 #pragma unroll
   for (int tn = 0; tn < TN; ++tn)
@@ -226,7 +234,7 @@ conv_img_kernel(ConvArgs a, int MT) {
       bias[tn][e] = EPI == EPI_FWD ? a.bias[rep * a.bias_rs + tn * 16 + 4 * lg + e] : 0.f;
   __syncthreads();  // every wave is done with the halo and weight tiles
 #pragma unroll
-  for (int tm = 0; tm < 2; ++tm)
+  for (int tm = 0; tm < TMW; ++tm)
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) {
       float v[4];
@@ -242,16 +250,17 @@ conv_img_kernel(ConvArgs a, int MT) {
       const uint32_t ad = stg + (uint32_t)(px * OROW + ((c ^ (px & (OCH - 1))) * 16) + (lg & 1) * 8);
       asm volatile("ds_write_b64 %0, %1" ::"v"(ad), "v"(o) : "memory");
     }
-  // The max pool reads the neighbouring wave's row too: every wave's staged
-  // rows must have landed before the barrier (the compiler does not count
-  // the asm writes, so the barrier alone does not wait for them).
+  // With one row per wave the max pool reads the neighbouring wave's row
+  // too: every wave's staged rows must have landed before the barrier (the
+  // compiler does not count the asm writes, so the barrier alone does not
+  // wait for them).
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   __syncthreads();
   // dgrad: ReLU mask of the layer below (value > 0), read in the same
   // 16-byte pieces; without a mask source every value passes
   const bf16_t *msk = (EPI == EPI_DGRAD && a.mask) ? reinterpret_cast<const bf16_t *>(a.mask) + rep * a.out_rs
                                                    : nullptr;
-  constexpr int QN = IMG * OCH / 64;      // pieces per lane
+  constexpr int QN = RPW * IMG * OCH / 64;  // pieces per lane
   u32x4 mv[QN];
 #pragma unroll
   for (int q = 0; q < QN; ++q) {
@@ -279,12 +288,17 @@ conv_img_kernel(ConvArgs a, int MT) {
     *reinterpret_cast<u32x4 *>(out + (int64_t)(pbase + px) * NO + 8 * c) = v;
   }
   if (EPI == EPI_FWD && a.pool_out) {
-    // 2 x 2 max pool: waves 2k and 2k+1 hold image rows h0+2k, h0+2k+1; each
-    // takes 8 of the 16 pooled pixels of pooled row h0/2 + k, one 16-byte
-    // channel chunk per lane (the maximum of bf16 values is exact)
-    const int pw = (wave & 1) * 8 + lane / OCH, c = lane % OCH;
+   // 2 x 2 max pool, one 16-byte channel chunk per lane (the maximum of bf16
+   // values is exact).  One row per wave: waves 2k and 2k+1 hold image rows
+   // h0+2k, h0+2k+1 and each takes 8 of the 16 pooled pixels of pooled row
+   // h0/2 + k.  Two rows per wave: wave k holds both rows of pooled row
+   // h0/2 + k and takes its 16 pooled pixels, 8 per pass.
+#pragma unroll
+   for (int ps = 0; ps < RPW; ++ps) {
+    const int pw = (RPW == 1 ? (wave & 1) * 8 : ps * 8) + lane / OCH, c = lane % OCH;
     if (lane < 8 * OCH) {
-      const uint32_t r0 = lds0 + (uint32_t)((wave & ~1) * IMG * OROW), r1 = r0 + (uint32_t)(IMG * OROW);
+      const uint32_t r0 = RPW == 1 ? lds0 + (uint32_t)((wave & ~1) * IMG * OROW) : stg;
+      const uint32_t r1 = r0 + (uint32_t)(IMG * OROW);
       u32x4 q4[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -311,11 +325,12 @@ conv_img_kernel(ConvArgs a, int MT) {
         code[d >> 1] |= (alo | (ahi << 8)) << (16 * (d & 1));
       }
       bf16_t *zo = reinterpret_cast<bf16_t *>(a.pool_out) + rep * a.pool_rs;
-      const int b = m0 / (IMG * IMG), hz = h0 / 2 + (wave >> 1);
+      const int b = m0 / (IMG * IMG), hz = h0 / 2 + (RPW == 1 ? (wave >> 1) : wave);
       const int64_t zi = ((int64_t)(b * (IMG / 2) + hz) * (IMG / 2) + pw) * NO + 8 * c;
       *reinterpret_cast<u32x4 *>(zo + zi) = z;
       if (a.pool_code) *reinterpret_cast<u32x2 *>(a.pool_code + rep * a.pool_rs + zi) = code;
     }
+   }
   }
 }
 
@@ -484,31 +499,41 @@ bool conv_img_ok(int dtype, const ConvArgs &a) {
 // Every instantiation is named in this (non-template) function.
 hipError_t launch_conv_img(const ConvArgs &a, hipStream_t s, std::string *label) {
   if (!conv_img_ok(GCPSL_BF16, a)) return hipErrorInvalidValue;
-  const int MT = a.Bt * IMG / TROWS;  // tiles of 8 image rows per replica
+  // the forward of a 32-channel input takes two image rows per wave (16-row
+  // tiles, so the weight matrix is staged once per 512 pixels); a 64-channel
+  // input's 18-row halo would not leave room for two workgroups per CU
+  const int rpw = (a.epi == EPI_FWD && a.Csrc == 32) ? 2 : 1;
+  const int MT = a.Bt * IMG / (8 * rpw);  // tiles of 8 rpw image rows per replica
   const dim3 g((uint32_t)MT * a.C);
   if (label)
-    *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16,256x" + std::to_string(a.N) +
-             "x" + std::to_string(9 * a.Csrc) + ",w8,img>";
-#define IMG_GO(CS, NO)                                                                                        \
-  do {                                                                                                        \
-    if (a.epi == EPI_FWD)                                                                                     \
-      hipLaunchKernelGGL((conv_img_kernel<CS, NO, EPI_FWD>), g, dim3(NTHR), (ImgCfg<CS, NO>::LDS), s, a, MT);   \
-    else                                                                                                      \
-      hipLaunchKernelGGL((conv_img_kernel<CS, NO, EPI_DGRAD>), g, dim3(NTHR), (ImgCfg<CS, NO>::LDS), s, a, MT); \
-  } while (0)
-  static_assert(ImgCfg<32, 32>::FITS2 && ImgCfg<32, 64>::FITS2 && ImgCfg<64, 32>::FITS2, "two per CU");
+    *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16," + std::to_string(256 * rpw) +
+             "x" + std::to_string(a.N) + "x" + std::to_string(9 * a.Csrc) + ",w8,img>";
+#define IMG_GO(CS, NO, E, RPW) \
+  hipLaunchKernelGGL((conv_img_kernel<CS, NO, E, RPW>), g, dim3(NTHR), (ImgCfg<CS, NO, RPW>::LDS), s, a, MT)
+  static_assert(ImgCfg<32, 32, 2>::FITS2 && ImgCfg<32, 64, 2>::FITS2 && ImgCfg<32, 32>::FITS2 &&
+                    ImgCfg<32, 64>::FITS2 && ImgCfg<64, 32>::FITS2,
+                "two per CU");
   static PerDeviceOnce attr;
   if (attr.needed()) {
-    for (const void *f : {reinterpret_cast<const void *>(&conv_img_kernel<64, 32, EPI_FWD>),
-                          reinterpret_cast<const void *>(&conv_img_kernel<64, 32, EPI_DGRAD>)}) {
+    for (const void *f : {reinterpret_cast<const void *>(&conv_img_kernel<64, 32, EPI_FWD, 1>),
+                          reinterpret_cast<const void *>(&conv_img_kernel<64, 32, EPI_DGRAD, 1>)}) {
       const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, ImgCfg<64, 32>::LDS);
       if (e != hipSuccess) return e;
     }
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&conv_img_kernel<32, 64, EPI_FWD, 2>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, ImgCfg<32, 64, 2>::LDS);
+    if (e != hipSuccess) return e;
     attr.mark();
   }
-  if (a.Csrc == 32 && a.N == 32) IMG_GO(32, 32);
-  else if (a.Csrc == 32) IMG_GO(32, 64);
-  else IMG_GO(64, 32);
+  if (a.epi == EPI_FWD) {
+    if (a.Csrc == 32 && a.N == 32) IMG_GO(32, 32, EPI_FWD, 2);
+    else if (a.Csrc == 32) IMG_GO(32, 64, EPI_FWD, 2);
+    else IMG_GO(64, 32, EPI_FWD, 1);
+  } else {
+    if (a.Csrc == 32 && a.N == 32) IMG_GO(32, 32, EPI_DGRAD, 1);
+    else if (a.Csrc == 32) IMG_GO(32, 64, EPI_DGRAD, 1);
+    else IMG_GO(64, 32, EPI_DGRAD, 1);
+  }
 #undef IMG_GO
   return hipGetLastError();
 }

@@ -69,10 +69,11 @@ def kernel_label(name: str) -> str:
             return f"{kind}<bf16,{m.group(1)}x{m.group(2)}x64,w{w},halo1>"
         kt = 192 if (mode == "halo" and m.group(2) == "64") else 64  # tap-row k tiles
         return f"{kind}<bf16,{m.group(1)}x{m.group(2)}x{kt},w{w},{mode}>"
-    m = re.search(r"conv_img_kernel<(\d+), (\d+), (\d)>", name)
-    if m:
+    m = re.search(r"conv_img_kernel<(\d+), (\d+), (\d)(, (\d))?>", name)
+    if m:  # (a last argument: image rows per wave, 256 pixels per tile each)
         kind = "conv_fwd" if m.group(3) == "0" else "conv_dgrad"
-        return f"{kind}<bf16,256x{m.group(2)}x{9 * int(m.group(1))},w8,img>"
+        tile = 256 * int(m.group(5) or 1)
+        return f"{kind}<bf16,{tile}x{m.group(2)}x{9 * int(m.group(1))},w8,img>"
     m = re.search(r"wgrad_col_kernel(<(true|false)>)?", name)
     if m:
         return "conv_wgrad<bf16,32x27,w4,img3>" if m.group(2) == "true" else "conv_wgrad<bf16,32x32,w4,col>"

@@ -17,9 +17,17 @@ from gpu_match import TOL, bar, LazyChoices, close, compare_params, master_ulp  
 from test_gpu_parity import check_metrics  # noqa: E402
 
 
-@pytest.mark.parametrize("name", ["tiny_epoch", "ragged_epoch", "ragged_bf16_epoch"])
+# the routing-code paths under the epoch schedule (replicas addressed
+# through the slot map, a waiting cluster): the image-side layer's codes
+# (img32_bf16) and the head's (halo_maxhead_bf16), with data and batch
+# sizes that make an epoch a few rounds long
+CODES_EPOCH = {"img32_bf16": dict(schedule="epoch", B=48, N_ex=322, T=6),
+               "halo_maxhead_bf16": dict(schedule="epoch", B=24, N_ex=203, T=7)}
+
+
+@pytest.mark.parametrize("name", ["tiny_epoch", "ragged_epoch", "ragged_bf16_epoch", *CODES_EPOCH])
 def test_epoch_schedule_parity(name):
-    cfg = get_config(name)
+    cfg = get_config(name, **CODES_EPOCH.get(name, {}))
     T = cfg["T"]
     print(f"epoch schedule parity: {name} T={T}", flush=True)
     ctx, assignment = driver.setup(cfg)
@@ -80,11 +88,12 @@ def _run(cfg, T, serial):
     return ctx, losses.cpu().numpy()
 
 
-@pytest.mark.parametrize("name", ["tiny_epoch", "ragged_bf16_epoch", "ragged", "ragged_bf16", "tiny_norm"])
+@pytest.mark.parametrize("name", ["tiny_epoch", "ragged_bf16_epoch", "ragged", "ragged_bf16", "tiny_norm",
+                                  *CODES_EPOCH])
 def test_sequential_equals_concurrent_bit_for_bit(name):
     # Eq. 6 compares running the cluster workloads one after another with
     # running them side by side: the same rounds, so the same results
-    cfg = get_config(name)
+    cfg = get_config(name, **CODES_EPOCH.get(name, {}))
     T = cfg["T"]
     print(f"sequential vs concurrent: {name} T={T}", flush=True)
     a, la = _run(cfg, T, serial=False)

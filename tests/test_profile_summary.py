@@ -43,6 +43,8 @@ def test_image_layer_labels():
     assert ps.kernel_label(ns + "conv_col_kernel<false>(ConvArgs, int)") == "conv_fwd<bf16,256x32x32,w4,col>"
     assert ps.kernel_label(ns + "wgrad_col_kernel<true>(WgradArgs)") == "conv_wgrad<bf16,32x27,w4,img3>"
     assert ps.kernel_label(ns + "wgrad_col_kernel<false>(WgradArgs)") == "conv_wgrad<bf16,32x32,w4,col>"
+    assert ps.kernel_label(ns + "conv_img_kernel<32, 64, 0, 2>(ConvArgs, int)") == "conv_fwd<bf16,512x64x288,w8,img>"
+    assert ps.kernel_label(ns + "conv_img_kernel<64, 32, 1, 1>(ConvArgs, int)") == "conv_dgrad<bf16,256x32x576,w8,img>"
     assert ps.kernel_label(ns + "wgrad_img_kernel<3, false>(WgradArgs)") == "conv_wgrad<bf16,64x288,w8,img>"
     assert ps.kernel_label(ns + "wgrad_img_kernel<3, true>(WgradArgs)") == "conv_wgrad<bf16,64x288,w8,img,pool>"
 
@@ -55,7 +57,7 @@ def test_image_layer_labels():
     ("conv_fwd<bf16,256x32x27,w4,img3>", "k_conv_img.hip"),
     ("conv_wgrad<bf16,32x27,w4,img3>", "k_wgrad_lds.hip"),
     ("conv_wgrad<bf16,64x288,w8,img,pool>", "k_wgrad_lds.hip"),
-    ("conv_fwd<bf16,256x64x288,w8,img>", "k_conv_img.hip"),
+    ("conv_fwd<bf16,512x64x288,w8,img>", "k_conv_img.hip"),
     ("conv_fwd<f32,128x128x32,w4,vec>", "k_conv.hip"),
     ("sgd", "k_misc.hip"),
     ("fuse", "k_misc.hip"),
