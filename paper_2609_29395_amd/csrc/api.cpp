@@ -64,6 +64,9 @@ struct LayerInfo {
   // backward routes through them, so its output is not kept (gpre is)
   bool hcode = false;
   size_t code_off = 0;
+  // splits > 1: this layer's split-K partials of the weights and the biases,
+  // in floats from Plan::off_part (the SGD pass sums them)
+  size_t part_off = 0, dbpart_off = 0;
 };
 
 // A ResNet basic block (GCPSL_BLOCK) as internal layers, each with its own
@@ -105,8 +108,13 @@ struct Plan {
   int schedule = GCPSL_SCHED_LOCKSTEP;
   int cut = 0;
   size_t off_ids = 0, off_off = 0, off_coe = 0, off_fw = 0, off_hits = 0, off_idx = 0, off_y = 0,
-         off_x = 0, off_dh = 0, off_grad = 0, off_part = 0, off_dbpart = 0, off_loss = 0, off_order = 0,
-         off_ident = 0, off_npart = 0, off_dev = 0, off_ghist = 0;
+         off_x = 0, off_dh = 0, off_grad = 0, off_part = 0, off_loss = 0, off_order = 0,
+         off_ident = 0, off_npart = 0, off_dev = 0, off_ghist = 0, off_sgdseg = 0;
+  // the SGD pass in segments of the parameter vector (SgdSeg): the split-K
+  // partials of every split layer are summed there; uploaded at creation
+  std::vector<SgdSeg> sgd_segs;
+  int sgd_blocks = 0, sgd_vec = 1;
+  double sgd_part_bytes = 0.0;  // partial floats the pass reads per step, in bytes
   size_t total = 0;
 };
 
@@ -312,7 +320,8 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   }
   p.x_rs = (int64_t)C * B * p.H * p.W * p.Kc;
   p.off_x = take((size_t)p.esz * p.max_window * p.x_rs);
-  size_t part = 0, dbpart = 0, npart = 0;
+  size_t part = 0, npart = 0;
+  std::vector<const LayerInfo *> split_layers;
   // split-K over pixels for a weight gradient of M pixels per replica with
   // Ci_eff columns per tap (taps 9, or 1 on im2col rows)
   auto plan_wgrad = [&](LayerInfo &l, int M, int Ci_eff, int taps, int Hh, int Ww) {
@@ -349,9 +358,12 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
     const int per = (nkt + splits - 1) / splits;
     l.chunk = per * kt;
     l.splits = (M + l.chunk - 1) / l.chunk;
-    if (l.splits > 1) {
-      part = std::max(part, (size_t)l.splits * C * l.nw);
-      dbpart = std::max(dbpart, (size_t)l.splits * C * l.Co);
+    if (l.splits > 1) {  // its own partials, 16-byte aligned, weights then biases
+      l.part_off = part;
+      part = (part + (size_t)l.splits * C * l.nw + 3) / 4 * 4;
+      l.dbpart_off = part;
+      part = (part + (size_t)l.splits * C * l.Co + 3) / 4 * 4;
+      split_layers.push_back(&l);
     }
   };
   // kernels address one replica's tensors with 32-bit byte offsets and mark
@@ -505,7 +517,40 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
   p.off_dh = take(sizeof(float) * (size_t)C * B * p.Ch_head);
   p.off_grad = take(sizeof(float) * (size_t)C * p.P);
   p.off_part = take(sizeof(float) * std::max<size_t>(part, 1));
-  p.off_dbpart = take(sizeof(float) * std::max<size_t>(dbpart, 1));
+  {
+    // SGD segments: each split layer's weights and biases from its partials,
+    // the rest of the parameter vector from grad; kSgdBlockElems per block
+    std::vector<SgdSeg> segs;
+    for (const LayerInfo *l : split_layers) {
+      segs.push_back(SgdSeg{l->w_off, l->nw, (int64_t)l->part_off, (int64_t)C * l->nw, l->nw, l->splits, 0});
+      segs.push_back(SgdSeg{l->b_off, l->Co, (int64_t)l->dbpart_off, (int64_t)C * l->Co, l->Co, l->splits, 0});
+      p.sgd_part_bytes += 4.0 * C * l->splits * (l->nw + l->Co);
+    }
+    std::sort(segs.begin(), segs.end(), [](const SgdSeg &a, const SgdSeg &b) { return a.begin < b.begin; });
+    int64_t at = 0;
+    for (const SgdSeg &g : segs) {
+      if (g.begin < at) return gcpsl_fail(GCPSL_EUNSUPPORTED, "overlapping parameter segments");
+      if (g.begin > at) p.sgd_segs.push_back(SgdSeg{at, g.begin - at, 0, 0, 0, 0, 0});
+      p.sgd_segs.push_back(g);
+      at = g.begin + g.len;
+    }
+    if (at > p.P) return gcpsl_fail(GCPSL_EUNSUPPORTED, "parameter segments beyond P");
+    if (at < p.P) p.sgd_segs.push_back(SgdSeg{at, p.P - at, 0, 0, 0, 0, 0});
+    p.sgd_vec = 4;
+    for (const SgdSeg &g : p.sgd_segs) {
+      const int64_t any = g.begin | g.len | g.src | g.ss | g.rs | p.P;
+      while (any % p.sgd_vec) p.sgd_vec /= 2;
+    }
+    int64_t blocks = 0;
+    for (SgdSeg &g : p.sgd_segs) {
+      const int64_t be = g.splits > 0 ? 256 * p.sgd_vec : kSgdBlockElems;
+      g.first_block = (int32_t)blocks;
+      blocks += (g.len + be - 1) / be;
+    }
+    if (blocks > INT32_MAX / 2) return gcpsl_fail(GCPSL_EUNSUPPORTED, "parameter vector too long");
+    p.sgd_blocks = (int)blocks;
+    p.off_sgdseg = take(sizeof(SgdSeg) * p.sgd_segs.size());
+  }
   p.off_loss = take(sizeof(float) * C);
   p.off_npart = take(sizeof(double) * std::max<size_t>(npart, 1));
   p.total = o;
@@ -768,6 +813,7 @@ int create_ctx(const gcpsl_desc *d, char *ws, size_t ws_bytes, gcpsl_ctx **out) 
   std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return rounds[a] > rounds[b]; });
   HIP_TRY(hipMemcpy(ws + p.off_order, order.data(), sizeof(int32_t) * p.C, hipMemcpyHostToDevice));
   HIP_TRY(hipMemcpy(ws + p.off_ident, ident.data(), sizeof(int32_t) * p.C, hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(ws + p.off_sgdseg, p.sgd_segs.data(), sizeof(SgdSeg) * p.sgd_segs.size(), hipMemcpyHostToDevice));
   gcpsl_ctx *ctx = new gcpsl_ctx();
   ctx->plan = std::move(p);
   ctx->desc = *d;
@@ -1009,9 +1055,9 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
     if (cv.splits == 1) {
       w.dw = grad + cv.w_off; w.dw_rs = p.P; w.dw_ss = 0;
       w.db = grad + cv.b_off; w.db_rs = p.P; w.db_ss = 0;
-    } else {
-      w.dw = ctx->at<float>(p.off_part); w.dw_rs = cv.nw; w.dw_ss = (int64_t)p.C * cv.nw;
-      w.db = ctx->at<float>(p.off_dbpart); w.db_rs = cv.Co; w.db_ss = (int64_t)p.C * cv.Co;
+    } else {  // the layer's own partials, summed by the SGD pass
+      w.dw = ctx->at<float>(p.off_part) + cv.part_off; w.dw_rs = cv.nw; w.dw_ss = (int64_t)p.C * cv.nw;
+      w.db = ctx->at<float>(p.off_part) + cv.dbpart_off; w.db_rs = cv.Co; w.db_ss = (int64_t)p.C * cv.Co;
     }
     {
       std::string lab;
@@ -1021,10 +1067,6 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
       tend(ctx, s, t_, lab, 2.0 * C * M * cv.nw,
            (double)C * (p.esz * M * (cv.Co + cv.Ci) + 4.0 * cv.splits * (cv.nw + cv.Co)));
     }
-    if (cv.splits > 1)
-      LAUNCH_T("wgrad_reduce", 0.0, 4.0 * C * (cv.nw + cv.Co) * (cv.splits + 1.0),
-               launch_wgrad_reduce(w.dw, w.db, cv.splits, w.dw_ss, w.dw_rs, w.db_ss, w.db_rs, grad, p.P, cv.w_off,
-                                   cv.b_off, cv.nw, cv.Co, C, rmap, s));
     return GCPSL_OK;
   };
   bool pool_done = false;  // the max pool after the last conv was written by it
@@ -1238,9 +1280,9 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
     if (l.splits == 1) {
       w.dw = grad + l.w_off; w.dw_rs = p.P; w.dw_ss = 0;
       w.db = grad + l.b_off; w.db_rs = p.P; w.db_ss = 0;
-    } else {
-      w.dw = ctx->at<float>(p.off_part); w.dw_rs = l.nw; w.dw_ss = (int64_t)p.C * l.nw;
-      w.db = ctx->at<float>(p.off_dbpart); w.db_rs = l.Co; w.db_ss = (int64_t)p.C * l.Co;
+    } else {  // the layer's own partials, summed by the SGD pass
+      w.dw = ctx->at<float>(p.off_part) + l.part_off; w.dw_rs = l.nw; w.dw_ss = (int64_t)p.C * l.nw;
+      w.db = ctx->at<float>(p.off_part) + l.dbpart_off; w.db_rs = l.Co; w.db_ss = (int64_t)p.C * l.Co;
     }
     {
       std::string lab;
@@ -1252,10 +1294,6 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
       LAUNCH(launch_wgrad(p.dtype, w, s, &lab));
       tend(ctx, s, t_, lab, fl, by);
     }
-    if (l.splits > 1)
-      LAUNCH_T("wgrad_reduce", 0.0, 4.0 * C * (l.nw + l.Co) * (l.splits + 1.0),
-               launch_wgrad_reduce(w.dw, w.db, l.splits, w.dw_ss, w.dw_rs, w.db_ss, w.db_rs, grad, p.P, l.w_off,
-                                   l.b_off, l.nw, l.Co, C, rmap, s));
     if (i == 0) break;
     // input gradient (the cut gradient when layer i-1 is the client's last pool)
     const LayerInfo &prev = p.ly[i - 1];
@@ -1300,9 +1338,13 @@ int run_round(gcpsl_ctx *ctx, int64_t step, const int32_t *rmap, int nrep, float
     }
   }
 
-  LAUNCH_T("sgd", 3.0 * C * p.P, 20.0 * C * p.P,
-           launch_sgd(d.theta, d.momentum_buf, grad, p.P, C, rmap, d.lr, d.momentum, d.weight_decay,
-                      d.nesterov, s));
+  // the update, with the split-K sums of the split layers' weight gradients
+  // (20 bytes per parameter and the partials)
+  LAUNCH_T("sgd", 3.0 * C * p.P, 20.0 * C * p.P + p.sgd_part_bytes,
+           launch_sgd_seg(d.theta, d.momentum_buf, grad, ctx->at<float>(p.off_part),
+                          reinterpret_cast<const SgdSeg *>(ctx->ws + p.off_sgdseg), (int)p.sgd_segs.size(),
+                          p.sgd_blocks, p.sgd_vec, 256 * p.sgd_vec, p.P, C, rmap, d.lr, d.momentum,
+                          d.weight_decay, d.nesterov, s));
   ctx->horizon = std::max<int64_t>(ctx->horizon, std::min<int64_t>(step + 1, p.max_steps));
   return GCPSL_OK;
 }

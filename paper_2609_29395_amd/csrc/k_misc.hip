@@ -1045,109 +1045,82 @@ head_pool_bwd_kernel(const T *__restrict__ a, const float *__restrict__ dh, T *_
   }
 }
 
-// ----------------------------------------------------- split-K reduction
-// grad[w_off + j] = sum over splits (in order) of the partial weight
-// gradients; grad[b_off + c] likewise for the bias.  The partials of 8
-// splits are loaded before they are added (in split order).
-__device__ __forceinline__ float ordered_sum(const float *__restrict__ p, int64_t stride, int splits) {
-  float s = 0.f;
-  int k = 0;
-  for (; k + 8 <= splits; k += 8) {
-    float v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = p[(k + u) * stride];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) s += v[u];
-  }
-  for (; k < splits; ++k) s += p[k * stride];
-  return s;
-}
-
-// Two consecutive weights per thread (every offset and stride even, so the
-// 8-byte accesses stay aligned); same order of additions as ordered_sum.
-__device__ __forceinline__ float2 ordered_sum2(const float *__restrict__ p, int64_t stride, int splits) {
-  float2 s = make_float2(0.f, 0.f);
-  int k = 0;
-  for (; k + 8 <= splits; k += 8) {
-    float2 v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = *reinterpret_cast<const float2 *>(p + (k + u) * stride);
-#pragma unroll
-    for (int u = 0; u < 8; ++u) s.x += v[u].x, s.y += v[u].y;
-  }
-  for (; k < splits; ++k) {
-    const float2 v = *reinterpret_cast<const float2 *>(p + k * stride);
-    s.x += v.x, s.y += v.y;
-  }
-  return s;
-}
-
-__global__ void __launch_bounds__(256)
-wgrad_reduce2_kernel(const float *__restrict__ dw, const float *__restrict__ db, int splits, int64_t dw_ss,
-                     int64_t dw_rs, int64_t db_ss, int64_t db_rs, float *__restrict__ grad, int64_t P,
-                     int64_t w_off, int64_t b_off, int64_t nw, int co, const int32_t *__restrict__ rmap) {
-  const int rep = replica_of(rmap, blockIdx.y);
-  const int64_t n2 = (nw + co) / 2;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n2; i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t j = 2 * i;
-    if (j < nw)
-      *reinterpret_cast<float2 *>(grad + rep * P + w_off + j) = ordered_sum2(dw + rep * dw_rs + j, dw_ss, splits);
-    else
-      *reinterpret_cast<float2 *>(grad + rep * P + b_off + (j - nw)) =
-          ordered_sum2(db + rep * db_rs + (j - nw), db_ss, splits);
-  }
-}
-
-__global__ void __launch_bounds__(256)
-wgrad_reduce_kernel(const float *__restrict__ dw, const float *__restrict__ db, int splits,
-                    int64_t dw_ss, int64_t dw_rs, int64_t db_ss, int64_t db_rs,
-                    float *__restrict__ grad, int64_t P, int64_t w_off, int64_t b_off, int64_t nw,
-                    int co, const int32_t *__restrict__ rmap) {
-  const int rep = replica_of(rmap, blockIdx.y);
-  for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < nw + co;
-       j += (int64_t)gridDim.x * blockDim.x) {
-    if (j < nw) {
-      grad[rep * P + w_off + j] = ordered_sum(dw + rep * dw_rs + j, dw_ss, splits);
-    } else {
-      const int64_t c = j - nw;
-      grad[rep * P + b_off + c] = ordered_sum(db + rep * db_rs + c, db_ss, splits);
-    }
-  }
-}
-
 // ------------------------------------------------------------------- SGD
 // g <- g + wd theta (weight decay); v <- mu v + g; theta <- theta - lr v, or
 // theta - lr (g + mu v) with the Nesterov term (Sec. V-A), on the P
 // parameters of the replica of slot blockIdx.y.  VEC divides P, so every
-// replica row stays aligned.
+// replica row stays aligned.  The pass runs by segments of the parameter
+// vector (sgd_seg_kernel) and also sums the split-K partials of the weight
+// gradients: the ordered sum over the splits, from zero in split order, the
+// partials of 8 splits loaded before they are added.
 template <int VEC> struct FVec;
 template <> struct FVec<1> { typedef float T; };
 template <> struct FVec<2> { typedef float2 T; };
 template <> struct FVec<4> { typedef float4 T; };
 
+// one parameter's update
+__device__ __forceinline__ void sgd_update(float &t, float &v, float g, float lr, float mu, float wd, int nesterov) {
+  const float ge = g + wd * t;
+  v = mu * v + ge;
+  t -= lr * (nesterov ? ge + mu * v : v);
+}
+
+// SGD by segments (SgdSeg): the split-K partials of a weight gradient are
+// summed here, in split order from zero (the partials of 8 splits loaded
+// before they are added), and the sum is written to grad before the update.
+// The block's segment is the last one whose first block is at most
+// blockIdx.x.
 template <int VEC>
 __global__ void __launch_bounds__(256)
-sgd_kernel(float *__restrict__ theta, float *__restrict__ mom, const float *__restrict__ grad, int64_t P,
-           const int32_t *__restrict__ rmap, float lr, float mu, float wd, int nesterov) {
+sgd_seg_kernel(float *__restrict__ theta, float *__restrict__ mom, float *__restrict__ grad,
+               const float *__restrict__ part, const SgdSeg *__restrict__ segs, int nseg, int split_elems,
+               int64_t P, const int32_t *__restrict__ rmap, float lr, float mu, float wd, int nesterov) {
   typedef typename FVec<VEC>::T V;
-  const int64_t base = (int64_t)replica_of(rmap, blockIdx.y) * P;
-  V *t4 = reinterpret_cast<V *>(theta + base);
-  V *m4 = reinterpret_cast<V *>(mom + base);
-  const V *g4 = reinterpret_cast<const V *>(grad + base);
-  const int64_t nv = P / VEC;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nv; i += (int64_t)gridDim.x * blockDim.x) {
-    V v = m4[i], t = t4[i];
-    const V g = g4[i];
+  int lo = 0, hi = nseg - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (segs[mid].first_block <= (int)blockIdx.x) lo = mid;
+    else hi = mid - 1;
+  }
+  const SgdSeg sg = segs[lo];
+  const int rep = replica_of(rmap, blockIdx.y);
+  const int64_t base = (int64_t)rep * P + sg.begin;
+  const int be = sg.splits > 0 ? split_elems : kSgdBlockElems;
+  const int64_t e0 = ((int64_t)blockIdx.x - sg.first_block) * be;
+  const int64_t e1 = min(sg.len, e0 + (int64_t)be);
+  const float *pr = part + sg.src + (int64_t)rep * sg.rs;
+  for (int64_t e = e0 + (int64_t)threadIdx.x * VEC; e < e1; e += 256 * VEC) {
+    V g;
+    if (sg.splits > 0) {
+      float *gs = reinterpret_cast<float *>(&g);
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) gs[q] = 0.f;
+      int k = 0;
+      for (; k + 8 <= sg.splits; k += 8) {
+        V pv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) pv[u] = *reinterpret_cast<const V *>(pr + (k + u) * sg.ss + e);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+          for (int q = 0; q < VEC; ++q) gs[q] += reinterpret_cast<const float *>(&pv[u])[q];
+      }
+      for (; k < sg.splits; ++k) {
+        const V pv = *reinterpret_cast<const V *>(pr + k * sg.ss + e);
+#pragma unroll
+        for (int q = 0; q < VEC; ++q) gs[q] += reinterpret_cast<const float *>(&pv)[q];
+      }
+      *reinterpret_cast<V *>(grad + base + e) = g;
+    } else {
+      g = *reinterpret_cast<const V *>(grad + base + e);
+    }
+    V v = *reinterpret_cast<const V *>(mom + base + e), t = *reinterpret_cast<const V *>(theta + base + e);
     float *vf = reinterpret_cast<float *>(&v), *tf = reinterpret_cast<float *>(&t);
     const float *gf = reinterpret_cast<const float *>(&g);
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      const float ge = gf[e] + wd * tf[e];
-      vf[e] = mu * vf[e] + ge;
-      tf[e] -= lr * (nesterov ? ge + mu * vf[e] : vf[e]);
-    }
-    m4[i] = v;
-    t4[i] = t;
+    for (int q = 0; q < VEC; ++q) sgd_update(tf[q], vf[q], gf[q], lr, mu, wd, nesterov);
+    *reinterpret_cast<V *>(mom + base + e) = v;
+    *reinterpret_cast<V *>(theta + base + e) = t;
   }
 }
 
@@ -1451,35 +1424,26 @@ hipError_t launch_head_pool_bwd(int dtype, const void *a, const float *dh, void 
   return head_pool_bwd_t((const float *)a, dh, (float *)gpre, C, rmap, Bt, H, W, Ch, maxpool, s, code, code_rs);
 }
 
-hipError_t launch_wgrad_reduce(const float *dw, const float *db, int splits, int64_t dw_ss,
-                               int64_t dw_rs, int64_t db_ss, int64_t db_rs, float *grad, int64_t P,
-                               int64_t w_off, int64_t b_off, int64_t nw, int co, int C, const int32_t *rmap,
-                               hipStream_t s) {
-  const bool even = ((P | w_off | b_off | nw | co | dw_ss | dw_rs | db_ss | db_rs) & 1) == 0 &&
-                    ((reinterpret_cast<uintptr_t>(dw) | reinterpret_cast<uintptr_t>(db) |
-                      reinterpret_cast<uintptr_t>(grad)) & 7) == 0;
-  if (even)
-    hipLaunchKernelGGL(wgrad_reduce2_kernel, dim3(grid_for((nw + co) / 2, 256, 4096), C), dim3(256), 0, s, dw,
-                       db, splits, dw_ss, dw_rs, db_ss, db_rs, grad, P, w_off, b_off, nw, co, rmap);
-  else
-    hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(grid_for(nw + co, 256, 4096), C), dim3(256), 0, s, dw,
-                       db, splits, dw_ss, dw_rs, db_ss, db_rs, grad, P, w_off, b_off, nw, co, rmap);
-  return hipGetLastError();
-}
-
-hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t P, int C, const int32_t *rmap, float lr,
-                      float mu, float wd, int nesterov, hipStream_t s) {
+hipError_t launch_sgd_seg(float *theta, float *mom, float *grad, const float *partials, const SgdSeg *segs, int nseg,
+                          int blocks, int vec, int split_elems, int64_t P, int C, const int32_t *rmap, float lr,
+                          float mu, float wd, int nesterov, hipStream_t s) {
+  if (nseg < 1 || blocks < 1 || split_elems < 1) return hipErrorInvalidValue;
+  // vec (4, 2 or 1) divides P and every segment's start, length, partial
+  // offset and strides (the plan's choice); the pointers must allow it too
   const uintptr_t al = reinterpret_cast<uintptr_t>(theta) | reinterpret_cast<uintptr_t>(mom) |
-                       reinterpret_cast<uintptr_t>(grad);
-  if (P % 4 == 0 && al % 16 == 0)
-    hipLaunchKernelGGL(sgd_kernel<4>, dim3(grid_for(P / 4, 256, 1024), C), dim3(256), 0, s, theta, mom, grad, P, rmap,
-                       lr, mu, wd, nesterov);
-  else if (P % 2 == 0 && al % 8 == 0)
-    hipLaunchKernelGGL(sgd_kernel<2>, dim3(grid_for(P / 2, 256, 1024), C), dim3(256), 0, s, theta, mom, grad, P, rmap,
-                       lr, mu, wd, nesterov);
+                       reinterpret_cast<uintptr_t>(grad) | reinterpret_cast<uintptr_t>(partials);
+  if (vec == 4 && al % 16 != 0) vec = al % 8 == 0 ? 2 : 1;
+  if (vec == 2 && al % 8 != 0) vec = 1;
+  const dim3 g((uint32_t)blocks, (uint32_t)C);
+  if (vec == 4)
+    hipLaunchKernelGGL(sgd_seg_kernel<4>, g, dim3(256), 0, s, theta, mom, grad, partials, segs, nseg, split_elems, P,
+                       rmap, lr, mu, wd, nesterov);
+  else if (vec == 2)
+    hipLaunchKernelGGL(sgd_seg_kernel<2>, g, dim3(256), 0, s, theta, mom, grad, partials, segs, nseg, split_elems, P,
+                       rmap, lr, mu, wd, nesterov);
   else
-    hipLaunchKernelGGL(sgd_kernel<1>, dim3(grid_for(P, 256, 1024), C), dim3(256), 0, s, theta, mom, grad, P, rmap,
-                       lr, mu, wd, nesterov);
+    hipLaunchKernelGGL(sgd_seg_kernel<1>, g, dim3(256), 0, s, theta, mom, grad, partials, segs, nseg, split_elems, P,
+                       rmap, lr, mu, wd, nesterov);
   return hipGetLastError();
 }
 

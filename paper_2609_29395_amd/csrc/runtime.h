@@ -210,13 +210,22 @@ hipError_t launch_linear_ce(int dtype, const void *h, const int32_t *y, const fl
 hipError_t launch_head_pool_bwd(int dtype, const void *a, const float *dh, void *gpre, int C, const int32_t *rmap,
                                 int Bt, int H, int W, int Ch, int maxpool, hipStream_t s,
                                 const uint8_t *code = nullptr, int64_t code_rs = 0);
-hipError_t launch_wgrad_reduce(const float *dw, const float *db, int splits, int64_t dw_ss,
-                               int64_t dw_rs, int64_t db_ss, int64_t db_rs, float *grad,
-                               int64_t P, int64_t w_off, int64_t b_off, int64_t nw, int co,
-                               int C, const int32_t *rmap, hipStream_t s);
 // SGD on the replicas of the launch's slots: P parameters each, row stride P.
-hipError_t launch_sgd(float *theta, float *mom, const float *grad, int64_t P, int C, const int32_t *rmap,
-                      float lr, float mu, float wd, int nesterov, hipStream_t s);
+// SGD over the parameter vector in segments: a segment [begin, begin + len)
+// takes its gradient from grad (splits = 0) or is the ordered sum of
+// `splits` split-K partials, element j of split k for replica r at
+// partials[src + k ss + r rs + j], which is also written to grad.  Blocks of
+// kSgdBlockElems elements, or split_elems in a segment of partials (one
+// vector per thread, so that the partial loads spread over enough blocks);
+// a segment's blocks start at first_block.
+struct SgdSeg {
+  int64_t begin, len, src, ss, rs;
+  int32_t splits, first_block;
+};
+constexpr int kSgdBlockElems = 4096;
+hipError_t launch_sgd_seg(float *theta, float *mom, float *grad, const float *partials, const SgdSeg *segs, int nseg,
+                          int blocks, int vec, int split_elems, int64_t P, int C, const int32_t *rmap, float lr,
+                          float mu, float wd, int nesterov, hipStream_t s);
 // Eq. 5 over C replicas of P parameters: weights from w_host through the
 // kernel arguments when C <= kMaxArgWeights, else from w_dev (device).
 constexpr int kMaxArgWeights = 64;

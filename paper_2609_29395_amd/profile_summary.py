@@ -89,8 +89,8 @@ def kernel_label(name: str) -> str:
     if m:
         w = int(m.group(3)) * int(m.group(4))
         return f"conv_wgrad<bf16,{m.group(1)}x{m.group(2)},w{w},lds>"
-    if re.search(r"wgrad_reduce2?_kernel", name):
-        return "wgrad_reduce"  # the timing label of both widths
+    if re.search(r"sgd_seg_kernel<", name):
+        return "sgd"  # the update with the split-K sums, the library's "sgd" launch
     m = re.search(r"::(\w+?)(_kernel)?[<(]", name)
     return m.group(1) if m else name
 

@@ -46,6 +46,7 @@ def test_image_layer_labels():
     assert ps.kernel_label(ns + "conv_img_kernel<32, 64, 0, 2>(ConvArgs, int)") == "conv_fwd<bf16,512x64x288,w8,img>"
     assert ps.kernel_label(ns + "conv_img_kernel<64, 32, 1, 1>(ConvArgs, int)") == "conv_dgrad<bf16,256x32x576,w8,img>"
     assert ps.kernel_label(ns + "wgrad_img_kernel<3, false>(WgradArgs)") == "conv_wgrad<bf16,64x288,w8,img>"
+    assert ps.kernel_label(ns + "sgd_seg_kernel<4>(float*, float*, float*)") == "sgd"
     assert ps.kernel_label(ns + "wgrad_img_kernel<3, true>(WgradArgs)") == "conv_wgrad<bf16,64x288,w8,img,pool>"
 
 

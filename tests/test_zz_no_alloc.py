@@ -58,7 +58,7 @@ def test_static_context_matches_caller_workspace_twice_in_a_row():
 
 
 def test_static_context_rejects_a_workspace_beyond_the_array():
-    cfg = get_config("gpsl")  # about 156 MiB of workspace
+    cfg = get_config("gpsl")  # about 218 MiB of workspace
     with pytest.raises(gcpsl.GCPSLError) as e:
         driver.setup(cfg, static=True)
     assert e.value.code == gcpsl.EINVAL and "static workspace" in str(e.value)
