@@ -149,13 +149,19 @@ def _one(pattern):
 
 
 def _update_profile(workload, kind, entries):
-    """Merge {label: {field: value}} of one kind (trace, mfma, traffic) into
-    profiles/profile.json, with the current source hash of each label's file."""
+    """Set the {label: {field: value}} of one kind (trace, mfma, traffic) of a
+    workload in profiles/profile.json, with the current source hash of each
+    label's file; labels of that kind the new run does not have are dropped."""
     rec = {}
     if os.path.exists(PROFILE_JSON):
         with open(PROFILE_JSON) as fh:
             rec = json.load(fh)
     w = rec.setdefault(workload, {})
+    for lab in list(w):
+        if lab not in entries:
+            w[lab].pop(kind, None)
+            if not w[lab]:
+                del w[lab]
     for lab, fields in entries.items():
         e = w.setdefault(lab, {})
         e[kind] = dict(fields, source_hash=file_hash(kernel_source(lab)))

@@ -113,6 +113,15 @@ def _private_profile(tmp_path, monkeypatch):
     monkeypatch.setattr(ps, "PROFILE_JSON", str(tmp_path / "profile.json"))
 
 
+def test_a_new_summary_drops_labels_the_run_no_longer_has():
+    ps._update_profile("wl", "trace", {"old": {"calls": 1, "avg_us": 1.0}, "sgd": {"calls": 1, "avg_us": 2.0}})
+    ps._update_profile("wl", "mfma", {"old": {"launches": 1}})
+    ps._update_profile("wl", "trace", {"sgd": {"calls": 2, "avg_us": 3.0}})
+    assert ps.profile_entry("wl", "old", "trace") is None
+    assert ps.profile_entry("wl", "old", "mfma") is not None  # another kind's entry stays
+    assert ps.profile_entry("wl", "sgd", "trace")["avg_us"] == 3.0
+
+
 def test_profile_entry_goes_stale_with_its_source(tmp_path, monkeypatch):
     ps._update_profile("wl", "trace", {"sgd": {"calls": 1, "avg_us": 2.0}})
     assert ps.profile_entry("wl", "sgd", "trace")["avg_us"] == 2.0
