@@ -34,6 +34,8 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
 
@@ -334,6 +336,331 @@ conv_img_kernel(ConvArgs a, int MT) {
   }
 }
 
+// The forward of a 32-channel input followed by the 2 x 2 max pool with
+// routing codes (the client's last conv before the cut), persistent: one
+// workgroup of 16 waves per CU; workgroup w of replica slot z takes the
+// 16-row tiles w, w + WPR, w + 2 WPR, ... of its replica, alternately by its
+// two teams of 8 waves.  The weight matrix is copied into LDS once per
+// workgroup and shared by both teams; each team has its own halo buffer.
+// While one team runs a tile's MFMAs, the other copies its next halo and
+// pools and stores its previous tile (121 KB of LDS, at most 128 registers
+// per wave; a third halo buffer, so that a copy could start a phase
+// earlier, measured slower).
+// Pixel fragment tm = 2 rr + hf of a wave holds the columns 2 li + hf of its
+// image row rr, so a lane ends with whole 2 x 2 pooling windows (4 channels
+// of pooled column li) and pools them in registers.  A halo row keeps its
+// even columns, then its odd ones (column w' in slot (w' mod 2) 17 + w' / 2),
+// and slot i keeps its 16-byte chunk c at c ^ ((i >> 1) & 3), so that the
+// 16-byte reads of 8 consecutive lanes (consecutive slots of one half) fall
+// on distinct banks; weight rows are 656 bytes apart (40 chunks and one of
+// padding) for the same reason, and a tap's fragments sit a fixed 64 bytes
+// after the previous tap's.
+template <int N> __device__ __forceinline__ void img_wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// packed unsigned 16-bit integer arithmetic (two halves per register), kept
+// as such (the compiler would otherwise split min(x, 1) into compares)
+__device__ __forceinline__ uint32_t pk_sub_u16(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_pk_sub_u16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ __forceinline__ uint32_t pk_min_u16(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_pk_min_u16 %0, %1, %2" : "=v"(r) : "v"(a), "s"(b));
+  return r;
+}
+__device__ __forceinline__ uint32_t pk_add_u16(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_pk_add_u16 %0, %1, %2" : "=v"(r) : "v"(a), "s"(b));
+  return r;
+}
+__device__ __forceinline__ uint32_t pk_mad_u16(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t r;
+  asm("v_pk_mad_u16 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "s"(c));
+  return r;
+}
+__device__ __forceinline__ uint32_t pk_mul_lo_u16(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_pk_mul_lo_u16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// the lane's index within its wave, computed afresh (mbcnt over all lanes)
+__device__ __forceinline__ int img_lane_id() {
+  int v;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(v));
+  return v;
+}
+
+template <int OFF> __device__ __forceinline__ void lds_read16(u32x4 &v, uint32_t ad) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(ad), "n"(OFF));
+}
+
+constexpr int IMGP_WROW = 656;  // bytes per weight row in LDS: 40 chunks and one of padding
+
+template <int TAP, int TN, int TN0 = 0> __device__ __forceinline__ void img_pool_wfrags(u32x4 (&w)[TN], uint32_t wb) {
+  if constexpr (TN0 < TN) {
+    // fragment tn: 16 weight rows further
+    lds_read16<64 * TAP + TN0 * 16 * IMGP_WROW>(w[TN0], wb);
+    img_pool_wfrags<TAP, TN, TN0 + 1>(w, wb);
+  }
+}
+
+// tap (r, s) = (TAP / 3, TAP % 3) of a 16-row tile: weight fragment tn at
+// wb + tn 16 rows + 64 TAP, pixel fragment tm = 2 rr + hf (columns
+// 2 li + hf + s) at xb[hf + s] + (rr + r) halo rows
+template <int TAP, int TN>
+__device__ __forceinline__ void img_pool_tap(f32x4_t (&acc)[4][TN], uint32_t wb, const uint32_t (&xb)[4]) {
+  constexpr int r = TAP / 3, s = TAP % 3, ROWB = HP * 64;  // bytes per halo row of 32 channels
+  u32x4 w[TN], x[4];
+  img_pool_wfrags<TAP, TN>(w, wb);
+  lds_read16<r * ROWB>(x[0], xb[s]);
+  lds_read16<r * ROWB>(x[1], xb[s + 1]);
+  lds_read16<(r + 1) * ROWB>(x[2], xb[s]);
+  lds_read16<(r + 1) * ROWB>(x[3], xb[s + 1]);
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < TN; ++i) asm volatile("" : "+v"(w[i]));
+#pragma unroll
+  for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(x[i]));
+#pragma unroll
+  for (int tm = 0; tm < 4; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) mma(acc[tm][tn], w[tn], x[tm]);
+}
+
+// LDS of the ping-pong kernel: two halo buffers, the weights, the bias
+template <int NO> struct ImgPool {
+  using CF = ImgCfg<32, NO, 2>;
+  // padded weight rows, in whole 1 KB copies (so that no copy reaches the bias)
+  static constexpr int W_LDS = (NO * IMGP_WROW + 1023) / 1024 * 1024;
+  static constexpr int W_OFF = 2 * CF::H_BYTES, B_OFF = W_OFF + W_LDS;
+  // the bias (256 bytes), then each team thread's halo copy table (16 bytes)
+  static constexpr int T_OFF = B_OFF + 256, LDS = T_OFF + NTHR * 16;
+  static_assert(NO * 4 <= 256 && CF::HQ <= 8, "bias and table sizes");
+  static_assert(LDS <= 160 * 1024, "one workgroup per CU");
+};
+
+template <int NO>
+__global__ void __launch_bounds__(2 * NTHR)
+conv_img_pool_kernel(ConvArgs a, int MT, int WPR) {
+  using CF = ImgCfg<32, NO, 2>;
+  using PL = ImgPool<NO>;
+  constexpr int CS = 32, TROWS = CF::TROWS, HPIX = CF::HPIX, TN = CF::TN, CPR = CF::CPR;
+  constexpr int W_OFF = PL::W_OFF, B_OFF = PL::B_OFF, T_OFF = PL::T_OFF;
+  constexpr int NST = 2 * TN;  // global stores per wave and tile (pooled values and codes per fragment)
+  static_assert(CPR == 4 && CF::KP * 2 == 640 && HP == 34, "4 chunks per halo pixel, 640-byte weight rows");
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int team = wave >> 3, tw = wave & 7;  // team 0 takes the even tiles, team 1 the odd ones
+  const uint32_t t = xcd_swizzle(blockIdx.x, (uint32_t)(WPR * a.C));
+  const int z = __builtin_amdgcn_readfirstlane((int)(t / (uint32_t)WPR));
+  const int w0 = __builtin_amdgcn_readfirstlane((int)(t - (uint32_t)z * (uint32_t)WPR));
+  const int nt = (MT - w0 + WPR - 1) / WPR;  // tiles of this workgroup: w0 + k WPR, k < nt
+  const int rep = replica_of(a.rmap, z);
+  const int M = a.Bt * IMG * IMG;
+  const bf16_t *src = reinterpret_cast<const bf16_t *>(a.src) + rep * a.src_rs;
+  const bf16_t *wt = reinterpret_cast<const bf16_t *>(a.wt) + rep * a.wt_rs;
+  const __amdgpu_buffer_rsrc_t rss = rsrc(src, (uint32_t)((int64_t)M * CS * 2));
+  const __amdgpu_buffer_rsrc_t rsw = rsrc(wt, (uint32_t)CF::W_BYTES);
+
+  // the weight matrix, once, by all 16 waves: row n at n * 656 bytes, its
+  // 40 chunks in order and a zero one
+  constexpr int WSLOTS = PL::W_LDS / 16, WROWC = IMGP_WROW / 16;
+#pragma unroll
+  for (int q = 0; q < (WSLOTS + 2 * NTHR - 1) / (2 * NTHR); ++q) {
+    const int slot0 = q * 2 * NTHR + wave * 64;
+    if (slot0 < WSLOTS) {  // (whole 64-slot copies: WSLOTS is a multiple of 64)
+      const int j = slot0 + lane;
+      const int row = j / WROWC, kc = j % WROWC;
+      const uint32_t off = (row < NO && kc < CF::WCH) ? (uint32_t)(row * CF::KP + 8 * kc) * 2u : kOob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsw, LDS_PTR(smem + W_OFF + slot0 * 16), 16, off, 0, 0, 0);
+    }
+  }
+  // The halo image rows h0 - 1 .. h0 + 16 of tile k with a one-pixel zero
+  // border, copied by the 8 waves of its team into the team's buffer.  A
+  // thread's 16-byte piece q lands in the same halo slot for every tile, so
+  // its source is tabled once per thread (ent, 16 bits per piece): the
+  // offset from the tile's first pixel in 16-byte units plus 128, and flags
+  // for a slot outside the image in the upper tile of an image (0x8000: the
+  // row above it), in the lower one (0x4000: the row below) and always
+  // (0x2000: the border columns, the padding past the halo).
+  auto issue_halo = [&](int k, const u32x4 &ent) {
+    const int m0 = (w0 + k * WPR) * (TROWS * IMG), h0 = (m0 / IMG) % IMG;
+    const uint32_t bad = h0 == 0 ? 0xa000u : 0x6000u;
+    const uint32_t base = (uint32_t)m0 * (CS * 2) - 128u * 16u;
+#pragma unroll
+    for (int q = 0; q < CF::HQ; ++q) {
+      const int byte = q * NTHR * 16 + tw * 1024;
+      if (byte < CF::H_BYTES) {
+        const uint32_t e = (ent[q >> 1] >> (16 * (q & 1))) & 0xffffu;
+        const uint32_t off = (e & bad) ? kOob : base + (e & 0x1fffu) * 16u;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rss, LDS_PTR(smem + team * CF::H_BYTES + byte), 16, off, 0, 0, 0);
+      }
+    }
+  };
+  if (team == 0) {
+    // the table: slot R of a halo row is column w' = 2 (R mod 17) + R / 17
+    // (even columns, then odd ones), and chunk c sits at c ^ ((w' >> 2) & 3)
+    uint32_t e16[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) e16[q] = 0x2000u;
+#pragma unroll
+    for (int q = 0; q < CF::HQ; ++q) {
+      const int j = q * NTHR + tw * 64 + lane;
+      const int R = j / CPR, cs = j % CPR;
+      const int hp = R / HP, rem = R - hp * HP;
+      const int idx = rem % (HP / 2), wp = 2 * idx + rem / (HP / 2);
+      const int c = cs ^ ((idx >> 1) & (CPR - 1));
+      const int w = wp - 1;
+      if (R < HPIX && (unsigned)w < (unsigned)IMG)
+        e16[q] = (uint32_t)(((hp - 1) * IMG + w) * CPR + c + 128) | (hp == 0 ? 0x8000u : 0u) |
+                 (hp == HPIX / HP - 1 ? 0x4000u : 0u);
+    }
+    const u32x4 ent = {e16[0] | (e16[1] << 16), e16[2] | (e16[3] << 16), e16[4] | (e16[5] << 16),
+                       e16[6] | (e16[7] << 16)};
+    *reinterpret_cast<u32x4 *>(smem + T_OFF + (tw * 64 + lane) * 16) = ent;
+    issue_halo(0, ent);
+  }
+  // the bias into LDS (read back with LDS reads the compiler does not see,
+  // so that it adds no wait for the copies in flight); loaded after the
+  // copies, so waiting for it also waits for them
+  if (tid < NO) reinterpret_cast<float *>(smem + B_OFF)[tid] = a.bias[rep * a.bias_rs + tid];
+  img_wait_vm<0>();
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+  const uint32_t lds0 = (uint32_t)(size_t)LDS_PTR(smem);
+  bf16_t *zo = reinterpret_cast<bf16_t *>(a.pool_out) + rep * a.pool_rs;
+  uint8_t *co = a.pool_code + rep * a.pool_rs;
+
+  // Phase ph: the team of tile ph (ph & 1) computes it from its buffer; the
+  // other team first copies its next tile (ph + 1) into its own buffer (read
+  // for the last time in phase ph - 1), then pools and stores its tile
+  // ph - 1, then waits for its copies.  One barrier per phase, so a copy has
+  // the other team's whole k loop to land, and the pooling of one team runs
+  // beside the other team's MFMAs.
+  f32x4_t acc[4][TN];
+  for (int ph = 0; ph <= nt; ++ph) {
+    if ((ph & 1) == team) {
+      if (ph < nt) {
+        // the accumulators start from the bias of their channels tn*16 +
+        // 4 lg .. + 3 (read with its own wait)
+        const uint32_t ba = lds0 + (uint32_t)(B_OFF + 16 * (img_lane_id() >> 4));
+        f32x4_t bv[4];
+        if constexpr (TN == 4)
+          asm volatile(
+              "ds_read_b128 %0, %4 offset:0\n\tds_read_b128 %1, %4 offset:64\n\t"
+              "ds_read_b128 %2, %4 offset:128\n\tds_read_b128 %3, %4 offset:192\n\ts_waitcnt lgkmcnt(0)"
+              : "=&v"(bv[0]), "=&v"(bv[1]), "=&v"(bv[2]), "=&v"(bv[3])
+              : "v"(ba)
+              : "memory");
+        else
+          asm volatile("ds_read_b128 %0, %2 offset:0\n\tds_read_b128 %1, %2 offset:64\n\ts_waitcnt lgkmcnt(0)"
+                       : "=&v"(bv[0]), "=&v"(bv[1])
+                       : "v"(ba)
+                       : "memory");
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[i][tn] = bv[tn];
+        // fragment read bases (from an opaque lane index, so that they are
+        // not held across the pooling branch): weight row li, chunk lg of
+        // tap 0; the team's halo buffer, pixel 2 li + hf + s of the wave's
+        // first halo row, chunk lg
+        const int ln = img_lane_id();
+        const int li = ln & 15, lg = ln >> 4;
+        const uint32_t wb = lds0 + (uint32_t)(W_OFF + li * IMGP_WROW + lg * 16);
+        const uint32_t hb = lds0 + (uint32_t)(team * CF::H_BYTES + 2 * tw * HP * CF::RB);
+        uint32_t xk[4];  // columns 2 li + e: plane e & 1, slot li + e / 2 of it
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int idx = li + (e >> 1);
+          xk[e] = hb + (uint32_t)(((e & 1) * (HP / 2) + idx) * CF::RB + ((lg ^ ((idx >> 1) & (CPR - 1))) * 16));
+        }
+        img_pool_tap<0>(acc, wb, xk);
+        img_pool_tap<1>(acc, wb, xk);
+        img_pool_tap<2>(acc, wb, xk);
+        img_pool_tap<3>(acc, wb, xk);
+        img_pool_tap<4>(acc, wb, xk);
+        img_pool_tap<5>(acc, wb, xk);
+        img_pool_tap<6>(acc, wb, xk);
+        img_pool_tap<7>(acc, wb, xk);
+        img_pool_tap<8>(acc, wb, xk);
+      }
+    } else {
+      if (ph + 1 < nt) {
+        u32x4 ent;
+        const uint32_t ta = lds0 + (uint32_t)(T_OFF + (tw * 64 + img_lane_id()) * 16);
+        asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(ent) : "v"(ta) : "memory");
+        issue_halo(ph + 1, ent);
+      }
+      if (ph >= 1) {
+        // pooling: lane (li, lg) holds channels tn*16 + 4 lg + e of columns
+        // 2 li (hf 0) and 2 li + 1 (hf 1) of image rows 2 tw (rr 0) and
+        // 2 tw + 1 (rr 1) -- pooled pixel li of pooled row h0 / 2 + tw.  The
+        // pre-activations are rounded to bf16 as the unpooled layer would
+        // store them (ReLU commutes with the rounding).  Positive bf16 values
+        // order as their bits read as signed 16-bit integers, and every
+        // other value (negative, -0) reads as at most 0, so the window's
+        // maximum with 0 is the pooled ReLU output, taken two channels at a
+        // time by packed 16-bit integer operations; the code is the first
+        // window position (row-major) holding it, or 4 where it is 0.
+        // (Lane-derived addresses from an opaque lane index, not held
+        // across the k loop.)
+        const int ln = img_lane_id();
+        const int eli = ln & 15, elg = ln >> 4;
+        const int m0 = (w0 + (ph - 1) * WPR) * (TROWS * IMG);
+        const int b = m0 / (IMG * IMG), hz = ((m0 / IMG) % IMG) / 2 + tw;
+        const int64_t zrow = ((int64_t)(b * (IMG / 2) + hz) * (IMG / 2) + eli) * NO + 4 * elg;
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) {
+          uint32_t zz[2], cc[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            // channels 2h, 2h + 1 of the four window positions p = 2 rr + hf
+            s16x2 v[4];
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+              v[p] = __builtin_bit_cast(s16x2, pack2_bf16(acc[p][tn][2 * h], acc[p][tn][2 * h + 1]));
+            const s16x2 zero = {0, 0};
+            const s16x2 m = __builtin_elementwise_max(__builtin_elementwise_max(__builtin_elementwise_max(v[0], v[1]),
+                                                                                __builtin_elementwise_max(v[2], v[3])),
+                                                      zero);
+            // ne_p = min(m - v_p, 1) is 0 exactly where position p holds the
+            // maximum (m >= v_p, so the 16-bit difference is m - v_p); the
+            // first such p is ne_0 (1 + ne_1 (1 + ne_2)) (3 when none of
+            // 0..2 does), and 4 replaces it where the maximum is 0
+            const uint32_t one = 0x00010001u, four = 0x00040004u;
+            const uint32_t mb = __builtin_bit_cast(uint32_t, m);
+            uint32_t ne[3];
+#pragma unroll
+            for (int p = 0; p < 3; ++p) ne[p] = pk_min_u16(pk_sub_u16(mb, __builtin_bit_cast(uint32_t, v[p])), one);
+            const uint32_t first = pk_mul_lo_u16(ne[0], pk_mad_u16(ne[1], pk_add_u16(ne[2], one), one));
+            const uint32_t pos = pk_min_u16(mb, one);
+            zz[h] = mb;
+            cc[h] = pk_mad_u16(pk_sub_u16(first, four), pos, four);
+          }
+          // codes of channels 0..3: the low bytes of the four 16-bit codes
+          const uint32_t code = __builtin_amdgcn_perm(cc[1], cc[0], 0x06040200u);
+          *reinterpret_cast<u32x2 *>(zo + zrow + tn * 16) = u32x2{zz[0], zz[1]};
+          *reinterpret_cast<uint32_t *>(co + zrow + tn * 16) = code;
+        }
+        // this team's copies have landed (they were issued before the NST
+        // stores, and the vector memory counter retires in issue order)
+        img_wait_vm<NST>();
+      } else {
+        img_wait_vm<0>();
+      }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  }
+}
+
 // The image layer: out[p][n] = act(bias[n] + sum_k A[p][k] W[n][k]) with k =
 // (r, s, c) over the 3 x 3 taps of the 3 image channels (27 columns,
 // zero-padded to 32) and 32 output channels.  A plain stream: each wave takes
@@ -505,9 +832,12 @@ hipError_t launch_conv_img(const ConvArgs &a, hipStream_t s, std::string *label)
   const int rpw = (a.epi == EPI_FWD && a.Csrc == 32) ? 2 : 1;
   const int MT = a.Bt * IMG / (8 * rpw);  // tiles of 8 rpw image rows per replica
   const dim3 g((uint32_t)MT * a.C);
+  // the forward into the pool and its codes: persistent workgroups, one per
+  // CU, each taking every WPR-th tile of its replica
+  const bool pers = a.epi == EPI_FWD && a.Csrc == 32 && a.pool_out && a.pool_code && !a.no_relu;
   if (label)
     *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16," + std::to_string(256 * rpw) +
-             "x" + std::to_string(a.N) + "x" + std::to_string(9 * a.Csrc) + ",w8,img>";
+             "x" + std::to_string(a.N) + "x" + std::to_string(9 * a.Csrc) + (pers ? ",w8,img,pool>" : ",w8,img>");
 #define IMG_GO(CS, NO, E, RPW) \
   hipLaunchKernelGGL((conv_img_kernel<CS, NO, E, RPW>), g, dim3(NTHR), (ImgCfg<CS, NO, RPW>::LDS), s, a, MT)
   static_assert(ImgCfg<32, 32, 2>::FITS2 && ImgCfg<32, 64, 2>::FITS2 && ImgCfg<32, 32>::FITS2 &&
@@ -520,10 +850,29 @@ hipError_t launch_conv_img(const ConvArgs &a, hipStream_t s, std::string *label)
       const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, ImgCfg<64, 32>::LDS);
       if (e != hipSuccess) return e;
     }
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&conv_img_kernel<32, 64, EPI_FWD, 2>),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, ImgCfg<32, 64, 2>::LDS);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&conv_img_kernel<32, 64, EPI_FWD, 2>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, ImgCfg<32, 64, 2>::LDS);
     if (e != hipSuccess) return e;
+    for (const void *f : {reinterpret_cast<const void *>(&conv_img_pool_kernel<64>),
+                          reinterpret_cast<const void *>(&conv_img_pool_kernel<32>)}) {
+      e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              f == reinterpret_cast<const void *>(&conv_img_pool_kernel<64>) ? ImgPool<64>::LDS
+                                                                                             : ImgPool<32>::LDS);
+      if (e != hipSuccess) return e;
+    }
     attr.mark();
+  }
+  if (pers) {
+    constexpr int kSlots = 256;  // one workgroup on each of the 256 CUs
+    const int want = std::max(1, std::min(MT, kSlots / std::max(1, a.C)));
+    const int per = (MT + want - 1) / want;  // tiles per workgroup
+    const int wpr = (MT + per - 1) / per;
+    const dim3 gp((uint32_t)wpr * a.C);
+    if (a.N == 64)
+      hipLaunchKernelGGL(conv_img_pool_kernel<64>, gp, dim3(2 * NTHR), ImgPool<64>::LDS, s, a, MT, wpr);
+    else
+      hipLaunchKernelGGL(conv_img_pool_kernel<32>, gp, dim3(2 * NTHR), ImgPool<32>::LDS, s, a, MT, wpr);
+    return hipGetLastError();
   }
   if (a.epi == EPI_FWD) {
     if (a.Csrc == 32 && a.N == 32) IMG_GO(32, 32, EPI_FWD, 2);

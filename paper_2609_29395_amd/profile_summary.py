@@ -74,6 +74,9 @@ def kernel_label(name: str) -> str:
         kind = "conv_fwd" if m.group(3) == "0" else "conv_dgrad"
         tile = 256 * int(m.group(5) or 1)
         return f"{kind}<bf16,{tile}x{m.group(2)}x{9 * int(m.group(1))},w8,img>"
+    m = re.search(r"conv_img_pool_kernel<(\d+)>", name)
+    if m:  # the persistent forward into the max pool and its routing codes
+        return f"conv_fwd<bf16,512x{m.group(1)}x288,w8,img,pool>"
     m = re.search(r"wgrad_col_kernel(<(true|false)>)?", name)
     if m:
         return "conv_wgrad<bf16,32x27,w4,img3>" if m.group(2) == "true" else "conv_wgrad<bf16,32x32,w4,col>"
@@ -105,7 +108,7 @@ def kernel_source(label: str) -> str:
         return "k_wgrad_lds.hip"
     if label.startswith("conv_") and label.endswith((",lds>", ",halo>", ",halo1>")):
         return "k_conv_lds.hip"
-    if label.startswith("conv_") and label.endswith((",img>", ",col>", ",img3>")):
+    if label.startswith("conv_") and label.endswith((",img>", ",col>", ",img3>", ",img,pool>")):
         return "k_conv_img.hip"
     if label.startswith("conv_"):
         return "k_conv.hip"

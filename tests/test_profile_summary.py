@@ -48,6 +48,8 @@ def test_image_layer_labels():
     assert ps.kernel_label(ns + "wgrad_img_kernel<3, false>(WgradArgs)") == "conv_wgrad<bf16,64x288,w8,img>"
     assert ps.kernel_label(ns + "sgd_seg_kernel<4>(float*, float*, float*)") == "sgd"
     assert ps.kernel_label(ns + "wgrad_img_kernel<3, true>(WgradArgs)") == "conv_wgrad<bf16,64x288,w8,img,pool>"
+    assert ps.kernel_label(ns + "conv_img_pool_kernel<64>(ConvArgs, int, int)") == \
+        "conv_fwd<bf16,512x64x288,w8,img,pool>"
 
 
 @pytest.mark.parametrize("label,source", [
@@ -59,6 +61,7 @@ def test_image_layer_labels():
     ("conv_wgrad<bf16,32x27,w4,img3>", "k_wgrad_lds.hip"),
     ("conv_wgrad<bf16,64x288,w8,img,pool>", "k_wgrad_lds.hip"),
     ("conv_fwd<bf16,512x64x288,w8,img>", "k_conv_img.hip"),
+    ("conv_fwd<bf16,512x64x288,w8,img,pool>", "k_conv_img.hip"),
     ("conv_fwd<f32,128x128x32,w4,vec>", "k_conv.hip"),
     ("sgd", "k_misc.hip"),
     ("fuse", "k_misc.hip"),
