@@ -34,8 +34,6 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef short s16x2 __attribute__((ext_vector_type(2)));
-typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
 
@@ -360,8 +358,20 @@ template <int N> __device__ __forceinline__ void img_wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// packed unsigned 16-bit integer arithmetic (two halves per register), kept
-// as such (the compiler would otherwise split min(x, 1) into compares)
+// packed 16-bit integer arithmetic (two halves per register), kept as such
+// (the compiler would otherwise split min(x, 1) into compares, and it has
+// folded a packed signed maximum of the second word of a loaded pair onto
+// the first word's)
+__device__ __forceinline__ uint32_t pk_max_i16(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_pk_max_i16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ __forceinline__ uint32_t pk_max0_i16(uint32_t a) {
+  uint32_t r;
+  asm("v_pk_max_i16 %0, %1, 0" : "=v"(r) : "v"(a));
+  return r;
+}
 __device__ __forceinline__ uint32_t pk_sub_u16(uint32_t a, uint32_t b) {
   uint32_t r;
   asm("v_pk_sub_u16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
@@ -623,23 +633,19 @@ conv_img_pool_kernel(ConvArgs a, int MT, int WPR) {
 #pragma unroll
           for (int h = 0; h < 2; ++h) {
             // channels 2h, 2h + 1 of the four window positions p = 2 rr + hf
-            s16x2 v[4];
+            uint32_t v[4];
 #pragma unroll
-            for (int p = 0; p < 4; ++p)
-              v[p] = __builtin_bit_cast(s16x2, pack2_bf16(acc[p][tn][2 * h], acc[p][tn][2 * h + 1]));
-            const s16x2 zero = {0, 0};
-            const s16x2 m = __builtin_elementwise_max(__builtin_elementwise_max(__builtin_elementwise_max(v[0], v[1]),
-                                                                                __builtin_elementwise_max(v[2], v[3])),
-                                                      zero);
+            for (int p = 0; p < 4; ++p) v[p] = pack2_bf16(acc[p][tn][2 * h], acc[p][tn][2 * h + 1]);
+            const uint32_t m = pk_max0_i16(pk_max_i16(pk_max_i16(v[0], v[1]), pk_max_i16(v[2], v[3])));
             // ne_p = min(m - v_p, 1) is 0 exactly where position p holds the
             // maximum (m >= v_p, so the 16-bit difference is m - v_p); the
             // first such p is ne_0 (1 + ne_1 (1 + ne_2)) (3 when none of
             // 0..2 does), and 4 replaces it where the maximum is 0
             const uint32_t one = 0x00010001u, four = 0x00040004u;
-            const uint32_t mb = __builtin_bit_cast(uint32_t, m);
+            const uint32_t mb = m;
             uint32_t ne[3];
 #pragma unroll
-            for (int p = 0; p < 3; ++p) ne[p] = pk_min_u16(pk_sub_u16(mb, __builtin_bit_cast(uint32_t, v[p])), one);
+            for (int p = 0; p < 3; ++p) ne[p] = pk_min_u16(pk_sub_u16(mb, v[p]), one);
             const uint32_t first = pk_mul_lo_u16(ne[0], pk_mad_u16(ne[1], pk_add_u16(ne[2], one), one));
             const uint32_t pos = pk_min_u16(mb, one);
             zz[h] = mb;
@@ -656,6 +662,271 @@ conv_img_pool_kernel(ConvArgs a, int MT, int WPR) {
       } else {
         img_wait_vm<0>();
       }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  }
+}
+
+// The input gradient of the cut layer (64 gradient channels at the pooled
+// resolution, 32 input channels), persistent and ping-ponged like the
+// forward above: one workgroup of 16 waves per CU walks every WPR-th 8-row
+// tile of one replica, alternately by its two teams of 8 waves (one image
+// row per wave).  The weight matrix is copied into LDS once per workgroup;
+// each team has its own halo buffer, which it fills for its next tile while
+// the other team runs its MFMAs: it loads the pooled gradient and the
+// routing codes of each halo piece into registers, then masks and stores its
+// previous tile, then writes the pieces routed (the gradient where the code
+// names the pixel's window position, zero elsewhere).  Each thread's pieces
+// sit at fixed halo slots, so their sources are tabled once in LDS.  A halo
+// pixel row is 128 bytes with chunk c at c ^ (w' & 7), weight rows are 1168
+// bytes apart (72 chunks and one of padding): the 16-byte fragment reads of
+// 8 consecutive lanes fall on distinct banks.
+constexpr int IMGD_WROW = 1168;  // bytes per weight row in LDS: 72 chunks and one of padding
+
+template <int OFF> __device__ __forceinline__ void lds_read16b(u32x4 &v, uint32_t ad) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(ad), "n"(OFF));
+}
+
+// tap (r, s) = (TAP / 3, TAP % 3): both 32-channel k groups; weight fragment
+// (tn, g) at wb + tn 16 rows + TAP 128 + g 64 bytes, pixel fragment (half, g)
+// at xb[s][g] + r halo rows + half 16 pixels
+template <int TAP>
+__device__ __forceinline__ void img_dgrad_tap(f32x4_t (&acc)[2][2], uint32_t wb, const uint32_t (&xb)[3][2]) {
+  constexpr int r = TAP / 3, s = TAP % 3, ROWB = HP * 128;
+  u32x4 w[2][2], x[2][2];  // [g][tn], [g][half]
+  lds_read16b<TAP * 128>(w[0][0], wb);
+  lds_read16b<16 * IMGD_WROW + TAP * 128>(w[0][1], wb);
+  lds_read16b<TAP * 128 + 64>(w[1][0], wb);
+  lds_read16b<16 * IMGD_WROW + TAP * 128 + 64>(w[1][1], wb);
+  lds_read16b<r * ROWB>(x[0][0], xb[s][0]);
+  lds_read16b<r * ROWB + 16 * 128>(x[0][1], xb[s][0]);
+  lds_read16b<r * ROWB>(x[1][0], xb[s][1]);
+  lds_read16b<r * ROWB + 16 * 128>(x[1][1], xb[s][1]);
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int g = 0; g < 2; ++g)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      asm volatile("" : "+v"(w[g][i]));
+      asm volatile("" : "+v"(x[g][i]));
+    }
+#pragma unroll
+  for (int g = 0; g < 2; ++g)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+      for (int tn = 0; tn < 2; ++tn) mma(acc[hf][tn], w[g][tn], x[g][hf]);
+}
+
+// LDS of the input-gradient kernel: two halo buffers, the weights, the table
+struct ImgDgrad {
+  using CF = ImgCfg<64, 32, 1>;
+  static constexpr int W_LDS = (32 * IMGD_WROW + 1023) / 1024 * 1024;
+  static constexpr int W_OFF = 2 * CF::H_BYTES, T_OFF = W_OFF + W_LDS, LDS = T_OFF + NTHR * 16;
+  static_assert(CF::HQ <= 8 && CF::TROWS == 8 && CF::CPR == 8 && CF::KP == 576, "8-row tiles of 64 channels");
+  static_assert(LDS <= 160 * 1024, "one workgroup per CU");
+};
+
+__global__ void __launch_bounds__(2 * NTHR)
+conv_img_dgrad_kernel(ConvArgs a, int MT, int WPR) {
+  using CF = ImgCfg<64, 32, 1>;
+  using PL = ImgDgrad;
+  constexpr int CS = 64, NO = 32, TROWS = 8, HPIX = CF::HPIX, CPR = CF::CPR, HQ = CF::HQ;
+  constexpr int W_OFF = PL::W_OFF, T_OFF = PL::T_OFF;
+  constexpr int PW = IMG / 2;  // pooled side
+  extern __shared__ __attribute__((aligned(1024))) char smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int team = wave >> 3, tw = wave & 7;  // team 0 takes the even tiles, team 1 the odd ones
+  const uint32_t t = xcd_swizzle(blockIdx.x, (uint32_t)(WPR * a.C));
+  const int z = __builtin_amdgcn_readfirstlane((int)(t / (uint32_t)WPR));
+  const int w0 = __builtin_amdgcn_readfirstlane((int)(t - (uint32_t)z * (uint32_t)WPR));
+  const int nt = (MT - w0 + WPR - 1) / WPR;  // tiles of this workgroup: w0 + k WPR, k < nt
+  const int rep = replica_of(a.rmap, z);
+  const bf16_t *gsrc = reinterpret_cast<const bf16_t *>(a.src) + rep * a.src_rs;  // pooled gradient
+  const uint8_t *csrc = a.pool_code + rep * a.src_rs;                              // its codes
+  const bf16_t *wt = reinterpret_cast<const bf16_t *>(a.wt) + rep * a.wt_rs;
+  const bf16_t *msk = reinterpret_cast<const bf16_t *>(a.mask) + rep * a.out_rs;
+  bf16_t *out = reinterpret_cast<bf16_t *>(a.out) + rep * a.out_rs;
+  const __amdgpu_buffer_rsrc_t rsw = rsrc(wt, (uint32_t)CF::W_BYTES);
+
+  // the weight matrix, once, by all 16 waves: row n at n * 1168 bytes, its
+  // 72 chunks in order and a zero one
+  constexpr int WSLOTS = PL::W_LDS / 16, WROWC = IMGD_WROW / 16;
+#pragma unroll
+  for (int q = 0; q < (WSLOTS + 2 * NTHR - 1) / (2 * NTHR); ++q) {
+    const int slot0 = q * 2 * NTHR + wave * 64;
+    if (slot0 < WSLOTS) {  // (whole 64-slot copies: WSLOTS is a multiple of 64)
+      const int j = slot0 + lane;
+      const int row = j / WROWC, kc = j % WROWC;
+      const uint32_t off = (row < NO && kc < CF::WCH) ? (uint32_t)(row * CF::KP + 8 * kc) * 2u : kOob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsw, LDS_PTR(smem + W_OFF + slot0 * 16), 16, off, 0, 0, 0);
+    }
+  }
+
+  // A thread's halo piece q of a tile (16-byte slot j = 512 q + 64 tw + lane
+  // of its team's buffer: pixel slot j / 8, chunk j % 8) is tabled as 16 bits:
+  // the pooled piece it comes from, counted in 16-byte units from the tile's
+  // pooled row above (10 bits), the pixel's window position (2 bits), and
+  // flags for a pixel outside the image in the top tile of an image (0x8000:
+  // the row above it), in the bottom tile (0x4000: the row below) and always
+  // (0x2000: the border columns, the padding past the halo).
+  u32x4 ent0;
+  if (team == 0) {
+    uint32_t e16[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) e16[q] = 0x2000u;
+#pragma unroll
+    for (int q = 0; q < HQ; ++q) {
+      const int j = q * NTHR + tw * 64 + lane;
+      const int R = j / CPR, cs = j % CPR;
+      const int hp = R / HP, wp = R - hp * HP;
+      const int c = cs ^ (wp & 7);
+      const int w = wp - 1;
+      if (R < HPIX && (unsigned)w < (unsigned)IMG) {
+        const int prr = (hp + 1) >> 1;  // pooled row of image row h0 - 1 + hp, from the one above h0 / 2
+        const int pos = (((hp - 1) & 1) << 1) | (w & 1);
+        e16[q] = (uint32_t)((prr * PW + (w >> 1)) * CPR + c) | ((uint32_t)pos << 10) | (hp == 0 ? 0x8000u : 0u) |
+                 (hp == HPIX / HP - 1 ? 0x4000u : 0u);
+      }
+    }
+    ent0 = u32x4{e16[0] | (e16[1] << 16), e16[2] | (e16[3] << 16), e16[4] | (e16[5] << 16), e16[6] | (e16[7] << 16)};
+    *reinterpret_cast<u32x4 *>(smem + T_OFF + (tw * 64 + lane) * 16) = ent0;
+  }
+  // the pooled gradient and codes of this thread's pieces of tile k, into
+  // registers (every load is issued, from a valid address; the flags are
+  // applied when the pieces are routed)
+  u32x4 gv[HQ];
+  u32x2 cv[HQ];
+  auto load_halo = [&](int k, const u32x4 &ent) {
+    const int m0 = (w0 + k * WPR) * (TROWS * IMG), h0 = (m0 / IMG) % IMG;
+    const int pbase = ((m0 / (IMG * IMG)) * PW * PW + (h0 / 2 - 1) * PW) * CS;  // element of the pooled row above
+    // a piece outside the image (above the first or below the last pooled
+    // row too) reads the replica's first piece instead
+    const uint32_t bad = h0 == 0 ? 0xa000u : (h0 == IMG - TROWS ? 0x6000u : 0x2000u);
+#pragma unroll
+    for (int q = 0; q < HQ; ++q) {
+      if (q * NTHR * 16 + tw * 1024 < CF::H_BYTES) {
+        const uint32_t e = (ent[q >> 1] >> (16 * (q & 1))) & 0xffffu;
+        const int el = (e & bad) ? 0 : pbase + (int)(e & 0x3ffu) * 8;
+        gv[q] = *reinterpret_cast<const u32x4 *>(gsrc + el);
+        cv[q] = *reinterpret_cast<const u32x2 *>(csrc + el);
+      }
+    }
+  };
+  // the routed pieces into the team's halo buffer
+  auto route_halo = [&](int k, const u32x4 &ent) {
+    const int m0 = (w0 + k * WPR) * (TROWS * IMG), h0 = (m0 / IMG) % IMG;
+    const uint32_t bad = h0 == 0 ? 0xa000u : (h0 == IMG - TROWS ? 0x6000u : 0x2000u);
+    const int ln = img_lane_id();
+#pragma unroll
+    for (int q = 0; q < HQ; ++q) {
+      const int byte = q * NTHR * 16 + tw * 1024;
+      if (byte < CF::H_BYTES) {
+        const uint32_t e = (ent[q >> 1] >> (16 * (q & 1))) & 0xffffu;
+        const uint32_t kpos = (e & bad) ? 0xffu : (e >> 10) & 3u;  // 0xff: no code matches
+        u32x4 v;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const uint32_t cb = cv[q][d >> 1] >> (16 * (d & 1));  // codes of channels 2d, 2d + 1
+          const uint32_t keep = ((cb & 0xffu) == kpos ? 0x0000ffffu : 0u) | (((cb >> 8) & 0xffu) == kpos ? 0xffff0000u : 0u);
+          v[d] = gv[q][d] & keep;
+        }
+        const uint32_t ad = (uint32_t)(size_t)LDS_PTR(smem + team * CF::H_BYTES + byte) + (uint32_t)ln * 16u;
+        asm volatile("ds_write_b128 %0, %1" ::"v"(ad), "v"(v) : "memory");
+      }
+    }
+  };
+  if (team == 0) {
+    load_halo(0, ent0);
+    img_wait_vm<0>();
+    route_halo(0, ent0);
+  }
+  img_wait_vm<0>();
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+  const uint32_t lds0 = (uint32_t)(size_t)LDS_PTR(smem);
+  // Phase ph: the team of tile ph (ph & 1) computes it from its buffer; the
+  // other team loads its next tile's pieces (ph + 1), masks and stores its
+  // tile ph - 1, then routes the pieces into its buffer (read for the last
+  // time in phase ph - 1).  One barrier per phase.
+  f32x4_t acc[2][2];
+  for (int ph = 0; ph <= nt; ++ph) {
+    if ((ph & 1) == team) {
+      if (ph < nt) {
+        // fragment read bases (from an opaque lane index): weight row li,
+        // chunk lg; the team's halo buffer, pixel li + s of the wave's first
+        // halo row, chunk 4 g + lg
+        const int ln = img_lane_id();
+        const int li = ln & 15, lg = ln >> 4;
+        const uint32_t wb = lds0 + (uint32_t)(W_OFF + li * IMGD_WROW + lg * 16);
+        uint32_t xb[3][2];
+#pragma unroll
+        for (int s = 0; s < 3; ++s)
+#pragma unroll
+          for (int g = 0; g < 2; ++g)
+            xb[s][g] = lds0 + (uint32_t)(team * CF::H_BYTES + (tw * HP + li + s) * CF::RB +
+                                         (((4 * g + lg) ^ ((li + s) & 7)) * 16));
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int k = 0; k < 2; ++k) acc[i][k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        img_dgrad_tap<0>(acc, wb, xb);
+        img_dgrad_tap<1>(acc, wb, xb);
+        img_dgrad_tap<2>(acc, wb, xb);
+        img_dgrad_tap<3>(acc, wb, xb);
+        img_dgrad_tap<4>(acc, wb, xb);
+        img_dgrad_tap<5>(acc, wb, xb);
+        img_dgrad_tap<6>(acc, wb, xb);
+        img_dgrad_tap<7>(acc, wb, xb);
+        img_dgrad_tap<8>(acc, wb, xb);
+      }
+    } else {
+      const bool next = ph + 1 < nt;
+      u32x4 ent;
+      if (next) {
+        const uint32_t ta = lds0 + (uint32_t)(T_OFF + (tw * 64 + img_lane_id()) * 16);
+        asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(ent) : "v"(ta) : "memory");
+      }
+      if (ph >= 1) {
+        // lane (li, lg) holds channels tn*16 + 4 lg + e of pixel
+        // 16 half + li of image row h0 + tw; the gradient passes where the
+        // layer below's output (the mask) is positive (positive bf16 values
+        // read as positive 16-bit integers)
+        const int ln = img_lane_id();
+        const int eli = ln & 15, elg = ln >> 4;
+        const int64_t p0 = (int64_t)(w0 + (ph - 1) * WPR) * (TROWS * IMG) + tw * IMG + eli;
+        u32x2 mv[2][2];
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int tn = 0; tn < 2; ++tn)
+            mv[hf][tn] = *reinterpret_cast<const u32x2 *>(msk + (p0 + 16 * hf) * NO + tn * 16 + 4 * elg);
+        if (next) load_halo(ph + 1, ent);
+        if (next) img_wait_vm<2 * HQ>();  // the masks (issued before the pieces)
+        else img_wait_vm<0>();
+        const uint32_t one = 0x00010001u;
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int tn = 0; tn < 2; ++tn) {
+            u32x2 o;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              const uint32_t v = pack2_bf16(acc[hf][tn][2 * h], acc[hf][tn][2 * h + 1]);
+              // 1 where the mask is positive, else 0, per 16-bit half
+              const uint32_t pass = pk_min_u16(pk_max0_i16(mv[hf][tn][h]), one);
+              o[h] = pk_mul_lo_u16(v, pass);
+            }
+            *reinterpret_cast<u32x2 *>(out + (p0 + 16 * hf) * NO + tn * 16 + 4 * elg) = o;
+          }
+        if (next) img_wait_vm<4>();  // the pieces (issued before the 4 stores)
+      } else if (next) {
+        load_halo(ph + 1, ent);
+        img_wait_vm<0>();
+      }
+      if (next) route_halo(ph + 1, ent);
     }
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   }
@@ -835,9 +1106,13 @@ hipError_t launch_conv_img(const ConvArgs &a, hipStream_t s, std::string *label)
   // the forward into the pool and its codes: persistent workgroups, one per
   // CU, each taking every WPR-th tile of its replica
   const bool pers = a.epi == EPI_FWD && a.Csrc == 32 && a.pool_out && a.pool_code && !a.no_relu;
+  // the input gradient from the pooled gradient and its codes, with a mask:
+  // persistent the same way
+  const bool pdg = a.epi == EPI_DGRAD && a.Csrc == 64 && a.N == 32 && a.pool_code && a.mask;
   if (label)
     *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16," + std::to_string(256 * rpw) +
-             "x" + std::to_string(a.N) + "x" + std::to_string(9 * a.Csrc) + (pers ? ",w8,img,pool>" : ",w8,img>");
+             "x" + std::to_string(a.N) + "x" + std::to_string(9 * a.Csrc) +
+             (pers || pdg ? ",w8,img,pool>" : ",w8,img>");
 #define IMG_GO(CS, NO, E, RPW) \
   hipLaunchKernelGGL((conv_img_kernel<CS, NO, E, RPW>), g, dim3(NTHR), (ImgCfg<CS, NO, RPW>::LDS), s, a, MT)
   static_assert(ImgCfg<32, 32, 2>::FITS2 && ImgCfg<32, 64, 2>::FITS2 && ImgCfg<32, 32>::FITS2 &&
@@ -852,6 +1127,9 @@ hipError_t launch_conv_img(const ConvArgs &a, hipStream_t s, std::string *label)
     }
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&conv_img_kernel<32, 64, EPI_FWD, 2>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, ImgCfg<32, 64, 2>::LDS);
+    if (e != hipSuccess) return e;
+    e = hipFuncSetAttribute(reinterpret_cast<const void *>(&conv_img_dgrad_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, ImgDgrad::LDS);
     if (e != hipSuccess) return e;
     for (const void *f : {reinterpret_cast<const void *>(&conv_img_pool_kernel<64>),
                           reinterpret_cast<const void *>(&conv_img_pool_kernel<32>)}) {
@@ -872,6 +1150,14 @@ hipError_t launch_conv_img(const ConvArgs &a, hipStream_t s, std::string *label)
       hipLaunchKernelGGL(conv_img_pool_kernel<64>, gp, dim3(2 * NTHR), ImgPool<64>::LDS, s, a, MT, wpr);
     else
       hipLaunchKernelGGL(conv_img_pool_kernel<32>, gp, dim3(2 * NTHR), ImgPool<32>::LDS, s, a, MT, wpr);
+    return hipGetLastError();
+  }
+  if (pdg) {
+    constexpr int kSlots = 256;
+    const int want = std::max(1, std::min(MT, kSlots / std::max(1, a.C)));
+    const int per = (MT + want - 1) / want;
+    const int wpr = (MT + per - 1) / per;
+    hipLaunchKernelGGL(conv_img_dgrad_kernel, dim3((uint32_t)wpr * a.C), dim3(2 * NTHR), ImgDgrad::LDS, s, a, MT, wpr);
     return hipGetLastError();
   }
   if (a.epi == EPI_FWD) {

@@ -77,6 +77,8 @@ def kernel_label(name: str) -> str:
     m = re.search(r"conv_img_pool_kernel<(\d+)>", name)
     if m:  # the persistent forward into the max pool and its routing codes
         return f"conv_fwd<bf16,512x{m.group(1)}x288,w8,img,pool>"
+    if re.search(r"conv_img_dgrad_kernel\b", name):  # the persistent input gradient from the pooled gradient
+        return "conv_dgrad<bf16,256x32x576,w8,img,pool>"
     m = re.search(r"wgrad_col_kernel(<(true|false)>)?", name)
     if m:
         return "conv_wgrad<bf16,32x27,w4,img3>" if m.group(2) == "true" else "conv_wgrad<bf16,32x32,w4,col>"

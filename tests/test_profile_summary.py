@@ -50,6 +50,7 @@ def test_image_layer_labels():
     assert ps.kernel_label(ns + "wgrad_img_kernel<3, true>(WgradArgs)") == "conv_wgrad<bf16,64x288,w8,img,pool>"
     assert ps.kernel_label(ns + "conv_img_pool_kernel<64>(ConvArgs, int, int)") == \
         "conv_fwd<bf16,512x64x288,w8,img,pool>"
+    assert ps.kernel_label(ns + "conv_img_dgrad_kernel(ConvArgs, int, int)") == "conv_dgrad<bf16,256x32x576,w8,img,pool>"
 
 
 @pytest.mark.parametrize("label,source", [
@@ -62,6 +63,7 @@ def test_image_layer_labels():
     ("conv_wgrad<bf16,64x288,w8,img,pool>", "k_wgrad_lds.hip"),
     ("conv_fwd<bf16,512x64x288,w8,img>", "k_conv_img.hip"),
     ("conv_fwd<bf16,512x64x288,w8,img,pool>", "k_conv_img.hip"),
+    ("conv_dgrad<bf16,256x32x576,w8,img,pool>", "k_conv_img.hip"),
     ("conv_fwd<f32,128x128x32,w4,vec>", "k_conv.hip"),
     ("sgd", "k_misc.hip"),
     ("fuse", "k_misc.hip"),
