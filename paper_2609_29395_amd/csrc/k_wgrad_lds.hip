@@ -697,6 +697,67 @@ __device__ __forceinline__ void wi_kgroup(f32x4_t (&acc)[wi::NF], f32x4_t &bacc,
   }
 }
 
+// one k group (image row kw of the tile: its g rows from sa, its input rows
+// from st) for 32 output channels: two g fragments (the second's chunk
+// differs from the first's in bit 1 of the swizzled chunk index: address
+// bit 5) and the wave's nine input fragments, read two at a time; eighteen
+// MFMAs (+2 against ones for the bias gradient)
+template <int I0, int NB>
+__device__ __forceinline__ void wi_bfrags(u32x4 (&b)[2], const uint32_t (&hb)[3][2][2], uint32_t st, int wn) {
+#pragma unroll
+  for (int u = 0; u < NB; ++u) {
+    // fragment f = 9 wn + i: tap t = f / 2 (r = t / 3, s = t % 3), block f % 2
+    const int i = I0 + u;
+    const int f0 = i, f1 = 9 + i;  // the wave's fragment for wn = 0 / 1
+    const int t0 = f0 / 2, t1 = f1 / 2;
+    // both choices are compile-time constants; wn selects one at run time
+    const uint32_t s0 = st + hb[t0 % 3][f0 % 2][0], s1 = st + hb[t1 % 3][f1 % 2][0];
+    const uint32_t e0 = st + hb[t0 % 3][f0 % 2][1], e1 = st + hb[t1 % 3][f1 % 2][1];
+    const uint32_t lo = wn ? s1 : s0, hi = wn ? e1 : e0;
+    const int r = wn ? t1 / 3 : t0 / 3;
+    const uint32_t ro = (uint32_t)(r * wi::FROW);
+    u32x2 l2, h2;
+    asm volatile("ds_read_b64_tr_b16 %0, %2 offset:%4\n\tds_read_b64_tr_b16 %1, %3 offset:%4"
+                 : "=&v"(l2), "=&v"(h2)
+                 : "v"(lo + ro), "v"(hi + ro), "n"(wi::A_BYTES));
+    b[u] = __builtin_shufflevector(l2, h2, 0, 1, 2, 3);
+  }
+}
+
+__device__ __forceinline__ void wi_kgroup2(f32x4_t (&acc)[2][wi::NF], f32x4_t (&bacc)[2], uint32_t ra,
+                                           const uint32_t (&hb)[3][2][2], uint32_t sa, uint32_t st, bool bias,
+                                           int wn) {
+  u32x4 a[2];
+  read_frag<0, wi::ROWA>(a[0], sa + ra);
+  read_frag<0, wi::ROWA>(a[1], sa + (ra ^ 32u));
+  auto step = [&](const u32x4 (&b)[2], int i0, int nb) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+      if (u < nb) {
+        mma(acc[0][i0 + u], a[0], b[u]);
+        mma(acc[1][i0 + u], a[1], b[u]);
+      }
+  };
+  u32x4 b[2];
+#define WI_GROUP(I0, NB)                                   \
+  wi_bfrags<I0, NB>(b, hb, st, wn);                        \
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");       \
+  asm volatile("" : "+v"(a[0]), "+v"(a[1]));               \
+  asm volatile("" : "+v"(b[0]), "+v"(b[1]));               \
+  step(b, I0, NB);
+  WI_GROUP(0, 2)
+  WI_GROUP(2, 2)
+  WI_GROUP(4, 2)
+  WI_GROUP(6, 2)
+  WI_GROUP(8, 1)
+#undef WI_GROUP
+  if (bias) {
+    const uint32_t one2 = 0x3F803F80u;  // two bf16 ones
+    mma(bacc[0], a[0], u32x4{one2, one2, one2, one2});
+    mma(bacc[1], a[1], u32x4{one2, one2, one2, one2});
+  }
+}
+
 // (at least four waves per SIMD: at most 128 registers, so that two
 // workgroups share a CU)
 template <int NST, bool POOL>
@@ -719,7 +780,10 @@ wgrad_img_kernel(WgradArgs a) {
   // (POOL: g and gc are the pooled gradient and its codes, a quarter of the pixels)
   const uint32_t gbytes = (uint32_t)((int64_t)M * wi::CO * 2 / (POOL ? 4 : 1)),
                  xbytes = (uint32_t)((int64_t)M * wi::CI * 2);
-  const int wm = wave >> 1, wn = wave & 1;
+  // wave (kw, wm2, wn): image row kw of every k tile, output channels
+  // 32 wm2 .. + 31, input fragments 9 wn .. 9 wn + 8; the two k rows' sums
+  // are added at the end
+  const int kw = wave >> 2, wm2 = (wave >> 1) & 1, wn = wave & 1;
   const bool do_bias = wn == 0 && a.db != nullptr;
 
   // this thread's copies: bytes q*8192 + wave*1024 + lane*16 of each region
@@ -743,7 +807,9 @@ wgrad_img_kernel(WgradArgs a) {
   const int j = lane & 15, lg = lane >> 4;
   const int frow = 8 * lg + (j >> 2);
   const int half = (j & 3) >> 1;
-  const uint32_t ra = (uint32_t)(frow * wi::ROWA + (((2 * wm + half) ^ swz<wi::ROWA / 16>(frow)) * 16) + (j & 1) * 8);
+  const uint32_t ra =
+      (uint32_t)(frow * wi::ROWA + (((4 * wm2 + half) ^ swz<wi::ROWA / 16>(frow)) * 16) + (j & 1) * 8);
+  static_assert(wi::ROWA == 128, "g fragment chunk index in address bits 4..6");
   uint32_t hb[3][2][2];
 #pragma unroll
   for (int s = 0; s < 3; ++s)
@@ -756,10 +822,15 @@ wgrad_img_kernel(WgradArgs a) {
       }
   const uint32_t lds0 = (uint32_t)(size_t)LDS_PTR(smem);
 
-  f32x4_t acc[wi::NF];
+  f32x4_t acc[2][wi::NF];
 #pragma unroll
-  for (int i = 0; i < wi::NF; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  f32x4_t bacc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int r2 = 0; r2 < 2; ++r2)
+#pragma unroll
+    for (int i = 0; i < wi::NF; ++i) acc[r2][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  f32x4_t bacc[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
+  // (the wave's k row: 32 g rows and one halo image row further)
+  const uint32_t koa = (uint32_t)(kw * 32 * wi::ROWA), kob = (uint32_t)(kw * wi::FROW);
+  auto kgroups = [&](uint32_t st) { wi_kgroup2(acc, bacc, ra, hb, st + koa, st + kob, do_bias, wn); };
 
   if constexpr (!POOL) {
 #pragma unroll
@@ -771,9 +842,7 @@ wgrad_img_kernel(WgradArgs a) {
       asm volatile("s_barrier" ::: "memory");
       if (kt + NST - 1 < nk)
         wi_issue<NST, false>(kt + NST - 1, smem, wave, lane, G, X, gc, gbytes, xbytes, p_begin, arow, acol, hrel, hh);
-      const uint32_t st = lds0 + (uint32_t)((kt % NST) * wi::STAGE);
-      wi_kgroup<0>(acc, bacc, ra, hb, st, do_bias, wn);
-      wi_kgroup<1>(acc, bacc, ra, hb, st, do_bias, wn);
+      kgroups(lds0 + (uint32_t)((kt % NST) * wi::STAGE));
     }
   } else {
     // copies NST - 1 = 2 k tiles ahead; g tile kt + 1 routed in LDS during
@@ -803,25 +872,55 @@ wgrad_img_kernel(WgradArgs a) {
       if (kt + 2 < nk) wi_issue<NST, true>(kt + 2, smem, wave, lane, G, X, gc, gbytes, xbytes, p_begin, arow, acol, hrel, hh);
       // stage (kt + 1) % NST's g tile was last read by tile kt - 2
       if (kt + 1 < nk) wi_route(smem + ((kt + 1) % NST) * wi::STAGE, tid, arow, acol);
-      const uint32_t st = lds0 + (uint32_t)((kt % NST) * wi::STAGE);
-      wi_kgroup<0>(acc, bacc, ra, hb, st, do_bias, wn);
-      wi_kgroup<1>(acc, bacc, ra, hb, st, do_bias, wn);
+      kgroups(lds0 + (uint32_t)((kt % NST) * wi::STAGE));
     }
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  // the second k row's sums to the first's waves through LDS (the stages
+  // are free now), one g fragment at a time: 4 waves x 40 floats per lane
+  static_assert(4 * 40 * 64 * 4 <= NST * wi::STAGE, "exchange fits the stages");
+  float *xch = reinterpret_cast<float *>(smem);
+  const int xw = wave & 3;
+#pragma unroll
+  for (int r2 = 0; r2 < 2; ++r2) {
+    __syncthreads();  // (r2 0: every wave is done with the stages; r2 1: with the exchange)
+    if (kw == 1) {
+#pragma unroll
+      for (int i = 0; i < wi::NF; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) xch[((xw * 40 + 4 * i + r) * 64) + lane] = acc[r2][i][r];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) xch[((xw * 40 + 36 + r) * 64) + lane] = bacc[r2][r];
+    }
+    __syncthreads();
+    if (kw == 0) {
+#pragma unroll
+      for (int i = 0; i < wi::NF; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[r2][i][r] += xch[((xw * 40 + 4 * i + r) * 64) + lane];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) bacc[r2][r] += xch[((xw * 40 + 36 + r) * 64) + lane];
+    }
+  }
+  if (kw != 0) return;
 
   // column of fragment f, lane j: (tap, channel) = (f / 2, 16 (f % 2) + j),
   // i.e. 16 f + j of the 288
   float *dw = a.dw + split * a.dw_ss + rep * a.dw_rs;
 #pragma unroll
-  for (int i = 0; i < wi::NF; ++i) {
-    const int n = 16 * (9 * wn + i) + j;
+  for (int r2 = 0; r2 < 2; ++r2) {
+    const int wm = 2 * wm2 + r2;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) dw[(int64_t)(wm * 16 + lg * 4 + r) * a.nw + n] = acc[i][r];
-  }
-  if (do_bias && j == 0) {
+    for (int i = 0; i < wi::NF; ++i) {
+      const int n = 16 * (9 * wn + i) + j;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) a.db[split * a.db_ss + rep * a.db_rs + wm * 16 + lg * 4 + r] = bacc[r];
+      for (int r = 0; r < 4; ++r) dw[(int64_t)(wm * 16 + lg * 4 + r) * a.nw + n] = acc[r2][i][r];
+    }
+    if (do_bias && j == 0) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) a.db[split * a.db_ss + rep * a.db_rs + wm * 16 + lg * 4 + r] = bacc[r2][r];
+    }
   }
 }
 
