@@ -332,20 +332,34 @@ int build_plan(const gcpsl_desc *d, Plan &p) {
     int splits;
     if (wgrad_lds_ok(p.dtype, l.Co, Ci_eff) || wgrad_col_ok(p.dtype, l.Co, Ci_eff, taps) ||
         (taps == 9 && conv_im3_ok(p.dtype, Ci_eff, l.Co, Hh, Ww))) {
-      // pick the split count that minimises (rounds of 256 x per_cu
-      // workgroups) x (k tiles per workgroup + the cost of writing and
-      // re-reading a partial tile, about 16 k tiles)
+      // Kernels that run one workgroup per CU (the halo weight gradients,
+      // MFMA-bound): pick the split count that minimises the time in units
+      // of one k tile of a workgroup on its CU, (workgroups / 256 CUs,
+      // rounded up) x (k tiles per workgroup), plus writing and re-reading
+      // all the partials (bm x bn floats per workgroup) at the chip's HBM
+      // rate B: with F = 5.9 TFLOP/s reached per CU and B = 6 TB/s, the
+      // 8 bytes of each partial float cost 4 F / (B kt) k tiles per partial
+      // tile on the whole chip (the tile's size cancels).  The others (two
+      // or four workgroups per CU, bound by their copies rather than the
+      // MFMAs): (rounds of 256 x per_cu workgroups) x (k tiles per
+      // workgroup + the cost of writing and re-reading a partial tile,
+      // about 16 k tiles).
       int tile_bk, per_cu;
       wgrad_lds_tile(l.Co, Ci_eff, Hh, Ww, taps, &bm, &bn, &tile_bk, &per_cu);
       kt = tile_bk;  // chunks are whole k tiles of the kernel the layer runs
       nkt = (M + kt - 1) / kt;
       const int64_t tiles = (int64_t)((l.Co + bm - 1) / bm) * ((nwc + bn - 1) / bn) * C;
       const int64_t slots = 256 * (int64_t)per_cu;
-      int64_t best = -1;
+      double best = -1.0;
       splits = 1;
       for (int sp = 1; sp <= std::min(64, nkt); ++sp) {
-        const int64_t rounds = (tiles * sp + slots - 1) / slots;
-        const int64_t cost = rounds * ((nkt + sp - 1) / sp + (sp > 1 ? 16 * 64 / kt : 0));
+        const double ktiles = (double)((nkt + sp - 1) / sp);
+        double cost;
+        if (per_cu == 1)
+          cost = (double)((tiles * sp + 255) / 256) * ktiles +
+                 (sp > 1 ? (double)(tiles * sp) * 4.0 * 5.9e12 / (6.0e12 * kt) : 0.0);
+        else
+          cost = (double)((tiles * sp + slots - 1) / slots) * (ktiles + (sp > 1 ? 16.0 * 64 / kt : 0.0));
         if (best < 0 || cost < best) best = cost, splits = sp;
       }
     } else {
