@@ -262,15 +262,17 @@ conv_lds_kernel(ConvArgs a, FastDiv fd_w, FastDiv fd_h, FastDiv fd_c, int MT, in
   using CF = Cfg<BM, BN, WM, WN, (HALO && HB == 1) ? 2 : 0>;
   static_assert(!HALO || (BM == 256 && !TAPS1 &&
                           ((BN == 256 && (WM == 4 || WM == 2) && WN == 4 && HB == 2) ||
-                           (BN == 64 && WM == 8 && WN == 2 && HB == 2) || (BN == 128 && WM == 4 && WN == 2 && HB == 1))),
+                           (BN == 64 && WM == 8 && WN == 2 && HB == 2) ||
+                           ((BN == 128 || BN == 64) && WM == 4 && WN == 2 && HB == 1))),
                 "halo mode tile");
   static_assert(HB == 2 || (HALO && HB == 1), "halo buffers");
   // AVG: the tile is one whole image (halo mode, forward) and writes the
   // means of its BN channels
   static_assert(!AVG || (HALO && (BN == 256 || BN == 128) && EPI == EPI_FWD), "image mean in the epilogue");
-  // halo mode, 64-wide weight tiles: a k tile is a whole tap row (three taps)
-  // so that each barrier covers three times the MFMAs of a one-tap tile
-  constexpr int TPK = (HALO && BN == 64) ? 3 : 1;
+  // halo mode, 64-wide weight tiles with two halo buffers: a k tile is a
+  // whole tap row (three taps) so that each barrier covers three times the
+  // MFMAs of a one-tap tile
+  constexpr int TPK = (HALO && BN == 64 && HB == 2) ? 3 : 1;
   constexpr int SA = CF::SA, SB = CF::SB, TM = CF::TM, TN = CF::TN, NTHR = CF::NTHR, PF = CF::PF;
   extern __shared__ __attribute__((aligned(1024))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -705,13 +707,17 @@ using Halo64Cfg = Cfg<256, 64, 8, 2>;
 // 128-wide weight tiles: 8 waves of 64 x 64, one halo buffer, two-pass
 // epilogue; two workgroups per CU
 using Halo128Cfg = Cfg<256, 128, 4, 2, 2>;
+// the same on 64-wide weight tiles (8 waves of 64 x 32): three LDS reads
+// per four MFMAs instead of the 16-wave tile's one per MFMA
+using Halo64hCfg = Cfg<256, 64, 4, 2, 2>;
 // dynamic LDS of a halo-mode launch: the k loop's buffers or the epilogue's
 // staging, whichever is larger
 template <typename CF, int TPK, int HB = 2> constexpr int halo_lds_of() {
   return halo::lds_bytes<CF::BN_, TPK, HB>() > CF::EP_BYTES ? halo::lds_bytes<CF::BN_, TPK, HB>() : CF::EP_BYTES;
 }
 static_assert(halo_lds_of<HaloCfg, 1>() <= 160 * 1024 && halo_lds_of<Halo64Cfg, 3>() <= 160 * 1024 &&
-              2 * halo_lds_of<Halo128Cfg, 1, 1>() <= 160 * 1024, "halo LDS");
+              2 * halo_lds_of<Halo128Cfg, 1, 1>() <= 160 * 1024 && 2 * halo_lds_of<Halo64hCfg, 1, 1>() <= 160 * 1024,
+              "halo LDS");
 
 // 16 x 16 images in 64-channel blocks: the halo layouts apply
 bool halo_img16(const ConvArgs &a) {
@@ -756,6 +762,12 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
                           reinterpret_cast<const void *>(&conv_lds_kernel<256, 64, 8, 2, EPI_DGRAD, false, true>)}) {
       const hipError_t e =
           hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, halo_lds_of<Halo64Cfg, 3>());
+      if (e != hipSuccess) return e;
+    }
+    {
+      const hipError_t e =
+          hipFuncSetAttribute(reinterpret_cast<const void *>(&conv_lds_kernel<256, 64, 4, 2, EPI_DGRAD, false, true, false, 1>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, halo_lds_of<Halo64hCfg, 1, 1>());
       if (e != hipSuccess) return e;
     }
     for (const void *f :
@@ -809,9 +821,13 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
   ConvArgs b = a;
   b.res_lds = (a.res != nullptr && a.res == a.src && a.taps == 9 && a.Csrc % BK == 0 && a.Csrc == a.N &&
                (bn == 256 || bn == 128)) ? 1 : 0;
+  // the input gradient on 64-wide halo tiles: 8 waves, one halo buffer
+  const bool use_h64 = use_halo64 && a.epi == EPI_DGRAD;
   if (label) {
     if (use_h128)
       *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16,256x128x64,w8,halo1>";
+    else if (use_h64)
+      *label = "conv_dgrad<bf16,256x64x64,w8,halo1>";
     else
       *label = std::string(a.epi == EPI_FWD ? "conv_fwd" : "conv_dgrad") + "<bf16," + std::to_string(bm) + "x" +
                std::to_string(bn) + (use_halo64 ? "x192,w16" : "x64,w") +
@@ -842,6 +858,11 @@ hipError_t launch_conv_lds(const ConvArgs &a, hipStream_t s, std::string *label)
     else
       hipLaunchKernelGGL((conv_lds_kernel<256, 256, kHaloWM, 4, EPI_DGRAD, false, true>), g, dim3(HaloCfg::NTHR),
                          (halo_lds_of<HaloCfg, 1>()), s, b, fw, fh, fc, MT, NT);
+    return hipGetLastError();
+  }
+  if (use_h64) {
+    hipLaunchKernelGGL((conv_lds_kernel<256, 64, 4, 2, EPI_DGRAD, false, true, false, 1>), g, dim3(Halo64hCfg::NTHR),
+                       (halo_lds_of<Halo64hCfg, 1, 1>()), s, b, fw, fh, fc, MT, NT);
     return hipGetLastError();
   }
   if (use_halo64) {
