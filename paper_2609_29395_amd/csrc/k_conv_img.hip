@@ -341,9 +341,9 @@ conv_img_kernel(ConvArgs a, int MT) {
 // two teams of 8 waves.  The weight matrix is copied into LDS once per
 // workgroup and shared by both teams; each team has its own halo buffer.
 // While one team runs a tile's MFMAs, the other copies its next halo and
-// pools and stores its previous tile (121 KB of LDS, at most 128 registers
-// per wave; a third halo buffer, so that a copy could start a phase
-// earlier, measured slower).
+// pools and stores its previous tile (127 KB of LDS with the bias and the
+// copy table, at most 128 registers per wave; a third halo buffer, so that
+// a copy could start a phase earlier, measured slower).
 // Pixel fragment tm = 2 rr + hf of a wave holds the columns 2 li + hf of its
 // image row rr, so a lane ends with whole 2 x 2 pooling windows (4 channels
 // of pooled column li) and pools them in registers.  A halo row keeps its
@@ -683,11 +683,6 @@ conv_img_pool_kernel(ConvArgs a, int MT, int WPR) {
 // 8 consecutive lanes fall on distinct banks.
 constexpr int IMGD_WROW = 1168;  // bytes per weight row in LDS: 72 chunks and one of padding
 
-template <int OFF> __device__ __forceinline__ void lds_read16b(u32x4 &v, uint32_t ad) {
-  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
-  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(ad), "n"(OFF));
-}
-
 // tap (r, s) = (TAP / 3, TAP % 3): both 32-channel k groups; weight fragment
 // (tn, g) at wb + tn 16 rows + TAP 128 + g 64 bytes, pixel fragment (half, g)
 // at xb[s][g] + r halo rows + half 16 pixels
@@ -695,14 +690,14 @@ template <int TAP>
 __device__ __forceinline__ void img_dgrad_tap(f32x4_t (&acc)[2][2], uint32_t wb, const uint32_t (&xb)[3][2]) {
   constexpr int r = TAP / 3, s = TAP % 3, ROWB = HP * 128;
   u32x4 w[2][2], x[2][2];  // [g][tn], [g][half]
-  lds_read16b<TAP * 128>(w[0][0], wb);
-  lds_read16b<16 * IMGD_WROW + TAP * 128>(w[0][1], wb);
-  lds_read16b<TAP * 128 + 64>(w[1][0], wb);
-  lds_read16b<16 * IMGD_WROW + TAP * 128 + 64>(w[1][1], wb);
-  lds_read16b<r * ROWB>(x[0][0], xb[s][0]);
-  lds_read16b<r * ROWB + 16 * 128>(x[0][1], xb[s][0]);
-  lds_read16b<r * ROWB>(x[1][0], xb[s][1]);
-  lds_read16b<r * ROWB + 16 * 128>(x[1][1], xb[s][1]);
+  lds_read16<TAP * 128>(w[0][0], wb);
+  lds_read16<16 * IMGD_WROW + TAP * 128>(w[0][1], wb);
+  lds_read16<TAP * 128 + 64>(w[1][0], wb);
+  lds_read16<16 * IMGD_WROW + TAP * 128 + 64>(w[1][1], wb);
+  lds_read16<r * ROWB>(x[0][0], xb[s][0]);
+  lds_read16<r * ROWB + 16 * 128>(x[0][1], xb[s][0]);
+  lds_read16<r * ROWB>(x[1][0], xb[s][1]);
+  lds_read16<r * ROWB + 16 * 128>(x[1][1], xb[s][1]);
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
   for (int g = 0; g < 2; ++g)
