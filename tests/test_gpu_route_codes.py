@@ -72,3 +72,33 @@ def test_codes_pool_and_routed_gradients_follow_the_gpu_state():
             assert np.abs(gw - dw).max() <= 1e-4 * np.abs(dw).max(), (s, n)
             want0 = dx * (a0[n] > 0)
             assert np.abs(gpre0[n] - want0).max() <= 2 ** -7 * np.abs(want0).max(), (s, n)
+
+
+def test_codes_break_exact_ties_at_the_first_window_position():
+    # With the 32 -> 64 layer's weights zero, every pre-activation of a
+    # channel is its bias, so all four values of every 2 x 2 window tie: the
+    # pool's code is the first position (0) where the bias is positive and 4
+    # (no positive value) where it is zero or negative, and the pooled value
+    # is the bf16 bias or 0, exactly (Sec. III-A's forward with the stored
+    # max pool; the first maximum in row-major window order).
+    cfg = get_config("gcpsl8")
+    C, B = cfg["C"], cfg["B"]
+    ctx, _ = driver.setup(cfg, max_steps=1)
+    lay = {(i, t): (shp, off) for i, t, shp, off in param_layout(cfg)}
+    (wshp, woff), (bshp, boff) = lay[(1, "w")], lay[(1, "b")]
+    co = int(bshp[0])
+    pattern = np.array([0.5, -0.25, 0.0, 1e-3])
+    bias = pattern[np.arange(co) % 4]
+    ctx.theta[:, woff:woff + int(np.prod(wshp))] = 0.0
+    ctx.theta[:, boff:boff + co] = torch.tensor(bias, dtype=torch.float32, device="cuda")
+    loss = torch.zeros(C, device="cuda")
+    ctx.sample(0)
+    ctx.step(0, loss)
+    torch.cuda.synchronize()
+    pool = to_np(ctx.tensor("act2")).reshape(C, B, 16, 16, co).astype(np.float64)
+    route = to_np(ctx.tensor("route2")).reshape(C, B, 16, 16, co).astype(np.int64)
+    want_code = np.where(bias > 0, 0, 4)
+    want_pool = round_bf16(np.maximum(bias, 0.0))
+    assert np.array_equal(route, np.broadcast_to(want_code, route.shape)), \
+        np.unique(route.reshape(-1, co), axis=0)[:4]
+    assert np.array_equal(pool, np.broadcast_to(want_pool, pool.shape))
