@@ -23,6 +23,8 @@ Parity status of each part (pins live in tests/test_oracle_*.py):
   epoch-barrier schedule (Eq. 6)       pinned (worked example, waiting
                                         clusters untouched, equal lengths
                                         reduce to the lockstep schedule)
-  multi-step end-to-end values         parity unpinned: the paper prints no
-                                        worked example of a training run
+  multi-step end-to-end values         pinned (per-replica torch autograd +
+                                        torch.optim.SGD training loops fused
+                                        by numpy's weighted average, across
+                                        fusions)
 """

@@ -89,6 +89,46 @@ def test_recipe_rounds_match_torch_training_loop():
         assert np.allclose(o.theta[0], p.detach().numpy(), rtol=1e-5, atol=1e-7), step
 
 
+@pytest.mark.parametrize("name, F, steps", [("ragged", 3, 7), ("tiny_recipe", 2, 5)])
+def test_run_across_fusions_matches_torch_training_loops(name, F, steps):
+    """Multi-round end-to-end values (Alg. 2, Eq. 5): C replicas, each trained
+    by its own torch.optim.SGD (momentum kept local) on torch.autograd
+    gradients in fp64 on the same batches, and every F rounds replaced by
+    numpy's weighted average of the replicas with the clusters' example counts
+    as weights.  The oracle's run must give the same loss for every cluster
+    and round, and the same parameters and momenta at the end."""
+    from test_oracle_model import torch_split_model_loss
+    cfg = get_config(name, F=F, dtype="f32")
+    C = cfg["C"]
+    o = GCPSLOracle(cfg)
+    w = np.bincount(o.assignment[o.coe], minlength=C)  # examples per cluster
+    assert w.sum() == cfg["N_ex"] and len(set(w.tolist())) == C  # unequal weights
+    ps = [torch.nn.Parameter(torch.tensor(o.theta[n], dtype=torch.float64)) for n in range(C)]
+    opts = [torch.optim.SGD([p], lr=cfg["lr"], momentum=cfg["momentum"], weight_decay=cfg["weight_decay"],
+                            nesterov=cfg["nesterov"]) for p in ps]
+    want = []
+    for s in range(steps):
+        want.append([])
+        for n in range(C):
+            _, x, y = o.batch(s, n)  # the keyed sampler, pinned on its own
+            loss, g = torch_split_model_loss(cfg, ps[n].detach().numpy(), x, y)
+            want[-1].append(loss)
+            ps[n].grad = torch.tensor(g)
+            opts[n].step()
+        if (s + 1) % F == 0:
+            avg = np.average(np.stack([p.detach().numpy() for p in ps]), axis=0, weights=w)
+            for p in ps:
+                p.data = torch.tensor(avg)
+    o.run(steps)
+    assert np.allclose(np.array(o.losses), np.array(want), rtol=1e-6, atol=0)
+    for n in range(C):
+        assert np.allclose(o.theta[n], ps[n].detach().numpy(), rtol=1e-5, atol=1e-7), n
+        buf = opts[n].state[ps[n]]["momentum_buffer"].numpy()
+        assert np.allclose(o.mom[n], buf, rtol=1e-5, atol=1e-7), n
+    # the run ends between fusions: the replicas have trained apart again
+    assert not np.array_equal(o.theta[0], o.theta[1])
+
+
 def test_fusion_worked_example():
     # tests/golden: weights 1, 2, 5 (W = 8): (1*[8,0] + 2*[0,4] + 5*[0.8,-1.6]) / 8 = [1.5, 0]
     g = load_golden("fusion_eq5_worked.txt")
