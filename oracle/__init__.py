@@ -26,5 +26,5 @@ Parity status of each part (pins live in tests/test_oracle_*.py):
   multi-step end-to-end values         pinned (per-replica torch autograd +
                                         torch.optim.SGD training loops fused
                                         by numpy's weighted average, across
-                                        fusions)
+                                        fusions, fp32 and bf16)
 """
