@@ -89,7 +89,8 @@ def test_recipe_rounds_match_torch_training_loop():
         assert np.allclose(o.theta[0], p.detach().numpy(), rtol=1e-5, atol=1e-7), step
 
 
-@pytest.mark.parametrize("name, F, steps", [("ragged", 3, 7), ("tiny_recipe", 2, 5), ("ragged_bf16", 2, 5)])
+@pytest.mark.parametrize("name, F, steps", [("ragged", 3, 7), ("tiny_recipe", 2, 5), ("ragged_bf16", 2, 5),
+                                           ("resnet_tiny", 2, 3)])
 def test_run_across_fusions_matches_torch_training_loops(name, F, steps):
     """Multi-round end-to-end values (Alg. 2, Eq. 5): C replicas, each trained
     by its own torch.optim.SGD (momentum kept local) on torch.autograd
@@ -134,6 +135,29 @@ def test_run_across_fusions_matches_torch_training_loops(name, F, steps):
         assert np.allclose(o.mom[n], buf, rtol=1e-5, atol=1e-7), n
     # the run ends between fusions: the replicas have trained apart again
     assert not np.array_equal(o.theta[0], o.theta[1])
+
+
+@pytest.mark.parametrize("name", ["resnet_tiny_bf16", "ragged_recipe_bf16"])
+def test_rounds_of_a_run_match_torch_at_the_oracles_parameters(name):
+    """bf16 runs with norm layers drift apart from a free-running torch loop
+    once a one-ulp difference in an fp32 master weight flips its bf16
+    rounding, so each round of a 4-round run with fusions (F = 2) is checked
+    from the oracle's own parameters at that point: the loss and gradient it
+    takes must be torch.autograd's at the same parameters and batch."""
+    from test_oracle_model import torch_split_model_loss
+    cfg = get_config(name, F=2)
+    o = GCPSLOracle(cfg)
+    for s in range(4):
+        theta = [t.copy() for t in o.theta]
+        losses, grads = o.round(s)
+        for n in range(cfg["C"]):
+            _, x, y = o.batch(s, n)
+            want_loss, g = torch_split_model_loss(cfg, theta[n], x, y)
+            assert losses[n] == pytest.approx(want_loss, rel=1e-12), (s, n)
+            assert np.allclose(grads[n], g, rtol=1e-9, atol=1e-12 * np.abs(g).max()), (s, n)
+        if (s + 1) % 2 == 0:
+            o.fuse()
+    assert np.array_equal(o.theta[0], o.theta[1])  # fused after the last round
 
 
 def test_fusion_worked_example():
