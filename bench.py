@@ -355,8 +355,8 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py runs on one GPU only (--gpus {args.gpus}, WORLD_SIZE {world}); the multi-GPU "
-              "fusion path is a design, not part of this build", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (--gpus {args.gpus}, WORLD_SIZE {world}); the library "
+              "drives one GPU and does not shard the replicas across GPUs", file=sys.stderr)
         sys.exit(2)
 
     import torch
