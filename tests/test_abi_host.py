@@ -243,3 +243,15 @@ def test_fuse_replicas_rejects_bad_arguments_before_device_work():
         rc = lib.gcpsl_fuse_replicas(fake, 3, 10, b.ctypes.data_as(C.POINTER(C.c_int64)), None)
         assert rc == g.EINVAL, bad
         assert "weights" in lib.gcpsl_last_error().decode()
+
+
+@pytest.mark.parametrize("argv, env", [(["--gpus", "2"], {}), (["--gpus", "8"], {}), ([], {"WORLD_SIZE": "2"})])
+def test_bench_refuses_more_than_one_gpu(argv, env):
+    """bench.py measures one GPU; asked for more it exits with status 2 and a
+    message before touching a device."""
+    import subprocess
+    import sys
+    e = dict(os.environ, **env)
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *argv, "--steps", "1", "--warmup", "0"],
+                       capture_output=True, text=True, timeout=120, env=e, cwd=ROOT)
+    assert r.returncode == 2 and "one GPU only" in r.stderr and r.stdout == ""
